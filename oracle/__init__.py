@@ -1,0 +1,190 @@
+"""CPU oracle for the MeanField joint-configuration search (test infrastructure).
+
+Only the tests, `__graft_entry__.smoke()` and the CPU-baseline leg of
+`bench.py` may import this package.  It wraps `mf_oracle.c` (plain fp64
+brute force; see that file's header for the definitions it follows) through
+ctypes.  It imports nothing from the HIP library's package and shares no code
+with it: instances arrive as duck-typed objects carrying numpy arrays.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "mf_oracle.c")
+GA_SRC = os.path.join(HERE, "mf_oracle_ga.c")
+LIB = os.path.join(HERE, "libmf_oracle.so")
+MAX_TOPK = 64
+
+
+def build(verbose: bool = False) -> str:
+    """Compile the oracle with gcc (fp contraction off, explicit fma)."""
+    srcs = [SRC] + ([GA_SRC] if os.path.exists(GA_SRC) else [])
+    cmd = ["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-march=x86-64-v3", "-std=c11",
+           "-Wall", "-shared", "-fPIC", "-o", LIB + ".tmp", *srcs, "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.check_call(cmd)
+    os.replace(LIB + ".tmp", LIB)
+    return LIB
+
+
+class _Inst(C.Structure):
+    _fields_ = [("n_models", C.c_int32), ("n_local", C.c_int32), ("n_agg", C.c_int32),
+                ("hidden1", C.c_int32), ("hidden2", C.c_int32), ("bf16", C.c_int32),
+                ("n_options", C.c_void_p), ("features", C.c_void_p), ("agg_cols", C.c_void_p),
+                ("vram_slot", C.c_int32), ("vram_cap", C.c_float), ("weights", C.c_void_p)]
+
+
+class _Result(C.Structure):
+    _fields_ = [("n_eval", C.c_uint64), ("n_vram", C.c_uint64), ("n_feas", C.c_uint64),
+                ("n_inexact_agg", C.c_uint64), ("n_near", C.c_uint64 * 4),
+                ("n_top", C.c_int32), ("pad", C.c_int32),
+                ("top_idx", C.c_uint64 * MAX_TOPK), ("top_J", C.c_double * MAX_TOPK)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            build()
+        L = C.CDLL(LIB)
+        P = C.c_void_p
+        L.orc_space_size.restype = C.c_uint64
+        L.orc_space_size.argtypes = [P]
+        L.orc_decode.argtypes = [P, C.c_uint64, P]
+        L.orc_encode.restype = C.c_uint64
+        L.orc_encode.argtypes = [P, P]
+        L.orc_aggregate.restype = C.c_int
+        L.orc_aggregate.argtypes = [P, P, P]
+        L.orc_eval.restype = C.c_int
+        L.orc_eval.argtypes = [P, C.c_uint64, P, P, P, P, P, P]
+        L.orc_search.restype = C.c_int
+        L.orc_search.argtypes = [P, C.c_uint64, C.c_uint64, P, P, C.c_int, C.c_int, P, P, P, P]
+        L.orc_eval_list.restype = C.c_int
+        L.orc_eval_list.argtypes = [P, P, C.c_int64, P, P, C.c_int, P, P, P, P]
+        L.orc_vram_feasible.restype = C.c_uint64
+        L.orc_vram_feasible.argtypes = [P, P, C.c_uint64]
+        L.orc_bf16_round.restype = C.c_double
+        L.orc_bf16_round.argtypes = [C.c_double]
+        if hasattr(L, "orc_philox4x64"):
+            L.orc_philox4x64.argtypes = [P, P, P]
+        if hasattr(L, "orc_ga"):
+            L.orc_ga.restype = C.c_int
+            L.orc_ga.argtypes = [P, P, P, P, P, P, P]
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(C.c_void_p)
+
+
+class Problem:
+    """Holds contiguous copies of an instance's arrays and the C descriptor."""
+
+    def __init__(self, inst):
+        self.n_options = np.ascontiguousarray(inst.n_options, dtype=np.int32)
+        self.features = np.ascontiguousarray(inst.features, dtype=np.float32)
+        self.agg_cols = np.ascontiguousarray(inst.agg_cols, dtype=np.int32)
+        self.weights = np.ascontiguousarray(inst.weights, dtype=np.float32)
+        self.N = int(self.n_options.shape[0])
+        self.c = _Inst(self.N, int(inst.n_local), int(inst.n_agg), int(inst.hidden1),
+                       int(inst.hidden2), 1 if inst.dtype == "bf16" else 0,
+                       _ptr(self.n_options).value, _ptr(self.features).value,
+                       _ptr(self.agg_cols).value, int(inst.vram_slot),
+                       float(inst.vram_cap), _ptr(self.weights).value)
+        self.ref = C.byref(self.c)
+
+    @property
+    def space_size(self) -> int:
+        return int(lib().orc_space_size(self.ref))
+
+    def decode(self, idx: int) -> np.ndarray:
+        d = np.zeros(self.N, np.int32)
+        lib().orc_decode(self.ref, C.c_uint64(idx), _ptr(d))
+        return d
+
+    def encode(self, digits) -> int:
+        d = np.ascontiguousarray(digits, dtype=np.int32)
+        return int(lib().orc_encode(self.ref, _ptr(d)))
+
+    def aggregate(self, digits):
+        d = np.ascontiguousarray(digits, dtype=np.int32)
+        a = np.zeros(int(self.c.n_agg), np.float32)
+        exact = lib().orc_aggregate(self.ref, _ptr(d), _ptr(a))
+        return a, bool(exact)
+
+    def eval(self, idx: int, sla, omega):
+        sla = np.ascontiguousarray(sla, np.float32)
+        om = np.ascontiguousarray(omega, np.float32)
+        lat = np.zeros(self.N)
+        thr = np.zeros(self.N)
+        J = np.zeros(1)
+        fl = np.zeros(1, np.uint32)
+        lib().orc_eval(self.ref, C.c_uint64(idx), _ptr(sla), _ptr(om), _ptr(lat), _ptr(thr),
+                       _ptr(J), _ptr(fl))
+        return lat, thr, float(J[0]), int(fl[0])
+
+    def search(self, sla, omega, k=1, lo=0, hi=None, threads=0, dump=False):
+        """Brute force over [lo, hi).  Returns a dict with counts and top-k;
+        with dump=True also per-config flags, J and (lat, thr) predictions."""
+        if hi is None:
+            hi = self.space_size
+        sla = np.ascontiguousarray(sla, np.float32)
+        om = np.ascontiguousarray(omega, np.float32)
+        res = _Result()
+        n = hi - lo
+        fl = pr = jd = None
+        if dump:
+            fl = np.zeros(n, np.uint32)
+            pr = np.zeros((n, self.N, 2), np.float64)
+            jd = np.zeros(n, np.float64)
+        rc = lib().orc_search(self.ref, C.c_uint64(lo), C.c_uint64(hi), _ptr(sla), _ptr(om),
+                              int(k), int(threads), C.byref(res),
+                              None if fl is None else _ptr(fl),
+                              None if pr is None else _ptr(pr),
+                              None if jd is None else _ptr(jd))
+        if rc != 0:
+            raise ValueError("orc_search rejected its arguments")
+        nt = int(res.n_top)
+        out = dict(n_eval=int(res.n_eval), n_vram=int(res.n_vram), n_feas=int(res.n_feas),
+                   n_inexact_agg=int(res.n_inexact_agg), n_near=[int(x) for x in res.n_near],
+                   top_idx=np.array(res.top_idx[:nt], np.uint64),
+                   top_J=np.array(res.top_J[:nt], np.float64))
+        if dump:
+            out.update(flags=fl, pred=pr, J=jd)
+        return out
+
+    def eval_list(self, idx, sla, omega, threads=0):
+        idx = np.ascontiguousarray(idx, np.uint64)
+        n = int(idx.shape[0])
+        sla = np.ascontiguousarray(sla, np.float32)
+        om = np.ascontiguousarray(omega, np.float32)
+        lat = np.zeros((n, self.N))
+        thr = np.zeros((n, self.N))
+        J = np.zeros(n)
+        fl = np.zeros(n, np.uint32)
+        lib().orc_eval_list(self.ref, _ptr(idx), n, _ptr(sla), _ptr(om), int(threads),
+                            _ptr(lat), _ptr(thr), _ptr(J), _ptr(fl))
+        return dict(lat=lat, thr=thr, J=J, flags=fl)
+
+    def vram_feasible(self) -> np.ndarray:
+        size = self.space_size
+        buf = np.zeros(size, np.uint32)
+        cnt = int(lib().orc_vram_feasible(self.ref, _ptr(buf), size))
+        return buf[:cnt].copy()
+
+
+def bf16_round(x: float) -> float:
+    return float(lib().orc_bf16_round(float(x)))
+
+
+FLAG_VRAM, FLAG_SLA, FLAG_FEAS, FLAG_EXACT = 1, 2, 4, 8

@@ -1,0 +1,363 @@
+/*
+ * CPU oracle for the MeanField joint-configuration search.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file: only the tests, the smoke check and the benchmark's CPU
+ * baseline leg use it.  It shares no code, header, table or helper with the
+ * HIP library; the two meet only in the arrays the seeded generator draws.
+ *
+ * What it computes (plain definitions, written out):
+ *   Joint space (Section II, Eq. 1): Lambda = prod_i Lambda_i.  A joint
+ *     configuration is a linear index in lexicographic order, model 0 most
+ *     significant (the order of itertools.product).
+ *   Aggregate state (Section II, Eq. 2; Section III-B): the surrogate of model
+ *     i sees its own option row plus an aggregate field summarising the
+ *     combined resource pressure of all co-runners.  Here slot k of the
+ *     aggregate is the sum, over all N models (model i included), of option
+ *     column agg_cols[k] of the option each model runs.
+ *   Surrogate (Section III-B, Eq. 6): one MLP g_i per model,
+ *     (lat_i, thr_i) = W3 relu(W2 relu(W1 z + b1) + b2) + b3, z = [x_i | a].
+ *   Constraints (Section II, Eq. 4 and the text after it): VRAM sum <= cap
+ *     (inclusive) and a per-model latency bound lat_i <= sla_i (inclusive);
+ *     any violation gives J = -inf.
+ *   Decision (Section II): lambda* = argmax J; here J = sum_i omega_i thr_i,
+ *     ties broken to the lowest linear index, top-k sorted by (J desc,
+ *     index asc).
+ *
+ * Precision: every floating-point step is fp64.  Each dot product is one
+ * fused multiply-add chain in ascending input order, starting from the bias;
+ * relu(x) = (x > 0 ? x : +0).  The aggregate is summed in fp32 (model order)
+ * and the oracle checks it against the fp64 sum: the generator's 2**-14 grid
+ * makes them equal.  In bf16 mode the weights hold bfloat16 values and the
+ * first hidden layer (the operand of the bf16 contraction) is rounded to
+ * bfloat16, ties to even, after the relu.
+ *
+ * Build: gcc -O2 -fopenmp -ffp-contract=off -march=x86-64-v3 -shared -fPIC.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <omp.h>
+
+#define ORC_MAX_MODELS 16
+#define ORC_MAX_TOPK 64
+#define ORC_MAX_AGG 16
+
+typedef struct {
+    int32_t n_models, n_local, n_agg, hidden1, hidden2, bf16;
+    const int32_t *n_options;   /* [N] */
+    const float *features;      /* [sum K][L] row-major, model i at offset sum_{j<i} K_j */
+    const int32_t *agg_cols;    /* [A] */
+    int32_t vram_slot;
+    float vram_cap;
+    const float *weights;       /* [N][stride]: W1[h1][L+A] b1[h1] W2[h2][h1] b2[h2] W3[2][h2] b3[2] */
+} orc_instance;
+
+typedef struct {
+    uint64_t n_eval, n_vram, n_feas;
+    uint64_t n_inexact_agg;     /* configs whose fp32 aggregate differs from fp64 (expected 0) */
+    uint64_t n_near[4];         /* (config, model) pairs with |lat - sla| <= {1e-5,1e-4,1e-3,2e-2} */
+    int32_t n_top;
+    int32_t pad;
+    uint64_t top_idx[ORC_MAX_TOPK];
+    double top_J[ORC_MAX_TOPK];
+} orc_result;
+
+/* ---------------------------------------------------------------- helpers */
+
+static int64_t stride_of(const orc_instance *in)
+{
+    int64_t nin = in->n_local + in->n_agg;
+    return (int64_t)in->hidden1 * nin + in->hidden1 + (int64_t)in->hidden2 * in->hidden1 +
+           in->hidden2 + 2 * in->hidden2 + 2;
+}
+
+/* Nearest bfloat16 value (8 significant bits), ties to even; x finite. */
+static double bf16_round(double x)
+{
+    if (x == 0.0) return x;
+    int e;
+    frexp(fabs(x), &e);                 /* |x| = m * 2^e, m in [0.5, 1) */
+    if (e < -125) e = -125;             /* bf16 subnormal spacing 2^-133 */
+    double scale = ldexp(1.0, 8 - e);   /* |x| * scale in [128, 256) */
+    return nearbyint(x * scale) / scale;
+}
+
+uint64_t orc_space_size(const orc_instance *in)
+{
+    uint64_t s = 1;
+    for (int i = 0; i < in->n_models; i++) {
+        uint64_t k = (uint64_t)in->n_options[i];
+        if (k == 0) return 0;
+        if (s > UINT64_MAX / k) return 0;   /* does not fit */
+        s *= k;
+    }
+    return s;
+}
+
+/* Eq. 1: mixed-radix digits, model N-1 least significant. */
+void orc_decode(const orc_instance *in, uint64_t idx, int32_t *digits)
+{
+    for (int i = in->n_models - 1; i >= 0; i--) {
+        uint64_t k = (uint64_t)in->n_options[i];
+        digits[i] = (int32_t)(idx % k);
+        idx /= k;
+    }
+}
+
+uint64_t orc_encode(const orc_instance *in, const int32_t *digits)
+{
+    uint64_t idx = 0;
+    for (int i = 0; i < in->n_models; i++) idx = idx * (uint64_t)in->n_options[i] + (uint64_t)digits[i];
+    return idx;
+}
+
+/* Aggregate field: slot k = sum over all models of column agg_cols[k] of the
+ * chosen option row.  Returns 1 when the fp32 sum equals the fp64 sum. */
+int orc_aggregate(const orc_instance *in, const int32_t *digits, float *a)
+{
+    int exact = 1;
+    for (int k = 0; k < in->n_agg; k++) {
+        float s32 = 0.0f;
+        double s64 = 0.0;
+        int64_t off = 0;
+        for (int i = 0; i < in->n_models; i++) {
+            float v = in->features[(off + digits[i]) * in->n_local + in->agg_cols[k]];
+            s32 = s32 + v;
+            s64 = s64 + (double)v;
+            off += in->n_options[i];
+        }
+        a[k] = s32;
+        if ((double)s32 != s64) exact = 0;
+    }
+    return exact;
+}
+
+/* One model's surrogate, canonical fp64.  w: fp64 copy of that model's packed
+ * weights.  z: [L + A] inputs.  y[0] latency, y[1] throughput. */
+static void mlp_forward(const double *w, int nin, int h1n, int h2n, int bf16,
+                        const double *z, double *h1, double *h2, double *y)
+{
+    const double *W1 = w, *b1 = W1 + (int64_t)h1n * nin, *W2 = b1 + h1n,
+                 *b2 = W2 + (int64_t)h2n * h1n, *W3 = b2 + h2n, *b3 = W3 + 2 * h2n;
+    for (int u = 0; u < h1n; u++) {
+        double c = b1[u];
+        for (int k = 0; k < nin; k++) c = fma(W1[(int64_t)u * nin + k], z[k], c);
+        c = c > 0.0 ? c : 0.0;
+        h1[u] = bf16 ? bf16_round(c) : c;
+    }
+    for (int v = 0; v < h2n; v++) {
+        double c = b2[v];
+        for (int u = 0; u < h1n; u++) c = fma(W2[(int64_t)v * h1n + u], h1[u], c);
+        h2[v] = c > 0.0 ? c : 0.0;
+    }
+    for (int o = 0; o < 2; o++) {
+        double c = b3[o];
+        for (int v = 0; v < h2n; v++) c = fma(W3[(int64_t)o * h2n + v], h2[v], c);
+        y[o] = c;
+    }
+}
+
+static double *weights_to_f64(const orc_instance *in)
+{
+    int64_t n = stride_of(in) * in->n_models;
+    double *w = (double *)malloc(sizeof(double) * (size_t)n);
+    if (!w) return NULL;
+    for (int64_t t = 0; t < n; t++) w[t] = (double)in->weights[t];
+    return w;
+}
+
+/* Full evaluation of one joint configuration.
+ * flags: bit0 VRAM ok, bit1 every latency bound met, bit2 feasible,
+ *        bit3 aggregate exact; bit (8+i): model i misses its latency bound. */
+static void eval_one(const orc_instance *in, const double *w64, uint64_t idx,
+                     const float *sla, const float *omega, double *lat, double *thr,
+                     double *J, uint32_t *flags, double *scratch)
+{
+    const int N = in->n_models, L = in->n_local, A = in->n_agg, nin = L + A;
+    const int64_t stride = stride_of(in);
+    int32_t d[ORC_MAX_MODELS];
+    float a[ORC_MAX_AGG];
+    double *z = scratch, *h1 = z + nin, *h2 = h1 + in->hidden1;
+    orc_decode(in, idx, d);
+    int exact = orc_aggregate(in, d, a);
+    int vram_ok = (double)a[in->vram_slot] <= (double)in->vram_cap;
+    int sla_ok = 1;
+    uint32_t f = 0;
+    int64_t off = 0;
+    for (int i = 0; i < N; i++) {
+        const float *x = in->features + (off + d[i]) * L;
+        for (int k = 0; k < L; k++) z[k] = (double)x[k];
+        for (int k = 0; k < A; k++) z[L + k] = (double)a[k];
+        double y[2];
+        mlp_forward(w64 + stride * i, nin, in->hidden1, in->hidden2, in->bf16, z, h1, h2, y);
+        lat[i] = y[0];
+        thr[i] = y[1];
+        if (!(y[0] <= (double)sla[i])) { sla_ok = 0; f |= 1u << (8 + i); }
+        off += in->n_options[i];
+    }
+    int feas = vram_ok && sla_ok;
+    double j = -INFINITY;
+    if (feas) {
+        j = 0.0;
+        for (int i = 0; i < N; i++) j = fma((double)omega[i], thr[i], j);
+    }
+    f |= (uint32_t)vram_ok | ((uint32_t)sla_ok << 1) | ((uint32_t)feas << 2) | ((uint32_t)exact << 3);
+    *J = j;
+    *flags = f;
+}
+
+static size_t scratch_doubles(const orc_instance *in)
+{
+    return (size_t)(in->n_local + in->n_agg + in->hidden1 + in->hidden2);
+}
+
+int orc_eval(const orc_instance *in, uint64_t idx, const float *sla, const float *omega,
+             double *lat, double *thr, double *J, uint32_t *flags)
+{
+    double *w64 = weights_to_f64(in);
+    double *scr = (double *)malloc(sizeof(double) * scratch_doubles(in));
+    if (!w64 || !scr) { free(w64); free(scr); return -1; }
+    eval_one(in, w64, idx, sla, omega, lat, thr, J, flags, scr);
+    free(w64);
+    free(scr);
+    return 0;
+}
+
+/* (J desc, idx asc) */
+static int better(double ja, uint64_t ia, double jb, uint64_t ib)
+{
+    return ja > jb || (ja == jb && ia < ib);
+}
+
+static void topk_insert(double *tj, uint64_t *ti, int *cnt, int k, double j, uint64_t idx)
+{
+    if (*cnt == k && !better(j, idx, tj[k - 1], ti[k - 1])) return;
+    int p = (*cnt < k) ? (*cnt)++ : k - 1;
+    while (p > 0 && better(j, idx, tj[p - 1], ti[p - 1])) {
+        tj[p] = tj[p - 1];
+        ti[p] = ti[p - 1];
+        p--;
+    }
+    tj[p] = j;
+    ti[p] = idx;
+}
+
+/* Brute force over [lo, hi).  flag_dump: (hi-lo) x uint32 flags or NULL.
+ * pred_dump: (hi-lo) x N x 2 doubles (lat, thr) or NULL.
+ * J_dump: (hi-lo) doubles or NULL.  Returns 0, or -1 on bad arguments. */
+int orc_search(const orc_instance *in, uint64_t lo, uint64_t hi, const float *sla,
+               const float *omega, int k, int nthreads, orc_result *out,
+               uint32_t *flag_dump, double *pred_dump, double *J_dump)
+{
+    const int N = in->n_models;
+    uint64_t size = orc_space_size(in);
+    if (N < 1 || N > ORC_MAX_MODELS || in->n_agg > ORC_MAX_AGG || k < 1 || k > ORC_MAX_TOPK ||
+        size == 0 || lo > hi || hi > size)
+        return -1;
+    double *w64 = weights_to_f64(in);
+    if (!w64) return -1;
+    memset(out, 0, sizeof(*out));
+    const double bands[4] = {1e-5, 1e-4, 1e-3, 2e-2};
+    double gJ[ORC_MAX_TOPK];
+    uint64_t gI[ORC_MAX_TOPK];
+    int gcnt = 0;
+    uint64_t n_vram = 0, n_feas = 0, n_inexact = 0, near[4] = {0, 0, 0, 0};
+    const int64_t n = (int64_t)(hi - lo);
+    if (nthreads < 1) nthreads = omp_get_max_threads();
+#pragma omp parallel num_threads(nthreads)
+    {
+        double tj[ORC_MAX_TOPK];
+        uint64_t ti[ORC_MAX_TOPK];
+        int tcnt = 0;
+        uint64_t lv = 0, lf = 0, lx = 0, ln[4] = {0, 0, 0, 0};
+        double lat[ORC_MAX_MODELS], thr[ORC_MAX_MODELS];
+        double *scr = (double *)malloc(sizeof(double) * scratch_doubles(in));
+#pragma omp for schedule(static)
+        for (int64_t t = 0; t < n; t++) {
+            uint64_t idx = lo + (uint64_t)t;
+            double J;
+            uint32_t f;
+            eval_one(in, w64, idx, sla, omega, lat, thr, &J, &f, scr);
+            lv += f & 1u;
+            lf += (f >> 2) & 1u;
+            lx += ((f >> 3) & 1u) ^ 1u;
+            for (int i = 0; i < N; i++) {
+                double dlt = fabs(lat[i] - (double)sla[i]);
+                for (int b = 0; b < 4; b++) ln[b] += dlt <= bands[b];
+            }
+            if ((f >> 2) & 1u) topk_insert(tj, ti, &tcnt, k, J, idx);
+            if (flag_dump) flag_dump[t] = f;
+            if (J_dump) J_dump[t] = J;
+            if (pred_dump)
+                for (int i = 0; i < N; i++) {
+                    pred_dump[((size_t)t * N + i) * 2 + 0] = lat[i];
+                    pred_dump[((size_t)t * N + i) * 2 + 1] = thr[i];
+                }
+        }
+#pragma omp critical
+        {
+            n_vram += lv;
+            n_feas += lf;
+            n_inexact += lx;
+            for (int b = 0; b < 4; b++) near[b] += ln[b];
+            for (int q = 0; q < tcnt; q++) topk_insert(gJ, gI, &gcnt, k, tj[q], ti[q]);
+        }
+        free(scr);
+    }
+    out->n_eval = (uint64_t)n;
+    out->n_vram = n_vram;
+    out->n_feas = n_feas;
+    out->n_inexact_agg = n_inexact;
+    for (int b = 0; b < 4; b++) out->n_near[b] = near[b];
+    out->n_top = gcnt;
+    for (int q = 0; q < ORC_MAX_TOPK; q++) {
+        out->top_idx[q] = q < gcnt ? gI[q] : UINT64_MAX;
+        out->top_J[q] = q < gcnt ? gJ[q] : -INFINITY;
+    }
+    free(w64);
+    return 0;
+}
+
+/* Canonical evaluation of a list of configurations (sampled parity at sizes
+ * too large for brute force).  lat/thr: [n][N]; J, flags: [n]. */
+int orc_eval_list(const orc_instance *in, const uint64_t *idx, int64_t n, const float *sla,
+                  const float *omega, int nthreads, double *lat, double *thr, double *J,
+                  uint32_t *flags)
+{
+    const int N = in->n_models;
+    double *w64 = weights_to_f64(in);
+    if (!w64) return -1;
+    if (nthreads < 1) nthreads = omp_get_max_threads();
+#pragma omp parallel num_threads(nthreads)
+    {
+        double *scr = (double *)malloc(sizeof(double) * scratch_doubles(in));
+#pragma omp for schedule(static)
+        for (int64_t t = 0; t < n; t++)
+            eval_one(in, w64, idx[t], sla, omega, lat + t * N, thr + t * N, J + t, flags + t, scr);
+        free(scr);
+    }
+    free(w64);
+    return 0;
+}
+
+/* Ascending list of the VRAM-feasible indices (the constructed feasible space
+ * of Section II).  Returns the count; writes at most cap entries. */
+uint64_t orc_vram_feasible(const orc_instance *in, uint32_t *list, uint64_t cap)
+{
+    uint64_t size = orc_space_size(in), cnt = 0;
+    int32_t d[ORC_MAX_MODELS];
+    float a[ORC_MAX_AGG];
+    for (uint64_t idx = 0; idx < size; idx++) {
+        orc_decode(in, idx, d);
+        orc_aggregate(in, d, a);
+        if ((double)a[in->vram_slot] <= (double)in->vram_cap) {
+            if (cnt < cap) list[cnt] = (uint32_t)idx;
+            cnt++;
+        }
+    }
+    return cnt;
+}
+
+double orc_bf16_round(double x) { return bf16_round(x); }

@@ -1,0 +1,298 @@
+"""Seeded synthetic scheduling instances shaped like the paper's workloads.
+
+The paper (Section II) schedules N co-running inference models on one GPU.
+Model i exposes a discrete option set Lambda_i = V_i x P_i (variants x runtime
+parameters); the LLM family and the vision family are the two model types.
+Its surrogate (Section III-B, Eq. 6) is one small MLP per model fed the model's
+local configuration and the aggregate GPU state.  The paper's profiling tables
+and trained weights are not published, so every table here is drawn from a
+seeded PCG64 stream with the shapes the paper describes.
+
+This module draws inputs only.  It holds no step of the method (no decode, no
+aggregate, no surrogate evaluation, no masking or scoring): both the HIP path
+and the CPU oracle receive the arrays it returns.
+
+Feature columns of an option row (L >= 8):
+  0  LLM one-hot          (constant per model: a model is one family)
+  1  vision one-hot
+  2  log2 batch           integer in {0..5}
+  3  SM share             U[0.1, 1]
+  4  VRAM (GB)            U[1, 40]
+  5  bandwidth demand     U[0.05, 0.6]
+  6+ noise                U[0, 1]
+Continuous columns are quantised to multiples of 2**-14, so every aggregate
+sum of at most 16 rows is exact in fp32 whatever the summation order.
+
+Aggregate slots (each the sum over all N models of one option column):
+  A=4: [sum SM, sum VRAM, sum BW, #LLM]
+  A=6: + [#vision, sum log2 batch]
+  A=8: + [sum noise6, sum noise7]
+
+Weights are N(0, 1/fan_in), biases 0, and input standardisation (per-column
+mean and SD of the local features; mean and SD of each aggregate slot under a
+uniform choice per model) is folded into the first layer, as a trained
+surrogate with standardised inputs would carry it.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+import numpy as np
+
+GRID = 2.0 ** -14
+COL_LLM, COL_VIS, COL_LOG2B, COL_SM, COL_VRAM, COL_BW = 0, 1, 2, 3, 4, 5
+AGG_COLS = {4: [COL_SM, COL_VRAM, COL_BW, COL_LLM],
+            6: [COL_SM, COL_VRAM, COL_BW, COL_LLM, COL_VIS, COL_LOG2B],
+            8: [COL_SM, COL_VRAM, COL_BW, COL_LLM, COL_VIS, COL_LOG2B, 6, 7]}
+VRAM_SLOT = 1
+N_OUT = 2                       # [0] latency, [1] throughput
+Z75 = 0.6744897501960817        # standard normal 75th percentile
+
+
+def model_stride(n_in: int, h1: int, h2: int) -> int:
+    """Floats per model in the packed weight block:
+    W1[h1][n_in], b1[h1], W2[h2][h1], b2[h2], W3[2][h2], b3[2]."""
+    return h1 * n_in + h1 + h2 * h1 + h2 + N_OUT * h2 + N_OUT
+
+
+def unpack_model(weights_row: np.ndarray, n_in: int, h1: int, h2: int):
+    """Split one model's packed weight row into (W1, b1, W2, b2, W3, b3) views."""
+    o = 0
+    out = []
+    for shape in ((h1, n_in), (h1,), (h2, h1), (h2,), (N_OUT, h2), (N_OUT,)):
+        size = int(np.prod(shape))
+        out.append(weights_row[o:o + size].reshape(shape))
+        o += size
+    return tuple(out)
+
+
+def _quantise(v: np.ndarray) -> np.ndarray:
+    return np.round(v / GRID) * GRID
+
+
+def _to_bf16_values(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to bfloat16 (via fp32, ties to even); return fp32."""
+    f = np.ascontiguousarray(x, dtype=np.float32)
+    b = f.view(np.uint32).astype(np.uint64)
+    b = (b + 0x7FFF + ((b >> 16) & 1)) & 0xFFFF0000
+    return b.astype(np.uint32).view(np.float32)
+
+
+@dataclass
+class Instance:
+    name: str
+    n_options: np.ndarray          # int32 [N]
+    model_type: np.ndarray         # int32 [N], 0 = LLM, 1 = vision
+    n_local: int
+    n_agg: int
+    hidden1: int
+    hidden2: int
+    features: np.ndarray           # float32 [sum K][L]
+    agg_cols: np.ndarray           # int32 [A]
+    vram_slot: int
+    vram_cap: float                # fp32 value
+    weights: np.ndarray            # float32 [N][model_stride]
+    sla: np.ndarray                # float32 [N] latency bound per model
+    omega: np.ndarray              # float32 [N] objective weight per model
+    dtype: str = "f32"             # "f32" or "bf16" (W1, W2, W3 hold bf16 values)
+    top_k: int = 1
+    seed: int = 0
+    extra: dict = field(default_factory=dict)
+
+    @property
+    def n_models(self) -> int:
+        return int(self.n_options.shape[0])
+
+    @property
+    def n_in(self) -> int:
+        return self.n_local + self.n_agg
+
+    @property
+    def space_size(self) -> int:
+        return int(np.prod([int(k) for k in self.n_options], dtype=object))
+
+    @property
+    def option_offsets(self) -> np.ndarray:
+        return np.concatenate([[0], np.cumsum(self.n_options)[:-1]]).astype(np.int64)
+
+    def model_weights(self, i: int):
+        return unpack_model(self.weights[i], self.n_in, self.hidden1, self.hidden2)
+
+
+def make_instance(n_options, n_local=8, n_agg=4, hidden1=32, hidden2=32, *,
+                  seed=0, dtype="f32", vram_cap=None, vram_quantile=None,
+                  sla_range=(0.5, 2.0), top_k=1, types=None,
+                  symmetric=False, name="custom") -> Instance:
+    """Draw one instance.
+
+    n_options: option count per model.  types: per-model family (0 LLM, 1
+    vision); default: the first ceil(N/2) models are LLMs, as in the paper's
+    N=2 (one LLM, one YOLO) and N=5 (three LLMs, two YOLO) mixes.
+    vram_cap: fixed cap in GB; vram_quantile: cap set at that quantile of the
+    normal approximation to the joint VRAM sum (a uniform choice per model).
+    symmetric: copy model 0's option table and weights to every model (all
+    options counts must agree).
+    """
+    n_options = np.asarray(n_options, dtype=np.int32)
+    N = int(n_options.shape[0])
+    if n_local < 8:
+        raise ValueError("n_local must be >= 8 (the column layout needs 8)")
+    if n_agg not in AGG_COLS:
+        raise ValueError(f"n_agg must be one of {sorted(AGG_COLS)}")
+    if types is None:
+        types = [0 if i < (N + 1) // 2 else 1 for i in range(N)]
+    types = np.asarray(types, dtype=np.int32)
+    rng = np.random.Generator(np.random.PCG64(seed))
+    L, A = n_local, n_agg
+    n_in = L + A
+
+    # --- option tables ---
+    rows = []
+    for i in range(N):
+        K = int(n_options[i])
+        f = np.zeros((K, L), dtype=np.float64)
+        f[:, COL_LLM] = 1.0 if types[i] == 0 else 0.0
+        f[:, COL_VIS] = 1.0 if types[i] == 1 else 0.0
+        f[:, COL_LOG2B] = rng.integers(0, 6, K)
+        f[:, COL_SM] = _quantise(rng.uniform(0.1, 1.0, K))
+        f[:, COL_VRAM] = _quantise(rng.uniform(1.0, 40.0, K))
+        f[:, COL_BW] = _quantise(rng.uniform(0.05, 0.6, K))
+        f[:, 6:] = _quantise(rng.uniform(0.0, 1.0, (K, L - 6)))
+        rows.append(f)
+    if symmetric:
+        if len(set(int(k) for k in n_options)) != 1:
+            raise ValueError("symmetric instances need equal option counts")
+        rows = [rows[0].copy() for _ in range(N)]
+        types[:] = types[0]
+    feats64 = np.concatenate(rows, axis=0)
+    agg_cols = np.asarray(AGG_COLS[A], dtype=np.int32)
+
+    # --- standardisation statistics (generator-side weight synthesis) ---
+    mu_loc = feats64.mean(axis=0)
+    sd_loc = feats64.std(axis=0)
+    mu_agg = np.zeros(A)
+    var_agg = np.zeros(A)
+    for i in range(N):
+        for j, c in enumerate(agg_cols):
+            mu_agg[j] += rows[i][:, c].mean()
+            var_agg[j] += rows[i][:, c].var()
+    sd_agg = np.sqrt(var_agg)
+    mu = np.concatenate([mu_loc, mu_agg])
+    sd = np.concatenate([sd_loc, sd_agg])
+    sd[sd == 0.0] = 1.0
+
+    # --- surrogate weights ---
+    stride = model_stride(n_in, hidden1, hidden2)
+    weights = np.zeros((N, stride), dtype=np.float32)
+    for i in range(N):
+        W1 = rng.standard_normal((hidden1, n_in)) / np.sqrt(n_in)
+        W2 = rng.standard_normal((hidden2, hidden1)) / np.sqrt(hidden1)
+        W3 = rng.standard_normal((N_OUT, hidden2)) / np.sqrt(hidden2)
+        W1f = W1 / sd[None, :]
+        b1f = -(W1f @ mu)
+        if dtype == "bf16":
+            W1q, W2q, W3q = (_to_bf16_values(w) for w in (W1f, W2, W3))
+        elif dtype == "f32":
+            W1q, W2q, W3q = (w.astype(np.float32) for w in (W1f, W2, W3))
+        else:
+            raise ValueError("dtype must be 'f32' or 'bf16'")
+        parts = [W1q.ravel(), b1f.astype(np.float32), W2q.ravel(),
+                 np.zeros(hidden2, np.float32), W3q.ravel(), np.zeros(N_OUT, np.float32)]
+        weights[i] = np.concatenate(parts)
+    if symmetric:
+        weights[1:] = weights[0]
+
+    # --- constraint parameters ---
+    lo, hi = sla_range
+    sla = rng.uniform(lo, hi, N).astype(np.float32)
+    if symmetric:
+        sla[:] = sla[0]
+    omega = np.ones(N, dtype=np.float32)
+    if vram_cap is None:
+        if vram_quantile is None:
+            raise ValueError("give vram_cap or vram_quantile")
+        m = sum(r[:, COL_VRAM].mean() for r in rows)
+        v = sum(r[:, COL_VRAM].var() for r in rows)
+        z = {0.75: Z75}.get(vram_quantile)
+        if z is None:
+            from statistics import NormalDist
+            z = NormalDist().inv_cdf(vram_quantile)
+        vram_cap = m + z * np.sqrt(v)
+    return Instance(name=name, n_options=n_options, model_type=types, n_local=L,
+                    n_agg=A, hidden1=hidden1, hidden2=hidden2,
+                    features=feats64.astype(np.float32), agg_cols=agg_cols,
+                    vram_slot=VRAM_SLOT, vram_cap=float(np.float32(vram_cap)),
+                    weights=weights, sla=sla, omega=omega, dtype=dtype,
+                    top_k=top_k, seed=seed)
+
+
+# ---------------------------------------------------------------------------
+# The five workloads (sizes from the scheduling study: N=2..8 models)
+# ---------------------------------------------------------------------------
+
+def cfg0(seed=0) -> Instance:
+    """N=2, 6 options each (36 joint configs), 12->32->32->2 fp32, VRAM cap
+    80 GB, argmax."""
+    return make_instance([6, 6], 8, 4, 32, 32, seed=seed, vram_cap=80.0,
+                         top_k=1, name="n2_k6x6_h32")
+
+
+def cfg1(seed=0) -> Instance:
+    """N=5, options (12,12,9,9,9) = 104,976 joint configs, same MLP; VRAM cap
+    at the 75th percentile of the joint VRAM sum (about 78k feasible); top-16."""
+    return make_instance([12, 12, 9, 9, 9], 8, 4, 32, 32, seed=seed,
+                         vram_quantile=0.75, top_k=16, name="n5_k12x12x9x9x9_h32")
+
+
+def cfg2(seed=0) -> Instance:
+    """N=6, 24 options each (191,102,976 joint configs), L=16, A=6,
+    22->64->64->2 fp32, VRAM cap 200 GB, argmax + feasible count."""
+    return make_instance([24] * 6, 16, 6, 64, 64, seed=seed, vram_cap=200.0,
+                         top_k=1, name="n6_k24_h64")
+
+
+def cfg4(seed=0) -> Instance:
+    """N=8, 16 options each (2**32 joint configs), L=32, A=8,
+    40->256->256->2 with bf16 weights, VRAM cap 288 GB, top-64."""
+    return make_instance([16] * 8, 32, 8, 256, 256, seed=seed, vram_cap=288.0,
+                         dtype="bf16", top_k=64, name="n8_k16_h256_bf16")
+
+
+@dataclass
+class GAScenarios:
+    sla: np.ndarray      # float32 [S][N]
+    omega: np.ndarray    # float32 [S][N]
+
+
+def ga_scenarios(n_models: int, n_scen: int = 64, seed: int = 0) -> GAScenarios:
+    """Scenario s re-draws the per-model latency bounds U[0.5, 2.0] and the
+    objective weights U[0.5, 1.5] from PCG64(seed*1000 + s)."""
+    sla = np.zeros((n_scen, n_models), np.float32)
+    om = np.zeros((n_scen, n_models), np.float32)
+    for s in range(n_scen):
+        r = np.random.Generator(np.random.PCG64(seed * 1000 + s))
+        sla[s] = r.uniform(0.5, 2.0, n_models)
+        om[s] = r.uniform(0.5, 1.5, n_models)
+    return GAScenarios(sla=sla, omega=om)
+
+
+@dataclass
+class GAParams:
+    n_scen: int = 64
+    pop: int = 2048
+    gens: int = 100          # offspring generations; (gens + 1) * pop evaluations per scenario
+    tourn_k: int = 3
+    p_cx: float = 0.7
+    p_swap: float = 0.5
+    p_mut: float = 0.05
+    seed: int = 0
+
+
+def cfg3(seed=0):
+    """GA at N=5 on the N=5 instance: 64 scenarios, population 2048,
+    100 generations, tournament 3, crossover 0.7 (uniform), mutation 0.05."""
+    inst = cfg1(seed)
+    inst.name = "ga_n5_s64_p2048_g100"
+    return inst, ga_scenarios(inst.n_models, 64, seed), GAParams(seed=seed)
+
+
+CONFIGS = {"cfg0": cfg0, "cfg1": cfg1, "cfg2": cfg2, "cfg4": cfg4}

@@ -1,0 +1,340 @@
+"""Pins for the CPU oracle, against facts fixed outside the oracle itself.
+
+Each pin is chosen so that a plausible mistake (a dropped term, a wrong sign
+or index, a transposed operand, an exclusive bound, a wrong tie-break) fails
+at least one of them:
+  * a hand-computed instance with integer weights (values worked out below);
+  * the MLP against torch.float64 F.linear (a library routine);
+  * decode against itertools.product (the definition of lexicographic order)
+    and the closed-form space sizes, including the paper's N=2 and N=5 ones;
+  * the aggregate: closed-form sum over the space and bitwise invariance under
+    relabelling the models;
+  * the VRAM-feasible count against a meet-in-the-middle count;
+  * top-k against an independent numpy brute force with np.lexsort;
+  * the lowest-index tie-break on a symmetric instance (exact ties);
+  * bfloat16 rounding against torch's conversion.
+"""
+import itertools
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_02109_amd import synth
+
+# --------------------------------------------------------------------------
+# Hand-computed instance: N=2, K=(2,2), L=2, A=1 (slot 0 = sum of column 0,
+# also the VRAM slot), H1=H2=2.
+# --------------------------------------------------------------------------
+HAND_FEATURES = np.array([[1, 2], [3, 1],      # model 0, options 0 and 1
+                          [0, 1], [2, 2]],     # model 1, options 0 and 1
+                         dtype=np.float32)
+# per model: W1[2][3] b1[2] W2[2][2] b2[2] W3[2][2] b3[2]
+HAND_W0 = [1, 0, 1, 0, 1, -1, 0, 1, 1, 1, 1, -1, 0, 0, 1, 0, 0, 2, 0, 1]
+HAND_W1 = [2, -1, 0, 1, 1, -2, -1, 0, 1, 0, -1, 1, 1, 0, 0, 1, 1, 1, -1, 0]
+
+
+def hand_instance(vram_cap=4.0, sla=(5.0, 0.0), omega=(1.0, 1.0), bf16=False, w0=None):
+    w = np.array([w0 if w0 is not None else HAND_W0, HAND_W1], np.float32)
+    return synth.Instance(name="hand", n_options=np.array([2, 2], np.int32),
+                          model_type=np.array([0, 1], np.int32), n_local=2, n_agg=1,
+                          hidden1=2, hidden2=2, features=HAND_FEATURES,
+                          agg_cols=np.array([0], np.int32), vram_slot=0,
+                          vram_cap=vram_cap, weights=w,
+                          sla=np.array(sla, np.float32), omega=np.array(omega, np.float32),
+                          dtype="bf16" if bf16 else "f32")
+
+
+# Worked by hand (z = [x0, x1, a], a = x_model0[0] + x_model1[0]):
+# idx 0 = (0,0): a=1.  model 0: s1=(2,2) h2=(4,0) y=(4,1);  model 1: s1=(-2,-1)
+#                h1=(0,0) s2=(1,0) y=(-1,1).                         J = 1+1 = 2
+# idx 1 = (0,1): a=3.  model 0: h1=(4,0) h2=(4,4) y=(4,9); model 1: h1=(1,0)
+#                h2=(2,0) y=(-1,2).                                  J = 9+2 = 11
+# idx 2 = (1,0): a=3.  model 0: h1=(6,0) h2=(6,6) y=(6,13); model 1: y=(-1,1)
+#                latency 6 > 5 violates model 0's bound.             J = -inf
+# idx 3 = (1,1): a=5 > 4 violates the VRAM cap. model 0: y=(8,17); model 1:
+#                y=(-1,2).                                           J = -inf
+HAND_LAT = np.array([[4, -1], [4, -1], [6, -1], [8, -1]], float)
+HAND_THR = np.array([[1, 1], [9, 2], [13, 1], [17, 2]], float)
+
+
+def test_hand_instance_values(orc):
+    p = orc.Problem(hand_instance())
+    inst = hand_instance()
+    r = p.search(inst.sla, inst.omega, k=4, dump=True)
+    np.testing.assert_array_equal(r["pred"][:, :, 0], HAND_LAT)
+    np.testing.assert_array_equal(r["pred"][:, :, 1], HAND_THR)
+    assert r["n_vram"] == 3 and r["n_feas"] == 2
+    assert list(r["top_idx"]) == [1, 0]
+    assert list(r["top_J"]) == [11.0, 2.0]
+    fl = r["flags"]
+    assert [int(f) & orc.FLAG_VRAM for f in fl] == [1, 1, 1, 0]
+    assert [bool(int(f) & orc.FLAG_FEAS) for f in fl] == [True, True, False, False]
+    assert r["J"][2] == -math.inf and r["J"][3] == -math.inf
+
+
+def test_hand_instance_weights_and_inclusive_bounds(orc):
+    # objective weights: J = 2*thr0 + 0.5*thr1
+    inst = hand_instance(omega=(2.0, 0.5))
+    r = orc.Problem(inst).search(inst.sla, inst.omega, k=2)
+    assert list(r["top_J"]) == [19.0, 2.5]
+    # VRAM bound is inclusive: cap 3 keeps the configs whose sum is exactly 3
+    inst = hand_instance(vram_cap=3.0)
+    assert orc.Problem(inst).search(inst.sla, inst.omega)["n_vram"] == 3
+    # latency bound is inclusive: bound 4 keeps latency exactly 4
+    inst = hand_instance(sla=(4.0, 0.0))
+    r = orc.Problem(inst).search(inst.sla, inst.omega, k=2)
+    assert r["n_feas"] == 2 and list(r["top_idx"]) == [1, 0]
+    # model 1's bound below its latency -1 makes everything infeasible
+    inst = hand_instance(sla=(5.0, -1.5))
+    r = orc.Problem(inst).search(inst.sla, inst.omega, k=2)
+    assert r["n_feas"] == 0 and len(r["top_idx"]) == 0
+
+
+def test_hand_instance_bf16_rounding(orc):
+    # Model 0 with W1 row 0 scaled so that at idx 0 s1[0] = 1 + 3*2^-8:
+    # bf16 keeps 8 significant bits, spacing 2^-7 at 1, so the value is a tie
+    # between 1+2^-7 (odd mantissa) and 1+2^-6 (even): it rounds to 1+2^-6.
+    # Then h2 = (h1_0 + h1_1, h1_0 - h1_1) and y = (h2_0, 2*h2_1 + 1).
+    w0 = list(HAND_W0)
+    w0[6] = 1 + 3 * 2 ** -8 - 2.0      # b1[0]: s1[0] = 1 + 1 + b1[0]
+    inst = hand_instance(bf16=True, w0=w0)
+    r = orc.Problem(inst).search(inst.sla, inst.omega, k=1, dump=True)
+    h10 = 1 + 2 ** -6
+    h11 = 2.0                           # s1[1] = 2, exact in bf16
+    assert r["pred"][0, 0, 0] == h10 + h11
+    # fp32 mode keeps the unrounded value
+    inst32 = hand_instance(bf16=False, w0=w0)
+    r32 = orc.Problem(inst32).search(inst32.sla, inst32.omega, k=1, dump=True)
+    assert r32["pred"][0, 0, 0] == (1 + 3 * 2 ** -8) + 2.0
+
+
+# --------------------------------------------------------------------------
+# Decode / space size
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("K", [(6, 6), (2, 3, 4), (12, 12, 9, 9, 9), (5,), (1, 7, 1, 3)])
+def test_decode_is_itertools_product_order(orc, K):
+    inst = synth.make_instance(list(K), seed=1, vram_cap=1e9)
+    p = orc.Problem(inst)
+    prod = list(itertools.product(*[range(k) for k in K]))
+    assert p.space_size == len(prod)
+    step = max(1, len(prod) // 4000)
+    for idx in range(0, len(prod), step):
+        d = p.decode(idx)
+        assert tuple(int(x) for x in d) == prod[idx]
+        assert p.encode(d) == idx
+
+
+def test_space_sizes_closed_form(orc):
+    sizes = {"cfg0": 36, "cfg1": 104_976, "cfg2": 191_102_976, "cfg4": 2 ** 32}
+    for name, n in sizes.items():
+        inst = synth.CONFIGS[name](0)
+        assert orc.Problem(inst).space_size == n == inst.space_size
+    # the paper's N=2 space: 6 LLM options x 27 vision options = 162, under
+    # four load regimes 648 measurements; its N=5 space: three LLMs with 6, 6
+    # and 3 options (the 7B model AWQ-only) and two vision models with 27 each
+    # gives 78,732 joint configurations
+    p2 = orc.Problem(synth.make_instance([6, 27], seed=0, vram_cap=1e9))
+    assert p2.space_size == 162 and 4 * p2.space_size == 648
+    p5 = orc.Problem(synth.make_instance([6, 6, 3, 27, 27], seed=0, vram_cap=1e9))
+    assert p5.space_size == 78_732
+    # LLM options are variants {FP16, AWQ} x concurrency {1,2,4}; vision are
+    # {n,s,m} x skip {1,2,4} x image size {320,480,640}
+    assert len(list(itertools.product(range(2), range(3)))) == 6
+    assert len(list(itertools.product(range(3), range(3), range(3)))) == 27
+
+
+def test_space_size_overflow_rejected(orc):
+    inst = synth.make_instance([255] * 9, seed=0, vram_cap=1e9)
+    assert orc.Problem(inst).space_size == 0   # 255^9 > 2^64 - 1
+
+
+# --------------------------------------------------------------------------
+# Aggregate
+# --------------------------------------------------------------------------
+
+def test_aggregate_closed_form_sum(orc):
+    inst = synth.make_instance([5, 4, 3], 8, 6, seed=3, vram_cap=1e9)
+    p = orc.Problem(inst)
+    n = p.space_size
+    tot = np.zeros(inst.n_agg)
+    for idx in range(n):
+        a, exact = p.aggregate(p.decode(idx))
+        assert exact
+        tot += a.astype(np.float64)
+    off = inst.option_offsets
+    expect = np.zeros(inst.n_agg)
+    for i, K in enumerate(inst.n_options):
+        rows = inst.features[off[i]:off[i] + K].astype(np.float64)
+        expect += (n // int(K)) * rows[:, inst.agg_cols].sum(axis=0)
+    np.testing.assert_array_equal(tot, expect)
+
+
+def test_permutation_invariance(orc):
+    inst = synth.make_instance([4, 3, 5, 2], 8, 6, seed=5, vram_quantile=0.6,
+                               types=[0, 1, 0, 1])
+    perm = [2, 0, 3, 1]
+    off = inst.option_offsets
+    feats = np.concatenate([inst.features[off[i]:off[i] + inst.n_options[i]] for i in perm])
+    pinst = synth.Instance(name="perm", n_options=inst.n_options[perm],
+                           model_type=inst.model_type[perm], n_local=inst.n_local,
+                           n_agg=inst.n_agg, hidden1=inst.hidden1, hidden2=inst.hidden2,
+                           features=feats, agg_cols=inst.agg_cols, vram_slot=inst.vram_slot,
+                           vram_cap=inst.vram_cap, weights=inst.weights[perm],
+                           sla=inst.sla[perm], omega=inst.omega[perm])
+    p, q = orc.Problem(inst), orc.Problem(pinst)
+    r = p.search(inst.sla, inst.omega, k=1, dump=True)
+    s = q.search(pinst.sla, pinst.omega, k=1, dump=True)
+    assert r["n_vram"] == s["n_vram"] and r["n_feas"] == s["n_feas"]
+    for idx in range(p.space_size):
+        d = p.decode(idx)
+        jdx = q.encode(d[perm])
+        a1, _ = p.aggregate(d)
+        a2, _ = q.aggregate(d[perm])
+        assert a1.tobytes() == a2.tobytes()
+        # per-model predictions are bitwise equal after relabelling
+        assert r["pred"][idx][perm].tobytes() == s["pred"][jdx].tobytes()
+        assert (r["flags"][idx] & 7) == (s["flags"][jdx] & 7)
+
+
+# --------------------------------------------------------------------------
+# VRAM count: meet in the middle
+# --------------------------------------------------------------------------
+
+def mitm_vram_count(inst, cap):
+    """Count joint configs with sum of VRAM <= cap by splitting the models in
+    two halves, sorting one half's sums and binary-searching the other's.
+    Exact: all values lie on the 2^-14 grid."""
+    off = inst.option_offsets
+    col = inst.agg_cols[inst.vram_slot]
+    per = [inst.features[off[i]:off[i] + inst.n_options[i], col].astype(np.float64)
+           for i in range(inst.n_models)]
+    h = len(per) // 2
+
+    def sums(group):
+        s = np.zeros(1)
+        for v in group:
+            s = (s[:, None] + v[None, :]).ravel()
+        return s
+    left, right = sums(per[:h]), np.sort(sums(per[h:]))
+    return int(np.searchsorted(right, cap - left, side="right").sum())
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_vram_count_matches_meet_in_the_middle(orc, seed):
+    inst = synth.cfg1(seed)
+    r = orc.Problem(inst).search(inst.sla, inst.omega, k=1)
+    assert r["n_vram"] == mitm_vram_count(inst, float(inst.vram_cap))
+    assert 70_000 < r["n_vram"] < 86_000      # "roughly 78k" of 104,976
+
+
+def test_vram_count_special_cases(orc):
+    inst = synth.make_instance([7, 5, 6], seed=9, vram_cap=1e9)
+    p = orc.Problem(inst)
+    off = inst.option_offsets
+    vr = [inst.features[off[i]:off[i] + inst.n_options[i], synth.COL_VRAM] for i in range(3)]
+    smax = float(sum(v.max() for v in vr))
+    smin = float(sum(v.min() for v in vr))
+    for cap, expect in [(smax, p.space_size), (smin - 2 ** -14, 0), (smin, None)]:
+        inst.vram_cap = cap
+        q = orc.Problem(inst)
+        n = q.search(inst.sla, inst.omega)["n_vram"]
+        if expect is None:
+            assert n == mitm_vram_count(inst, cap) >= 1
+        else:
+            assert n == expect
+
+
+# --------------------------------------------------------------------------
+# MLP and top-k against library routines
+# --------------------------------------------------------------------------
+
+def torch_predictions(inst):
+    """All configs' (lat, thr) with torch.float64 F.linear."""
+    K = [int(k) for k in inst.n_options]
+    digits = np.array(list(itertools.product(*[range(k) for k in K])), np.int64)
+    off = inst.option_offsets
+    rows = [inst.features[off[i] + digits[:, i]].astype(np.float64) for i in range(len(K))]
+    agg = sum(r[:, inst.agg_cols] for r in rows)
+    lat = np.zeros((len(digits), len(K)))
+    thr = np.zeros_like(lat)
+    for i in range(len(K)):
+        W1, b1, W2, b2, W3, b3 = (torch.from_numpy(np.asarray(w, np.float64))
+                                  for w in inst.model_weights(i))
+        z = torch.from_numpy(np.concatenate([rows[i], agg], axis=1))
+        h1 = torch.relu(torch.nn.functional.linear(z, W1, b1))
+        h2 = torch.relu(torch.nn.functional.linear(h1, W2, b2))
+        y = torch.nn.functional.linear(h2, W3, b3).numpy()
+        lat[:, i], thr[:, i] = y[:, 0], y[:, 1]
+    vram = agg[:, inst.vram_slot]
+    return digits, lat, thr, vram
+
+
+@pytest.mark.parametrize("maker", [lambda: synth.cfg0(0), lambda: synth.cfg0(1),
+                                   lambda: synth.make_instance([5, 7, 4], 16, 6, 64, 64, seed=4,
+                                                               vram_quantile=0.7,
+                                                               sla_range=(-0.2, 0.6))])
+def test_mlp_matches_torch_float64(orc, maker):
+    inst = maker()
+    r = orc.Problem(inst).search(inst.sla, inst.omega, k=1, dump=True)
+    _, lat, thr, vram = torch_predictions(inst)
+    scale = max(1.0, float(np.abs(r["pred"]).max()))
+    np.testing.assert_allclose(r["pred"][:, :, 0], lat, rtol=0, atol=1e-12 * scale)
+    np.testing.assert_allclose(r["pred"][:, :, 1], thr, rtol=0, atol=1e-12 * scale)
+    assert r["n_vram"] == int((vram <= inst.vram_cap).sum())
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_topk_matches_numpy_lexsort(orc, seed):
+    inst = synth.cfg1(seed)
+    k = inst.top_k
+    r = orc.Problem(inst).search(inst.sla, inst.omega, k=k)
+    _, lat, thr, vram = torch_predictions(inst)
+    feas = (vram <= inst.vram_cap) & np.all(lat <= inst.sla.astype(np.float64), axis=1)
+    J = np.where(feas, thr @ inst.omega.astype(np.float64), -np.inf)
+    idx = np.arange(len(J))
+    order = np.lexsort((idx, -J))[:k]
+    # the library sum may differ from the fused chain in the last bits: the
+    # order is compared where the gap between neighbours is well above that
+    assert r["n_feas"] == int(feas.sum())
+    np.testing.assert_allclose(r["top_J"], J[order], rtol=0, atol=1e-12)
+    gaps = np.abs(np.diff(J[order]))
+    for q in range(k):
+        if (q == 0 or gaps[q - 1] > 1e-9) and (q == k - 1 or gaps[q] > 1e-9):
+            assert int(r["top_idx"][q]) == int(order[q])
+
+
+def test_symmetric_instance_breaks_ties_to_lowest_index(orc):
+    # identical models and option tables: J(x, y) == J(y, x) exactly (the
+    # aggregate is order-free and fp addition commutes), so every optimum
+    # with x != y is tied with its mirror and the lower index must win
+    inst = synth.make_instance([9, 9], seed=11, vram_cap=1e9, symmetric=True,
+                               sla_range=(3.0, 3.0))
+    p = orc.Problem(inst)
+    r = p.search(inst.sla, inst.omega, k=4, dump=True)
+    for idx in range(p.space_size):
+        x, y = p.decode(idx)
+        assert r["J"][idx] == r["J"][p.encode([y, x])]
+    top = [int(t) for t in r["top_idx"]]
+    x, y = p.decode(top[0])
+    if x != y:
+        mirror = p.encode([y, x])
+        assert top[0] < mirror and top[1] == mirror
+        assert r["top_J"][0] == r["top_J"][1]
+
+
+# --------------------------------------------------------------------------
+# bfloat16 rounding
+# --------------------------------------------------------------------------
+
+def test_bf16_round_matches_torch(orc):
+    rng = np.random.default_rng(7)
+    vals = np.concatenate([rng.standard_normal(2000).astype(np.float32),
+                           (rng.standard_normal(500) * 1e-30).astype(np.float32),
+                           np.array([1 + 2 ** -8, 1 + 3 * 2 ** -8, -(1 + 2 ** -8), 0.0,
+                                     2 ** -130, 3 * 2 ** -134], np.float32)])
+    ref = torch.from_numpy(vals).to(torch.bfloat16).to(torch.float64).numpy()
+    got = np.array([orc.bf16_round(float(v)) for v in vals])
+    np.testing.assert_array_equal(got, ref)
