@@ -1,0 +1,211 @@
+/*
+ * mf.h: C ABI of the MeanField joint-configuration search for MI355X (gfx950).
+ *
+ * The method (Ennouri and Ha, "MeanField Surrogate Modeling for Scalable
+ * Runtime Scheduling of Concurrent Heterogeneous AI Inference on Shared GPUs"):
+ * N models share one GPU; model i runs one option from its discrete set
+ * Lambda_i (Section II); a joint configuration picks one option per model
+ * (Eq. 1).  A per-model surrogate g_i predicts the model's performance from its
+ * own option and an aggregate GPU state (Section III-B, Eq. 6); the scheduler
+ * takes the argmax of a utility J over the joint space (Section II, decision
+ * rule before Eq. 3) subject to a VRAM cap and per-model service bounds (Eq. 4);
+ * infeasible candidates score -inf and are never chosen.
+ *
+ * This library evaluates that decision step over a whole index range of the
+ * joint space (exhaustive surrogate search, Section IV-C) or over a genetic
+ * algorithm's population (the GA scheduler of Section IV-C), on the GPU.
+ *
+ * Conventions for every entry point:
+ *  - Every call returns mf_status.  Arguments are validated on the host before
+ *    anything is launched; on an error nothing has been enqueued.  No call
+ *    prints, throws or exits.
+ *  - Pointers prefixed d_ are device memory (any allocation the HIP runtime
+ *    accepts, e.g. torch tensors); h_ are host memory.  All are caller-owned
+ *    and borrowed only for the duration of the call unless stated otherwise.
+ *  - `stream` is a hipStream_t (0 = the null stream) passed as void*.
+ *  - Calls that return results on the host (mf_search, mf_ga_run) synchronise
+ *    the stream before returning.  Others only enqueue work.
+ *  - A problem may be used from several streams at once provided each call
+ *    gets its own workspace.  Calls sharing one workspace must not overlap.
+ *
+ * Definitions (all indices 0-based):
+ *  - Joint index: lexicographic order over (lambda_0, ..., lambda_{N-1}),
+ *    model 0 most significant (the order of itertools.product).
+ *  - Option table F: float [sum_i K_i][L] row-major; model i's K_i rows start
+ *    at row sum_{j<i} K_j.
+ *  - Aggregate state a (Eq. 2 recast per candidate): slot k is the fp32 sum,
+ *    in model order 0..N-1, of column agg_cols[k] of every model's chosen row
+ *    (each model's own row included).
+ *  - Surrogate of model i (Eq. 6): z = [F row of lambda_i (L) | a (A)],
+ *    h1 = relu(W1 z + b1), h2 = relu(W2 h1 + b2), (lat, thr) = W3 h2 + b3.
+ *  - Feasible: a[vram_slot] <= vram_cap and lat_i <= sla_i for every i
+ *    (both inclusive, Eq. 4).  J = sum_i omega_i thr_i if feasible, else -inf.
+ *  - Results are defined by canonical fp64 semantics: each dot product is one
+ *    fused multiply-add chain in ascending input order starting from the bias,
+ *    relu(x) = x > 0 ? x : +0, J is the fma chain over models in order.  In
+ *    MF_BF16 mode W1, W2, W3 hold bfloat16 values and h1 is rounded to
+ *    bfloat16 (nearest, ties to even) after the relu.  The GPU evaluates in
+ *    fp32 (MFMA) and re-evaluates canonically every decision the fast path
+ *    cannot prove (see mf_search), so counts, masks and top-k are exact.
+ *  - Top-k order: J descending, then index ascending.
+ */
+#ifndef MF_H
+#define MF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MF_OK = 0,
+    MF_EINVAL = 1,        /* invalid argument (null pointer, bad size, non-finite value, ...) */
+    MF_ENOMEM = 2,        /* workspace smaller than mf_workspace_size reports, or host allocation failed */
+    MF_EDEVICE = 3,       /* a HIP runtime call or kernel launch failed */
+    MF_EUNSUPPORTED = 4,  /* shape outside what the kernels are built for (see mf_desc) */
+    MF_EOVERFLOW = 5,     /* prod K_i does not fit in 64 bits, or a range bound exceeds |Lambda| */
+    MF_EINTERNAL = 6      /* a self-check failed (fast-path error bound violated); result unusable */
+} mf_status;
+
+typedef enum { MF_F32 = 0, MF_BF16 = 1 } mf_dtype;
+
+#define MF_MAX_MODELS 16
+#define MF_MAX_TOPK 64
+
+typedef struct mf_problem mf_problem;   /* opaque */
+
+/* Problem shape.  Supported: 1 <= n_models <= 16; 1 <= n_options[i] <= 255;
+ * n_local >= 1; n_agg in {2,4,6,8}; hidden1 == hidden2 in {32, 64} for MF_F32.
+ * (Other shapes return MF_EUNSUPPORTED.) */
+typedef struct {
+    int32_t n_models;           /* N */
+    int32_t n_local;            /* L: local features per option row */
+    int32_t n_agg;              /* A: aggregate slots */
+    int32_t hidden1, hidden2;   /* H1, H2; the output layer has 2 units: [0] latency, [1] throughput */
+    const int32_t *h_n_options; /* host [N] */
+    const int32_t *h_agg_cols;  /* host [A], each in [0, L) */
+    int32_t vram_slot;          /* aggregate slot compared with vram_cap, in [0, A) */
+    float vram_cap;             /* finite */
+    mf_dtype dtype;
+} mf_desc;
+
+/* Create a problem.  d_features: float [sum K_i][L].  d_weights: float
+ * [N][S] with S = H1*(L+A) + H1 + H2*H1 + H2 + 2*H2 + 2, per model packed as
+ * W1[H1][L+A], b1[H1], W2[H2][H1], b2[H2], W3[2][H2], b3[2] (row-major).
+ * Both are copied: the caller may free them after the call returns.
+ * Validates every value is finite (and bf16-representable for MF_BF16 W*),
+ * derives the fast path's error bounds, and builds the device-resident
+ * tables (per-option first-layer precompute included) on `stream`; returns
+ * after the stream has finished that work.  The library allocates the
+ * problem's device tables itself (freed by mf_problem_destroy). */
+mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const float *d_weights,
+                            void *stream, mf_problem **out);
+void mf_problem_destroy(mf_problem *p);
+
+/* |Lambda| = prod K_i. */
+mf_status mf_space_size(const mf_problem *p, uint64_t *out);
+
+/* Host helper: digits[N] of joint index idx (idx < |Lambda|). */
+mf_status mf_decode(const mf_problem *p, uint64_t idx, int32_t *h_digits);
+
+/* ---------------------------------------------------------------- search */
+
+#define MF_DUMP 1u   /* write d_mask and d_pred for every index of [lo, hi) */
+
+typedef struct {
+    uint64_t lo, hi;           /* half-open index range, lo <= hi <= |Lambda| */
+    int32_t top_k;             /* 1..64 */
+    uint32_t flags;            /* MF_DUMP */
+    const float *d_sla;        /* device [N] latency bound per model, finite */
+    const float *d_omega;      /* device [N] objective weight per model, finite */
+    /* MF_DUMP outputs (device, hi - lo <= 2^31 entries):
+     *   d_mask[t]: bit0 VRAM ok, bit1 every latency bound met, bit2 feasible,
+     *              bit3 the fast path left a latency decision to the
+     *              canonical re-evaluation;
+     *   d_pred[(t*N + i)*2 + {0,1}]: fast-path fp32 (lat, thr) of model i. */
+    uint8_t *d_mask;
+    float *d_pred;
+} mf_search_args;
+
+typedef struct {
+    uint64_t n_eval;           /* hi - lo */
+    uint64_t n_vram;           /* VRAM-feasible configurations */
+    uint64_t n_feas;           /* feasible (VRAM and every latency bound) */
+    uint64_t n_flagged;        /* configurations re-evaluated canonically for a latency decision */
+    uint64_t n_topk_collect;   /* candidates gathered by the top-k fallback pass (0 if none ran) */
+    int32_t n_top;             /* min(top_k, n_feas) */
+    int32_t n_splits;          /* range splits forced by a full certification list */
+    uint64_t top_idx[MF_MAX_TOPK];  /* joint indices; UINT64_MAX past n_top */
+    double top_J[MF_MAX_TOPK];      /* canonical J; -inf past n_top */
+    float main_kernel_ms;      /* HIP-event time of the fast search kernel(s) on `stream` */
+    float pad;
+} mf_result;
+
+/* Bytes of device workspace mf_search needs for these arguments. */
+mf_status mf_workspace_size(const mf_problem *p, const mf_search_args *args, size_t *bytes);
+
+/* Exhaustive surrogate search over [lo, hi) (Section IV-C): counts, and the
+ * exact top-k under canonical semantics.  d_ws: device workspace of at least
+ * mf_workspace_size bytes (contents need not be initialised; 256-byte
+ * aligned).  Blocking: returns after the result is on the host in *h_out.
+ * Empty feasible set: MF_OK with n_top = 0. */
+mf_status mf_search(mf_problem *p, const mf_search_args *args, void *d_ws, size_t ws_bytes,
+                    void *stream, mf_result *h_out);
+
+/* ------------------------------------------------------------ evaluation */
+
+/* Fast-path (fp32 MFMA) predictions of an index list, as the search kernel
+ * computes them.  d_idx: device uint64 [n], each < |Lambda|.  d_pred: device
+ * float [n][N][2] (lat, thr).  Enqueues only. */
+mf_status mf_eval_fast(mf_problem *p, const uint64_t *d_idx, int64_t n, float *d_pred, void *stream);
+
+/* Canonical fp64 evaluation of an index list (the semantics results are
+ * defined by).  d_pred: device double [n][N][2]; d_J: device double [n]
+ * (-inf when infeasible); d_flags: device uint32 [n] (bit0 VRAM ok, bit1 all
+ * latency bounds met, bit2 feasible, bit 8+i model i misses its bound).  Any
+ * output may be NULL.  Enqueues only. */
+mf_status mf_eval_canonical(mf_problem *p, const uint64_t *d_idx, int64_t n, const float *d_sla,
+                            const float *d_omega, double *d_pred, double *d_J, uint32_t *d_flags,
+                            void *stream);
+
+/* -------------------------------------------------------------------- GA */
+
+/* Genetic-algorithm scheduler (Section IV-C) over S independent scenarios,
+ * each with its own latency bounds and objective weights.  Fitness is the
+ * canonical J of each individual (the same decode, aggregate, surrogate, mask
+ * and score steps as the search).  Random draws come from Philox4x64-10
+ * (Salmon et al., SC'11) keyed by `seed`; see mf_ga.hip for the counter
+ * layout and operator order. */
+typedef struct {
+    int32_t n_scen;            /* S >= 1 */
+    int32_t pop;               /* population, even, 4..4096 */
+    int32_t gens;              /* offspring generations (>= 0); (gens+1)*pop evaluations per scenario */
+    int32_t tourn_k;           /* tournament size 1..8 (with replacement) */
+    float p_cx;                /* crossover probability per parent pair */
+    float p_swap;              /* per-gene swap probability inside a crossover */
+    float p_mut;               /* per-gene mutation probability */
+    float pad;
+    uint64_t seed;
+    const float *d_sla;        /* device [S][N] */
+    const float *d_omega;      /* device [S][N] */
+} mf_ga_args;
+
+mf_status mf_ga_workspace_size(const mf_problem *p, const mf_ga_args *args, size_t *bytes);
+
+/* Runs the GA.  h_best_idx / h_best_J: host [S], the best individual ever
+ * evaluated per scenario (J desc, index asc); UINT64_MAX / -inf if none was
+ * feasible.  d_final_pop (optional, device uint64 [S][pop]): the last
+ * population's joint indices.  Blocking. */
+mf_status mf_ga_run(mf_problem *p, const mf_ga_args *args, void *d_ws, size_t ws_bytes,
+                    void *stream, uint64_t *h_best_idx, double *h_best_J, uint64_t *d_final_pop);
+
+/* Human-readable status name. */
+const char *mf_status_string(mf_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MF_H */

@@ -1,0 +1,710 @@
+// Host side of libmf: argument validation, the fast path's a-priori error
+// bounds, device tables, the search driver (range chunking, splitting on a
+// full certification list, the top-k fallback pass) and result merging.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <limits>
+#include <new>
+#include <vector>
+
+#include "mf_internal.h"
+
+using namespace mfi;
+
+struct mf_problem {
+    int N = 0, L = 0, A = 0, H1 = 0, H2 = 0;
+    bool bf16 = false;
+    std::vector<int32_t> K, agg_cols, opt_off;
+    int vram_slot = 0;
+    float vram_cap = 0.f;
+    uint64_t space = 0;
+    int64_t wstride = 0;
+    int sumK = 0;
+    bool fast_ok = false;
+    int num_cus = 0;
+    int device = 0;
+    // device memory (one allocation)
+    void *d_mem = nullptr;
+    float4 *d_image = nullptr;
+    float *d_canon = nullptr, *d_features = nullptr, *d_zeros = nullptr;
+    int32_t *d_agg_cols = nullptr, *d_row_model = nullptr;
+    FastLayout lay{};
+    FastConst fc{};
+};
+
+namespace {
+
+constexpr double kU32 = 0x1p-24;   // fp32 unit roundoff (round to nearest)
+constexpr double kU64 = 0x1p-53;   // fp64 unit roundoff
+
+double gam(double n, double u) { return n * u / (1.0 - n * u); }
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+bool all_finite(const std::vector<float> &v)
+{
+    for (float x : v)
+        if (!std::isfinite(x)) return false;
+    return true;
+}
+
+bool bf16_exact(float x)
+{
+    uint32_t b;
+    std::memcpy(&b, &x, 4);
+    return (b & 0xFFFFu) == 0u;
+}
+
+// Per model: a-priori bounds on |fast fp32 path - canonical fp64| for both
+// outputs, and a magnitude bound on throughput.  Each dot product of n terms
+// computed as any sequence of n correctly rounded fused multiply-adds (the
+// measured behaviour of v_mfma_f32_32x32x2f32 and of v_fma_f32/f64) has error
+// <= gamma_n * (|bias| + sum |w||x|) (Higham, Accuracy and Stability of
+// Numerical Algorithms, 2nd ed., Sec. 3.1).  Errors of a layer's input
+// propagate through |W| (relu is 1-Lipschitz).  Magnitudes use the largest
+// |input| over all options and all joint configurations.
+void model_bounds(const mf_problem &p, const std::vector<float> &F, const std::vector<float> &W, int i,
+                  double *b_lat, double *b_thr, double *m_thr)
+{
+    const int L = p.L, A = p.A, H1 = p.H1, H2 = p.H2, nin = L + A;
+    const float *w = W.data() + (int64_t)i * p.wstride;
+    const float *W1 = w, *b1 = W1 + (int64_t)H1 * nin, *W2 = b1 + H1, *b2 = W2 + (int64_t)H2 * H1, *W3 = b2 + H2,
+                *b3 = W3 + 2 * H2;
+    std::vector<double> xmax(L, 0.0), amax(A, 0.0);
+    for (int o = 0; o < p.K[i]; o++)
+        for (int k = 0; k < L; k++)
+            xmax[k] = std::max(xmax[k], (double)std::fabs(F[(int64_t)(p.opt_off[i] + o) * L + k]));
+    for (int j = 0; j < p.N; j++)
+        for (int k = 0; k < A; k++) {
+            double m = 0.0;
+            for (int o = 0; o < p.K[j]; o++)
+                m = std::max(m, (double)std::fabs(F[(int64_t)(p.opt_off[j] + o) * L + p.agg_cols[k]]));
+            amax[k] += m;
+        }
+    std::vector<double> M1(H1), e1f(H1), e1c(H1), M2(H2), e2f(H2), e2c(H2);
+    for (int h = 0; h < H1; h++) {
+        double pm = std::fabs((double)b1[h]), am = 0.0;
+        for (int k = 0; k < L; k++) pm += std::fabs((double)W1[(int64_t)h * nin + k]) * xmax[k];
+        for (int k = 0; k < A; k++) am += std::fabs((double)W1[(int64_t)h * nin + L + k]) * amax[k];
+        M1[h] = pm + am;
+        // fast: P in fp64 (L fmas) rounded to fp32, then A fp32 fmas onto it
+        e1f[h] = gam(L, kU64) * pm + kU32 * pm * (1 + gam(L, kU64)) + gam(A, kU32) * M1[h] * (1 + 2 * kU32);
+        e1c[h] = gam(nin, kU64) * M1[h];
+    }
+    for (int v = 0; v < H2; v++) {
+        double m = std::fabs((double)b2[v]), pf = 0.0, pc = 0.0, mf = m, mc = m;
+        for (int h = 0; h < H1; h++) {
+            const double aw = std::fabs((double)W2[(int64_t)v * H1 + h]);
+            m += aw * M1[h];
+            pf += aw * e1f[h];
+            pc += aw * e1c[h];
+            mf += aw * (M1[h] + e1f[h]);
+            mc += aw * (M1[h] + e1c[h]);
+        }
+        M2[v] = m;
+        e2f[v] = pf + gam(H1, kU32) * mf;
+        e2c[v] = pc + gam(H1, kU64) * mc;
+    }
+    double out_b[2], out_m = 0.0;
+    for (int o = 0; o < 2; o++) {
+        double pf = 0.0, pc = 0.0, mf = std::fabs((double)b3[o]), mc = mf, m = mf;
+        for (int v = 0; v < H2; v++) {
+            const double aw = std::fabs((double)W3[o * H2 + v]);
+            pf += aw * e2f[v];
+            pc += aw * e2c[v];
+            mf += aw * (M2[v] + e2f[v]);
+            mc += aw * (M2[v] + e2c[v]);
+            m += aw * M2[v];
+        }
+        // fast layer 3: per-half fma chains of H2/2 terms, one cross add, + b3
+        const double ef = pf + gam(H2 / 2 + 2, kU32) * mf;
+        const double ec = pc + gam(H2, kU64) * mc;
+        out_b[o] = (ef + ec) * 1.01 + 1e-30;
+        if (o == 1) out_m = m + ef;
+    }
+    *b_lat = out_b[0];
+    *b_thr = out_b[1];
+    *m_thr = out_m;
+}
+
+uint32_t magic_for(int K) { return K <= 1 ? 0u : (uint32_t)((0x100000000ull / (uint64_t)K) + 1ull); }
+
+int choose_kp(int top_k)
+{
+    if (top_k <= 8) return 16;
+    if (top_k <= 16) return 32;
+    return 64;
+}
+
+void stride_digits(const mf_problem &p, uint64_t stride, uint32_t *out)
+{
+    const uint64_t s = stride % p.space;
+    uint64_t x = s;
+    for (int i = p.N - 1; i >= 0; i--) {
+        out[i] = (uint32_t)(x % (uint64_t)p.K[i]);
+        x /= (uint64_t)p.K[i];
+    }
+    for (int i = p.N; i < kMaxN; i++) out[i] = 0;
+}
+
+// Workspace layout for one search launch set over n configurations.
+struct WsLayout {
+    size_t res, work, collect, lists, cand, entJ, entF, total;
+    uint32_t work_cap, collect_cap;
+    int kp, grid;
+};
+
+WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k)
+{
+    WsLayout w{};
+    w.kp = choose_kp(top_k);
+    const uint64_t tiles = (n + 31) / 32;
+    uint64_t g = (tiles + kSearchWaves - 1) / kSearchWaves;
+    w.grid = (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)p.num_cus));
+    const uint64_t cap = std::min<uint64_t>(std::max<uint64_t>(n, 1024), (uint64_t)kDefaultWorklist);
+    w.work_cap = (uint32_t)cap;
+    w.collect_cap = (uint32_t)cap;
+    size_t o = 0;
+    w.res = o; o = align256(o + sizeof(DevResult));
+    w.work = o; o = align256(o + (size_t)w.work_cap * 4);
+    w.collect = o; o = align256(o + (size_t)w.collect_cap * 4);
+    w.lists = o; o = align256(o + (size_t)w.grid * w.kp * 8);
+    w.cand = o; o = align256(o + (size_t)w.kp * 8);
+    const size_t n_ent = (size_t)w.kp + w.work_cap + w.collect_cap;
+    w.entJ = o; o = align256(o + n_ent * 8);
+    w.entF = o; o = align256(o + n_ent * 4);
+    w.total = o;
+    return w;
+}
+
+constexpr uint64_t kMaxLaunch = 1ull << 32;   // offsets within one launch set fit in 32 bits
+
+mf_status hip_status(hipError_t e) { return e == hipSuccess ? MF_OK : MF_EDEVICE; }
+
+#define MF_HIP(x)                                         \
+    do {                                                  \
+        hipError_t e_ = (x);                              \
+        if (e_ != hipSuccess) return MF_EDEVICE;          \
+    } while (0)
+
+void merge_into(mf_result &acc, const mf_result &part, int k)
+{
+    acc.n_eval += part.n_eval;
+    acc.n_vram += part.n_vram;
+    acc.n_feas += part.n_feas;
+    acc.n_flagged += part.n_flagged;
+    acc.n_topk_collect += part.n_topk_collect;
+    acc.n_splits += part.n_splits;
+    acc.main_kernel_ms += part.main_kernel_ms;
+    std::vector<std::pair<double, uint64_t>> v;
+    for (int q = 0; q < acc.n_top; q++) v.push_back({acc.top_J[q], acc.top_idx[q]});
+    for (int q = 0; q < part.n_top; q++) v.push_back({part.top_J[q], part.top_idx[q]});
+    std::sort(v.begin(), v.end(), [](const auto &x, const auto &y) {
+        return x.first > y.first || (x.first == y.first && x.second < y.second);
+    });
+    acc.n_top = (int32_t)std::min<size_t>(v.size(), (size_t)k);
+    for (int q = 0; q < MF_MAX_TOPK; q++) {
+        acc.top_idx[q] = q < acc.n_top ? v[q].second : UINT64_MAX;
+        acc.top_J[q] = q < acc.n_top ? v[q].first : -INFINITY;
+    }
+}
+
+void empty_result(mf_result &r)
+{
+    std::memset(&r, 0, sizeof(r));
+    for (int q = 0; q < MF_MAX_TOPK; q++) {
+        r.top_idx[q] = UINT64_MAX;
+        r.top_J[q] = -INFINITY;
+    }
+}
+
+enum RangeOutcome { kRangeOk, kRangeSplit };
+
+// One launch set over [lo, lo + n), n <= 2^32.
+mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint64_t n, char *ws, hipStream_t s,
+                    mf_result &out, RangeOutcome &outcome)
+{
+    const WsLayout w = ws_layout(*p, n, args->top_k);
+    DevResult *R = reinterpret_cast<DevResult *>(ws + w.res);
+    uint32_t *work = reinterpret_cast<uint32_t *>(ws + w.work);
+    uint32_t *collect = reinterpret_cast<uint32_t *>(ws + w.collect);
+    unsigned long long *lists = reinterpret_cast<unsigned long long *>(ws + w.lists);
+    unsigned long long *cand = reinterpret_cast<unsigned long long *>(ws + w.cand);
+    double *entJ = reinterpret_cast<double *>(ws + w.entJ);
+    uint32_t *entF = reinterpret_cast<uint32_t *>(ws + w.entF);
+    const bool dump = (args->flags & MF_DUMP) != 0;
+    const uint64_t dump_off = lo - args->lo;
+
+    FastArgs fa{};
+    fa.image = p->d_image;
+    fa.image_f4 = p->lay.total_floats / 4;
+    fa.lay = p->lay;
+    fa.lo = lo;
+    fa.n = n;
+    fa.total_waves = w.grid * kSearchWaves;
+    stride_digits(*p, (uint64_t)fa.total_waves * 32u, fa.stride_digits);
+    fa.sla = args->d_sla;
+    fa.omega = args->d_omega;
+    fa.res = R;
+    fa.work = work;
+    fa.work_cap = w.work_cap;
+    fa.collect = collect;
+    fa.collect_cap = w.collect_cap;
+    fa.wg_lists = lists;
+    fa.mask = dump ? args->d_mask + dump_off : nullptr;
+    fa.pred = dump ? args->d_pred + dump_off * (uint64_t)p->N * 2u : nullptr;
+
+    CanonArgs ca{};
+    ca.n_models = p->N; ca.L = p->L; ca.A = p->A; ca.H1 = p->H1; ca.H2 = p->H2; ca.bf16 = p->bf16;
+    for (int i = 0; i < p->N; i++) { ca.K[i] = p->K[i]; ca.opt_off[i] = p->opt_off[i]; }
+    ca.agg_cols = p->d_agg_cols; ca.vram_slot = p->vram_slot; ca.vram_cap = p->vram_cap;
+    ca.features = p->d_features; ca.weights = p->d_canon; ca.wstride = p->wstride;
+    ca.sla = args->d_sla; ca.omega = args->d_omega;
+    ca.lo = lo;
+    ca.cand_keys = cand; ca.n_cand_keys = w.kp;
+    ca.work = work; ca.n_work_ptr = &R->n_work; ca.work_cap = w.work_cap;
+    ca.collect = collect; ca.n_collect_ptr = nullptr; ca.collect_cap = w.collect_cap;
+    ca.ent_J = entJ; ca.ent_flags = entF;
+    ca.mask = fa.mask;
+
+    SelectArgs sa{};
+    sa.top_k = args->top_k; sa.kp = w.kp; sa.cand_keys = cand; sa.work = work; sa.collect = collect;
+    sa.work_cap = w.work_cap; sa.collect_cap = w.collect_cap; sa.ent_J = entJ; sa.ent_flags = entF;
+    sa.lo = lo; sa.collect_mode = 0; sa.res = R;
+
+    hipEvent_t ev0 = nullptr, ev1 = nullptr;
+    MF_HIP(hipEventCreate(&ev0));
+    if (hipEventCreate(&ev1) != hipSuccess) { (void)hipEventDestroy(ev0); return MF_EDEVICE; }
+    auto cleanup = [&]() { (void)hipEventDestroy(ev0); (void)hipEventDestroy(ev1); };
+#define MF_HIP2(x)                                  \
+    do {                                            \
+        if ((x) != hipSuccess) { cleanup(); return MF_EDEVICE; } \
+    } while (0)
+
+    MF_HIP2(hipMemsetAsync(R, 0, sizeof(DevResult), s));
+    MF_HIP2(hipEventRecord(ev0, s));
+    MF_HIP2(launch_fast_impl(fa, p->fc, w.grid, w.kp, kModeSearch, s));
+    MF_HIP2(hipEventRecord(ev1, s));
+    MF_HIP2(launch_merge_lists(lists, w.grid, w.kp, cand, s));
+    MF_HIP2(launch_canonical(ca, w.kp + (int)std::min<uint64_t>(w.work_cap, 1u << 20), true, s));
+    MF_HIP2(launch_select(sa, p->fc, args->d_omega, s));
+    DevResult h{};
+    MF_HIP2(hipMemcpyAsync(&h, R, sizeof(DevResult), hipMemcpyDeviceToHost, s));
+    MF_HIP2(hipStreamSynchronize(s));
+    float ms = 0.f;
+    MF_HIP2(hipEventElapsedTime(&ms, ev0, ev1));
+
+    if (h.status & kStatWorkOverflow) {
+        cleanup();
+        outcome = kRangeSplit;
+        return MF_OK;
+    }
+    if (h.status & kStatSelfCheck) { cleanup(); return MF_EINTERNAL; }
+    uint64_t n_collect = 0;
+    if (!(h.status & kStatVerified)) {
+        // top-k fallback: gather every sure-feasible configuration whose fast
+        // J could reach the k-th canonical value, then select canonically
+        fa.theta = h.theta;
+        fa.mask = nullptr;
+        fa.pred = nullptr;
+        MF_HIP2(hipMemsetAsync(&R->n_collect, 0, sizeof(unsigned long long), s));
+        MF_HIP2(hipEventRecord(ev0, s));
+        MF_HIP2(launch_fast_impl(fa, p->fc, w.grid, w.kp, kModeCollect, s));
+        MF_HIP2(hipEventRecord(ev1, s));
+        ca.n_cand_keys = 0;
+        ca.n_collect_ptr = &R->n_collect;
+        ca.mask = nullptr;
+        MF_HIP2(launch_canonical(ca, (int)std::min<uint64_t>((uint64_t)w.work_cap + w.collect_cap, 1u << 20), true, s));
+        sa.collect_mode = 1;
+        MF_HIP2(launch_select(sa, p->fc, args->d_omega, s));
+        DevResult h2{};
+        MF_HIP2(hipMemcpyAsync(&h2, R, sizeof(DevResult), hipMemcpyDeviceToHost, s));
+        MF_HIP2(hipStreamSynchronize(s));
+        float ms2 = 0.f;
+        MF_HIP2(hipEventElapsedTime(&ms2, ev0, ev1));
+        ms += ms2;
+        if (h2.status & kStatCollectOverflow) {
+            cleanup();
+            outcome = kRangeSplit;
+            return MF_OK;
+        }
+        n_collect = h2.n_collect;
+        h.n_top = h2.n_top;
+        std::memcpy(h.top_idx, h2.top_idx, sizeof(h.top_idx));
+        std::memcpy(h.top_J, h2.top_J, sizeof(h.top_J));
+    }
+    cleanup();
+#undef MF_HIP2
+    empty_result(out);
+    out.n_eval = n;
+    out.n_vram = h.n_vram;
+    out.n_feas = h.n_feas_sure + h.n_feas_cert;
+    out.n_flagged = h.n_work;
+    out.n_topk_collect = n_collect;
+    out.n_top = h.n_top;
+    for (int q = 0; q < MF_MAX_TOPK; q++) {
+        out.top_idx[q] = q < h.n_top ? h.top_idx[q] : UINT64_MAX;
+        out.top_J[q] = q < h.n_top ? h.top_J[q] : -INFINITY;
+    }
+    out.main_kernel_ms = ms;
+    outcome = kRangeOk;
+    return MF_OK;
+}
+
+mf_status search_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint64_t n, char *ws, hipStream_t s,
+                       mf_result &acc, int depth)
+{
+    if (n == 0) return MF_OK;
+    if (n > kMaxLaunch) {
+        const uint64_t h = n / 2;
+        mf_status st = search_range(p, args, lo, h, ws, s, acc, depth);
+        if (st != MF_OK) return st;
+        return search_range(p, args, lo + h, n - h, ws, s, acc, depth);
+    }
+    mf_result part;
+    RangeOutcome oc;
+    mf_status st = run_range(p, args, lo, n, ws, s, part, oc);
+    if (st != MF_OK) return st;
+    if (oc == kRangeSplit) {
+        if (n < 2 || depth > 40) return MF_ENOMEM;
+        const uint64_t h = n / 2;
+        acc.n_splits += 1;
+        st = search_range(p, args, lo, h, ws, s, acc, depth + 1);
+        if (st != MF_OK) return st;
+        return search_range(p, args, lo + h, n - h, ws, s, acc, depth + 1);
+    }
+    merge_into(acc, part, args->top_k);
+    return MF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *mf_status_string(mf_status s)
+{
+    switch (s) {
+        case MF_OK: return "MF_OK";
+        case MF_EINVAL: return "MF_EINVAL: invalid argument";
+        case MF_ENOMEM: return "MF_ENOMEM: workspace too small or allocation failed";
+        case MF_EDEVICE: return "MF_EDEVICE: HIP runtime call or kernel launch failed";
+        case MF_EUNSUPPORTED: return "MF_EUNSUPPORTED: shape not supported by the kernels";
+        case MF_EOVERFLOW: return "MF_EOVERFLOW: joint space or range does not fit";
+        case MF_EINTERNAL: return "MF_EINTERNAL: fast-path self-check failed";
+    }
+    return "unknown mf_status";
+}
+
+mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const float *d_weights, void *stream,
+                            mf_problem **out)
+{
+    if (!desc || !d_features || !d_weights || !out) return MF_EINVAL;
+    *out = nullptr;
+    const int N = desc->n_models, L = desc->n_local, A = desc->n_agg, H1 = desc->hidden1, H2 = desc->hidden2;
+    if (N < 1 || N > MF_MAX_MODELS || L < 1 || A < 1 || A > 16 || L + A > 64 || H1 < 1 || H1 > 256 || H2 < 1 ||
+        H2 > 256 || !desc->h_n_options || !desc->h_agg_cols)
+        return MF_EINVAL;
+    if (desc->dtype != MF_F32 && desc->dtype != MF_BF16) return MF_EINVAL;
+    if (desc->vram_slot < 0 || desc->vram_slot >= A || !std::isfinite(desc->vram_cap)) return MF_EINVAL;
+    mf_problem *p = new (std::nothrow) mf_problem();
+    if (!p) return MF_ENOMEM;
+    p->N = N; p->L = L; p->A = A; p->H1 = H1; p->H2 = H2;
+    p->bf16 = desc->dtype == MF_BF16;
+    p->vram_slot = desc->vram_slot;
+    p->vram_cap = desc->vram_cap;
+    p->K.assign(desc->h_n_options, desc->h_n_options + N);
+    p->agg_cols.assign(desc->h_agg_cols, desc->h_agg_cols + A);
+    uint64_t space = 1;
+    int sumK = 0;
+    for (int i = 0; i < N; i++) {
+        const int k = p->K[i];
+        if (k < 1 || k > 255) { delete p; return MF_EINVAL; }
+        if (space > UINT64_MAX / (uint64_t)k) { delete p; return MF_EOVERFLOW; }
+        space *= (uint64_t)k;
+        p->opt_off.push_back(sumK);
+        sumK += k;
+    }
+    for (int k = 0; k < A; k++)
+        if (p->agg_cols[k] < 0 || p->agg_cols[k] >= L) { delete p; return MF_EINVAL; }
+    p->space = space;
+    p->sumK = sumK;
+    const int nin = L + A;
+    p->wstride = (int64_t)H1 * nin + H1 + (int64_t)H2 * H1 + H2 + 2 * H2 + 2;
+
+    hipStream_t s = (hipStream_t)stream;
+    std::vector<float> F((size_t)sumK * L), W((size_t)N * p->wstride);
+    if (hipMemcpy(F.data(), d_features, F.size() * 4, hipMemcpyDefault) != hipSuccess ||
+        hipMemcpy(W.data(), d_weights, W.size() * 4, hipMemcpyDefault) != hipSuccess) {
+        delete p;
+        return MF_EINVAL;
+    }
+    if (!all_finite(F) || !all_finite(W)) { delete p; return MF_EINVAL; }
+    if (p->bf16) {
+        for (int i = 0; i < N; i++) {
+            const float *w = W.data() + (int64_t)i * p->wstride;
+            const int64_t n1 = (int64_t)H1 * nin, n2 = (int64_t)H2 * H1;
+            for (int64_t t = 0; t < n1; t++)
+                if (!bf16_exact(w[t])) { delete p; return MF_EINVAL; }
+            for (int64_t t = 0; t < n2; t++)
+                if (!bf16_exact(w[n1 + H1 + t])) { delete p; return MF_EINVAL; }
+            for (int64_t t = 0; t < 2 * H2; t++)
+                if (!bf16_exact(w[n1 + H1 + n2 + H2 + t])) { delete p; return MF_EINVAL; }
+        }
+    }
+    if (hipGetDevice(&p->device) != hipSuccess ||
+        hipDeviceGetAttribute(&p->num_cus, hipDeviceAttributeMultiprocessorCount, p->device) != hipSuccess) {
+        delete p;
+        return MF_EDEVICE;
+    }
+
+    // ---- fast path (fp32, H1 == H2 in {32, 64}, A in {2,4,6,8})
+    p->fast_ok = !p->bf16 && H1 == H2 && fast_kernel_supported(N, A, H1, 64);
+    const int H = H1;
+    FastLayout &ly = p->lay;
+    std::vector<float> img;
+    if (p->fast_ok) {
+        ly.H = H; ly.A = A; ly.AP = 8; ly.MB = H / 32; ly.S1 = A / 2; ly.PST = H + 4;
+        int o = 0;
+        ly.off_w1a = o; o += N * ly.MB * ly.S1 * 64;
+        ly.off_b2 = o; o += N * H;
+        ly.off_w2 = o; o += N * H * H;
+        ly.off_w3 = o; o += N * 2 * H;
+        ly.off_b3 = o; o += N * 4;
+        ly.off_p = o; o += sumK * ly.PST;
+        ly.off_g = o; o += sumK * ly.AP;
+        ly.total_floats = (o + 3) & ~3;
+        const size_t lds = (size_t)ly.total_floats * 4 + 64 * 4 + (size_t)kSearchWaves * 64 * 8;
+        if (lds > 163840) p->fast_ok = false;
+    }
+    if (p->fast_ok) {
+        img.assign(ly.total_floats, 0.f);
+        // internal aggregate slot order: the VRAM slot first
+        std::vector<int> perm;
+        perm.push_back(p->vram_slot);
+        for (int k = 0; k < A; k++)
+            if (k != p->vram_slot) perm.push_back(k);
+        for (int i = 0; i < N; i++) {
+            const float *w = W.data() + (int64_t)i * p->wstride;
+            const float *W1 = w, *b1 = W1 + (int64_t)H * nin, *W2 = b1 + H, *b2 = W2 + (int64_t)H * H,
+                        *W3 = b2 + H, *b3 = W3 + 2 * H;
+            (void)b1;
+            for (int mb = 0; mb < ly.MB; mb++)
+                for (int st = 0; st < ly.S1; st++)
+                    for (int l = 0; l < 64; l++)
+                        img[ly.off_w1a + ((i * ly.MB + mb) * ly.S1 + st) * 64 + l] =
+                            W1[(int64_t)(32 * mb + l % 32) * nin + L + perm[2 * st + l / 32]];
+            for (int h = 0; h < H; h++) img[ly.off_b2 + i * H + h] = b2[h];
+            for (int mb2 = 0; mb2 < ly.MB; mb2++)
+                for (int mb1 = 0; mb1 < ly.MB; mb1++)
+                    for (int q = 0; q < 4; q++)
+                        for (int l = 0; l < 64; l++)
+                            for (int j = 0; j < 4; j++)
+                                img[ly.off_w2 + i * H * H + ((((mb2 * ly.MB + mb1) * 4 + q) * 64 + l) * 4 + j)] =
+                                    W2[(int64_t)(32 * mb2 + l % 32) * H + 32 * mb1 + 8 * q + 4 * (l / 32) + j];
+            for (int o2 = 0; o2 < 2; o2++)
+                for (int mb = 0; mb < ly.MB; mb++)
+                    for (int q = 0; q < 4; q++)
+                        for (int hf = 0; hf < 2; hf++)
+                            for (int j = 0; j < 4; j++)
+                                img[ly.off_w3 + i * 2 * H + (((o2 * ly.MB + mb) * 4 + q) * 2 + hf) * 4 + j] =
+                                    W3[o2 * H + 32 * mb + 8 * q + 4 * hf + j];
+            img[ly.off_b3 + 4 * i + 0] = b3[0];
+            img[ly.off_b3 + 4 * i + 1] = b3[1];
+        }
+        // aggregate rows as [half][s]: internal slot 2s + half
+        for (int r = 0; r < sumK; r++)
+            for (int hf = 0; hf < 2; hf++)
+                for (int st = 0; st < 4; st++) {
+                    const int k = 2 * st + hf;
+                    img[ly.off_g + r * ly.AP + hf * 4 + st] = k < A ? F[(int64_t)r * L + p->agg_cols[perm[k]]] : 0.f;
+                }
+        FastConst &fc = p->fc;
+        fc.n_models = N;
+        for (int i = 0; i < N; i++) {
+            fc.K[i] = p->K[i];
+            fc.opt_off[i] = p->opt_off[i];
+            fc.magic[i] = magic_for(p->K[i]);
+            model_bounds(*p, F, W, i, &fc.bound_lat[i], &fc.bound_thr[i], &fc.mag_thr[i]);
+        }
+        fc.vram_cap = p->vram_cap;
+    }
+
+    // ---- canonical image: per model W1T[nin][H1] b1 W2T[H1][H2] b2 W3[2][H2] b3
+    std::vector<float> canon((size_t)N * p->wstride);
+    for (int i = 0; i < N; i++) {
+        const float *w = W.data() + (int64_t)i * p->wstride;
+        float *c = canon.data() + (int64_t)i * p->wstride;
+        const float *W1 = w, *b1 = W1 + (int64_t)H1 * nin, *W2 = b1 + H1, *rest = W2 + (int64_t)H2 * H1;
+        float *cW1T = c, *cb1 = c + (int64_t)nin * H1, *cW2T = cb1 + H1, *crest = cW2T + (int64_t)H1 * H2;
+        for (int h = 0; h < H1; h++)
+            for (int k = 0; k < nin; k++) cW1T[(int64_t)k * H1 + h] = W1[(int64_t)h * nin + k];
+        std::memcpy(cb1, b1, (size_t)H1 * 4);
+        for (int v = 0; v < H2; v++)
+            for (int h = 0; h < H1; h++) cW2T[(int64_t)h * H2 + v] = W2[(int64_t)v * H1 + h];
+        std::memcpy(crest, rest, (size_t)(H2 + 2 * H2 + 2) * 4);
+    }
+    std::vector<int32_t> row_model(sumK);
+    for (int i = 0; i < N; i++)
+        for (int o = 0; o < p->K[i]; o++) row_model[p->opt_off[i] + o] = i;
+
+    // ---- one device allocation
+    size_t off = 0;
+    const size_t o_img = off; off = align256(off + img.size() * 4);
+    const size_t o_can = off; off = align256(off + canon.size() * 4);
+    const size_t o_fea = off; off = align256(off + F.size() * 4);
+    const size_t o_agg = off; off = align256(off + (size_t)A * 4);
+    const size_t o_rm = off; off = align256(off + (size_t)sumK * 4);
+    const size_t o_z = off; off = align256(off + 64 * 4);
+    if (hipMalloc(&p->d_mem, off) != hipSuccess) { delete p; return MF_ENOMEM; }
+    char *base = (char *)p->d_mem;
+    p->d_image = reinterpret_cast<float4 *>(base + o_img);
+    p->d_canon = reinterpret_cast<float *>(base + o_can);
+    p->d_features = reinterpret_cast<float *>(base + o_fea);
+    p->d_agg_cols = reinterpret_cast<int32_t *>(base + o_agg);
+    p->d_row_model = reinterpret_cast<int32_t *>(base + o_rm);
+    p->d_zeros = reinterpret_cast<float *>(base + o_z);
+    bool ok = true;
+    ok = ok && hipMemsetAsync(p->d_zeros, 0, 64 * 4, s) == hipSuccess;
+    if (!img.empty()) ok = ok && hipMemcpyAsync(p->d_image, img.data(), img.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
+    ok = ok && hipMemcpyAsync(p->d_canon, canon.data(), canon.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
+    ok = ok && hipMemcpyAsync(p->d_features, F.data(), F.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
+    ok = ok && hipMemcpyAsync(p->d_agg_cols, p->agg_cols.data(), (size_t)A * 4, hipMemcpyHostToDevice, s) == hipSuccess;
+    ok = ok && hipMemcpyAsync(p->d_row_model, row_model.data(), (size_t)sumK * 4, hipMemcpyHostToDevice, s) == hipSuccess;
+    if (ok && p->fast_ok)
+        ok = launch_precompute_p(p->d_features, p->d_canon, sumK, L, A, H, p->wstride, p->d_row_model,
+                                 reinterpret_cast<float *>(p->d_image) + ly.off_p, ly.PST, s) == hipSuccess;
+    ok = ok && hipStreamSynchronize(s) == hipSuccess;
+    if (!ok) {
+        (void)hipFree(p->d_mem);
+        delete p;
+        return MF_EDEVICE;
+    }
+    *out = p;
+    return MF_OK;
+}
+
+void mf_problem_destroy(mf_problem *p)
+{
+    if (!p) return;
+    if (p->d_mem) (void)hipFree(p->d_mem);
+    delete p;
+}
+
+mf_status mf_space_size(const mf_problem *p, uint64_t *out)
+{
+    if (!p || !out) return MF_EINVAL;
+    *out = p->space;
+    return MF_OK;
+}
+
+mf_status mf_decode(const mf_problem *p, uint64_t idx, int32_t *h_digits)
+{
+    if (!p || !h_digits || idx >= p->space) return MF_EINVAL;
+    for (int i = p->N - 1; i >= 0; i--) {
+        h_digits[i] = (int32_t)(idx % (uint64_t)p->K[i]);
+        idx /= (uint64_t)p->K[i];
+    }
+    return MF_OK;
+}
+
+static mf_status check_search_args(const mf_problem *p, const mf_search_args *a)
+{
+    if (!p || !a) return MF_EINVAL;
+    if (a->lo > a->hi) return MF_EINVAL;
+    if (a->hi > p->space) return MF_EOVERFLOW;
+    if (a->top_k < 1 || a->top_k > MF_MAX_TOPK) return MF_EINVAL;
+    if (!a->d_sla || !a->d_omega) return MF_EINVAL;
+    if (a->flags & ~MF_DUMP) return MF_EINVAL;
+    if ((a->flags & MF_DUMP) && (!a->d_mask || !a->d_pred || a->hi - a->lo > (1ull << 31))) return MF_EINVAL;
+    if (!p->fast_ok) return MF_EUNSUPPORTED;
+    return MF_OK;
+}
+
+mf_status mf_workspace_size(const mf_problem *p, const mf_search_args *args, size_t *bytes)
+{
+    if (!bytes) return MF_EINVAL;
+    mf_status st = check_search_args(p, args);
+    if (st != MF_OK) return st;
+    const uint64_t n = std::min<uint64_t>(args->hi - args->lo, kMaxLaunch);
+    *bytes = ws_layout(*p, n, args->top_k).total;
+    return MF_OK;
+}
+
+mf_status mf_search(mf_problem *p, const mf_search_args *args, void *d_ws, size_t ws_bytes, void *stream,
+                    mf_result *h_out)
+{
+    if (!h_out || !d_ws) return MF_EINVAL;
+    mf_status st = check_search_args(p, args);
+    if (st != MF_OK) return st;
+    const uint64_t n = args->hi - args->lo;
+    const uint64_t n1 = std::min<uint64_t>(n, kMaxLaunch);
+    if (ws_bytes < ws_layout(*p, n1, args->top_k).total) return MF_ENOMEM;
+    if (((uintptr_t)d_ws & 255u) != 0) return MF_EINVAL;
+    mf_result acc;
+    empty_result(acc);
+    st = search_range(p, args, args->lo, n, (char *)d_ws, (hipStream_t)stream, acc, 0);
+    if (st != MF_OK) return st;
+    *h_out = acc;
+    return MF_OK;
+}
+
+mf_status mf_eval_fast(mf_problem *p, const uint64_t *d_idx, int64_t n, float *d_pred, void *stream)
+{
+    if (!p || n < 0 || (n > 0 && (!d_idx || !d_pred))) return MF_EINVAL;
+    if (!p->fast_ok) return MF_EUNSUPPORTED;
+    if (n == 0) return MF_OK;
+    FastArgs fa{};
+    fa.image = p->d_image;
+    fa.image_f4 = p->lay.total_floats / 4;
+    fa.lay = p->lay;
+    fa.lo = 0;
+    fa.n = (uint64_t)n;
+    fa.idx_list = d_idx;
+    const uint64_t tiles = ((uint64_t)n + 31) / 32;
+    const int grid = (int)std::max<uint64_t>(1, std::min<uint64_t>((tiles + kSearchWaves - 1) / kSearchWaves,
+                                                                    (uint64_t)p->num_cus));
+    fa.total_waves = grid * kSearchWaves;
+    fa.sla = p->d_zeros;
+    fa.omega = p->d_zeros;
+    fa.pred = d_pred;
+    return hip_status(launch_fast_impl(fa, p->fc, grid, 16, kModeList, (hipStream_t)stream));
+}
+
+mf_status mf_eval_canonical(mf_problem *p, const uint64_t *d_idx, int64_t n, const float *d_sla,
+                            const float *d_omega, double *d_pred, double *d_J, uint32_t *d_flags, void *stream)
+{
+    if (!p || n < 0 || (n > 0 && (!d_idx || !d_sla || !d_omega))) return MF_EINVAL;
+    if (n == 0) return MF_OK;
+    CanonArgs ca{};
+    ca.n_models = p->N; ca.L = p->L; ca.A = p->A; ca.H1 = p->H1; ca.H2 = p->H2; ca.bf16 = p->bf16;
+    for (int i = 0; i < p->N; i++) { ca.K[i] = p->K[i]; ca.opt_off[i] = p->opt_off[i]; }
+    ca.agg_cols = p->d_agg_cols; ca.vram_slot = p->vram_slot; ca.vram_cap = p->vram_cap;
+    ca.features = p->d_features; ca.weights = p->d_canon; ca.wstride = p->wstride;
+    ca.sla = d_sla; ca.omega = d_omega;
+    ca.idx64 = d_idx;
+    ca.n_list = n;
+    ca.ent_J = d_J;
+    ca.ent_flags = d_flags;
+    ca.pred = d_pred;
+    return hip_status(launch_canonical(ca, (int)std::min<int64_t>(n, 1 << 20), false, (hipStream_t)stream));
+}
+
+mf_status mf_ga_workspace_size(const mf_problem *p, const mf_ga_args *args, size_t *bytes)
+{
+    if (!p || !args || !bytes) return MF_EINVAL;
+    return MF_EUNSUPPORTED;
+}
+
+mf_status mf_ga_run(mf_problem *p, const mf_ga_args *args, void *d_ws, size_t ws_bytes, void *stream,
+                    uint64_t *h_best_idx, double *h_best_J, uint64_t *d_final_pop)
+{
+    (void)d_ws; (void)ws_bytes; (void)stream; (void)d_final_pop;
+    if (!p || !args || !h_best_idx || !h_best_J) return MF_EINVAL;
+    return MF_EUNSUPPORTED;
+}
+
+}  // extern "C"

@@ -1,0 +1,315 @@
+// Canonical fp64 evaluation and the exact top-k selection.
+//
+// Results of the search are defined by canonical fp64 semantics (each dot
+// product one fused multiply-add chain, ascending inputs, starting from the
+// bias; relu(x) = x > 0 ? x : +0; J the fma chain over models).  The fast
+// fp32 MFMA path settles every latency decision whose margin exceeds its
+// a-priori error bound; the rest, and every top-k candidate, are evaluated
+// here with that exact chain (v_fma_f64 is correctly rounded, so the values
+// are the canonical ones bit for bit).
+//
+// One single-wave workgroup per entry: lanes take hidden units, the uniform
+// parts (decode, aggregate, output units) run redundantly per lane.
+#include "mf_internal.h"
+
+namespace mfi {
+
+constexpr int kCanonMaxH = 256;
+constexpr int kCanonMaxIn = 64;
+
+__device__ __forceinline__ double bf16_round_d(double x)
+{
+    // nearest bfloat16 value (8 significant bits), ties to even; x finite
+    if (x == 0.0) return x;
+    int e = ilogb(x);
+    if (e < -126) e = -126;                 // bf16 subnormal spacing 2^-133
+    const double scale = ldexp(1.0, 7 - e); // |x| * scale in [128, 256)
+    return rint(x * scale) / scale;
+}
+
+__device__ __forceinline__ uint64_t ord_f64(double x)
+{
+    const uint64_t b = (uint64_t)__double_as_longlong(x);
+    return (b & 0x8000000000000000ull) ? ~b : (b | 0x8000000000000000ull);
+}
+
+// Canonical image per model (fp32 values, exact in fp64):
+//   W1T[nin][H1], b1[H1], W2T[H1][H2], b2[H2], W3[2][H2], b3[2]
+template <bool BF16>
+__global__ void __launch_bounds__(64)
+canon_kernel(const CanonArgs a, const int search_mode)
+{
+    __shared__ double h1s[kCanonMaxH];
+    __shared__ double h2s[kCanonMaxH];
+    __shared__ double zs[kCanonMaxIn];
+    __shared__ int32_t ds[kMaxN];
+    __shared__ float aggs[16];
+    const int lane = threadIdx.x;
+    const int N = a.n_models, L = a.L, A = a.A, H1 = a.H1, H2 = a.H2, nin = L + A;
+
+    int64_t n_cand = 0, n_work = 0, n_coll = 0, n_ent;
+    if (search_mode) {
+        n_cand = a.n_cand_keys;
+        n_work = a.n_work_ptr ? (int64_t)min(*a.n_work_ptr, (unsigned long long)a.work_cap) : 0;
+        n_coll = a.n_collect_ptr ? (int64_t)min(*a.n_collect_ptr, (unsigned long long)a.collect_cap) : 0;
+        n_ent = n_cand + n_work + n_coll;
+    } else {
+        n_ent = a.n_list;
+    }
+
+    for (int64_t e = blockIdx.x; e < n_ent; e += gridDim.x) {
+        uint64_t idx, off = 0;
+        if (search_mode) {
+            if (e < n_cand) {
+                const unsigned long long key = a.cand_keys[e];
+                if (key == 0ull) {
+                    if (lane == 0) { a.ent_J[e] = -INFINITY; a.ent_flags[e] = 0; }
+                    continue;
+                }
+                off = 0xFFFFFFFFu - (uint32_t)(key & 0xFFFFFFFFull);
+            } else if (e < n_cand + n_work) {
+                off = a.work[e - n_cand];
+            } else {
+                off = a.collect[e - n_cand - n_work];
+            }
+            idx = a.lo + off;
+        } else {
+            idx = a.idx64[e];
+        }
+        // decode (model N-1 least significant): lane i < N takes digit i
+        if (lane < N) {
+            uint64_t stride = 1;
+            for (int j = N - 1; j > lane; j--) stride *= (uint64_t)a.K[j];
+            ds[lane] = (int32_t)((idx / stride) % (uint64_t)a.K[lane]);
+        }
+        __syncthreads();
+        // aggregate field: lane k < A sums slot k in fp32, model order
+        if (lane < A) {
+            float s = 0.f;
+            for (int i = 0; i < N; i++)
+                s = s + a.features[(int64_t)(a.opt_off[i] + ds[i]) * L + a.agg_cols[lane]];
+            aggs[lane] = s;
+        }
+        __syncthreads();
+        const bool vram_ok = (double)aggs[a.vram_slot] <= (double)a.vram_cap;
+        bool sla_ok = true;
+        uint32_t fl = 0;
+        double J = 0.0;
+        for (int i = 0; i < N; i++) {
+            const float *w = a.weights + (int64_t)i * a.wstride;
+            const float *W1T = w, *b1 = W1T + (int64_t)nin * H1, *W2T = b1 + H1, *b2 = W2T + (int64_t)H1 * H2,
+                        *W3 = b2 + H2, *b3 = W3 + 2 * H2;
+            const float *x = a.features + (int64_t)(a.opt_off[i] + ds[i]) * L;
+            for (int k = lane; k < nin; k += 64) zs[k] = k < L ? (double)x[k] : (double)aggs[k - L];
+            __syncthreads();
+            for (int u = lane; u < H1; u += 64) {
+                double c = (double)b1[u];
+                for (int k = 0; k < nin; k++) c = fma((double)W1T[(int64_t)k * H1 + u], zs[k], c);
+                c = c > 0.0 ? c : 0.0;
+                h1s[u] = BF16 ? bf16_round_d(c) : c;
+            }
+            __syncthreads();
+            for (int v = lane; v < H2; v += 64) {
+                double c = (double)b2[v];
+                for (int u = 0; u < H1; u++) c = fma((double)W2T[(int64_t)u * H2 + v], h1s[u], c);
+                h2s[v] = c > 0.0 ? c : 0.0;
+            }
+            __syncthreads();
+            double y = 0.0;
+            if (lane < 2) {
+                double c = (double)b3[lane];
+                for (int v = 0; v < H2; v++) c = fma((double)W3[lane * H2 + v], h2s[v], c);
+                y = c;
+            }
+            const double lat = __shfl(y, 0), thr = __shfl(y, 1);
+            if (!(lat <= (double)a.sla[i])) { sla_ok = false; fl |= 1u << (8 + i); }
+            J = fma((double)a.omega[i], thr, J);
+            if (a.pred && lane == 0) {
+                a.pred[(e * N + i) * 2 + 0] = lat;
+                a.pred[(e * N + i) * 2 + 1] = thr;
+            }
+            __syncthreads();
+        }
+        const bool feas = vram_ok && sla_ok;
+        fl |= (vram_ok ? 1u : 0u) | (sla_ok ? 2u : 0u) | (feas ? 4u : 0u);
+        if (lane == 0) {
+            if (a.ent_J) a.ent_J[e] = feas ? J : -INFINITY;
+            if (a.ent_flags) a.ent_flags[e] = fl;
+            if (search_mode && a.mask && e >= n_cand && e < n_cand + n_work)
+                a.mask[off] = (uint8_t)((a.mask[off] & 1u) | (sla_ok ? 2u : 0u) | (feas ? 4u : 0u) | 8u);
+        }
+    }
+}
+
+hipError_t launch_canonical(const CanonArgs &a, int n_entries_max, bool search_mode, hipStream_t s)
+{
+    int grid = n_entries_max < 1 ? 1 : n_entries_max;
+    if (grid > 4096) grid = 4096;
+    if (a.bf16)
+        hipLaunchKernelGGL(canon_kernel<true>, dim3(grid), dim3(64), 0, s, a, search_mode ? 1 : 0);
+    else
+        hipLaunchKernelGGL(canon_kernel<false>, dim3(grid), dim3(64), 0, s, a, search_mode ? 1 : 0);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Exact top-k over the canonically evaluated entries.  128-bit keys:
+// (order-preserving bits of canonical J, bitwise-not of the index) so that
+// larger keys are better and equal J prefers the lower index.
+// ---------------------------------------------------------------------------
+struct K128 {
+    unsigned long long hi, lo;
+};
+__device__ __forceinline__ bool gt128(const K128 &x, const K128 &y)
+{
+    return x.hi > y.hi || (x.hi == y.hi && x.lo > y.lo);
+}
+__device__ __forceinline__ bool nz128(const K128 &x) { return (x.hi | x.lo) != 0ull; }
+
+__device__ __forceinline__ unsigned long long rl64(unsigned long long x, int src)
+{
+    const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)x, src);
+    const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), src);
+    return ((unsigned long long)hi << 32) | lo;
+}
+__device__ __forceinline__ unsigned long long up64(unsigned long long x)
+{
+    const uint32_t lo = __shfl_up((int)(uint32_t)x, 1);
+    const uint32_t hi = __shfl_up((int)(uint32_t)(x >> 32), 1);
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+__device__ void list128_offer(K128 &slot, const K128 &mine, int lane, int k, K128 &thr)
+{
+    unsigned long long cm = __ballot(nz128(mine) && gt128(mine, thr));
+    while (cm) {
+        const int src = __ffsll((long long)cm) - 1;
+        cm &= cm - 1;
+        const K128 nk = {rl64(mine.hi, src), rl64(mine.lo, src)};
+        if (!gt128(nk, thr)) continue;
+        const int pos = __popcll(__ballot(lane < k && gt128(slot, nk)));
+        const K128 prev = {up64(slot.hi), up64(slot.lo)};
+        if (lane < k) slot = lane < pos ? slot : (lane == pos ? nk : prev);
+        thr = {rl64(slot.hi, k - 1), rl64(slot.lo, k - 1)};
+    }
+}
+
+constexpr int kSelWaves = 16;
+
+__device__ double call_eJ(const FastConst &fc, const float *omega)
+{
+    const int N = fc.n_models;
+    const double g = N * 0x1p-24 / (1.0 - N * 0x1p-24);
+    double e = 0.0, m = 0.0;
+    for (int i = 0; i < N; i++) {
+        const double w = fabs((double)omega[i]);
+        e += w * (fc.bound_thr[i] + g * (fc.mag_thr[i] + fc.bound_thr[i]));
+        m += w * fc.mag_thr[i];
+    }
+    return (e + m * 0x1p-50) * (1.0 + 0x1p-20) + 1e-30;
+}
+
+__device__ __forceinline__ float unord_f32(uint32_t o)
+{
+    const uint32_t b = (o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o;
+    return __uint_as_float(b);
+}
+
+__global__ void __launch_bounds__(kSelWaves * 64)
+select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
+{
+    __shared__ K128 lst[kSelWaves * 64];
+    __shared__ unsigned long long s_feas;
+    __shared__ unsigned int s_stat;
+    __shared__ double s_maxd;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    DevResult *R = a.res;
+    if (threadIdx.x == 0) { s_feas = 0; s_stat = 0; s_maxd = 0.0; }
+    __syncthreads();
+    const double eJ = call_eJ(fc, omega);
+    const int64_t n_cand = a.collect_mode ? 0 : a.kp;
+    const int64_t n_work = (int64_t)min(R->n_work, (unsigned long long)a.work_cap);
+    const int64_t n_coll = a.collect_mode ? (int64_t)min(R->n_collect, (unsigned long long)a.collect_cap) : 0;
+    const int64_t n_ent = n_cand + n_work + n_coll;
+    const int k = a.top_k;
+    K128 slot = {0, 0}, thr = {0, 0};
+    unsigned long long my_feas = 0;
+    for (int64_t base = (int64_t)wv * 64; base < n_ent; base += kSelWaves * 64) {
+        const int64_t e = base + lane;
+        K128 key = {0, 0};
+        if (e < n_ent) {
+            const uint32_t fl = a.ent_flags[e];
+            uint64_t off = 0;
+            bool have = true;
+            if (e < n_cand) {
+                const unsigned long long ck = a.cand_keys[e];
+                have = ck != 0ull;
+                off = 0xFFFFFFFFu - (uint32_t)(ck & 0xFFFFFFFFull);
+                if (have) {
+                    if (!(fl & 4u)) atomicOr(&s_stat, kStatSelfCheck);
+                    const double jf = (double)unord_f32((uint32_t)(ck >> 32));
+                    const double dj = fabs(jf - a.ent_J[e]);
+                    if (!(dj <= eJ)) atomicOr(&s_stat, kStatSelfCheck);
+                    atomicMax((unsigned long long *)&s_maxd, (unsigned long long)__double_as_longlong(dj));
+                }
+            } else if (e < n_cand + n_work) {
+                off = a.work[e - n_cand];
+                if (fl & 4u) my_feas++;
+            } else {
+                off = a.collect[e - n_cand - n_work];
+            }
+            if (have && (fl & 4u)) key = {ord_f64(a.ent_J[e]), ~(a.lo + off)};
+        }
+        list128_offer(slot, key, lane, k, thr);
+    }
+    if (my_feas) atomicAdd(&s_feas, my_feas);
+    lst[wv * 64 + lane] = lane < k ? slot : K128{0, 0};
+    __syncthreads();
+    if (wv == 0) {
+        for (int w = 1; w < kSelWaves; w++) list128_offer(slot, lst[w * 64 + lane], lane, k, thr);
+        const int n_top = __popcll(__ballot(lane < k && nz128(slot)));
+        const uint64_t kth_hi = rl64(slot.hi, k - 1);
+        if (lane < MF_MAX_TOPK) {
+            const bool ok = lane < n_top;
+            R->top_idx[lane] = ok ? ~slot.lo : ~0ull;
+            const uint64_t o = slot.hi;
+            const uint64_t b = (o & 0x8000000000000000ull) ? (o & 0x7FFFFFFFFFFFFFFFull) : ~o;
+            R->top_J[lane] = ok ? __longlong_as_double((long long)b) : -INFINITY;
+        }
+        if (lane == 0) {
+            R->n_top = n_top;
+            R->eJ = eJ;
+            unsigned stat = s_stat;
+            if (!a.collect_mode) {
+                R->n_feas_cert = s_feas;
+                R->check_max_dJ = s_maxd;
+                const unsigned long long tail = a.cand_keys[a.kp - 1];
+                const bool full = tail != 0ull;
+                if (full) stat |= kStatListFull;
+                const double tailJ = full ? (double)unord_f32((uint32_t)(tail >> 32)) : -INFINITY;
+                R->tail_J = tailJ;
+                bool verified = !full;
+                if (full && n_top >= k) {
+                    const uint64_t b = (kth_hi & 0x8000000000000000ull) ? (kth_hi & 0x7FFFFFFFFFFFFFFFull) : ~kth_hi;
+                    const double Ck = __longlong_as_double((long long)b);
+                    verified = Ck > tailJ + eJ;
+                    R->theta = Ck - eJ - (fabs(Ck) + eJ) * 0x1p-20 - 1e-30;
+                }
+                if (verified) stat |= kStatVerified;
+            } else {
+                stat |= kStatVerified;
+            }
+            if (R->n_work > a.work_cap) stat |= kStatWorkOverflow;
+            if (a.collect_mode && R->n_collect > a.collect_cap) stat |= kStatCollectOverflow;
+            R->status |= stat;
+        }
+    }
+}
+
+hipError_t launch_select(const SelectArgs &a, const FastConst &fc, const float *omega, hipStream_t s)
+{
+    hipLaunchKernelGGL(select_kernel, dim3(1), dim3(kSelWaves * 64), 0, s, a, fc, omega);
+    return hipGetLastError();
+}
+
+}  // namespace mfi

@@ -1,0 +1,143 @@
+// Internal declarations of libmf: device-side layouts, kernel argument blocks
+// and the host-side launchers each .hip file provides.  Not installed; the C
+// ABI is include/mf.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/mf.h"
+
+namespace mfi {
+
+constexpr int kMaxN = MF_MAX_MODELS;
+constexpr int kSearchWaves = 8;          // waves per workgroup of the fast search kernel
+constexpr int kCertWaves = 4;            // waves per workgroup of the canonical kernels
+constexpr int kDefaultWorklist = 1 << 20; // certification list capacity (entries)
+
+// ---------------------------------------------------------------------------
+// Fast-path LDS image.  The device copy of the image is laid out exactly as
+// the fast kernel wants it in LDS, so its prologue is one straight copy.
+// Offsets are in floats from the image start; every block is 16-byte aligned.
+//   w1a[i][mb][s][lane]            A operand of layer 1 (aggregate columns)
+//   b2 [i][H]                      layer-2 bias (accumulator init)
+//   w2 [i][mb2][mb1][q][lane][j]   A operand of layer 2
+//   w3 [i][o][mb2][q][half][j]     layer-3 weights in accumulator row order
+//   b3 [i][2]  (padded to 4)
+//   p  [row][pst]                  per-option first-layer precompute
+//                                  b1 + W1_local x (fp64, rounded to fp32),
+//                                  row = global option row
+//   g  [row][half][4]              aggregate columns of each option row in
+//                                  internal slot order (slot 0 = the VRAM
+//                                  slot); internal slot 2s+half at [half][s]
+// ---------------------------------------------------------------------------
+struct FastLayout {
+    int H, A, AP, MB, S1, PST;
+    int off_w1a, off_b2, off_w2, off_w3, off_b3, off_p, off_g;
+    int total_floats;          // multiple of 4
+};
+
+// Per-problem constants of the fast kernels (kernel-argument block).
+struct FastConst {
+    int32_t n_models;
+    int32_t K[kMaxN];
+    int32_t opt_off[kMaxN];     // first global option row of model i
+    uint32_t magic[kMaxN];      // floor(2^32 / K) + 1 (K > 1), 0 for K == 1
+    float vram_cap;
+    // a-priori bound on |fast - canonical| for (lat, thr) of model i, and on |thr|
+    double bound_lat[kMaxN], bound_thr[kMaxN], mag_thr[kMaxN];
+};
+
+// Counters and results the search kernels fill in device memory.
+struct DevResult {
+    unsigned long long n_vram, n_feas_sure, n_work, n_collect;
+    unsigned long long n_feas_cert, n_cand;
+    unsigned int status;        // see kStat*
+    int n_top;
+    unsigned long long top_idx[MF_MAX_TOPK];
+    double top_J[MF_MAX_TOPK];
+    double theta;               // fallback collect threshold (fast J >= theta)
+    double eJ;                  // bound on |fast J - canonical J| for this call
+    double tail_J;              // fast J of the last fast candidate (list full)
+    double check_max_dJ;        // max |fast J - canonical J| seen on candidates
+};
+constexpr unsigned kStatVerified = 1u;      // top-k exactness condition held
+constexpr unsigned kStatSelfCheck = 2u;     // a fast decision disagreed with canonical
+constexpr unsigned kStatWorkOverflow = 4u;
+constexpr unsigned kStatCollectOverflow = 8u;
+constexpr unsigned kStatListFull = 16u;
+
+// Kernel mode of the fast kernel.
+enum FastMode { kModeSearch = 0, kModeCollect = 1, kModeList = 2 };
+
+struct FastArgs {
+    const float4 *image;
+    int image_f4;
+    FastLayout lay;
+    uint64_t lo, n;             // range [lo, lo+n); list mode: n entries of idx_list
+    const uint64_t *idx_list;   // list mode only
+    uint32_t stride_digits[kMaxN]; // mixed-radix digits of (total waves * 32) mod |Lambda|
+    int total_waves;
+    const float *sla;           // device [N]
+    const float *omega;         // device [N]
+    DevResult *res;
+    uint32_t *work;             // certification list (range offsets)
+    uint32_t work_cap;
+    uint32_t *collect;          // fallback candidate list
+    uint32_t collect_cap;
+    double theta;               // collect mode threshold
+    unsigned long long *wg_lists; // [grid][KP] fast top-KP keys per workgroup
+    uint8_t *mask;              // dump (optional)
+    float *pred;                // dump (optional)
+};
+
+// Canonical (fp64) evaluation of entries.
+struct CanonArgs {
+    int n_models, L, A, H1, H2, bf16;
+    int32_t K[kMaxN];
+    int32_t opt_off[kMaxN];
+    const int32_t *agg_cols;    // device [A] (original order)
+    int vram_slot;
+    float vram_cap;
+    const float *features;      // device [sumK][L]
+    const float *weights;       // device [N][stride]
+    int64_t wstride;
+    const float *sla, *omega;   // device [N]
+    uint64_t lo;                // entries hold offsets from lo (search) ...
+    const uint64_t *idx64;      // ... or absolute indices (list mode) when non-null
+    // search mode entry sources: fast candidates (keys) then the work list then the collect list
+    const unsigned long long *cand_keys; int n_cand_keys;
+    const uint32_t *work; const unsigned long long *n_work_ptr; uint32_t work_cap;
+    const uint32_t *collect; const unsigned long long *n_collect_ptr; uint32_t collect_cap;
+    int64_t n_list;             // list mode entry count
+    // outputs per entry
+    double *ent_J;
+    uint32_t *ent_flags;
+    double *pred;               // list mode optional [n][N][2]
+    uint8_t *mask;              // search dump: patch worklist entries
+};
+
+struct SelectArgs {
+    int top_k, kp;
+    const unsigned long long *cand_keys;   // [kp] fast candidates (0 = empty)
+    const uint32_t *work; const uint32_t *collect;
+    uint32_t work_cap, collect_cap;
+    const double *ent_J;
+    const uint32_t *ent_flags;
+    uint64_t lo;
+    int collect_mode;           // 1: the collect pass ran; candidates = collect list
+    DevResult *res;
+};
+
+// launchers (return hipError_t of the launch)
+hipError_t launch_precompute_p(const float *features, const float *weights, int n_rows, int L,
+                               int A, int H, int64_t wstride, const int32_t *row_model,
+                               float *image_p, int pst, hipStream_t s);
+hipError_t launch_fast_impl(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode, hipStream_t s);
+int fast_kernel_supported(int n_models, int A, int H, int kp);
+hipError_t launch_merge_lists(const unsigned long long *lists, int n_lists, int kp,
+                              unsigned long long *out, hipStream_t s);
+hipError_t launch_canonical(const CanonArgs &a, int n_entries_max, bool search_mode, hipStream_t s);
+hipError_t launch_select(const SelectArgs &a, const FastConst &fc, const float *omega, hipStream_t s);
+
+}  // namespace mfi

@@ -1,0 +1,452 @@
+// Fast path of the exhaustive surrogate search (fp32 MFMA), gfx950.
+//
+// One wave evaluates a tile of 32 consecutive joint indices per step:
+//   decode       mixed-radix digits (Eq. 1) by odometer: the wave decodes its
+//                first tile once and then adds a fixed stride in mixed radix;
+//                each lane adds its column (0..31) with carries
+//   aggregate    fp32 sum in model order of every model's option row
+//                (the aggregate field of Section III-B), from LDS; slot 0 is
+//                the VRAM sum, compared with the cap (Eq. 4)
+//   surrogate    per model (Eq. 6): layer 1 = per-option precompute
+//                P[row] = b1 + W1_local x (the option's own columns, done once
+//                per option) as the accumulator init, plus W1_agg a on MFMA;
+//                layer 2 on v_mfma_f32_32x32x2f32 with the layer-1 accumulator
+//                registers fed back directly as the B operand (the accumulator
+//                row order is absorbed into the A-operand layout of W2);
+//                layer 3 (2 outputs) on VALU with one cross-half add
+//   mask/score   latency bound per model decided with an a-priori error bound:
+//                sure pass, sure fail, or "left to canonical re-evaluation";
+//                J = fma chain over models of omega_i thr_i
+//   top-K'       sure-feasible keys (J, lowest index) kept in a sorted
+//                register list per wave (lane l holds slot l), merged per
+//                workgroup at the end
+// Everything the kernel reads per configuration lives in LDS; the only HBM
+// traffic is the image load in the prologue and O(K') results.
+#include "mf_internal.h"
+
+namespace mfi {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ uint32_t ord_f32(float f)
+{
+    const uint32_t b = __float_as_uint(f);
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ unsigned long long readlane64(unsigned long long x, int src)
+{
+    const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)x, src);
+    const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), src);
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+__device__ __forceinline__ unsigned long long shfl_up1_64(unsigned long long x)
+{
+    const uint32_t lo = __shfl_up((int)(uint32_t)x, 1);
+    const uint32_t hi = __shfl_up((int)(uint32_t)(x >> 32), 1);
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+__device__ __forceinline__ unsigned long long wave_sum64(unsigned long long x)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+        const uint32_t lo = __shfl_xor((int)(uint32_t)x, m);
+        const uint32_t hi = __shfl_xor((int)(uint32_t)(x >> 32), m);
+        x += ((unsigned long long)hi << 32) | lo;
+    }
+    return x;
+}
+
+// Insert key nk (not yet present) into the wave's descending list: lane l < kp
+// holds slot l.  thr becomes the smallest key of the list (0 while not full).
+__device__ __forceinline__ void list_insert(unsigned long long &slot, unsigned long long nk, int lane,
+                                            int kp, unsigned long long &thr)
+{
+    const unsigned long long gt = __ballot(lane < kp && slot > nk);
+    const int pos = __popcll(gt);
+    const unsigned long long prev = shfl_up1_64(slot);
+    if (lane < kp) slot = lane < pos ? slot : (lane == pos ? nk : prev);
+    thr = readlane64(slot, kp - 1);
+}
+
+// Offer every lane's key to the list (keys of 0 are never inserted).
+__device__ __forceinline__ void list_offer(unsigned long long &slot, unsigned long long mykey, int lane,
+                                           int kp, unsigned long long &thr)
+{
+    unsigned long long cm = __ballot(mykey > thr);
+    while (cm) {
+        const int src = __ffsll((long long)cm) - 1;
+        cm &= cm - 1;
+        const unsigned long long nk = readlane64(mykey, src);
+        if (nk > thr) list_insert(slot, nk, lane, kp, thr);
+    }
+}
+
+// Append flagged lanes' values to a device list; the counter keeps counting
+// past cap so the host can see an overflow.
+__device__ __forceinline__ void list_append(bool flag, uint32_t value, int lane, unsigned long long *count,
+                                            uint32_t *list, uint32_t cap)
+{
+    const unsigned long long m = __ballot(flag);
+    if (m == 0) return;
+    unsigned long long base = 0;
+    if (lane == 0) base = atomicAdd(count, (unsigned long long)__popcll(m));
+    base = readlane64(base, 0);
+    const unsigned long long rank = __popcll(m & ((1ull << lane) - 1ull));
+    if (flag && base + rank < cap) list[base + rank] = value;
+}
+
+template <int MAXN, int A, int H>
+__global__ void __launch_bounds__(kSearchWaves * 64, 1)
+fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int kp)
+{
+    constexpr int MB = H / 32;         // 32-row blocks of a hidden layer
+    constexpr int S1 = A / 2;          // layer-1 MFMA k-steps (K = 2 each)
+    constexpr int AP = 8;              // aggregate row stride in LDS: [half][4]
+    extern __shared__ float4 smem4[];
+    float *smem = reinterpret_cast<float *>(smem4);
+    const FastLayout &Ly = args.lay;
+    const int N = fc.n_models;
+
+    for (int t = threadIdx.x; t < args.image_f4; t += blockDim.x) smem4[t] = args.image[t];
+    // [0,16) sla_lo  [16,32) sla_hi  [32,48) omega  [48,64) first option row per model (int)
+    float *par = smem + Ly.total_floats;
+    int *par_off = reinterpret_cast<int *>(par + 48);
+    unsigned long long *lst = reinterpret_cast<unsigned long long *>(par + 64);
+#pragma unroll
+    for (int i = 0; i < kMaxN; i++) {
+        // compile-time index into the argument block (keeps it out of scratch)
+        if (threadIdx.x == (unsigned)i && i < N) {
+            const double s = (double)args.sla[i], b = fc.bound_lat[i];
+            const double slack = (fabs(s) + b) * 0x1p-22 + 1e-30;
+            par[i] = (float)(s - b - slack);       // lat <= this  => canonical lat <= sla
+            par[16 + i] = (float)(s + b + slack);  // lat >  this  => canonical lat >  sla
+            par[32 + i] = args.omega[i];
+            par_off[i] = fc.opt_off[i];
+        }
+    }
+    __syncthreads();
+
+    const int lane = threadIdx.x & 63, half = lane >> 5, col = lane & 31;
+    const int wv = threadIdx.x >> 6;
+    const int gw = blockIdx.x * kSearchWaves + wv;
+    const uint64_t n = args.n;
+    const uint64_t n_tiles = (n + 31) >> 5;
+    const float theta = (float)args.theta;
+
+    uint32_t bd[MAXN];
+    if (mode != kModeList) {
+        uint64_t x = args.lo + (uint64_t)gw * 32u;
+#pragma unroll
+        for (int j = MAXN - 1; j >= 0; j--) {
+            if (j < N) {
+                const uint64_t k = (uint64_t)fc.K[j];
+                bd[j] = (uint32_t)(x % k);
+                x /= k;
+            } else {
+                bd[j] = 0;
+            }
+        }
+    }
+
+    unsigned long long slot = 0, thr_key = 0;
+    uint32_t c_vram = 0, c_feas = 0;
+
+    for (uint64_t tile = gw; tile < n_tiles; tile += (uint64_t)args.total_waves) {
+        const uint64_t off = tile * 32u + (uint64_t)col;
+        const bool valid = off < n;
+        uint32_t d[MAXN];
+        if (mode == kModeList) {
+            uint64_t x = args.idx_list[valid ? off : n - 1];
+#pragma unroll
+            for (int j = MAXN - 1; j >= 0; j--) {
+                if (j < N) {
+                    const uint64_t k = (uint64_t)fc.K[j];
+                    d[j] = (uint32_t)(x % k);
+                    x /= k;
+                } else {
+                    d[j] = 0;
+                }
+            }
+        } else {
+            uint32_t carry = (uint32_t)col;
+#pragma unroll
+            for (int j = MAXN - 1; j >= 0; j--) {
+                if (j < N) {
+                    const uint32_t t = bd[j] + carry;
+                    const uint32_t q = fc.magic[j] ? __umulhi(t, fc.magic[j]) : t;
+                    d[j] = t - q * (uint32_t)fc.K[j];
+                    carry = q;
+                } else {
+                    d[j] = 0;
+                }
+            }
+        }
+
+        // aggregate field (model order, fp32).  Lane half h accumulates the
+        // slots it feeds to layer 1 as B operand: internal slots 2s + h.
+        // Slot 0 (half 0, s 0) is the VRAM sum.
+        float ah[4] = {0.f, 0.f, 0.f, 0.f};
+        uint64_t dig0 = 0, dig1 = 0;   // digits packed 8 bits each: models 0..7, 8..15
+#pragma unroll
+        for (int j = 0; j < MAXN; j++) {
+            if (j < N) {
+                if (j < 8) dig0 |= (uint64_t)d[j] << (8 * j);
+                else dig1 |= (uint64_t)d[j] << (8 * (j - 8));
+                const uint32_t row = (uint32_t)fc.opt_off[j] + d[j];
+                const float4 v = *reinterpret_cast<const float4 *>(smem + Ly.off_g + row * AP + 4 * half);
+                ah[0] += v.x;
+                ah[1] += v.y;
+                ah[2] += v.z;
+                ah[3] += v.w;
+            }
+        }
+        const bool vram_ok = ah[0] <= fc.vram_cap;
+
+        float J = 0.f;
+        bool anyfail = false, anyunc = false;
+        for (int i = 0; i < N; i++) {
+            const uint64_t sel = (uint64_t)0 - (uint64_t)(i >= 8);
+            const uint64_t dw = dig0 ^ ((dig0 ^ dig1) & sel);
+            const uint32_t row = (uint32_t)par_off[i] + (uint32_t)((dw >> (8 * (i & 7))) & 0xFFu);
+            // ---- layer 1: P[row] + W1_agg a
+            floatx16 acc1[MB];
+            const float *prow = smem + Ly.off_p + row * (uint32_t)Ly.PST + 4 * half;
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                for (int q = 0; q < 4; q++) {
+                    const float4 v = *reinterpret_cast<const float4 *>(prow + 32 * mb + 8 * q);
+                    acc1[mb][4 * q + 0] = v.x;
+                    acc1[mb][4 * q + 1] = v.y;
+                    acc1[mb][4 * q + 2] = v.z;
+                    acc1[mb][4 * q + 3] = v.w;
+                }
+            const float *w1a = smem + Ly.off_w1a + i * (MB * S1 * 64) + lane;
+#pragma unroll
+            for (int s = 0; s < S1; s++) {
+                const float bop = ah[s];
+#pragma unroll
+                for (int mb = 0; mb < MB; mb++)
+                    acc1[mb] = __builtin_amdgcn_mfma_f32_32x32x2f32(w1a[(mb * S1 + s) * 64], bop, acc1[mb], 0, 0, 0);
+            }
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                for (int r = 0; r < 16; r++) acc1[mb][r] = fmaxf(acc1[mb][r], 0.f);
+            // ---- layer 2: b2 + W2 h1
+            floatx16 acc2[MB];
+            const float *b2 = smem + Ly.off_b2 + i * H + 4 * half;
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                for (int q = 0; q < 4; q++) {
+                    const float4 v = *reinterpret_cast<const float4 *>(b2 + 32 * mb + 8 * q);
+                    acc2[mb][4 * q + 0] = v.x;
+                    acc2[mb][4 * q + 1] = v.y;
+                    acc2[mb][4 * q + 2] = v.z;
+                    acc2[mb][4 * q + 3] = v.w;
+                }
+            const float *w2 = smem + Ly.off_w2 + i * (H * H) + lane * 4;
+#pragma unroll
+            for (int mb1 = 0; mb1 < MB; mb1++)
+#pragma unroll
+                for (int q = 0; q < 4; q++) {
+                    float4 wv4[MB];
+#pragma unroll
+                    for (int mb2 = 0; mb2 < MB; mb2++)
+                        wv4[mb2] = *reinterpret_cast<const float4 *>(w2 + ((mb2 * MB + mb1) * 4 + q) * 256);
+#pragma unroll
+                    for (int mb2 = 0; mb2 < MB; mb2++) {
+                        acc2[mb2] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv4[mb2].x, acc1[mb1][4 * q + 0], acc2[mb2], 0, 0, 0);
+                        acc2[mb2] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv4[mb2].y, acc1[mb1][4 * q + 1], acc2[mb2], 0, 0, 0);
+                        acc2[mb2] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv4[mb2].z, acc1[mb1][4 * q + 2], acc2[mb2], 0, 0, 0);
+                        acc2[mb2] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv4[mb2].w, acc1[mb1][4 * q + 3], acc2[mb2], 0, 0, 0);
+                    }
+                }
+            // ---- layer 3 (2 outputs) on VALU
+            const float *w3 = smem + Ly.off_w3 + i * (2 * H) + 4 * half;
+            float pl = 0.f, pt = 0.f;
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                for (int q = 0; q < 4; q++) {
+                    const float4 wl = *reinterpret_cast<const float4 *>(w3 + ((0 * MB + mb) * 4 + q) * 8);
+                    const float4 wt = *reinterpret_cast<const float4 *>(w3 + ((1 * MB + mb) * 4 + q) * 8);
+                    const float h0 = fmaxf(acc2[mb][4 * q + 0], 0.f), h1 = fmaxf(acc2[mb][4 * q + 1], 0.f);
+                    const float h2 = fmaxf(acc2[mb][4 * q + 2], 0.f), h3 = fmaxf(acc2[mb][4 * q + 3], 0.f);
+                    pl = fmaf(wl.x, h0, pl); pt = fmaf(wt.x, h0, pt);
+                    pl = fmaf(wl.y, h1, pl); pt = fmaf(wt.y, h1, pt);
+                    pl = fmaf(wl.z, h2, pl); pt = fmaf(wt.z, h2, pt);
+                    pl = fmaf(wl.w, h3, pl); pt = fmaf(wt.w, h3, pt);
+                }
+            pl += __shfl_xor(pl, 32);
+            pt += __shfl_xor(pt, 32);
+            const float *b3 = smem + Ly.off_b3 + 4 * i;
+            const float lat = pl + b3[0], thr = pt + b3[1];
+            const bool pass = lat <= par[i], fail = lat > par[16 + i];
+            anyfail |= fail;
+            anyunc |= !(pass || fail);
+            J = fmaf(par[32 + i], thr, J);
+            if (args.pred && valid && half == 0) {
+                args.pred[(off * (uint64_t)N + (uint64_t)i) * 2u + 0u] = lat;
+                args.pred[(off * (uint64_t)N + (uint64_t)i) * 2u + 1u] = thr;
+            }
+        }
+
+        if (mode != kModeList) {
+            const bool mine = valid && half == 0;
+            const bool sla_sure = !anyfail && !anyunc;
+            const bool feas_sure = mine && vram_ok && sla_sure;
+            // a latency decision the bound cannot settle: re-evaluated
+            // canonically when it can change the count (VRAM ok) or, in dump
+            // mode, the mask
+            const bool unc = mine && !anyfail && anyunc && (vram_ok || args.mask != nullptr);
+            if (mode == kModeSearch) {
+                c_vram += (mine && vram_ok) ? 1u : 0u;
+                c_feas += feas_sure ? 1u : 0u;
+                list_append(unc, (uint32_t)off, lane, &args.res->n_work, args.work, args.work_cap);
+                const unsigned long long key = feas_sure
+                    ? (((unsigned long long)ord_f32(J) << 32) | (unsigned long long)(0xFFFFFFFFu - (uint32_t)off))
+                    : 0ull;
+                list_offer(slot, key, lane, kp, thr_key);
+                if (args.mask && mine)
+                    args.mask[off] = (uint8_t)((vram_ok ? 1u : 0u) | (sla_sure ? 2u : 0u) |
+                                               (feas_sure ? 4u : 0u) | (unc ? 8u : 0u));
+            } else {
+                list_append(feas_sure && J >= theta, (uint32_t)off, lane, &args.res->n_collect,
+                            args.collect, args.collect_cap);
+            }
+        }
+
+        if (mode != kModeList) {
+            // advance the tile base by the grid stride, in mixed radix
+            uint32_t carry = 0;
+#pragma unroll
+            for (int j = MAXN - 1; j >= 0; j--) {
+                if (j < N) {
+                    uint32_t t = bd[j] + args.stride_digits[j] + carry;
+                    carry = t >= (uint32_t)fc.K[j] ? 1u : 0u;
+                    bd[j] = carry ? t - (uint32_t)fc.K[j] : t;
+                }
+            }
+        }
+    }
+
+    if (mode == kModeSearch) {
+        const unsigned long long sv = wave_sum64(c_vram), sf = wave_sum64(c_feas);
+        if (lane == 0) {
+            if (sv) atomicAdd(&args.res->n_vram, sv);
+            if (sf) atomicAdd(&args.res->n_feas_sure, sf);
+        }
+        if (lane < kp) lst[wv * kp + lane] = slot;
+        __syncthreads();
+        if (wv == 0) {
+            for (int w = 1; w < kSearchWaves; w++) {
+                const unsigned long long k2 = lane < kp ? lst[w * kp + lane] : 0ull;
+                list_offer(slot, k2, lane, kp, thr_key);
+            }
+            if (lane < kp) args.wg_lists[(uint64_t)blockIdx.x * kp + lane] = slot;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Merge the per-workgroup lists into one sorted top-kp list (one workgroup).
+// ---------------------------------------------------------------------------
+constexpr int kMergeWaves = 16;
+
+__global__ void __launch_bounds__(kMergeWaves * 64)
+merge_lists_kernel(const unsigned long long *lists, int n_keys, int kp, unsigned long long *out)
+{
+    __shared__ unsigned long long lst[kMergeWaves * 64];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    unsigned long long slot = 0, thr = 0;
+    for (int base = wv * 64; base < n_keys; base += kMergeWaves * 64) {
+        const int t = base + lane;
+        const unsigned long long k = t < n_keys ? lists[t] : 0ull;
+        list_offer(slot, k, lane, kp, thr);
+    }
+    lst[wv * 64 + lane] = lane < kp ? slot : 0ull;
+    __syncthreads();
+    if (wv == 0) {
+        for (int w = 1; w < kMergeWaves; w++) list_offer(slot, lst[w * 64 + lane], lane, kp, thr);
+        if (lane < kp) out[lane] = slot;
+    }
+}
+
+template <int MAXN, int A, int H>
+static hipError_t launch_fast_t(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode,
+                                hipStream_t s)
+{
+    const size_t lds = (size_t)a.lay.total_floats * 4 + 64 * 4 + (size_t)kSearchWaves * kp * 8;
+    auto fn = fast_kernel<MAXN, A, H>;
+    hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(kSearchWaves * 64), lds, s, a, fc, mode, kp);
+    return hipGetLastError();
+}
+
+int fast_kernel_supported(int n_models, int A, int H, int kp)
+{
+    if (n_models < 1 || n_models > 16) return 0;
+    if (!(A == 2 || A == 4 || A == 6 || A == 8)) return 0;
+    if (!(H == 32 || H == 64)) return 0;
+    if (kp < 1 || kp > 64) return 0;
+    return 1;
+}
+
+hipError_t launch_fast_impl(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode, hipStream_t s)
+{
+    const int N = fc.n_models, A = a.lay.A, H = a.lay.H;
+#define MF_FAST_CASE(MN, AA, HH) \
+    if (N <= MN && A == AA && H == HH) return launch_fast_t<MN, AA, HH>(a, fc, grid, kp, mode, s);
+#define MF_FAST_A(MN, HH) MF_FAST_CASE(MN, 2, HH) MF_FAST_CASE(MN, 4, HH) MF_FAST_CASE(MN, 6, HH) MF_FAST_CASE(MN, 8, HH)
+    MF_FAST_A(8, 32) MF_FAST_A(8, 64) MF_FAST_A(16, 32) MF_FAST_A(16, 64)
+#undef MF_FAST_A
+#undef MF_FAST_CASE
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_merge_lists(const unsigned long long *lists, int n_lists, int kp, unsigned long long *out,
+                              hipStream_t s)
+{
+    hipLaunchKernelGGL(merge_lists_kernel, dim3(1), dim3(kMergeWaves * 64), 0, s, lists, n_lists * kp, kp, out);
+    return hipGetLastError();
+}
+
+}  // namespace mfi
+
+namespace mfi {
+
+// Per-option first-layer precompute (the option's own columns, Eq. 6):
+// P[row][h] = b1[h] + sum_k W1[h][k] x[row][k] over the L local columns, as
+// one fp64 fma chain, rounded to fp32.  Reads the canonical image (W1T[k][h]).
+__global__ void precompute_p_kernel(const float *features, const float *canon_w, int n_rows, int L, int A,
+                                    int H, int64_t wstride, const int32_t *row_model, float *image_p, int pst)
+{
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (int64_t)n_rows * H) return;
+    const int row = (int)(t / H), h = (int)(t % H);
+    const int nin = L + A;
+    const float *w = canon_w + (int64_t)row_model[row] * wstride;
+    const float *W1T = w, *b1 = w + (int64_t)nin * H;
+    double c = (double)b1[h];
+    for (int k = 0; k < L; k++) c = fma((double)W1T[(int64_t)k * H + h], (double)features[(int64_t)row * L + k], c);
+    image_p[(int64_t)row * pst + h] = (float)c;
+}
+
+hipError_t launch_precompute_p(const float *features, const float *weights, int n_rows, int L, int A, int H,
+                               int64_t wstride, const int32_t *row_model, float *image_p, int pst, hipStream_t s)
+{
+    const int64_t total = (int64_t)n_rows * H;
+    const int blk = 256;
+    const int grid = (int)((total + blk - 1) / blk);
+    hipLaunchKernelGGL(precompute_p_kernel, dim3(grid), dim3(blk), 0, s, features, weights, n_rows, L, A, H, wstride,
+                       row_model, image_p, pst);
+    return hipGetLastError();
+}
+
+}  // namespace mfi

@@ -1,0 +1,257 @@
+"""ctypes binding of libmf.so (include/mf.h).
+
+Marshalling only: torch tensors supply device memory and the HIP stream;
+every step of the search runs in the library's kernels.  Importing this module
+fails loudly when the HIP library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmf.so")
+
+MF_OK, MF_EINVAL, MF_ENOMEM, MF_EDEVICE, MF_EUNSUPPORTED, MF_EOVERFLOW, MF_EINTERNAL = range(7)
+MF_F32, MF_BF16 = 0, 1
+MF_DUMP = 1
+MAX_TOPK = 64
+MAX_MODELS = 16
+
+EXPORTS = ["mf_problem_create", "mf_problem_destroy", "mf_space_size", "mf_decode",
+           "mf_workspace_size", "mf_search", "mf_eval_fast", "mf_eval_canonical",
+           "mf_ga_workspace_size", "mf_ga_run", "mf_status_string"]
+
+
+class MfError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {status_string(status)}")
+        self.status = status
+
+
+class Desc(C.Structure):
+    _fields_ = [("n_models", C.c_int32), ("n_local", C.c_int32), ("n_agg", C.c_int32),
+                ("hidden1", C.c_int32), ("hidden2", C.c_int32),
+                ("h_n_options", C.c_void_p), ("h_agg_cols", C.c_void_p),
+                ("vram_slot", C.c_int32), ("vram_cap", C.c_float), ("dtype", C.c_int32)]
+
+
+class SearchArgs(C.Structure):
+    _fields_ = [("lo", C.c_uint64), ("hi", C.c_uint64), ("top_k", C.c_int32), ("flags", C.c_uint32),
+                ("d_sla", C.c_void_p), ("d_omega", C.c_void_p), ("d_mask", C.c_void_p),
+                ("d_pred", C.c_void_p)]
+
+
+class Result(C.Structure):
+    _fields_ = [("n_eval", C.c_uint64), ("n_vram", C.c_uint64), ("n_feas", C.c_uint64),
+                ("n_flagged", C.c_uint64), ("n_topk_collect", C.c_uint64),
+                ("n_top", C.c_int32), ("n_splits", C.c_int32),
+                ("top_idx", C.c_uint64 * MAX_TOPK), ("top_J", C.c_double * MAX_TOPK),
+                ("main_kernel_ms", C.c_float), ("pad", C.c_float)]
+
+
+class GAArgs(C.Structure):
+    _fields_ = [("n_scen", C.c_int32), ("pop", C.c_int32), ("gens", C.c_int32), ("tourn_k", C.c_int32),
+                ("p_cx", C.c_float), ("p_swap", C.c_float), ("p_mut", C.c_float), ("pad", C.c_float),
+                ("seed", C.c_uint64), ("d_sla", C.c_void_p), ("d_omega", C.c_void_p)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python -m paper_2609_02109_amd.build` (or __graft_entry__.build())")
+    L = C.CDLL(LIB_PATH)
+    P = C.c_void_p
+    S = C.c_int
+    sig = {
+        "mf_problem_create": (S, [P, P, P, P, P]),
+        "mf_problem_destroy": (None, [P]),
+        "mf_space_size": (S, [P, P]),
+        "mf_decode": (S, [P, C.c_uint64, P]),
+        "mf_workspace_size": (S, [P, P, P]),
+        "mf_search": (S, [P, P, P, C.c_size_t, P, P]),
+        "mf_eval_fast": (S, [P, P, C.c_int64, P, P]),
+        "mf_eval_canonical": (S, [P, P, C.c_int64, P, P, P, P, P, P]),
+        "mf_ga_workspace_size": (S, [P, P, P]),
+        "mf_ga_run": (S, [P, P, P, C.c_size_t, P, P, P, P]),
+        "mf_status_string": (C.c_char_p, [S]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    return L
+
+
+lib = _load()
+
+
+def status_string(s: int) -> str:
+    return lib.mf_status_string(int(s)).decode()
+
+
+def _check(s: int, where: str):
+    if s != MF_OK:
+        raise MfError(s, where)
+
+
+def _ptr(t):
+    """Device (or host) address of a torch tensor or numpy array; None -> NULL."""
+    if t is None:
+        return None
+    if hasattr(t, "data_ptr"):
+        return C.c_void_p(t.data_ptr())
+    return t.ctypes.data_as(C.c_void_p)
+
+
+def _stream(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+class Problem:
+    """A created problem (mf_problem).  `inst` carries the instance arrays
+    (n_options, features, agg_cols, weights, ...), e.g. a synth.Instance."""
+
+    def __init__(self, inst, device="cuda", stream=None):
+        import torch
+        self.inst = inst
+        self.N = int(inst.n_models)
+        self.device = torch.device(device)
+        self._n_options = np.ascontiguousarray(inst.n_options, np.int32)
+        self._agg_cols = np.ascontiguousarray(inst.agg_cols, np.int32)
+        feats = torch.from_numpy(np.ascontiguousarray(inst.features, np.float32)).to(self.device)
+        w = torch.from_numpy(np.ascontiguousarray(inst.weights, np.float32)).to(self.device)
+        self.desc = Desc(self.N, int(inst.n_local), int(inst.n_agg), int(inst.hidden1),
+                         int(inst.hidden2), _ptr(self._n_options), _ptr(self._agg_cols),
+                         int(inst.vram_slot), float(inst.vram_cap),
+                         MF_BF16 if inst.dtype == "bf16" else MF_F32)
+        h = C.c_void_p()
+        _check(lib.mf_problem_create(C.byref(self.desc), _ptr(feats), _ptr(w), _stream(stream),
+                                     C.byref(h)), "mf_problem_create")
+        self.handle = h
+        self._ws = None
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib.mf_problem_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def space_size(self) -> int:
+        out = C.c_uint64()
+        _check(lib.mf_space_size(self.handle, C.byref(out)), "mf_space_size")
+        return int(out.value)
+
+    def decode(self, idx: int) -> np.ndarray:
+        d = np.zeros(self.N, np.int32)
+        _check(lib.mf_decode(self.handle, C.c_uint64(idx), _ptr(d)), "mf_decode")
+        return d
+
+    def _dev(self, a, dtype):
+        import torch
+        if a is None:
+            return None
+        if isinstance(a, torch.Tensor):
+            return a.to(self.device, dtype).contiguous()
+        return torch.as_tensor(np.asarray(a), dtype=dtype, device=self.device).contiguous()
+
+    def workspace(self, nbytes: int):
+        import torch
+        if self._ws is None or self._ws.numel() < nbytes:
+            self._ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+        return self._ws
+
+    def search(self, sla, omega, k=1, lo=0, hi=None, dump=False, stream=None):
+        """Exhaustive search over [lo, hi).  Returns a dict of counts and the
+        exact top-k; with dump=True also the per-index mask and fast-path
+        predictions (device tensors)."""
+        import torch
+        if hi is None:
+            hi = self.space_size
+        d_sla = self._dev(sla, torch.float32)
+        d_om = self._dev(omega, torch.float32)
+        mask = pred = None
+        if dump:
+            mask = torch.zeros(max(hi - lo, 1), dtype=torch.uint8, device=self.device)
+            pred = torch.zeros((max(hi - lo, 1), self.N, 2), dtype=torch.float32, device=self.device)
+        args = SearchArgs(lo, hi, int(k), MF_DUMP if dump else 0, _ptr(d_sla), _ptr(d_om),
+                          _ptr(mask), _ptr(pred))
+        nbytes = C.c_size_t()
+        _check(lib.mf_workspace_size(self.handle, C.byref(args), C.byref(nbytes)), "mf_workspace_size")
+        ws = self.workspace(nbytes.value)
+        res = Result()
+        _check(lib.mf_search(self.handle, C.byref(args), _ptr(ws), C.c_size_t(ws.numel()),
+                             _stream(stream), C.byref(res)), "mf_search")
+        nt = int(res.n_top)
+        out = dict(n_eval=int(res.n_eval), n_vram=int(res.n_vram), n_feas=int(res.n_feas),
+                   n_flagged=int(res.n_flagged), n_topk_collect=int(res.n_topk_collect),
+                   n_splits=int(res.n_splits), main_kernel_ms=float(res.main_kernel_ms),
+                   top_idx=np.array(res.top_idx[:nt], np.uint64),
+                   top_J=np.array(res.top_J[:nt], np.float64))
+        if dump:
+            out.update(mask=mask[:hi - lo], pred=pred[:hi - lo])
+        return out
+
+    def search_raw(self, args: SearchArgs, ws, stream=None) -> Result:
+        """Direct call for timing loops: caller-built SearchArgs and workspace."""
+        res = Result()
+        _check(lib.mf_search(self.handle, C.byref(args), _ptr(ws), C.c_size_t(ws.numel()),
+                             _stream(stream), C.byref(res)), "mf_search")
+        return res
+
+    def eval_fast(self, idx, stream=None):
+        import torch
+        d_idx = self._dev(idx, torch.int64)
+        n = int(d_idx.numel())
+        pred = torch.zeros((max(n, 1), self.N, 2), dtype=torch.float32, device=self.device)
+        _check(lib.mf_eval_fast(self.handle, _ptr(d_idx), n, _ptr(pred), _stream(stream)),
+               "mf_eval_fast")
+        return pred[:n]
+
+    def eval_canonical(self, idx, sla, omega, stream=None):
+        import torch
+        d_idx = self._dev(idx, torch.int64)
+        n = int(d_idx.numel())
+        pred = torch.zeros((max(n, 1), self.N, 2), dtype=torch.float64, device=self.device)
+        J = torch.zeros(max(n, 1), dtype=torch.float64, device=self.device)
+        fl = torch.zeros(max(n, 1), dtype=torch.int32, device=self.device)
+        # the call only enqueues: inputs must stay alive (referenced) until it
+        # has been issued; stream order covers their later reuse
+        d_sla = self._dev(sla, torch.float32)
+        d_om = self._dev(omega, torch.float32)
+        _check(lib.mf_eval_canonical(self.handle, _ptr(d_idx), n, _ptr(d_sla), _ptr(d_om), _ptr(pred),
+                                     _ptr(J), _ptr(fl), _stream(stream)), "mf_eval_canonical")
+        return dict(pred=pred[:n], J=J[:n], flags=fl[:n], _inputs=(d_idx, d_sla, d_om))
+
+    def ga(self, sla, omega, pop=2048, gens=100, tourn_k=3, p_cx=0.7, p_swap=0.5, p_mut=0.05,
+           seed=0, final_pop=False, stream=None):
+        """GA scheduler over S scenarios (rows of sla / omega)."""
+        import torch
+        d_sla = self._dev(sla, torch.float32)
+        d_om = self._dev(omega, torch.float32)
+        S = int(d_sla.shape[0])
+        args = GAArgs(S, int(pop), int(gens), int(tourn_k), float(p_cx), float(p_swap), float(p_mut),
+                      0.0, int(seed), _ptr(d_sla), _ptr(d_om))
+        nbytes = C.c_size_t()
+        _check(lib.mf_ga_workspace_size(self.handle, C.byref(args), C.byref(nbytes)),
+               "mf_ga_workspace_size")
+        ws = self.workspace(nbytes.value)
+        best_idx = np.zeros(S, np.uint64)
+        best_J = np.zeros(S, np.float64)
+        fp = torch.zeros((S, pop), dtype=torch.int64, device=self.device) if final_pop else None
+        _check(lib.mf_ga_run(self.handle, C.byref(args), _ptr(ws), C.c_size_t(ws.numel()),
+                             _stream(stream), _ptr(best_idx), _ptr(best_J), _ptr(fp)), "mf_ga_run")
+        out = dict(best_idx=best_idx, best_J=best_J)
+        if final_pop:
+            out["final_pop"] = fp
+        return out

@@ -24,6 +24,7 @@ Continuous columns are quantised to multiples of 2**-14, so every aggregate
 sum of at most 16 rows is exact in fp32 whatever the summation order.
 
 Aggregate slots (each the sum over all N models of one option column):
+  A=2: [sum SM, sum VRAM]
   A=4: [sum SM, sum VRAM, sum BW, #LLM]
   A=6: + [#vision, sum log2 batch]
   A=8: + [sum noise6, sum noise7]
@@ -40,7 +41,8 @@ import numpy as np
 
 GRID = 2.0 ** -14
 COL_LLM, COL_VIS, COL_LOG2B, COL_SM, COL_VRAM, COL_BW = 0, 1, 2, 3, 4, 5
-AGG_COLS = {4: [COL_SM, COL_VRAM, COL_BW, COL_LLM],
+AGG_COLS = {2: [COL_SM, COL_VRAM],
+            4: [COL_SM, COL_VRAM, COL_BW, COL_LLM],
             6: [COL_SM, COL_VRAM, COL_BW, COL_LLM, COL_VIS, COL_LOG2B],
             8: [COL_SM, COL_VRAM, COL_BW, COL_LLM, COL_VIS, COL_LOG2B, 6, 7]}
 VRAM_SLOT = 1
