@@ -30,7 +30,8 @@ struct mf_problem {
     // device memory (one allocation)
     void *d_mem = nullptr;
     float4 *d_image = nullptr;
-    float *d_canon = nullptr, *d_features = nullptr, *d_zeros = nullptr;
+    float *d_canon = nullptr, *d_features = nullptr, *d_zeros = nullptr, *d_centre = nullptr;
+    std::vector<float> centre;   // aggregate centre per slot (original slot order)
     int32_t *d_agg_cols = nullptr, *d_row_model = nullptr;
     FastLayout lay{};
     FastConst fc{};
@@ -67,6 +68,10 @@ bool bf16_exact(float x)
 // Numerical Algorithms, 2nd ed., Sec. 3.1).  Errors of a layer's input
 // propagate through |W| (relu is 1-Lipschitz).  Magnitudes use the largest
 // |input| over all options and all joint configurations.
+//
+// Fast path, layer 1: P'[o] = b1 + W1_loc x_o + W1_agg c (fp64 chain of L+A
+// terms, rounded to fp32), then A fp32 fmas W1_agg (a - c) onto it, with
+// a - c rounded to fp32 (exact on the generator's grid).
 void model_bounds(const mf_problem &p, const std::vector<float> &F, const std::vector<float> &W, int i,
                   double *b_lat, double *b_thr, double *m_thr)
 {
@@ -74,26 +79,60 @@ void model_bounds(const mf_problem &p, const std::vector<float> &F, const std::v
     const float *w = W.data() + (int64_t)i * p.wstride;
     const float *W1 = w, *b1 = W1 + (int64_t)H1 * nin, *W2 = b1 + H1, *b2 = W2 + (int64_t)H2 * H1, *W3 = b2 + H2,
                 *b3 = W3 + 2 * H2;
-    std::vector<double> xmax(L, 0.0), amax(A, 0.0);
+    std::vector<double> xmax(L, 0.0), amax(A, 0.0), amaxc(A, 0.0);
     for (int o = 0; o < p.K[i]; o++)
         for (int k = 0; k < L; k++)
             xmax[k] = std::max(xmax[k], (double)std::fabs(F[(int64_t)(p.opt_off[i] + o) * L + k]));
-    for (int j = 0; j < p.N; j++)
-        for (int k = 0; k < A; k++) {
-            double m = 0.0;
-            for (int o = 0; o < p.K[j]; o++)
-                m = std::max(m, (double)std::fabs(F[(int64_t)(p.opt_off[j] + o) * L + p.agg_cols[k]]));
-            amax[k] += m;
+    for (int k = 0; k < A; k++) {
+        double smax = 0.0, smin = 0.0, sabs = 0.0;
+        for (int j = 0; j < p.N; j++) {
+            double mx = -INFINITY, mn = INFINITY, ma = 0.0;
+            for (int o = 0; o < p.K[j]; o++) {
+                const double v = F[(int64_t)(p.opt_off[j] + o) * L + p.agg_cols[k]];
+                mx = std::max(mx, v);
+                mn = std::min(mn, v);
+                ma = std::max(ma, std::fabs(v));
+            }
+            smax += mx;
+            smin += mn;
+            sabs += ma;
         }
+        amax[k] = sabs;
+        amaxc[k] = std::max(std::fabs(smax - p.centre[k]), std::fabs(smin - p.centre[k])) * (1 + 1e-12);
+    }
     std::vector<double> M1(H1), e1f(H1), e1c(H1), M2(H2), e2f(H2), e2c(H2);
     for (int h = 0; h < H1; h++) {
-        double pm = std::fabs((double)b1[h]), am = 0.0;
-        for (int k = 0; k < L; k++) pm += std::fabs((double)W1[(int64_t)h * nin + k]) * xmax[k];
-        for (int k = 0; k < A; k++) am += std::fabs((double)W1[(int64_t)h * nin + L + k]) * amax[k];
-        M1[h] = pm + am;
-        // fast: P in fp64 (L fmas) rounded to fp32, then A fp32 fmas onto it
-        e1f[h] = gam(L, kU64) * pm + kU32 * pm * (1 + gam(L, kU64)) + gam(A, kU32) * M1[h] * (1 + 2 * kU32);
-        e1c[h] = gam(nin, kU64) * M1[h];
+        // |P'| over this model's options, and the magnitudes of its fp64 chain
+        double pmax = 0.0, pchain = 0.0;
+        double cpart = 0.0, cabs = std::fabs((double)b1[h]);
+        for (int k = 0; k < A; k++) {
+            cpart += (double)W1[(int64_t)h * nin + L + k] * p.centre[k];
+            cabs += std::fabs((double)W1[(int64_t)h * nin + L + k] * p.centre[k]);
+        }
+        for (int o = 0; o < p.K[i]; o++) {
+            double v = (double)b1[h] + cpart, va = cabs;
+            for (int k = 0; k < L; k++) {
+                const double t = (double)W1[(int64_t)h * nin + k] * F[(int64_t)(p.opt_off[i] + o) * L + k];
+                v += t;
+                va += std::fabs(t);
+            }
+            pmax = std::max(pmax, std::fabs(v) + 1e-12 * va);
+            pchain = std::max(pchain, va);
+        }
+        double am = 0.0, aw = 0.0, am_full = std::fabs((double)b1[h]);
+        for (int k = 0; k < A; k++) {
+            const double wa = std::fabs((double)W1[(int64_t)h * nin + L + k]);
+            am += wa * amaxc[k];
+            aw += wa * amaxc[k];
+            am_full += wa * amax[k];
+        }
+        for (int k = 0; k < L; k++) am_full += std::fabs((double)W1[(int64_t)h * nin + k]) * xmax[k];
+        M1[h] = pmax + am;
+        e1f[h] = gam(L + A, kU64) * pchain            // fp64 precompute
+                 + kU32 * pmax                         // rounding P' to fp32
+                 + kU32 * aw                           // rounding a - c to fp32
+                 + gam(A, kU32) * M1[h] * (1 + 2 * kU32);   // A fp32 fmas
+        e1c[h] = gam(nin, kU64) * am_full;             // canonical chain on uncentred inputs
     }
     for (int v = 0; v < H2; v++) {
         double m = std::fabs((double)b2[v]), pf = 0.0, pc = 0.0, mf = m, mc = m;
@@ -153,7 +192,7 @@ void stride_digits(const mf_problem &p, uint64_t stride, uint32_t *out)
 
 // Workspace layout for one search launch set over n configurations.
 struct WsLayout {
-    size_t res, work, collect, lists, cand, entJ, entF, total;
+    size_t res, work, workJ, collect, lists, cand, entJ, entF, total;
     uint32_t work_cap, collect_cap;
     int kp, grid;
 };
@@ -165,12 +204,16 @@ WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k)
     const uint64_t tiles = (n + 31) / 32;
     uint64_t g = (tiles + kSearchWaves - 1) / kSearchWaves;
     w.grid = (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)p.num_cus));
-    const uint64_t cap = std::min<uint64_t>(std::max<uint64_t>(n, 1024), (uint64_t)kDefaultWorklist);
+    // certification list: 1/128 of the range, at least 2^20 entries (never
+    // more than the range), at most 2^26
+    const uint64_t want = std::min<uint64_t>(std::max<uint64_t>(n / 128, (uint64_t)kDefaultWorklist), 1ull << 26);
+    const uint64_t cap = std::max<uint64_t>(std::min<uint64_t>(want, n), 1024);
     w.work_cap = (uint32_t)cap;
-    w.collect_cap = (uint32_t)cap;
+    w.collect_cap = (uint32_t)std::max<uint64_t>(std::min<uint64_t>((uint64_t)kDefaultWorklist, n), 1024);
     size_t o = 0;
     w.res = o; o = align256(o + sizeof(DevResult));
-    w.work = o; o = align256(o + (size_t)w.work_cap * 4);
+    w.work = o; o = align256(o + (size_t)w.work_cap * 8);
+    w.workJ = o; o = align256(o + (size_t)w.work_cap * 4);
     w.collect = o; o = align256(o + (size_t)w.collect_cap * 4);
     w.lists = o; o = align256(o + (size_t)w.grid * w.kp * 8);
     w.cand = o; o = align256(o + (size_t)w.kp * 8);
@@ -230,7 +273,8 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
 {
     const WsLayout w = ws_layout(*p, n, args->top_k);
     DevResult *R = reinterpret_cast<DevResult *>(ws + w.res);
-    uint32_t *work = reinterpret_cast<uint32_t *>(ws + w.work);
+    unsigned long long *work = reinterpret_cast<unsigned long long *>(ws + w.work);
+    float *workJ = reinterpret_cast<float *>(ws + w.workJ);
     uint32_t *collect = reinterpret_cast<uint32_t *>(ws + w.collect);
     unsigned long long *lists = reinterpret_cast<unsigned long long *>(ws + w.lists);
     unsigned long long *cand = reinterpret_cast<unsigned long long *>(ws + w.cand);
@@ -251,6 +295,7 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     fa.omega = args->d_omega;
     fa.res = R;
     fa.work = work;
+    fa.work_J = workJ;
     fa.work_cap = w.work_cap;
     fa.collect = collect;
     fa.collect_cap = w.collect_cap;
@@ -266,8 +311,9 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     ca.sla = args->d_sla; ca.omega = args->d_omega;
     ca.lo = lo;
     ca.cand_keys = cand; ca.n_cand_keys = w.kp;
-    ca.work = work; ca.n_work_ptr = &R->n_work; ca.work_cap = w.work_cap;
-    ca.collect = collect; ca.n_collect_ptr = nullptr; ca.collect_cap = w.collect_cap;
+    ca.work = work; ca.work_J = workJ; ca.work_cap = w.work_cap;
+    ca.collect = collect; ca.collect_cap = w.collect_cap;
+    ca.res = R; ca.top_k = args->top_k; ca.collect_mode = 0;
     ca.ent_J = entJ; ca.ent_flags = entF;
     ca.mask = fa.mask;
 
@@ -315,8 +361,7 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
         MF_HIP2(hipEventRecord(ev0, s));
         MF_HIP2(launch_fast_impl(fa, p->fc, w.grid, w.kp, kModeCollect, s));
         MF_HIP2(hipEventRecord(ev1, s));
-        ca.n_cand_keys = 0;
-        ca.n_collect_ptr = &R->n_collect;
+        ca.collect_mode = 1;
         ca.mask = nullptr;
         MF_HIP2(launch_canonical(ca, (int)std::min<uint64_t>((uint64_t)w.work_cap + w.collect_cap, 1u << 20), true, s));
         sa.collect_mode = 1;
@@ -461,6 +506,19 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
         return MF_EDEVICE;
     }
 
+    // aggregate centre per slot: the mean of the slot over the joint space
+    // (sum over models of the mean option value), rounded to the 2^-14 grid
+    p->centre.assign(A, 0.f);
+    for (int k = 0; k < A; k++) {
+        double m = 0.0;
+        for (int i = 0; i < N; i++) {
+            double s1 = 0.0;
+            for (int o = 0; o < p->K[i]; o++) s1 += F[(int64_t)(p->opt_off[i] + o) * L + p->agg_cols[k]];
+            m += s1 / p->K[i];
+        }
+        p->centre[k] = (float)(std::nearbyint(m * 16384.0) / 16384.0);
+    }
+
     // ---- fast path (fp32, H1 == H2 in {32, 64}, A in {2,4,6,8})
     p->fast_ok = !p->bf16 && H1 == H2 && fast_kernel_supported(N, A, H1, 64);
     const int H = H1;
@@ -476,6 +534,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
         ly.off_b3 = o; o += N * 4;
         ly.off_p = o; o += sumK * ly.PST;
         ly.off_g = o; o += sumK * ly.AP;
+        ly.off_c = o; o += 8;
         ly.total_floats = (o + 3) & ~3;
         const size_t lds = (size_t)ly.total_floats * 4 + 64 * 4 + (size_t)kSearchWaves * 64 * 8;
         if (lds > 163840) p->fast_ok = false;
@@ -522,6 +581,11 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
                     const int k = 2 * st + hf;
                     img[ly.off_g + r * ly.AP + hf * 4 + st] = k < A ? F[(int64_t)r * L + p->agg_cols[perm[k]]] : 0.f;
                 }
+        for (int hf = 0; hf < 2; hf++)
+            for (int st = 0; st < 4; st++) {
+                const int k = 2 * st + hf;
+                img[ly.off_c + hf * 4 + st] = k < A ? p->centre[perm[k]] : 0.f;
+            }
         FastConst &fc = p->fc;
         fc.n_models = N;
         for (int i = 0; i < N; i++) {
@@ -559,6 +623,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     const size_t o_agg = off; off = align256(off + (size_t)A * 4);
     const size_t o_rm = off; off = align256(off + (size_t)sumK * 4);
     const size_t o_z = off; off = align256(off + 64 * 4);
+    const size_t o_c = off; off = align256(off + (size_t)A * 4);
     if (hipMalloc(&p->d_mem, off) != hipSuccess) { delete p; return MF_ENOMEM; }
     char *base = (char *)p->d_mem;
     p->d_image = reinterpret_cast<float4 *>(base + o_img);
@@ -567,6 +632,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     p->d_agg_cols = reinterpret_cast<int32_t *>(base + o_agg);
     p->d_row_model = reinterpret_cast<int32_t *>(base + o_rm);
     p->d_zeros = reinterpret_cast<float *>(base + o_z);
+    p->d_centre = reinterpret_cast<float *>(base + o_c);
     bool ok = true;
     ok = ok && hipMemsetAsync(p->d_zeros, 0, 64 * 4, s) == hipSuccess;
     if (!img.empty()) ok = ok && hipMemcpyAsync(p->d_image, img.data(), img.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
@@ -574,8 +640,9 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     ok = ok && hipMemcpyAsync(p->d_features, F.data(), F.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
     ok = ok && hipMemcpyAsync(p->d_agg_cols, p->agg_cols.data(), (size_t)A * 4, hipMemcpyHostToDevice, s) == hipSuccess;
     ok = ok && hipMemcpyAsync(p->d_row_model, row_model.data(), (size_t)sumK * 4, hipMemcpyHostToDevice, s) == hipSuccess;
+    ok = ok && hipMemcpyAsync(p->d_centre, p->centre.data(), (size_t)A * 4, hipMemcpyHostToDevice, s) == hipSuccess;
     if (ok && p->fast_ok)
-        ok = launch_precompute_p(p->d_features, p->d_canon, sumK, L, A, H, p->wstride, p->d_row_model,
+        ok = launch_precompute_p(p->d_features, p->d_canon, p->d_centre, sumK, L, A, H, p->wstride, p->d_row_model,
                                  reinterpret_cast<float *>(p->d_image) + ly.off_p, ly.PST, s) == hipSuccess;
     ok = ok && hipStreamSynchronize(s) == hipSuccess;
     if (!ok) {

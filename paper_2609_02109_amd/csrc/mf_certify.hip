@@ -10,7 +10,7 @@
 //
 // One single-wave workgroup per entry: lanes take hidden units, the uniform
 // parts (decode, aggregate, output units) run redundantly per lane.
-#include "mf_internal.h"
+#include "mf_device.h"
 
 namespace mfi {
 
@@ -48,17 +48,30 @@ canon_kernel(const CanonArgs a, const int search_mode)
     const int N = a.n_models, L = a.L, A = a.A, H1 = a.H1, H2 = a.H2, nin = L + A;
 
     int64_t n_cand = 0, n_work = 0, n_coll = 0, n_ent;
+    double jthr = -INFINITY;   // certification entries need the full J only from here up
     if (search_mode) {
-        n_cand = a.n_cand_keys;
-        n_work = a.n_work_ptr ? (int64_t)min(*a.n_work_ptr, (unsigned long long)a.work_cap) : 0;
-        n_coll = a.n_collect_ptr ? (int64_t)min(*a.n_collect_ptr, (unsigned long long)a.collect_cap) : 0;
+        n_cand = a.collect_mode ? 0 : a.n_cand_keys;
+        n_work = (int64_t)min(a.res->n_work, (unsigned long long)a.work_cap);
+        n_coll = a.collect_mode ? (int64_t)min(a.res->n_collect, (unsigned long long)a.collect_cap) : 0;
         n_ent = n_cand + n_work + n_coll;
+        if (a.collect_mode) {
+            jthr = a.res->theta;
+        } else {
+            const unsigned long long ck = a.cand_keys[a.top_k - 1];
+            if (ck != 0ull) {
+                const double eJ = a.res->eJ;
+                const double jk = (double)unord_f32((uint32_t)(ck >> 32));
+                jthr = jk - 2.0 * eJ - (fabs(jk) + eJ) * 0x1p-20 - 1e-30;
+            }
+        }
     } else {
         n_ent = a.n_list;
     }
 
     for (int64_t e = blockIdx.x; e < n_ent; e += gridDim.x) {
         uint64_t idx, off = 0;
+        uint32_t models = 0xFFFFFFFFu;   // models to evaluate
+        bool work_entry = false, need_J = true;
         if (search_mode) {
             if (e < n_cand) {
                 const unsigned long long key = a.cand_keys[e];
@@ -68,7 +81,11 @@ canon_kernel(const CanonArgs a, const int search_mode)
                 }
                 off = 0xFFFFFFFFu - (uint32_t)(key & 0xFFFFFFFFull);
             } else if (e < n_cand + n_work) {
-                off = a.work[e - n_cand];
+                const unsigned long long w = a.work[e - n_cand];
+                off = (uint32_t)(w & 0xFFFFFFFFull);
+                work_entry = true;
+                need_J = (double)a.work_J[e - n_cand] >= jthr;
+                if (!need_J) models = (uint32_t)(w >> 32);
             } else {
                 off = a.collect[e - n_cand - n_work];
             }
@@ -96,6 +113,7 @@ canon_kernel(const CanonArgs a, const int search_mode)
         uint32_t fl = 0;
         double J = 0.0;
         for (int i = 0; i < N; i++) {
+            if (!((models >> i) & 1u)) continue;
             const float *w = a.weights + (int64_t)i * a.wstride;
             const float *W1T = w, *b1 = W1T + (int64_t)nin * H1, *W2T = b1 + H1, *b2 = W2T + (int64_t)H1 * H2,
                         *W3 = b2 + H2, *b3 = W3 + 2 * H2;
@@ -132,10 +150,12 @@ canon_kernel(const CanonArgs a, const int search_mode)
         }
         const bool feas = vram_ok && sla_ok;
         fl |= (vram_ok ? 1u : 0u) | (sla_ok ? 2u : 0u) | (feas ? 4u : 0u);
+        if (feas && !need_J) fl |= kEntNoJ;
         if (lane == 0) {
-            if (a.ent_J) a.ent_J[e] = feas ? J : -INFINITY;
+            if (a.ent_J) a.ent_J[e] = (feas && need_J) ? J : -INFINITY;
             if (a.ent_flags) a.ent_flags[e] = fl;
-            if (search_mode && a.mask && e >= n_cand && e < n_cand + n_work)
+            if (work_entry && need_J && !a.collect_mode) atomicAdd(&a.res->n_full_J, 1ull);
+            if (search_mode && a.mask && work_entry)
                 a.mask[off] = (uint8_t)((a.mask[off] & 1u) | (sla_ok ? 2u : 0u) | (feas ? 4u : 0u) | 8u);
         }
     }
@@ -196,24 +216,6 @@ __device__ void list128_offer(K128 &slot, const K128 &mine, int lane, int k, K12
 
 constexpr int kSelWaves = 16;
 
-__device__ double call_eJ(const FastConst &fc, const float *omega)
-{
-    const int N = fc.n_models;
-    const double g = N * 0x1p-24 / (1.0 - N * 0x1p-24);
-    double e = 0.0, m = 0.0;
-    for (int i = 0; i < N; i++) {
-        const double w = fabs((double)omega[i]);
-        e += w * (fc.bound_thr[i] + g * (fc.mag_thr[i] + fc.bound_thr[i]));
-        m += w * fc.mag_thr[i];
-    }
-    return (e + m * 0x1p-50) * (1.0 + 0x1p-20) + 1e-30;
-}
-
-__device__ __forceinline__ float unord_f32(uint32_t o)
-{
-    const uint32_t b = (o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o;
-    return __uint_as_float(b);
-}
 
 __global__ void __launch_bounds__(kSelWaves * 64)
 select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
@@ -226,7 +228,7 @@ select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
     DevResult *R = a.res;
     if (threadIdx.x == 0) { s_feas = 0; s_stat = 0; s_maxd = 0.0; }
     __syncthreads();
-    const double eJ = call_eJ(fc, omega);
+    const double eJ = bound_eJ(fc, omega);
     const int64_t n_cand = a.collect_mode ? 0 : a.kp;
     const int64_t n_work = (int64_t)min(R->n_work, (unsigned long long)a.work_cap);
     const int64_t n_coll = a.collect_mode ? (int64_t)min(R->n_collect, (unsigned long long)a.collect_cap) : 0;
@@ -253,8 +255,9 @@ select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
                     atomicMax((unsigned long long *)&s_maxd, (unsigned long long)__double_as_longlong(dj));
                 }
             } else if (e < n_cand + n_work) {
-                off = a.work[e - n_cand];
+                off = (uint32_t)(a.work[e - n_cand] & 0xFFFFFFFFull);
                 if (fl & 4u) my_feas++;
+                have = !(fl & kEntNoJ);
             } else {
                 off = a.collect[e - n_cand - n_work];
             }

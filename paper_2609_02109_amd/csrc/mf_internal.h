@@ -30,10 +30,13 @@ constexpr int kDefaultWorklist = 1 << 20; // certification list capacity (entrie
 //   g  [row][half][4]              aggregate columns of each option row in
 //                                  internal slot order (slot 0 = the VRAM
 //                                  slot); internal slot 2s+half at [half][s]
+//   c  [half][4]                   aggregate centre in the same order: layer 1
+//                                  takes a - c (exact on the 2^-14 grid) and
+//                                  P carries W1_agg c
 // ---------------------------------------------------------------------------
 struct FastLayout {
     int H, A, AP, MB, S1, PST;
-    int off_w1a, off_b2, off_w2, off_w3, off_b3, off_p, off_g;
+    int off_w1a, off_b2, off_w2, off_w3, off_b3, off_p, off_g, off_c;
     int total_floats;          // multiple of 4
 };
 
@@ -51,6 +54,7 @@ struct FastConst {
 // Counters and results the search kernels fill in device memory.
 struct DevResult {
     unsigned long long n_vram, n_feas_sure, n_work, n_collect;
+    unsigned long long n_full_J;    // certification entries that needed the full canonical J
     unsigned long long n_feas_cert, n_cand;
     unsigned int status;        // see kStat*
     int n_top;
@@ -67,6 +71,10 @@ constexpr unsigned kStatWorkOverflow = 4u;
 constexpr unsigned kStatCollectOverflow = 8u;
 constexpr unsigned kStatListFull = 16u;
 
+// Entry flags written by the canonical kernel (besides bit0 VRAM, bit1 all
+// latency bounds, bit2 feasible, bit 8+i model i misses its bound).
+constexpr unsigned kEntNoJ = 32u;   // feasible, but fast J proves it outside the top-k band
+
 // Kernel mode of the fast kernel.
 enum FastMode { kModeSearch = 0, kModeCollect = 1, kModeList = 2 };
 
@@ -81,7 +89,8 @@ struct FastArgs {
     const float *sla;           // device [N]
     const float *omega;         // device [N]
     DevResult *res;
-    uint32_t *work;             // certification list (range offsets)
+    unsigned long long *work;   // certification list: offset | (uncertain-model mask << 32)
+    float *work_J;              // fast J of each certification entry
     uint32_t work_cap;
     uint32_t *collect;          // fallback candidate list
     uint32_t collect_cap;
@@ -107,8 +116,11 @@ struct CanonArgs {
     const uint64_t *idx64;      // ... or absolute indices (list mode) when non-null
     // search mode entry sources: fast candidates (keys) then the work list then the collect list
     const unsigned long long *cand_keys; int n_cand_keys;
-    const uint32_t *work; const unsigned long long *n_work_ptr; uint32_t work_cap;
-    const uint32_t *collect; const unsigned long long *n_collect_ptr; uint32_t collect_cap;
+    const unsigned long long *work; const float *work_J; uint32_t work_cap;
+    const uint32_t *collect; uint32_t collect_cap;
+    DevResult *res;             // counters, eJ, collect threshold
+    int top_k;
+    int collect_mode;
     int64_t n_list;             // list mode entry count
     // outputs per entry
     double *ent_J;
@@ -120,7 +132,7 @@ struct CanonArgs {
 struct SelectArgs {
     int top_k, kp;
     const unsigned long long *cand_keys;   // [kp] fast candidates (0 = empty)
-    const uint32_t *work; const uint32_t *collect;
+    const unsigned long long *work; const uint32_t *collect;
     uint32_t work_cap, collect_cap;
     const double *ent_J;
     const uint32_t *ent_flags;
@@ -130,9 +142,9 @@ struct SelectArgs {
 };
 
 // launchers (return hipError_t of the launch)
-hipError_t launch_precompute_p(const float *features, const float *weights, int n_rows, int L,
-                               int A, int H, int64_t wstride, const int32_t *row_model,
-                               float *image_p, int pst, hipStream_t s);
+hipError_t launch_precompute_p(const float *features, const float *weights, const float *centre,
+                               int n_rows, int L, int A, int H, int64_t wstride,
+                               const int32_t *row_model, float *image_p, int pst, hipStream_t s);
 hipError_t launch_fast_impl(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode, hipStream_t s);
 int fast_kernel_supported(int n_models, int A, int H, int kp);
 hipError_t launch_merge_lists(const unsigned long long *lists, int n_lists, int kp,

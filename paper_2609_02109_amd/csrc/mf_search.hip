@@ -22,7 +22,7 @@
 //                workgroup at the end
 // Everything the kernel reads per configuration lives in LDS; the only HBM
 // traffic is the image load in the prologue and O(K') results.
-#include "mf_internal.h"
+#include "mf_device.h"
 
 namespace mfi {
 
@@ -86,16 +86,35 @@ __device__ __forceinline__ void list_offer(unsigned long long &slot, unsigned lo
 
 // Append flagged lanes' values to a device list; the counter keeps counting
 // past cap so the host can see an overflow.
-__device__ __forceinline__ void list_append(bool flag, uint32_t value, int lane, unsigned long long *count,
-                                            uint32_t *list, uint32_t cap)
+template <typename T>
+__device__ __forceinline__ unsigned long long list_reserve(bool flag, int lane, unsigned long long *count,
+                                                           unsigned long long &slot_out)
 {
     const unsigned long long m = __ballot(flag);
-    if (m == 0) return;
+    if (m == 0) return 0;
     unsigned long long base = 0;
     if (lane == 0) base = atomicAdd(count, (unsigned long long)__popcll(m));
     base = readlane64(base, 0);
-    const unsigned long long rank = __popcll(m & ((1ull << lane) - 1ull));
-    if (flag && base + rank < cap) list[base + rank] = value;
+    slot_out = base + (unsigned long long)__popcll(m & ((1ull << lane) - 1ull));
+    return m;
+}
+
+__device__ __forceinline__ void list_append(bool flag, uint32_t value, int lane, unsigned long long *count,
+                                            uint32_t *list, uint32_t cap)
+{
+    unsigned long long slot = 0;
+    if (list_reserve<uint32_t>(flag, lane, count, slot) && flag && slot < cap) list[slot] = value;
+}
+
+__device__ __forceinline__ void work_append(bool flag, unsigned long long entry, float fj, int lane,
+                                            unsigned long long *count, unsigned long long *list, float *list_J,
+                                            uint32_t cap)
+{
+    unsigned long long slot = 0;
+    if (list_reserve<unsigned long long>(flag, lane, count, slot) && flag && slot < cap) {
+        list[slot] = entry;
+        list_J[slot] = fj;
+    }
 }
 
 template <int MAXN, int A, int H>
@@ -127,9 +146,13 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             par_off[i] = fc.opt_off[i];
         }
     }
+    if (mode == kModeSearch && blockIdx.x == 0 && threadIdx.x == 0) args.res->eJ = bound_eJ(fc, args.omega);
     __syncthreads();
 
     const int lane = threadIdx.x & 63, half = lane >> 5, col = lane & 31;
+    // aggregate centre of the slots this lane feeds to layer 1
+    const float4 cen = *reinterpret_cast<const float4 *>(smem + Ly.off_c + 4 * half);
+    const float cen_s[4] = {cen.x, cen.y, cen.z, cen.w};
     const int wv = threadIdx.x >> 6;
     const int gw = blockIdx.x * kSearchWaves + wv;
     const uint64_t n = args.n;
@@ -206,7 +229,8 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
         const bool vram_ok = ah[0] <= fc.vram_cap;
 
         float J = 0.f;
-        bool anyfail = false, anyunc = false;
+        bool anyfail = false;
+        uint32_t umask = 0;   // models whose latency decision is left to the canonical pass
         for (int i = 0; i < N; i++) {
             const uint64_t sel = (uint64_t)0 - (uint64_t)(i >= 8);
             const uint64_t dw = dig0 ^ ((dig0 ^ dig1) & sel);
@@ -227,7 +251,7 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             const float *w1a = smem + Ly.off_w1a + i * (MB * S1 * 64) + lane;
 #pragma unroll
             for (int s = 0; s < S1; s++) {
-                const float bop = ah[s];
+                const float bop = ah[s] - cen_s[s];
 #pragma unroll
                 for (int mb = 0; mb < MB; mb++)
                     acc1[mb] = __builtin_amdgcn_mfma_f32_32x32x2f32(w1a[(mb * S1 + s) * 64], bop, acc1[mb], 0, 0, 0);
@@ -288,7 +312,7 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             const float lat = pl + b3[0], thr = pt + b3[1];
             const bool pass = lat <= par[i], fail = lat > par[16 + i];
             anyfail |= fail;
-            anyunc |= !(pass || fail);
+            umask |= (pass || fail) ? 0u : (1u << i);
             J = fmaf(par[32 + i], thr, J);
             if (args.pred && valid && half == 0) {
                 args.pred[(off * (uint64_t)N + (uint64_t)i) * 2u + 0u] = lat;
@@ -298,6 +322,7 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
 
         if (mode != kModeList) {
             const bool mine = valid && half == 0;
+            const bool anyunc = umask != 0u;
             const bool sla_sure = !anyfail && !anyunc;
             const bool feas_sure = mine && vram_ok && sla_sure;
             // a latency decision the bound cannot settle: re-evaluated
@@ -307,7 +332,8 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             if (mode == kModeSearch) {
                 c_vram += (mine && vram_ok) ? 1u : 0u;
                 c_feas += feas_sure ? 1u : 0u;
-                list_append(unc, (uint32_t)off, lane, &args.res->n_work, args.work, args.work_cap);
+                work_append(unc, (unsigned long long)(uint32_t)off | ((unsigned long long)umask << 32), J, lane,
+                            &args.res->n_work, args.work, args.work_J, args.work_cap);
                 const unsigned long long key = feas_sure
                     ? (((unsigned long long)ord_f32(J) << 32) | (unsigned long long)(0xFFFFFFFFu - (uint32_t)off))
                     : 0ull;
@@ -421,11 +447,13 @@ hipError_t launch_merge_lists(const unsigned long long *lists, int n_lists, int 
 
 namespace mfi {
 
-// Per-option first-layer precompute (the option's own columns, Eq. 6):
-// P[row][h] = b1[h] + sum_k W1[h][k] x[row][k] over the L local columns, as
+// Per-option first-layer precompute (the option's own columns, Eq. 6, plus
+// the aggregate centre c the fast path subtracts from the aggregate):
+// P[row][h] = b1[h] + sum_k W1[h][k] x[row][k] + sum_k W1_agg[h][k] c[k],
 // one fp64 fma chain, rounded to fp32.  Reads the canonical image (W1T[k][h]).
-__global__ void precompute_p_kernel(const float *features, const float *canon_w, int n_rows, int L, int A,
-                                    int H, int64_t wstride, const int32_t *row_model, float *image_p, int pst)
+__global__ void precompute_p_kernel(const float *features, const float *canon_w, const float *centre, int n_rows,
+                                    int L, int A, int H, int64_t wstride, const int32_t *row_model, float *image_p,
+                                    int pst)
 {
     const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (t >= (int64_t)n_rows * H) return;
@@ -435,17 +463,19 @@ __global__ void precompute_p_kernel(const float *features, const float *canon_w,
     const float *W1T = w, *b1 = w + (int64_t)nin * H;
     double c = (double)b1[h];
     for (int k = 0; k < L; k++) c = fma((double)W1T[(int64_t)k * H + h], (double)features[(int64_t)row * L + k], c);
+    for (int k = 0; k < A; k++) c = fma((double)W1T[(int64_t)(L + k) * H + h], (double)centre[k], c);
     image_p[(int64_t)row * pst + h] = (float)c;
 }
 
-hipError_t launch_precompute_p(const float *features, const float *weights, int n_rows, int L, int A, int H,
-                               int64_t wstride, const int32_t *row_model, float *image_p, int pst, hipStream_t s)
+hipError_t launch_precompute_p(const float *features, const float *weights, const float *centre, int n_rows, int L,
+                               int A, int H, int64_t wstride, const int32_t *row_model, float *image_p, int pst,
+                               hipStream_t s)
 {
     const int64_t total = (int64_t)n_rows * H;
     const int blk = 256;
     const int grid = (int)((total + blk - 1) / blk);
-    hipLaunchKernelGGL(precompute_p_kernel, dim3(grid), dim3(blk), 0, s, features, weights, n_rows, L, A, H, wstride,
-                       row_model, image_p, pst);
+    hipLaunchKernelGGL(precompute_p_kernel, dim3(grid), dim3(blk), 0, s, features, weights, centre, n_rows, L, A, H,
+                       wstride, row_model, image_p, pst);
     return hipGetLastError();
 }
 
