@@ -26,6 +26,19 @@ sys.path.insert(0, ROOT)
 
 PEAK_FP32_TFLOPS = 157.3
 CPU_SAMPLE = 1 << 22
+# HBM bytes per launch of the fast search kernel from rocprofv3 FETCH_SIZE /
+# WRITE_SIZE passes (profiles/fast_kernel_n6_k24_h64_hbm_counters.md), valid
+# only for the kernel source they were taken on
+TRAFFIC_BYTES = 1_702_912 + 27_242_304
+TRAFFIC_SOURCE_SHA = "6fee0f9891e0caa9"
+
+
+def measured_traffic():
+    import hashlib
+    src = os.path.join(ROOT, "paper_2609_02109_amd", "csrc", "mf_search.hip")
+    with open(src, "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()[:16]
+    return TRAFFIC_BYTES if sha == TRAFFIC_SOURCE_SHA else None
 
 
 def log(*a):
@@ -58,6 +71,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="run one plain device copy kernel of this many bytes read (and written) "
+                         "before the search: the calibration point for HBM byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (--gpus {args.gpus} requested): the search is "
@@ -79,6 +95,14 @@ def main():
     nbytes = ctypes.c_size_t()
     mf._check(mf.lib.mf_workspace_size(p.handle, ctypes.byref(sargs), ctypes.byref(nbytes)), "ws")
     ws = torch.empty(nbytes.value, dtype=torch.uint8, device=dev)
+
+    if args.copy_bytes:
+        src = torch.ones(args.copy_bytes // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     for _ in range(args.warmup):
         r = p.search_raw(sargs, ws)
@@ -121,8 +145,8 @@ def main():
                    "joint_configs": n, "ms_to_argmax": ms, "n_feas": int(r.n_feas),
                    "argmax": int(r.top_idx[0]), "n_flagged": int(r.n_flagged)},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_FP32_TFLOPS, "traffic": None,
-                     "kernel": "fast_kernel<16,6,64>", "kernel_ms": kms,
+                     "frac": achieved / PEAK_FP32_TFLOPS, "traffic": measured_traffic(),
+                     "kernel": "fast_kernel<8,6,64>", "kernel_ms": kms,
                      "flops_per_config": algorithmic_flops_per_config(inst)},
         "cpu_baseline": cpu,
     }
