@@ -74,11 +74,11 @@ def lib():
         L.orc_vram_feasible.argtypes = [P, P, C.c_uint64]
         L.orc_bf16_round.restype = C.c_double
         L.orc_bf16_round.argtypes = [C.c_double]
-        if hasattr(L, "orc_philox4x64"):
-            L.orc_philox4x64.argtypes = [P, P, P]
-        if hasattr(L, "orc_ga"):
-            L.orc_ga.restype = C.c_int
-            L.orc_ga.argtypes = [P, P, P, P, P, P, P]
+        L.orc_philox4x64.argtypes = [P, P, P]
+        L.orc_ga.restype = C.c_int
+        L.orc_ga.argtypes = [P, P, P, P, P, P, P, C.c_int]
+        L.orc_ga_next.restype = C.c_int
+        L.orc_ga_next.argtypes = [P, P, C.c_int, C.c_int, P, P, P, C.c_uint64, P]
         _lib = L
     return _lib
 
@@ -181,6 +181,65 @@ class Problem:
         buf = np.zeros(size, np.uint32)
         cnt = int(lib().orc_vram_feasible(self.ref, _ptr(buf), size))
         return buf[:cnt].copy()
+
+
+class GAParams(C.Structure):
+    _fields_ = [("n_scen", C.c_int32), ("pop", C.c_int32), ("gens", C.c_int32), ("tourn_k", C.c_int32),
+                ("p_cx", C.c_float), ("p_swap", C.c_float), ("p_mut", C.c_float), ("pad", C.c_float),
+                ("seed", C.c_uint64)]
+
+
+def ga_params(n_scen, pop, gens, tourn_k=3, p_cx=0.7, p_swap=0.5, p_mut=0.05, seed=0):
+    return GAParams(int(n_scen), int(pop), int(gens), int(tourn_k), float(p_cx), float(p_swap),
+                    float(p_mut), 0.0, int(seed))
+
+
+def _ga(self, sla, omega, pop=2048, gens=100, tourn_k=3, p_cx=0.7, p_swap=0.5, p_mut=0.05, seed=0,
+        threads=0, final_pop=False):
+    """GA replay (see mf_oracle_ga.c).  sla, omega: [S][N]."""
+    sla = np.ascontiguousarray(sla, np.float32)
+    om = np.ascontiguousarray(omega, np.float32)
+    S = int(sla.shape[0])
+    gp = ga_params(S, pop, gens, tourn_k, p_cx, p_swap, p_mut, seed)
+    bi = np.zeros(S, np.uint64)
+    bj = np.zeros(S, np.float64)
+    fp = np.zeros((S, pop), np.uint64) if final_pop else None
+    rc = lib().orc_ga(self.ref, C.byref(gp), _ptr(sla), _ptr(om), _ptr(bi), _ptr(bj),
+                      None if fp is None else _ptr(fp), int(threads))
+    if rc != 0:
+        raise ValueError("orc_ga rejected its arguments")
+    out = dict(best_idx=bi, best_J=bj)
+    if final_pop:
+        out["final_pop"] = fp
+    return out
+
+
+def _ga_next(self, s, g, pop_idx, fitness, feasible, pop, tourn_k=3, p_cx=0.7, p_swap=0.5, p_mut=0.05,
+             seed=0):
+    """One application of the GA operators (elitism, tournaments, crossover,
+    mutation, repair) to a population with given fitness."""
+    gp = ga_params(1, pop, 1, tourn_k, p_cx, p_swap, p_mut, seed)
+    idx = np.ascontiguousarray(pop_idx, np.uint64)
+    fit = np.ascontiguousarray(fitness, np.float64)
+    fl = np.ascontiguousarray(feasible, np.uint32)
+    out = np.zeros(pop, np.uint64)
+    rc = lib().orc_ga_next(self.ref, C.byref(gp), int(s), int(g), _ptr(idx), _ptr(fit), _ptr(fl),
+                           C.c_uint64(len(fl)), _ptr(out))
+    if rc != 0:
+        raise ValueError("orc_ga_next rejected its arguments")
+    return out
+
+
+Problem.ga = _ga
+Problem.ga_next = _ga_next
+
+
+def philox4x64(ctr, key):
+    c = np.ascontiguousarray(ctr, np.uint64)
+    k = np.ascontiguousarray(key, np.uint64)
+    o = np.zeros(4, np.uint64)
+    lib().orc_philox4x64(_ptr(c), _ptr(k), _ptr(o))
+    return [int(x) for x in o]
 
 
 def bf16_round(x: float) -> float:

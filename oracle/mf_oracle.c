@@ -40,29 +40,7 @@
 #include <string.h>
 #include <omp.h>
 
-#define ORC_MAX_MODELS 16
-#define ORC_MAX_TOPK 64
-#define ORC_MAX_AGG 16
-
-typedef struct {
-    int32_t n_models, n_local, n_agg, hidden1, hidden2, bf16;
-    const int32_t *n_options;   /* [N] */
-    const float *features;      /* [sum K][L] row-major, model i at offset sum_{j<i} K_j */
-    const int32_t *agg_cols;    /* [A] */
-    int32_t vram_slot;
-    float vram_cap;
-    const float *weights;       /* [N][stride]: W1[h1][L+A] b1[h1] W2[h2][h1] b2[h2] W3[2][h2] b3[2] */
-} orc_instance;
-
-typedef struct {
-    uint64_t n_eval, n_vram, n_feas;
-    uint64_t n_inexact_agg;     /* configs whose fp32 aggregate differs from fp64 (expected 0) */
-    uint64_t n_near[4];         /* (config, model) pairs with |lat - sla| <= {1e-5,1e-4,1e-3,2e-2} */
-    int32_t n_top;
-    int32_t pad;
-    uint64_t top_idx[ORC_MAX_TOPK];
-    double top_J[ORC_MAX_TOPK];
-} orc_result;
+#include "mf_oracle.h"
 
 /* ---------------------------------------------------------------- helpers */
 
@@ -159,7 +137,7 @@ static void mlp_forward(const double *w, int nin, int h1n, int h2n, int bf16,
     }
 }
 
-static double *weights_to_f64(const orc_instance *in)
+double *orc_weights_f64(const orc_instance *in)
 {
     int64_t n = stride_of(in) * in->n_models;
     double *w = (double *)malloc(sizeof(double) * (size_t)n);
@@ -171,7 +149,7 @@ static double *weights_to_f64(const orc_instance *in)
 /* Full evaluation of one joint configuration.
  * flags: bit0 VRAM ok, bit1 every latency bound met, bit2 feasible,
  *        bit3 aggregate exact; bit (8+i): model i misses its latency bound. */
-static void eval_one(const orc_instance *in, const double *w64, uint64_t idx,
+void orc_eval_w(const orc_instance *in, const double *w64, uint64_t idx,
                      const float *sla, const float *omega, double *lat, double *thr,
                      double *J, uint32_t *flags, double *scratch)
 {
@@ -208,7 +186,7 @@ static void eval_one(const orc_instance *in, const double *w64, uint64_t idx,
     *flags = f;
 }
 
-static size_t scratch_doubles(const orc_instance *in)
+size_t orc_scratch_doubles(const orc_instance *in)
 {
     return (size_t)(in->n_local + in->n_agg + in->hidden1 + in->hidden2);
 }
@@ -216,10 +194,10 @@ static size_t scratch_doubles(const orc_instance *in)
 int orc_eval(const orc_instance *in, uint64_t idx, const float *sla, const float *omega,
              double *lat, double *thr, double *J, uint32_t *flags)
 {
-    double *w64 = weights_to_f64(in);
-    double *scr = (double *)malloc(sizeof(double) * scratch_doubles(in));
+    double *w64 = orc_weights_f64(in);
+    double *scr = (double *)malloc(sizeof(double) * orc_scratch_doubles(in));
     if (!w64 || !scr) { free(w64); free(scr); return -1; }
-    eval_one(in, w64, idx, sla, omega, lat, thr, J, flags, scr);
+    orc_eval_w(in, w64, idx, sla, omega, lat, thr, J, flags, scr);
     free(w64);
     free(scr);
     return 0;
@@ -256,7 +234,7 @@ int orc_search(const orc_instance *in, uint64_t lo, uint64_t hi, const float *sl
     if (N < 1 || N > ORC_MAX_MODELS || in->n_agg > ORC_MAX_AGG || k < 1 || k > ORC_MAX_TOPK ||
         size == 0 || lo > hi || hi > size)
         return -1;
-    double *w64 = weights_to_f64(in);
+    double *w64 = orc_weights_f64(in);
     if (!w64) return -1;
     memset(out, 0, sizeof(*out));
     const double bands[4] = {1e-5, 1e-4, 1e-3, 2e-2};
@@ -273,13 +251,13 @@ int orc_search(const orc_instance *in, uint64_t lo, uint64_t hi, const float *sl
         int tcnt = 0;
         uint64_t lv = 0, lf = 0, lx = 0, ln[4] = {0, 0, 0, 0};
         double lat[ORC_MAX_MODELS], thr[ORC_MAX_MODELS];
-        double *scr = (double *)malloc(sizeof(double) * scratch_doubles(in));
+        double *scr = (double *)malloc(sizeof(double) * orc_scratch_doubles(in));
 #pragma omp for schedule(static)
         for (int64_t t = 0; t < n; t++) {
             uint64_t idx = lo + (uint64_t)t;
             double J;
             uint32_t f;
-            eval_one(in, w64, idx, sla, omega, lat, thr, &J, &f, scr);
+            orc_eval_w(in, w64, idx, sla, omega, lat, thr, &J, &f, scr);
             lv += f & 1u;
             lf += (f >> 2) & 1u;
             lx += ((f >> 3) & 1u) ^ 1u;
@@ -327,15 +305,15 @@ int orc_eval_list(const orc_instance *in, const uint64_t *idx, int64_t n, const 
                   uint32_t *flags)
 {
     const int N = in->n_models;
-    double *w64 = weights_to_f64(in);
+    double *w64 = orc_weights_f64(in);
     if (!w64) return -1;
     if (nthreads < 1) nthreads = omp_get_max_threads();
 #pragma omp parallel num_threads(nthreads)
     {
-        double *scr = (double *)malloc(sizeof(double) * scratch_doubles(in));
+        double *scr = (double *)malloc(sizeof(double) * orc_scratch_doubles(in));
 #pragma omp for schedule(static)
         for (int64_t t = 0; t < n; t++)
-            eval_one(in, w64, idx[t], sla, omega, lat + t * N, thr + t * N, J + t, flags + t, scr);
+            orc_eval_w(in, w64, idx[t], sla, omega, lat + t * N, thr + t * N, J + t, flags + t, scr);
         free(scr);
     }
     free(w64);

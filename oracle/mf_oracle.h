@@ -1,0 +1,42 @@
+/* Types shared by the CPU oracle's C files (test infrastructure only). */
+#ifndef MF_ORACLE_H
+#define MF_ORACLE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#define ORC_MAX_MODELS 16
+#define ORC_MAX_TOPK 64
+#define ORC_MAX_AGG 16
+
+typedef struct {
+    int32_t n_models, n_local, n_agg, hidden1, hidden2, bf16;
+    const int32_t *n_options;   /* [N] */
+    const float *features;      /* [sum K][L] row-major, model i at offset sum_{j<i} K_j */
+    const int32_t *agg_cols;    /* [A] */
+    int32_t vram_slot;
+    float vram_cap;
+    const float *weights;       /* [N][stride]: W1[h1][L+A] b1[h1] W2[h2][h1] b2[h2] W3[2][h2] b3[2] */
+} orc_instance;
+
+typedef struct {
+    uint64_t n_eval, n_vram, n_feas;
+    uint64_t n_inexact_agg;     /* configs whose fp32 aggregate differs from fp64 (expected 0) */
+    uint64_t n_near[4];         /* (config, model) pairs with |lat - sla| <= {1e-5,1e-4,1e-3,2e-2} */
+    int32_t n_top;
+    int32_t pad;
+    uint64_t top_idx[ORC_MAX_TOPK];
+    double top_J[ORC_MAX_TOPK];
+} orc_result;
+
+uint64_t orc_space_size(const orc_instance *in);
+void orc_decode(const orc_instance *in, uint64_t idx, int32_t *digits);
+uint64_t orc_encode(const orc_instance *in, const int32_t *digits);
+int orc_aggregate(const orc_instance *in, const int32_t *digits, float *a);
+double *orc_weights_f64(const orc_instance *in);
+size_t orc_scratch_doubles(const orc_instance *in);
+void orc_eval_w(const orc_instance *in, const double *w64, uint64_t idx, const float *sla, const float *omega,
+                double *lat, double *thr, double *J, uint32_t *flags, double *scratch);
+uint64_t orc_vram_feasible(const orc_instance *in, uint32_t *list, uint64_t cap);
+
+#endif
