@@ -31,6 +31,7 @@ struct mf_problem {
     void *d_mem = nullptr;
     float4 *d_image = nullptr;
     float *d_canon = nullptr, *d_features = nullptr, *d_zeros = nullptr, *d_centre = nullptr;
+    double *d_w64 = nullptr;     // packed weights as fp64 (GA fitness)
     std::vector<float> centre;   // aggregate centre per slot (original slot order)
     int32_t *d_agg_cols = nullptr, *d_row_model = nullptr;
     FastLayout lay{};
@@ -624,6 +625,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     const size_t o_rm = off; off = align256(off + (size_t)sumK * 4);
     const size_t o_z = off; off = align256(off + 64 * 4);
     const size_t o_c = off; off = align256(off + (size_t)A * 4);
+    const size_t o_w64 = off; off = align256(off + W.size() * 8);
     if (hipMalloc(&p->d_mem, off) != hipSuccess) { delete p; return MF_ENOMEM; }
     char *base = (char *)p->d_mem;
     p->d_image = reinterpret_cast<float4 *>(base + o_img);
@@ -633,6 +635,8 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     p->d_row_model = reinterpret_cast<int32_t *>(base + o_rm);
     p->d_zeros = reinterpret_cast<float *>(base + o_z);
     p->d_centre = reinterpret_cast<float *>(base + o_c);
+    p->d_w64 = reinterpret_cast<double *>(base + o_w64);
+    std::vector<double> w64(W.begin(), W.end());
     bool ok = true;
     ok = ok && hipMemsetAsync(p->d_zeros, 0, 64 * 4, s) == hipSuccess;
     if (!img.empty()) ok = ok && hipMemcpyAsync(p->d_image, img.data(), img.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
@@ -641,6 +645,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     ok = ok && hipMemcpyAsync(p->d_agg_cols, p->agg_cols.data(), (size_t)A * 4, hipMemcpyHostToDevice, s) == hipSuccess;
     ok = ok && hipMemcpyAsync(p->d_row_model, row_model.data(), (size_t)sumK * 4, hipMemcpyHostToDevice, s) == hipSuccess;
     ok = ok && hipMemcpyAsync(p->d_centre, p->centre.data(), (size_t)A * 4, hipMemcpyHostToDevice, s) == hipSuccess;
+    ok = ok && hipMemcpyAsync(p->d_w64, w64.data(), w64.size() * 8, hipMemcpyHostToDevice, s) == hipSuccess;
     if (ok && p->fast_ok)
         ok = launch_precompute_p(p->d_features, p->d_canon, p->d_centre, sumK, L, A, H, p->wstride, p->d_row_model,
                                  reinterpret_cast<float *>(p->d_image) + ly.off_p, ly.PST, s) == hipSuccess;
@@ -760,18 +765,107 @@ mf_status mf_eval_canonical(mf_problem *p, const uint64_t *d_idx, int64_t n, con
     return hip_status(launch_canonical(ca, (int)std::min<int64_t>(n, 1 << 20), false, (hipStream_t)stream));
 }
 
+static mf_status check_ga_args(const mf_problem *p, const mf_ga_args *a)
+{
+    if (!p || !a) return MF_EINVAL;
+    if (a->n_scen < 1 || a->pop < 4 || a->pop > 4096 || (a->pop & 1) || a->gens < 0 || a->tourn_k < 1 ||
+        a->tourn_k > 8 || !a->d_sla || !a->d_omega)
+        return MF_EINVAL;
+    for (float q : {a->p_cx, a->p_swap, a->p_mut})
+        if (!std::isfinite(q)) return MF_EINVAL;
+    if (p->space > (1ull << 32)) return MF_EUNSUPPORTED;
+    if (!ga_fitness_supported(p->L + p->A, p->H1, p->H2)) return MF_EUNSUPPORTED;
+    return MF_OK;
+}
+
+struct GaWs {
+    size_t cnt, off, nfl, fl, popA, popB, fit, bJ, bI, total;
+};
+
+static GaWs ga_ws(const mf_problem *p, const mf_ga_args *a)
+{
+    GaWs w{};
+    const uint64_t n_blk = (p->space + 255) / 256;
+    const size_t sp = (size_t)a->n_scen * a->pop;
+    size_t o = 0;
+    w.cnt = o; o = align256(o + n_blk * 4);
+    w.off = o; o = align256(o + n_blk * 8);
+    w.nfl = o; o = align256(o + 8);
+    w.fl = o; o = align256(o + p->space * 4);
+    w.popA = o; o = align256(o + sp * 8);
+    w.popB = o; o = align256(o + sp * 8);
+    w.fit = o; o = align256(o + sp * 8);
+    w.bJ = o; o = align256(o + (size_t)a->n_scen * 8);
+    w.bI = o; o = align256(o + (size_t)a->n_scen * 8);
+    w.total = o;
+    return w;
+}
+
 mf_status mf_ga_workspace_size(const mf_problem *p, const mf_ga_args *args, size_t *bytes)
 {
-    if (!p || !args || !bytes) return MF_EINVAL;
-    return MF_EUNSUPPORTED;
+    if (!bytes) return MF_EINVAL;
+    mf_status st = check_ga_args(p, args);
+    if (st != MF_OK) return st;
+    *bytes = ga_ws(p, args).total;
+    return MF_OK;
 }
 
 mf_status mf_ga_run(mf_problem *p, const mf_ga_args *args, void *d_ws, size_t ws_bytes, void *stream,
                     uint64_t *h_best_idx, double *h_best_J, uint64_t *d_final_pop)
 {
-    (void)d_ws; (void)ws_bytes; (void)stream; (void)d_final_pop;
-    if (!p || !args || !h_best_idx || !h_best_J) return MF_EINVAL;
-    return MF_EUNSUPPORTED;
+    if (!h_best_idx || !h_best_J || !d_ws) return MF_EINVAL;
+    mf_status st = check_ga_args(p, args);
+    if (st != MF_OK) return st;
+    const GaWs w = ga_ws(p, args);
+    if (ws_bytes < w.total) return MF_ENOMEM;
+    if (((uintptr_t)d_ws & 255u) != 0) return MF_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    char *ws = (char *)d_ws;
+    uint32_t *cnt = reinterpret_cast<uint32_t *>(ws + w.cnt);
+    uint64_t *blk_off = reinterpret_cast<uint64_t *>(ws + w.off);
+    unsigned long long *n_fl = reinterpret_cast<unsigned long long *>(ws + w.nfl);
+    uint32_t *fl = reinterpret_cast<uint32_t *>(ws + w.fl);
+    uint64_t *pa = reinterpret_cast<uint64_t *>(ws + w.popA), *pb = reinterpret_cast<uint64_t *>(ws + w.popB);
+    double *fit = reinterpret_cast<double *>(ws + w.fit);
+    double *bJ = reinterpret_cast<double *>(ws + w.bJ);
+    uint64_t *bI = reinterpret_cast<uint64_t *>(ws + w.bI);
+
+    GAConst c{};
+    c.N = p->N; c.L = p->L; c.A = p->A; c.H1 = p->H1; c.H2 = p->H2; c.bf16 = p->bf16;
+    for (int i = 0; i < p->N; i++) { c.K[i] = p->K[i]; c.opt_off[i] = p->opt_off[i]; }
+    c.vram_col = p->agg_cols[p->vram_slot];
+    c.vram_slot = p->vram_slot;
+    c.vram_cap = p->vram_cap;
+    c.space = p->space;
+    c.features = p->d_features;
+    c.agg_cols = p->d_agg_cols;
+    c.w64 = p->d_w64;
+    c.wstride = p->wstride;
+
+    const int S = args->n_scen, P = args->pop;
+    MF_HIP(launch_ga_feasible(c, cnt, blk_off, n_fl, fl, s));
+    unsigned long long h_nfl = 0;
+    MF_HIP(hipMemcpyAsync(&h_nfl, n_fl, 8, hipMemcpyDeviceToHost, s));
+    MF_HIP(hipStreamSynchronize(s));
+    if (h_nfl == 0) {
+        for (int q = 0; q < S; q++) { h_best_idx[q] = UINT64_MAX; h_best_J[q] = -INFINITY; }
+        if (d_final_pop) {
+            MF_HIP(hipMemsetAsync(d_final_pop, 0xFF, (size_t)S * P * 8, s));
+            MF_HIP(hipStreamSynchronize(s));
+        }
+        return MF_OK;
+    }
+    MF_HIP(launch_ga_init(args->seed, S, P, fl, n_fl, pa, bJ, bI, s));
+    for (int g = 0; g <= args->gens; g++) {
+        MF_HIP(launch_ga_fitness(c, S, P, pa, args->d_sla, args->d_omega, fit, s));
+        MF_HIP(launch_ga_ops(c, args->seed, S, P, g, args->gens, args->tourn_k, args->p_cx, args->p_swap,
+                             args->p_mut, fl, n_fl, pa, fit, pb, bJ, bI, d_final_pop, s));
+        std::swap(pa, pb);
+    }
+    MF_HIP(hipMemcpyAsync(h_best_J, bJ, (size_t)S * 8, hipMemcpyDeviceToHost, s));
+    MF_HIP(hipMemcpyAsync(h_best_idx, bI, (size_t)S * 8, hipMemcpyDeviceToHost, s));
+    MF_HIP(hipStreamSynchronize(s));
+    return MF_OK;
 }
 
 }  // extern "C"

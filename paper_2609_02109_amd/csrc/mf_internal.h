@@ -141,6 +141,21 @@ struct SelectArgs {
     DevResult *res;
 };
 
+// GA problem constants (kernel-argument block).
+struct GAConst {
+    int N, L, A, H1, H2, bf16;
+    int32_t K[kMaxN];
+    int32_t opt_off[kMaxN];
+    int vram_col;               // option column of the VRAM aggregate slot
+    int vram_slot;
+    float vram_cap;
+    uint64_t space;
+    const float *features;      // [sumK][L]
+    const int32_t *agg_cols;    // [A]
+    const double *w64;          // [N][stride] packed weights (W1 b1 W2 b2 W3 b3) as fp64
+    int64_t wstride;
+};
+
 // launchers (return hipError_t of the launch)
 hipError_t launch_precompute_p(const float *features, const float *weights, const float *centre,
                                int n_rows, int L, int A, int H, int64_t wstride,
@@ -151,5 +166,16 @@ hipError_t launch_merge_lists(const unsigned long long *lists, int n_lists, int 
                               unsigned long long *out, hipStream_t s);
 hipError_t launch_canonical(const CanonArgs &a, int n_entries_max, bool search_mode, hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, const FastConst &fc, const float *omega, hipStream_t s);
+int ga_fitness_supported(int nin, int h1, int h2);
+hipError_t launch_ga_feasible(const GAConst &c, uint32_t *blk_count, uint64_t *blk_off, unsigned long long *n_fl,
+                              uint32_t *fl, hipStream_t st);
+hipError_t launch_ga_init(uint64_t seed, int S, int P, const uint32_t *fl, const unsigned long long *n_fl,
+                          uint64_t *pop, double *best_J, uint64_t *best_idx, hipStream_t st);
+hipError_t launch_ga_fitness(const GAConst &c, int S, int P, const uint64_t *pop, const float *sla,
+                             const float *omega, double *fit, hipStream_t st);
+hipError_t launch_ga_ops(const GAConst &c, uint64_t seed, int S, int P, int gen, int gens, int tk, float p_cx,
+                         float p_swap, float p_mut, const uint32_t *fl, const unsigned long long *n_fl,
+                         const uint64_t *pop, const double *fit, uint64_t *next, double *best_J,
+                         uint64_t *best_idx, uint64_t *final_pop, hipStream_t st);
 
 }  // namespace mfi

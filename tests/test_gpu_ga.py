@@ -1,0 +1,81 @@
+"""GPU GA (mf_ga_run) against the oracle's GA replay.
+
+Fitness is the canonical J on both sides and every random draw comes from the
+same counter-based Philox stream, so the whole trajectory is reproduced: the
+best individual per scenario and the final population must be identical.
+"""
+import numpy as np
+import pytest
+
+from paper_2609_02109_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def mf():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_02109_amd import mf as mfmod
+    return mfmod
+
+
+def run_both(mf, orc, inst, sla, omega, **kw):
+    print(f"[ga] {inst.name} S={len(sla)} {kw}", flush=True)
+    g = mf.Problem(inst).ga(sla, omega, final_pop=True, **kw)
+    r = orc.Problem(inst).ga(sla, omega, final_pop=True, **kw)
+    np.testing.assert_array_equal(g["best_idx"], r["best_idx"])
+    assert g["best_J"].tobytes() == r["best_J"].tobytes()
+    np.testing.assert_array_equal(g["final_pop"].cpu().numpy().astype(np.uint64), r["final_pop"])
+    return g, r
+
+
+def test_ga_n5_subset_full_length(mf, orc):
+    inst, sc, gp = synth.cfg3(0)
+    run_both(mf, orc, inst, sc.sla[:8], sc.omega[:8], pop=gp.pop, gens=gp.gens, tourn_k=gp.tourn_k,
+             p_cx=gp.p_cx, p_swap=gp.p_swap, p_mut=gp.p_mut, seed=gp.seed)
+
+
+def test_ga_n5_all_scenarios(mf, orc):
+    inst, sc, gp = synth.cfg3(1)
+    g, r = run_both(mf, orc, inst, sc.sla, sc.omega, pop=gp.pop, gens=gp.gens, seed=gp.seed)
+    # the GA never beats the exhaustive optimum of its scenario
+    p = mf.Problem(inst)
+    for s in range(0, 64, 9):
+        ex = p.search(sc.sla[s], sc.omega[s], k=1)
+        assert g["best_J"][s] <= ex["top_J"][0]
+
+
+@pytest.mark.parametrize("kw", [dict(pop=64, gens=7, tourn_k=1, p_cx=1.0, p_mut=0.3),
+                                dict(pop=130, gens=3, tourn_k=8, p_cx=0.0, p_mut=0.0),
+                                dict(pop=4, gens=2, tourn_k=2)])
+def test_ga_operator_settings(mf, orc, kw):
+    inst, sc, _ = synth.cfg3(2)
+    run_both(mf, orc, inst, sc.sla[:3], sc.omega[:3], seed=5, **kw)
+
+
+def test_ga_small_space_and_wide_model(mf, orc):
+    inst = synth.cfg0(2)
+    sc = synth.ga_scenarios(2, 5, seed=2)
+    run_both(mf, orc, inst, sc.sla, sc.omega, pop=32, gens=10, seed=9)
+    inst2 = synth.make_instance([6, 5, 4], 16, 6, 64, 64, seed=3, vram_quantile=0.5)
+    sc2 = synth.ga_scenarios(3, 4, seed=4)
+    run_both(mf, orc, inst2, sc2.sla, sc2.omega, pop=96, gens=6, seed=1)
+
+
+def test_ga_no_feasible_configuration(mf, orc):
+    inst = synth.cfg1(0)
+    inst.vram_cap = 1.0
+    sc = synth.ga_scenarios(5, 3, seed=0)
+    g = mf.Problem(inst).ga(sc.sla, sc.omega, pop=16, gens=2, final_pop=True)
+    assert np.all(g["best_idx"] == np.uint64(2 ** 64 - 1)) and np.all(np.isneginf(g["best_J"]))
+
+
+def test_ga_rejects_bad_arguments(mf):
+    inst, sc, _ = synth.cfg3(0)
+    p = mf.Problem(inst)
+    for kw in [dict(pop=7), dict(pop=2), dict(tourn_k=0), dict(tourn_k=9), dict(gens=-1)]:
+        with pytest.raises(mf.MfError) as e:
+            p.ga(sc.sla[:2], sc.omega[:2], **kw)
+        assert e.value.status == mf.MF_EINVAL
