@@ -64,6 +64,57 @@ def cpu_baseline(inst, threads):
                       f"fp64 brute force, {dt:.2f} s"}
 
 
+def measure_search(mf, torch, inst, k, steps, warmup):
+    import ctypes
+    import numpy as np
+    n = inst.space_size
+    p = mf.Problem(inst)
+    dev = p.device
+    d_sla = torch.as_tensor(inst.sla, device=dev)
+    d_om = torch.as_tensor(inst.omega, device=dev)
+    sargs = mf.SearchArgs(0, n, k, 0, d_sla.data_ptr(), d_om.data_ptr(), None, None)
+    nbytes = ctypes.c_size_t()
+    mf._check(mf.lib.mf_workspace_size(p.handle, ctypes.byref(sargs), ctypes.byref(nbytes)), "ws")
+    ws = torch.empty(nbytes.value, dtype=torch.uint8, device=dev)
+    for _ in range(warmup):
+        r = p.search_raw(sargs, ws)
+    torch.cuda.synchronize()
+    kernel_ms = []
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        r = p.search_raw(sargs, ws)
+        kernel_ms.append(r.main_kernel_ms)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    return (t1 - t0) * 1e3 / steps, float(np.mean(kernel_ms)), r
+
+
+def bench_ga(args):
+    import torch
+    from paper_2609_02109_amd import mf, synth
+    inst, sc, gp = synth.cfg3(args.seed)
+    p = mf.Problem(inst)
+    run = lambda: p.ga(sc.sla, sc.omega, pop=gp.pop, gens=gp.gens, tourn_k=gp.tourn_k, p_cx=gp.p_cx,
+                       p_swap=gp.p_swap, p_mut=gp.p_mut, seed=gp.seed)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        r = run()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    evals = gp.n_scen * gp.pop * (gp.gens + 1)
+    line = {"metric": "GA fitness evaluations/sec (64 scenarios, population 2048, 100 generations, N=5)",
+            "value": evals / (ms * 1e-3), "unit": "evaluations/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "f64", "data": "synthetic (seeded generator, seed %d)" % args.seed,
+            "config": {"workload": "GA on the N=5 instance (12,12,9,9,9 options): 64 scenarios x 2048 x "
+                                   "(100+1) generations, tournament 3, crossover 0.7, mutation 0.05",
+                       "ms_per_ga_run": ms, "best_J_mean": float(r["best_J"].mean())}}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -71,6 +122,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--workload", choices=["n6", "ga"], default="n6",
+                    help="n6: the N=6 exhaustive search (the benchmark step); ga: the N=5 GA scheduler")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="run one plain device copy kernel of this many bytes read (and written) "
                          "before the search: the calibration point for HBM byte counters")
@@ -80,44 +133,26 @@ def main():
               "single-GPU; multi-GPU sharding is a design note, not a measured path", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
     from paper_2609_02109_amd import mf, synth
-
-    inst = synth.cfg2(args.seed)
-    n = inst.space_size
-    p = mf.Problem(inst)
-    dev = p.device
-    d_sla = torch.as_tensor(inst.sla, device=dev)
-    d_om = torch.as_tensor(inst.omega, device=dev)
-    sargs = mf.SearchArgs(0, n, 1, 0, d_sla.data_ptr(), d_om.data_ptr(), None, None)
-    import ctypes
-    nbytes = ctypes.c_size_t()
-    mf._check(mf.lib.mf_workspace_size(p.handle, ctypes.byref(sargs), ctypes.byref(nbytes)), "ws")
-    ws = torch.empty(nbytes.value, dtype=torch.uint8, device=dev)
+    if args.workload == "ga":
+        return bench_ga(args)
 
     if args.copy_bytes:
-        src = torch.ones(args.copy_bytes // 4, dtype=torch.float32, device=dev)
+        src = torch.ones(args.copy_bytes // 4, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
         torch.neg(src, out=dst)
         torch.cuda.synchronize()
         del src, dst
 
-    for _ in range(args.warmup):
-        r = p.search_raw(sargs, ws)
-    torch.cuda.synchronize()
-    kernel_ms = []
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        r = p.search_raw(sargs, ws)
-        kernel_ms.append(r.main_kernel_ms)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms = (t1 - t0) * 1e3 / args.steps
-    kms = float(np.mean(kernel_ms))
+    inst = synth.cfg2(args.seed)
+    n = inst.space_size
+    ms, kms, r = measure_search(mf, torch, inst, 1, args.steps, args.warmup)
     flops = algorithmic_flops_per_config(inst) * n
     achieved = flops / (kms * 1e-3) / 1e12
+    inst5 = synth.cfg1(args.seed)
+    ms5, kms5, r5 = measure_search(mf, torch, inst5, 16, max(args.steps, 20), max(args.warmup, 3))
     log(f"search: {ms:.2f} ms/step, fast kernel {kms:.2f} ms, n_feas={r.n_feas} "
         f"n_flagged={r.n_flagged} argmax={r.top_idx[0]} J={r.top_J[0]!r}")
 
@@ -143,7 +178,11 @@ def main():
         "config": {"workload": "N=6 models x 24 options (191,102,976 joint configs), "
                                "22-64-64-2 fp32 surrogate per model, VRAM cap 200 GB, argmax + feasible count",
                    "joint_configs": n, "ms_to_argmax": ms, "n_feas": int(r.n_feas),
-                   "argmax": int(r.top_idx[0]), "n_flagged": int(r.n_flagged)},
+                   "argmax": int(r.top_idx[0]), "n_flagged": int(r.n_flagged),
+                   "n5": {"workload": "N=5 models, options 12,12,9,9,9 (104,976 joint configs), 12-32-32-2 fp32, "
+                                      "top-16 + counts", "ms_to_argmax": ms5,
+                          "joint_configs_per_s": inst5.space_size / (ms5 * 1e-3), "fast_kernel_ms": kms5,
+                          "n_feas": int(r5.n_feas), "argmax": int(r5.top_idx[0])}},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_FP32_TFLOPS, "traffic": measured_traffic(),
                      "kernel": "fast_kernel<8,6,64>", "kernel_ms": kms,
