@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <cstdlib>
 #include <cstring>
 #include <limits>
 #include <new>
@@ -195,20 +196,26 @@ void stride_digits(const mf_problem &p, uint64_t stride, uint32_t *out)
 struct WsLayout {
     size_t res, work, workJ, collect, lists, cand, entJ, entF, total;
     uint32_t work_cap, collect_cap;
-    int kp, grid;
+    int kp, grid, waves;
 };
 
 WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k)
 {
     WsLayout w{};
     w.kp = choose_kp(top_k);
+    w.waves = fast_waves_for(p.N, p.lay, w.kp);
     const uint64_t tiles = (n + 31) / 32;
-    uint64_t g = (tiles + kSearchWaves - 1) / kSearchWaves;
+    uint64_t g = (tiles + w.waves - 1) / w.waves;
     w.grid = (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)p.num_cus));
     // certification list: 1/128 of the range, at least 2^20 entries (never
     // more than the range), at most 2^26
     const uint64_t want = std::min<uint64_t>(std::max<uint64_t>(n / 128, (uint64_t)kDefaultWorklist), 1ull << 26);
-    const uint64_t cap = std::max<uint64_t>(std::min<uint64_t>(want, n), 1024);
+    uint64_t cap = std::max<uint64_t>(std::min<uint64_t>(want, n), 1024);
+    // MF_WORKLIST_CAP shrinks the certification list (tests of the range-split path)
+    if (const char *env = std::getenv("MF_WORKLIST_CAP")) {
+        const long long v = std::atoll(env);
+        if (v >= 1) cap = std::min<uint64_t>(cap, (uint64_t)v);
+    }
     w.work_cap = (uint32_t)cap;
     w.collect_cap = (uint32_t)std::max<uint64_t>(std::min<uint64_t>((uint64_t)kDefaultWorklist, n), 1024);
     size_t o = 0;
@@ -290,7 +297,8 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     fa.lay = p->lay;
     fa.lo = lo;
     fa.n = n;
-    fa.total_waves = w.grid * kSearchWaves;
+    fa.total_waves = w.grid * w.waves;
+    fa.waves = w.waves;
     stride_digits(*p, (uint64_t)fa.total_waves * 32u, fa.stride_digits);
     fa.sla = args->d_sla;
     fa.omega = args->d_omega;
@@ -737,9 +745,10 @@ mf_status mf_eval_fast(mf_problem *p, const uint64_t *d_idx, int64_t n, float *d
     fa.n = (uint64_t)n;
     fa.idx_list = d_idx;
     const uint64_t tiles = ((uint64_t)n + 31) / 32;
-    const int grid = (int)std::max<uint64_t>(1, std::min<uint64_t>((tiles + kSearchWaves - 1) / kSearchWaves,
+    fa.waves = fast_waves_for(p->N, p->lay, 16);
+    const int grid = (int)std::max<uint64_t>(1, std::min<uint64_t>((tiles + fa.waves - 1) / fa.waves,
                                                                     (uint64_t)p->num_cus));
-    fa.total_waves = grid * kSearchWaves;
+    fa.total_waves = grid * fa.waves;
     fa.sla = p->d_zeros;
     fa.omega = p->d_zeros;
     fa.pred = d_pred;

@@ -11,7 +11,8 @@
 namespace mfi {
 
 constexpr int kMaxN = MF_MAX_MODELS;
-constexpr int kSearchWaves = 8;          // waves per workgroup of the fast search kernel
+constexpr int kSearchWaves = 8;          // waves per workgroup of the fast search kernel (base)
+constexpr int kSearchWavesWide = 16;     // ... when registers and LDS allow 4 waves per SIMD
 constexpr int kCertWaves = 4;            // waves per workgroup of the canonical kernels
 constexpr int kDefaultWorklist = 1 << 20; // certification list capacity (entries)
 
@@ -86,6 +87,7 @@ struct FastArgs {
     const uint64_t *idx_list;   // list mode only
     uint32_t stride_digits[kMaxN]; // mixed-radix digits of (total waves * 32) mod |Lambda|
     int total_waves;
+    int waves;                  // waves per workgroup (kSearchWaves or kSearchWavesWide)
     const float *sla;           // device [N]
     const float *omega;         // device [N]
     DevResult *res;
@@ -161,6 +163,7 @@ hipError_t launch_precompute_p(const float *features, const float *weights, cons
                                int n_rows, int L, int A, int H, int64_t wstride,
                                const int32_t *row_model, float *image_p, int pst, hipStream_t s);
 hipError_t launch_fast_impl(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode, hipStream_t s);
+int fast_waves_for(int n_models, const FastLayout &lay, int kp);
 int fast_kernel_supported(int n_models, int A, int H, int kp);
 hipError_t launch_merge_lists(const unsigned long long *lists, int n_lists, int kp,
                               unsigned long long *out, hipStream_t s);

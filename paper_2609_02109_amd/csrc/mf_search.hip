@@ -117,8 +117,8 @@ __device__ __forceinline__ void work_append(bool flag, unsigned long long entry,
     }
 }
 
-template <int MAXN, int A, int H>
-__global__ void __launch_bounds__(kSearchWaves * 64, 1)
+template <int MAXN, int A, int H, int WAVES>
+__global__ void __launch_bounds__(WAVES * 64, 1)
 fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int kp)
 {
     constexpr int MB = H / 32;         // 32-row blocks of a hidden layer
@@ -154,7 +154,7 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
     const float4 cen = *reinterpret_cast<const float4 *>(smem + Ly.off_c + 4 * half);
     const float cen_s[4] = {cen.x, cen.y, cen.z, cen.w};
     const int wv = threadIdx.x >> 6;
-    const int gw = blockIdx.x * kSearchWaves + wv;
+    const int gw = blockIdx.x * WAVES + wv;
     const uint64_t n = args.n;
     const uint64_t n_tiles = (n + 31) >> 5;
     const float theta = (float)args.theta;
@@ -370,7 +370,7 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
         if (lane < kp) lst[wv * kp + lane] = slot;
         __syncthreads();
         if (wv == 0) {
-            for (int w = 1; w < kSearchWaves; w++) {
+            for (int w = 1; w < WAVES; w++) {
                 const unsigned long long k2 = lane < kp ? lst[w * kp + lane] : 0ull;
                 list_offer(slot, k2, lane, kp, thr_key);
             }
@@ -403,15 +403,15 @@ merge_lists_kernel(const unsigned long long *lists, int n_keys, int kp, unsigned
     }
 }
 
-template <int MAXN, int A, int H>
+template <int MAXN, int A, int H, int WAVES>
 static hipError_t launch_fast_t(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode,
                                 hipStream_t s)
 {
-    const size_t lds = (size_t)a.lay.total_floats * 4 + 64 * 4 + (size_t)kSearchWaves * kp * 8;
-    auto fn = fast_kernel<MAXN, A, H>;
+    const size_t lds = (size_t)a.lay.total_floats * 4 + 64 * 4 + (size_t)WAVES * kp * 8;
+    auto fn = fast_kernel<MAXN, A, H, WAVES>;
     hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(fn, dim3(grid), dim3(kSearchWaves * 64), lds, s, a, fc, mode, kp);
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(WAVES * 64), lds, s, a, fc, mode, kp);
     return hipGetLastError();
 }
 
@@ -424,13 +424,29 @@ int fast_kernel_supported(int n_models, int A, int H, int kp)
     return 1;
 }
 
+// 16 waves per workgroup (4 per SIMD) when the per-wave registers fit 128
+// VGPRs (up to 8 models) and the image plus 16 candidate lists fit in LDS.
+int fast_waves_for(int n_models, const FastLayout &lay, int kp)
+{
+    const size_t lds = (size_t)lay.total_floats * 4 + 64 * 4 + (size_t)kSearchWavesWide * kp * 8;
+    return (n_models <= 8 && lds <= 163840) ? kSearchWavesWide : kSearchWaves;
+}
+
 hipError_t launch_fast_impl(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode, hipStream_t s)
 {
     const int N = fc.n_models, A = a.lay.A, H = a.lay.H;
-#define MF_FAST_CASE(MN, AA, HH) \
-    if (N <= MN && A == AA && H == HH) return launch_fast_t<MN, AA, HH>(a, fc, grid, kp, mode, s);
+    const bool wide = a.waves == kSearchWavesWide;
+#define MF_FAST_CASE(MN, AA, HH)                                                                        \
+    if (N <= MN && A == AA && H == HH) {                                                                \
+        if (wide) return launch_fast_t<MN, AA, HH, kSearchWavesWide>(a, fc, grid, kp, mode, s);         \
+        return launch_fast_t<MN, AA, HH, kSearchWaves>(a, fc, grid, kp, mode, s);                       \
+    }
 #define MF_FAST_A(MN, HH) MF_FAST_CASE(MN, 2, HH) MF_FAST_CASE(MN, 4, HH) MF_FAST_CASE(MN, 6, HH) MF_FAST_CASE(MN, 8, HH)
-    MF_FAST_A(8, 32) MF_FAST_A(8, 64) MF_FAST_A(16, 32) MF_FAST_A(16, 64)
+    MF_FAST_A(8, 32) MF_FAST_A(8, 64)
+#undef MF_FAST_CASE
+#define MF_FAST_CASE(MN, AA, HH) \
+    if (N <= MN && A == AA && H == HH) return launch_fast_t<MN, AA, HH, kSearchWaves>(a, fc, grid, kp, mode, s);
+    MF_FAST_A(16, 32) MF_FAST_A(16, 64)
 #undef MF_FAST_A
 #undef MF_FAST_CASE
     return hipErrorInvalidValue;

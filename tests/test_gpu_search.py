@@ -187,3 +187,35 @@ def test_eval_fast_and_canonical_sampled_full_size(mf, orc):
     assert can["J"].cpu().numpy().tobytes() == ref["J"].tobytes()
     np.testing.assert_array_equal(can["flags"].cpu().numpy().astype(np.uint32) & 0xFFFF07,
                                   ref["flags"] & 0xFFFF07)
+
+
+def test_topk_fallback_on_exact_ties(mf, orc):
+    # throughput independent of the configuration: every feasible config has
+    # J = N exactly, the fast list cannot separate the k-th candidate from
+    # the rest, and the fallback pass gathers and certifies all of them
+    inst = synth.make_instance([12, 12, 9], seed=4, vram_quantile=0.7, sla_range=(0.2, 1.0))
+    for i in range(inst.n_models):
+        W1, b1, W2, b2, W3, b3 = inst.model_weights(i)
+        W3[1, :] = 0.0
+        b3[1] = 1.0
+    r = orc.Problem(inst).search(inst.sla, inst.omega, k=5)
+    assert r["n_feas"] > 64            # more tied candidates than the fast list holds
+    g = mf.Problem(inst).search(inst.sla, inst.omega, k=5)
+    assert g["n_topk_collect"] > 0
+    assert g["n_feas"] == r["n_feas"]
+    assert list(g["top_idx"]) == list(r["top_idx"])
+    assert g["top_J"].tobytes() == r["top_J"].tobytes()
+
+
+def test_range_splits_when_certification_list_fills(mf, orc, monkeypatch):
+    inst = synth.make_instance([12, 12, 9, 9, 9], seed=5, vram_quantile=0.75,
+                               sla_range=(-0.15, 0.15), top_k=16)
+    r = orc.Problem(inst).search(inst.sla, inst.omega, k=16)
+    g0 = mf.Problem(inst).search(inst.sla, inst.omega, k=16)
+    assert g0["n_flagged"] >= 8
+    monkeypatch.setenv("MF_WORKLIST_CAP", "4")
+    g = mf.Problem(inst).search(inst.sla, inst.omega, k=16)
+    assert g["n_splits"] > 0, g0["n_flagged"]
+    assert g["n_feas"] == r["n_feas"] and g["n_vram"] == r["n_vram"]
+    assert list(g["top_idx"]) == list(r["top_idx"])
+    assert g["top_J"].tobytes() == r["top_J"].tobytes()
