@@ -29,8 +29,10 @@
  * relu(x) = (x > 0 ? x : +0).  The aggregate is summed in fp32 (model order)
  * and the oracle checks it against the fp64 sum: the generator's 2**-14 grid
  * makes them equal.  In bf16 mode the weights hold bfloat16 values and the
- * first hidden layer (the operand of the bf16 contraction) is rounded to
- * bfloat16, ties to even, after the relu.
+ * first hidden layer (the operand of the bf16 contraction) is quantised to
+ * bfloat16: its pre-activation is accumulated in fp32 (the precision of the
+ * contraction's accumulator: one fmaf chain in input order from the bias),
+ * then relu, then rounded to bfloat16, ties to even; layers 2 and 3 stay fp64.
  *
  * Build: gcc -O2 -fopenmp -ffp-contract=off -march=x86-64-v3 -shared -fPIC.
  */
@@ -120,10 +122,19 @@ static void mlp_forward(const double *w, int nin, int h1n, int h2n, int bf16,
     const double *W1 = w, *b1 = W1 + (int64_t)h1n * nin, *W2 = b1 + h1n,
                  *b2 = W2 + (int64_t)h2n * h1n, *W3 = b2 + h2n, *b3 = W3 + 2 * h2n;
     for (int u = 0; u < h1n; u++) {
-        double c = b1[u];
-        for (int k = 0; k < nin; k++) c = fma(W1[(int64_t)u * nin + k], z[k], c);
-        c = c > 0.0 ? c : 0.0;
-        h1[u] = bf16 ? bf16_round(c) : c;
+        if (bf16) {
+            /* the bf16 layer-1 activation is a quantisation decided in the
+             * precision the contraction accumulates in: fp32, one fused
+             * multiply-add chain in input order from the bias */
+            float c = (float)b1[u];
+            for (int k = 0; k < nin; k++) c = fmaf((float)W1[(int64_t)u * nin + k], (float)z[k], c);
+            c = c > 0.0f ? c : 0.0f;
+            h1[u] = bf16_round((double)c);
+        } else {
+            double c = b1[u];
+            for (int k = 0; k < nin; k++) c = fma(W1[(int64_t)u * nin + k], z[k], c);
+            h1[u] = c > 0.0 ? c : 0.0;
+        }
     }
     for (int v = 0; v < h2n; v++) {
         double c = b2[v];

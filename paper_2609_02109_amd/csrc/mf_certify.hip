@@ -2,7 +2,8 @@
 //
 // Results of the search are defined by canonical fp64 semantics (each dot
 // product one fused multiply-add chain, ascending inputs, starting from the
-// bias; relu(x) = x > 0 ? x : +0; J the fma chain over models).  The fast
+// bias; relu(x) = x > 0 ? x : +0; J the fma chain over models; in bf16 mode
+// the first hidden layer accumulates in fp32 and is rounded to bfloat16).  The fast
 // fp32 MFMA path settles every latency decision whose margin exceeds its
 // a-priori error bound; the rest, and every top-k candidate, are evaluated
 // here with that exact chain (v_fma_f64 is correctly rounded, so the values
@@ -121,10 +122,19 @@ canon_kernel(const CanonArgs a, const int search_mode)
             for (int k = lane; k < nin; k += 64) zs[k] = k < L ? (double)x[k] : (double)aggs[k - L];
             __syncthreads();
             for (int u = lane; u < H1; u += 64) {
-                double c = (double)b1[u];
-                for (int k = 0; k < nin; k++) c = fma((double)W1T[(int64_t)k * H1 + u], zs[k], c);
-                c = c > 0.0 ? c : 0.0;
-                h1s[u] = BF16 ? bf16_round_d(c) : c;
+                if (BF16) {
+                    // bf16 mode: the layer-1 pre-activation accumulates in fp32
+                    // (one fmaf chain in input order from the bias), then
+                    // relu and rounding to bfloat16
+                    float c = b1[u];
+                    for (int k = 0; k < nin; k++) c = fmaf(W1T[(int64_t)k * H1 + u], (float)zs[k], c);
+                    c = c > 0.f ? c : 0.f;
+                    h1s[u] = bf16_round_d((double)c);
+                } else {
+                    double c = (double)b1[u];
+                    for (int k = 0; k < nin; k++) c = fma((double)W1T[(int64_t)k * H1 + u], zs[k], c);
+                    h1s[u] = c > 0.0 ? c : 0.0;
+                }
             }
             __syncthreads();
             for (int v = lane; v < H2; v += 64) {

@@ -175,19 +175,21 @@ __global__ void __launch_bounds__(256) ga_fitness_kernel(const GAConst c, int S,
         double h1[H1];
 #pragma unroll
         for (int u = 0; u < H1; u++) {
-            double a = b1[u];
-#pragma unroll
-            for (int k = 0; k < NIN; k++) a = fma(W1[u * NIN + k], z[k], a);
-            a = a > 0.0 ? a : 0.0;
             if (BF16) {
-                if (a != 0.0) {
-                    int e = ilogb(a);
-                    if (e < -126) e = -126;
-                    const double sc = ldexp(1.0, 7 - e);
-                    a = rint(a * sc) / sc;
-                }
+                // fp32 accumulation in input order, relu, round to bfloat16
+                float a = (float)b1[u];
+#pragma unroll
+                for (int k = 0; k < NIN; k++) a = fmaf((float)W1[u * NIN + k], (float)z[k], a);
+                a = a > 0.f ? a : 0.f;
+                const uint32_t bits = __float_as_uint(a);
+                const uint32_t r = (bits + 0x7FFFu + ((bits >> 16) & 1u)) & 0xFFFF0000u;
+                h1[u] = (double)__uint_as_float(r);
+            } else {
+                double a = b1[u];
+#pragma unroll
+                for (int k = 0; k < NIN; k++) a = fma(W1[u * NIN + k], z[k], a);
+                h1[u] = a > 0.0 ? a : 0.0;
             }
-            h1[u] = a;
         }
         double y0 = b3[0], y1 = b3[1];
         for (int v = 0; v < H2; v++) {

@@ -110,6 +110,62 @@ def test_hand_instance_bf16_rounding(orc):
     assert r32["pred"][0, 0, 0] == (1 + 3 * 2 ** -8) + 2.0
 
 
+def test_bf16_layer1_is_an_fp32_chain(orc):
+    # bf16 mode quantises h1 from an fp32 fma chain in input order.  With
+    # weights and inputs of few significant bits every product is exact in
+    # fp32, so the chain equals sequential float32 additions, which numpy
+    # performs with correct rounding; layers 2 and 3 in float64 (torch).
+    rng = np.random.default_rng(3)
+    inst = synth.make_instance([4, 3], 8, 4, 32, 32, seed=6, vram_cap=1e9, dtype="bf16")
+    # weights +-2^-e: every product with a feature (<= 22 significant bits on
+    # the 2^-14 grid) is exact in fp32
+    for i in range(2):
+        W1, b1, W2, b2, W3, b3 = inst.model_weights(i)
+        W1[:] = rng.choice([-1, 1], W1.shape) * 2.0 ** -rng.integers(0, 4, W1.shape)
+        b1[:] = np.round(rng.uniform(-1, 1, b1.shape) * 2 ** 20) / 2 ** 20
+    p = orc.Problem(inst)
+    r = p.search(inst.sla, inst.omega, k=1, dump=True)
+    K = [int(k) for k in inst.n_options]
+    off = inst.option_offsets
+    for idx in range(p.space_size):
+        d = p.decode(idx)
+        rows = [inst.features[off[i] + d[i]] for i in range(2)]
+        agg = sum(rw[inst.agg_cols] for rw in rows).astype(np.float32)
+        for i in range(2):
+            W1, b1, W2, b2, W3, b3 = inst.model_weights(i)
+            z = np.concatenate([rows[i], agg]).astype(np.float32)
+            s = b1.astype(np.float32).copy()
+            for k in range(z.shape[0]):
+                s = (s + (W1[:, k] * z[k]).astype(np.float32)).astype(np.float32)
+            h1 = torch.from_numpy(np.maximum(s, 0)).to(torch.bfloat16).double()
+            h2 = torch.relu(torch.nn.functional.linear(h1, torch.from_numpy(W2.astype(np.float64)),
+                                                       torch.from_numpy(b2.astype(np.float64))))
+            y = torch.nn.functional.linear(h2, torch.from_numpy(W3.astype(np.float64)),
+                                           torch.from_numpy(b3.astype(np.float64))).numpy()
+            np.testing.assert_allclose(r["pred"][idx, i], y, rtol=0, atol=1e-12)
+
+
+def test_bf16_layer1_quantises_the_fp32_chain_not_the_exact_sum(orc):
+    # One model, one option, one hidden unit: s1 = b1 + 2^-25 x0 + 2^-25 x1
+    # with b1 = 1 + 2^-8 (the bf16 midpoint between 1 and 1 + 2^-7) and
+    # x = (1, 1).  In fp32 each 2^-25 is a quarter ulp at 1 and is rounded
+    # away: s1 = 1 + 2^-8, a tie that rounds to even, h1 = 1.  The exact sum
+    # 1 + 2^-8 + 2^-24 would round up to 1 + 2^-7.  Output = h1 for both rows.
+    w = np.array([[2 ** -25, 2 ** -25, 0.0, 1 + 2 ** -8, 1.0, 0.0, 1.0, 1.0, 0.0, 0.0]], np.float32)
+    def inst(dtype):
+        return synth.Instance(name="q", n_options=np.array([1], np.int32), model_type=np.array([0], np.int32),
+                              n_local=2, n_agg=1, hidden1=1, hidden2=1,
+                              features=np.array([[1.0, 1.0]], np.float32), agg_cols=np.array([0], np.int32),
+                              vram_slot=0, vram_cap=10.0, weights=w, sla=np.array([5.0], np.float32),
+                              omega=np.array([1.0], np.float32), dtype=dtype)
+    b = inst("bf16")
+    r = orc.Problem(b).search(b.sla, b.omega, k=1, dump=True)
+    assert r["pred"][0, 0, 0] == 1.0 and r["pred"][0, 0, 1] == 1.0
+    f = inst("f32")
+    r = orc.Problem(f).search(f.sla, f.omega, k=1, dump=True)
+    assert r["pred"][0, 0, 0] == 1 + 2 ** -8 + 2 ** -24
+
+
 # --------------------------------------------------------------------------
 # Decode / space size
 # --------------------------------------------------------------------------
