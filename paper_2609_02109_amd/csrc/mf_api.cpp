@@ -345,7 +345,11 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     MF_HIP2(launch_fast_impl(fa, p->fc, w.grid, w.kp, kModeSearch, s));
     MF_HIP2(hipEventRecord(ev1, s));
     MF_HIP2(launch_merge_lists(lists, w.grid, w.kp, cand, s));
-    MF_HIP2(launch_canonical(ca, w.kp + (int)std::min<uint64_t>(w.work_cap, 1u << 20), true, s));
+    ca.phase = 0;
+    MF_HIP2(launch_canonical(ca, w.kp, true, s));
+    MF_HIP2(launch_kth_candidate(cand, entJ, entF, w.kp, args->top_k, R, s));
+    ca.phase = 1;
+    MF_HIP2(launch_canonical(ca, (int)std::min<uint64_t>(w.work_cap, 1u << 20), true, s));
     MF_HIP2(launch_select(sa, p->fc, args->d_omega, s));
     DevResult h{};
     MF_HIP2(hipMemcpyAsync(&h, R, sizeof(DevResult), hipMemcpyDeviceToHost, s));
@@ -371,6 +375,7 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
         MF_HIP2(launch_fast_impl(fa, p->fc, w.grid, w.kp, kModeCollect, s));
         MF_HIP2(hipEventRecord(ev1, s));
         ca.collect_mode = 1;
+        ca.phase = 1;
         ca.mask = nullptr;
         MF_HIP2(launch_canonical(ca, (int)std::min<uint64_t>((uint64_t)w.work_cap + w.collect_cap, 1u << 20), true, s));
         sa.collect_mode = 1;

@@ -48,28 +48,28 @@ canon_kernel(const CanonArgs a, const int search_mode)
     const int lane = threadIdx.x;
     const int N = a.n_models, L = a.L, A = a.A, H1 = a.H1, H2 = a.H2, nin = L + A;
 
-    int64_t n_cand = 0, n_work = 0, n_coll = 0, n_ent;
+    int64_t n_cand = 0, n_work = 0, n_coll = 0, n_ent, e0 = 0;
     double jthr = -INFINITY;   // certification entries need the full J only from here up
     if (search_mode) {
         n_cand = a.collect_mode ? 0 : a.n_cand_keys;
         n_work = (int64_t)min(a.res->n_work, (unsigned long long)a.work_cap);
         n_coll = a.collect_mode ? (int64_t)min(a.res->n_collect, (unsigned long long)a.collect_cap) : 0;
-        n_ent = n_cand + n_work + n_coll;
-        if (a.collect_mode) {
-            jthr = a.res->theta;
+        // phase 0: the fast candidates; phase 1: certification (+ collected) entries
+        if (a.phase == 0) {
+            n_ent = n_cand;
         } else {
-            const unsigned long long ck = a.cand_keys[a.top_k - 1];
-            if (ck != 0ull) {
-                const double eJ = a.res->eJ;
-                const double jk = (double)unord_f32((uint32_t)(ck >> 32));
-                jthr = jk - 2.0 * eJ - (fabs(jk) + eJ) * 0x1p-20 - 1e-30;
-            }
+            e0 = n_cand;
+            n_ent = n_cand + n_work + n_coll;
+            // an entry whose upper bound U is below the k-th canonical J of
+            // the candidates (the collect threshold in the fallback pass)
+            // cannot enter the top-k: only its uncertain models are needed
+            jthr = a.collect_mode ? a.res->theta : a.res->ck_cand;
         }
     } else {
         n_ent = a.n_list;
     }
 
-    for (int64_t e = blockIdx.x; e < n_ent; e += gridDim.x) {
+    for (int64_t e = e0 + blockIdx.x; e < n_ent; e += gridDim.x) {
         uint64_t idx, off = 0;
         uint32_t models = 0xFFFFFFFFu;   // models to evaluate
         bool work_entry = false, need_J = true;
@@ -226,6 +226,35 @@ __device__ void list128_offer(K128 &slot, const K128 &mine, int lane, int k, K12
 
 constexpr int kSelWaves = 16;
 
+// k-th canonical J among the fast candidates (by J desc, index asc); -inf if
+// fewer than k are feasible.  One workgroup; kp <= 1024.
+__global__ void __launch_bounds__(1024) kth_candidate_kernel(const unsigned long long *cand, const double *ent_J,
+                                                             const uint32_t *ent_flags, int kp, int k, DevResult *R)
+{
+    const int e = threadIdx.x;
+    if (e == 0) R->ck_cand = -INFINITY;
+    __syncthreads();
+    if (e >= kp) return;
+    const bool ok = cand[e] != 0ull && (ent_flags[e] & 4u);
+    const double v = ok ? ent_J[e] : -INFINITY;
+    const uint64_t iv = ok ? (uint64_t)(0xFFFFFFFFu - (uint32_t)(cand[e] & 0xFFFFFFFFull)) : ~0ull;
+    int rank = 0;
+    for (int f = 0; f < kp; f++) {
+        const bool okf = cand[f] != 0ull && (ent_flags[f] & 4u);
+        const double vf = okf ? ent_J[f] : -INFINITY;
+        const uint64_t ivf = okf ? (uint64_t)(0xFFFFFFFFu - (uint32_t)(cand[f] & 0xFFFFFFFFull)) : ~0ull;
+        rank += (vf > v || (vf == v && ivf < iv) || (vf == v && ivf == iv && f < e)) ? 1 : 0;
+    }
+    if (ok && rank == k - 1) R->ck_cand = v;
+}
+
+hipError_t launch_kth_candidate(const unsigned long long *cand_keys, const double *ent_J, const uint32_t *ent_flags,
+                                int kp, int k, DevResult *res, hipStream_t s)
+{
+    hipLaunchKernelGGL(kth_candidate_kernel, dim3(1), dim3(1024), 0, s, cand_keys, ent_J, ent_flags, kp, k, res);
+    return hipGetLastError();
+}
+
 
 __global__ void __launch_bounds__(kSelWaves * 64)
 select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
@@ -238,7 +267,8 @@ select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
     DevResult *R = a.res;
     if (threadIdx.x == 0) { s_feas = 0; s_stat = 0; s_maxd = 0.0; }
     __syncthreads();
-    const double eJ = bound_eJ(fc, omega);
+    (void)fc;
+    (void)omega;
     const int64_t n_cand = a.collect_mode ? 0 : a.kp;
     const int64_t n_work = (int64_t)min(R->n_work, (unsigned long long)a.work_cap);
     const int64_t n_coll = a.collect_mode ? (int64_t)min(R->n_collect, (unsigned long long)a.collect_cap) : 0;
@@ -258,11 +288,14 @@ select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
                 have = ck != 0ull;
                 off = 0xFFFFFFFFu - (uint32_t)(ck & 0xFFFFFFFFull);
                 if (have) {
+                    // a sure-feasible fast decision must be canonically
+                    // feasible, and the key's U must bound the canonical J
                     if (!(fl & 4u)) atomicOr(&s_stat, kStatSelfCheck);
-                    const double jf = (double)unord_f32((uint32_t)(ck >> 32));
-                    const double dj = fabs(jf - a.ent_J[e]);
-                    if (!(dj <= eJ)) atomicOr(&s_stat, kStatSelfCheck);
-                    atomicMax((unsigned long long *)&s_maxd, (unsigned long long)__double_as_longlong(dj));
+                    const double U = (double)unord_f32((uint32_t)(ck >> 32));
+                    const double dj = U - a.ent_J[e];
+                    if (!(dj >= 0.0)) atomicOr(&s_stat, kStatSelfCheck);
+                    if (dj >= 0.0)
+                        atomicMax((unsigned long long *)&s_maxd, (unsigned long long)__double_as_longlong(dj));
                 }
             } else if (e < n_cand + n_work) {
                 off = (uint32_t)(a.work[e - n_cand] & 0xFFFFFFFFull);
@@ -291,7 +324,6 @@ select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
         }
         if (lane == 0) {
             R->n_top = n_top;
-            R->eJ = eJ;
             unsigned stat = s_stat;
             if (!a.collect_mode) {
                 R->n_feas_cert = s_feas;
@@ -299,14 +331,17 @@ select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
                 const unsigned long long tail = a.cand_keys[a.kp - 1];
                 const bool full = tail != 0ull;
                 if (full) stat |= kStatListFull;
-                const double tailJ = full ? (double)unord_f32((uint32_t)(tail >> 32)) : -INFINITY;
-                R->tail_J = tailJ;
+                // every sure-feasible configuration outside the list has an
+                // upper bound U <= tail_U: exact when the k-th canonical J
+                // exceeds it; otherwise the fallback collects all U >= C_k
+                const double tailU = full ? (double)unord_f32((uint32_t)(tail >> 32)) : -INFINITY;
+                R->tail_U = tailU;
                 bool verified = !full;
                 if (full && n_top >= k) {
                     const uint64_t b = (kth_hi & 0x8000000000000000ull) ? (kth_hi & 0x7FFFFFFFFFFFFFFFull) : ~kth_hi;
                     const double Ck = __longlong_as_double((long long)b);
-                    verified = Ck > tailJ + eJ;
-                    R->theta = Ck - eJ - (fabs(Ck) + eJ) * 0x1p-20 - 1e-30;
+                    verified = Ck > tailU;
+                    R->theta = Ck;
                 }
                 if (verified) stat |= kStatVerified;
             } else {

@@ -21,6 +21,15 @@ __device__ inline double bound_eJ(const FastConst &fc, const float *omega)
     return (e + m * 0x1p-48) * (1.0 + 0x1p-20) + 1e-30;
 }
 
+// Smallest float >= x (x finite double).
+__device__ __forceinline__ float f32_up(double x)
+{
+    float f = (float)x;
+    if ((double)f < x) f = __uint_as_float(f >= 0.f ? __float_as_uint(f) + 1u
+                                                     : (f == -0.f ? 1u : __float_as_uint(f) - 1u));
+    return f;
+}
+
 __device__ __forceinline__ float unord_f32(uint32_t o)
 {
     const uint32_t b = (o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o;

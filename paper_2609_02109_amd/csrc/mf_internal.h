@@ -61,10 +61,11 @@ struct DevResult {
     int n_top;
     unsigned long long top_idx[MF_MAX_TOPK];
     double top_J[MF_MAX_TOPK];
-    double theta;               // fallback collect threshold (fast J >= theta)
-    double eJ;                  // bound on |fast J - canonical J| for this call
-    double tail_J;              // fast J of the last fast candidate (list full)
-    double check_max_dJ;        // max |fast J - canonical J| seen on candidates
+    double theta;               // fallback collect threshold on the upper bound U
+    double eJ;                  // global bound on |fast J - canonical J| (fp32 path)
+    double tail_U;              // upper bound U of the last fast candidate (list full)
+    double check_max_dJ;        // max (U - canonical J) seen on candidates
+    double ck_cand;             // k-th canonical J among the fast candidates
 };
 constexpr unsigned kStatVerified = 1u;      // top-k exactness condition held
 constexpr unsigned kStatSelfCheck = 2u;     // a fast decision disagreed with canonical
@@ -92,12 +93,12 @@ struct FastArgs {
     const float *omega;         // device [N]
     DevResult *res;
     unsigned long long *work;   // certification list: offset | (uncertain-model mask << 32)
-    float *work_J;              // fast J of each certification entry
+    float *work_J;              // upper bound U >= canonical J of each certification entry
     uint32_t work_cap;
     uint32_t *collect;          // fallback candidate list
     uint32_t collect_cap;
-    double theta;               // collect mode threshold
-    unsigned long long *wg_lists; // [grid][KP] fast top-KP keys per workgroup
+    double theta;               // collect mode threshold on U
+    unsigned long long *wg_lists; // [grid][KP] top-KP keys (U, lowest index) per workgroup
     uint8_t *mask;              // dump (optional)
     float *pred;                // dump (optional)
 };
@@ -123,6 +124,7 @@ struct CanonArgs {
     DevResult *res;             // counters, eJ, collect threshold
     int top_k;
     int collect_mode;
+    int phase;                  // search mode: 0 fast candidates, 1 certification (+ collect) entries
     int64_t n_list;             // list mode entry count
     // outputs per entry
     double *ent_J;
@@ -168,6 +170,8 @@ int fast_kernel_supported(int n_models, int A, int H, int kp);
 hipError_t launch_merge_lists(const unsigned long long *lists, int n_lists, int kp,
                               unsigned long long *out, hipStream_t s);
 hipError_t launch_canonical(const CanonArgs &a, int n_entries_max, bool search_mode, hipStream_t s);
+hipError_t launch_kth_candidate(const unsigned long long *cand_keys, const double *ent_J, const uint32_t *ent_flags,
+                                int kp, int k, DevResult *res, hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, const FastConst &fc, const float *omega, hipStream_t s);
 int ga_fitness_supported(int nin, int h1, int h2);
 hipError_t launch_ga_feasible(const GAConst &c, uint32_t *blk_count, uint64_t *blk_off, unsigned long long *n_fl,

@@ -146,7 +146,10 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             par_off[i] = fc.opt_off[i];
         }
     }
-    if (mode == kModeSearch && blockIdx.x == 0 && threadIdx.x == 0) args.res->eJ = bound_eJ(fc, args.omega);
+    // global bound on |fast J - canonical J|: keys and certification entries
+    // carry the upper bound U = J + eJ
+    const double eJ = bound_eJ(fc, args.omega);
+    if (mode == kModeSearch && blockIdx.x == 0 && threadIdx.x == 0) args.res->eJ = eJ;
     __syncthreads();
 
     const int lane = threadIdx.x & 63, half = lane >> 5, col = lane & 31;
@@ -157,7 +160,6 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
     const int gw = blockIdx.x * WAVES + wv;
     const uint64_t n = args.n;
     const uint64_t n_tiles = (n + 31) >> 5;
-    const float theta = (float)args.theta;
 
     uint32_t bd[MAXN];
     if (mode != kModeList) {
@@ -329,20 +331,21 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             // canonically when it can change the count (VRAM ok) or, in dump
             // mode, the mask
             const bool unc = mine && !anyfail && anyunc && (vram_ok || args.mask != nullptr);
+            const float U = f32_up((double)J + eJ);
             if (mode == kModeSearch) {
                 c_vram += (mine && vram_ok) ? 1u : 0u;
                 c_feas += feas_sure ? 1u : 0u;
-                work_append(unc, (unsigned long long)(uint32_t)off | ((unsigned long long)umask << 32), J, lane,
+                work_append(unc, (unsigned long long)(uint32_t)off | ((unsigned long long)umask << 32), U, lane,
                             &args.res->n_work, args.work, args.work_J, args.work_cap);
                 const unsigned long long key = feas_sure
-                    ? (((unsigned long long)ord_f32(J) << 32) | (unsigned long long)(0xFFFFFFFFu - (uint32_t)off))
+                    ? (((unsigned long long)ord_f32(U) << 32) | (unsigned long long)(0xFFFFFFFFu - (uint32_t)off))
                     : 0ull;
                 list_offer(slot, key, lane, kp, thr_key);
                 if (args.mask && mine)
                     args.mask[off] = (uint8_t)((vram_ok ? 1u : 0u) | (sla_sure ? 2u : 0u) |
                                                (feas_sure ? 4u : 0u) | (unc ? 8u : 0u));
             } else {
-                list_append(feas_sure && J >= theta, (uint32_t)off, lane, &args.res->n_collect,
+                list_append(feas_sure && (double)U >= args.theta, (uint32_t)off, lane, &args.res->n_collect,
                             args.collect, args.collect_cap);
             }
         }
