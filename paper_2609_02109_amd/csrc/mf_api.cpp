@@ -37,6 +37,12 @@ struct mf_problem {
     int32_t *d_agg_cols = nullptr, *d_row_model = nullptr;
     FastLayout lay{};
     FastConst fc{};
+    // bf16 fast path
+    bool bf_ok = false;
+    Bf16Layout blay{};
+    Bf16Const bcst{};
+    float4 *d_bmodels = nullptr, *d_bg = nullptr;
+    float *d_phat = nullptr;
 };
 
 namespace {
@@ -172,13 +178,89 @@ void model_bounds(const mf_problem &p, const std::vector<float> &F, const std::v
     *m_thr = out_m;
 }
 
+// Smallest float >= x.
+float f32_up_host(double x)
+{
+    float f = (float)x;
+    if ((double)f < x) f = std::nextafter(f, INFINITY);
+    return f;
+}
+
+// Per model, the constants of the bf16 path's per-configuration bounds (see
+// the bf16 kernel): cst[2 + o] fixed terms of output o (the |b3| part of the
+// fp32 layer-3 bound and the fp64 rounding of the canonical layers 2 and 3),
+// cst[4 + o] = sum_v |W3[o][v]| |b2[v]|, cst[6 + o] = max_u sum_v
+// |W3[o][v]| |W2[v][u]|; *mag_thr bounds |thr| over the joint space.  Layer 1
+// is identical on both sides (the same fp32 chain and bf16 rounding).
+void bf16_bounds(const mf_problem &p, const std::vector<float> &F, const std::vector<float> &W, int i, float *cst,
+                 float *mag_thr)
+{
+    const int L = p.L, A = p.A, H = p.H1, nin = L + A;
+    const float *w = W.data() + (int64_t)i * p.wstride;
+    const float *W1 = w, *b1 = W1 + (int64_t)H * nin, *W2 = b1 + H, *b2 = W2 + (int64_t)H * H, *W3 = b2 + H,
+                *b3 = W3 + 2 * H;
+    // largest |input| of model i: its own options' local columns, and per
+    // aggregate slot the sum over models of the largest |column value|
+    std::vector<double> zmax(nin, 0.0);
+    for (int o = 0; o < p.K[i]; o++)
+        for (int k = 0; k < L; k++)
+            zmax[k] = std::max(zmax[k], (double)std::fabs(F[(int64_t)(p.opt_off[i] + o) * L + k]));
+    for (int k = 0; k < A; k++) {
+        double s = 0.0;
+        for (int j = 0; j < p.N; j++) {
+            double m = 0.0;
+            for (int o = 0; o < p.K[j]; o++)
+                m = std::max(m, (double)std::fabs(F[(int64_t)(p.opt_off[j] + o) * L + p.agg_cols[k]]));
+            s += m;
+        }
+        zmax[L + k] = s;
+    }
+    // |h1| (fp32 chain, then bf16 rounding), |h2| bounds
+    std::vector<double> M1(H), M2(H);
+    for (int u = 0; u < H; u++) {
+        double m = std::fabs((double)b1[u]);
+        for (int k = 0; k < nin; k++) m += std::fabs((double)W1[(int64_t)u * nin + k]) * zmax[k];
+        M1[u] = m * (1.0 + gam(nin, kU32)) * (1.0 + 0x1p-8);
+    }
+    for (int v = 0; v < H; v++) {
+        double m = std::fabs((double)b2[v]);
+        for (int u = 0; u < H; u++) m += std::fabs((double)W2[(int64_t)v * H + u]) * M1[u];
+        M2[v] = m * (1.0 + 1e-12);
+    }
+    const double g3 = gam(H / 2 + 2, kU32), g64 = gam(H + 1, kU64);
+    for (int o = 0; o < 2; o++) {
+        double cb = 0.0, e64 = 0.0, m3 = std::fabs((double)b3[o]);
+        for (int v = 0; v < H; v++) {
+            const double a3 = std::fabs((double)W3[o * H + v]);
+            cb += a3 * std::fabs((double)b2[v]);
+            e64 += a3 * g64 * M2[v];          // canonical layer 2 (fp64 chain)
+            m3 += a3 * M2[v];
+        }
+        e64 += g64 * m3;                      // canonical layer 3 (fp64 chain)
+        double rmax = 0.0;
+        for (int u = 0; u < H; u++) {
+            double r = 0.0;
+            for (int v = 0; v < H; v++)
+                r += std::fabs((double)W3[o * H + v]) * std::fabs((double)W2[(int64_t)v * H + u]);
+            rmax = std::max(rmax, r);
+        }
+        cst[2 + o] = f32_up_host((g3 * std::fabs((double)b3[o]) + e64) * 1.01 + 1e-30);
+        cst[4 + o] = f32_up_host(cb * (1.0 + 1e-6));
+        cst[6 + o] = f32_up_host(rmax * (1.0 + 1e-6));
+        if (o == 1) *mag_thr = f32_up_host(m3 * 1.01);
+    }
+}
+
 uint32_t magic_for(int K) { return K <= 1 ? 0u : (uint32_t)((0x100000000ull / (uint64_t)K) + 1ull); }
 
-int choose_kp(int top_k)
+// Length of the fast candidate list: twice the top-k (so that the k-th
+// canonical value usually clears the list's last upper bound), within the
+// kernel's limit.
+int choose_kp(int top_k, int max_kp)
 {
-    if (top_k <= 8) return 16;
-    if (top_k <= 16) return 32;
-    return 64;
+    int kp = 16;
+    while (kp < 2 * top_k && kp < max_kp) kp *= 2;
+    return kp;
 }
 
 void stride_digits(const mf_problem &p, uint64_t stride, uint32_t *out)
@@ -202,11 +284,19 @@ struct WsLayout {
 WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k)
 {
     WsLayout w{};
-    w.kp = choose_kp(top_k);
-    w.waves = fast_waves_for(p.N, p.lay, w.kp);
-    const uint64_t tiles = (n + 31) / 32;
-    uint64_t g = (tiles + w.waves - 1) / w.waves;
-    w.grid = (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)p.num_cus));
+    if (p.bf_ok) {
+        w.kp = choose_kp(top_k, 128);
+        w.waves = kBf16Waves;
+        const uint64_t per_wg = (uint64_t)kBf16Waves * kBf16Tiles * 32;
+        const uint64_t g = (n + per_wg - 1) / per_wg;
+        w.grid = (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)p.num_cus));
+    } else {
+        w.kp = choose_kp(top_k, 64);
+        w.waves = fast_waves_for(p.N, p.lay, w.kp);
+        const uint64_t tiles = (n + 31) / 32;
+        const uint64_t g = (tiles + w.waves - 1) / w.waves;
+        w.grid = (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)p.num_cus));
+    }
     // certification list: 1/128 of the range, at least 2^20 entries (never
     // more than the range), at most 2^26
     const uint64_t want = std::min<uint64_t>(std::max<uint64_t>(n / 128, (uint64_t)kDefaultWorklist), 1ull << 26);
@@ -271,6 +361,34 @@ void empty_result(mf_result &r)
         r.top_idx[q] = UINT64_MAX;
         r.top_J[q] = -INFINITY;
     }
+}
+
+// Launch the fast kernel of the problem's path (fp32 or bf16) over the range,
+// list or collect pass described by fa.
+hipError_t launch_fast_path(const mf_problem *p, const FastArgs &fa, int grid, int kp, int mode, hipStream_t s)
+{
+    if (!p->bf_ok) return launch_fast_impl(fa, p->fc, grid, kp, mode, s);
+    Bf16Args ba{};
+    ba.models = p->d_bmodels;
+    ba.g_image = p->d_bg;
+    ba.phat = p->d_phat;
+    ba.lay = p->blay;
+    ba.lo = fa.lo;
+    ba.n = fa.n;
+    ba.idx_list = fa.idx_list;
+    ba.sla = fa.sla;
+    ba.omega = fa.omega;
+    ba.res = fa.res;
+    ba.work = fa.work;
+    ba.work_J = fa.work_J;
+    ba.work_cap = fa.work_cap;
+    ba.collect = fa.collect;
+    ba.collect_cap = fa.collect_cap;
+    ba.theta = fa.theta;
+    ba.wg_lists = fa.wg_lists;
+    ba.mask = fa.mask;
+    ba.pred = fa.pred;
+    return launch_bf16_impl(ba, p->fc, p->bcst, grid, kp, mode, s);
 }
 
 enum RangeOutcome { kRangeOk, kRangeSplit };
@@ -342,7 +460,7 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
 
     MF_HIP2(hipMemsetAsync(R, 0, sizeof(DevResult), s));
     MF_HIP2(hipEventRecord(ev0, s));
-    MF_HIP2(launch_fast_impl(fa, p->fc, w.grid, w.kp, kModeSearch, s));
+    MF_HIP2(launch_fast_path(p, fa, w.grid, w.kp, kModeSearch, s));
     MF_HIP2(hipEventRecord(ev1, s));
     MF_HIP2(launch_merge_lists(lists, w.grid, w.kp, cand, s));
     ca.phase = 0;
@@ -372,7 +490,7 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
         fa.pred = nullptr;
         MF_HIP2(hipMemsetAsync(&R->n_collect, 0, sizeof(unsigned long long), s));
         MF_HIP2(hipEventRecord(ev0, s));
-        MF_HIP2(launch_fast_impl(fa, p->fc, w.grid, w.kp, kModeCollect, s));
+        MF_HIP2(launch_fast_path(p, fa, w.grid, w.kp, kModeCollect, s));
         MF_HIP2(hipEventRecord(ev1, s));
         ca.collect_mode = 1;
         ca.phase = 1;
@@ -600,15 +718,86 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
                 const int k = 2 * st + hf;
                 img[ly.off_c + hf * 4 + st] = k < A ? p->centre[perm[k]] : 0.f;
             }
+        for (int i = 0; i < N; i++)
+            model_bounds(*p, F, W, i, &p->fc.bound_lat[i], &p->fc.bound_thr[i], &p->fc.mag_thr[i]);
+    }
+    {
         FastConst &fc = p->fc;
         fc.n_models = N;
         for (int i = 0; i < N; i++) {
             fc.K[i] = p->K[i];
             fc.opt_off[i] = p->opt_off[i];
             fc.magic[i] = magic_for(p->K[i]);
-            model_bounds(*p, F, W, i, &fc.bound_lat[i], &fc.bound_thr[i], &fc.mag_thr[i]);
         }
         fc.vram_cap = p->vram_cap;
+    }
+
+    // ---- bf16 fast path (H1 == H2 in {64, 128, 256}, A in {2,4,6,8})
+    p->bf_ok = p->bf16 && H1 == H2 && bf16_kernel_supported(N, A, H1);
+    Bf16Layout &bl = p->blay;
+    std::vector<float> bimg, bg;
+    if (p->bf_ok) {
+        bl.H = H; bl.A = A; bl.MB = H / 32; bl.KS = H / 16; bl.S1 = A / 2; bl.PST = H;
+        int o = 0;
+        bl.off_w2a = o; o += bl.MB * bl.KS * 64 * 4;
+        bl.off_w1a = o; o += bl.MB * bl.S1 * 64;
+        bl.off_b2 = o; o += H;
+        bl.off_w3 = o; o += 2 * H;
+        bl.off_cst = o; o += 8;
+        bl.model_floats = (o + 3) & ~3;
+        bl.sumK = sumK;
+        bl.gv_floats = (sumK + 3) & ~3;
+        if (bf16_lds_bytes(bl, 128) > 163840) p->bf_ok = false;
+    }
+    if (p->bf_ok) {
+        bimg.assign((size_t)N * bl.model_floats, 0.f);
+        for (int i = 0; i < N; i++) {
+            const float *w = W.data() + (int64_t)i * p->wstride;
+            const float *W1 = w, *b1 = W1 + (int64_t)H * nin, *W2 = b1 + H, *b2 = W2 + (int64_t)H * H,
+                        *W3 = b2 + H, *b3 = W3 + 2 * H;
+            float *blk = bimg.data() + (size_t)i * bl.model_floats;
+            uint16_t *w2a = reinterpret_cast<uint16_t *>(blk + bl.off_w2a);
+            for (int mb2 = 0; mb2 < bl.MB; mb2++)
+                for (int ks = 0; ks < bl.KS; ks++)
+                    for (int l = 0; l < 64; l++)
+                        for (int j = 0; j < 8; j++) {
+                            const int v = 32 * mb2 + l % 32;
+                            const int u = 32 * (ks / 2) + 16 * (ks % 2) + 8 * (j / 4) + 4 * (l / 32) + j % 4;
+                            uint32_t bits;
+                            std::memcpy(&bits, &W2[(int64_t)v * H + u], 4);
+                            w2a[(((size_t)mb2 * bl.KS + ks) * 64 + l) * 8 + j] = (uint16_t)(bits >> 16);
+                        }
+            for (int mb = 0; mb < bl.MB; mb++)
+                for (int st = 0; st < bl.S1; st++)
+                    for (int l = 0; l < 64; l++)
+                        blk[bl.off_w1a + (mb * bl.S1 + st) * 64 + l] =
+                            W1[(int64_t)(32 * mb + l % 32) * nin + L + 2 * st + l / 32];
+            for (int h = 0; h < H; h++) blk[bl.off_b2 + h] = b2[h];
+            for (int o2 = 0; o2 < 2; o2++)
+                for (int mb = 0; mb < bl.MB; mb++)
+                    for (int q = 0; q < 4; q++)
+                        for (int hf = 0; hf < 2; hf++)
+                            for (int j = 0; j < 4; j++)
+                                blk[bl.off_w3 + (((o2 * bl.MB + mb) * 4 + q) * 2 + hf) * 4 + j] =
+                                    W3[o2 * H + 32 * mb + 8 * q + 4 * hf + j];
+            float cst[8];
+            bf16_bounds(*p, F, W, i, cst, &p->bcst.mag_thr[i]);
+            cst[0] = b3[0];
+            cst[1] = b3[1];
+            for (int t = 0; t < 8; t++) blk[bl.off_cst + t] = cst[t];
+        }
+        bg.assign((size_t)sumK * 8 + bl.gv_floats, 0.f);
+        for (int r = 0; r < sumK; r++) {
+            for (int hf = 0; hf < 2; hf++)
+                for (int st = 0; st < 4; st++) {
+                    const int k = 2 * st + hf;
+                    bg[(size_t)r * 8 + hf * 4 + st] = k < A ? F[(int64_t)r * L + p->agg_cols[k]] : 0.f;
+                }
+            bg[(size_t)sumK * 8 + r] = F[(int64_t)r * L + p->agg_cols[p->vram_slot]];
+        }
+        p->bcst.g2 = f32_up_host(gam(2.0 * bl.KS, kU32));
+        p->bcst.g3 = f32_up_host(gam(H / 2 + 2, kU32));
+        p->bcst.gN = f32_up_host(gam(N, kU32));
     }
 
     // ---- canonical image: per model W1T[nin][H1] b1 W2T[H1][H2] b2 W3[2][H2] b3
@@ -639,6 +828,9 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     const size_t o_z = off; off = align256(off + 64 * 4);
     const size_t o_c = off; off = align256(off + (size_t)A * 4);
     const size_t o_w64 = off; off = align256(off + W.size() * 8);
+    const size_t o_bm = off; off = align256(off + bimg.size() * 4);
+    const size_t o_bg = off; off = align256(off + bg.size() * 4);
+    const size_t o_ph = off; off = align256(off + (p->bf_ok ? (size_t)sumK * bl.PST * 4 : 0));
     if (hipMalloc(&p->d_mem, off) != hipSuccess) { delete p; return MF_ENOMEM; }
     char *base = (char *)p->d_mem;
     p->d_image = reinterpret_cast<float4 *>(base + o_img);
@@ -649,6 +841,9 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     p->d_zeros = reinterpret_cast<float *>(base + o_z);
     p->d_centre = reinterpret_cast<float *>(base + o_c);
     p->d_w64 = reinterpret_cast<double *>(base + o_w64);
+    p->d_bmodels = reinterpret_cast<float4 *>(base + o_bm);
+    p->d_bg = reinterpret_cast<float4 *>(base + o_bg);
+    p->d_phat = reinterpret_cast<float *>(base + o_ph);
     std::vector<double> w64(W.begin(), W.end());
     bool ok = true;
     ok = ok && hipMemsetAsync(p->d_zeros, 0, 64 * 4, s) == hipSuccess;
@@ -659,6 +854,11 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     ok = ok && hipMemcpyAsync(p->d_row_model, row_model.data(), (size_t)sumK * 4, hipMemcpyHostToDevice, s) == hipSuccess;
     ok = ok && hipMemcpyAsync(p->d_centre, p->centre.data(), (size_t)A * 4, hipMemcpyHostToDevice, s) == hipSuccess;
     ok = ok && hipMemcpyAsync(p->d_w64, w64.data(), w64.size() * 8, hipMemcpyHostToDevice, s) == hipSuccess;
+    if (!bimg.empty()) ok = ok && hipMemcpyAsync(p->d_bmodels, bimg.data(), bimg.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
+    if (!bg.empty()) ok = ok && hipMemcpyAsync(p->d_bg, bg.data(), bg.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
+    if (ok && p->bf_ok)
+        ok = launch_precompute_phat(p->d_features, p->d_canon, sumK, L, A, H, p->wstride, p->d_row_model, p->d_phat,
+                                    bl.PST, s) == hipSuccess;
     if (ok && p->fast_ok)
         ok = launch_precompute_p(p->d_features, p->d_canon, p->d_centre, sumK, L, A, H, p->wstride, p->d_row_model,
                                  reinterpret_cast<float *>(p->d_image) + ly.off_p, ly.PST, s) == hipSuccess;
@@ -705,7 +905,7 @@ static mf_status check_search_args(const mf_problem *p, const mf_search_args *a)
     if (!a->d_sla || !a->d_omega) return MF_EINVAL;
     if (a->flags & ~MF_DUMP) return MF_EINVAL;
     if ((a->flags & MF_DUMP) && (!a->d_mask || !a->d_pred || a->hi - a->lo > (1ull << 31))) return MF_EINVAL;
-    if (!p->fast_ok) return MF_EUNSUPPORTED;
+    if (!p->fast_ok && !p->bf_ok) return MF_EUNSUPPORTED;
     return MF_OK;
 }
 
@@ -740,8 +940,21 @@ mf_status mf_search(mf_problem *p, const mf_search_args *args, void *d_ws, size_
 mf_status mf_eval_fast(mf_problem *p, const uint64_t *d_idx, int64_t n, float *d_pred, void *stream)
 {
     if (!p || n < 0 || (n > 0 && (!d_idx || !d_pred))) return MF_EINVAL;
-    if (!p->fast_ok) return MF_EUNSUPPORTED;
+    if (!p->fast_ok && !p->bf_ok) return MF_EUNSUPPORTED;
     if (n == 0) return MF_OK;
+    if (p->bf_ok) {
+        FastArgs fa{};
+        fa.lo = 0;
+        fa.n = (uint64_t)n;
+        fa.idx_list = d_idx;
+        fa.sla = p->d_zeros;
+        fa.omega = p->d_zeros;
+        fa.pred = d_pred;
+        const uint64_t per_wg = (uint64_t)kBf16Waves * kBf16Tiles * 32;
+        const int grid = (int)std::max<uint64_t>(1, std::min<uint64_t>(((uint64_t)n + per_wg - 1) / per_wg,
+                                                                        (uint64_t)p->num_cus));
+        return hip_status(launch_fast_path(p, fa, grid, 16, kModeList, (hipStream_t)stream));
+    }
     FastArgs fa{};
     fa.image = p->d_image;
     fa.image_f4 = p->lay.total_floats / 4;

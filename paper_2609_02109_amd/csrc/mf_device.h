@@ -21,6 +21,127 @@ __device__ inline double bound_eJ(const FastConst &fc, const float *omega)
     return (e + m * 0x1p-48) * (1.0 + 0x1p-20) + 1e-30;
 }
 
+__device__ __forceinline__ uint32_t ord_f32(float f)
+{
+    const uint32_t b = __float_as_uint(f);
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ unsigned long long readlane64(unsigned long long x, int src)
+{
+    const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)x, src);
+    const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), src);
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+__device__ __forceinline__ unsigned long long shfl_up1_64(unsigned long long x)
+{
+    const uint32_t lo = __shfl_up((int)(uint32_t)x, 1);
+    const uint32_t hi = __shfl_up((int)(uint32_t)(x >> 32), 1);
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+__device__ __forceinline__ unsigned long long wave_sum64(unsigned long long x)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+        const uint32_t lo = __shfl_xor((int)(uint32_t)x, m);
+        const uint32_t hi = __shfl_xor((int)(uint32_t)(x >> 32), m);
+        x += ((unsigned long long)hi << 32) | lo;
+    }
+    return x;
+}
+
+// A wave's descending list of up to 64*NS distinct 64-bit keys in registers:
+// slot q = j*64 + lane lives in s[j].  thr is the smallest key while the
+// list is full (kp entries), 0 before.  Keys of 0 are never inserted.
+template <int NS>
+struct WaveList {
+    unsigned long long s[NS];
+    unsigned long long thr;
+};
+
+template <int NS>
+__device__ __forceinline__ void wl_init(WaveList<NS> &L)
+{
+#pragma unroll
+    for (int j = 0; j < NS; j++) L.s[j] = 0ull;
+    L.thr = 0ull;
+}
+
+template <int NS>
+__device__ __forceinline__ void wl_insert(WaveList<NS> &L, unsigned long long nk, int lane, int kp)
+{
+    int pos = 0;
+#pragma unroll
+    for (int j = 0; j < NS; j++) pos += __popcll(__ballot(j * 64 + lane < kp && L.s[j] > nk));
+    unsigned long long prev[NS];
+#pragma unroll
+    for (int j = 0; j < NS; j++) {
+        prev[j] = shfl_up1_64(L.s[j]);
+        if (j > 0) {
+            const unsigned long long last = readlane64(L.s[j - 1], 63);
+            if (lane == 0) prev[j] = last;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < NS; j++) {
+        const int q = j * 64 + lane;
+        if (q < kp) L.s[j] = q < pos ? L.s[j] : (q == pos ? nk : prev[j]);
+    }
+    const int t = kp - 1;
+    unsigned long long th = 0ull;
+#pragma unroll
+    for (int j = 0; j < NS; j++)
+        if (t / 64 == j) th = readlane64(L.s[j], t % 64);
+    L.thr = th;
+}
+
+// Offer every lane's key (0 = none) to the list.
+template <int NS>
+__device__ __forceinline__ void wl_offer(WaveList<NS> &L, unsigned long long mykey, int lane, int kp)
+{
+    unsigned long long cm = __ballot(mykey > L.thr);
+    while (cm) {
+        const int src = __ffsll((long long)cm) - 1;
+        cm &= cm - 1;
+        const unsigned long long nk = readlane64(mykey, src);
+        if (nk > L.thr) wl_insert(L, nk, lane, kp);
+    }
+}
+
+// Append flagged lanes' values to a device list; the counter keeps counting
+// past cap so the host can see an overflow.
+__device__ __forceinline__ unsigned long long list_reserve(bool flag, int lane, unsigned long long *count,
+                                                           unsigned long long &slot_out)
+{
+    const unsigned long long m = __ballot(flag);
+    if (m == 0) return 0;
+    unsigned long long base = 0;
+    if (lane == 0) base = atomicAdd(count, (unsigned long long)__popcll(m));
+    base = readlane64(base, 0);
+    slot_out = base + (unsigned long long)__popcll(m & ((1ull << lane) - 1ull));
+    return m;
+}
+
+__device__ __forceinline__ void list_append(bool flag, uint32_t value, int lane, unsigned long long *count,
+                                            uint32_t *list, uint32_t cap)
+{
+    unsigned long long slot = 0;
+    if (list_reserve(flag, lane, count, slot) && flag && slot < cap) list[slot] = value;
+}
+
+__device__ __forceinline__ void work_append(bool flag, unsigned long long entry, float fj, int lane,
+                                            unsigned long long *count, unsigned long long *list, float *list_J,
+                                            uint32_t cap)
+{
+    unsigned long long slot = 0;
+    if (list_reserve(flag, lane, count, slot) && flag && slot < cap) {
+        list[slot] = entry;
+        list_J[slot] = fj;
+    }
+}
+
 // Smallest float >= x (x finite double).
 __device__ __forceinline__ float f32_up(double x)
 {

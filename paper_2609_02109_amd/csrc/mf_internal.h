@@ -15,6 +15,9 @@ constexpr int kSearchWaves = 8;          // waves per workgroup of the fast sear
 constexpr int kSearchWavesWide = 16;     // ... when registers and LDS allow 4 waves per SIMD
 constexpr int kCertWaves = 4;            // waves per workgroup of the canonical kernels
 constexpr int kDefaultWorklist = 1 << 20; // certification list capacity (entries)
+constexpr int kBf16Waves = 8;            // waves per workgroup of the bf16 fast kernel
+constexpr int kBf16Tiles = 8;            // 32-configuration tiles per wave and model staging
+constexpr int kBf16TilesPerPass = 1;     // tiles sharing each LDS read of a W2 fragment
 
 // ---------------------------------------------------------------------------
 // Fast-path LDS image.  The device copy of the image is laid out exactly as
@@ -103,6 +106,52 @@ struct FastArgs {
     float *pred;                // dump (optional)
 };
 
+// ---------------------------------------------------------------------------
+// bf16 fast path.  Per model, one block staged into LDS (offsets in floats):
+//   w2a [mb2][ks][lane][8 bf16]   A operand of layer 2: lane l, element j holds
+//                                 W2[32 mb2 + l%32][32 (ks/2) + 16 (ks%2) + 8 (j/4) + 4 (l/32) + j%4]
+//   w1a [mb][s][lane]             A operand of layer 1 (aggregate slot 2s + l/32)
+//   b2  [H]
+//   w3  [o][mb][q][half][4]       W3[o][32 mb + 8 q + 4 half + j]
+//   cst [8]                       b3[0], b3[1], then per output (lat, thr):
+//                                 k0 (fixed bound terms), |W3||b2|, max_u (|W3||W2|)_u
+// Resident in LDS for the whole launch: g [sumK][half][4] aggregate slots of
+// every option row (slot 2s + half at [half][s], original slot order) and the
+// VRAM column gv [sumK].  In global memory: phat [sumK][PST], the fp32 chain
+// of each option's local columns from b1.
+// ---------------------------------------------------------------------------
+struct Bf16Layout {
+    int H, A, MB, KS, S1, PST;
+    int off_w2a, off_w1a, off_b2, off_w3, off_cst;
+    int model_floats;          // multiple of 4
+    int sumK, gv_floats;       // gv_floats: sumK rounded up to a multiple of 4
+};
+
+struct Bf16Const {
+    float g2, g3, gN;          // gamma_{2 KS}, gamma_{H/2+2}, gamma_N at fp32 unit roundoff
+    float mag_thr[kMaxN];      // a-priori bound on |thr| of model i
+};
+
+struct Bf16Args {
+    const float4 *models;      // [N][model_floats / 4]
+    const float4 *g_image;     // [(sumK * 8 + gv_floats) / 4]
+    const float *phat;         // [sumK][PST]
+    Bf16Layout lay;
+    uint64_t lo, n;
+    const uint64_t *idx_list;  // list mode only
+    const float *sla, *omega;
+    DevResult *res;
+    unsigned long long *work;
+    float *work_J;
+    uint32_t work_cap;
+    uint32_t *collect;
+    uint32_t collect_cap;
+    double theta;
+    unsigned long long *wg_lists;
+    uint8_t *mask;
+    float *pred;
+};
+
 // Canonical (fp64) evaluation of entries.
 struct CanonArgs {
     int n_models, L, A, H1, H2, bf16;
@@ -167,6 +216,12 @@ hipError_t launch_precompute_p(const float *features, const float *weights, cons
 hipError_t launch_fast_impl(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode, hipStream_t s);
 int fast_waves_for(int n_models, const FastLayout &lay, int kp);
 int fast_kernel_supported(int n_models, int A, int H, int kp);
+int bf16_kernel_supported(int n_models, int A, int H);
+size_t bf16_lds_bytes(const Bf16Layout &lay, int kp);
+hipError_t launch_bf16_impl(const Bf16Args &a, const FastConst &fc, const Bf16Const &bc, int grid, int kp, int mode,
+                            hipStream_t s);
+hipError_t launch_precompute_phat(const float *features, const float *canon_w, int n_rows, int L, int A, int H,
+                                  int64_t wstride, const int32_t *row_model, float *phat, int pst, hipStream_t s);
 hipError_t launch_merge_lists(const unsigned long long *lists, int n_lists, int kp,
                               unsigned long long *out, hipStream_t s);
 hipError_t launch_canonical(const CanonArgs &a, int n_entries_max, bool search_mode, hipStream_t s);

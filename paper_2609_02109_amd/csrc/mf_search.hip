@@ -28,95 +28,6 @@ namespace mfi {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-__device__ __forceinline__ uint32_t ord_f32(float f)
-{
-    const uint32_t b = __float_as_uint(f);
-    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
-}
-
-__device__ __forceinline__ unsigned long long readlane64(unsigned long long x, int src)
-{
-    const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)x, src);
-    const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), src);
-    return ((unsigned long long)hi << 32) | lo;
-}
-
-__device__ __forceinline__ unsigned long long shfl_up1_64(unsigned long long x)
-{
-    const uint32_t lo = __shfl_up((int)(uint32_t)x, 1);
-    const uint32_t hi = __shfl_up((int)(uint32_t)(x >> 32), 1);
-    return ((unsigned long long)hi << 32) | lo;
-}
-
-__device__ __forceinline__ unsigned long long wave_sum64(unsigned long long x)
-{
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-        const uint32_t lo = __shfl_xor((int)(uint32_t)x, m);
-        const uint32_t hi = __shfl_xor((int)(uint32_t)(x >> 32), m);
-        x += ((unsigned long long)hi << 32) | lo;
-    }
-    return x;
-}
-
-// Insert key nk (not yet present) into the wave's descending list: lane l < kp
-// holds slot l.  thr becomes the smallest key of the list (0 while not full).
-__device__ __forceinline__ void list_insert(unsigned long long &slot, unsigned long long nk, int lane,
-                                            int kp, unsigned long long &thr)
-{
-    const unsigned long long gt = __ballot(lane < kp && slot > nk);
-    const int pos = __popcll(gt);
-    const unsigned long long prev = shfl_up1_64(slot);
-    if (lane < kp) slot = lane < pos ? slot : (lane == pos ? nk : prev);
-    thr = readlane64(slot, kp - 1);
-}
-
-// Offer every lane's key to the list (keys of 0 are never inserted).
-__device__ __forceinline__ void list_offer(unsigned long long &slot, unsigned long long mykey, int lane,
-                                           int kp, unsigned long long &thr)
-{
-    unsigned long long cm = __ballot(mykey > thr);
-    while (cm) {
-        const int src = __ffsll((long long)cm) - 1;
-        cm &= cm - 1;
-        const unsigned long long nk = readlane64(mykey, src);
-        if (nk > thr) list_insert(slot, nk, lane, kp, thr);
-    }
-}
-
-// Append flagged lanes' values to a device list; the counter keeps counting
-// past cap so the host can see an overflow.
-template <typename T>
-__device__ __forceinline__ unsigned long long list_reserve(bool flag, int lane, unsigned long long *count,
-                                                           unsigned long long &slot_out)
-{
-    const unsigned long long m = __ballot(flag);
-    if (m == 0) return 0;
-    unsigned long long base = 0;
-    if (lane == 0) base = atomicAdd(count, (unsigned long long)__popcll(m));
-    base = readlane64(base, 0);
-    slot_out = base + (unsigned long long)__popcll(m & ((1ull << lane) - 1ull));
-    return m;
-}
-
-__device__ __forceinline__ void list_append(bool flag, uint32_t value, int lane, unsigned long long *count,
-                                            uint32_t *list, uint32_t cap)
-{
-    unsigned long long slot = 0;
-    if (list_reserve<uint32_t>(flag, lane, count, slot) && flag && slot < cap) list[slot] = value;
-}
-
-__device__ __forceinline__ void work_append(bool flag, unsigned long long entry, float fj, int lane,
-                                            unsigned long long *count, unsigned long long *list, float *list_J,
-                                            uint32_t cap)
-{
-    unsigned long long slot = 0;
-    if (list_reserve<unsigned long long>(flag, lane, count, slot) && flag && slot < cap) {
-        list[slot] = entry;
-        list_J[slot] = fj;
-    }
-}
-
 template <int MAXN, int A, int H, int WAVES>
 __global__ void __launch_bounds__(WAVES * 64, 1)
 fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int kp)
@@ -176,7 +87,8 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
         }
     }
 
-    unsigned long long slot = 0, thr_key = 0;
+    WaveList<1> wl;
+    wl_init(wl);
     uint32_t c_vram = 0, c_feas = 0;
 
     for (uint64_t tile = gw; tile < n_tiles; tile += (uint64_t)args.total_waves) {
@@ -340,7 +252,7 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
                 const unsigned long long key = feas_sure
                     ? (((unsigned long long)ord_f32(U) << 32) | (unsigned long long)(0xFFFFFFFFu - (uint32_t)off))
                     : 0ull;
-                list_offer(slot, key, lane, kp, thr_key);
+                wl_offer(wl, key, lane, kp);
                 if (args.mask && mine)
                     args.mask[off] = (uint8_t)((vram_ok ? 1u : 0u) | (sla_sure ? 2u : 0u) |
                                                (feas_sure ? 4u : 0u) | (unc ? 8u : 0u));
@@ -370,14 +282,14 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             if (sv) atomicAdd(&args.res->n_vram, sv);
             if (sf) atomicAdd(&args.res->n_feas_sure, sf);
         }
-        if (lane < kp) lst[wv * kp + lane] = slot;
+        if (lane < kp) lst[wv * kp + lane] = wl.s[0];
         __syncthreads();
         if (wv == 0) {
             for (int w = 1; w < WAVES; w++) {
                 const unsigned long long k2 = lane < kp ? lst[w * kp + lane] : 0ull;
-                list_offer(slot, k2, lane, kp, thr_key);
+                wl_offer(wl, k2, lane, kp);
             }
-            if (lane < kp) args.wg_lists[(uint64_t)blockIdx.x * kp + lane] = slot;
+            if (lane < kp) args.wg_lists[(uint64_t)blockIdx.x * kp + lane] = wl.s[0];
         }
     }
 }
@@ -387,22 +299,28 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
 // ---------------------------------------------------------------------------
 constexpr int kMergeWaves = 16;
 
+template <int NS>
 __global__ void __launch_bounds__(kMergeWaves * 64)
 merge_lists_kernel(const unsigned long long *lists, int n_keys, int kp, unsigned long long *out)
 {
-    __shared__ unsigned long long lst[kMergeWaves * 64];
+    __shared__ unsigned long long lst[kMergeWaves * 64 * NS];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    unsigned long long slot = 0, thr = 0;
+    WaveList<NS> L;
+    wl_init(L);
     for (int base = wv * 64; base < n_keys; base += kMergeWaves * 64) {
         const int t = base + lane;
-        const unsigned long long k = t < n_keys ? lists[t] : 0ull;
-        list_offer(slot, k, lane, kp, thr);
+        wl_offer(L, t < n_keys ? lists[t] : 0ull, lane, kp);
     }
-    lst[wv * 64 + lane] = lane < kp ? slot : 0ull;
+#pragma unroll
+    for (int j = 0; j < NS; j++) lst[(wv * NS + j) * 64 + lane] = (j * 64 + lane < kp) ? L.s[j] : 0ull;
     __syncthreads();
     if (wv == 0) {
-        for (int w = 1; w < kMergeWaves; w++) list_offer(slot, lst[w * 64 + lane], lane, kp, thr);
-        if (lane < kp) out[lane] = slot;
+        for (int w = 1; w < kMergeWaves; w++)
+#pragma unroll
+            for (int j = 0; j < NS; j++) wl_offer(L, lst[(w * NS + j) * 64 + lane], lane, kp);
+#pragma unroll
+        for (int j = 0; j < NS; j++)
+            if (j * 64 + lane < kp) out[j * 64 + lane] = L.s[j];
     }
 }
 
@@ -458,7 +376,10 @@ hipError_t launch_fast_impl(const FastArgs &a, const FastConst &fc, int grid, in
 hipError_t launch_merge_lists(const unsigned long long *lists, int n_lists, int kp, unsigned long long *out,
                               hipStream_t s)
 {
-    hipLaunchKernelGGL(merge_lists_kernel, dim3(1), dim3(kMergeWaves * 64), 0, s, lists, n_lists * kp, kp, out);
+    if (kp <= 64)
+        hipLaunchKernelGGL(merge_lists_kernel<1>, dim3(1), dim3(kMergeWaves * 64), 0, s, lists, n_lists * kp, kp, out);
+    else
+        hipLaunchKernelGGL(merge_lists_kernel<2>, dim3(1), dim3(kMergeWaves * 64), 0, s, lists, n_lists * kp, kp, out);
     return hipGetLastError();
 }
 
