@@ -89,6 +89,38 @@ def measure_search(mf, torch, inst, k, steps, warmup):
     return (t1 - t0) * 1e3 / steps, float(np.mean(kernel_ms)), r
 
 
+PEAK_BF16_TFLOPS = 2500.0
+
+
+def n8_roofline(inst, kernel_ms):
+    # The bf16 kernel mixes three pipes: layer 1's aggregate part on the fp32
+    # matrix cores (an exact fp32 chain), layer 2 on the bf16 matrix cores,
+    # layer 3 on fp32 vector ALUs.  Its floor is the sum of each part's
+    # algorithmic flops over that part's peak; frac = floor / measured time.
+    N, A, H = inst.n_models, inst.n_agg, inst.hidden1
+    n = inst.space_size
+    f32 = N * 2 * A * H * n
+    bf16 = N * 2 * H * H * n
+    valu = N * 2 * 2 * H * n
+    floor_s = f32 / (PEAK_FP32_TFLOPS * 1e12) + bf16 / (PEAK_BF16_TFLOPS * 1e12) + valu / (PEAK_FP32_TFLOPS * 1e12)
+    return {"bound": "mfma", "floor_ms": floor_s * 1e3, "kernel_ms": kernel_ms,
+            "frac": floor_s * 1e3 / kernel_ms, "flops_per_config": {"fp32_mfma": f32 // n, "bf16_mfma": bf16 // n,
+                                                                   "fp32_valu": valu // n}}
+
+
+def bench_n8(mf, torch, seed, steps, warmup):
+    from paper_2609_02109_amd import synth
+    inst = synth.cfg4(seed)
+    ms, kms, r = measure_search(mf, torch, inst, 64, steps, warmup)
+    log(f"n8 search: {ms:.1f} ms/step, fast kernel {kms:.1f} ms, n_feas={r.n_feas} n_flagged={r.n_flagged} "
+        f"collect={r.n_topk_collect} argmax={r.top_idx[0]}")
+    return {"workload": "N=8 models x 16 options (4,294,967,296 joint configs), 40-256-256-2 bf16 weights with fp32 "
+                        "accumulation, VRAM cap 288 GB, top-64 + counts",
+            "ms_to_top64": ms, "joint_configs_per_s": inst.space_size / (ms * 1e-3), "fast_kernel_ms": kms,
+            "n_feas": int(r.n_feas), "n_flagged": int(r.n_flagged), "n_topk_collect": int(r.n_topk_collect),
+            "argmax": int(r.top_idx[0]), "roofline": n8_roofline(inst, kms)}
+
+
 def bench_ga(args):
     import torch
     from paper_2609_02109_amd import mf, synth
@@ -122,8 +154,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--workload", choices=["n6", "ga"], default="n6",
-                    help="n6: the N=6 exhaustive search (the benchmark step); ga: the N=5 GA scheduler")
+    ap.add_argument("--workload", choices=["n6", "ga", "n8"], default="n6",
+                    help="n6: the N=6 exhaustive search (the benchmark step); ga: the N=5 GA scheduler; "
+                         "n8: only the N=8 bf16 search")
+    ap.add_argument("--no-n8", action="store_true", help="skip the N=8 bf16 search in the n6 line")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="run one plain device copy kernel of this many bytes read (and written) "
                          "before the search: the calibration point for HBM byte counters")
@@ -137,6 +171,9 @@ def main():
     from paper_2609_02109_amd import mf, synth
     if args.workload == "ga":
         return bench_ga(args)
+    if args.workload == "n8":
+        print(json.dumps(bench_n8(mf, torch, args.seed, args.steps, args.warmup)), flush=True)
+        return
 
     if args.copy_bytes:
         src = torch.ones(args.copy_bytes // 4, dtype=torch.float32, device="cuda")
@@ -155,6 +192,8 @@ def main():
     ms5, kms5, r5 = measure_search(mf, torch, inst5, 16, max(args.steps, 20), max(args.warmup, 3))
     log(f"search: {ms:.2f} ms/step, fast kernel {kms:.2f} ms, n_feas={r.n_feas} "
         f"n_flagged={r.n_flagged} argmax={r.top_idx[0]} J={r.top_J[0]!r}")
+
+    n8 = None if args.no_n8 else bench_n8(mf, torch, args.seed, 2, 1)
 
     cpu = None
     if not args.no_cpu:
@@ -182,7 +221,8 @@ def main():
                    "n5": {"workload": "N=5 models, options 12,12,9,9,9 (104,976 joint configs), 12-32-32-2 fp32, "
                                       "top-16 + counts", "ms_to_argmax": ms5,
                           "joint_configs_per_s": inst5.space_size / (ms5 * 1e-3), "fast_kernel_ms": kms5,
-                          "n_feas": int(r5.n_feas), "argmax": int(r5.top_idx[0])}},
+                          "n_feas": int(r5.n_feas), "argmax": int(r5.top_idx[0])},
+                   "n8": n8},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_FP32_TFLOPS, "traffic": measured_traffic(),
                      "kernel": "fast_kernel<8,6,64>", "kernel_ms": kms,

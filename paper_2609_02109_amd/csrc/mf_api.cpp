@@ -190,8 +190,11 @@ float f32_up_host(double x)
 // the bf16 kernel): cst[2 + o] fixed terms of output o (the |b3| part of the
 // fp32 layer-3 bound and the fp64 rounding of the canonical layers 2 and 3),
 // cst[4 + o] = sum_v |W3[o][v]| |b2[v]|, cst[6 + o] = max_u sum_v
-// |W3[o][v]| |W2[v][u]|; *mag_thr bounds |thr| over the joint space.  Layer 1
-// is identical on both sides (the same fp32 chain and bf16 rounding).
+// |W3[o][v]| |W2[v][u]|, cst[8 + o] = max_v |W3[o][v]|; *mag_thr bounds |thr|
+// over the joint space.  Layer 1 is identical on both sides (the same fp32
+// chain and bf16 rounding).  Layer 3 runs as four partial fp32 chains of H/8
+// terms per output, summed pairwise, plus the cross-half add and b3: at most
+// H/8 + 4 roundings.
 void bf16_bounds(const mf_problem &p, const std::vector<float> &F, const std::vector<float> &W, int i, float *cst,
                  float *mag_thr)
 {
@@ -227,7 +230,7 @@ void bf16_bounds(const mf_problem &p, const std::vector<float> &F, const std::ve
         for (int u = 0; u < H; u++) m += std::fabs((double)W2[(int64_t)v * H + u]) * M1[u];
         M2[v] = m * (1.0 + 1e-12);
     }
-    const double g3 = gam(H / 2 + 2, kU32), g64 = gam(H + 1, kU64);
+    const double g3 = gam(H / 8 + 4, kU32), g64 = gam(H + 1, kU64);
     for (int o = 0; o < 2; o++) {
         double cb = 0.0, e64 = 0.0, m3 = std::fabs((double)b3[o]);
         for (int v = 0; v < H; v++) {
@@ -247,6 +250,9 @@ void bf16_bounds(const mf_problem &p, const std::vector<float> &F, const std::ve
         cst[2 + o] = f32_up_host((g3 * std::fabs((double)b3[o]) + e64) * 1.01 + 1e-30);
         cst[4 + o] = f32_up_host(cb * (1.0 + 1e-6));
         cst[6 + o] = f32_up_host(rmax * (1.0 + 1e-6));
+        double w3max = 0.0;
+        for (int v = 0; v < H; v++) w3max = std::max(w3max, std::fabs((double)W3[o * H + v]));
+        cst[8 + o] = f32_up_host(w3max);
         if (o == 1) *mag_thr = f32_up_host(m3 * 1.01);
     }
 }
@@ -743,7 +749,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
         bl.off_w1a = o; o += bl.MB * bl.S1 * 64;
         bl.off_b2 = o; o += H;
         bl.off_w3 = o; o += 2 * H;
-        bl.off_cst = o; o += 8;
+        bl.off_cst = o; o += 12;
         bl.model_floats = (o + 3) & ~3;
         bl.sumK = sumK;
         bl.gv_floats = (sumK + 3) & ~3;
@@ -780,11 +786,11 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
                             for (int j = 0; j < 4; j++)
                                 blk[bl.off_w3 + (((o2 * bl.MB + mb) * 4 + q) * 2 + hf) * 4 + j] =
                                     W3[o2 * H + 32 * mb + 8 * q + 4 * hf + j];
-            float cst[8];
+            float cst[12] = {};
             bf16_bounds(*p, F, W, i, cst, &p->bcst.mag_thr[i]);
             cst[0] = b3[0];
             cst[1] = b3[1];
-            for (int t = 0; t < 8; t++) blk[bl.off_cst + t] = cst[t];
+            for (int t = 0; t < 12; t++) blk[bl.off_cst + t] = cst[t];
         }
         bg.assign((size_t)sumK * 8 + bl.gv_floats, 0.f);
         for (int r = 0; r < sumK; r++) {
@@ -796,7 +802,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
             bg[(size_t)sumK * 8 + r] = F[(int64_t)r * L + p->agg_cols[p->vram_slot]];
         }
         p->bcst.g2 = f32_up_host(gam(2.0 * bl.KS, kU32));
-        p->bcst.g3 = f32_up_host(gam(H / 2 + 2, kU32));
+        p->bcst.g3 = f32_up_host(gam(H / 8 + 4, kU32));
         p->bcst.gN = f32_up_host(gam(N, kU32));
     }
 

@@ -17,7 +17,6 @@ constexpr int kCertWaves = 4;            // waves per workgroup of the canonical
 constexpr int kDefaultWorklist = 1 << 20; // certification list capacity (entries)
 constexpr int kBf16Waves = 8;            // waves per workgroup of the bf16 fast kernel
 constexpr int kBf16Tiles = 8;            // 32-configuration tiles per wave and model staging
-constexpr int kBf16TilesPerPass = 1;     // tiles sharing each LDS read of a W2 fragment
 
 // ---------------------------------------------------------------------------
 // Fast-path LDS image.  The device copy of the image is laid out exactly as
@@ -113,8 +112,9 @@ struct FastArgs {
 //   w1a [mb][s][lane]             A operand of layer 1 (aggregate slot 2s + l/32)
 //   b2  [H]
 //   w3  [o][mb][q][half][4]       W3[o][32 mb + 8 q + 4 half + j]
-//   cst [8]                       b3[0], b3[1], then per output (lat, thr):
-//                                 k0 (fixed bound terms), |W3||b2|, max_u (|W3||W2|)_u
+//   cst [12]                      b3[0], b3[1], then per output (lat, thr):
+//                                 k0 (fixed bound terms), |W3||b2|, max_u (|W3||W2|)_u,
+//                                 max_v |W3[o][v]|
 // Resident in LDS for the whole launch: g [sumK][half][4] aggregate slots of
 // every option row (slot 2s + half at [half][s], original slot order) and the
 // VRAM column gv [sumK].  In global memory: phat [sumK][PST], the fp32 chain
@@ -128,7 +128,7 @@ struct Bf16Layout {
 };
 
 struct Bf16Const {
-    float g2, g3, gN;          // gamma_{2 KS}, gamma_{H/2+2}, gamma_N at fp32 unit roundoff
+    float g2, g3, gN;          // gamma_{2 KS}, gamma_{H/8+4}, gamma_N at fp32 unit roundoff
     float mag_thr[kMaxN];      // a-priori bound on |thr| of model i
 };
 

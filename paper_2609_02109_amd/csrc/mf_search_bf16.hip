@@ -13,14 +13,16 @@
 //             row order is absorbed into W2's A-operand layout); fp32
 //             accumulation.  W2 (128 KB per model at H=256) is staged in LDS
 //             one model at a time: a workgroup runs the model over all of its
-//             tiles before staging the next, and each A fragment read from
-//             LDS feeds TT tiles.
-//   layer 3   VALU fp32.  The only difference from the canonical values is
-//             the fp32 accumulation of layers 2 and 3, bounded per
-//             configuration: gamma_{2KS} (|W3||b2| + max_u r_u sum h1), with
-//             r = |W3||W2|, plus gamma_{H/2+2} (|b3| + |W3| h2).
-// Per-tile state (J, its bound, flags) rotates through registers so that the
-// runtime tile loop never indexes a private array.
+//             tiles before staging the next.
+//   layer 3   VALU fp32, four partial chains per output.  The only difference
+//             from the canonical values is the fp32 accumulation of layers 2
+//             and 3, bounded per configuration by
+//               gamma_{2 KS} (|W3||b2| + max_u r_u sum_u h1[u]),  r = |W3||W2|
+//             + gamma_{H/8+4} (|b3| + max_v |W3[o][v]| sum_v h2[v]).
+// Within a tile, the MFMAs of each 32-row block overlap the VALU epilogue of
+// the previous block (relu and bf16 packing after layer 1, relu and layer 3
+// after layer 2).  Per-tile state (J, its bound, flags) rotates through
+// registers so that the runtime tile loop never indexes a private array.
 #include "mf_device.h"
 
 namespace mfi {
@@ -31,8 +33,24 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr uint32_t kFlagFail = 0x80000000u;   // some model surely misses its bound
 constexpr uint32_t kFlagVram = 0x40000000u;   // VRAM cap met
 
-// max(x, 0) for the non-NaN accumulator values (one v_med3_f32)
-__device__ __forceinline__ float relu(float x) { return __builtin_amdgcn_fmed3f(x, 0.f, INFINITY); }
+// relu for finite fp32 values as one integer max: negative values (and -0)
+// have a negative bit pattern and map to +0, the rest are unchanged
+__device__ __forceinline__ float relu(float x) { return __int_as_float(max(__float_as_int(x), 0)); }
+
+// 16 accumulator rows of one 32-row block: [q][j] = p[8 q + j], j < 4
+__device__ __forceinline__ floatx16 load16(const float *p)
+{
+    floatx16 r;
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        const float4 v = *reinterpret_cast<const float4 *>(p + 8 * q);
+        r[4 * q + 0] = v.x;
+        r[4 * q + 1] = v.y;
+        r[4 * q + 2] = v.z;
+        r[4 * q + 3] = v.w;
+    }
+    return r;
+}
 
 __device__ __forceinline__ bf16x8 pack8(const float *x)
 {
@@ -42,13 +60,53 @@ __device__ __forceinline__ bf16x8 pack8(const float *x)
     return r;
 }
 
-template <int MAXN, int A, int H, int TT>
+// relu, running sum of the activations, bfloat16 B operands (rows 0-7, 8-15)
+__device__ __forceinline__ void layer1_epilogue(const floatx16 &acc, bf16x8 &lo, bf16x8 &hi, float &sh)
+{
+    float x[16];
+#pragma unroll
+    for (int r = 0; r < 16; r++) {
+        x[r] = relu(acc[r]);
+        sh += x[r];
+    }
+    lo = pack8(x);
+    hi = pack8(x + 8);
+}
+
+// Layer-3 weights of one 32-row block for this lane's half: [q] = rows 8 q + j
+__device__ __forceinline__ void load_w3(const float *wl, const float *wt, float4 *pwl, float4 *pwt)
+{
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        pwl[q] = *reinterpret_cast<const float4 *>(wl + 8 * q);
+        pwt[q] = *reinterpret_cast<const float4 *>(wt + 8 * q);
+    }
+}
+
+__device__ __forceinline__ float f4get(const float4 &v, int j)
+{
+    return j == 0 ? v.x : (j == 1 ? v.y : (j == 2 ? v.z : v.w));
+}
+
+// relu of accumulator row r (= 4 q + j) of a layer-2 block and its layer-3
+// contribution: partial chain q takes rows 8 q + j; s2 sums the activations
+// (for the rounding bound).  r is a compile-time constant after unrolling.
+__device__ __forceinline__ void layer3_row(const floatx16 &acc, int r, const float4 *pwl, const float4 *pwt,
+                                           float *yl, float *yt, float &s2)
+{
+    const int q = r >> 2, j = r & 3;
+    const float h = relu(acc[r]);
+    yl[q] = fmaf(f4get(pwl[q], j), h, yl[q]);
+    yt[q] = fmaf(f4get(pwt[q], j), h, yt[q]);
+    s2 += h;
+}
+
+template <int MAXN, int A, int H>
 __global__ void __launch_bounds__(kBf16Waves * 64, 1)
 fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, const int mode, const int kp)
 {
     constexpr int MB = H / 32, KS = H / 16, S1 = A / 2;
     constexpr int WAVES = kBf16Waves, TW = kBf16Tiles;
-    static_assert(TW % TT == 0, "tiles per wave must be a multiple of tiles per pass");
     constexpr uint64_t SUP = (uint64_t)WAVES * TW * 32;
     extern __shared__ float4 smem4[];
     float *smem = reinterpret_cast<float *>(smem4);
@@ -117,190 +175,154 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
             const float *cst = smem + Ly.off_cst;
             const float b30 = cst[0], b31 = cst[1];
             const float k0l = cst[2], k0t = cst[3], cbl = cst[4], cbt = cst[5], rml = cst[6], rmt = cst[7];
+            const float m3l = cst[8], m3t = cst[9];
             const float sla_i = par[i], om_i = par[32 + i];
             const uint32_t row0 = (uint32_t)par_off[i];
 
-            for (int t0 = 0; t0 < TW; t0 += TT) {
+            for (int t = 0; t < TW; t++) {
                 // The staged weights are re-read from LDS for every tile: an
                 // opaque zero offset keeps the compiler from hoisting those
                 // reads out of the tile loop (they would not fit in registers).
                 int z0 = 0;
                 asm volatile("" : "+v"(z0));
-                const uint4 *w2a = reinterpret_cast<const uint4 *>(smem + Ly.off_w2a + z0);
-                const float *w1a = smem + Ly.off_w1a + z0;
+                const uint4 *w2a = reinterpret_cast<const uint4 *>(smem + Ly.off_w2a + z0) + lane;
+                const float *w1a = smem + Ly.off_w1a + z0 + lane;
                 const float *b2 = smem + Ly.off_b2 + 4 * half + z0;
                 const float *w3 = smem + Ly.off_w3 + 4 * half + z0;
-                uint64_t off[TT];
-                bool valid[TT];
-                bf16x8 hp[TT][KS];
-                float sum_h1[TT], vsum[TT];
+                const uint64_t off = wbase + (uint64_t)t * 32 + (uint64_t)col;
+                const bool valid = off < n;
+                uint32_t d[MAXN];
+                if (list_mode) {
+                    uint64_t x = valid ? args.idx_list[off] : 0ull;
 #pragma unroll
-                for (int tt = 0; tt < TT; tt++) {
-                    off[tt] = wbase + (uint64_t)(t0 + tt) * 32 + (uint64_t)col;
-                    valid[tt] = off[tt] < n;
-                    uint32_t d[MAXN];
-                    if (list_mode) {
-                        uint64_t x = valid[tt] ? args.idx_list[off[tt]] : 0ull;
-#pragma unroll
-                        for (int j = MAXN - 1; j >= 0; j--) {
-                            if (j < N) {
-                                const uint64_t k = (uint64_t)fc.K[j];
-                                d[j] = (uint32_t)(x % k);
-                                x /= k;
-                            } else {
-                                d[j] = 0;
-                            }
-                        }
-                    } else {
-                        uint32_t carry = (uint32_t)((t0 + tt) * 32 + col);
-#pragma unroll
-                        for (int j = MAXN - 1; j >= 0; j--) {
-                            if (j < N) {
-                                const uint32_t s = bd[j] + carry;
-                                const uint32_t q = fc.magic[j] ? __umulhi(s, fc.magic[j]) : s;
-                                d[j] = s - q * (uint32_t)fc.K[j];
-                                carry = q;
-                            } else {
-                                d[j] = 0;
-                            }
-                        }
-                    }
-                    // aggregate (fp32, model order) and this model's option row
-                    float ah[4] = {0.f, 0.f, 0.f, 0.f};
-                    float vs = 0.f;
-                    uint64_t dig0 = 0, dig1 = 0;
-#pragma unroll
-                    for (int j = 0; j < MAXN; j++) {
+                    for (int j = MAXN - 1; j >= 0; j--) {
                         if (j < N) {
-                            if (j < 8) dig0 |= (uint64_t)d[j] << (8 * j);
-                            else dig1 |= (uint64_t)d[j] << (8 * (j - 8));
-                            const uint32_t r = (uint32_t)fc.opt_off[j] + d[j];
-                            const float4 v = *reinterpret_cast<const float4 *>(G + r * 8 + 4 * half);
-                            ah[0] += v.x;
-                            ah[1] += v.y;
-                            ah[2] += v.z;
-                            ah[3] += v.w;
-                            vs += Gv[r];
+                            const uint64_t k = (uint64_t)fc.K[j];
+                            d[j] = (uint32_t)(x % k);
+                            x /= k;
+                        } else {
+                            d[j] = 0;
                         }
                     }
-                    vsum[tt] = vs;
-                    const uint64_t sel = (uint64_t)0 - (uint64_t)(i >= 8);
-                    const uint64_t dw = dig0 ^ ((dig0 ^ dig1) & sel);
-                    const uint32_t row = row0 + (uint32_t)((dw >> (8 * (i & 7))) & 0xFFu);
-
-                    // layer 1 (the canonical fp32 chain) -> relu -> bf16 B operands
-                    const float *prow = args.phat + (size_t)row * Ly.PST + 4 * half;
-                    float sh = 0.f;
+                } else {
+                    uint32_t carry = (uint32_t)(t * 32 + col);
 #pragma unroll
-                    for (int mb = 0; mb < MB; mb++) {
-                        floatx16 acc;
-#pragma unroll
-                        for (int q = 0; q < 4; q++) {
-                            const float4 v = *reinterpret_cast<const float4 *>(prow + 32 * mb + 8 * q);
-                            acc[4 * q + 0] = v.x;
-                            acc[4 * q + 1] = v.y;
-                            acc[4 * q + 2] = v.z;
-                            acc[4 * q + 3] = v.w;
+                    for (int j = MAXN - 1; j >= 0; j--) {
+                        if (j < N) {
+                            const uint32_t sj = bd[j] + carry;
+                            const uint32_t q = fc.magic[j] ? __umulhi(sj, fc.magic[j]) : sj;
+                            d[j] = sj - q * (uint32_t)fc.K[j];
+                            carry = q;
+                        } else {
+                            d[j] = 0;
                         }
-#pragma unroll
-                        for (int s = 0; s < S1; s++)
-                            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(w1a[(mb * S1 + s) * 64 + lane], ah[s], acc, 0,
-                                                                       0, 0);
-                        float x[16];
-#pragma unroll
-                        for (int r = 0; r < 16; r++) {
-                            x[r] = relu(acc[r]);
-                            sh += x[r];
-                        }
-                        hp[tt][2 * mb + 0] = pack8(x);
-                        hp[tt][2 * mb + 1] = pack8(x + 8);
                     }
-                    sum_h1[tt] = sh;
                 }
-
-                // layer 2 (bf16 MFMA, one A fragment per TT tiles) -> relu -> layer 3
-                float yl[TT], yt[TT], bl3[TT], bt3[TT];
+                // aggregate (fp32, model order) and this model's option row
+                float ah[4] = {0.f, 0.f, 0.f, 0.f};
+                float vsum = 0.f;
+                uint64_t dig0 = 0, dig1 = 0;
 #pragma unroll
-                for (int tt = 0; tt < TT; tt++) { yl[tt] = 0.f; yt[tt] = 0.f; bl3[tt] = 0.f; bt3[tt] = 0.f; }
+                for (int j = 0; j < MAXN; j++) {
+                    if (j < N) {
+                        if (j < 8) dig0 |= (uint64_t)d[j] << (8 * j);
+                        else dig1 |= (uint64_t)d[j] << (8 * (j - 8));
+                        const uint32_t r = (uint32_t)fc.opt_off[j] + d[j];
+                        const float4 v = *reinterpret_cast<const float4 *>(G + r * 8 + 4 * half);
+                        ah[0] += v.x;
+                        ah[1] += v.y;
+                        ah[2] += v.z;
+                        ah[3] += v.w;
+                        vsum += Gv[r];
+                    }
+                }
+                const uint64_t sel = (uint64_t)0 - (uint64_t)(i >= 8);
+                const uint64_t dw = dig0 ^ ((dig0 ^ dig1) & sel);
+                const uint32_t row = row0 + (uint32_t)((dw >> (8 * (i & 7))) & 0xFFu);
+                const float *prow = args.phat + (size_t)row * Ly.PST + 4 * half;
+
+                // ---- layer 1: the canonical fp32 chain, seeded with the
+                // option's local part; block mb's MFMAs overlap block mb-1's
+                // relu / bf16 packing
+                bf16x8 hp[KS];
+                float sh = 0.f;
+                floatx16 seed = load16(prow);
+                floatx16 prev1 = seed;
+#pragma unroll
+                for (int mb = 0; mb < MB; mb++) {
+                    floatx16 acc = seed;
+                    if (mb + 1 < MB) seed = load16(prow + 32 * (mb + 1));
+#pragma unroll
+                    for (int s1 = 0; s1 < S1; s1++)
+                        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(w1a[(mb * S1 + s1) * 64], ah[s1], acc, 0, 0, 0);
+                    if (mb > 0) layer1_epilogue(prev1, hp[2 * mb - 2], hp[2 * mb - 1], sh);
+                    prev1 = acc;
+                }
+                layer1_epilogue(prev1, hp[KS - 2], hp[KS - 1], sh);
+
+                // ---- layer 2 (bf16 MFMA, A fragments prefetched 4 ahead) and
+                // layer 3 (four partial chains per output); block mb2's MFMAs
+                // overlap block mb2-1's layer-3 work
+                constexpr int PF = 4, NF = MB * KS, EPS = 16 / KS;   // epilogue rows per MFMA step
+                uint4 af[PF];
+#pragma unroll
+                for (int f = 0; f < PF; f++) af[f] = w2a[f * 64];
+                float yl[4] = {0.f, 0.f, 0.f, 0.f}, yt[4] = {0.f, 0.f, 0.f, 0.f};
+                float s2 = 0.f;
+                floatx16 prev2 = {};
+                float4 pwl[4], pwt[4];
 #pragma unroll
                 for (int mb2 = 0; mb2 < MB; mb2++) {
-                    floatx16 acc2[TT];
-#pragma unroll
-                    for (int q = 0; q < 4; q++) {
-                        const float4 v = *reinterpret_cast<const float4 *>(b2 + 32 * mb2 + 8 * q);
-#pragma unroll
-                        for (int tt = 0; tt < TT; tt++) {
-                            acc2[tt][4 * q + 0] = v.x;
-                            acc2[tt][4 * q + 1] = v.y;
-                            acc2[tt][4 * q + 2] = v.z;
-                            acc2[tt][4 * q + 3] = v.w;
-                        }
-                    }
+                    floatx16 acc2 = load16(b2 + 32 * mb2);
+                    if (mb2 > 0) load_w3(w3 + (mb2 - 1) * 32, w3 + (MB + mb2 - 1) * 32, pwl, pwt);
 #pragma unroll
                     for (int ks = 0; ks < KS; ks++) {
-                        const uint4 a = w2a[(mb2 * KS + ks) * 64 + lane];
+                        const int f = mb2 * KS + ks;
+                        const uint4 a = af[f % PF];
+                        if (f + PF < NF) af[f % PF] = w2a[(f + PF) * 64];
                         bf16x8 av;
                         __builtin_memcpy(&av, &a, 16);
+                        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, hp[ks], acc2, 0, 0, 0);
+                        // the previous block's relu and layer-3 rows, a share per step
+                        if (mb2 > 0) {
 #pragma unroll
-                        for (int tt = 0; tt < TT; tt++)
-                            acc2[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, hp[tt][ks], acc2[tt], 0, 0, 0);
+                            for (int e = 0; e < EPS; e++) layer3_row(prev2, ks * EPS + e, pwl, pwt, yl, yt, s2);
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
                     }
-#pragma unroll
-                    for (int q = 0; q < 4; q++) {
-                        const float4 wl4 = *reinterpret_cast<const float4 *>(w3 + ((0 * MB + mb2) * 4 + q) * 8);
-                        const float4 wt4 = *reinterpret_cast<const float4 *>(w3 + ((1 * MB + mb2) * 4 + q) * 8);
-                        const float wls[4] = {wl4.x, wl4.y, wl4.z, wl4.w};
-                        const float wts[4] = {wt4.x, wt4.y, wt4.z, wt4.w};
-#pragma unroll
-                        for (int tt = 0; tt < TT; tt++)
-#pragma unroll
-                            for (int j = 0; j < 4; j++) {
-                                const float h = relu(acc2[tt][4 * q + j]);
-                                yl[tt] = fmaf(wls[j], h, yl[tt]);
-                                yt[tt] = fmaf(wts[j], h, yt[tt]);
-                                bl3[tt] = fmaf(fabsf(wls[j]), h, bl3[tt]);
-                                bt3[tt] = fmaf(fabsf(wts[j]), h, bt3[tt]);
-                            }
-                    }
+                    prev2 = acc2;
                 }
+                load_w3(w3 + (MB - 1) * 32, w3 + (2 * MB - 1) * 32, pwl, pwt);
+#pragma unroll
+                for (int r = 0; r < 16; r++) layer3_row(prev2, r, pwl, pwt, yl, yt, s2);
 
+                float ylf = (yl[0] + yl[1]) + (yl[2] + yl[3]);
+                float ytf = (yt[0] + yt[1]) + (yt[2] + yt[3]);
+                ylf += __shfl_xor(ylf, 32);
+                ytf += __shfl_xor(ytf, 32);
+                s2 += __shfl_xor(s2, 32);
+                sh += __shfl_xor(sh, 32);
+                const float lat = ylf + b30, thr = ytf + b31;
+                // per-configuration bounds on |fast - canonical|, inflated
+                // for their own fp32 evaluation (sum h1 >= sum of its bf16
+                // roundings / (1 + 2^-8))
+                const float el = (k0l + bc.g2 * (cbl + rml * sh * 1.0079f) + bc.g3 * m3l * s2) * 1.001f + 1e-30f;
+                const float et = (k0t + bc.g2 * (cbt + rmt * sh * 1.0079f) + bc.g3 * m3t * s2) * 1.001f + 1e-30f;
+                const float slack = el + (fabsf(lat) + fabsf(sla_i)) * 0x1p-20f;
+                const bool pass = lat + slack <= sla_i, fail = lat - slack > sla_i;
+                uint32_t fl = Ft[0] | (fail ? kFlagFail : 0u) | ((pass || fail) ? 0u : (1u << i));
+                if (i == 0 && (double)vsum <= (double)fc.vram_cap) fl |= kFlagVram;
+                const float jn = fmaf(om_i, thr, Jt[0]);
+                const float en = Et[0] + fabsf(om_i) * (et + bc.gN * fabsf(thr));
+                // rotate the per-tile state: slot 0 becomes the next tile
 #pragma unroll
-                for (int tt = 0; tt < TT; tt++) {
-                    const float ylf = yl[tt] + __shfl_xor(yl[tt], 32);
-                    const float ytf = yt[tt] + __shfl_xor(yt[tt], 32);
-                    const float bl = bl3[tt] + __shfl_xor(bl3[tt], 32);
-                    const float bt = bt3[tt] + __shfl_xor(bt3[tt], 32);
-                    const float sh = sum_h1[tt] + __shfl_xor(sum_h1[tt], 32);
-                    const float lat = ylf + b30, thr = ytf + b31;
-                    // per-configuration bounds on |fast - canonical|, inflated
-                    // for their own fp32 evaluation (sum h1 >= sum of its bf16
-                    // roundings / (1 + 2^-8))
-                    const float el = (k0l + bc.g2 * (cbl + rml * sh * 1.0079f) + bc.g3 * bl) * 1.001f + 1e-30f;
-                    const float et = (k0t + bc.g2 * (cbt + rmt * sh * 1.0079f) + bc.g3 * bt) * 1.001f + 1e-30f;
-                    const float slack = el + (fabsf(lat) + fabsf(sla_i)) * 0x1p-20f;
-                    const bool pass = lat + slack <= sla_i, fail = lat - slack > sla_i;
-                    uint32_t f = Ft[tt] | (fail ? kFlagFail : 0u) | ((pass || fail) ? 0u : (1u << i));
-                    if (i == 0 && (double)vsum[tt] <= (double)fc.vram_cap) f |= kFlagVram;
-                    Ft[tt] = f;
-                    Jt[tt] = fmaf(om_i, thr, Jt[tt]);
-                    Et[tt] = Et[tt] + fabsf(om_i) * (et + bc.gN * fabsf(thr));
-                    if (args.pred && valid[tt] && half == 0) {
-                        args.pred[(off[tt] * (uint64_t)N + (uint64_t)i) * 2u + 0u] = lat;
-                        args.pred[(off[tt] * (uint64_t)N + (uint64_t)i) * 2u + 1u] = thr;
-                    }
-                }
-                // rotate the per-tile state by TT: slots [0, TT) become the next tiles
-                float jr[TT], er[TT];
-                uint32_t fr[TT];
-#pragma unroll
-                for (int tt = 0; tt < TT; tt++) { jr[tt] = Jt[tt]; er[tt] = Et[tt]; fr[tt] = Ft[tt]; }
-#pragma unroll
-                for (int u = 0; u < TW - TT; u++) { Jt[u] = Jt[u + TT]; Et[u] = Et[u + TT]; Ft[u] = Ft[u + TT]; }
-#pragma unroll
-                for (int tt = 0; tt < TT; tt++) {
-                    Jt[TW - TT + tt] = jr[tt];
-                    Et[TW - TT + tt] = er[tt];
-                    Ft[TW - TT + tt] = fr[tt];
+                for (int u = 0; u < TW - 1; u++) { Jt[u] = Jt[u + 1]; Et[u] = Et[u + 1]; Ft[u] = Ft[u + 1]; }
+                Jt[TW - 1] = jn;
+                Et[TW - 1] = en;
+                Ft[TW - 1] = fl;
+                if (args.pred && valid && half == 0) {
+                    args.pred[(off * (uint64_t)N + (uint64_t)i) * 2u + 0u] = lat;
+                    args.pred[(off * (uint64_t)N + (uint64_t)i) * 2u + 1u] = thr;
                 }
             }
         }
@@ -403,7 +425,7 @@ static hipError_t launch_bf16_t(const Bf16Args &a, const FastConst &fc, const Bf
                                 int mode, hipStream_t s)
 {
     const size_t lds = bf16_lds_bytes(a.lay, kp);
-    auto fn = fast_bf16_kernel<MAXN, A, H, kBf16TilesPerPass>;
+    auto fn = fast_bf16_kernel<MAXN, A, H>;
     hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(grid), dim3(kBf16Waves * 64), lds, s, a, fc, bc, mode, kp);
