@@ -743,16 +743,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     Bf16Layout &bl = p->blay;
     std::vector<float> bimg, bg;
     if (p->bf_ok) {
-        bl.H = H; bl.A = A; bl.MB = H / 32; bl.KS = H / 16; bl.S1 = A / 2; bl.PST = H;
-        int o = 0;
-        bl.off_w2a = o; o += bl.MB * bl.KS * 64 * 4;
-        bl.off_w1a = o; o += bl.MB * bl.S1 * 64;
-        bl.off_b2 = o; o += H;
-        bl.off_w3 = o; o += 2 * H;
-        bl.off_cst = o; o += 12;
-        bl.model_floats = (o + 3) & ~3;
-        bl.sumK = sumK;
-        bl.gv_floats = (sumK + 3) & ~3;
+        bl = bf16_layout(H, A, sumK);
         if (bf16_lds_bytes(bl, 128) > 163840) p->bf_ok = false;
     }
     if (p->bf_ok) {

@@ -123,9 +123,29 @@ struct FastArgs {
 struct Bf16Layout {
     int H, A, MB, KS, S1, PST;
     int off_w2a, off_w1a, off_b2, off_w3, off_cst;
-    int model_floats;          // multiple of 4
+    int model_floats;          // multiple of 256 (1 KB)
     int sumK, gv_floats;       // gv_floats: sumK rounded up to a multiple of 4
 };
+
+constexpr Bf16Layout bf16_layout(int H, int A, int sumK)
+{
+    Bf16Layout l{};
+    l.H = H;
+    l.A = A;
+    l.MB = H / 32;
+    l.KS = H / 16;
+    l.S1 = A / 2;
+    l.PST = H;
+    l.off_w2a = 0;
+    l.off_w1a = l.off_w2a + l.MB * l.KS * 64 * 4;
+    l.off_b2 = l.off_w1a + l.MB * l.S1 * 64;
+    l.off_w3 = l.off_b2 + H;
+    l.off_cst = l.off_w3 + 2 * H;
+    l.model_floats = (l.off_cst + 12 + 255) & ~255;   // whole 1 KB chunks (direct LDS loads)
+    l.sumK = sumK;
+    l.gv_floats = (sumK + 3) & ~3;
+    return l;
+}
 
 struct Bf16Const {
     float g2, g3, gN;          // gamma_{2 KS}, gamma_{H/8+4}, gamma_N at fp32 unit roundoff
@@ -219,6 +239,12 @@ int fast_kernel_supported(int n_models, int A, int H, int kp);
 int bf16_kernel_supported(int n_models, int A, int H);
 size_t bf16_lds_bytes(const Bf16Layout &lay, int kp);
 hipError_t launch_bf16_impl(const Bf16Args &a, const FastConst &fc, const Bf16Const &bc, int grid, int kp, int mode,
+                            hipStream_t s);
+hipError_t launch_bf16_h64(const Bf16Args &a, const FastConst &fc, const Bf16Const &bc, int grid, int kp, int mode,
+                           hipStream_t s);
+hipError_t launch_bf16_h128(const Bf16Args &a, const FastConst &fc, const Bf16Const &bc, int grid, int kp, int mode,
+                            hipStream_t s);
+hipError_t launch_bf16_h256(const Bf16Args &a, const FastConst &fc, const Bf16Const &bc, int grid, int kp, int mode,
                             hipStream_t s);
 hipError_t launch_precompute_phat(const float *features, const float *canon_w, int n_rows, int L, int A, int H,
                                   int64_t wstride, const int32_t *row_model, float *phat, int pst, hipStream_t s);
