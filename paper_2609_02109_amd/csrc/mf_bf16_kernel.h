@@ -36,9 +36,6 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr uint32_t kFlagFail = 0x80000000u;   // some model surely misses its bound
 constexpr uint32_t kFlagVram = 0x40000000u;   // VRAM cap met
 
-// relu for finite fp32 values as one integer max: negative values (and -0)
-// have a negative bit pattern and map to +0, the rest are unchanged
-__device__ __forceinline__ float relu(float x) { return __int_as_float(max(__float_as_int(x), 0)); }
 
 // 16 accumulator rows of one 32-row block: [q][j] = p[8 q + j], j < 4
 __device__ __forceinline__ floatx16 load16(const float *p)
@@ -119,7 +116,7 @@ __device__ __forceinline__ void layer3_row(const floatx16 &acc, int r, const flo
                                            float *yl, float *yt, float &s2)
 {
     const int q = r >> 2, j = r & 3;
-    const float h = relu(acc[r]);
+    const float h = relu_f32(acc[r]);
     yl[q] = fmaf(f4get(pwl[q], j), h, yl[q]);
     yt[q] = fmaf(f4get(pwt[q], j), h, yt[q]);
     s2 += h;

@@ -21,6 +21,10 @@ __device__ inline double bound_eJ(const FastConst &fc, const float *omega)
     return (e + m * 0x1p-48) * (1.0 + 0x1p-20) + 1e-30;
 }
 
+// relu of a finite fp32 value as one integer max: negative values (and -0)
+// have a negative bit pattern and map to +0, the rest are unchanged
+__device__ __forceinline__ float relu_f32(float x) { return __int_as_float(max(__float_as_int(x), 0)); }
+
 __device__ __forceinline__ uint32_t ord_f32(float f)
 {
     const uint32_t b = __float_as_uint(f);

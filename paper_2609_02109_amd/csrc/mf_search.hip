@@ -173,7 +173,7 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
 #pragma unroll
             for (int mb = 0; mb < MB; mb++)
 #pragma unroll
-                for (int r = 0; r < 16; r++) acc1[mb][r] = fmaxf(acc1[mb][r], 0.f);
+                for (int r = 0; r < 16; r++) acc1[mb][r] = relu_f32(acc1[mb][r]);
             // ---- layer 2: b2 + W2 h1
             floatx16 acc2[MB];
             const float *b2 = smem + Ly.off_b2 + i * H + 4 * half;
@@ -213,8 +213,8 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
                 for (int q = 0; q < 4; q++) {
                     const float4 wl = *reinterpret_cast<const float4 *>(w3 + ((0 * MB + mb) * 4 + q) * 8);
                     const float4 wt = *reinterpret_cast<const float4 *>(w3 + ((1 * MB + mb) * 4 + q) * 8);
-                    const float h0 = fmaxf(acc2[mb][4 * q + 0], 0.f), h1 = fmaxf(acc2[mb][4 * q + 1], 0.f);
-                    const float h2 = fmaxf(acc2[mb][4 * q + 2], 0.f), h3 = fmaxf(acc2[mb][4 * q + 3], 0.f);
+                    const float h0 = relu_f32(acc2[mb][4 * q + 0]), h1 = relu_f32(acc2[mb][4 * q + 1]);
+                    const float h2 = relu_f32(acc2[mb][4 * q + 2]), h3 = relu_f32(acc2[mb][4 * q + 3]);
                     pl = fmaf(wl.x, h0, pl); pt = fmaf(wt.x, h0, pt);
                     pl = fmaf(wl.y, h1, pl); pt = fmaf(wt.y, h1, pt);
                     pl = fmaf(wl.z, h2, pl); pt = fmaf(wt.z, h2, pt);

@@ -44,6 +44,8 @@ def bf16_parity(mf, orc, inst, lo, hi, k):
     dict(n_options=[1, 13, 1, 6], n_local=8, n_agg=6, hidden=64),      # options count 1
     dict(n_options=[2] * 16, n_local=8, n_agg=4, hidden=64),           # N = 16
     dict(n_options=[5, 4, 3], n_local=32, n_agg=8, hidden=256),        # the N=8 workload's model shape
+    dict(n_options=[3, 1, 2, 2, 1, 3, 2, 2], n_local=8, n_agg=4, hidden=64),   # N = 8 with one-option models
+    dict(n_options=[2, 3, 2, 2, 3, 2, 2, 2], n_local=16, n_agg=6, hidden=128),  # N = 8, every count > 1
 ])
 def test_bf16_full_space(mf, orc, shape):
     inst = synth.make_instance(shape["n_options"], shape["n_local"], shape["n_agg"], shape["hidden"],
@@ -146,5 +148,40 @@ def test_bf16_topk_fallback_on_exact_ties(mf, orc):
     g = mf.Problem(inst).search(inst.sla, inst.omega, k=64)
     assert g["n_topk_collect"] > 0
     assert g["n_feas"] == r["n_feas"]
+    assert list(g["top_idx"]) == list(r["top_idx"])
+    assert g["top_J"].tobytes() == r["top_J"].tobytes()
+
+
+def test_bf16_degenerate_ranges(mf, orc):
+    inst = synth.cfg4(2)
+    p = mf.Problem(inst)
+    g = p.search(inst.sla, inst.omega, k=64, lo=1000, hi=1000)
+    assert g["n_eval"] == 0 and g["n_feas"] == 0 and len(g["top_idx"]) == 0
+    for lo in (0, 12_345_678, inst.space_size - 1):
+        r = orc.Problem(inst).search(inst.sla, inst.omega, k=3, lo=lo, hi=lo + 1)
+        g = p.search(inst.sla, inst.omega, k=3, lo=lo, hi=lo + 1)
+        assert g["n_feas"] == r["n_feas"] and g["n_vram"] == r["n_vram"]
+        assert list(g["top_idx"]) == list(r["top_idx"])
+        assert g["top_J"].tobytes() == r["top_J"].tobytes()
+
+
+def test_bf16_range_splits_when_certification_list_fills(mf, orc, monkeypatch):
+    # model 0's latency is the constant 0.25 and its bound is exactly 0.25:
+    # every configuration sits on the (inclusive) boundary, so every one is
+    # certified, and a 4-entry certification list forces many range splits
+    inst = synth.make_instance([9, 8, 7, 6], 8, 4, 64, 64, seed=21, vram_quantile=0.8, sla_range=(0.2, 1.0),
+                               dtype="bf16")
+    W1, b1, W2, b2, W3, b3 = inst.model_weights(0)
+    W3[0, :] = 0.0
+    b3[0] = 0.25
+    inst.sla[0] = 0.25
+    r = orc.Problem(inst).search(inst.sla, inst.omega, k=16)
+    assert r["n_feas"] > 0
+    g0 = mf.Problem(inst).search(inst.sla, inst.omega, k=16)
+    assert g0["n_flagged"] >= r["n_feas"]
+    monkeypatch.setenv("MF_WORKLIST_CAP", "4")
+    g = mf.Problem(inst).search(inst.sla, inst.omega, k=16)
+    assert g["n_splits"] > 0
+    assert g["n_feas"] == r["n_feas"] and g["n_vram"] == r["n_vram"]
     assert list(g["top_idx"]) == list(r["top_idx"])
     assert g["top_J"].tobytes() == r["top_J"].tobytes()
