@@ -33,11 +33,21 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+MAX_VARIANTS = 4
+
+
+class _Obj(C.Structure):
+    _fields_ = [("variant", C.c_void_p), ("fmin", C.c_void_p), ("fmax", C.c_void_p), ("quality", C.c_void_p),
+                ("reload_cost", C.c_void_p), ("prev_variant", C.c_void_p), ("tau", C.c_void_p),
+                ("alpha", C.c_float), ("beta", C.c_float), ("delta", C.c_float)]
+
+
 class _Inst(C.Structure):
     _fields_ = [("n_models", C.c_int32), ("n_local", C.c_int32), ("n_agg", C.c_int32),
                 ("hidden1", C.c_int32), ("hidden2", C.c_int32), ("bf16", C.c_int32),
                 ("n_options", C.c_void_p), ("features", C.c_void_p), ("agg_cols", C.c_void_p),
-                ("vram_slot", C.c_int32), ("vram_cap", C.c_float), ("weights", C.c_void_p)]
+                ("vram_slot", C.c_int32), ("vram_cap", C.c_float), ("weights", C.c_void_p),
+                ("obj", C.c_void_p)]
 
 
 class _Result(C.Structure):
@@ -88,9 +98,13 @@ def _ptr(a: np.ndarray):
 
 
 class Problem:
-    """Holds contiguous copies of an instance's arrays and the C descriptor."""
+    """Holds contiguous copies of an instance's arrays and the C descriptor.
+    `objective` (optional): an object with the arrays of the full utility of
+    Eq. 3 (variant [sum K], fmin/fmax/quality [N][4], reload_cost [N],
+    prev_variant [N], tau [N]) and alpha, beta, delta; None selects the
+    linear objective."""
 
-    def __init__(self, inst):
+    def __init__(self, inst, objective=None):
         self.n_options = np.ascontiguousarray(inst.n_options, dtype=np.int32)
         self.features = np.ascontiguousarray(inst.features, dtype=np.float32)
         self.agg_cols = np.ascontiguousarray(inst.agg_cols, dtype=np.int32)
@@ -100,7 +114,19 @@ class Problem:
                        int(inst.hidden2), 1 if inst.dtype == "bf16" else 0,
                        _ptr(self.n_options).value, _ptr(self.features).value,
                        _ptr(self.agg_cols).value, int(inst.vram_slot),
-                       float(inst.vram_cap), _ptr(self.weights).value)
+                       float(inst.vram_cap), _ptr(self.weights).value, None)
+        self.obj = None
+        if objective is not None:
+            o = objective
+            self._oa = [np.ascontiguousarray(o.variant, np.int32),
+                        np.ascontiguousarray(o.fmin, np.float32).reshape(self.N, MAX_VARIANTS),
+                        np.ascontiguousarray(o.fmax, np.float32).reshape(self.N, MAX_VARIANTS),
+                        np.ascontiguousarray(o.quality, np.float32).reshape(self.N, MAX_VARIANTS),
+                        np.ascontiguousarray(o.reload_cost, np.float32),
+                        np.ascontiguousarray(o.prev_variant, np.int32),
+                        np.ascontiguousarray(o.tau, np.float32)]
+            self.obj = _Obj(*[_ptr(a).value for a in self._oa], float(o.alpha), float(o.beta), float(o.delta))
+            self.c.obj = C.addressof(self.obj)
         self.ref = C.byref(self.c)
 
     @property

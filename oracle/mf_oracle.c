@@ -23,6 +23,16 @@
  *   Decision (Section II): lambda* = argmax J; here J = sum_i omega_i thr_i,
  *     ties broken to the lowest linear index, top-k sorted by (J desc,
  *     index asc).
+ *   Full utility (Section II, Eq. 3, when an objective block is given): with
+ *     v the variant of model i's option, the normalised throughput is
+ *     f_i = (thr_i - fmin_{i,v}) / (fmax_{i,v} - fmin_{i,v}) (per-variant
+ *     min-max scaling); J = sum_i omega_i Q_{i,v} f_i
+ *     - alpha sum_i eta_i c_i - beta sum_i max(0, tau_i + delta - f_i)^2,
+ *     eta_i = 1 when model i changes variant from the previous step; the
+ *     floor f_i >= tau_i joins the hard constraints (constraint after Eq. 3).
+ *     Each model's term is evaluated in fp64 in this order: Rg = fmax - fmin,
+ *     f = (thr - fmin) / Rg, q = Q f, J = fma(omega, q, J), J = J - alpha c
+ *     (variant changed), d = (tau + delta) - f, J = J - beta (d d) if d > 0.
  *
  * Precision: every floating-point step is fp64.  Each dot product is one
  * fused multiply-add chain in ascending input order, starting from the bias;
@@ -158,8 +168,9 @@ double *orc_weights_f64(const orc_instance *in)
 }
 
 /* Full evaluation of one joint configuration.
- * flags: bit0 VRAM ok, bit1 every latency bound met, bit2 feasible,
- *        bit3 aggregate exact; bit (8+i): model i misses its latency bound. */
+ * flags: bit0 VRAM ok, bit1 every service constraint met (latency bounds;
+ *        with an objective block also the throughput floors), bit2 feasible,
+ *        bit3 aggregate exact; bit (8+i): model i misses one of them. */
 void orc_eval_w(const orc_instance *in, const double *w64, uint64_t idx,
                      const float *sla, const float *omega, double *lat, double *thr,
                      double *J, uint32_t *flags, double *scratch)
@@ -186,11 +197,34 @@ void orc_eval_w(const orc_instance *in, const double *w64, uint64_t idx,
         if (!(y[0] <= (double)sla[i])) { sla_ok = 0; f |= 1u << (8 + i); }
         off += in->n_options[i];
     }
+    const orc_objective *ob = in->obj;
+    double jq = 0.0;   /* Eq. 3 utility, model by model */
+    if (ob) {
+        int64_t row0 = 0;
+        for (int i = 0; i < N; i++) {
+            const int v = ob->variant[row0 + d[i]];
+            const double fmin = (double)ob->fmin[i * ORC_MAX_VARIANTS + v];
+            const double rg = (double)ob->fmax[i * ORC_MAX_VARIANTS + v] - fmin;
+            const double fn = (thr[i] - fmin) / rg;                  /* per-variant min-max scaling */
+            if (!(fn >= (double)ob->tau[i])) { sla_ok = 0; f |= 1u << (8 + i); }   /* throughput floor */
+            const double q = (double)ob->quality[i * ORC_MAX_VARIANTS + v] * fn;
+            jq = fma((double)omega[i], q, jq);
+            if (ob->prev_variant[i] >= 0 && v != ob->prev_variant[i])       /* eta_i = 1: reload */
+                jq = jq - (double)ob->alpha * (double)ob->reload_cost[i];
+            const double dd = ((double)ob->tau[i] + (double)ob->delta) - fn;
+            if (dd > 0.0) jq = jq - (double)ob->beta * (dd * dd);     /* soft SLA penalty */
+            row0 += in->n_options[i];
+        }
+    }
     int feas = vram_ok && sla_ok;
     double j = -INFINITY;
     if (feas) {
-        j = 0.0;
-        for (int i = 0; i < N; i++) j = fma((double)omega[i], thr[i], j);
+        if (ob) {
+            j = jq;
+        } else {
+            j = 0.0;
+            for (int i = 0; i < N; i++) j = fma((double)omega[i], thr[i], j);
+        }
     }
     f |= (uint32_t)vram_ok | ((uint32_t)sla_ok << 1) | ((uint32_t)feas << 2) | ((uint32_t)exact << 3);
     *J = j;

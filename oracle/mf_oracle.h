@@ -8,6 +8,20 @@
 #define ORC_MAX_MODELS 16
 #define ORC_MAX_TOPK 64
 #define ORC_MAX_AGG 16
+#define ORC_MAX_VARIANTS 4
+
+/* The full utility of Section II (Eq. 3) with the throughput floor of the
+ * constraint after it; NULL in orc_instance selects J = sum_i omega_i thr_i
+ * with the latency bounds as the only service constraint. */
+typedef struct {
+    const int32_t *variant;       /* [sum K] variant of each option row */
+    const float *fmin, *fmax;     /* [N][ORC_MAX_VARIANTS] per-variant throughput extremes */
+    const float *quality;         /* [N][ORC_MAX_VARIANTS] Q of each variant */
+    const float *reload_cost;     /* [N] c_i^rel */
+    const int32_t *prev_variant;  /* [N] variant deployed at the previous step, -1 for none */
+    const float *tau;             /* [N] floor on the normalised throughput (-inf: none) */
+    float alpha, beta, delta;
+} orc_objective;
 
 typedef struct {
     int32_t n_models, n_local, n_agg, hidden1, hidden2, bf16;
@@ -17,6 +31,7 @@ typedef struct {
     int32_t vram_slot;
     float vram_cap;
     const float *weights;       /* [N][stride]: W1[h1][L+A] b1[h1] W2[h2][h1] b2[h2] W3[2][h2] b3[2] */
+    const orc_objective *obj;   /* NULL: linear objective */
 } orc_instance;
 
 typedef struct {

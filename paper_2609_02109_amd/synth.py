@@ -259,6 +259,83 @@ def cfg4(seed=0) -> Instance:
                          dtype="bf16", top_k=64, name="n8_k16_h256_bf16")
 
 
+# ---------------------------------------------------------------------------
+# Variant metadata of the full utility (Section II, Eq. 3)
+# ---------------------------------------------------------------------------
+
+MAX_VARIANTS = 4
+Q_LLM = (1.000, 0.979)           # FP16, AWQ (relative perplexity)
+Q_VIS = (0.73, 0.96, 1.00)       # YOLO11 n, s, m (mAP50-95, best = 1)
+RELOAD_LLM, RELOAD_VIS = 30.0, 5.0
+
+
+@dataclass
+class Objective:
+    variant: np.ndarray          # int32 [sum K]: variant of each option row
+    n_variants: np.ndarray       # int32 [N]
+    fmin: np.ndarray             # float32 [N][4]: per-variant throughput extremes
+    fmax: np.ndarray             # float32 [N][4]
+    quality: np.ndarray          # float32 [N][4]
+    reload_cost: np.ndarray      # float32 [N]
+    prev_variant: np.ndarray     # int32 [N]: variant deployed at the previous step (-1: none)
+    tau: np.ndarray              # float32 [N]: floor on the normalised throughput
+    alpha: float = 1.0 / 60.0
+    beta: float = 5.0
+    delta: float = 0.05
+
+
+def make_objective(inst: Instance, seed: int = 0, tau_range=(0.2, 0.35), with_prev=True) -> Objective:
+    """Draw the variant metadata for `inst`.  An option set is variants x
+    runtime parameters (Section II), so option o of a model with K options
+    and V variants belongs to variant (o V) // K.  LLMs have two variants,
+    vision models three, with the quality values and reload costs the paper
+    reports; the per-variant throughput extremes (profiling data in the paper)
+    and the floors tau (a percentile of profiled performance in the paper)
+    are drawn here around the surrogates' output scale."""
+    rng = np.random.Generator(np.random.PCG64(seed * 7919 + 17))
+    N = inst.n_models
+    K = [int(k) for k in inst.n_options]
+    variant = np.zeros(int(sum(K)), np.int32)
+    nv = np.zeros(N, np.int32)
+    fmin = np.zeros((N, MAX_VARIANTS), np.float32)
+    fmax = np.ones((N, MAX_VARIANTS), np.float32)
+    qual = np.zeros((N, MAX_VARIANTS), np.float32)
+    cost = np.zeros(N, np.float32)
+    prev = np.full(N, -1, np.int32)
+    off = 0
+    for i in range(N):
+        llm = int(inst.model_type[i]) == 0
+        q = Q_LLM if llm else Q_VIS
+        V = min(len(q), K[i])
+        nv[i] = V
+        for o in range(K[i]):
+            variant[off + o] = (o * V) // K[i]
+        for v in range(V):
+            qual[i, v] = q[len(q) - V + v]
+            fmin[i, v] = _quantise(rng.uniform(-2.0, -1.0))
+            fmax[i, v] = _quantise(rng.uniform(1.0, 2.0))
+        cost[i] = RELOAD_LLM if llm else RELOAD_VIS
+        if with_prev:
+            prev[i] = variant[off + int(rng.integers(0, K[i]))]
+        off += K[i]
+    tau = rng.uniform(tau_range[0], tau_range[1], N).astype(np.float32)
+    return Objective(variant=variant, n_variants=nv, fmin=fmin, fmax=fmax, quality=qual, reload_cost=cost,
+                     prev_variant=prev, tau=tau)
+
+
+def linear_objective(inst: Instance) -> Objective:
+    """Metadata under which the full utility equals sum_i omega_i thr_i and
+    no floor binds: one variant, Q = 1, extremes (0, 1), no reload, no
+    penalty."""
+    N = inst.n_models
+    fmax = np.ones((N, MAX_VARIANTS), np.float32)
+    return Objective(variant=np.zeros(int(np.sum(inst.n_options)), np.int32), n_variants=np.ones(N, np.int32),
+                     fmin=np.zeros((N, MAX_VARIANTS), np.float32), fmax=fmax,
+                     quality=np.ones((N, MAX_VARIANTS), np.float32), reload_cost=np.zeros(N, np.float32),
+                     prev_variant=np.full(N, -1, np.int32), tau=np.full(N, -np.inf, np.float32),
+                     alpha=0.0, beta=0.0, delta=0.0)
+
+
 @dataclass
 class GAScenarios:
     sla: np.ndarray      # float32 [S][N]
