@@ -76,9 +76,26 @@ typedef enum { MF_F32 = 0, MF_BF16 = 1 } mf_dtype;
 
 typedef struct mf_problem mf_problem;   /* opaque */
 
+#define MF_MAX_VARIANTS 4
+
+/* Variant metadata of the full utility (Section II, Eq. 3): an option set is
+ * variants x runtime parameters, and each variant v of model i carries the
+ * throughput extremes observed for it (f_i is min-max scaled per variant), a
+ * quality Q, and model i a reload cost c_i.  Host arrays, copied at creation.
+ * Validation: 1 <= n_variants[i] <= MF_MAX_VARIANTS, 0 <= variant < n_variants,
+ * fmin < fmax, all values finite, reload costs >= 0; else MF_EINVAL. */
+typedef struct {
+    const int32_t *h_variant;      /* [sum K_i] variant of each option row */
+    const int32_t *h_n_variants;   /* [N] */
+    const float *h_fmin;           /* [N][MF_MAX_VARIANTS] */
+    const float *h_fmax;           /* [N][MF_MAX_VARIANTS] */
+    const float *h_quality;        /* [N][MF_MAX_VARIANTS] */
+    const float *h_reload_cost;    /* [N] */
+} mf_variants;
+
 /* Problem shape.  Supported: 1 <= n_models <= 16; 1 <= n_options[i] <= 255;
- * n_local >= 1; n_agg in {2,4,6,8}; hidden1 == hidden2 in {32, 64} for MF_F32.
- * (Other shapes return MF_EUNSUPPORTED.) */
+ * n_local >= 1; n_agg in {2,4,6,8}; hidden1 == hidden2 in {32, 64} for MF_F32,
+ * in {64, 128, 256} for MF_BF16.  (Other shapes return MF_EUNSUPPORTED.) */
 typedef struct {
     int32_t n_models;           /* N */
     int32_t n_local;            /* L: local features per option row */
@@ -89,6 +106,7 @@ typedef struct {
     int32_t vram_slot;          /* aggregate slot compared with vram_cap, in [0, A) */
     float vram_cap;             /* finite */
     mf_dtype dtype;
+    const mf_variants *variants; /* NULL: only the linear objective is available */
 } mf_desc;
 
 /* Create a problem.  d_features: float [sum K_i][L].  d_weights: float
@@ -114,25 +132,51 @@ mf_status mf_decode(const mf_problem *p, uint64_t idx, int32_t *h_digits);
 
 #define MF_DUMP 1u   /* write d_mask and d_pred for every index of [lo, hi) */
 
+typedef enum {
+    MF_OBJ_LINEAR = 0,  /* J = sum_i omega_i thr_i (Section II with unit quality) */
+    MF_OBJ_EQ3 = 1      /* the full utility of Eq. 3 with the throughput floor (needs mf_desc.variants) */
+} mf_objective_kind;
+
+/* Objective of a search.  MF_OBJ_EQ3 (Section II, Eq. 3 and the constraint
+ * after it), with v the variant of model i's option:
+ *   f_i = (thr_i - fmin_{i,v}) / (fmax_{i,v} - fmin_{i,v})
+ *   J   = sum_i omega_i Q_{i,v} f_i - alpha sum_i eta_i c_i
+ *         - beta sum_i max(0, tau_i + delta - f_i)^2,
+ *   eta_i = 1 iff prev_variant[i] >= 0 and v != prev_variant[i];
+ * feasible additionally requires f_i >= tau_i (tau_i = -inf: no floor).
+ * Canonical evaluation per model, in fp64 and in this order: Rg = fmax - fmin,
+ * f = (thr - fmin) / Rg, q = Q f, J = fma(omega, q, J), J = J - alpha c (if
+ * eta), d = (tau + delta) - f, J = J - beta (d d) (if d > 0).  The latency
+ * bounds d_sla still apply (pass +inf to drop them).  Validation: alpha, beta,
+ * delta finite, beta >= 0; tau not NaN or +inf; -1 <= prev_variant[i] < n_variants[i]. */
+typedef struct {
+    int32_t kind;                           /* mf_objective_kind */
+    float alpha, beta, delta;
+    float tau[MF_MAX_MODELS];
+    int32_t prev_variant[MF_MAX_MODELS];
+} mf_objective;
+
 typedef struct {
     uint64_t lo, hi;           /* half-open index range, lo <= hi <= |Lambda| */
     int32_t top_k;             /* 1..64 */
     uint32_t flags;            /* MF_DUMP */
-    const float *d_sla;        /* device [N] latency bound per model, finite */
+    const float *d_sla;        /* device [N] latency bound per model (+inf: none) */
     const float *d_omega;      /* device [N] objective weight per model, finite */
     /* MF_DUMP outputs (device, hi - lo <= 2^31 entries):
-     *   d_mask[t]: bit0 VRAM ok, bit1 every latency bound met, bit2 feasible,
-     *              bit3 the fast path left a latency decision to the
+     *   d_mask[t]: bit0 VRAM ok, bit1 every service constraint met (latency
+     *              bounds; throughput floors under MF_OBJ_EQ3), bit2 feasible,
+     *              bit3 the fast path left a service decision to the
      *              canonical re-evaluation;
      *   d_pred[(t*N + i)*2 + {0,1}]: fast-path fp32 (lat, thr) of model i. */
     uint8_t *d_mask;
     float *d_pred;
+    mf_objective objective;    /* zero-initialised: MF_OBJ_LINEAR */
 } mf_search_args;
 
 typedef struct {
     uint64_t n_eval;           /* hi - lo */
     uint64_t n_vram;           /* VRAM-feasible configurations */
-    uint64_t n_feas;           /* feasible (VRAM and every latency bound) */
+    uint64_t n_feas;           /* feasible (VRAM and every service constraint) */
     uint64_t n_flagged;        /* configurations re-evaluated canonically for a latency decision */
     uint64_t n_topk_collect;   /* candidates gathered by the top-k fallback pass (0 if none ran) */
     int32_t n_top;             /* min(top_k, n_feas) */

@@ -37,6 +37,10 @@ struct mf_problem {
     int32_t *d_agg_cols = nullptr, *d_row_model = nullptr;
     FastLayout lay{};
     FastConst fc{};
+    // variant metadata of the full utility (Eq. 3)
+    bool has_var = false;
+    std::vector<int32_t> n_var;
+    float4 *d_vrow = nullptr;    // [sumK][2]: (fmin, fmax, 1/range, Q), (variant bits, reload cost, 0, 0)
     // bf16 fast path
     bool bf_ok = false;
     Bf16Layout blay{};
@@ -369,6 +373,21 @@ void empty_result(mf_result &r)
     }
 }
 
+ObjArgs obj_args(const mf_problem *p, const mf_objective &o)
+{
+    ObjArgs a{};
+    a.kind = o.kind;
+    a.alpha = o.alpha;
+    a.beta = o.beta;
+    a.delta = o.delta;
+    for (int i = 0; i < kMaxN; i++) {
+        a.tau[i] = i < p->N ? o.tau[i] : 0.f;
+        a.prev[i] = i < p->N ? o.prev_variant[i] : -1;
+    }
+    a.vrow = p->d_vrow;
+    return a;
+}
+
 // Launch the fast kernel of the problem's path (fp32 or bf16) over the range,
 // list or collect pass described by fa.
 hipError_t launch_fast_path(const mf_problem *p, const FastArgs &fa, int grid, int kp, int mode, hipStream_t s)
@@ -394,6 +413,7 @@ hipError_t launch_fast_path(const mf_problem *p, const FastArgs &fa, int grid, i
     ba.wg_lists = fa.wg_lists;
     ba.mask = fa.mask;
     ba.pred = fa.pred;
+    ba.obj = fa.obj;
     return launch_bf16_impl(ba, p->fc, p->bcst, grid, kp, mode, s);
 }
 
@@ -435,6 +455,7 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     fa.wg_lists = lists;
     fa.mask = dump ? args->d_mask + dump_off : nullptr;
     fa.pred = dump ? args->d_pred + dump_off * (uint64_t)p->N * 2u : nullptr;
+    fa.obj = obj_args(p, args->objective);
 
     CanonArgs ca{};
     ca.n_models = p->N; ca.L = p->L; ca.A = p->A; ca.H1 = p->H1; ca.H2 = p->H2; ca.bf16 = p->bf16;
@@ -449,6 +470,7 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     ca.res = R; ca.top_k = args->top_k; ca.collect_mode = 0;
     ca.ent_J = entJ; ca.ent_flags = entF;
     ca.mask = fa.mask;
+    ca.obj = fa.obj;
 
     SelectArgs sa{};
     sa.top_k = args->top_k; sa.kp = w.kp; sa.cand_keys = cand; sa.work = work; sa.collect = collect;
@@ -626,6 +648,41 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
         return MF_EINVAL;
     }
     if (!all_finite(F) || !all_finite(W)) { delete p; return MF_EINVAL; }
+    std::vector<float> vrow;
+    if (desc->variants) {
+        const mf_variants *mv = desc->variants;
+        if (!mv->h_variant || !mv->h_n_variants || !mv->h_fmin || !mv->h_fmax || !mv->h_quality ||
+            !mv->h_reload_cost) { delete p; return MF_EINVAL; }
+        p->n_var.assign(mv->h_n_variants, mv->h_n_variants + N);
+        vrow.assign((size_t)sumK * 8, 0.f);
+        for (int i = 0; i < N; i++) {
+            const int nv = p->n_var[i];
+            const float c = mv->h_reload_cost[i];
+            if (nv < 1 || nv > MF_MAX_VARIANTS || !std::isfinite(c) || c < 0.f) { delete p; return MF_EINVAL; }
+            for (int v = 0; v < nv; v++) {
+                const float lo = mv->h_fmin[i * MF_MAX_VARIANTS + v], hi = mv->h_fmax[i * MF_MAX_VARIANTS + v];
+                const float q = mv->h_quality[i * MF_MAX_VARIANTS + v];
+                if (!std::isfinite(lo) || !std::isfinite(hi) || !std::isfinite(q) || !(lo < hi) ||
+                    !std::isfinite((double)hi - (double)lo) || !std::isfinite(1.0 / ((double)hi - (double)lo))) {
+                    delete p;
+                    return MF_EINVAL;
+                }
+            }
+            for (int o = 0; o < p->K[i]; o++) {
+                const int r = p->opt_off[i] + o, v = mv->h_variant[r];
+                if (v < 0 || v >= nv) { delete p; return MF_EINVAL; }
+                const float lo = mv->h_fmin[i * MF_MAX_VARIANTS + v], hi = mv->h_fmax[i * MF_MAX_VARIANTS + v];
+                float *e = vrow.data() + (size_t)r * 8;
+                e[0] = lo;
+                e[1] = hi;
+                e[2] = (float)(1.0 / ((double)hi - (double)lo));
+                e[3] = mv->h_quality[i * MF_MAX_VARIANTS + v];
+                std::memcpy(&e[4], &v, 4);
+                e[5] = c;
+            }
+        }
+        p->has_var = true;
+    }
     if (p->bf16) {
         for (int i = 0; i < N; i++) {
             const float *w = W.data() + (int64_t)i * p->wstride;
@@ -674,7 +731,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
         ly.off_g = o; o += sumK * ly.AP;
         ly.off_c = o; o += 8;
         ly.total_floats = (o + 3) & ~3;
-        const size_t lds = (size_t)ly.total_floats * 4 + 64 * 4 + (size_t)kSearchWaves * 64 * 8;
+        const size_t lds = (size_t)ly.total_floats * 4 + kFastPar * 4 + (size_t)kSearchWaves * 64 * 8;
         if (lds > 163840) p->fast_ok = false;
     }
     if (p->fast_ok) {
@@ -828,6 +885,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     const size_t o_bm = off; off = align256(off + bimg.size() * 4);
     const size_t o_bg = off; off = align256(off + bg.size() * 4);
     const size_t o_ph = off; off = align256(off + (p->bf_ok ? (size_t)sumK * bl.PST * 4 : 0));
+    const size_t o_vr = off; off = align256(off + vrow.size() * 4);
     if (hipMalloc(&p->d_mem, off) != hipSuccess) { delete p; return MF_ENOMEM; }
     char *base = (char *)p->d_mem;
     p->d_image = reinterpret_cast<float4 *>(base + o_img);
@@ -841,6 +899,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     p->d_bmodels = reinterpret_cast<float4 *>(base + o_bm);
     p->d_bg = reinterpret_cast<float4 *>(base + o_bg);
     p->d_phat = reinterpret_cast<float *>(base + o_ph);
+    p->d_vrow = reinterpret_cast<float4 *>(base + o_vr);
     std::vector<double> w64(W.begin(), W.end());
     bool ok = true;
     ok = ok && hipMemsetAsync(p->d_zeros, 0, 64 * 4, s) == hipSuccess;
@@ -853,6 +912,8 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     ok = ok && hipMemcpyAsync(p->d_w64, w64.data(), w64.size() * 8, hipMemcpyHostToDevice, s) == hipSuccess;
     if (!bimg.empty()) ok = ok && hipMemcpyAsync(p->d_bmodels, bimg.data(), bimg.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
     if (!bg.empty()) ok = ok && hipMemcpyAsync(p->d_bg, bg.data(), bg.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
+    if (!vrow.empty())
+        ok = ok && hipMemcpyAsync(p->d_vrow, vrow.data(), vrow.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
     if (ok && p->bf_ok)
         ok = launch_precompute_phat(p->d_features, p->d_canon, sumK, L, A, H, p->wstride, p->d_row_model, p->d_phat,
                                     bl.PST, s) == hipSuccess;
@@ -903,6 +964,17 @@ static mf_status check_search_args(const mf_problem *p, const mf_search_args *a)
     if (a->flags & ~MF_DUMP) return MF_EINVAL;
     if ((a->flags & MF_DUMP) && (!a->d_mask || !a->d_pred || a->hi - a->lo > (1ull << 31))) return MF_EINVAL;
     if (!p->fast_ok && !p->bf_ok) return MF_EUNSUPPORTED;
+    const mf_objective &o = a->objective;
+    if (o.kind != MF_OBJ_LINEAR && o.kind != MF_OBJ_EQ3) return MF_EINVAL;
+    if (o.kind == MF_OBJ_EQ3) {
+        if (!p->has_var) return MF_EINVAL;
+        if (!std::isfinite(o.alpha) || !std::isfinite(o.beta) || !std::isfinite(o.delta) || o.beta < 0.f)
+            return MF_EINVAL;
+        for (int i = 0; i < p->N; i++) {
+            if (std::isnan(o.tau[i]) || o.tau[i] == INFINITY) return MF_EINVAL;
+            if (o.prev_variant[i] < -1 || o.prev_variant[i] >= p->n_var[i]) return MF_EINVAL;
+        }
+    }
     return MF_OK;
 }
 

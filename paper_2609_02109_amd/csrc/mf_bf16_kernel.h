@@ -125,7 +125,8 @@ __device__ __forceinline__ void layer3_row(const floatx16 &acc, int r, const flo
 // FULL: the problem has exactly MAXN models, each with more than one option
 // (no per-model range checks, no special case in the decode).
 // LIST: evaluate the configurations of args.idx_list (predictions only).
-template <int MAXN, int A, int H, bool FULL, bool LIST>
+// OBJ: score with the full utility of Eq. 3 (otherwise the linear objective).
+template <int MAXN, int A, int H, bool FULL, bool LIST, bool OBJ>
 __global__ void __launch_bounds__(kBf16Waves * 64, 1)
 fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, const int mode, const int kp)
 {
@@ -139,9 +140,11 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
     const int N = FULL ? MAXN : fc.n_models;
     float *G = smem + CL.model_floats;            // [sumK][half][4]: slot 2s+half at [half][s]
     float *Gv = G + Ly.sumK * 8;                   // [sumK] VRAM column
-    float *par = Gv + Ly.gv_floats;                // [0,16) sla [16,32) |thr| bound [32,48) omega [48,64) rows
+    // [0,16) sla [16,32) |thr| bound [32,48) omega [48,64) rows [64,80) floor tau [80,96) previous variant
+    float *par = Gv + Ly.gv_floats;
     int *par_off = reinterpret_cast<int *>(par + 48);
-    unsigned long long *lst = reinterpret_cast<unsigned long long *>(par + 64);
+    int *par_prev = reinterpret_cast<int *>(par + 80);
+    unsigned long long *lst = reinterpret_cast<unsigned long long *>(par + kBf16Par);
 
     for (int t = threadIdx.x; t < (Ly.sumK * 8 + Ly.gv_floats) / 4; t += blockDim.x)
         reinterpret_cast<float4 *>(G)[t] = args.g_image[t];
@@ -152,9 +155,14 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
             par[16 + i] = bc.mag_thr[i];
             par[32 + i] = args.omega[i];
             par_off[i] = fc.opt_off[i];
+            if constexpr (OBJ) {
+                par[64 + i] = args.obj.tau[i];
+                par_prev[i] = args.obj.prev[i];
+            }
         }
     }
     __syncthreads();
+    constexpr bool eq3 = OBJ;
 
     const int lane = threadIdx.x & 63, half = lane >> 5, col = lane & 31;
     const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -214,6 +222,8 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
             const float k0l = cst[2], k0t = cst[3], cbl = cst[4], cbt = cst[5], rml = cst[6], rmt = cst[7];
             const float m3l = cst[8], m3t = cst[9];
             const float sla_i = par[i], om_i = par[32 + i];
+            const float tau_i = OBJ ? par[64 + i] : 0.f;
+            const int prev_i = OBJ ? par_prev[i] : -1;
             const uint32_t row0 = (uint32_t)par_off[i];
 
             for (int t = 0; t < TW; t++) {
@@ -347,11 +357,22 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
                 const float el = (k0l + bc.g2 * (cbl + rml * sh * 1.001f) + bc.g3 * m3l * s2) * 1.001f + 1e-30f;
                 const float et = (k0t + bc.g2 * (cbt + rmt * sh * 1.001f) + bc.g3 * m3t * s2) * 1.001f + 1e-30f;
                 const float slack = el + (fabsf(lat) + fabsf(sla_i)) * 0x1p-20f;
-                const bool pass = lat + slack <= sla_i, fail = lat - slack > sla_i;
+                bool pass = lat + slack <= sla_i, fail = lat - slack > sla_i;
+                float jn, en;
+                if constexpr (eq3) {
+                    const Eq3Term q3 = eq3_term(args.obj.vrow[2 * row], args.obj.vrow[2 * row + 1], thr, et, om_i,
+                                                tau_i, prev_i, args.obj.alpha, args.obj.beta, args.obj.delta);
+                    pass = pass && q3.pass;
+                    fail = fail || q3.fail;
+                    jn = Jt[0] + q3.c;
+                    // the fp32 sum over models: N u relative to each term's magnitude
+                    en = Et[0] + q3.e + q3.mag * (float)N * 0x1p-22f;
+                } else {
+                    jn = fmaf(om_i, thr, Jt[0]);
+                    en = Et[0] + fabsf(om_i) * (et + bc.gN * fabsf(thr));
+                }
                 uint32_t fl = Ft[0] | (fail ? kFlagFail : 0u) | ((pass || fail) ? 0u : (1u << i));
                 if (i == 0 && (double)vsum <= (double)fc.vram_cap) fl |= kFlagVram;
-                const float jn = fmaf(om_i, thr, Jt[0]);
-                const float en = Et[0] + fabsf(om_i) * (et + bc.gN * fabsf(thr));
                 // rotate the per-tile state: slot 0 becomes the next tile
 #pragma unroll
                 for (int u = 0; u < TW - 1; u++) { Jt[u] = Jt[u + 1]; Et[u] = Et[u + 1]; Ft[u] = Ft[u + 1]; }
@@ -422,12 +443,12 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
     }
 }
 
-template <int MAXN, int A, int H, bool FULL, bool LIST>
+template <int MAXN, int A, int H, bool FULL, bool LIST, bool OBJ>
 hipError_t launch_bf16_t(const Bf16Args &a, const FastConst &fc, const Bf16Const &bc, int grid, int kp, int mode,
                          hipStream_t s)
 {
     const size_t lds = bf16_lds_bytes(a.lay, kp);
-    auto fn = fast_bf16_kernel<MAXN, A, H, FULL, LIST>;
+    auto fn = fast_bf16_kernel<MAXN, A, H, FULL, LIST, OBJ>;
     hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(grid), dim3(kBf16Waves * 64), lds, s, a, fc, bc, mode, kp);
@@ -435,7 +456,8 @@ hipError_t launch_bf16_t(const Bf16Args &a, const FastConst &fc, const Bf16Const
 }
 
 // Instantiations for one hidden width: search/collect kernels for up to 8 and
-// up to 16 models (with exact-count variants), list kernels for up to 16.
+// up to 16 models (with exact-count variants), list kernels for up to 16;
+// under the full utility of Eq. 3 the exact-8 kernel and the generic one.
 template <int H>
 hipError_t launch_bf16_for_width(const Bf16Args &a, const FastConst &fc, const Bf16Const &bc, int grid, int kp,
                                  int mode, hipStream_t s)
@@ -443,13 +465,18 @@ hipError_t launch_bf16_for_width(const Bf16Args &a, const FastConst &fc, const B
     const int N = fc.n_models, A = a.lay.A;
     bool multi = true;   // every option count exceeds 1
     for (int j = 0; j < N; j++) multi = multi && fc.K[j] > 1;
-#define MF_BF_CASE(AA)                                                                                   \
-    if (A == AA) {                                                                                       \
-        if (mode == kModeList) return launch_bf16_t<16, AA, H, false, true>(a, fc, bc, grid, kp, mode, s); \
-        if (N == 8 && multi) return launch_bf16_t<8, AA, H, true, false>(a, fc, bc, grid, kp, mode, s);             \
-        if (N <= 8) return launch_bf16_t<8, AA, H, false, false>(a, fc, bc, grid, kp, mode, s);             \
-        if (N == 16 && multi) return launch_bf16_t<16, AA, H, true, false>(a, fc, bc, grid, kp, mode, s);           \
-        return launch_bf16_t<16, AA, H, false, false>(a, fc, bc, grid, kp, mode, s);                       \
+    const bool obj = a.obj.kind != 0;
+#define MF_BF_CASE(AA)                                                                                          \
+    if (A == AA) {                                                                                              \
+        if (mode == kModeList) return launch_bf16_t<16, AA, H, false, true, false>(a, fc, bc, grid, kp, mode, s); \
+        if (obj) {                                                                                              \
+            if (N == 8 && multi) return launch_bf16_t<8, AA, H, true, false, true>(a, fc, bc, grid, kp, mode, s);  \
+            return launch_bf16_t<16, AA, H, false, false, true>(a, fc, bc, grid, kp, mode, s);                  \
+        }                                                                                                       \
+        if (N == 8 && multi) return launch_bf16_t<8, AA, H, true, false, false>(a, fc, bc, grid, kp, mode, s);     \
+        if (N <= 8) return launch_bf16_t<8, AA, H, false, false, false>(a, fc, bc, grid, kp, mode, s);            \
+        if (N == 16 && multi) return launch_bf16_t<16, AA, H, true, false, false>(a, fc, bc, grid, kp, mode, s);  \
+        return launch_bf16_t<16, AA, H, false, false, false>(a, fc, bc, grid, kp, mode, s);                      \
     }
     MF_BF_CASE(2) MF_BF_CASE(4) MF_BF_CASE(6) MF_BF_CASE(8)
 #undef MF_BF_CASE

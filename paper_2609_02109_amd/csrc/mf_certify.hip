@@ -45,7 +45,17 @@ canon_kernel(const CanonArgs a, const int search_mode)
     __shared__ double zs[kCanonMaxIn];
     __shared__ int32_t ds[kMaxN];
     __shared__ float aggs[16];
+    __shared__ float s_tau[kMaxN];
+    __shared__ int32_t s_prev[kMaxN];
     const int lane = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < kMaxN; i++)   // compile-time index into the argument block
+        if (lane == i) {
+            s_tau[i] = a.obj.tau[i];
+            s_prev[i] = a.obj.prev[i];
+        }
+    __syncthreads();
+    const bool eq3 = a.obj.kind != 0;
     const int N = a.n_models, L = a.L, A = a.A, H1 = a.H1, H2 = a.H2, nin = L + A;
 
     int64_t n_cand = 0, n_work = 0, n_coll = 0, n_ent, e0 = 0;
@@ -151,7 +161,24 @@ canon_kernel(const CanonArgs a, const int search_mode)
             }
             const double lat = __shfl(y, 0), thr = __shfl(y, 1);
             if (!(lat <= (double)a.sla[i])) { sla_ok = false; fl |= 1u << (8 + i); }
-            J = fma((double)a.omega[i], thr, J);
+            if (eq3) {
+                // Eq. 3 (Section II): per-variant min-max throughput, quality,
+                // reload penalty, soft SLA penalty; the throughput floor
+                const int64_t row = (int64_t)a.opt_off[i] + ds[i];
+                const float4 r0 = a.obj.vrow[2 * row], r1 = a.obj.vrow[2 * row + 1];
+                const int var = __float_as_int(r1.x);
+                const double fmin = (double)r0.x;
+                const double rg = (double)r0.y - fmin;
+                const double f = (thr - fmin) / rg;
+                if (!(f >= (double)s_tau[i])) { sla_ok = false; fl |= 1u << (8 + i); }
+                const double q = (double)r0.w * f;
+                J = fma((double)a.omega[i], q, J);
+                if (s_prev[i] >= 0 && var != s_prev[i]) J = J - (double)a.obj.alpha * (double)r1.y;
+                const double dd = ((double)s_tau[i] + (double)a.obj.delta) - f;
+                if (dd > 0.0) J = J - (double)a.obj.beta * (dd * dd);
+            } else {
+                J = fma((double)a.omega[i], thr, J);
+            }
             if (a.pred && lane == 0) {
                 a.pred[(e * N + i) * 2 + 0] = lat;
                 a.pred[(e * N + i) * 2 + 1] = thr;

@@ -21,6 +21,53 @@ __device__ inline double bound_eJ(const FastConst &fc, const float *omega)
     return (e + m * 0x1p-48) * (1.0 + 0x1p-20) + 1e-30;
 }
 
+// Fast-path term of the full utility (Section II, Eq. 3) for one model.
+// r0 = (fmin, fmax, 1/(fmax - fmin) in fp32, Q), r1 = (variant bits, reload
+// cost); thr is the fast fp32 throughput and e_thr a bound on its distance
+// from the canonical one.  Returns the term c (omega Q f - alpha c eta -
+// beta max(0, tau + delta - f)^2 in fp32), e with |c - canonical term| <= e,
+// mag >= |c| (for the rounding of the sum over models), and the floor
+// decision f >= tau: pass / fail when the bound settles it.
+struct Eq3Term {
+    float c, e, mag;
+    bool pass, fail;
+};
+
+__device__ __forceinline__ Eq3Term eq3_term(const float4 r0, const float4 r1, float thr, float e_thr, float omega,
+                                            float tau, int prev, float alpha, float beta, float delta)
+{
+    const float fmin = r0.x, inv = r0.z, Q = r0.w;
+    const int var = __float_as_int(r1.x);
+    const float num = thr - fmin;
+    const float f = num * inv;
+    // the throughput error through 1/range, and the fp32 rounding of the
+    // subtraction, of 1/range and of the product (3 u relative < 2^-22)
+    const float e_f = (e_thr + fabsf(num) * 0x1p-22f) * fabsf(inv) * 1.001f + 1e-30f;
+    const float w = omega * Q;
+    const float P = (prev >= 0 && var != prev) ? alpha * r1.y : 0.f;
+    Eq3Term t;
+    float pen = 0.f, epen = 0.f;
+    if (tau == -INFINITY) {
+        t.pass = true;
+        t.fail = false;
+    } else {
+        const float slack = e_f + (fabsf(f) + fabsf(tau)) * 0x1p-22f;
+        t.pass = f - slack >= tau;
+        t.fail = f + slack < tau;
+        const float d = (tau + delta) - f;
+        const float e_d = e_f + (fabsf(tau) + fabsf(delta) + fabsf(f)) * 0x1p-22f;
+        const float dp = d > 0.f ? d : 0.f;
+        pen = beta * (dp * dp);
+        // max(0, d)^2 moves by at most (2 max(0, d) + e_d) e_d when d moves by e_d
+        epen = beta * (2.f * dp + e_d) * e_d;
+    }
+    const float wf = w * f;
+    t.c = (wf - P) - pen;
+    t.mag = fabsf(wf) + P + pen;
+    t.e = fabsf(w) * e_f + epen + t.mag * 0x1p-20f + 1e-30f;
+    return t;
+}
+
 // relu of a finite fp32 value as one integer max: negative values (and -0)
 // have a negative bit pattern and map to +0, the rest are unchanged
 __device__ __forceinline__ float relu_f32(float x) { return __int_as_float(max(__float_as_int(x), 0)); }

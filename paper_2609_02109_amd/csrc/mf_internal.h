@@ -15,8 +15,10 @@ constexpr int kSearchWaves = 8;          // waves per workgroup of the fast sear
 constexpr int kSearchWavesWide = 16;     // ... when registers and LDS allow 4 waves per SIMD
 constexpr int kCertWaves = 4;            // waves per workgroup of the canonical kernels
 constexpr int kDefaultWorklist = 1 << 20; // certification list capacity (entries)
+constexpr int kFastPar = 128;            // floats of per-model parameters after the fp32 fast image in LDS
 constexpr int kBf16Waves = 8;            // waves per workgroup of the bf16 fast kernel
 constexpr int kBf16Tiles = 8;            // 32-configuration tiles per wave and model staging
+constexpr int kBf16Par = 128;            // floats of per-model parameters after the bf16 tables in LDS
 
 // ---------------------------------------------------------------------------
 // Fast-path LDS image.  The device copy of the image is laid out exactly as
@@ -52,6 +54,17 @@ struct FastConst {
     float vram_cap;
     // a-priori bound on |fast - canonical| for (lat, thr) of model i, and on |thr|
     double bound_lat[kMaxN], bound_thr[kMaxN], mag_thr[kMaxN];
+};
+
+// Objective of a search (the full utility of Eq. 3 when kind == 1).  vrow
+// holds two float4 per option row: (fmin, fmax, 1/(fmax - fmin) rounded to
+// fp32, Q) and (variant as int bits, reload cost of the row's model, 0, 0).
+struct ObjArgs {
+    int32_t kind;
+    float alpha, beta, delta;
+    float tau[kMaxN];
+    int32_t prev[kMaxN];
+    const float4 *vrow;
 };
 
 // Counters and results the search kernels fill in device memory.
@@ -103,6 +116,7 @@ struct FastArgs {
     unsigned long long *wg_lists; // [grid][KP] top-KP keys (U, lowest index) per workgroup
     uint8_t *mask;              // dump (optional)
     float *pred;                // dump (optional)
+    ObjArgs obj;
 };
 
 // ---------------------------------------------------------------------------
@@ -170,6 +184,7 @@ struct Bf16Args {
     unsigned long long *wg_lists;
     uint8_t *mask;
     float *pred;
+    ObjArgs obj;
 };
 
 // Canonical (fp64) evaluation of entries.
@@ -200,6 +215,7 @@ struct CanonArgs {
     uint32_t *ent_flags;
     double *pred;               // list mode optional [n][N][2]
     uint8_t *mask;              // search dump: patch worklist entries
+    ObjArgs obj;
 };
 
 struct SelectArgs {

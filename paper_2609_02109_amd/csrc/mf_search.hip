@@ -28,7 +28,8 @@ namespace mfi {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-template <int MAXN, int A, int H, int WAVES>
+// OBJ: score with the full utility of Eq. 3 (otherwise the linear objective)
+template <int MAXN, int A, int H, int WAVES, bool OBJ>
 __global__ void __launch_bounds__(WAVES * 64, 1)
 fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int kp)
 {
@@ -42,21 +43,30 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
 
     for (int t = threadIdx.x; t < args.image_f4; t += blockDim.x) smem4[t] = args.image[t];
     // [0,16) sla_lo  [16,32) sla_hi  [32,48) omega  [48,64) first option row per model (int)
+    // [64,80) floor tau  [80,96) previous variant (int)  [96,112) throughput bound
     float *par = smem + Ly.total_floats;
     int *par_off = reinterpret_cast<int *>(par + 48);
-    unsigned long long *lst = reinterpret_cast<unsigned long long *>(par + 64);
+    int *par_prev = reinterpret_cast<int *>(par + 80);
+    unsigned long long *lst = reinterpret_cast<unsigned long long *>(par + kFastPar);
 #pragma unroll
     for (int i = 0; i < kMaxN; i++) {
         // compile-time index into the argument block (keeps it out of scratch)
         if (threadIdx.x == (unsigned)i && i < N) {
             const double s = (double)args.sla[i], b = fc.bound_lat[i];
             const double slack = (fabs(s) + b) * 0x1p-22 + 1e-30;
-            par[i] = (float)(s - b - slack);       // lat <= this  => canonical lat <= sla
-            par[16 + i] = (float)(s + b + slack);  // lat >  this  => canonical lat >  sla
+            const bool inf = isinf(s);
+            par[i] = inf ? (float)s : (float)(s - b - slack);       // lat <= this  => canonical lat <= sla
+            par[16 + i] = inf ? (float)s : (float)(s + b + slack);  // lat >  this  => canonical lat >  sla
             par[32 + i] = args.omega[i];
             par_off[i] = fc.opt_off[i];
+            if constexpr (OBJ) {
+                par[64 + i] = args.obj.tau[i];
+                par_prev[i] = args.obj.prev[i];
+                par[96 + i] = f32_up(fc.bound_thr[i]);
+            }
         }
     }
+    constexpr bool eq3 = OBJ;
     // global bound on |fast J - canonical J|: keys and certification entries
     // carry the upper bound U = J + eJ
     const double eJ = bound_eJ(fc, args.omega);
@@ -142,9 +152,9 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
         }
         const bool vram_ok = ah[0] <= fc.vram_cap;
 
-        float J = 0.f;
+        float J = 0.f, EJ = 0.f, MJ = 0.f;   // fast J; under Eq. 3 its bound and magnitude
         bool anyfail = false;
-        uint32_t umask = 0;   // models whose latency decision is left to the canonical pass
+        uint32_t umask = 0;   // models whose service decision is left to the canonical pass
         for (int i = 0; i < N; i++) {
             const uint64_t sel = (uint64_t)0 - (uint64_t)(i >= 8);
             const uint64_t dw = dig0 ^ ((dig0 ^ dig1) & sel);
@@ -224,10 +234,21 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             pt += __shfl_xor(pt, 32);
             const float *b3 = smem + Ly.off_b3 + 4 * i;
             const float lat = pl + b3[0], thr = pt + b3[1];
-            const bool pass = lat <= par[i], fail = lat > par[16 + i];
+            bool pass = lat <= par[i], fail = lat > par[16 + i];
+            if constexpr (eq3) {
+                const Eq3Term t = eq3_term(args.obj.vrow[2 * row], args.obj.vrow[2 * row + 1], thr, par[96 + i],
+                                           par[32 + i], par[64 + i], par_prev[i], args.obj.alpha, args.obj.beta,
+                                           args.obj.delta);
+                fail = fail || t.fail;
+                pass = pass && t.pass;
+                J += t.c;
+                EJ += t.e;
+                MJ += t.mag;
+            } else {
+                J = fmaf(par[32 + i], thr, J);
+            }
             anyfail |= fail;
             umask |= (pass || fail) ? 0u : (1u << i);
-            J = fmaf(par[32 + i], thr, J);
             if (args.pred && valid && half == 0) {
                 args.pred[(off * (uint64_t)N + (uint64_t)i) * 2u + 0u] = lat;
                 args.pred[(off * (uint64_t)N + (uint64_t)i) * 2u + 1u] = thr;
@@ -243,7 +264,10 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             // canonically when it can change the count (VRAM ok) or, in dump
             // mode, the mask
             const bool unc = mine && !anyfail && anyunc && (vram_ok || args.mask != nullptr);
-            const float U = f32_up((double)J + eJ);
+            // Eq. 3: the sum of per-model bounds, plus the fp32 sum over models
+            // (N u relative to the magnitudes)
+            const float U = eq3 ? f32_up((double)J + (double)EJ * (1.0 + 0x1p-10) + (double)MJ * N * 0x1p-22 + 1e-30)
+                                : f32_up((double)J + eJ);
             if (mode == kModeSearch) {
                 c_vram += (mine && vram_ok) ? 1u : 0u;
                 c_feas += feas_sure ? 1u : 0u;
@@ -328,8 +352,8 @@ template <int MAXN, int A, int H, int WAVES>
 static hipError_t launch_fast_t(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode,
                                 hipStream_t s)
 {
-    const size_t lds = (size_t)a.lay.total_floats * 4 + 64 * 4 + (size_t)WAVES * kp * 8;
-    auto fn = fast_kernel<MAXN, A, H, WAVES>;
+    const size_t lds = (size_t)a.lay.total_floats * 4 + kFastPar * 4 + (size_t)WAVES * kp * 8;
+    auto fn = a.obj.kind != 0 ? fast_kernel<MAXN, A, H, WAVES, true> : fast_kernel<MAXN, A, H, WAVES, false>;
     hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(grid), dim3(WAVES * 64), lds, s, a, fc, mode, kp);
@@ -349,7 +373,7 @@ int fast_kernel_supported(int n_models, int A, int H, int kp)
 // VGPRs (up to 8 models) and the image plus 16 candidate lists fit in LDS.
 int fast_waves_for(int n_models, const FastLayout &lay, int kp)
 {
-    const size_t lds = (size_t)lay.total_floats * 4 + 64 * 4 + (size_t)kSearchWavesWide * kp * 8;
+    const size_t lds = (size_t)lay.total_floats * 4 + kFastPar * 4 + (size_t)kSearchWavesWide * kp * 8;
     return (n_models <= 8 && lds <= 163840) ? kSearchWavesWide : kSearchWaves;
 }
 

@@ -31,7 +31,7 @@ hipError_t launch_precompute_phat(const float *features, const float *canon_w, i
 
 size_t bf16_lds_bytes(const Bf16Layout &lay, int kp)
 {
-    return (size_t)(lay.model_floats + lay.sumK * 8 + lay.gv_floats + 64) * 4 + (size_t)kBf16Waves * kp * 8;
+    return (size_t)(lay.model_floats + lay.sumK * 8 + lay.gv_floats + kBf16Par) * 4 + (size_t)kBf16Waves * kp * 8;
 }
 
 int bf16_kernel_supported(int n_models, int A, int H)

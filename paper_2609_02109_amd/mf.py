@@ -31,17 +31,46 @@ class MfError(RuntimeError):
         self.status = status
 
 
+MAX_VARIANTS = 4
+MF_OBJ_LINEAR, MF_OBJ_EQ3 = 0, 1
+
+
+class Variants(C.Structure):
+    _fields_ = [("h_variant", C.c_void_p), ("h_n_variants", C.c_void_p), ("h_fmin", C.c_void_p),
+                ("h_fmax", C.c_void_p), ("h_quality", C.c_void_p), ("h_reload_cost", C.c_void_p)]
+
+
 class Desc(C.Structure):
     _fields_ = [("n_models", C.c_int32), ("n_local", C.c_int32), ("n_agg", C.c_int32),
                 ("hidden1", C.c_int32), ("hidden2", C.c_int32),
                 ("h_n_options", C.c_void_p), ("h_agg_cols", C.c_void_p),
-                ("vram_slot", C.c_int32), ("vram_cap", C.c_float), ("dtype", C.c_int32)]
+                ("vram_slot", C.c_int32), ("vram_cap", C.c_float), ("dtype", C.c_int32),
+                ("variants", C.c_void_p)]
+
+
+class Objective(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("alpha", C.c_float), ("beta", C.c_float), ("delta", C.c_float),
+                ("tau", C.c_float * MAX_MODELS), ("prev_variant", C.c_int32 * MAX_MODELS)]
 
 
 class SearchArgs(C.Structure):
     _fields_ = [("lo", C.c_uint64), ("hi", C.c_uint64), ("top_k", C.c_int32), ("flags", C.c_uint32),
                 ("d_sla", C.c_void_p), ("d_omega", C.c_void_p), ("d_mask", C.c_void_p),
-                ("d_pred", C.c_void_p)]
+                ("d_pred", C.c_void_p), ("objective", Objective)]
+
+
+def objective_args(obj, n_models: int) -> Objective:
+    """mf_objective for a search: None -> the linear objective; otherwise an
+    object with alpha, beta, delta, tau [N] and prev_variant [N] (Eq. 3)."""
+    o = Objective()
+    if obj is None:
+        return o
+    o.kind = MF_OBJ_EQ3
+    o.alpha, o.beta, o.delta = float(obj.alpha), float(obj.beta), float(obj.delta)
+    for i in range(n_models):
+        o.tau[i] = float(obj.tau[i])
+        o.prev_variant[i] = int(obj.prev_variant[i])
+    return o
 
 
 class Result(C.Structure):
@@ -116,7 +145,7 @@ class Problem:
     """A created problem (mf_problem).  `inst` carries the instance arrays
     (n_options, features, agg_cols, weights, ...), e.g. a synth.Instance."""
 
-    def __init__(self, inst, device="cuda", stream=None):
+    def __init__(self, inst, device="cuda", stream=None, variants=None):
         import torch
         self.inst = inst
         self.N = int(inst.n_models)
@@ -125,10 +154,23 @@ class Problem:
         self._agg_cols = np.ascontiguousarray(inst.agg_cols, np.int32)
         feats = torch.from_numpy(np.ascontiguousarray(inst.features, np.float32)).to(self.device)
         w = torch.from_numpy(np.ascontiguousarray(inst.weights, np.float32)).to(self.device)
+        self._var = None
+        if variants is not None:
+            # static variant metadata of Eq. 3 (variant per option row,
+            # per-variant extremes and quality, reload cost per model)
+            v = variants
+            self._var_arrays = [np.ascontiguousarray(v.variant, np.int32),
+                                np.ascontiguousarray(v.n_variants, np.int32),
+                                np.ascontiguousarray(v.fmin, np.float32).reshape(self.N, MAX_VARIANTS),
+                                np.ascontiguousarray(v.fmax, np.float32).reshape(self.N, MAX_VARIANTS),
+                                np.ascontiguousarray(v.quality, np.float32).reshape(self.N, MAX_VARIANTS),
+                                np.ascontiguousarray(v.reload_cost, np.float32)]
+            self._var = Variants(*[_ptr(a).value for a in self._var_arrays])
         self.desc = Desc(self.N, int(inst.n_local), int(inst.n_agg), int(inst.hidden1),
                          int(inst.hidden2), _ptr(self._n_options), _ptr(self._agg_cols),
                          int(inst.vram_slot), float(inst.vram_cap),
-                         MF_BF16 if inst.dtype == "bf16" else MF_F32)
+                         MF_BF16 if inst.dtype == "bf16" else MF_F32,
+                         C.addressof(self._var) if self._var is not None else None)
         h = C.c_void_p()
         _check(lib.mf_problem_create(C.byref(self.desc), _ptr(feats), _ptr(w), _stream(stream),
                                      C.byref(h)), "mf_problem_create")
@@ -171,10 +213,12 @@ class Problem:
             self._ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
         return self._ws
 
-    def search(self, sla, omega, k=1, lo=0, hi=None, dump=False, stream=None):
+    def search(self, sla, omega, k=1, lo=0, hi=None, dump=False, stream=None, objective=None):
         """Exhaustive search over [lo, hi).  Returns a dict of counts and the
         exact top-k; with dump=True also the per-index mask and fast-path
-        predictions (device tensors)."""
+        predictions (device tensors).  objective: None (linear) or an object
+        with alpha, beta, delta, tau, prev_variant (Eq. 3; the problem must
+        have been created with variants)."""
         import torch
         if hi is None:
             hi = self.space_size
@@ -185,7 +229,7 @@ class Problem:
             mask = torch.zeros(max(hi - lo, 1), dtype=torch.uint8, device=self.device)
             pred = torch.zeros((max(hi - lo, 1), self.N, 2), dtype=torch.float32, device=self.device)
         args = SearchArgs(lo, hi, int(k), MF_DUMP if dump else 0, _ptr(d_sla), _ptr(d_om),
-                          _ptr(mask), _ptr(pred))
+                          _ptr(mask), _ptr(pred), objective_args(objective, self.N))
         nbytes = C.c_size_t()
         _check(lib.mf_workspace_size(self.handle, C.byref(args), C.byref(nbytes)), "mf_workspace_size")
         ws = self.workspace(nbytes.value)
