@@ -47,7 +47,7 @@ class _Inst(C.Structure):
                 ("hidden1", C.c_int32), ("hidden2", C.c_int32), ("bf16", C.c_int32),
                 ("n_options", C.c_void_p), ("features", C.c_void_p), ("agg_cols", C.c_void_p),
                 ("vram_slot", C.c_int32), ("vram_cap", C.c_float), ("weights", C.c_void_p),
-                ("obj", C.c_void_p)]
+                ("obj", C.c_void_p), ("fixed_state", C.c_void_p)]
 
 
 class _Result(C.Structure):
@@ -102,9 +102,11 @@ class Problem:
     `objective` (optional): an object with the arrays of the full utility of
     Eq. 3 (variant [sum K], fmin/fmax/quality [N][4], reload_cost [N],
     prev_variant [N], tau [N]) and alpha, beta, delta; None selects the
-    linear objective."""
+    linear objective.  `state` (optional): the observed aggregate state [A]
+    fed to every surrogate, held fixed over the search (the paper's own
+    semantics); None derives the aggregate from each candidate."""
 
-    def __init__(self, inst, objective=None):
+    def __init__(self, inst, objective=None, state=None):
         self.n_options = np.ascontiguousarray(inst.n_options, dtype=np.int32)
         self.features = np.ascontiguousarray(inst.features, dtype=np.float32)
         self.agg_cols = np.ascontiguousarray(inst.agg_cols, dtype=np.int32)
@@ -114,7 +116,11 @@ class Problem:
                        int(inst.hidden2), 1 if inst.dtype == "bf16" else 0,
                        _ptr(self.n_options).value, _ptr(self.features).value,
                        _ptr(self.agg_cols).value, int(inst.vram_slot),
-                       float(inst.vram_cap), _ptr(self.weights).value, None)
+                       float(inst.vram_cap), _ptr(self.weights).value, None, None)
+        self.state = None
+        if state is not None:
+            self.state = np.ascontiguousarray(state, np.float32)
+            self.c.fixed_state = _ptr(self.state).value
         self.obj = None
         if objective is not None:
             o = objective

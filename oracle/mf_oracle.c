@@ -23,6 +23,11 @@
  *   Decision (Section II): lambda* = argmax J; here J = sum_i omega_i thr_i,
  *     ties broken to the lowest linear index, top-k sorted by (J desc,
  *     index asc).
+ *   Fixed observed state (Section III-B, the paper's own semantics, when
+ *     fixed_state is given): the surrogate's aggregate input is the observed
+ *     state, held fixed over the whole search, so model i's prediction
+ *     depends on its own option only; the VRAM constraint still sums the
+ *     candidate's options.
  *   Full utility (Section II, Eq. 3, when an objective block is given): with
  *     v the variant of model i's option, the normalised throughput is
  *     f_i = (thr_i - fmin_{i,v}) / (fmax_{i,v} - fmin_{i,v}) (per-variant
@@ -189,7 +194,7 @@ void orc_eval_w(const orc_instance *in, const double *w64, uint64_t idx,
     for (int i = 0; i < N; i++) {
         const float *x = in->features + (off + d[i]) * L;
         for (int k = 0; k < L; k++) z[k] = (double)x[k];
-        for (int k = 0; k < A; k++) z[L + k] = (double)a[k];
+        for (int k = 0; k < A; k++) z[L + k] = (double)(in->fixed_state ? in->fixed_state[k] : a[k]);
         double y[2];
         mlp_forward(w64 + stride * i, nin, in->hidden1, in->hidden2, in->bf16, z, h1, h2, y);
         lat[i] = y[0];

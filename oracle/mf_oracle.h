@@ -32,6 +32,8 @@ typedef struct {
     float vram_cap;
     const float *weights;       /* [N][stride]: W1[h1][L+A] b1[h1] W2[h2][h1] b2[h2] W3[2][h2] b3[2] */
     const orc_objective *obj;   /* NULL: linear objective */
+    const float *fixed_state;   /* [A] observed aggregate state fed to every surrogate (Section III-B:
+                                   held fixed during the search); NULL: derived from each candidate */
 } orc_instance;
 
 typedef struct {

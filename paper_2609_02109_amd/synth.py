@@ -259,6 +259,24 @@ def cfg4(seed=0) -> Instance:
                          dtype="bf16", top_k=64, name="n8_k16_h256_bf16")
 
 
+def make_state(inst: Instance, seed: int = 0, spread: float = 0.5) -> np.ndarray:
+    """An observed aggregate state (what the runtime monitor reports,
+    Section II), float32 [A]: each slot drawn around its mean under a uniform
+    choice per model, `spread` standard deviations wide, on the 2^-14 grid.
+    The statistics come from the option tables alone."""
+    rng = np.random.Generator(np.random.PCG64(seed * 104729 + 3))
+    offs = np.concatenate([[0], np.cumsum(inst.n_options)])
+    st = np.zeros(inst.n_agg)
+    for k, c in enumerate(inst.agg_cols):
+        mu = var = 0.0
+        for i in range(inst.n_models):
+            col = inst.features[offs[i]:offs[i + 1], c].astype(np.float64)
+            mu += col.mean()
+            var += col.var()
+        st[k] = mu + spread * np.sqrt(var) * rng.standard_normal()
+    return _quantise(st).astype(np.float32)
+
+
 # ---------------------------------------------------------------------------
 # Variant metadata of the full utility (Section II, Eq. 3)
 # ---------------------------------------------------------------------------
