@@ -131,6 +131,8 @@ mf_status mf_decode(const mf_problem *p, uint64_t idx, int32_t *h_digits);
 /* ---------------------------------------------------------------- search */
 
 #define MF_DUMP 1u   /* write d_mask and d_pred for every index of [lo, hi) */
+#define MF_FIXED_STATE 2u  /* hold the surrogates' aggregate input at `state` (see mf_search_args) */
+#define MF_MAX_AGG 16
 
 typedef enum {
     MF_OBJ_LINEAR = 0,  /* J = sum_i omega_i thr_i (Section II with unit quality) */
@@ -159,7 +161,7 @@ typedef struct {
 typedef struct {
     uint64_t lo, hi;           /* half-open index range, lo <= hi <= |Lambda| */
     int32_t top_k;             /* 1..64 */
-    uint32_t flags;            /* MF_DUMP */
+    uint32_t flags;            /* MF_DUMP | MF_FIXED_STATE */
     const float *d_sla;        /* device [N] latency bound per model (+inf: none) */
     const float *d_omega;      /* device [N] objective weight per model, finite */
     /* MF_DUMP outputs (device, hi - lo <= 2^31 entries):
@@ -167,10 +169,22 @@ typedef struct {
      *              bounds; throughput floors under MF_OBJ_EQ3), bit2 feasible,
      *              bit3 the fast path left a service decision to the
      *              canonical re-evaluation;
-     *   d_pred[(t*N + i)*2 + {0,1}]: fast-path fp32 (lat, thr) of model i. */
+     *   d_pred[(t*N + i)*2 + {0,1}]: fast-path fp32 (lat, thr) of model i
+     *              (MF_FIXED_STATE: the canonical values rounded to fp32). */
     uint8_t *d_mask;
     float *d_pred;
     mf_objective objective;    /* zero-initialised: MF_OBJ_LINEAR */
+    /* MF_FIXED_STATE (Section III-B: the aggregate GPU state is observed by
+     * the runtime monitor and held fixed during the search): every surrogate
+     * takes state[0..A) (original slot order, finite) as its aggregate input
+     * instead of the candidate's own aggregate, so model i's prediction
+     * depends on its option only; the VRAM constraint still sums the
+     * candidate's options.  The search then runs the surrogates once per
+     * option row (canonical semantics) and scans the joint space over those
+     * tables, exactly: any created shape is supported (no fast-path shape
+     * limits), d_pred receives the canonical (lat, thr) rounded to fp32, mask
+     * bit3 and n_flagged / n_topk_collect / n_splits stay 0. */
+    float state[MF_MAX_AGG];
 } mf_search_args;
 
 typedef struct {

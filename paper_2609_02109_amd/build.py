@@ -14,7 +14,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libmf.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["mf_search.hip", "mf_search_bf16.hip", "mf_search_bf16_h64.hip", "mf_search_bf16_h128.hip",
-           "mf_search_bf16_h256.hip", "mf_certify.hip", "mf_ga.hip", "mf_api.cpp"]
+           "mf_search_bf16_h256.hip", "mf_certify.hip", "mf_fixed.hip", "mf_ga.hip", "mf_api.cpp"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=off",
          # packed fp32 VALU forms are kept out of every kernel
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

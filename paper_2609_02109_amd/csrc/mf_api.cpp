@@ -586,6 +586,103 @@ mf_status search_range(mf_problem *p, const mf_search_args *args, uint64_t lo, u
     return MF_OK;
 }
 
+// ---- fixed observed state (MF_FIXED_STATE)
+
+constexpr uint64_t kFixedChunk = 1ull << 36;   // configurations per scan launch set
+
+struct FixedWs {
+    size_t res, rows, prow, lists, total;
+    int grid;
+};
+
+FixedWs fixed_ws_layout(const mf_problem &p, uint64_t n, int top_k)
+{
+    FixedWs w{};
+    const uint64_t tiles = (n + 63) / 64;
+    const uint64_t g = (tiles + kFixedWaves - 1) / kFixedWaves;
+    w.grid = (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)p.num_cus * 8));
+    size_t o = 0;
+    w.res = o; o = align256(o + sizeof(DevResult));
+    w.rows = o; o = align256(o + (size_t)p.sumK * sizeof(FixedRow));
+    w.prow = o; o = align256(o + (size_t)p.sumK * 8);
+    w.lists = o; o = align256(o + (size_t)w.grid * top_k * sizeof(K128));
+    w.total = o;
+    return w;
+}
+
+// The search with the aggregate input held at args->state: one table of
+// canonical per-row terms, then scans of the joint space in chunks.
+mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipStream_t s, mf_result &acc)
+{
+    const uint64_t n_all = args->hi - args->lo;
+    if (n_all == 0) return MF_OK;
+    const FixedWs w = fixed_ws_layout(*p, std::min<uint64_t>(n_all, kFixedChunk), args->top_k);
+    FixedArgs a{};
+    a.n_models = p->N; a.L = p->L; a.A = p->A; a.H1 = p->H1; a.H2 = p->H2; a.bf16 = p->bf16; a.sumK = p->sumK;
+    for (int i = 0; i < p->N; i++) {
+        a.K[i] = p->K[i];
+        a.opt_off[i] = p->opt_off[i];
+        a.magic[i] = magic_for(p->K[i]);
+    }
+    a.row_model = p->d_row_model;
+    a.features = p->d_features;
+    a.weights = p->d_canon;
+    a.wstride = p->wstride;
+    for (int k = 0; k < p->A; k++) a.state[k] = args->state[k];
+    a.vram_col = p->agg_cols[p->vram_slot];
+    a.vram_cap = p->vram_cap;
+    a.sla = args->d_sla;
+    a.omega = args->d_omega;
+    a.top_k = args->top_k;
+    a.rows = reinterpret_cast<FixedRow *>(ws + w.rows);
+    a.pred_rows = reinterpret_cast<float2 *>(ws + w.prow);
+    a.wg_lists = reinterpret_cast<K128 *>(ws + w.lists);
+    a.res = reinterpret_cast<DevResult *>(ws + w.res);
+    a.obj = obj_args(p, args->objective);
+    const bool dump = (args->flags & MF_DUMP) != 0;
+
+    hipEvent_t ev0 = nullptr, ev1 = nullptr;
+    MF_HIP(hipEventCreate(&ev0));
+    if (hipEventCreate(&ev1) != hipSuccess) { (void)hipEventDestroy(ev0); return MF_EDEVICE; }
+    mf_status st = MF_OK;
+    for (uint64_t lo = args->lo; lo < args->hi && st == MF_OK;) {
+        const uint64_t n = std::min<uint64_t>(args->hi - lo, kFixedChunk);
+        const FixedWs wc = fixed_ws_layout(*p, n, args->top_k);
+        a.lo = lo;
+        a.n = n;
+        a.total_waves = wc.grid * kFixedWaves;
+        stride_digits(*p, (uint64_t)a.total_waves * 64u, a.stride_digits);
+        a.mask = dump ? args->d_mask + (lo - args->lo) : nullptr;
+        a.pred = dump ? args->d_pred + (lo - args->lo) * (uint64_t)p->N * 2u : nullptr;
+        DevResult h{};
+        float ms = 0.f;
+        if (hipMemsetAsync(a.res, 0, sizeof(DevResult), s) != hipSuccess ||
+            launch_fixed(a, wc.grid, lo == args->lo, s, ev0, ev1) != hipSuccess ||
+            hipMemcpyAsync(&h, a.res, sizeof(DevResult), hipMemcpyDeviceToHost, s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess || hipEventElapsedTime(&ms, ev0, ev1) != hipSuccess) {
+            st = MF_EDEVICE;
+            break;
+        }
+        if (!(h.status & kStatVerified)) { st = MF_EINTERNAL; break; }
+        mf_result part;
+        empty_result(part);
+        part.n_eval = n;
+        part.n_vram = h.n_vram;
+        part.n_feas = h.n_feas_sure;
+        part.n_top = h.n_top;
+        for (int q = 0; q < h.n_top; q++) {
+            part.top_idx[q] = h.top_idx[q];
+            part.top_J[q] = h.top_J[q];
+        }
+        part.main_kernel_ms = ms;
+        merge_into(acc, part, args->top_k);
+        lo += n;
+    }
+    (void)hipEventDestroy(ev0);
+    (void)hipEventDestroy(ev1);
+    return st;
+}
+
 }  // namespace
 
 extern "C" {
@@ -610,7 +707,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     if (!desc || !d_features || !d_weights || !out) return MF_EINVAL;
     *out = nullptr;
     const int N = desc->n_models, L = desc->n_local, A = desc->n_agg, H1 = desc->hidden1, H2 = desc->hidden2;
-    if (N < 1 || N > MF_MAX_MODELS || L < 1 || A < 1 || A > 16 || L + A > 64 || H1 < 1 || H1 > 256 || H2 < 1 ||
+    if (N < 1 || N > MF_MAX_MODELS || L < 1 || A < 1 || A > MF_MAX_AGG || L + A > 64 || H1 < 1 || H1 > 256 || H2 < 1 ||
         H2 > 256 || !desc->h_n_options || !desc->h_agg_cols)
         return MF_EINVAL;
     if (desc->dtype != MF_F32 && desc->dtype != MF_BF16) return MF_EINVAL;
@@ -961,9 +1058,14 @@ static mf_status check_search_args(const mf_problem *p, const mf_search_args *a)
     if (a->hi > p->space) return MF_EOVERFLOW;
     if (a->top_k < 1 || a->top_k > MF_MAX_TOPK) return MF_EINVAL;
     if (!a->d_sla || !a->d_omega) return MF_EINVAL;
-    if (a->flags & ~MF_DUMP) return MF_EINVAL;
+    if (a->flags & ~(MF_DUMP | MF_FIXED_STATE)) return MF_EINVAL;
     if ((a->flags & MF_DUMP) && (!a->d_mask || !a->d_pred || a->hi - a->lo > (1ull << 31))) return MF_EINVAL;
-    if (!p->fast_ok && !p->bf_ok) return MF_EUNSUPPORTED;
+    if (a->flags & MF_FIXED_STATE) {
+        for (int k = 0; k < p->A; k++)
+            if (!std::isfinite(a->state[k])) return MF_EINVAL;
+    } else if (!p->fast_ok && !p->bf_ok) {
+        return MF_EUNSUPPORTED;
+    }
     const mf_objective &o = a->objective;
     if (o.kind != MF_OBJ_LINEAR && o.kind != MF_OBJ_EQ3) return MF_EINVAL;
     if (o.kind == MF_OBJ_EQ3) {
@@ -983,6 +1085,10 @@ mf_status mf_workspace_size(const mf_problem *p, const mf_search_args *args, siz
     if (!bytes) return MF_EINVAL;
     mf_status st = check_search_args(p, args);
     if (st != MF_OK) return st;
+    if (args->flags & MF_FIXED_STATE) {
+        *bytes = fixed_ws_layout(*p, std::min<uint64_t>(args->hi - args->lo, kFixedChunk), args->top_k).total;
+        return MF_OK;
+    }
     const uint64_t n = std::min<uint64_t>(args->hi - args->lo, kMaxLaunch);
     *bytes = ws_layout(*p, n, args->top_k).total;
     return MF_OK;
@@ -995,12 +1101,17 @@ mf_status mf_search(mf_problem *p, const mf_search_args *args, void *d_ws, size_
     mf_status st = check_search_args(p, args);
     if (st != MF_OK) return st;
     const uint64_t n = args->hi - args->lo;
-    const uint64_t n1 = std::min<uint64_t>(n, kMaxLaunch);
-    if (ws_bytes < ws_layout(*p, n1, args->top_k).total) return MF_ENOMEM;
+    const bool fixed = (args->flags & MF_FIXED_STATE) != 0;
+    const size_t need = fixed ? fixed_ws_layout(*p, std::min<uint64_t>(n, kFixedChunk), args->top_k).total
+                              : ws_layout(*p, std::min<uint64_t>(n, kMaxLaunch), args->top_k).total;
+    if (ws_bytes < need) return MF_ENOMEM;
     if (((uintptr_t)d_ws & 255u) != 0) return MF_EINVAL;
     mf_result acc;
     empty_result(acc);
-    st = search_range(p, args, args->lo, n, (char *)d_ws, (hipStream_t)stream, acc, 0);
+    if (fixed)
+        st = search_fixed(p, args, (char *)d_ws, (hipStream_t)stream, acc);
+    else
+        st = search_range(p, args, args->lo, n, (char *)d_ws, (hipStream_t)stream, acc, 0);
     if (st != MF_OK) return st;
     *h_out = acc;
     return MF_OK;

@@ -11,28 +11,10 @@
 //
 // One single-wave workgroup per entry: lanes take hidden units, the uniform
 // parts (decode, aggregate, output units) run redundantly per lane.
-#include "mf_device.h"
+#include "mf_canon.h"
 
 namespace mfi {
 
-constexpr int kCanonMaxH = 256;
-constexpr int kCanonMaxIn = 64;
-
-__device__ __forceinline__ double bf16_round_d(double x)
-{
-    // nearest bfloat16 value (8 significant bits), ties to even; x finite
-    if (x == 0.0) return x;
-    int e = ilogb(x);
-    if (e < -126) e = -126;                 // bf16 subnormal spacing 2^-133
-    const double scale = ldexp(1.0, 7 - e); // |x| * scale in [128, 256)
-    return rint(x * scale) / scale;
-}
-
-__device__ __forceinline__ uint64_t ord_f64(double x)
-{
-    const uint64_t b = (uint64_t)__double_as_longlong(x);
-    return (b & 0x8000000000000000ull) ? ~b : (b | 0x8000000000000000ull);
-}
 
 // Canonical image per model (fp32 values, exact in fp64):
 //   W1T[nin][H1], b1[H1], W2T[H1][H2], b2[H2], W3[2][H2], b3[2]
@@ -125,57 +107,23 @@ canon_kernel(const CanonArgs a, const int search_mode)
         double J = 0.0;
         for (int i = 0; i < N; i++) {
             if (!((models >> i) & 1u)) continue;
-            const float *w = a.weights + (int64_t)i * a.wstride;
-            const float *W1T = w, *b1 = W1T + (int64_t)nin * H1, *W2T = b1 + H1, *b2 = W2T + (int64_t)H1 * H2,
-                        *W3 = b2 + H2, *b3 = W3 + 2 * H2;
             const float *x = a.features + (int64_t)(a.opt_off[i] + ds[i]) * L;
             for (int k = lane; k < nin; k += 64) zs[k] = k < L ? (double)x[k] : (double)aggs[k - L];
             __syncthreads();
-            for (int u = lane; u < H1; u += 64) {
-                if (BF16) {
-                    // bf16 mode: the layer-1 pre-activation accumulates in fp32
-                    // (one fmaf chain in input order from the bias), then
-                    // relu and rounding to bfloat16
-                    float c = b1[u];
-                    for (int k = 0; k < nin; k++) c = fmaf(W1T[(int64_t)k * H1 + u], (float)zs[k], c);
-                    c = c > 0.f ? c : 0.f;
-                    h1s[u] = bf16_round_d((double)c);
-                } else {
-                    double c = (double)b1[u];
-                    for (int k = 0; k < nin; k++) c = fma((double)W1T[(int64_t)k * H1 + u], zs[k], c);
-                    h1s[u] = c > 0.0 ? c : 0.0;
-                }
-            }
-            __syncthreads();
-            for (int v = lane; v < H2; v += 64) {
-                double c = (double)b2[v];
-                for (int u = 0; u < H1; u++) c = fma((double)W2T[(int64_t)u * H2 + v], h1s[u], c);
-                h2s[v] = c > 0.0 ? c : 0.0;
-            }
-            __syncthreads();
-            double y = 0.0;
-            if (lane < 2) {
-                double c = (double)b3[lane];
-                for (int v = 0; v < H2; v++) c = fma((double)W3[lane * H2 + v], h2s[v], c);
-                y = c;
-            }
-            const double lat = __shfl(y, 0), thr = __shfl(y, 1);
+            double lat, thr;
+            canon_model<BF16>(a.weights + (int64_t)i * a.wstride, nin, H1, H2, zs, h1s, h2s, lane, lat, thr);
             if (!(lat <= (double)a.sla[i])) { sla_ok = false; fl |= 1u << (8 + i); }
             if (eq3) {
                 // Eq. 3 (Section II): per-variant min-max throughput, quality,
                 // reload penalty, soft SLA penalty; the throughput floor
                 const int64_t row = (int64_t)a.opt_off[i] + ds[i];
-                const float4 r0 = a.obj.vrow[2 * row], r1 = a.obj.vrow[2 * row + 1];
-                const int var = __float_as_int(r1.x);
-                const double fmin = (double)r0.x;
-                const double rg = (double)r0.y - fmin;
-                const double f = (thr - fmin) / rg;
-                if (!(f >= (double)s_tau[i])) { sla_ok = false; fl |= 1u << (8 + i); }
-                const double q = (double)r0.w * f;
+                double q, P, pen;
+                bool do_P, do_pen;
+                const bool floor_ok = canon_eq3(a.obj, row, thr, s_tau[i], s_prev[i], q, P, do_P, pen, do_pen);
+                if (!floor_ok) { sla_ok = false; fl |= 1u << (8 + i); }
                 J = fma((double)a.omega[i], q, J);
-                if (s_prev[i] >= 0 && var != s_prev[i]) J = J - (double)a.obj.alpha * (double)r1.y;
-                const double dd = ((double)s_tau[i] + (double)a.obj.delta) - f;
-                if (dd > 0.0) J = J - (double)a.obj.beta * (dd * dd);
+                if (do_P) J = J - P;
+                if (do_pen) J = J - pen;
             } else {
                 J = fma((double)a.omega[i], thr, J);
             }
@@ -210,47 +158,8 @@ hipError_t launch_canonical(const CanonArgs &a, int n_entries_max, bool search_m
 }
 
 // ---------------------------------------------------------------------------
-// Exact top-k over the canonically evaluated entries.  128-bit keys:
-// (order-preserving bits of canonical J, bitwise-not of the index) so that
-// larger keys are better and equal J prefers the lower index.
+// Exact top-k over the canonically evaluated entries (128-bit keys K128).
 // ---------------------------------------------------------------------------
-struct K128 {
-    unsigned long long hi, lo;
-};
-__device__ __forceinline__ bool gt128(const K128 &x, const K128 &y)
-{
-    return x.hi > y.hi || (x.hi == y.hi && x.lo > y.lo);
-}
-__device__ __forceinline__ bool nz128(const K128 &x) { return (x.hi | x.lo) != 0ull; }
-
-__device__ __forceinline__ unsigned long long rl64(unsigned long long x, int src)
-{
-    const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)x, src);
-    const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), src);
-    return ((unsigned long long)hi << 32) | lo;
-}
-__device__ __forceinline__ unsigned long long up64(unsigned long long x)
-{
-    const uint32_t lo = __shfl_up((int)(uint32_t)x, 1);
-    const uint32_t hi = __shfl_up((int)(uint32_t)(x >> 32), 1);
-    return ((unsigned long long)hi << 32) | lo;
-}
-
-__device__ void list128_offer(K128 &slot, const K128 &mine, int lane, int k, K128 &thr)
-{
-    unsigned long long cm = __ballot(nz128(mine) && gt128(mine, thr));
-    while (cm) {
-        const int src = __ffsll((long long)cm) - 1;
-        cm &= cm - 1;
-        const K128 nk = {rl64(mine.hi, src), rl64(mine.lo, src)};
-        if (!gt128(nk, thr)) continue;
-        const int pos = __popcll(__ballot(lane < k && gt128(slot, nk)));
-        const K128 prev = {up64(slot.hi), up64(slot.lo)};
-        if (lane < k) slot = lane < pos ? slot : (lane == pos ? nk : prev);
-        thr = {rl64(slot.hi, k - 1), rl64(slot.lo, k - 1)};
-    }
-}
-
 constexpr int kSelWaves = 16;
 
 // k-th canonical J among the fast candidates (by J desc, index asc); -inf if
@@ -336,12 +245,12 @@ select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
         list128_offer(slot, key, lane, k, thr);
     }
     if (my_feas) atomicAdd(&s_feas, my_feas);
-    lst[wv * 64 + lane] = lane < k ? slot : K128{0, 0};
+    lst[wv * 64 + lane] = key_if(lane < k, slot);
     __syncthreads();
     if (wv == 0) {
         for (int w = 1; w < kSelWaves; w++) list128_offer(slot, lst[w * 64 + lane], lane, k, thr);
         const int n_top = __popcll(__ballot(lane < k && nz128(slot)));
-        const uint64_t kth_hi = rl64(slot.hi, k - 1);
+        const uint64_t kth_hi = readlane64(slot.hi, k - 1);
         if (lane < MF_MAX_TOPK) {
             const bool ok = lane < n_top;
             R->top_idx[lane] = ok ? ~slot.lo : ~0ull;

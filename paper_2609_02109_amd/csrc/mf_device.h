@@ -161,6 +161,49 @@ __device__ __forceinline__ void wl_offer(WaveList<NS> &L, unsigned long long myk
     }
 }
 
+// Selection on 128-bit keys (K128): a wave keeps the best k <= 64 keys
+// sorted, slot lane in lane (thr: the k-th key once the list is full, 0
+// before).
+__device__ __forceinline__ bool gt128(const K128 &x, const K128 &y)
+{
+    return x.hi > y.hi || (x.hi == y.hi && x.lo > y.lo);
+}
+__device__ __forceinline__ bool nz128(const K128 &x) { return (x.hi | x.lo) != 0ull; }
+__device__ __forceinline__ K128 key_if(bool c, const K128 &x)
+{
+    return K128{c ? x.hi : 0ull, c ? x.lo : 0ull};
+}
+
+__device__ __forceinline__ uint64_t ord_f64(double x)
+{
+    const uint64_t b = (uint64_t)__double_as_longlong(x);
+    return (b & 0x8000000000000000ull) ? ~b : (b | 0x8000000000000000ull);
+}
+
+__device__ __forceinline__ double unord_f64(uint64_t o)
+{
+    const uint64_t b = (o & 0x8000000000000000ull) ? (o & 0x7FFFFFFFFFFFFFFFull) : ~o;
+    return __longlong_as_double((long long)b);
+}
+
+__device__ __forceinline__ void list128_offer(K128 &slot, const K128 &mine, int lane, int k, K128 &thr)
+{
+    unsigned long long cm = __ballot(nz128(mine) && gt128(mine, thr));
+    while (cm) {
+        const int src = __ffsll((long long)cm) - 1;
+        cm &= cm - 1;
+        const K128 nk = {readlane64(mine.hi, src), readlane64(mine.lo, src)};
+        if (!gt128(nk, thr)) continue;
+        const int pos = __popcll(__ballot(lane < k && gt128(slot, nk)));
+        const K128 prev = {shfl_up1_64(slot.hi), shfl_up1_64(slot.lo)};
+        if (lane < k) {   // per field: a select of whole structs goes through scratch
+            slot.hi = lane < pos ? slot.hi : (lane == pos ? nk.hi : prev.hi);
+            slot.lo = lane < pos ? slot.lo : (lane == pos ? nk.lo : prev.lo);
+        }
+        thr = {readlane64(slot.hi, k - 1), readlane64(slot.lo, k - 1)};
+    }
+}
+
 // Append flagged lanes' values to a device list; the counter keeps counting
 // past cap so the host can see an overflow.
 __device__ __forceinline__ unsigned long long list_reserve(bool flag, int lane, unsigned long long *count,

@@ -92,6 +92,13 @@ constexpr unsigned kStatListFull = 16u;
 // latency bounds, bit2 feasible, bit 8+i model i misses its bound).
 constexpr unsigned kEntNoJ = 32u;   // feasible, but fast J proves it outside the top-k band
 
+// 128-bit selection key: (order-preserving bits of an fp64 J, bitwise-not of
+// the joint index), so that a larger key is better and equal J prefers the
+// lower index; 0 is "no entry".
+struct K128 {
+    unsigned long long hi, lo;
+};
+
 // Kernel mode of the fast kernel.
 enum FastMode { kModeSearch = 0, kModeCollect = 1, kModeList = 2 };
 
@@ -230,6 +237,44 @@ struct SelectArgs {
     DevResult *res;
 };
 
+// Fixed observed state (Section III-B): per option row, the canonical terms
+// of the row's model under the fixed aggregate input, 32 bytes.  flags:
+// kRowOk the latency bound (and floor) holds, kRowP / kRowPen subtract P /
+// pen after J = fma(omega, q, J) (Eq. 3 only; the linear objective has q =
+// thr and neither).
+constexpr int kFixedWaves = 8;               // waves per workgroup of the fixed-state scan
+constexpr unsigned kRowOk = 1u, kRowP = 2u, kRowPen = 4u;
+struct FixedRow {
+    double q, P, pen;
+    float vram;
+    uint32_t flags;
+};
+
+struct FixedArgs {
+    int n_models, L, A, H1, H2, bf16, sumK;
+    int32_t K[kMaxN];
+    int32_t opt_off[kMaxN];
+    uint32_t magic[kMaxN];
+    uint32_t stride_digits[kMaxN];   // mixed-radix digits of (total waves * 64) mod |Lambda|
+    const int32_t *row_model;        // device [sumK]
+    const float *features;           // device [sumK][L]
+    const float *weights;            // device canonical image [N][wstride]
+    int64_t wstride;
+    float state[kMaxN];              // observed aggregate, original slot order ([A])
+    int vram_col;                    // feature column of the VRAM slot
+    float vram_cap;
+    const float *sla, *omega;        // device [N]
+    uint64_t lo, n;
+    int total_waves, top_k;
+    FixedRow *rows;                  // [sumK]
+    float2 *pred_rows;               // [sumK] canonical (lat, thr) rounded to fp32
+    K128 *wg_lists;                  // [grid][top_k]
+    DevResult *res;
+    uint8_t *mask;                   // dump (optional)
+    float *pred;                     // dump (optional)
+    ObjArgs obj;
+};
+
 // GA problem constants (kernel-argument block).
 struct GAConst {
     int N, L, A, H1, H2, bf16;
@@ -270,6 +315,8 @@ hipError_t launch_canonical(const CanonArgs &a, int n_entries_max, bool search_m
 hipError_t launch_kth_candidate(const unsigned long long *cand_keys, const double *ent_J, const uint32_t *ent_flags,
                                 int kp, int k, DevResult *res, hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, const FastConst &fc, const float *omega, hipStream_t s);
+size_t fixed_lds_bytes(int sumK);
+hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 int ga_fitness_supported(int nin, int h1, int h2);
 hipError_t launch_ga_feasible(const GAConst &c, uint32_t *blk_count, uint64_t *blk_off, unsigned long long *n_fl,
                               uint32_t *fl, hipStream_t st);

@@ -17,6 +17,8 @@ LIB_PATH = os.path.join(HERE, "libmf.so")
 MF_OK, MF_EINVAL, MF_ENOMEM, MF_EDEVICE, MF_EUNSUPPORTED, MF_EOVERFLOW, MF_EINTERNAL = range(7)
 MF_F32, MF_BF16 = 0, 1
 MF_DUMP = 1
+MF_FIXED_STATE = 2
+MAX_AGG = 16
 MAX_TOPK = 64
 MAX_MODELS = 16
 
@@ -56,7 +58,7 @@ class Objective(C.Structure):
 class SearchArgs(C.Structure):
     _fields_ = [("lo", C.c_uint64), ("hi", C.c_uint64), ("top_k", C.c_int32), ("flags", C.c_uint32),
                 ("d_sla", C.c_void_p), ("d_omega", C.c_void_p), ("d_mask", C.c_void_p),
-                ("d_pred", C.c_void_p), ("objective", Objective)]
+                ("d_pred", C.c_void_p), ("objective", Objective), ("state", C.c_float * MAX_AGG)]
 
 
 def objective_args(obj, n_models: int) -> Objective:
@@ -149,6 +151,7 @@ class Problem:
         import torch
         self.inst = inst
         self.N = int(inst.n_models)
+        self.A = int(inst.n_agg)
         self.device = torch.device(device)
         self._n_options = np.ascontiguousarray(inst.n_options, np.int32)
         self._agg_cols = np.ascontiguousarray(inst.agg_cols, np.int32)
@@ -213,12 +216,14 @@ class Problem:
             self._ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
         return self._ws
 
-    def search(self, sla, omega, k=1, lo=0, hi=None, dump=False, stream=None, objective=None):
+    def search(self, sla, omega, k=1, lo=0, hi=None, dump=False, stream=None, objective=None, state=None):
         """Exhaustive search over [lo, hi).  Returns a dict of counts and the
         exact top-k; with dump=True also the per-index mask and fast-path
         predictions (device tensors).  objective: None (linear) or an object
         with alpha, beta, delta, tau, prev_variant (Eq. 3; the problem must
-        have been created with variants)."""
+        have been created with variants).  state: None (each candidate's own
+        aggregate feeds the surrogates) or the observed aggregate [A] held
+        fixed for the whole search (Section III-B)."""
         import torch
         if hi is None:
             hi = self.space_size
@@ -228,8 +233,15 @@ class Problem:
         if dump:
             mask = torch.zeros(max(hi - lo, 1), dtype=torch.uint8, device=self.device)
             pred = torch.zeros((max(hi - lo, 1), self.N, 2), dtype=torch.float32, device=self.device)
-        args = SearchArgs(lo, hi, int(k), MF_DUMP if dump else 0, _ptr(d_sla), _ptr(d_om),
+        flags = (MF_DUMP if dump else 0) | (MF_FIXED_STATE if state is not None else 0)
+        args = SearchArgs(lo, hi, int(k), flags, _ptr(d_sla), _ptr(d_om),
                           _ptr(mask), _ptr(pred), objective_args(objective, self.N))
+        if state is not None:
+            st = np.asarray(state, np.float32).reshape(-1)
+            if st.size != self.A:
+                raise ValueError(f"state has {st.size} values, the problem {self.A} aggregate slots")
+            for t in range(st.size):
+                args.state[t] = float(st[t])
         nbytes = C.c_size_t()
         _check(lib.mf_workspace_size(self.handle, C.byref(args), C.byref(nbytes)), "mf_workspace_size")
         ws = self.workspace(nbytes.value)
