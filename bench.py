@@ -64,7 +64,7 @@ def cpu_baseline(inst, threads):
                       f"fp64 brute force, {dt:.2f} s"}
 
 
-def measure_search(mf, torch, inst, k, steps, warmup, objective=None):
+def measure_search(mf, torch, inst, k, steps, warmup, objective=None, state=None):
     import ctypes
     import numpy as np
     n = inst.space_size
@@ -72,8 +72,11 @@ def measure_search(mf, torch, inst, k, steps, warmup, objective=None):
     dev = p.device
     d_sla = torch.as_tensor(inst.sla, device=dev)
     d_om = torch.as_tensor(inst.omega, device=dev)
-    sargs = mf.SearchArgs(0, n, k, 0, d_sla.data_ptr(), d_om.data_ptr(), None, None,
-                          mf.objective_args(objective, inst.n_models))
+    sargs = mf.SearchArgs(0, n, k, 0 if state is None else mf.MF_FIXED_STATE, d_sla.data_ptr(), d_om.data_ptr(),
+                          None, None, mf.objective_args(objective, inst.n_models))
+    if state is not None:
+        for t, v in enumerate(state):
+            sargs.state[t] = float(v)
     nbytes = ctypes.c_size_t()
     mf._check(mf.lib.mf_workspace_size(p.handle, ctypes.byref(sargs), ctypes.byref(nbytes)), "ws")
     ws = torch.empty(nbytes.value, dtype=torch.uint8, device=dev)
@@ -122,6 +125,40 @@ def bench_n8(mf, torch, seed, steps, warmup):
             "argmax": int(r.top_idx[0]), "roofline": n8_roofline(inst, kms)}
 
 
+# LDS bandwidth of the chip: 128 bytes per clock per CU, 256 CUs, 2.4 GHz
+PEAK_LDS_GBS = 128 * 256 * 2.4
+
+
+def fixed_row_bytes(inst):
+    # the scan reads one 32-byte per-option record per model from LDS
+    return 32 * inst.n_models
+
+
+def bench_fixed(mf, torch, seed, steps, warmup):
+    """The searches with the observed state held fixed (Section III-B): the
+    surrogates run once per option row, the joint space is scanned over the
+    per-row canonical terms."""
+    from paper_2609_02109_amd import synth
+    out = {}
+    for name, inst, k, ob in (("n6", synth.cfg2(seed), 1, None),
+                              ("n6_eq3", synth.cfg2(seed), 1, "eq3"),
+                              ("n8", synth.cfg4(seed), 64, None)):
+        obj = synth.make_objective(inst, seed) if ob else None
+        st = synth.make_state(inst, seed)
+        ms, kms, r = measure_search(mf, torch, inst, k, steps, warmup, objective=obj, state=st)
+        n = inst.space_size
+        lds = fixed_row_bytes(inst) * n / (kms * 1e-3) / 1e9
+        log(f"fixed-state {name}: {ms:.3f} ms/step, scan kernel {kms:.3f} ms, n_feas={r.n_feas} "
+            f"argmax={r.top_idx[0]}")
+        out[name] = {"ms_to_top": ms, "top_k": k, "joint_configs_per_s": n / (ms * 1e-3), "scan_kernel_ms": kms,
+                     "n_feas": int(r.n_feas), "argmax": int(r.top_idx[0]),
+                     "roofline": {"bound": "lds", "achieved": lds, "peak": PEAK_LDS_GBS, "unit": "GB/s",
+                                  "frac": lds / PEAK_LDS_GBS, "bytes_per_config": fixed_row_bytes(inst)}}
+    out["workload"] = ("the N=6 and N=8 searches with the surrogates' aggregate input held at a seeded observed "
+                       "state (linear objective; N=6 also with Eq. 3)")
+    return out
+
+
 def bench_ga(args):
     import torch
     from paper_2609_02109_amd import mf, synth
@@ -155,10 +192,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--workload", choices=["n6", "ga", "n8"], default="n6",
+    ap.add_argument("--workload", choices=["n6", "ga", "n8", "fixed"], default="n6",
                     help="n6: the N=6 exhaustive search (the benchmark step); ga: the N=5 GA scheduler; "
-                         "n8: only the N=8 bf16 search")
+                         "n8: only the N=8 bf16 search; fixed: only the fixed-state searches")
     ap.add_argument("--no-n8", action="store_true", help="skip the N=8 bf16 search in the n6 line")
+    ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-state searches in the n6 line")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="run one plain device copy kernel of this many bytes read (and written) "
                          "before the search: the calibration point for HBM byte counters")
@@ -174,6 +212,9 @@ def main():
         return bench_ga(args)
     if args.workload == "n8":
         print(json.dumps(bench_n8(mf, torch, args.seed, args.steps, args.warmup)), flush=True)
+        return
+    if args.workload == "fixed":
+        print(json.dumps(bench_fixed(mf, torch, args.seed, args.steps, args.warmup)), flush=True)
         return
 
     if args.copy_bytes:
@@ -200,6 +241,8 @@ def main():
     ob = synth.make_objective(inst, args.seed)
     ms3, kms3, r3 = measure_search(mf, torch, inst, 1, args.steps, args.warmup, objective=ob)
     log(f"eq3 search: {ms3:.2f} ms/step, fast kernel {kms3:.2f} ms, n_feas={r3.n_feas} n_flagged={r3.n_flagged}")
+
+    fixed = None if args.no_fixed else bench_fixed(mf, torch, args.seed, max(args.steps, 20), max(args.warmup, 3))
 
     cpu = None
     if not args.no_cpu:
@@ -234,7 +277,8 @@ def main():
                               "joint_configs_per_s": n / (ms3 * 1e-3), "fast_kernel_ms": kms3,
                               "fast_kernel_frac": algorithmic_flops_per_config(inst) * n / (kms3 * 1e-3) / 1e12
                               / PEAK_FP32_TFLOPS, "n_feas": int(r3.n_feas), "n_flagged": int(r3.n_flagged),
-                              "argmax": int(r3.top_idx[0])}},
+                              "argmax": int(r3.top_idx[0])},
+                   "fixed_state": fixed},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_FP32_TFLOPS, "traffic": measured_traffic(),
                      "kernel": "fast_kernel<8,6,64>", "kernel_ms": kms,

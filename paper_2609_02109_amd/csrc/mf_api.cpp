@@ -589,40 +589,91 @@ mf_status search_range(mf_problem *p, const mf_search_args *args, uint64_t lo, u
 // ---- fixed observed state (MF_FIXED_STATE)
 
 constexpr uint64_t kFixedChunk = 1ull << 36;   // configurations per scan launch set
+constexpr uint32_t kFixedInnerMin = 256;       // inner configurations per block (unless the space is smaller)
 
 struct FixedWs {
-    size_t res, rows, prow, lists, total;
+    size_t res, rows, pens, prow, lists, total;
     int grid;
 };
 
-FixedWs fixed_ws_layout(const mf_problem &p, uint64_t n, int top_k)
+// Inner models: the shortest suffix whose configurations number at least
+// kFixedInnerMin (all models if none does).
+void fixed_split(const mf_problem &p, int &n_outer, uint32_t &inner)
+{
+    uint64_t m = 1;
+    int j = p.N;
+    while (j > 0 && m < kFixedInnerMin) {
+        j--;
+        m *= (uint64_t)p.K[j];
+    }
+    n_outer = j;
+    inner = (uint32_t)m;
+}
+
+uint64_t fixed_blocks(const mf_problem &p, uint64_t lo, uint64_t n, uint64_t &block0)
+{
+    int n_outer;
+    uint32_t M;
+    fixed_split(p, n_outer, M);
+    block0 = lo / M;
+    const uint64_t hi = lo + n;
+    const uint64_t block_end = hi / M + (hi % M != 0 ? 1 : 0);
+    return block_end - block0;
+}
+
+// One wave per block at least; at most the workgroups the CUs hold at once
+// (every wave gets the same number of blocks, so one resident round).
+int fixed_grid(const mf_problem &p, uint64_t n_blocks, int wgs_per_cu)
+{
+    const uint64_t g = (n_blocks + kFixedWaves - 1) / kFixedWaves;
+    return (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)p.num_cus * wgs_per_cu));
+}
+
+FixedWs fixed_ws_layout(const mf_problem &p, int grid, int top_k)
 {
     FixedWs w{};
-    const uint64_t tiles = (n + 63) / 64;
-    const uint64_t g = (tiles + kFixedWaves - 1) / kFixedWaves;
-    w.grid = (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)p.num_cus * 8));
+    w.grid = grid;
     size_t o = 0;
     w.res = o; o = align256(o + sizeof(DevResult));
     w.rows = o; o = align256(o + (size_t)p.sumK * sizeof(FixedRow));
+    w.pens = o; o = align256(o + (size_t)p.sumK * sizeof(FixedPen));
     w.prow = o; o = align256(o + (size_t)p.sumK * 8);
-    w.lists = o; o = align256(o + (size_t)w.grid * top_k * sizeof(K128));
+    w.lists = o; o = align256(o + (size_t)grid * top_k * sizeof(K128));
     w.total = o;
     return w;
+}
+
+size_t fixed_ws_bytes(const mf_problem &p, int top_k)
+{
+    return fixed_ws_layout(p, p.num_cus * kFixedMaxWgsPerCu, top_k).total;
 }
 
 // The search with the aggregate input held at args->state: one table of
 // canonical per-row terms, then scans of the joint space in chunks.
 mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipStream_t s, mf_result &acc)
 {
-    const uint64_t n_all = args->hi - args->lo;
-    if (n_all == 0) return MF_OK;
-    const FixedWs w = fixed_ws_layout(*p, std::min<uint64_t>(n_all, kFixedChunk), args->top_k);
+    if (args->hi == args->lo) return MF_OK;
+    const FixedWs w = fixed_ws_layout(*p, p->num_cus * kFixedMaxWgsPerCu, args->top_k);
     FixedArgs a{};
     a.n_models = p->N; a.L = p->L; a.A = p->A; a.H1 = p->H1; a.H2 = p->H2; a.bf16 = p->bf16; a.sumK = p->sumK;
     for (int i = 0; i < p->N; i++) {
         a.K[i] = p->K[i];
         a.opt_off[i] = p->opt_off[i];
         a.magic[i] = magic_for(p->K[i]);
+    }
+    fixed_split(*p, a.n_outer, a.inner);
+    for (int t = 0; t < p->N - a.n_outer; t++) {
+        a.in_K[t] = p->K[a.n_outer + t];
+        a.in_off[t] = p->opt_off[a.n_outer + t];
+        a.in_magic[t] = magic_for(p->K[a.n_outer + t]);
+    }
+    // lane-constant last digit: two inner models, the last with a power of
+    // two options dividing 64, and the block a whole number of 64-tiles
+    a.lc_shift = -1;
+    if (p->N - a.n_outer == 2 && a.inner % 64 == 0) {
+        const int kb = a.in_K[1];
+        for (int sh = 0; sh <= 6; sh++)
+            if (kb == (1 << sh)) a.lc_shift = sh;
     }
     a.row_model = p->d_row_model;
     a.features = p->d_features;
@@ -635,29 +686,32 @@ mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipS
     a.omega = args->d_omega;
     a.top_k = args->top_k;
     a.rows = reinterpret_cast<FixedRow *>(ws + w.rows);
+    a.pens = reinterpret_cast<FixedPen *>(ws + w.pens);
     a.pred_rows = reinterpret_cast<float2 *>(ws + w.prow);
     a.wg_lists = reinterpret_cast<K128 *>(ws + w.lists);
     a.res = reinterpret_cast<DevResult *>(ws + w.res);
     a.obj = obj_args(p, args->objective);
     const bool dump = (args->flags & MF_DUMP) != 0;
+    const int wgs_per_cu = fixed_wgs_per_cu(a);
 
     hipEvent_t ev0 = nullptr, ev1 = nullptr;
     MF_HIP(hipEventCreate(&ev0));
     if (hipEventCreate(&ev1) != hipSuccess) { (void)hipEventDestroy(ev0); return MF_EDEVICE; }
     mf_status st = MF_OK;
-    for (uint64_t lo = args->lo; lo < args->hi && st == MF_OK;) {
+    for (uint64_t lo = args->lo; lo < args->hi;) {
         const uint64_t n = std::min<uint64_t>(args->hi - lo, kFixedChunk);
-        const FixedWs wc = fixed_ws_layout(*p, n, args->top_k);
         a.lo = lo;
         a.n = n;
-        a.total_waves = wc.grid * kFixedWaves;
-        stride_digits(*p, (uint64_t)a.total_waves * 64u, a.stride_digits);
+        a.n_blocks = fixed_blocks(*p, lo, n, a.block0);
+        const int grid = fixed_grid(*p, a.n_blocks, wgs_per_cu);
+        const uint64_t waves = (uint64_t)grid * kFixedWaves;
+        a.blocks_per_wave = (a.n_blocks + waves - 1) / waves;
         a.mask = dump ? args->d_mask + (lo - args->lo) : nullptr;
         a.pred = dump ? args->d_pred + (lo - args->lo) * (uint64_t)p->N * 2u : nullptr;
         DevResult h{};
         float ms = 0.f;
         if (hipMemsetAsync(a.res, 0, sizeof(DevResult), s) != hipSuccess ||
-            launch_fixed(a, wc.grid, lo == args->lo, s, ev0, ev1) != hipSuccess ||
+            launch_fixed(a, grid, lo == args->lo, s, ev0, ev1) != hipSuccess ||
             hipMemcpyAsync(&h, a.res, sizeof(DevResult), hipMemcpyDeviceToHost, s) != hipSuccess ||
             hipStreamSynchronize(s) != hipSuccess || hipEventElapsedTime(&ms, ev0, ev1) != hipSuccess) {
             st = MF_EDEVICE;
@@ -1086,7 +1140,7 @@ mf_status mf_workspace_size(const mf_problem *p, const mf_search_args *args, siz
     mf_status st = check_search_args(p, args);
     if (st != MF_OK) return st;
     if (args->flags & MF_FIXED_STATE) {
-        *bytes = fixed_ws_layout(*p, std::min<uint64_t>(args->hi - args->lo, kFixedChunk), args->top_k).total;
+        *bytes = fixed_ws_bytes(*p, args->top_k);
         return MF_OK;
     }
     const uint64_t n = std::min<uint64_t>(args->hi - args->lo, kMaxLaunch);
@@ -1102,7 +1156,7 @@ mf_status mf_search(mf_problem *p, const mf_search_args *args, void *d_ws, size_
     if (st != MF_OK) return st;
     const uint64_t n = args->hi - args->lo;
     const bool fixed = (args->flags & MF_FIXED_STATE) != 0;
-    const size_t need = fixed ? fixed_ws_layout(*p, std::min<uint64_t>(n, kFixedChunk), args->top_k).total
+    const size_t need = fixed ? fixed_ws_bytes(*p, args->top_k)
                               : ws_layout(*p, std::min<uint64_t>(n, kMaxLaunch), args->top_k).total;
     if (ws_bytes < need) return MF_ENOMEM;
     if (((uintptr_t)d_ws & 255u) != 0) return MF_EINVAL;

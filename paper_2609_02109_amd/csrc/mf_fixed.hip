@@ -5,11 +5,14 @@
 // With the aggregate input fixed, model i's prediction depends on its own
 // option only, so the surrogates run once per option row (sum_i K_i canonical
 // forwards, `fixed_table_kernel`) and the joint search sums table entries
-// under the VRAM cap (`fixed_scan_kernel`): per configuration a decode, N LDS
-// reads, an fp32 VRAM sum and the canonical fp64 objective chain.  Every value
-// the scan combines is canonical, and it combines them in the canonical order,
-// so the search is exact without any certification: top-k are selected on
-// 128-bit (J, index) keys, per wave, per workgroup, then over the grid.
+// under the VRAM cap (`fixed_scan_kernel`).  Every value the scan combines is
+// canonical and it combines them in the canonical order (model 0 first), so
+// the search is exact without any certification.  The scan shares the chain's
+// prefix: per block of configurations that agree on the outer models, the
+// outer part of the chain (J, VRAM sum, service flag) is computed once, and
+// each lane adds the inner models of its own configuration (two LDS rows per
+// configuration at the usual shapes).  Top-k are selected on 128-bit (J,
+// index) keys, per wave, per workgroup, then over the grid.
 #include "mf_canon.h"
 
 namespace mfi {
@@ -43,152 +46,278 @@ __global__ void __launch_bounds__(64) fixed_table_kernel(const FixedArgs a)
         canon_model<BF16>(a.weights + (int64_t)i * a.wstride, nin, a.H1, a.H2, zs, h1s, h2s, lane, lat, thr);
         if (lane == 0) {
             FixedRow row;
+            FixedPen pp = {0.0, 0.0};
             uint32_t fl = lat <= (double)a.sla[i] ? kRowOk : 0u;
             row.q = thr;
-            row.P = 0.0;
-            row.pen = 0.0;
             if (a.obj.kind != 0) {
                 bool do_P, do_pen;
-                if (!canon_eq3(a.obj, r, thr, s_tau[i], s_prev[i], row.q, row.P, do_P, row.pen, do_pen)) fl = 0u;
+                if (!canon_eq3(a.obj, r, thr, s_tau[i], s_prev[i], row.q, pp.P, do_P, pp.pen, do_pen)) fl = 0u;
                 fl |= (do_P ? kRowP : 0u) | (do_pen ? kRowPen : 0u);
             }
             row.vram = x[a.vram_col];
             row.flags = fl;
             a.rows[r] = row;
+            a.pens[r] = pp;
             a.pred_rows[r] = make_float2((float)lat, (float)thr);
         }
     }
 }
 
+// One model's step of the canonical chain: VRAM sum, service flags (ANDed;
+// kRowOk is bit 0), J.
+template <bool EQ3>
+__device__ __forceinline__ void chain_step(const FixedRow &r, const FixedPen *pens, uint32_t row, double om,
+                                           double &J, float &v, uint32_t &fl)
+{
+    v += r.vram;
+    fl &= r.flags;
+    J = fma(om, r.q, J);
+    if (EQ3) {
+        const FixedPen pp = pens[row];
+        if (r.flags & kRowP) J = J - pp.P;
+        if (r.flags & kRowPen) J = J - pp.pen;
+    }
+}
+
+template <bool EQ3>
+__device__ __forceinline__ void chain_row(const FixedRow *rows, const FixedPen *pens, uint32_t row, double om,
+                                          double &J, float &v, uint32_t &fl)
+{
+    chain_step<EQ3>(rows[row], pens, row, om, J, v, fl);
+}
+
+// Offer the lanes' feasible (J, index) to the wave's top-k list.  A key can
+// only enter if its J is at least the J of the list's k-th key (thrJ, -inf
+// while the list is not full), so that test screens lanes before any 128-bit
+// key is formed.
+__device__ __forceinline__ void offer_feasible(K128 &slot, K128 &thr, double &thrJ, bool feas, double J, uint64_t idx,
+                                               int lane, int k)
+{
+    const bool cand = feas && J >= thrJ;
+    if (__ballot(cand) == 0ull) return;
+    list128_offer(slot, key_if(cand, K128{ord_f64(J), ~idx}), lane, k, thr);
+    thrJ = nz128(thr) ? unord_f64(thr.hi) : -INFINITY;
+}
+
 // ---------------------------------------------------------------------------
-// Scan: one configuration per lane, 64 per wave and step.
+// Scan: per wave a run of consecutive blocks; per block the outer prefix once
+// (wave-uniform, from LDS), then the inner configurations 64 at a time, one
+// per lane.  NI: compile-time bound on the number of inner models.  LC (NI =
+// 2 only): the last model's digit is lane-constant (its row lives in
+// registers) and the other inner digit is a shift of the tile offset.
 // ---------------------------------------------------------------------------
-template <int MAXN>
+template <int NI, bool EQ3, bool LC>
 __global__ void __launch_bounds__(kFixedWaves * 64) fixed_scan_kernel(const FixedArgs a)
 {
     extern __shared__ float4 smem4[];
+    __shared__ double s_om[kMaxN];
+    __shared__ int32_t s_off[kMaxN], s_K[kMaxN];
+    __shared__ uint32_t s_od[kFixedWaves][kMaxN];   // outer digits of each wave's current block
     FixedRow *rows = reinterpret_cast<FixedRow *>(smem4);
-    double *om = reinterpret_cast<double *>(rows + a.sumK);
-    K128 *lst = reinterpret_cast<K128 *>(om + kMaxN);
-    const int N = a.n_models, k = a.top_k;
-    for (int t = threadIdx.x; t < a.sumK; t += blockDim.x) rows[t] = a.rows[t];
+    FixedPen *pens = reinterpret_cast<FixedPen *>(rows + a.sumK);
+    K128 *lst = reinterpret_cast<K128 *>(pens + (EQ3 ? a.sumK : 0));
+    const int N = a.n_models, nout = a.n_outer, ni = N - nout, k = a.top_k;
+#pragma unroll 1
+    for (int t = threadIdx.x; t < a.sumK; t += blockDim.x) {   // not unrolled: keeps registers for the scan
+        rows[t] = a.rows[t];
+        if (EQ3) pens[t] = a.pens[t];
+    }
+    if (threadIdx.x < (unsigned)N) s_om[threadIdx.x] = (double)a.omega[threadIdx.x];
 #pragma unroll
-    for (int i = 0; i < kMaxN; i++)
-        if (threadIdx.x == (unsigned)i && i < N) om[i] = (double)a.omega[i];
-    __syncthreads();
+    for (int j = 0; j < kMaxN; j++)   // compile-time index into the argument block
+        if (threadIdx.x == (unsigned)j) {
+            s_off[j] = a.opt_off[j];
+            s_K[j] = a.K[j];
+        }
+    double omi[NI];
+#pragma unroll
+    for (int t = 0; t < NI; t++) omi[t] = t < ni ? (double)a.omega[nout + t] : 0.0;
 
     const int lane = threadIdx.x & 63;
     const int wv = threadIdx.x >> 6;
-    const int gw = blockIdx.x * kFixedWaves + wv;
-    const uint64_t n = a.n;
-    const uint64_t n_tiles = (n + 63) >> 6;
-
-    // digits of this wave's first tile; advanced by the grid stride in mixed radix
-    uint32_t bd[MAXN];
-    {
-        uint64_t x = a.lo + (uint64_t)gw * 64u;
-#pragma unroll
-        for (int j = MAXN - 1; j >= 0; j--) {
-            if (j < N) {
-                bd[j] = (uint32_t)(x % (uint64_t)a.K[j]);
-                x /= (uint64_t)a.K[j];
-            } else {
-                bd[j] = 0;
-            }
-        }
-    }
-    K128 slot = {0ull, 0ull}, thr = {0ull, 0ull};
-    uint32_t c_vram = 0, c_feas = 0;
-
-    for (uint64_t tile = gw; tile < n_tiles; tile += (uint64_t)a.total_waves) {
-        const uint64_t off = tile * 64u + (uint64_t)lane;
-        const bool valid = off < n;
-        uint32_t carry = (uint32_t)lane;
-        float vram = 0.f;
-        bool ok = true;
-        double J = 0.0;
-        uint32_t rowj[MAXN];
-#pragma unroll
-        for (int j = MAXN - 1; j >= 0; j--) {
-            if (j < N) {
-                const uint32_t t = bd[j] + carry;
-                const uint32_t q = a.magic[j] ? __umulhi(t, a.magic[j]) : t;
-                rowj[j] = (uint32_t)a.opt_off[j] + (t - q * (uint32_t)a.K[j]);
-                carry = q;
-            } else {
-                rowj[j] = 0;
-            }
-        }
-        // VRAM sum and the objective chain, model order
-#pragma unroll
-        for (int j = 0; j < MAXN; j++) {
-            if (j < N) {
-                const FixedRow r = rows[rowj[j]];
-                vram += r.vram;
-                ok = ok && (r.flags & kRowOk);
-                J = fma(om[j], r.q, J);
-                if (r.flags & kRowP) J = J - r.P;
-                if (r.flags & kRowPen) J = J - r.pen;
-            }
-        }
-        const bool vram_ok = (double)vram <= (double)a.vram_cap;
-        const bool feas = valid && vram_ok && ok;
-        c_vram += (valid && vram_ok) ? 1u : 0u;
-        c_feas += feas ? 1u : 0u;
-        const K128 key = key_if(feas, K128{ord_f64(J), ~(a.lo + off)});
-        list128_offer(slot, key, lane, k, thr);
-        if (a.mask && valid) {
-            a.mask[off] = (uint8_t)((vram_ok ? 1u : 0u) | (ok ? 2u : 0u) | (feas ? 4u : 0u));
-#pragma unroll
-            for (int j = 0; j < MAXN; j++)
-                if (j < N) {
-                    const float2 pr = a.pred_rows[rowj[j]];
-                    a.pred[(off * (uint64_t)N + (uint64_t)j) * 2u + 0u] = pr.x;
-                    a.pred[(off * (uint64_t)N + (uint64_t)j) * 2u + 1u] = pr.y;
-                }
-        }
-        // advance the base digits by the grid stride
-        uint32_t c2 = 0;
-#pragma unroll
-        for (int j = MAXN - 1; j >= 0; j--) {
-            if (j < N) {
-                const uint32_t t = bd[j] + a.stride_digits[j] + c2;
-                c2 = t >= (uint32_t)a.K[j] ? 1u : 0u;
-                bd[j] = c2 ? t - (uint32_t)a.K[j] : t;
-            }
-        }
-    }
-
-    const unsigned long long sv = wave_sum64(c_vram), sf = wave_sum64(c_feas);
+    const uint64_t gw = (uint64_t)blockIdx.x * kFixedWaves + wv;
+    const uint64_t b_first = gw * a.blocks_per_wave;
+    const uint64_t b_begin = a.block0 + (b_first < a.n_blocks ? b_first : a.n_blocks);
+    const uint64_t b_end = a.block0 + (b_first + a.blocks_per_wave < a.n_blocks ? b_first + a.blocks_per_wave
+                                                                                : a.n_blocks);
+    const uint64_t idx_lo = a.lo, idx_hi = a.lo + a.n;
+    const uint32_t M = a.inner;
+    const float cap = a.vram_cap;
+    uint32_t *od = s_od[wv];
     if (lane == 0) {
-        if (sv) atomicAdd(&a.res->n_vram, sv);
-        if (sf) atomicAdd(&a.res->n_feas_sure, sf);
+        uint64_t x = b_begin;
+        for (int j = nout - 1; j >= 0; j--) {
+            od[j] = (uint32_t)(x % (uint64_t)a.K[j]);
+            x /= (uint64_t)a.K[j];
+        }
+    }
+    __syncthreads();
+
+    // LC: the last model's row of this lane, and the first row of the other
+    // inner model this lane starts at
+    FixedRow rb = {0.0, 0.f, 0u};
+    uint32_t row_b = 0, row_a0 = 0;
+    if (LC) {
+        const int sh = a.lc_shift;
+        row_b = (uint32_t)a.in_off[1] + ((uint32_t)lane & ((1u << sh) - 1u));
+        rb = rows[row_b];
+        row_a0 = (uint32_t)a.in_off[0] + ((uint32_t)lane >> sh);
+    }
+
+    K128 slot = {0ull, 0ull}, thr = {0ull, 0ull};
+    double thrJ = -INFINITY;
+    unsigned long long c_vram = 0, c_feas = 0;   // wave-uniform
+    double Jc = 0.0;      // chain over outer models 0..nout-2
+    float vc = 0.f;
+    uint32_t flc = ~0u;
+    bool need_full = true;
+
+    for (uint64_t b = b_begin; b < b_end; b++) {
+        if (need_full) {
+            Jc = 0.0;
+            vc = 0.f;
+            flc = ~0u;
+#pragma unroll 1
+            for (int j = 0; j < nout - 1; j++) chain_row<EQ3>(rows, pens, (uint32_t)s_off[j] + od[j], s_om[j], Jc, vc, flc);
+            need_full = false;
+        }
+        double Jp = Jc;
+        float vp = vc;
+        uint32_t flp = flc;
+        if (nout > 0)
+            chain_row<EQ3>(rows, pens, (uint32_t)s_off[nout - 1] + od[nout - 1], s_om[nout - 1], Jp, vp, flp);
+
+        const uint64_t base = b * (uint64_t)M;
+        // the block's valid offsets [u_lo, u_hi): whole except at the range ends
+        const uint32_t u_lo = base < idx_lo ? (uint32_t)(idx_lo - base) : 0u;
+        const uint32_t u_hi = idx_hi - base < (uint64_t)M ? (uint32_t)(idx_hi - base) : M;
+        for (uint32_t t0 = 0; t0 < M; t0 += 64) {
+            const uint32_t u = t0 + (uint32_t)lane;
+            const bool valid = u >= u_lo && u < u_hi;
+            uint32_t rr[NI];
+            double J = Jp;
+            float v = vp;
+            uint32_t fl = flp;
+            if (LC) {
+                rr[0] = row_a0 + (t0 >> a.lc_shift);
+                rr[1] = row_b;
+                chain_row<EQ3>(rows, pens, rr[0], omi[0], J, v, fl);
+                chain_step<EQ3>(rb, pens, row_b, omi[1], J, v, fl);
+            } else {
+                uint32_t uu = u < M ? u : 0u;
+#pragma unroll
+                for (int t = NI - 1; t >= 0; t--) {
+                    rr[t] = 0;
+                    if (t < ni) {
+                        // the first inner digit is what remains (uu < K there)
+                        const uint32_t q = (t > 0 && a.in_magic[t]) ? __umulhi(uu, a.in_magic[t]) : (t > 0 ? uu : 0u);
+                        rr[t] = (uint32_t)a.in_off[t] + (uu - q * (uint32_t)a.in_K[t]);
+                        uu = q;
+                    }
+                }
+#pragma unroll
+                for (int t = 0; t < NI; t++)
+                    if (t < ni) chain_row<EQ3>(rows, pens, rr[t], omi[t], J, v, fl);
+            }
+            const bool vram_ok = v <= cap;
+            const bool ok = (fl & kRowOk) != 0u;
+            const bool feas = valid && vram_ok && ok;
+            c_vram += (unsigned long long)__popcll(__ballot(valid && vram_ok));
+            c_feas += (unsigned long long)__popcll(__ballot(feas));
+            const uint64_t idx = base + u;
+            offer_feasible(slot, thr, thrJ, feas, J, idx, lane, k);
+            if (a.mask && valid) {
+                const uint64_t off = idx - idx_lo;
+                a.mask[off] = (uint8_t)((vram_ok ? 1u : 0u) | (ok ? 2u : 0u) | (feas ? 4u : 0u));
+                float *pd = a.pred + off * (uint64_t)N * 2u;
+#pragma unroll 1
+                for (int j = 0; j < nout; j++) {
+                    const float2 pr = a.pred_rows[s_off[j] + od[j]];
+                    pd[2 * j] = pr.x;
+                    pd[2 * j + 1] = pr.y;
+                }
+#pragma unroll
+                for (int t = 0; t < NI; t++)
+                    if (t < ni) {
+                        const float2 pr = a.pred_rows[rr[t]];
+                        pd[2 * (nout + t)] = pr.x;
+                        pd[2 * (nout + t) + 1] = pr.y;
+                    }
+            }
+        }
+        // next block: outer odometer (lane 0 writes the wave's digits; the
+        // wave reads them back after the write); a change above the last
+        // outer digit invalidates the cached prefix
+        bool carry = true;
+        for (int j = nout - 1; j >= 0 && carry; j--) {
+            uint32_t d = od[j] + 1u;
+            carry = d == (uint32_t)s_K[j];
+            if (carry) d = 0u;
+            __builtin_amdgcn_wave_barrier();
+            if (lane == 0) od[j] = d;
+            __builtin_amdgcn_wave_barrier();
+            if (j < nout - 1) need_full = true;
+        }
+    }
+
+    if (lane == 0) {
+        if (c_vram) atomicAdd(&a.res->n_vram, c_vram);
+        if (c_feas) atomicAdd(&a.res->n_feas_sure, c_feas);
     }
     lst[wv * 64 + lane] = key_if(lane < k, slot);
     __syncthreads();
     if (wv == 0) {
+#pragma unroll 1
         for (int w = 1; w < kFixedWaves; w++) list128_offer(slot, lst[w * 64 + lane], lane, k, thr);
         if (lane < k) a.wg_lists[(uint64_t)blockIdx.x * k + lane] = slot;
     }
 }
 
 // ---------------------------------------------------------------------------
-// Merge: the workgroup lists into the final top-k (one workgroup).
+// Merge: the workgroup lists into the final top-k (one workgroup).  Each list
+// is sorted and holds k keys, so the largest k-th key of any list bounds the
+// final k-th key from below: keys under it are dropped before selection.
+// Keys are loaded several per lane ahead of their selection.
 // ---------------------------------------------------------------------------
 constexpr int kFixedMergeWaves = 16;
+constexpr int kMergeAhead = 4;
 
 __global__ void __launch_bounds__(kFixedMergeWaves * 64)
 fixed_merge_kernel(const K128 *lists, int n_lists, int k, DevResult *R)
 {
     __shared__ K128 lst[kFixedMergeWaves * 64];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    // the largest k-th key over the lists
+    K128 lb = {0ull, 0ull};
+    for (int l = threadIdx.x; l < n_lists; l += blockDim.x) {
+        const K128 x = lists[(int64_t)l * k + (k - 1)];
+        if (gt128(x, lb)) lb = x;
+    }
+    lst[threadIdx.x] = lb;
+    __syncthreads();
+    for (int s = blockDim.x / 2; s > 0; s >>= 1) {
+        if ((int)threadIdx.x < s && gt128(lst[threadIdx.x + s], lst[threadIdx.x])) lst[threadIdx.x] = lst[threadIdx.x + s];
+        __syncthreads();
+    }
+    lb = lst[0];
+    __syncthreads();
+
     K128 slot = {0ull, 0ull}, thr = {0ull, 0ull};
     const int64_t n_keys = (int64_t)n_lists * k;
-    for (int64_t base = (int64_t)wv * 64; base < n_keys; base += kFixedMergeWaves * 64) {
-        const int64_t e = base + lane;
-        K128 key = {0ull, 0ull};
-        if (e < n_keys) key = lists[e];
-        list128_offer(slot, key, lane, k, thr);
+    const int64_t per_wave = (n_keys + kFixedMergeWaves - 1) / kFixedMergeWaves;
+    const int64_t e0 = (int64_t)wv * per_wave;
+    const int64_t e1 = e0 + per_wave < n_keys ? e0 + per_wave : n_keys;
+    for (int64_t base = e0; base < e1; base += 64 * kMergeAhead) {
+        K128 key[kMergeAhead];
+#pragma unroll
+        for (int q = 0; q < kMergeAhead; q++) {
+            const int64_t e = base + q * 64 + lane;
+            key[q] = K128{0ull, 0ull};
+            if (e < e1) key[q] = lists[e];
+        }
+#pragma unroll
+        for (int q = 0; q < kMergeAhead; q++)
+            list128_offer(slot, key_if(!gt128(lb, key[q]), key[q]), lane, k, thr);
     }
     lst[wv * 64 + lane] = key_if(lane < k, slot);
     __syncthreads();
@@ -207,9 +336,33 @@ fixed_merge_kernel(const K128 *lists, int n_lists, int k, DevResult *R)
     }
 }
 
-size_t fixed_lds_bytes(int sumK)
+size_t fixed_lds_bytes(int sumK, bool eq3)
 {
-    return (size_t)sumK * sizeof(FixedRow) + kMaxN * 8 + (size_t)kFixedWaves * 64 * sizeof(K128);
+    return (size_t)sumK * sizeof(FixedRow) + (eq3 ? (size_t)sumK * sizeof(FixedPen) : 0) +
+           (size_t)kFixedWaves * 64 * sizeof(K128);
+}
+
+using ScanFn = void (*)(const FixedArgs);
+
+static ScanFn scan_fn(const FixedArgs &a)
+{
+    const bool eq3 = a.obj.kind != 0;
+    const int ni = a.n_models - a.n_outer;
+    if (a.lc_shift >= 0) return eq3 ? fixed_scan_kernel<2, true, true> : fixed_scan_kernel<2, false, true>;
+    return ni <= 2 ? (eq3 ? fixed_scan_kernel<2, true, false> : fixed_scan_kernel<2, false, false>)
+         : ni <= 4 ? (eq3 ? fixed_scan_kernel<4, true, false> : fixed_scan_kernel<4, false, false>)
+                   : (eq3 ? fixed_scan_kernel<kMaxN, true, false> : fixed_scan_kernel<kMaxN, false, false>);
+}
+
+int fixed_wgs_per_cu(const FixedArgs &a)
+{
+    const ScanFn fn = scan_fn(a);
+    const size_t lds = fixed_lds_bytes(a.sumK, a.obj.kind != 0);
+    if (hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+        return 1;
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, kFixedWaves * 64, lds) != hipSuccess || n < 1) return 1;
+    return n < kFixedMaxWgsPerCu ? n : kFixedMaxWgsPerCu;
 }
 
 hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1)
@@ -222,8 +375,8 @@ hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s,
             hipLaunchKernelGGL(fixed_table_kernel<false>, dim3(a.sumK), dim3(64), 0, s, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    const size_t lds = fixed_lds_bytes(a.sumK);
-    auto fn = a.n_models <= 8 ? fixed_scan_kernel<8> : fixed_scan_kernel<16>;
+    const size_t lds = fixed_lds_bytes(a.sumK, a.obj.kind != 0);
+    const ScanFn fn = scan_fn(a);
     e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     if ((e = hipEventRecord(ev0, s)) != hipSuccess) return e;

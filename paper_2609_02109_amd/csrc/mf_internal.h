@@ -238,24 +238,41 @@ struct SelectArgs {
 };
 
 // Fixed observed state (Section III-B): per option row, the canonical terms
-// of the row's model under the fixed aggregate input, 32 bytes.  flags:
-// kRowOk the latency bound (and floor) holds, kRowP / kRowPen subtract P /
-// pen after J = fma(omega, q, J) (Eq. 3 only; the linear objective has q =
-// thr and neither).
+// of the row's model under the fixed aggregate input.  FixedRow (16 bytes):
+// q (thr for the linear objective, Q f under Eq. 3), the row's VRAM value and
+// flags: kRowOk the latency bound (and floor) holds, kRowP / kRowPen subtract
+// FixedPen's P / pen after J = fma(omega, q, J) (Eq. 3 only).
 constexpr int kFixedWaves = 8;               // waves per workgroup of the fixed-state scan
+constexpr int kFixedMaxWgsPerCu = 4;         // resident scan workgroups per CU at most (grid = CUs x that)
 constexpr unsigned kRowOk = 1u, kRowP = 2u, kRowPen = 4u;
 struct FixedRow {
-    double q, P, pen;
+    double q;
     float vram;
     uint32_t flags;
 };
+struct FixedPen {
+    double P, pen;
+};
 
+// The scan splits the models into an outer prefix 0..n_outer-1 and the inner
+// models n_outer..N-1 (inner space of `inner` configurations, at least 256
+// unless the whole space is smaller).  Joint index = block * inner + u; a
+// wave takes blocks_per_wave consecutive blocks, computes the outer prefix of
+// the canonical chain once per block and the inner models per lane.
 struct FixedArgs {
     int n_models, L, A, H1, H2, bf16, sumK;
     int32_t K[kMaxN];
     int32_t opt_off[kMaxN];
     uint32_t magic[kMaxN];
-    uint32_t stride_digits[kMaxN];   // mixed-radix digits of (total waves * 64) mod |Lambda|
+    int n_outer;
+    uint32_t inner;
+    int32_t in_K[kMaxN];             // K, first row and magic of inner model n_outer + t
+    int32_t in_off[kMaxN];
+    uint32_t in_magic[kMaxN];
+    uint64_t block0, n_blocks, blocks_per_wave;
+    int lc_shift;                    // >= 0: two inner models, the last with 2^lc_shift options
+                                     // dividing 64 and a block of whole 64-tiles (its digit is
+                                     // lane-constant); -1: general inner decode
     const int32_t *row_model;        // device [sumK]
     const float *features;           // device [sumK][L]
     const float *weights;            // device canonical image [N][wstride]
@@ -264,9 +281,10 @@ struct FixedArgs {
     int vram_col;                    // feature column of the VRAM slot
     float vram_cap;
     const float *sla, *omega;        // device [N]
-    uint64_t lo, n;
-    int total_waves, top_k;
+    uint64_t lo, n;                  // index range [lo, lo + n)
+    int top_k;
     FixedRow *rows;                  // [sumK]
+    FixedPen *pens;                  // [sumK]
     float2 *pred_rows;               // [sumK] canonical (lat, thr) rounded to fp32
     K128 *wg_lists;                  // [grid][top_k]
     DevResult *res;
@@ -315,7 +333,8 @@ hipError_t launch_canonical(const CanonArgs &a, int n_entries_max, bool search_m
 hipError_t launch_kth_candidate(const unsigned long long *cand_keys, const double *ent_J, const uint32_t *ent_flags,
                                 int kp, int k, DevResult *res, hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, const FastConst &fc, const float *omega, hipStream_t s);
-size_t fixed_lds_bytes(int sumK);
+size_t fixed_lds_bytes(int sumK, bool eq3);
+int fixed_wgs_per_cu(const FixedArgs &a);
 hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 int ga_fitness_supported(int nin, int h1, int h2);
 hipError_t launch_ga_feasible(const GAConst &c, uint32_t *blk_count, uint64_t *blk_off, unsigned long long *n_fl,
