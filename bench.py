@@ -125,13 +125,26 @@ def bench_n8(mf, torch, seed, steps, warmup):
             "argmax": int(r.top_idx[0]), "roofline": n8_roofline(inst, kms)}
 
 
-# LDS bandwidth of the chip: 128 bytes per clock per CU, 256 CUs, 2.4 GHz
-PEAK_LDS_GBS = 128 * 256 * 2.4
+# Vector issue of the chip: one wave64 VALU instruction per clock per CU
+# (4 SIMD16 units, 4 clocks each), 256 CUs at 2.4 GHz, in G instructions/s
+PEAK_VALU_GINST = 256 * 2.4
 
 
-def fixed_row_bytes(inst):
-    # the scan reads one 32-byte per-option record per model from LDS
-    return 32 * inst.n_models
+def fixed_inner_models(inst):
+    """Models whose digits vary inside a block of the fixed-state scan: the
+    shortest suffix with at least 256 joint options (the library's split)."""
+    m, j = 1, inst.n_models
+    while j > 0 and m < 256:
+        j -= 1
+        m *= int(inst.n_options[j])
+    return inst.n_models - j
+
+
+def fixed_alg_ops(inst):
+    # per configuration: the inner models' chain steps (fp64 FMA, fp32 VRAM
+    # add, service-flag OR each) and the three decisions (VRAM cap, service,
+    # J screen against the k-th best); the outer prefix is shared per block
+    return 3 * fixed_inner_models(inst) + 3
 
 
 def bench_fixed(mf, torch, seed, steps, warmup):
@@ -147,13 +160,15 @@ def bench_fixed(mf, torch, seed, steps, warmup):
         st = synth.make_state(inst, seed)
         ms, kms, r = measure_search(mf, torch, inst, k, steps, warmup, objective=obj, state=st)
         n = inst.space_size
-        lds = fixed_row_bytes(inst) * n / (kms * 1e-3) / 1e9
+        ops = fixed_alg_ops(inst)
+        ach = ops / 64 * n / (kms * 1e-3) / 1e9
         log(f"fixed-state {name}: {ms:.3f} ms/step, scan kernel {kms:.3f} ms, n_feas={r.n_feas} "
             f"argmax={r.top_idx[0]}")
         out[name] = {"ms_to_top": ms, "top_k": k, "joint_configs_per_s": n / (ms * 1e-3), "scan_kernel_ms": kms,
                      "n_feas": int(r.n_feas), "argmax": int(r.top_idx[0]),
-                     "roofline": {"bound": "lds", "achieved": lds, "peak": PEAK_LDS_GBS, "unit": "GB/s",
-                                  "frac": lds / PEAK_LDS_GBS, "bytes_per_config": fixed_row_bytes(inst)}}
+                     "roofline": {"bound": "alu", "achieved": ach, "peak": PEAK_VALU_GINST,
+                                  "unit": "G VALU wave-instr/s", "frac": ach / PEAK_VALU_GINST,
+                                  "alg_lane_ops_per_config": ops}}
     out["workload"] = ("the N=6 and N=8 searches with the surrogates' aggregate input held at a seeded observed "
                        "state (linear objective; N=6 also with Eq. 3)")
     return out

@@ -668,9 +668,9 @@ mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipS
         a.in_magic[t] = magic_for(p->K[a.n_outer + t]);
     }
     // lane-constant last digit: two inner models, the last with a power of
-    // two options dividing 64, and the block a whole number of 64-tiles
+    // two options dividing 64, and the block whole pairs of 64-tiles
     a.lc_shift = -1;
-    if (p->N - a.n_outer == 2 && a.inner % 64 == 0) {
+    if (p->N - a.n_outer == 2 && a.inner % 128 == 0) {
         const int kb = a.in_K[1];
         for (int sh = 0; sh <= 6; sh++)
             if (kb == (1 << sh)) a.lc_shift = sh;
@@ -703,6 +703,8 @@ mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipS
         a.lo = lo;
         a.n = n;
         a.n_blocks = fixed_blocks(*p, lo, n, a.block0);
+        a.part_block_lo = lo % a.inner ? lo / a.inner : ~0ull;
+        a.part_block_hi = (lo + n) % a.inner ? (lo + n) / a.inner : ~0ull;
         const int grid = fixed_grid(*p, a.n_blocks, wgs_per_cu);
         const uint64_t waves = (uint64_t)grid * kFixedWaves;
         a.blocks_per_wave = (a.n_blocks + waves - 1) / waves;

@@ -47,11 +47,11 @@ __global__ void __launch_bounds__(64) fixed_table_kernel(const FixedArgs a)
         if (lane == 0) {
             FixedRow row;
             FixedPen pp = {0.0, 0.0};
-            uint32_t fl = lat <= (double)a.sla[i] ? kRowOk : 0u;
+            uint32_t fl = lat <= (double)a.sla[i] ? 0u : kRowBad;
             row.q = thr;
             if (a.obj.kind != 0) {
                 bool do_P, do_pen;
-                if (!canon_eq3(a.obj, r, thr, s_tau[i], s_prev[i], row.q, pp.P, do_P, pp.pen, do_pen)) fl = 0u;
+                if (!canon_eq3(a.obj, r, thr, s_tau[i], s_prev[i], row.q, pp.P, do_P, pp.pen, do_pen)) fl = kRowBad;
                 fl |= (do_P ? kRowP : 0u) | (do_pen ? kRowPen : 0u);
             }
             row.vram = x[a.vram_col];
@@ -63,14 +63,14 @@ __global__ void __launch_bounds__(64) fixed_table_kernel(const FixedArgs a)
     }
 }
 
-// One model's step of the canonical chain: VRAM sum, service flags (ANDed;
-// kRowOk is bit 0), J.
+// One model's step of the canonical chain: VRAM sum, service flags (ORed;
+// kRowBad is the sign bit), J.
 template <bool EQ3>
 __device__ __forceinline__ void chain_step(const FixedRow &r, const FixedPen *pens, uint32_t row, double om,
                                            double &J, float &v, uint32_t &fl)
 {
     v += r.vram;
-    fl &= r.flags;
+    fl |= r.flags;
     J = fma(om, r.q, J);
     if (EQ3) {
         const FixedPen pp = pens[row];
@@ -86,25 +86,103 @@ __device__ __forceinline__ void chain_row(const FixedRow *rows, const FixedPen *
     chain_step<EQ3>(rows[row], pens, row, om, J, v, fl);
 }
 
-// Offer the lanes' feasible (J, index) to the wave's top-k list.  A key can
-// only enter if its J is at least the J of the list's k-th key (thrJ, -inf
-// while the list is not full), so that test screens lanes before any 128-bit
-// key is formed.
-__device__ __forceinline__ void offer_feasible(K128 &slot, K128 &thr, double &thrJ, bool feas, double J, uint64_t idx,
-                                               int lane, int k)
+template <bool B>
+struct BoolC {
+    static constexpr bool value = B;
+};
+
+// Wave ballot of a lane predicate, straight into a scalar mask.
+__device__ __forceinline__ unsigned long long ballot64(bool b) { return __builtin_amdgcn_ballot_w64(b); }
+
+// Offer the lanes of candidate mask cm to the wave's top-k list, and refresh
+// thrJ, the J of the list's k-th key (-inf while the list is not full): a key
+// can only enter if its J is at least thrJ, so that test screens lanes before
+// any 128-bit key is formed.
+__device__ __forceinline__ void offer_mask(K128 &slot, K128 &thr, double &thrJ, unsigned long long cm, double J,
+                                        uint64_t idx, int lane, int k)
 {
-    const bool cand = feas && J >= thrJ;
-    if (__ballot(cand) == 0ull) return;
-    list128_offer(slot, key_if(cand, K128{ord_f64(J), ~idx}), lane, k, thr);
+    const bool mine = ((cm >> lane) & 1ull) != 0ull;
+    list128_offer(slot, key_if(mine, K128{ord_f64(J), ~idx}), lane, k, thr);
     thrJ = nz128(thr) ? unord_f64(thr.hi) : -INFINITY;
+}
+
+// One 64-configuration tile of a block: inner rows, and the chain from the
+// block's outer prefix.
+template <int NI>
+struct Tile {
+    double J;
+    float v;
+    uint32_t fl;
+    uint32_t rr[NI];
+};
+
+template <int NI, bool EQ3, bool LC>
+__device__ __forceinline__ Tile<NI> eval_tile(const FixedArgs &a, const FixedRow *rows, const FixedPen *pens,
+                                              uint32_t u, uint32_t t0, int ni, uint32_t M, const double *omi,
+                                              double Jp, float vp, uint32_t flp, const FixedRow &rb,
+                                              uint32_t row_a0, uint32_t row_b)
+{
+    Tile<NI> o;
+    o.J = Jp;
+    o.v = vp;
+    o.fl = flp;
+    if (LC) {
+        o.rr[0] = row_a0 + (t0 >> a.lc_shift);
+        o.rr[1] = row_b;
+        chain_row<EQ3>(rows, pens, o.rr[0], omi[0], o.J, o.v, o.fl);
+        chain_step<EQ3>(rb, pens, row_b, omi[1], o.J, o.v, o.fl);
+    } else {
+        uint32_t uu = u < M ? u : 0u;
+#pragma unroll
+        for (int t = NI - 1; t >= 0; t--) {
+            o.rr[t] = 0;
+            if (t < ni) {
+                // the first inner digit is what remains (uu < K there)
+                const uint32_t q = (t > 0 && a.in_magic[t]) ? __umulhi(uu, a.in_magic[t]) : (t > 0 ? uu : 0u);
+                o.rr[t] = (uint32_t)a.in_off[t] + (uu - q * (uint32_t)a.in_K[t]);
+                uu = q;
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < NI; t++)
+            if (t < ni) chain_row<EQ3>(rows, pens, o.rr[t], omi[t], o.J, o.v, o.fl);
+    }
+    return o;
+}
+
+template <int NI>
+__device__ __forceinline__ void dump_tile(const FixedArgs &a, const Tile<NI> &x, bool valid, float cap, uint64_t idx,
+                                          const int32_t *s_off, const uint32_t *od, uint32_t dl, int nout, int ni)
+{
+    if (!valid) return;
+    const bool vram_ok = x.v <= cap, ok = (int32_t)x.fl >= 0;
+    const int N = a.n_models;
+    const uint64_t off = idx - a.lo;
+    a.mask[off] = (uint8_t)((vram_ok ? 1u : 0u) | (ok ? 2u : 0u) | (vram_ok && ok ? 4u : 0u));
+    float *pd = a.pred + off * (uint64_t)N * 2u;
+#pragma unroll 1
+    for (int j = 0; j < nout; j++) {
+        const float2 pr = a.pred_rows[s_off[j] + (j == nout - 1 ? dl : od[j])];
+        pd[2 * j] = pr.x;
+        pd[2 * j + 1] = pr.y;
+    }
+#pragma unroll
+    for (int t = 0; t < NI; t++)
+        if (t < ni) {
+            const float2 pr = a.pred_rows[x.rr[t]];
+            pd[2 * (nout + t)] = pr.x;
+            pd[2 * (nout + t) + 1] = pr.y;
+        }
 }
 
 // ---------------------------------------------------------------------------
 // Scan: per wave a run of consecutive blocks; per block the outer prefix once
-// (wave-uniform, from LDS), then the inner configurations 64 at a time, one
-// per lane.  NI: compile-time bound on the number of inner models.  LC (NI =
-// 2 only): the last model's digit is lane-constant (its row lives in
-// registers) and the other inner digit is a shift of the tile offset.
+// (wave-uniform, from LDS), then the inner configurations two 64-tiles at a
+// time, one configuration per lane and tile.  Decisions become wave masks at
+// once (counts by popcount, candidates by mask).  NI: compile-time bound on
+// the number of inner models.  LC (NI = 2 only): the last model's digit is
+// lane-constant (its row lives in registers) and the other inner digit is a
+// shift of the tile offset.
 // ---------------------------------------------------------------------------
 template <int NI, bool EQ3, bool LC>
 __global__ void __launch_bounds__(kFixedWaves * 64) fixed_scan_kernel(const FixedArgs a)
@@ -134,7 +212,9 @@ __global__ void __launch_bounds__(kFixedWaves * 64) fixed_scan_kernel(const Fixe
     for (int t = 0; t < NI; t++) omi[t] = t < ni ? (double)a.omega[nout + t] : 0.0;
 
     const int lane = threadIdx.x & 63;
-    const int wv = threadIdx.x >> 6;
+    // the wave index is wave-uniform: say so, so that everything derived from
+    // it (blocks, digits, masks) stays in scalar registers
+    const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const uint64_t gw = (uint64_t)blockIdx.x * kFixedWaves + wv;
     const uint64_t b_first = gw * a.blocks_per_wave;
     const uint64_t b_begin = a.block0 + (b_first < a.n_blocks ? b_first : a.n_blocks);
@@ -169,14 +249,20 @@ __global__ void __launch_bounds__(kFixedWaves * 64) fixed_scan_kernel(const Fixe
     unsigned long long c_vram = 0, c_feas = 0;   // wave-uniform
     double Jc = 0.0;      // chain over outer models 0..nout-2
     float vc = 0.f;
-    uint32_t flc = ~0u;
+    uint32_t flc = 0u;
     bool need_full = true;
+    // the last outer model: its digit dl lives in a scalar register (the
+    // odometer in LDS is touched only when dl wraps)
+    uint32_t dl = nout > 0 ? od[nout - 1] : 0u;
+    const uint32_t K_last = nout > 0 ? (uint32_t)a.K[nout - 1] : 1u;
+    const uint32_t off_last = nout > 0 ? (uint32_t)a.opt_off[nout - 1] : 0u;
+    const double om_last = nout > 0 ? (double)a.omega[nout - 1] : 0.0;
 
     for (uint64_t b = b_begin; b < b_end; b++) {
         if (need_full) {
             Jc = 0.0;
             vc = 0.f;
-            flc = ~0u;
+            flc = 0u;
 #pragma unroll 1
             for (int j = 0; j < nout - 1; j++) chain_row<EQ3>(rows, pens, (uint32_t)s_off[j] + od[j], s_om[j], Jc, vc, flc);
             need_full = false;
@@ -184,79 +270,72 @@ __global__ void __launch_bounds__(kFixedWaves * 64) fixed_scan_kernel(const Fixe
         double Jp = Jc;
         float vp = vc;
         uint32_t flp = flc;
-        if (nout > 0)
-            chain_row<EQ3>(rows, pens, (uint32_t)s_off[nout - 1] + od[nout - 1], s_om[nout - 1], Jp, vp, flp);
+        if (nout > 0) chain_row<EQ3>(rows, pens, off_last + dl, om_last, Jp, vp, flp);
 
         const uint64_t base = b * (uint64_t)M;
-        // the block's valid offsets [u_lo, u_hi): whole except at the range ends
-        const uint32_t u_lo = base < idx_lo ? (uint32_t)(idx_lo - base) : 0u;
-        const uint32_t u_hi = idx_hi - base < (uint64_t)M ? (uint32_t)(idx_hi - base) : M;
-        for (uint32_t t0 = 0; t0 < M; t0 += 64) {
-            const uint32_t u = t0 + (uint32_t)lane;
-            const bool valid = u >= u_lo && u < u_hi;
-            uint32_t rr[NI];
-            double J = Jp;
-            float v = vp;
-            uint32_t fl = flp;
-            if (LC) {
-                rr[0] = row_a0 + (t0 >> a.lc_shift);
-                rr[1] = row_b;
-                chain_row<EQ3>(rows, pens, rr[0], omi[0], J, v, fl);
-                chain_step<EQ3>(rb, pens, row_b, omi[1], J, v, fl);
-            } else {
-                uint32_t uu = u < M ? u : 0u;
-#pragma unroll
-                for (int t = NI - 1; t >= 0; t--) {
-                    rr[t] = 0;
-                    if (t < ni) {
-                        // the first inner digit is what remains (uu < K there)
-                        const uint32_t q = (t > 0 && a.in_magic[t]) ? __umulhi(uu, a.in_magic[t]) : (t > 0 ? uu : 0u);
-                        rr[t] = (uint32_t)a.in_off[t] + (uu - q * (uint32_t)a.in_K[t]);
-                        uu = q;
-                    }
-                }
-#pragma unroll
-                for (int t = 0; t < NI; t++)
-                    if (t < ni) chain_row<EQ3>(rows, pens, rr[t], omi[t], J, v, fl);
-            }
-            const bool vram_ok = v <= cap;
-            const bool ok = (fl & kRowOk) != 0u;
-            const bool feas = valid && vram_ok && ok;
-            c_vram += (unsigned long long)__popcll(__ballot(valid && vram_ok));
-            c_feas += (unsigned long long)__popcll(__ballot(feas));
-            const uint64_t idx = base + u;
-            offer_feasible(slot, thr, thrJ, feas, J, idx, lane, k);
-            if (a.mask && valid) {
-                const uint64_t off = idx - idx_lo;
-                a.mask[off] = (uint8_t)((vram_ok ? 1u : 0u) | (ok ? 2u : 0u) | (feas ? 4u : 0u));
-                float *pd = a.pred + off * (uint64_t)N * 2u;
+        // every lane of every tile valid unless the block holds a range end
+        // (or a partial last tile)
+        const bool whole = b != a.part_block_lo && b != a.part_block_hi && (M & 63u) == 0u;
+        const uint32_t u_lo = whole ? 0u : (base < idx_lo ? (uint32_t)(idx_lo - base) : 0u);
+        const uint32_t u_hi = whole ? M : (idx_hi - base < (uint64_t)M ? (uint32_t)(idx_hi - base) : M);
+        const uint32_t u_span = u_hi - u_lo;
+
+        // the block's tiles, two at a time; WHOLE and DUMP are compile-time
+        auto tiles = [&](auto whole_c, auto dump_c) {
+            constexpr bool WHOLE = decltype(whole_c)::value, DUMP = decltype(dump_c)::value;
+            uint32_t cv = 0, cf = 0;
 #pragma unroll 1
-                for (int j = 0; j < nout; j++) {
-                    const float2 pr = a.pred_rows[s_off[j] + od[j]];
-                    pd[2 * j] = pr.x;
-                    pd[2 * j + 1] = pr.y;
+            for (uint32_t t0 = 0; t0 < M; t0 += 128) {
+                // second tile: past the block end it repeats the first with no
+                // valid lane (LC blocks are whole 128-tiles)
+                const bool two = LC || t0 + 64 < M;
+                const uint32_t t1 = two ? t0 + 64 : t0;
+                const uint32_t ux = t0 + (uint32_t)lane, uy = t1 + (uint32_t)lane;
+                const Tile<NI> x = eval_tile<NI, EQ3, LC>(a, rows, pens, ux, t0, ni, M, omi, Jp, vp, flp, rb, row_a0, row_b);
+                const Tile<NI> y = eval_tile<NI, EQ3, LC>(a, rows, pens, uy, t1, ni, M, omi, Jp, vp, flp, rb, row_a0, row_b);
+                unsigned long long mvx = ~0ull, mvy = two ? ~0ull : 0ull;   // valid lanes
+                if (!WHOLE) {
+                    mvx = ballot64(ux - u_lo < u_span);
+                    mvy = two ? ballot64(uy - u_lo < u_span) : 0ull;
                 }
-#pragma unroll
-                for (int t = 0; t < NI; t++)
-                    if (t < ni) {
-                        const float2 pr = a.pred_rows[rr[t]];
-                        pd[2 * (nout + t)] = pr.x;
-                        pd[2 * (nout + t) + 1] = pr.y;
-                    }
+                const unsigned long long vx = mvx & ballot64(x.v <= cap), vy = mvy & ballot64(y.v <= cap);
+                const unsigned long long fx = vx & ballot64((int32_t)x.fl >= 0), fy = vy & ballot64((int32_t)y.fl >= 0);
+                const unsigned long long cx = fx & ballot64(x.J >= thrJ), cy = fy & ballot64(y.J >= thrJ);
+                cv += (uint32_t)(__popcll(vx) + __popcll(vy));
+                cf += (uint32_t)(__popcll(fx) + __popcll(fy));
+                if (cx) offer_mask(slot, thr, thrJ, cx, x.J, base + ux, lane, k);
+                if (cy) offer_mask(slot, thr, thrJ, cy, y.J, base + uy, lane, k);
+                if (DUMP) {
+                    dump_tile<NI>(a, x, ((mvx >> lane) & 1ull) != 0ull, cap, base + ux, s_off, od, dl, nout, ni);
+                    dump_tile<NI>(a, y, ((mvy >> lane) & 1ull) != 0ull, cap, base + uy, s_off, od, dl, nout, ni);
+                }
             }
+            c_vram += cv;
+            c_feas += cf;
+        };
+        if (a.mask) {
+            if (whole) tiles(BoolC<true>{}, BoolC<true>{});
+            else tiles(BoolC<false>{}, BoolC<true>{});
+        } else {
+            if (whole) tiles(BoolC<true>{}, BoolC<false>{});
+            else tiles(BoolC<false>{}, BoolC<false>{});
         }
-        // next block: outer odometer (lane 0 writes the wave's digits; the
-        // wave reads them back after the write); a change above the last
-        // outer digit invalidates the cached prefix
-        bool carry = true;
-        for (int j = nout - 1; j >= 0 && carry; j--) {
-            uint32_t d = od[j] + 1u;
-            carry = d == (uint32_t)s_K[j];
-            if (carry) d = 0u;
-            __builtin_amdgcn_wave_barrier();
-            if (lane == 0) od[j] = d;
-            __builtin_amdgcn_wave_barrier();
-            if (j < nout - 1) need_full = true;
+
+        // next block: the last outer digit, and on its wrap the odometer of
+        // the others (lane 0 writes the wave's digits; the wave reads them
+        // back after the write), which invalidates the cached prefix
+        if (nout > 0 && ++dl == K_last) {
+            dl = 0u;
+            bool carry = true;
+            for (int j = nout - 2; j >= 0 && carry; j--) {
+                uint32_t d = od[j] + 1u;
+                carry = d == (uint32_t)s_K[j];
+                if (carry) d = 0u;
+                __builtin_amdgcn_wave_barrier();
+                if (lane == 0) od[j] = d;
+                __builtin_amdgcn_wave_barrier();
+            }
+            need_full = true;
         }
     }
 

@@ -240,11 +240,12 @@ struct SelectArgs {
 // Fixed observed state (Section III-B): per option row, the canonical terms
 // of the row's model under the fixed aggregate input.  FixedRow (16 bytes):
 // q (thr for the linear objective, Q f under Eq. 3), the row's VRAM value and
-// flags: kRowOk the latency bound (and floor) holds, kRowP / kRowPen subtract
-// FixedPen's P / pen after J = fma(omega, q, J) (Eq. 3 only).
+// flags: kRowBad (the sign bit, so that an OR over a configuration's rows is
+// tested by one signed compare) the latency bound or floor fails, kRowP /
+// kRowPen subtract FixedPen's P / pen after J = fma(omega, q, J) (Eq. 3 only).
 constexpr int kFixedWaves = 8;               // waves per workgroup of the fixed-state scan
 constexpr int kFixedMaxWgsPerCu = 4;         // resident scan workgroups per CU at most (grid = CUs x that)
-constexpr unsigned kRowOk = 1u, kRowP = 2u, kRowPen = 4u;
+constexpr unsigned kRowBad = 0x80000000u, kRowP = 2u, kRowPen = 4u;
 struct FixedRow {
     double q;
     float vram;
@@ -270,9 +271,10 @@ struct FixedArgs {
     int32_t in_off[kMaxN];
     uint32_t in_magic[kMaxN];
     uint64_t block0, n_blocks, blocks_per_wave;
+    uint64_t part_block_lo, part_block_hi;   // blocks holding the range ends mid-block (~0: none)
     int lc_shift;                    // >= 0: two inner models, the last with 2^lc_shift options
-                                     // dividing 64 and a block of whole 64-tiles (its digit is
-                                     // lane-constant); -1: general inner decode
+                                     // dividing 64 and a block of whole 128-configuration pairs
+                                     // of tiles (its digit is lane-constant); -1: general decode
     const int32_t *row_model;        // device [sumK]
     const float *features;           // device [sumK][L]
     const float *weights;            // device canonical image [N][wstride]

@@ -77,7 +77,7 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
     // aggregate centre of the slots this lane feeds to layer 1
     const float4 cen = *reinterpret_cast<const float4 *>(smem + Ly.off_c + 4 * half);
     const float cen_s[4] = {cen.x, cen.y, cen.z, cen.w};
-    const int wv = threadIdx.x >> 6;
+    const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));   // wave-uniform
     const int gw = blockIdx.x * WAVES + wv;
     const uint64_t n = args.n;
     const uint64_t n_tiles = (n + 31) >> 5;
