@@ -29,8 +29,8 @@ CPU_SAMPLE = 1 << 22
 # HBM bytes per launch of the fast search kernel from rocprofv3 FETCH_SIZE /
 # WRITE_SIZE passes (profiles/fast_kernel_n6_k24_h64_hbm_counters.md), valid
 # only for the kernel source they were taken on
-TRAFFIC_BYTES = 1_778_048 + 27_539_488
-TRAFFIC_SOURCE_SHA = "d64410872610224b"
+TRAFFIC_BYTES = 1_778_944 + 27_547_008
+TRAFFIC_SOURCE_SHA = "a793e9e18f593588"
 
 
 def measured_traffic():
