@@ -212,6 +212,52 @@ mf_status mf_workspace_size(const mf_problem *p, const mf_search_args *args, siz
 mf_status mf_search(mf_problem *p, const mf_search_args *args, void *d_ws, size_t ws_bytes,
                     void *stream, mf_result *h_out);
 
+/* ------------------------------------------------- static (multi-step) search */
+
+#define MF_MAX_STEPS 32
+
+/* One configuration held over T decision steps: the static schedulers of
+ * Section IV-C (Table II; StaticFull picks it with access to the whole
+ * space).  Step t evaluates every surrogate at the observed state
+ * h_state[t] (Section III-B, as MF_FIXED_STATE), with the step's latency
+ * bounds d_sla[t] and weights d_omega[t]; the previous deployment is
+ * objective.prev_variant at step 0 and the configuration itself afterwards
+ * (no reload after step 0).  J_t is the step's canonical utility (as
+ * mf_search computes it) and S = ((J_0 + J_1) + J_2) + ... in step order,
+ * fp64.  A configuration is feasible when its VRAM sum meets the cap and
+ * every step's latency bounds (and floors under MF_OBJ_EQ3) hold. */
+typedef struct {
+    uint64_t lo, hi;           /* half-open index range (search) */
+    int32_t top_k;             /* 1..64 (search) */
+    int32_t n_steps;           /* T, 1..MF_MAX_STEPS */
+    const float *d_sla;        /* device [T][N] */
+    const float *d_omega;      /* device [T][N], finite */
+    const float *h_state;      /* host [T][A] observed aggregate per step, finite */
+    mf_objective objective;    /* MF_OBJ_LINEAR or MF_OBJ_EQ3 (shared by the steps) */
+    uint8_t *d_mask;           /* optional device [hi - lo] (search, hi - lo <= 2^31): bit0 VRAM ok,
+                                  bit1 every step's service constraints met, bit2 feasible */
+} mf_static_args;
+
+/* Bytes of device workspace mf_search_static / mf_eval_static need. */
+mf_status mf_static_workspace_size(const mf_problem *p, const mf_static_args *args, size_t *bytes);
+
+/* argmax of S over the configurations of [lo, hi) feasible at every step;
+ * counts (n_vram, n_feas) and the exact top-k by (S desc, index asc) in
+ * h_out (top_J holds S).  Any created shape; T x sum K_i option rows must
+ * fit in LDS (MF_EUNSUPPORTED otherwise).  Blocking. */
+mf_status mf_search_static(mf_problem *p, const mf_static_args *args, void *d_ws, size_t ws_bytes,
+                           void *stream, mf_result *h_out);
+
+/* Per-step evaluation of an index list: d_J [n][T] the utility J_t (its
+ * value also where a constraint fails), d_S [n] the step-order sum, d_flags
+ * [n][T] (bit0 VRAM ok, bit1 the step's service constraints met).  Any
+ * output may be NULL; lo, hi, top_k and d_mask are ignored.  With T = 1 and
+ * objective.prev_variant set to the previous decision it evaluates one
+ * step of a dynamic schedule.  Blocking. */
+mf_status mf_eval_static(mf_problem *p, const mf_static_args *args, const uint64_t *d_idx, int64_t n,
+                         double *d_J, double *d_S, uint32_t *d_flags, void *d_ws, size_t ws_bytes,
+                         void *stream);
+
 /* ------------------------------------------------------------ evaluation */
 
 /* Fast-path (fp32 MFMA) predictions of an index list, as the search kernel

@@ -47,7 +47,7 @@ class _Inst(C.Structure):
                 ("hidden1", C.c_int32), ("hidden2", C.c_int32), ("bf16", C.c_int32),
                 ("n_options", C.c_void_p), ("features", C.c_void_p), ("agg_cols", C.c_void_p),
                 ("vram_slot", C.c_int32), ("vram_cap", C.c_float), ("weights", C.c_void_p),
-                ("obj", C.c_void_p), ("fixed_state", C.c_void_p)]
+                ("obj", C.c_void_p), ("fixed_state", C.c_void_p), ("raw_J", C.c_int32)]
 
 
 class _Result(C.Structure):
@@ -195,7 +195,9 @@ class Problem:
             out.update(flags=fl, pred=pr, J=jd)
         return out
 
-    def eval_list(self, idx, sla, omega, threads=0):
+    def eval_list(self, idx, sla, omega, threads=0, raw=False):
+        """Evaluate an index list.  raw=True: J is the utility value also where
+        a constraint fails (the flags say which)."""
         idx = np.ascontiguousarray(idx, np.uint64)
         n = int(idx.shape[0])
         sla = np.ascontiguousarray(sla, np.float32)
@@ -204,8 +206,12 @@ class Problem:
         thr = np.zeros((n, self.N))
         J = np.zeros(n)
         fl = np.zeros(n, np.uint32)
-        lib().orc_eval_list(self.ref, _ptr(idx), n, _ptr(sla), _ptr(om), int(threads),
-                            _ptr(lat), _ptr(thr), _ptr(J), _ptr(fl))
+        self.c.raw_J = 1 if raw else 0
+        try:
+            lib().orc_eval_list(self.ref, _ptr(idx), n, _ptr(sla), _ptr(om), int(threads),
+                                _ptr(lat), _ptr(thr), _ptr(J), _ptr(fl))
+        finally:
+            self.c.raw_J = 0
         return dict(lat=lat, thr=thr, J=J, flags=fl)
 
     def vram_feasible(self) -> np.ndarray:
@@ -264,6 +270,56 @@ def _ga_next(self, s, g, pop_idx, fitness, feasible, pop, tourn_k=3, p_cx=0.7, p
 
 Problem.ga = _ga
 Problem.ga_next = _ga_next
+
+
+def _step_objective(objective, t, n_models):
+    # the deployment before step 0 is the objective's previous variants; a
+    # static configuration is its own previous deployment afterwards (no
+    # reload after step 0)
+    if objective is None or t == 0:
+        return objective
+    from dataclasses import replace
+    return replace(objective, prev_variant=np.full(n_models, -1, np.int32))
+
+
+def static_eval(inst, objective, states, slas, omegas, idx, threads=0):
+    """One configuration held over T steps (the static schedulers of Section
+    IV-C, Table II).  Step t is the canonical evaluation with the step's
+    observed state states[t] (Section III-B), bounds slas[t] and weights
+    omegas[t].  Returns J [n][T] (the utility value, also where a constraint
+    fails), flags [n][T] and S [n] = ((J_0 + J_1) + J_2) + ... in step order."""
+    idx = np.ascontiguousarray(idx, np.uint64)
+    T = len(states)
+    N = int(inst.n_models)
+    J = np.zeros((len(idx), T))
+    F = np.zeros((len(idx), T), np.uint32)
+    for t in range(T):
+        r = Problem(inst, _step_objective(objective, t, N), state=states[t]).eval_list(
+            idx, slas[t], omegas[t], threads=threads, raw=True)
+        J[:, t] = r["J"]
+        F[:, t] = r["flags"]
+    S = J[:, 0].copy()
+    for t in range(1, T):
+        S = S + J[:, t]
+    return J, F, S
+
+
+def static_search(inst, objective, states, slas, omegas, k=1, lo=0, hi=None, threads=0):
+    """argmax over [lo, hi) of S(lambda) = sum_t J_t(lambda) among the
+    configurations feasible at every step (VRAM cap once; every step's
+    latency bounds and floors); top-k by (S desc, index asc)."""
+    if hi is None:
+        hi = int(np.prod([int(x) for x in inst.n_options], dtype=object))
+    idx = np.arange(lo, hi, dtype=np.uint64)
+    J, F, S = static_eval(inst, objective, states, slas, omegas, idx, threads)
+    vram = (F[:, 0] & FLAG_VRAM) != 0
+    svc = np.all((F & FLAG_SLA) != 0, axis=1)
+    feas = vram & svc
+    sel = np.flatnonzero(feas)
+    order = np.lexsort((idx[sel], -S[sel]))[:k]
+    flags = vram.astype(np.uint32) | (svc.astype(np.uint32) << 1) | (feas.astype(np.uint32) << 2)
+    return dict(n_vram=int(vram.sum()), n_feas=int(feas.sum()), top_idx=idx[sel][order],
+                top_J=S[sel][order], flags=flags, S=S, J=J, step_flags=F)
 
 
 def philox4x64(ctr, key):

@@ -223,7 +223,7 @@ void orc_eval_w(const orc_instance *in, const double *w64, uint64_t idx,
     }
     int feas = vram_ok && sla_ok;
     double j = -INFINITY;
-    if (feas) {
+    if (feas || in->raw_J) {
         if (ob) {
             j = jq;
         } else {

@@ -34,6 +34,9 @@ typedef struct {
     const orc_objective *obj;   /* NULL: linear objective */
     const float *fixed_state;   /* [A] observed aggregate state fed to every surrogate (Section III-B:
                                    held fixed during the search); NULL: derived from each candidate */
+    int32_t raw_J;              /* nonzero: J is the utility value also where a constraint fails
+                                   (the flags still say which); for evaluating decisions that break
+                                   a bound, as a random scheduler's do (Section IV-C, Table II) */
 } orc_instance;
 
 typedef struct {

@@ -650,10 +650,9 @@ size_t fixed_ws_bytes(const mf_problem &p, int top_k)
 
 // The search with the aggregate input held at args->state: one table of
 // canonical per-row terms, then scans of the joint space in chunks.
-mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipStream_t s, mf_result &acc)
+// Shape, block split and table pointers of a fixed-state (or static) scan.
+FixedArgs fixed_base(const mf_problem *p, const mf_objective &objective, int top_k)
 {
-    if (args->hi == args->lo) return MF_OK;
-    const FixedWs w = fixed_ws_layout(*p, p->num_cus * kFixedMaxWgsPerCu, args->top_k);
     FixedArgs a{};
     a.n_models = p->N; a.L = p->L; a.A = p->A; a.H1 = p->H1; a.H2 = p->H2; a.bf16 = p->bf16; a.sumK = p->sumK;
     for (int i = 0; i < p->N; i++) {
@@ -679,18 +678,26 @@ mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipS
     a.features = p->d_features;
     a.weights = p->d_canon;
     a.wstride = p->wstride;
-    for (int k = 0; k < p->A; k++) a.state[k] = args->state[k];
     a.vram_col = p->agg_cols[p->vram_slot];
     a.vram_cap = p->vram_cap;
+    a.top_k = top_k;
+    a.obj = obj_args(p, objective);
+    return a;
+}
+
+mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipStream_t s, mf_result &acc)
+{
+    if (args->hi == args->lo) return MF_OK;
+    const FixedWs w = fixed_ws_layout(*p, p->num_cus * kFixedMaxWgsPerCu, args->top_k);
+    FixedArgs a = fixed_base(p, args->objective, args->top_k);
+    for (int k = 0; k < p->A; k++) a.state[k] = args->state[k];
     a.sla = args->d_sla;
     a.omega = args->d_omega;
-    a.top_k = args->top_k;
     a.rows = reinterpret_cast<FixedRow *>(ws + w.rows);
     a.pens = reinterpret_cast<FixedPen *>(ws + w.pens);
     a.pred_rows = reinterpret_cast<float2 *>(ws + w.prow);
     a.wg_lists = reinterpret_cast<K128 *>(ws + w.lists);
     a.res = reinterpret_cast<DevResult *>(ws + w.res);
-    a.obj = obj_args(p, args->objective);
     const bool dump = (args->flags & MF_DUMP) != 0;
     const int wgs_per_cu = fixed_wgs_per_cu(a);
 
@@ -714,6 +721,145 @@ mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipS
         float ms = 0.f;
         if (hipMemsetAsync(a.res, 0, sizeof(DevResult), s) != hipSuccess ||
             launch_fixed(a, grid, lo == args->lo, s, ev0, ev1) != hipSuccess ||
+            hipMemcpyAsync(&h, a.res, sizeof(DevResult), hipMemcpyDeviceToHost, s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess || hipEventElapsedTime(&ms, ev0, ev1) != hipSuccess) {
+            st = MF_EDEVICE;
+            break;
+        }
+        if (!(h.status & kStatVerified)) { st = MF_EINTERNAL; break; }
+        mf_result part;
+        empty_result(part);
+        part.n_eval = n;
+        part.n_vram = h.n_vram;
+        part.n_feas = h.n_feas_sure;
+        part.n_top = h.n_top;
+        for (int q = 0; q < h.n_top; q++) {
+            part.top_idx[q] = h.top_idx[q];
+            part.top_J[q] = h.top_J[q];
+        }
+        part.main_kernel_ms = ms;
+        merge_into(acc, part, args->top_k);
+        lo += n;
+    }
+    (void)hipEventDestroy(ev0);
+    (void)hipEventDestroy(ev1);
+    return st;
+}
+
+// ---- static (multi-step) search
+
+struct StaticWs {
+    size_t res, rows, pens, prow, lists, total;
+};
+
+StaticWs static_ws_layout(const mf_problem &p, int n_steps, int top_k)
+{
+    StaticWs w{};
+    const size_t tr = (size_t)n_steps * p.sumK;
+    size_t o = 0;
+    w.res = o; o = align256(o + sizeof(DevResult));
+    w.rows = o; o = align256(o + tr * sizeof(FixedRow));
+    w.pens = o; o = align256(o + tr * sizeof(FixedPen));
+    w.prow = o; o = align256(o + (size_t)p.sumK * 8);
+    w.lists = o; o = align256(o + (size_t)p.num_cus * kFixedMaxWgsPerCu * top_k * sizeof(K128));
+    w.total = o;
+    return w;
+}
+
+// static LDS of the static scan kernel besides the dynamic part
+constexpr size_t kStaticLdsFixed = 4 * kMaxN * 2 + 4 * kFixedWaves * kMaxN + (8 + 4) * kFixedWaves * MF_MAX_STEPS;
+
+mf_status check_objective(const mf_problem *p, const mf_objective &o)
+{
+    if (o.kind != MF_OBJ_LINEAR && o.kind != MF_OBJ_EQ3) return MF_EINVAL;
+    if (o.kind == MF_OBJ_EQ3) {
+        if (!p->has_var) return MF_EINVAL;
+        if (!std::isfinite(o.alpha) || !std::isfinite(o.beta) || !std::isfinite(o.delta) || o.beta < 0.f)
+            return MF_EINVAL;
+        for (int i = 0; i < p->N; i++) {
+            if (std::isnan(o.tau[i]) || o.tau[i] == INFINITY) return MF_EINVAL;
+            if (o.prev_variant[i] < -1 || o.prev_variant[i] >= p->n_var[i]) return MF_EINVAL;
+        }
+    }
+    return MF_OK;
+}
+
+mf_status check_static_args(const mf_problem *p, const mf_static_args *a, bool search)
+{
+    if (!p || !a) return MF_EINVAL;
+    if (a->n_steps < 1 || a->n_steps > MF_MAX_STEPS) return MF_EINVAL;
+    if (!a->d_sla || !a->d_omega || !a->h_state) return MF_EINVAL;
+    for (int64_t t = 0; t < (int64_t)a->n_steps * p->A; t++)
+        if (!std::isfinite(a->h_state[t])) return MF_EINVAL;
+    mf_status st = check_objective(p, a->objective);
+    if (st != MF_OK) return st;
+    if (search) {
+        if (a->lo > a->hi) return MF_EINVAL;
+        if (a->hi > p->space) return MF_EOVERFLOW;
+        if (a->top_k < 1 || a->top_k > MF_MAX_TOPK) return MF_EINVAL;
+        if (a->d_mask && a->hi - a->lo > (1ull << 31)) return MF_EINVAL;
+    }
+    if (static_lds_bytes(a->n_steps, p->sumK, p->N, a->objective.kind != MF_OBJ_LINEAR) + kStaticLdsFixed > 163840)
+        return MF_EUNSUPPORTED;
+    return MF_OK;
+}
+
+// Per-step tables: step t's observed state, bounds and previous deployment
+// (the objective's at step 0, none afterwards: the configuration is its own).
+mf_status static_setup(mf_problem *p, const mf_static_args *args, char *ws, int top_k, hipStream_t s, StaticArgs &sa)
+{
+    const StaticWs w = static_ws_layout(*p, args->n_steps, top_k);
+    FixedArgs a = fixed_base(p, args->objective, top_k);
+    a.rows = nullptr;
+    a.pred_rows = reinterpret_cast<float2 *>(ws + w.prow);
+    a.wg_lists = reinterpret_cast<K128 *>(ws + w.lists);
+    a.res = reinterpret_cast<DevResult *>(ws + w.res);
+    sa = StaticArgs{};
+    sa.n_steps = args->n_steps;
+    sa.omega_steps = args->d_omega;
+    sa.rows_steps = reinterpret_cast<FixedRow *>(ws + w.rows);
+    sa.pens_steps = reinterpret_cast<FixedPen *>(ws + w.pens);
+    for (int t = 0; t < args->n_steps; t++) {
+        FixedArgs ft = a;
+        for (int k = 0; k < p->A; k++) ft.state[k] = args->h_state[(size_t)t * p->A + k];
+        ft.sla = args->d_sla + (size_t)t * p->N;
+        ft.omega = args->d_omega + (size_t)t * p->N;
+        ft.rows = sa.rows_steps + (size_t)t * p->sumK;
+        ft.pens = sa.pens_steps + (size_t)t * p->sumK;
+        if (t > 0)
+            for (int i = 0; i < kMaxN; i++) ft.obj.prev[i] = -1;
+        if (launch_fixed_table(ft, s) != hipSuccess) return MF_EDEVICE;
+    }
+    a.sla = args->d_sla;
+    a.omega = args->d_omega;
+    sa.f = a;
+    return MF_OK;
+}
+
+mf_status search_static(mf_problem *p, const mf_static_args *args, char *ws, hipStream_t s, mf_result &acc)
+{
+    if (args->hi == args->lo) return MF_OK;
+    StaticArgs sa;
+    mf_status st = static_setup(p, args, ws, args->top_k, s, sa);
+    if (st != MF_OK) return st;
+    const int wgs_per_cu = static_wgs_per_cu(sa);
+    hipEvent_t ev0 = nullptr, ev1 = nullptr;
+    MF_HIP(hipEventCreate(&ev0));
+    if (hipEventCreate(&ev1) != hipSuccess) { (void)hipEventDestroy(ev0); return MF_EDEVICE; }
+    for (uint64_t lo = args->lo; lo < args->hi;) {
+        const uint64_t n = std::min<uint64_t>(args->hi - lo, kFixedChunk);
+        FixedArgs &a = sa.f;
+        a.lo = lo;
+        a.n = n;
+        a.n_blocks = fixed_blocks(*p, lo, n, a.block0);
+        const int grid = fixed_grid(*p, a.n_blocks, wgs_per_cu);
+        const uint64_t waves = (uint64_t)grid * kFixedWaves;
+        a.blocks_per_wave = (a.n_blocks + waves - 1) / waves;
+        a.mask = args->d_mask ? args->d_mask + (lo - args->lo) : nullptr;
+        DevResult h{};
+        float ms = 0.f;
+        if (hipMemsetAsync(a.res, 0, sizeof(DevResult), s) != hipSuccess ||
+            launch_static(sa, grid, s, ev0, ev1) != hipSuccess ||
             hipMemcpyAsync(&h, a.res, sizeof(DevResult), hipMemcpyDeviceToHost, s) != hipSuccess ||
             hipStreamSynchronize(s) != hipSuccess || hipEventElapsedTime(&ms, ev0, ev1) != hipSuccess) {
             st = MF_EDEVICE;
@@ -1122,18 +1268,7 @@ static mf_status check_search_args(const mf_problem *p, const mf_search_args *a)
     } else if (!p->fast_ok && !p->bf_ok) {
         return MF_EUNSUPPORTED;
     }
-    const mf_objective &o = a->objective;
-    if (o.kind != MF_OBJ_LINEAR && o.kind != MF_OBJ_EQ3) return MF_EINVAL;
-    if (o.kind == MF_OBJ_EQ3) {
-        if (!p->has_var) return MF_EINVAL;
-        if (!std::isfinite(o.alpha) || !std::isfinite(o.beta) || !std::isfinite(o.delta) || o.beta < 0.f)
-            return MF_EINVAL;
-        for (int i = 0; i < p->N; i++) {
-            if (std::isnan(o.tau[i]) || o.tau[i] == INFINITY) return MF_EINVAL;
-            if (o.prev_variant[i] < -1 || o.prev_variant[i] >= p->n_var[i]) return MF_EINVAL;
-        }
-    }
-    return MF_OK;
+    return check_objective(p, a->objective);
 }
 
 mf_status mf_workspace_size(const mf_problem *p, const mf_search_args *args, size_t *bytes)
@@ -1170,6 +1305,53 @@ mf_status mf_search(mf_problem *p, const mf_search_args *args, void *d_ws, size_
         st = search_range(p, args, args->lo, n, (char *)d_ws, (hipStream_t)stream, acc, 0);
     if (st != MF_OK) return st;
     *h_out = acc;
+    return MF_OK;
+}
+
+mf_status mf_static_workspace_size(const mf_problem *p, const mf_static_args *args, size_t *bytes)
+{
+    if (!bytes) return MF_EINVAL;
+    mf_status st = check_static_args(p, args, false);
+    if (st != MF_OK) return st;
+    *bytes = static_ws_layout(*p, args->n_steps, MF_MAX_TOPK).total;
+    return MF_OK;
+}
+
+mf_status mf_search_static(mf_problem *p, const mf_static_args *args, void *d_ws, size_t ws_bytes, void *stream,
+                           mf_result *h_out)
+{
+    if (!h_out || !d_ws) return MF_EINVAL;
+    mf_status st = check_static_args(p, args, true);
+    if (st != MF_OK) return st;
+    if (ws_bytes < static_ws_layout(*p, args->n_steps, MF_MAX_TOPK).total) return MF_ENOMEM;
+    if (((uintptr_t)d_ws & 255u) != 0) return MF_EINVAL;
+    mf_result acc;
+    empty_result(acc);
+    st = search_static(p, args, (char *)d_ws, (hipStream_t)stream, acc);
+    if (st != MF_OK) return st;
+    *h_out = acc;
+    return MF_OK;
+}
+
+mf_status mf_eval_static(mf_problem *p, const mf_static_args *args, const uint64_t *d_idx, int64_t n, double *d_J,
+                         double *d_S, uint32_t *d_flags, void *d_ws, size_t ws_bytes, void *stream)
+{
+    if (!d_ws || n < 0 || (n > 0 && !d_idx)) return MF_EINVAL;
+    mf_status st = check_static_args(p, args, false);
+    if (st != MF_OK) return st;
+    if (ws_bytes < static_ws_layout(*p, args->n_steps, MF_MAX_TOPK).total) return MF_ENOMEM;
+    if (((uintptr_t)d_ws & 255u) != 0) return MF_EINVAL;
+    if (n == 0) return MF_OK;
+    hipStream_t s = (hipStream_t)stream;
+    StaticArgs sa;
+    st = static_setup(p, args, (char *)d_ws, 1, s, sa);
+    if (st != MF_OK) return st;
+    sa.idx = d_idx;
+    sa.n_list = n;
+    sa.out_J = d_J;
+    sa.out_S = d_S;
+    sa.out_flags = d_flags;
+    if (launch_static_eval(sa, s) != hipSuccess || hipStreamSynchronize(s) != hipSuccess) return MF_EDEVICE;
     return MF_OK;
 }
 

@@ -447,13 +447,7 @@ int fixed_wgs_per_cu(const FixedArgs &a)
 hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1)
 {
     hipError_t e;
-    if (table) {
-        if (a.bf16)
-            hipLaunchKernelGGL(fixed_table_kernel<true>, dim3(a.sumK), dim3(64), 0, s, a);
-        else
-            hipLaunchKernelGGL(fixed_table_kernel<false>, dim3(a.sumK), dim3(64), 0, s, a);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
+    if (table && (e = launch_fixed_table(a, s)) != hipSuccess) return e;
     const size_t lds = fixed_lds_bytes(a.sumK, a.obj.kind != 0);
     const ScanFn fn = scan_fn(a);
     e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -464,6 +458,285 @@ hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s,
     if ((e = hipEventRecord(ev1, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(fixed_merge_kernel, dim3(1), dim3(kFixedMergeWaves * 64), 0, s, a.wg_lists, grid, a.top_k,
                        a.res);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Static (multi-step) search: S = sum over steps of J_t, one configuration
+// for all steps.  Per step t the table kernel has filled rows_steps[t]; the
+// VRAM sum is the same at every step.
+// ---------------------------------------------------------------------------
+
+// One model's step of step t's chain: service flags and J (VRAM apart).
+template <bool EQ3>
+__device__ __forceinline__ void chain_J(const FixedRow &r, const FixedPen *pens, uint32_t row, double om, double &J,
+                                        uint32_t &fl)
+{
+    fl |= r.flags;
+    J = fma(om, r.q, J);
+    if (EQ3) {
+        const FixedPen pp = pens[row];
+        if (r.flags & kRowP) J = J - pp.P;
+        if (r.flags & kRowPen) J = J - pp.pen;
+    }
+}
+
+__host__ __device__ constexpr size_t static_om_doubles(int n_steps, int n_models)
+{
+    return ((size_t)n_steps * n_models + 1) & ~(size_t)1;   // 16-byte multiple
+}
+
+size_t static_lds_bytes(int n_steps, int sumK, int n_models, bool eq3)
+{
+    const size_t rows = (size_t)n_steps * sumK;
+    return rows * sizeof(FixedRow) + (eq3 ? rows * sizeof(FixedPen) : 0) +
+           static_om_doubles(n_steps, n_models) * 8 + (size_t)kFixedWaves * 64 * sizeof(K128);
+}
+
+template <int NI, bool EQ3>
+__global__ void __launch_bounds__(kFixedWaves * 64) static_scan_kernel(const StaticArgs sa)
+{
+    const FixedArgs &a = sa.f;
+    extern __shared__ float4 smem4[];
+    __shared__ int32_t s_off[kMaxN], s_K[kMaxN];
+    __shared__ uint32_t s_od[kFixedWaves][kMaxN];
+    __shared__ double s_preJ[kFixedWaves][MF_MAX_STEPS];     // outer prefix of each step's chain
+    __shared__ uint32_t s_preF[kFixedWaves][MF_MAX_STEPS];
+    const int T = sa.n_steps, sumK = a.sumK, N = a.n_models, nout = a.n_outer, ni = N - nout, k = a.top_k;
+    const int TR = T * sumK;
+    FixedRow *rows = reinterpret_cast<FixedRow *>(smem4);                    // [T][sumK]
+    FixedPen *pens = reinterpret_cast<FixedPen *>(rows + TR);                // [T][sumK] (Eq. 3)
+    double *om = reinterpret_cast<double *>(pens + (EQ3 ? TR : 0));          // [T][N]
+    K128 *lst = reinterpret_cast<K128 *>(om + static_om_doubles(T, N));
+#pragma unroll 1
+    for (int t = threadIdx.x; t < TR; t += blockDim.x) {
+        rows[t] = sa.rows_steps[t];
+        if (EQ3) pens[t] = sa.pens_steps[t];
+    }
+    for (int t = threadIdx.x; t < T * N; t += blockDim.x) om[t] = (double)sa.omega_steps[t];
+#pragma unroll
+    for (int j = 0; j < kMaxN; j++)
+        if (threadIdx.x == (unsigned)j) {
+            s_off[j] = a.opt_off[j];
+            s_K[j] = a.K[j];
+        }
+
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const uint64_t gw = (uint64_t)blockIdx.x * kFixedWaves + wv;
+    const uint64_t b_first = gw * a.blocks_per_wave;
+    const uint64_t b_begin = a.block0 + (b_first < a.n_blocks ? b_first : a.n_blocks);
+    const uint64_t b_end = a.block0 + (b_first + a.blocks_per_wave < a.n_blocks ? b_first + a.blocks_per_wave
+                                                                                : a.n_blocks);
+    const uint64_t idx_lo = a.lo, idx_hi = a.lo + a.n;
+    const uint32_t M = a.inner;
+    const float cap = a.vram_cap;
+    uint32_t *od = s_od[wv];
+    if (lane == 0) {
+        uint64_t x = b_begin;
+        for (int j = nout - 1; j >= 0; j--) {
+            od[j] = (uint32_t)(x % (uint64_t)a.K[j]);
+            x /= (uint64_t)a.K[j];
+        }
+    }
+    __syncthreads();
+
+    K128 slot = {0ull, 0ull}, thr = {0ull, 0ull};
+    double thrS = -INFINITY;
+    unsigned long long c_vram = 0, c_feas = 0;
+
+    for (uint64_t b = b_begin; b < b_end; b++) {
+        // outer prefix: the VRAM sum once, each step's chain (wave-uniform)
+        float vp = 0.f;
+#pragma unroll 1
+        for (int j = 0; j < nout; j++) vp += rows[s_off[j] + od[j]].vram;
+#pragma unroll 1
+        for (int t = 0; t < T; t++) {
+            double J = 0.0;
+            uint32_t fl = 0u;
+#pragma unroll 1
+            for (int j = 0; j < nout; j++) {
+                const uint32_t row = (uint32_t)(t * sumK + s_off[j]) + od[j];
+                chain_J<EQ3>(rows[row], pens, row, om[t * N + j], J, fl);
+            }
+            __builtin_amdgcn_wave_barrier();
+            if (lane == 0) {
+                s_preJ[wv][t] = J;
+                s_preF[wv][t] = fl;
+            }
+            __builtin_amdgcn_wave_barrier();
+        }
+        const uint64_t base = b * (uint64_t)M;
+        const uint32_t u_lo = base < idx_lo ? (uint32_t)(idx_lo - base) : 0u;
+        const uint32_t u_hi = idx_hi - base < (uint64_t)M ? (uint32_t)(idx_hi - base) : M;
+        const uint32_t u_span = u_hi - u_lo;
+        uint32_t cv = 0, cf = 0;
+#pragma unroll 1
+        for (uint32_t t0 = 0; t0 < M; t0 += 64) {
+            const uint32_t u = t0 + (uint32_t)lane;
+            uint32_t uu = u < M ? u : 0u;
+            uint32_t rr[NI];
+#pragma unroll
+            for (int q = NI - 1; q >= 0; q--) {
+                rr[q] = 0;
+                if (q < ni) {
+                    const uint32_t qq = (q > 0 && a.in_magic[q]) ? __umulhi(uu, a.in_magic[q]) : (q > 0 ? uu : 0u);
+                    rr[q] = (uint32_t)a.in_off[q] + (uu - qq * (uint32_t)a.in_K[q]);
+                    uu = qq;
+                }
+            }
+            float v = vp;
+#pragma unroll
+            for (int q = 0; q < NI; q++)
+                if (q < ni) v += rows[rr[q]].vram;
+            double S = 0.0;
+            uint32_t fall = 0u;
+#pragma unroll 1
+            for (int t = 0; t < T; t++) {
+                double J = s_preJ[wv][t];
+                uint32_t fl = s_preF[wv][t];
+#pragma unroll
+                for (int q = 0; q < NI; q++)
+                    if (q < ni) {
+                        const uint32_t row = (uint32_t)(t * sumK) + rr[q];
+                        chain_J<EQ3>(rows[row], pens, row, om[t * N + nout + q], J, fl);
+                    }
+                S = t == 0 ? J : S + J;
+                fall |= fl;
+            }
+            const unsigned long long mv = ballot64(u - u_lo < u_span);
+            const unsigned long long vm = mv & ballot64(v <= cap);
+            const unsigned long long fm = vm & ballot64((int32_t)fall >= 0);
+            const unsigned long long cm = fm & ballot64(S >= thrS);
+            cv += (uint32_t)__popcll(vm);
+            cf += (uint32_t)__popcll(fm);
+            if (cm) offer_mask(slot, thr, thrS, cm, S, base + u, lane, k);
+            if (a.mask && ((mv >> lane) & 1ull)) {
+                const bool vok = v <= cap, sok = (int32_t)fall >= 0;
+                a.mask[base + u - idx_lo] = (uint8_t)((vok ? 1u : 0u) | (sok ? 2u : 0u) | (vok && sok ? 4u : 0u));
+            }
+        }
+        c_vram += cv;
+        c_feas += cf;
+        bool carry = true;
+        for (int j = nout - 1; j >= 0 && carry; j--) {
+            uint32_t d = od[j] + 1u;
+            carry = d == (uint32_t)s_K[j];
+            if (carry) d = 0u;
+            __builtin_amdgcn_wave_barrier();
+            if (lane == 0) od[j] = d;
+            __builtin_amdgcn_wave_barrier();
+        }
+    }
+
+    if (lane == 0) {
+        if (c_vram) atomicAdd(&a.res->n_vram, c_vram);
+        if (c_feas) atomicAdd(&a.res->n_feas_sure, c_feas);
+    }
+    lst[wv * 64 + lane] = key_if(lane < k, slot);
+    __syncthreads();
+    if (wv == 0) {
+#pragma unroll 1
+        for (int w = 1; w < kFixedWaves; w++) list128_offer(slot, lst[w * 64 + lane], lane, k, thr);
+        if (lane < k) a.wg_lists[(uint64_t)blockIdx.x * k + lane] = slot;
+    }
+}
+
+// List mode: one thread per index, every model decoded, each step's chain.
+template <bool EQ3>
+__global__ void __launch_bounds__(256) static_eval_kernel(const StaticArgs sa)
+{
+    const FixedArgs &a = sa.f;
+    const int T = sa.n_steps, sumK = a.sumK, N = a.n_models;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < sa.n_list;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        uint64_t x = sa.idx[e];
+        uint32_t row[kMaxN];
+#pragma unroll
+        for (int j = kMaxN - 1; j >= 0; j--) {
+            row[j] = 0;
+            if (j < N) {
+                row[j] = (uint32_t)a.opt_off[j] + (uint32_t)(x % (uint64_t)a.K[j]);
+                x /= (uint64_t)a.K[j];
+            }
+        }
+        float v = 0.f;
+#pragma unroll
+        for (int j = 0; j < kMaxN; j++)
+            if (j < N) v += sa.rows_steps[row[j]].vram;
+        const uint32_t vok = v <= a.vram_cap ? 1u : 0u;
+        double S = 0.0;
+        for (int t = 0; t < T; t++) {
+            double J = 0.0;
+            uint32_t fl = 0u;
+#pragma unroll
+            for (int j = 0; j < kMaxN; j++)
+                if (j < N) {
+                    const uint32_t r = (uint32_t)(t * sumK) + row[j];
+                    chain_J<EQ3>(sa.rows_steps[r], sa.pens_steps, r, (double)sa.omega_steps[t * N + j], J, fl);
+                }
+            S = t == 0 ? J : S + J;
+            if (sa.out_J) sa.out_J[e * T + t] = J;
+            if (sa.out_flags) sa.out_flags[e * T + t] = vok | ((int32_t)fl >= 0 ? 2u : 0u);
+        }
+        if (sa.out_S) sa.out_S[e] = S;
+    }
+}
+
+using StaticFn = void (*)(const StaticArgs);
+
+static StaticFn static_fn(const StaticArgs &a)
+{
+    const bool eq3 = a.f.obj.kind != 0;
+    const int ni = a.f.n_models - a.f.n_outer;
+    return ni <= 2 ? (eq3 ? static_scan_kernel<2, true> : static_scan_kernel<2, false>)
+         : ni <= 4 ? (eq3 ? static_scan_kernel<4, true> : static_scan_kernel<4, false>)
+                   : (eq3 ? static_scan_kernel<kMaxN, true> : static_scan_kernel<kMaxN, false>);
+}
+
+int static_wgs_per_cu(const StaticArgs &a)
+{
+    const StaticFn fn = static_fn(a);
+    const size_t lds = static_lds_bytes(a.n_steps, a.f.sumK, a.f.n_models, a.f.obj.kind != 0);
+    if (hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+        return 1;
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, kFixedWaves * 64, lds) != hipSuccess || n < 1) return 1;
+    return n < kFixedMaxWgsPerCu ? n : kFixedMaxWgsPerCu;
+}
+
+hipError_t launch_fixed_table(const FixedArgs &a, hipStream_t s)
+{
+    if (a.bf16)
+        hipLaunchKernelGGL(fixed_table_kernel<true>, dim3(a.sumK), dim3(64), 0, s, a);
+    else
+        hipLaunchKernelGGL(fixed_table_kernel<false>, dim3(a.sumK), dim3(64), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_static(const StaticArgs &a, int grid, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1)
+{
+    const size_t lds = static_lds_bytes(a.n_steps, a.f.sumK, a.f.n_models, a.f.obj.kind != 0);
+    const StaticFn fn = static_fn(a);
+    hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    if ((e = hipEventRecord(ev0, s)) != hipSuccess) return e;
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(kFixedWaves * 64), lds, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = hipEventRecord(ev1, s)) != hipSuccess) return e;
+    hipLaunchKernelGGL(fixed_merge_kernel, dim3(1), dim3(kFixedMergeWaves * 64), 0, s, a.f.wg_lists, grid,
+                       a.f.top_k, a.f.res);
+    return hipGetLastError();
+}
+
+hipError_t launch_static_eval(const StaticArgs &a, hipStream_t s)
+{
+    const int64_t blocks = (a.n_list + 255) / 256;
+    const int grid = (int)(blocks < 4096 ? (blocks > 0 ? blocks : 1) : 4096);
+    if (a.f.obj.kind != 0)
+        hipLaunchKernelGGL(static_eval_kernel<true>, dim3(grid), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(static_eval_kernel<false>, dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

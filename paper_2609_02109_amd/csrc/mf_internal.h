@@ -295,6 +295,24 @@ struct FixedArgs {
     ObjArgs obj;
 };
 
+// Static (multi-step) search: one configuration held over T steps.  f
+// carries the shape, the block split, the range and the outputs; per step t
+// the table kernel fills rows_steps[t][sumK] (and pens_steps) from the
+// step's observed state, bounds and previous deployment.
+struct StaticArgs {
+    FixedArgs f;
+    int n_steps;
+    const float *omega_steps;        // device [T][N]
+    FixedRow *rows_steps;            // [T][sumK]
+    FixedPen *pens_steps;            // [T][sumK]
+    // list mode
+    const uint64_t *idx;
+    int64_t n_list;
+    double *out_J;                   // [n][T] or null
+    double *out_S;                   // [n] or null
+    uint32_t *out_flags;             // [n][T] or null
+};
+
 // GA problem constants (kernel-argument block).
 struct GAConst {
     int N, L, A, H1, H2, bf16;
@@ -336,6 +354,11 @@ hipError_t launch_kth_candidate(const unsigned long long *cand_keys, const doubl
                                 int kp, int k, DevResult *res, hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, const FastConst &fc, const float *omega, hipStream_t s);
 size_t fixed_lds_bytes(int sumK, bool eq3);
+size_t static_lds_bytes(int n_steps, int sumK, int n_models, bool eq3);
+hipError_t launch_fixed_table(const FixedArgs &a, hipStream_t s);
+hipError_t launch_static(const StaticArgs &a, int grid, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
+hipError_t launch_static_eval(const StaticArgs &a, hipStream_t s);
+int static_wgs_per_cu(const StaticArgs &a);
 int fixed_wgs_per_cu(const FixedArgs &a);
 hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 int ga_fitness_supported(int nin, int h1, int h2);

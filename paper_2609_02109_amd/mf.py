@@ -24,6 +24,7 @@ MAX_MODELS = 16
 
 EXPORTS = ["mf_problem_create", "mf_problem_destroy", "mf_space_size", "mf_decode",
            "mf_workspace_size", "mf_search", "mf_eval_fast", "mf_eval_canonical",
+           "mf_static_workspace_size", "mf_search_static", "mf_eval_static",
            "mf_ga_workspace_size", "mf_ga_run", "mf_status_string"]
 
 
@@ -83,6 +84,15 @@ class Result(C.Structure):
                 ("main_kernel_ms", C.c_float), ("pad", C.c_float)]
 
 
+MAX_STEPS = 32
+
+
+class StaticArgs(C.Structure):
+    _fields_ = [("lo", C.c_uint64), ("hi", C.c_uint64), ("top_k", C.c_int32), ("n_steps", C.c_int32),
+                ("d_sla", C.c_void_p), ("d_omega", C.c_void_p), ("h_state", C.c_void_p),
+                ("objective", Objective), ("d_mask", C.c_void_p)]
+
+
 class GAArgs(C.Structure):
     _fields_ = [("n_scen", C.c_int32), ("pop", C.c_int32), ("gens", C.c_int32), ("tourn_k", C.c_int32),
                 ("p_cx", C.c_float), ("p_swap", C.c_float), ("p_mut", C.c_float), ("pad", C.c_float),
@@ -105,6 +115,9 @@ def _load():
         "mf_search": (S, [P, P, P, C.c_size_t, P, P]),
         "mf_eval_fast": (S, [P, P, C.c_int64, P, P]),
         "mf_eval_canonical": (S, [P, P, C.c_int64, P, P, P, P, P, P]),
+        "mf_static_workspace_size": (S, [P, P, P]),
+        "mf_search_static": (S, [P, P, P, C.c_size_t, P, P]),
+        "mf_eval_static": (S, [P, P, P, C.c_int64, P, P, P, P, C.c_size_t, P]),
         "mf_ga_workspace_size": (S, [P, P, P]),
         "mf_ga_run": (S, [P, P, P, C.c_size_t, P, P, P, P]),
         "mf_status_string": (C.c_char_p, [S]),
@@ -257,6 +270,54 @@ class Problem:
         if dump:
             out.update(mask=mask[:hi - lo], pred=pred[:hi - lo])
         return out
+
+    def _static_args(self, states, slas, omegas, objective, k=1, lo=0, hi=None, mask=None):
+        import torch
+        st = np.ascontiguousarray(states, np.float32).reshape(-1, self.A)
+        T = int(st.shape[0])
+        d_sla = self._dev(np.asarray(slas, np.float32).reshape(T, self.N), torch.float32)
+        d_om = self._dev(np.asarray(omegas, np.float32).reshape(T, self.N), torch.float32)
+        args = StaticArgs(int(lo), int(self.space_size if hi is None else hi), int(k), T, _ptr(d_sla), _ptr(d_om),
+                          _ptr(st), objective_args(objective, self.N), _ptr(mask))
+        nbytes = C.c_size_t()
+        _check(lib.mf_static_workspace_size(self.handle, C.byref(args), C.byref(nbytes)), "mf_static_workspace_size")
+        return args, self.workspace(nbytes.value), (st, d_sla, d_om)
+
+    def search_static(self, states, slas, omegas, k=1, lo=0, hi=None, objective=None, dump=False, stream=None):
+        """One configuration held over T steps (states [T][A], slas and omegas
+        [T][N]): the exact top-k of S = sum_t J_t among the configurations
+        feasible at every step; with dump=True also the per-index mask."""
+        import torch
+        if hi is None:
+            hi = self.space_size
+        mask = torch.zeros(max(hi - lo, 1), dtype=torch.uint8, device=self.device) if dump else None
+        args, ws, keep = self._static_args(states, slas, omegas, objective, k, lo, hi, mask)
+        res = Result()
+        _check(lib.mf_search_static(self.handle, C.byref(args), _ptr(ws), C.c_size_t(ws.numel()), _stream(stream),
+                                    C.byref(res)), "mf_search_static")
+        nt = int(res.n_top)
+        out = dict(n_eval=int(res.n_eval), n_vram=int(res.n_vram), n_feas=int(res.n_feas),
+                   main_kernel_ms=float(res.main_kernel_ms), top_idx=np.array(res.top_idx[:nt], np.uint64),
+                   top_J=np.array(res.top_J[:nt], np.float64))
+        if dump:
+            out["mask"] = mask[:hi - lo]
+        return out
+
+    def eval_static(self, idx, states, slas, omegas, objective=None, stream=None):
+        """Per-step utilities of an index list held over T steps: J [n][T],
+        S [n] (step-order sum), flags [n][T] (bit0 VRAM, bit1 the step's
+        service constraints)."""
+        import torch
+        d_idx = self._dev(np.asarray(idx, np.uint64).astype(np.int64), torch.int64)
+        n = int(d_idx.numel())
+        args, ws, keep = self._static_args(states, slas, omegas, objective)
+        T = int(args.n_steps)
+        J = torch.zeros((max(n, 1), T), dtype=torch.float64, device=self.device)
+        S = torch.zeros(max(n, 1), dtype=torch.float64, device=self.device)
+        F = torch.zeros((max(n, 1), T), dtype=torch.int32, device=self.device)
+        _check(lib.mf_eval_static(self.handle, C.byref(args), _ptr(d_idx), n, _ptr(J), _ptr(S), _ptr(F), _ptr(ws),
+                                  C.c_size_t(ws.numel()), _stream(stream)), "mf_eval_static")
+        return dict(J=J[:n].cpu().numpy(), S=S[:n].cpu().numpy(), flags=F[:n].cpu().numpy().astype(np.uint32))
 
     def search_raw(self, args: SearchArgs, ws, stream=None) -> Result:
         """Direct call for timing loops: caller-built SearchArgs and workspace."""

@@ -259,22 +259,72 @@ def cfg4(seed=0) -> Instance:
                          dtype="bf16", top_k=64, name="n8_k16_h256_bf16")
 
 
+def _slot_stats(inst: Instance):
+    """Mean and SD of each aggregate slot under a uniform choice per model,
+    from the option tables alone."""
+    offs = np.concatenate([[0], np.cumsum(inst.n_options)])
+    mu = np.zeros(inst.n_agg)
+    var = np.zeros(inst.n_agg)
+    for k, c in enumerate(inst.agg_cols):
+        for i in range(inst.n_models):
+            col = inst.features[offs[i]:offs[i + 1], c].astype(np.float64)
+            mu[k] += col.mean()
+            var[k] += col.var()
+    return mu, np.sqrt(var)
+
+
 def make_state(inst: Instance, seed: int = 0, spread: float = 0.5) -> np.ndarray:
     """An observed aggregate state (what the runtime monitor reports,
     Section II), float32 [A]: each slot drawn around its mean under a uniform
     choice per model, `spread` standard deviations wide, on the 2^-14 grid.
     The statistics come from the option tables alone."""
     rng = np.random.Generator(np.random.PCG64(seed * 104729 + 3))
-    offs = np.concatenate([[0], np.cumsum(inst.n_options)])
-    st = np.zeros(inst.n_agg)
-    for k, c in enumerate(inst.agg_cols):
-        mu = var = 0.0
-        for i in range(inst.n_models):
-            col = inst.features[offs[i]:offs[i + 1], c].astype(np.float64)
-            mu += col.mean()
-            var += col.var()
-        st[k] = mu + spread * np.sqrt(var) * rng.standard_normal()
+    mu, sd = _slot_stats(inst)
+    st = np.array([mu[k] + spread * sd[k] * rng.standard_normal() for k in range(inst.n_agg)])
     return _quantise(st).astype(np.float32)
+
+
+@dataclass
+class Scenarios:
+    """Dynamic scenarios of the scheduling protocol (Section IV-C, Table II):
+    per scenario s and decision step t the observed aggregate state, the
+    latency bounds and the objective weights."""
+    states: np.ndarray           # float32 [S][T][A]
+    sla: np.ndarray              # float32 [S][T][N]
+    omega: np.ndarray            # float32 [S][T][N]
+    elevated: np.ndarray         # int32 [S]: the model whose weight a scenario raises
+
+
+def make_scenarios(inst: Instance, n_scen: int = 8, n_steps: int = 12, seed: int = 0, rho: float = 0.8,
+                   walk: float = 0.3, elevate: float = 2.0, latency_bounds: bool = False) -> Scenarios:
+    """Seeded dynamic scenarios.  The observed state follows an AR(1) walk per
+    slot toward the slot mean (start mean + 0.5 SD z, then mean + rho (x -
+    mean) + walk SD z), on the 2^-14 grid; one model per scenario has its
+    weight raised to `elevate` over a window of steps (the others 1: Section
+    II sets omega_i = 1 unless a scenario elevates one).  The service
+    constraint is the throughput floor of Eq. 3, so the latency bounds are
+    +inf unless latency_bounds (then the instance's bounds at every step)."""
+    N, A, T = inst.n_models, inst.n_agg, n_steps
+    mu, sd = _slot_stats(inst)
+    states = np.zeros((n_scen, T, A), np.float32)
+    sla = np.full((n_scen, T, N), np.inf, np.float32)
+    omega = np.ones((n_scen, T, N), np.float32)
+    elevated = np.zeros(n_scen, np.int32)
+    for s in range(n_scen):
+        rng = np.random.Generator(np.random.PCG64(seed * 7919 + 1009 * s + 11))
+        x = mu + 0.5 * sd * rng.standard_normal(A)
+        for t in range(T):
+            if t > 0:
+                x = mu + rho * (x - mu) + walk * sd * rng.standard_normal(A)
+            states[s, t] = _quantise(x).astype(np.float32)
+        e = int(rng.integers(N))
+        a = int(rng.integers(0, max(T // 2, 1)))
+        b = min(T, a + max(T // 3, 1))
+        omega[s, a:b, e] = elevate
+        elevated[s] = e
+        if latency_bounds:
+            sla[s] = inst.sla[None, :]
+    return Scenarios(states, sla, omega, elevated)
 
 
 # ---------------------------------------------------------------------------
