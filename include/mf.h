@@ -279,7 +279,8 @@ mf_status mf_eval_canonical(mf_problem *p, const uint64_t *d_idx, int64_t n, con
 /* Genetic-algorithm scheduler (Section IV-C) over S independent scenarios,
  * each with its own latency bounds and objective weights.  Fitness is the
  * canonical J of each individual (the same decode, aggregate, surrogate, mask
- * and score steps as the search).  Random draws come from Philox4x64-10
+ * and score steps as the search, including the objective and the fixed
+ * observed state when given).  Random draws come from Philox4x64-10
  * (Salmon et al., SC'11) keyed by `seed`; see mf_ga.hip for the counter
  * layout and operator order. */
 typedef struct {
@@ -294,6 +295,9 @@ typedef struct {
     uint64_t seed;
     const float *d_sla;        /* device [S][N] */
     const float *d_omega;      /* device [S][N] */
+    uint32_t flags;            /* MF_FIXED_STATE: the surrogates see state[] (as in mf_search) */
+    float state[MF_MAX_AGG];   /* MF_FIXED_STATE: observed aggregate, original slot order, finite */
+    mf_objective objective;    /* zero-initialised: MF_OBJ_LINEAR; MF_OBJ_EQ3 as in mf_search */
 } mf_ga_args;
 
 mf_status mf_ga_workspace_size(const mf_problem *p, const mf_ga_args *args, size_t *bytes);

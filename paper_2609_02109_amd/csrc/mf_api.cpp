@@ -1418,6 +1418,12 @@ static mf_status check_ga_args(const mf_problem *p, const mf_ga_args *a)
         return MF_EINVAL;
     for (float q : {a->p_cx, a->p_swap, a->p_mut})
         if (!std::isfinite(q)) return MF_EINVAL;
+    if (a->flags & ~MF_FIXED_STATE) return MF_EINVAL;
+    if (a->flags & MF_FIXED_STATE)
+        for (int k = 0; k < p->A; k++)
+            if (!std::isfinite(a->state[k])) return MF_EINVAL;
+    mf_status st = check_objective(p, a->objective);
+    if (st != MF_OK) return st;
     if (p->space > (1ull << 32)) return MF_EUNSUPPORTED;
     if (!ga_fitness_supported(p->L + p->A, p->H1, p->H2)) return MF_EUNSUPPORTED;
     return MF_OK;
@@ -1486,6 +1492,9 @@ mf_status mf_ga_run(mf_problem *p, const mf_ga_args *args, void *d_ws, size_t ws
     c.agg_cols = p->d_agg_cols;
     c.w64 = p->d_w64;
     c.wstride = p->wstride;
+    c.fixed = (args->flags & MF_FIXED_STATE) ? 1 : 0;
+    for (int k = 0; k < p->A; k++) c.state[k] = c.fixed ? args->state[k] : 0.f;
+    c.obj = obj_args(p, args->objective);
 
     const int S = args->n_scen, P = args->pop;
     MF_HIP(launch_ga_feasible(c, cnt, blk_off, n_fl, fl, s));

@@ -14,7 +14,7 @@
 // mutation / repair, slot for initialisation):
 //   INIT 1 (gen 0), SEL 2 + m/4 (draw m of 2k), CX 8, SWAP 9 + i/4 (gene i),
 //   MUT 16 + w/4 (word w = 2i: mutate?, 2i+1: new value), REP 32.
-#include "mf_device.h"
+#include "mf_canon.h"
 
 namespace mfi {
 
@@ -137,6 +137,15 @@ template <int NIN, int H1, int H2, bool BF16>
 __global__ void __launch_bounds__(256) ga_fitness_kernel(const GAConst c, int S, int P, const uint64_t *pop,
                                                          const float *sla, const float *omega, double *fit)
 {
+    __shared__ float s_tau[kMaxN];
+    __shared__ int32_t s_prev[kMaxN];
+#pragma unroll
+    for (int j = 0; j < kMaxN; j++)   // compile-time index into the argument block
+        if (threadIdx.x == (unsigned)j) {
+            s_tau[j] = c.obj.tau[j];
+            s_prev[j] = c.obj.prev[j];
+        }
+    __syncthreads();
     const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (t >= (int64_t)S * P) return;
     const int s = (int)(t / P);
@@ -158,7 +167,9 @@ __global__ void __launch_bounds__(256) ga_fitness_kernel(const GAConst c, int S,
             const int col = c.agg_cols[k - L];
             float a = 0.f;
             for (int i = 0; i < N; i++) a = a + c.features[(int64_t)(c.opt_off[i] + d[i]) * L + col];
-            z[k] = (double)a;
+            // the surrogates' aggregate input: the candidate's, or the
+            // observed state held fixed (the VRAM cap still sees the candidate)
+            z[k] = c.fixed ? (double)c.state[k - L] : (double)a;
             if (k - L == c.vram_slot) agg_v = a;
         }
     }
@@ -201,7 +212,19 @@ __global__ void __launch_bounds__(256) ga_fitness_kernel(const GAConst c, int S,
             y1 = fma(W3[H2 + v], a, y1);
         }
         if (!(y0 <= (double)sla[(int64_t)s * N + i])) sla_ok = false;
-        J = fma((double)omega[(int64_t)s * N + i], y1, J);
+        const double om = (double)omega[(int64_t)s * N + i];
+        if (c.obj.kind != 0) {
+            // the full utility of Eq. 3, canonical term order
+            double q, Pr, pen;
+            bool do_P, do_pen;
+            if (!canon_eq3(c.obj, c.opt_off[i] + d[i], y1, s_tau[i], s_prev[i], q, Pr, do_P, pen, do_pen))
+                sla_ok = false;
+            J = fma(om, q, J);
+            if (do_P) J = J - Pr;
+            if (do_pen) J = J - pen;
+        } else {
+            J = fma(om, y1, J);
+        }
     }
     fit[t] = (vram_ok && sla_ok) ? J : -INFINITY;
 }

@@ -326,6 +326,9 @@ struct GAConst {
     const int32_t *agg_cols;    // [A]
     const double *w64;          // [N][stride] packed weights (W1 b1 W2 b2 W3 b3) as fp64
     int64_t wstride;
+    int fixed;                  // the surrogates see state[] instead of the candidate's aggregate
+    float state[kMaxN];
+    ObjArgs obj;
 };
 
 // launchers (return hipError_t of the launch)

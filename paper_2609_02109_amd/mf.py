@@ -96,7 +96,8 @@ class StaticArgs(C.Structure):
 class GAArgs(C.Structure):
     _fields_ = [("n_scen", C.c_int32), ("pop", C.c_int32), ("gens", C.c_int32), ("tourn_k", C.c_int32),
                 ("p_cx", C.c_float), ("p_swap", C.c_float), ("p_mut", C.c_float), ("pad", C.c_float),
-                ("seed", C.c_uint64), ("d_sla", C.c_void_p), ("d_omega", C.c_void_p)]
+                ("seed", C.c_uint64), ("d_sla", C.c_void_p), ("d_omega", C.c_void_p),
+                ("flags", C.c_uint32), ("state", C.c_float * MAX_AGG), ("objective", Objective)]
 
 
 def _load():
@@ -351,14 +352,23 @@ class Problem:
         return dict(pred=pred[:n], J=J[:n], flags=fl[:n], _inputs=(d_idx, d_sla, d_om))
 
     def ga(self, sla, omega, pop=2048, gens=100, tourn_k=3, p_cx=0.7, p_swap=0.5, p_mut=0.05,
-           seed=0, final_pop=False, stream=None):
-        """GA scheduler over S scenarios (rows of sla / omega)."""
+           seed=0, final_pop=False, stream=None, objective=None, state=None):
+        """GA scheduler over S scenarios (rows of sla / omega); objective and
+        state as in search()."""
         import torch
         d_sla = self._dev(sla, torch.float32)
         d_om = self._dev(omega, torch.float32)
         S = int(d_sla.shape[0])
         args = GAArgs(S, int(pop), int(gens), int(tourn_k), float(p_cx), float(p_swap), float(p_mut),
                       0.0, int(seed), _ptr(d_sla), _ptr(d_om))
+        args.objective = objective_args(objective, self.N)
+        if state is not None:
+            st = np.asarray(state, np.float32).reshape(-1)
+            if st.size != self.A:
+                raise ValueError(f"state has {st.size} values, the problem {self.A} aggregate slots")
+            args.flags = MF_FIXED_STATE
+            for t in range(st.size):
+                args.state[t] = float(st[t])
         nbytes = C.c_size_t()
         _check(lib.mf_ga_workspace_size(self.handle, C.byref(args), C.byref(nbytes)),
                "mf_ga_workspace_size")

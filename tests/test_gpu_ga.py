@@ -79,3 +79,39 @@ def test_ga_rejects_bad_arguments(mf):
         with pytest.raises(mf.MfError) as e:
             p.ga(sc.sla[:2], sc.omega[:2], **kw)
         assert e.value.status == mf.MF_EINVAL
+
+
+def run_both_obj(mf, orc, inst, sla, omega, ob, st, **kw):
+    print(f"[ga] {inst.name} S={len(sla)} eq3={ob is not None} fixed={st is not None} {kw}", flush=True)
+    g = mf.Problem(inst, variants=ob).ga(sla, omega, final_pop=True, objective=ob, state=st, **kw)
+    r = orc.Problem(inst, ob, state=st).ga(sla, omega, final_pop=True, **kw)
+    np.testing.assert_array_equal(g["best_idx"], r["best_idx"])
+    assert g["best_J"].tobytes() == r["best_J"].tobytes()
+    np.testing.assert_array_equal(g["final_pop"].cpu().numpy().astype(np.uint64), r["final_pop"])
+    return g, r
+
+
+def test_ga_fixed_state_eq3(mf, orc):
+    # the paper's GA setting (Section IV-C): population 100, 30 generations,
+    # crossover 0.7, mutation 0.1, tournament 3, with the observed state
+    # held fixed and the full utility of Eq. 3
+    inst = synth.cfg1(0)
+    ob = synth.make_objective(inst, 0)
+    st = synth.make_state(inst, 0)
+    sc = synth.ga_scenarios(5, 6, seed=1)
+    g, r = run_both_obj(mf, orc, inst, sc.sla, sc.omega, ob, st, pop=100, gens=30, p_mut=0.1, seed=3)
+    p = mf.Problem(inst, variants=ob)
+    for s in range(6):
+        ex = p.search(sc.sla[s], sc.omega[s], k=1, objective=ob, state=st)
+        assert g["best_J"][s] <= ex["top_J"][0]
+
+
+def test_ga_objective_and_state_apart(mf, orc):
+    inst = synth.cfg1(2)
+    sc = synth.ga_scenarios(5, 3, seed=2)
+    run_both_obj(mf, orc, inst, sc.sla, sc.omega, synth.make_objective(inst, 2), None, pop=64, gens=8, seed=7)
+    run_both_obj(mf, orc, inst, sc.sla, sc.omega, None, synth.make_state(inst, 2), pop=64, gens=8, seed=8)
+    bf = synth.make_instance([7, 9, 3, 5], 8, 4, 64, 64, seed=9, vram_quantile=0.7, dtype="bf16")
+    sc2 = synth.ga_scenarios(4, 2, seed=9)
+    run_both_obj(mf, orc, bf, sc2.sla, sc2.omega, synth.make_objective(bf, 9), synth.make_state(bf, 9),
+                 pop=32, gens=5, seed=2)
