@@ -174,6 +174,31 @@ def bench_fixed(mf, torch, seed, steps, warmup):
     return out
 
 
+def bench_protocol(seeds=(0, 1, 2), n_scen=8, n_steps=12):
+    """The scheduling protocol of Table II (Section IV-C) on the N=5 instance:
+    8 synthetic dynamic scenarios x 12 steps x 3 seeds, full utility of Eq. 3
+    with the observed state held fixed per step."""
+    import numpy as np
+    from paper_2609_02109_amd import protocol, synth
+    runs, t0 = [], time.perf_counter()
+    for seed in seeds:
+        inst = synth.cfg1(seed)
+        ob = synth.make_objective(inst, seed)
+        sc = synth.make_scenarios(inst, n_scen, n_steps, seed=seed)
+        dr = synth.protocol_draws(inst, n_scen, n_steps, seed=seed)
+        runs.append(protocol.Protocol(inst, ob).run(sc, dr))
+    wall = time.perf_counter() - t0
+    table = protocol.metrics(runs)
+    lat = {name: float(np.median(np.concatenate([r[name]["ms"].ravel() for r in runs])))
+           for name in ("exhaustive", "ga", "random")}
+    log(f"protocol: {wall:.1f} s; " + "; ".join(f"{k} J={v['mean_J']:.4f} gap={v['avg_gap']:.2f}% "
+                                                 f"sla={v['sla_pct']:.2f}%" for k, v in table.items()))
+    return {"workload": f"Table II protocol: N=5 instance (12,12,9,9,9 options), {n_scen} dynamic scenarios x "
+                        f"{n_steps} steps x {len(seeds)} seeds, Eq. 3 with floors, observed state per step; "
+                        "GA population 100, 30 generations, mutation 0.1",
+            "table": table, "median_decision_ms": lat, "wall_s": wall}
+
+
 def bench_ga(args):
     import torch
     from paper_2609_02109_amd import mf, synth
@@ -207,11 +232,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--workload", choices=["n6", "ga", "n8", "fixed"], default="n6",
+    ap.add_argument("--workload", choices=["n6", "ga", "n8", "fixed", "protocol"], default="n6",
                     help="n6: the N=6 exhaustive search (the benchmark step); ga: the N=5 GA scheduler; "
-                         "n8: only the N=8 bf16 search; fixed: only the fixed-state searches")
+                         "n8: only the N=8 bf16 search; fixed: only the fixed-state searches; protocol: "
+                         "only the Table II scheduling protocol")
     ap.add_argument("--no-n8", action="store_true", help="skip the N=8 bf16 search in the n6 line")
     ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-state searches in the n6 line")
+    ap.add_argument("--no-protocol", action="store_true", help="skip the Table II protocol in the n6 line")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="run one plain device copy kernel of this many bytes read (and written) "
                          "before the search: the calibration point for HBM byte counters")
@@ -230,6 +257,9 @@ def main():
         return
     if args.workload == "fixed":
         print(json.dumps(bench_fixed(mf, torch, args.seed, args.steps, args.warmup)), flush=True)
+        return
+    if args.workload == "protocol":
+        print(json.dumps(bench_protocol()), flush=True)
         return
 
     if args.copy_bytes:
@@ -258,6 +288,7 @@ def main():
     log(f"eq3 search: {ms3:.2f} ms/step, fast kernel {kms3:.2f} ms, n_feas={r3.n_feas} n_flagged={r3.n_flagged}")
 
     fixed = None if args.no_fixed else bench_fixed(mf, torch, args.seed, max(args.steps, 20), max(args.warmup, 3))
+    proto = None if args.no_protocol else bench_protocol()
 
     cpu = None
     if not args.no_cpu:
@@ -293,7 +324,8 @@ def main():
                               "fast_kernel_frac": algorithmic_flops_per_config(inst) * n / (kms3 * 1e-3) / 1e12
                               / PEAK_FP32_TFLOPS, "n_feas": int(r3.n_feas), "n_flagged": int(r3.n_flagged),
                               "argmax": int(r3.top_idx[0])},
-                   "fixed_state": fixed},
+                   "fixed_state": fixed,
+                   "protocol": proto},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_FP32_TFLOPS, "traffic": measured_traffic(),
                      "kernel": "fast_kernel<8,6,64>", "kernel_ms": kms,

@@ -405,6 +405,28 @@ def linear_objective(inst: Instance) -> Objective:
 
 
 @dataclass
+class ProtocolDraws:
+    """The random choices of the scheduling protocol (Section IV-C), drawn
+    here so that every implementation of the protocol makes the same ones."""
+    budget: np.ndarray           # uint64 [S][K_max]: uniform joint indices, StaticBudgetK's offline samples
+    random: np.ndarray           # uint64 [S][T][R]: uniform joint indices, the Random scheduler's candidates
+    ga_seed: np.ndarray          # uint64 [S][T]: the GA's generator key per decision
+
+
+def protocol_draws(inst: Instance, n_scen: int, n_steps: int, seed: int = 0, k_max: int = 5000,
+                   n_random: int = 64) -> ProtocolDraws:
+    """Uniform joint indices for StaticBudgetK (the budgets use prefixes of
+    one list) and candidates for the Random scheduler (it takes the first one
+    that meets the VRAM cap), and one GA key per scenario and step."""
+    rng = np.random.Generator(np.random.PCG64(seed * 104723 + 29))
+    n = inst.space_size
+    budget = rng.integers(0, n, (n_scen, k_max), dtype=np.uint64)
+    rand = rng.integers(0, n, (n_scen, n_steps, n_random), dtype=np.uint64)
+    ga_seed = rng.integers(0, 2 ** 62, (n_scen, n_steps), dtype=np.uint64)
+    return ProtocolDraws(budget, rand, ga_seed)
+
+
+@dataclass
 class GAScenarios:
     sla: np.ndarray      # float32 [S][N]
     omega: np.ndarray    # float32 [S][N]

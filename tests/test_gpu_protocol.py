@@ -1,0 +1,55 @@
+"""The scheduling protocol (Section IV-C, Table II) on the GPU against the
+oracle's protocol, through the C ABI: every decision and recorded utility
+identical, the Table II columns equal to rounding."""
+import numpy as np
+import pytest
+
+from paper_2609_02109_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def proto():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_02109_amd import protocol
+    return protocol
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_protocol_matches_the_oracle(proto, orc, seed):
+    import oracle.protocol as op
+    inst = synth.cfg1(seed)
+    ob = synth.make_objective(inst, seed)
+    sc = synth.make_scenarios(inst, 3, 5, seed=seed)
+    dr = synth.protocol_draws(inst, 3, 5, seed=seed)
+    P = proto.ProtocolParams()
+    print(f"[protocol] seed={seed} S=3 T=5", flush=True)
+    g = proto.Protocol(inst, ob, P).run(sc, dr)
+    r = op.run(inst, ob, sc, dr, P, proto.scheduler_names(P))
+    for name in proto.scheduler_names(P):
+        np.testing.assert_array_equal(g[name]["idx"], r[name]["idx"], err_msg=name)
+        assert g[name]["J"].tobytes() == r[name]["J"].tobytes(), name
+        np.testing.assert_array_equal(g[name]["ok"], r[name]["ok"], err_msg=name)
+    tg, tr = proto.metrics(g), op.table([r])
+    for name in tg:
+        for col in ("mean_J", "avg_gap", "worst_gap", "sla_pct"):
+            assert abs(tg[name][col] - tr[name][col]) <= 1e-9 * max(1.0, abs(tr[name][col])), (name, col)
+    assert tg["exhaustive"]["avg_gap"] == 0.0
+
+
+def test_protocol_with_latency_bounds_and_derived_gaps(proto, orc):
+    import oracle.protocol as op
+    inst = synth.cfg0(1)
+    ob = synth.make_objective(inst, 1)
+    sc = synth.make_scenarios(inst, 2, 6, seed=3, latency_bounds=True)
+    dr = synth.protocol_draws(inst, 2, 6, seed=3, k_max=40, n_random=8)
+    P = proto.ProtocolParams(budgets=(40, 10), ga_pop=8, ga_gens=3)
+    g = proto.Protocol(inst, ob, P).run(sc, dr)
+    r = op.run(inst, ob, sc, dr, P, proto.scheduler_names(P))
+    for name in proto.scheduler_names(P):
+        np.testing.assert_array_equal(g[name]["idx"], r[name]["idx"], err_msg=name)
+        assert g[name]["J"].tobytes() == r[name]["J"].tobytes(), name
+        np.testing.assert_array_equal(g[name]["ok"], r[name]["ok"], err_msg=name)
