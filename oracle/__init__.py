@@ -47,7 +47,7 @@ class _Inst(C.Structure):
                 ("hidden1", C.c_int32), ("hidden2", C.c_int32), ("bf16", C.c_int32),
                 ("n_options", C.c_void_p), ("features", C.c_void_p), ("agg_cols", C.c_void_p),
                 ("vram_slot", C.c_int32), ("vram_cap", C.c_float), ("weights", C.c_void_p),
-                ("obj", C.c_void_p), ("fixed_state", C.c_void_p), ("raw_J", C.c_int32)]
+                ("obj", C.c_void_p), ("fixed_state", C.c_void_p), ("raw_J", C.c_int32), ("sigmoid", C.c_int32)]
 
 
 class _Result(C.Structure):
@@ -84,6 +84,9 @@ def lib():
         L.orc_vram_feasible.argtypes = [P, P, C.c_uint64]
         L.orc_bf16_round.restype = C.c_double
         L.orc_bf16_round.argtypes = [C.c_double]
+        for fn in ("orc_exp", "orc_sigmoid"):
+            getattr(L, fn).restype = C.c_double
+            getattr(L, fn).argtypes = [C.c_double]
         L.orc_philox4x64.argtypes = [P, P, P]
         L.orc_ga.restype = C.c_int
         L.orc_ga.argtypes = [P, P, P, P, P, P, P, C.c_int]
@@ -116,7 +119,8 @@ class Problem:
                        int(inst.hidden2), 1 if inst.dtype == "bf16" else 0,
                        _ptr(self.n_options).value, _ptr(self.features).value,
                        _ptr(self.agg_cols).value, int(inst.vram_slot),
-                       float(inst.vram_cap), _ptr(self.weights).value, None, None)
+                       float(inst.vram_cap), _ptr(self.weights).value, None, None, 0,
+                       1 if getattr(inst, "act", "identity") == "sigmoid" else 0)
         self.state = None
         if state is not None:
             self.state = np.ascontiguousarray(state, np.float32)
@@ -332,6 +336,15 @@ def philox4x64(ctr, key):
 
 def bf16_round(x: float) -> float:
     return float(lib().orc_bf16_round(float(x)))
+
+
+def exp(x: float) -> float:
+    """The oracle's e^x (|x| <= 700; the algorithm of mf_oracle.c)."""
+    return float(lib().orc_exp(float(x)))
+
+
+def sigmoid(y: float) -> float:
+    return float(lib().orc_sigmoid(float(y)))
 
 
 FLAG_VRAM, FLAG_SLA, FLAG_FEAS, FLAG_EXACT = 1, 2, 4, 8

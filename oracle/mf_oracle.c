@@ -39,6 +39,14 @@
  *     f = (thr - fmin) / Rg, q = Q f, J = fma(omega, q, J), J = J - alpha c
  *     (variant changed), d = (tau + delta) - f, J = J - beta (d d) if d > 0.
  *
+ *   Output activation (Section III-B: the predictor ends in a sigmoid, when
+ *     the sigmoid flag is set): lat = s(y0), thr = s(y1) with
+ *     s(y) = 1 / (1 + e^-y), y clamped to [-700, 700] first.  e^x is defined
+ *     by this algorithm (so that it is one function on every machine):
+ *     k = rint(x * (1/ln 2)); r = x - k ln2_hi - k ln2_lo (two fmas, ln2_hi
+ *     = ln 2 rounded to 24 bits); e^r by its Taylor series to degree 13
+ *     (Horner, coefficients 1/n! rounded once, fma); times 2^k.
+ *
  * Precision: every floating-point step is fp64.  Each dot product is one
  * fused multiply-add chain in ascending input order, starting from the bias;
  * relu(x) = (x > 0 ? x : +0).  The aggregate is summed in fp32 (model order)
@@ -131,7 +139,33 @@ int orc_aggregate(const orc_instance *in, const int32_t *digits, float *a)
 
 /* One model's surrogate, canonical fp64.  w: fp64 copy of that model's packed
  * weights.  z: [L + A] inputs.  y[0] latency, y[1] throughput. */
-static void mlp_forward(const double *w, int nin, int h1n, int h2n, int bf16,
+/* e^x for |x| <= 700 (see the header comment for the definition). */
+double orc_exp(double x)
+{
+    const double inv_ln2 = 1.4426950408889634;          /* 1 / ln 2 */
+    const double ln2_hi = 0.693147182464599609375;      /* ln 2 to 24 significant bits */
+    const double ln2_lo = -1.904654299957768e-09;       /* ln 2 - ln2_hi */
+    const double k = rint(x * inv_ln2);
+    double r = fma(-k, ln2_hi, x);
+    r = fma(-k, ln2_lo, r);
+    double fact = 1.0;
+    double inv_fact[14];
+    for (int n = 0; n < 14; n++) {
+        if (n > 0) fact *= (double)n;
+        inv_fact[n] = 1.0 / fact;
+    }
+    double p = inv_fact[13];
+    for (int n = 12; n >= 0; n--) p = fma(p, r, inv_fact[n]);
+    return ldexp(p, (int)k);
+}
+
+double orc_sigmoid(double y)
+{
+    const double c = y < -700.0 ? -700.0 : (y > 700.0 ? 700.0 : y);
+    return 1.0 / (1.0 + orc_exp(-c));
+}
+
+static void mlp_forward(const double *w, int nin, int h1n, int h2n, int bf16, int sigmoid,
                         const double *z, double *h1, double *h2, double *y)
 {
     const double *W1 = w, *b1 = W1 + (int64_t)h1n * nin, *W2 = b1 + h1n,
@@ -159,7 +193,7 @@ static void mlp_forward(const double *w, int nin, int h1n, int h2n, int bf16,
     for (int o = 0; o < 2; o++) {
         double c = b3[o];
         for (int v = 0; v < h2n; v++) c = fma(W3[(int64_t)o * h2n + v], h2[v], c);
-        y[o] = c;
+        y[o] = sigmoid ? orc_sigmoid(c) : c;
     }
 }
 
@@ -196,7 +230,7 @@ void orc_eval_w(const orc_instance *in, const double *w64, uint64_t idx,
         for (int k = 0; k < L; k++) z[k] = (double)x[k];
         for (int k = 0; k < A; k++) z[L + k] = (double)(in->fixed_state ? in->fixed_state[k] : a[k]);
         double y[2];
-        mlp_forward(w64 + stride * i, nin, in->hidden1, in->hidden2, in->bf16, z, h1, h2, y);
+        mlp_forward(w64 + stride * i, nin, in->hidden1, in->hidden2, in->bf16, in->sigmoid, z, h1, h2, y);
         lat[i] = y[0];
         thr[i] = y[1];
         if (!(y[0] <= (double)sla[i])) { sla_ok = 0; f |= 1u << (8 + i); }

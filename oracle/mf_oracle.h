@@ -37,7 +37,12 @@ typedef struct {
     int32_t raw_J;              /* nonzero: J is the utility value also where a constraint fails
                                    (the flags still say which); for evaluating decisions that break
                                    a bound, as a random scheduler's do (Section IV-C, Table II) */
+    int32_t sigmoid;            /* nonzero: both surrogate outputs pass a sigmoid (the predictor's
+                                   output layer, Section III-B); zero: identity output */
 } orc_instance;
+
+double orc_exp(double x);
+double orc_sigmoid(double y);
 
 typedef struct {
     uint64_t n_eval, n_vram, n_feas;

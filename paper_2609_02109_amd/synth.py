@@ -99,6 +99,7 @@ class Instance:
     top_k: int = 1
     seed: int = 0
     extra: dict = field(default_factory=dict)
+    act: str = "identity"          # output activation: "identity" or "sigmoid" (the paper's predictor)
 
     @property
     def n_models(self) -> int:
@@ -123,7 +124,7 @@ class Instance:
 def make_instance(n_options, n_local=8, n_agg=4, hidden1=32, hidden2=32, *,
                   seed=0, dtype="f32", vram_cap=None, vram_quantile=None,
                   sla_range=(0.5, 2.0), top_k=1, types=None,
-                  symmetric=False, name="custom") -> Instance:
+                  symmetric=False, name="custom", act="identity") -> Instance:
     """Draw one instance.
 
     n_options: option count per model.  types: per-model family (0 LLM, 1
@@ -132,8 +133,11 @@ def make_instance(n_options, n_local=8, n_agg=4, hidden1=32, hidden2=32, *,
     vram_cap: fixed cap in GB; vram_quantile: cap set at that quantile of the
     normal approximation to the joint VRAM sum (a uniform choice per model).
     symmetric: copy model 0's option table and weights to every model (all
-    options counts must agree).
+    options counts must agree).  act: the surrogates' output activation
+    ("sigmoid": outputs in (0, 1), so latency bounds belong in (0, 1)).
     """
+    if act not in ("identity", "sigmoid"):
+        raise ValueError(f"unknown output activation {act!r}")
     n_options = np.asarray(n_options, dtype=np.int32)
     N = int(n_options.shape[0])
     if n_local < 8:
@@ -224,7 +228,7 @@ def make_instance(n_options, n_local=8, n_agg=4, hidden1=32, hidden2=32, *,
                     features=feats64.astype(np.float32), agg_cols=agg_cols,
                     vram_slot=VRAM_SLOT, vram_cap=float(np.float32(vram_cap)),
                     weights=weights, sla=sla, omega=omega, dtype=dtype,
-                    top_k=top_k, seed=seed)
+                    top_k=top_k, seed=seed, act=act)
 
 
 # ---------------------------------------------------------------------------
@@ -378,10 +382,12 @@ def make_objective(inst: Instance, seed: int = 0, tau_range=(0.2, 0.35), with_pr
         nv[i] = V
         for o in range(K[i]):
             variant[off + o] = (o * V) // K[i]
+        # extremes on the surrogate's output scale: sigmoid outputs lie in (0, 1)
+        lo_r, hi_r = ((0.0, 0.2), (0.8, 1.0)) if inst.act == "sigmoid" else ((-2.0, -1.0), (1.0, 2.0))
         for v in range(V):
             qual[i, v] = q[len(q) - V + v]
-            fmin[i, v] = _quantise(rng.uniform(-2.0, -1.0))
-            fmax[i, v] = _quantise(rng.uniform(1.0, 2.0))
+            fmin[i, v] = _quantise(rng.uniform(*lo_r))
+            fmax[i, v] = _quantise(rng.uniform(*hi_r))
         cost[i] = RELOAD_LLM if llm else RELOAD_VIS
         if with_prev:
             prev[i] = variant[off + int(rng.integers(0, K[i]))]
