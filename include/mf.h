@@ -37,7 +37,13 @@
  *    in model order 0..N-1, of column agg_cols[k] of every model's chosen row
  *    (each model's own row included).
  *  - Surrogate of model i (Eq. 6): z = [F row of lambda_i (L) | a (A)],
- *    h1 = relu(W1 z + b1), h2 = relu(W2 h1 + b2), (lat, thr) = W3 h2 + b3.
+ *    h1 = relu(W1 z + b1), h2 = relu(W2 h1 + b2), (lat, thr) = out(W3 h2 + b3)
+ *    with out the identity or, for MF_ACT_SIGMOID (the predictor's sigmoid
+ *    output, Section III-B), s(y) = 1 / (1 + e^-y) on y clamped to
+ *    [-700, 700].  Canonically e^x is this algorithm: k = rint(x * (1/ln 2)),
+ *    r = fma(-k, ln2_hi, x) then r = fma(-k, ln2_lo, r) (ln2_hi = ln 2 to 24
+ *    significant bits), e^r = the degree-13 Taylor polynomial by Horner with
+ *    fma and coefficients 1/n! each rounded once, times 2^k.
  *  - Feasible: a[vram_slot] <= vram_cap and lat_i <= sla_i for every i
  *    (both inclusive, Eq. 4).  J = sum_i omega_i thr_i if feasible, else -inf.
  *  - Results are defined by canonical fp64 semantics: each dot product is one
@@ -70,6 +76,8 @@ typedef enum {
 } mf_status;
 
 typedef enum { MF_F32 = 0, MF_BF16 = 1 } mf_dtype;
+
+typedef enum { MF_ACT_IDENTITY = 0, MF_ACT_SIGMOID = 1 } mf_activation;
 
 #define MF_MAX_MODELS 16
 #define MF_MAX_TOPK 64
@@ -107,6 +115,7 @@ typedef struct {
     float vram_cap;             /* finite */
     mf_dtype dtype;
     const mf_variants *variants; /* NULL: only the linear objective is available */
+    int32_t output_act;          /* mf_activation of both surrogate outputs (zero: identity) */
 } mf_desc;
 
 /* Create a problem.  d_features: float [sum K_i][L].  d_weights: float

@@ -19,6 +19,7 @@ using namespace mfi;
 struct mf_problem {
     int N = 0, L = 0, A = 0, H1 = 0, H2 = 0;
     bool bf16 = false;
+    int act = MF_ACT_IDENTITY;   // output activation of both surrogate outputs
     std::vector<int32_t> K, agg_cols, opt_off;
     int vram_slot = 0;
     float vram_cap = 0.f;
@@ -302,7 +303,7 @@ WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k)
         w.grid = (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)p.num_cus));
     } else {
         w.kp = choose_kp(top_k, 64);
-        w.waves = fast_waves_for(p.N, p.lay, w.kp);
+        w.waves = fast_waves_for(p.N, p.lay, w.kp, p.act);
         const uint64_t tiles = (n + 31) / 32;
         const uint64_t g = (tiles + w.waves - 1) / w.waves;
         w.grid = (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)p.num_cus));
@@ -458,7 +459,7 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     fa.obj = obj_args(p, args->objective);
 
     CanonArgs ca{};
-    ca.n_models = p->N; ca.L = p->L; ca.A = p->A; ca.H1 = p->H1; ca.H2 = p->H2; ca.bf16 = p->bf16;
+    ca.n_models = p->N; ca.L = p->L; ca.A = p->A; ca.H1 = p->H1; ca.H2 = p->H2; ca.bf16 = p->bf16; ca.act = p->act;
     for (int i = 0; i < p->N; i++) { ca.K[i] = p->K[i]; ca.opt_off[i] = p->opt_off[i]; }
     ca.agg_cols = p->d_agg_cols; ca.vram_slot = p->vram_slot; ca.vram_cap = p->vram_cap;
     ca.features = p->d_features; ca.weights = p->d_canon; ca.wstride = p->wstride;
@@ -655,6 +656,7 @@ FixedArgs fixed_base(const mf_problem *p, const mf_objective &objective, int top
 {
     FixedArgs a{};
     a.n_models = p->N; a.L = p->L; a.A = p->A; a.H1 = p->H1; a.H2 = p->H2; a.bf16 = p->bf16; a.sumK = p->sumK;
+    a.act = p->act;
     for (int i = 0; i < p->N; i++) {
         a.K[i] = p->K[i];
         a.opt_off[i] = p->opt_off[i];
@@ -913,11 +915,13 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
         H2 > 256 || !desc->h_n_options || !desc->h_agg_cols)
         return MF_EINVAL;
     if (desc->dtype != MF_F32 && desc->dtype != MF_BF16) return MF_EINVAL;
+    if (desc->output_act != MF_ACT_IDENTITY && desc->output_act != MF_ACT_SIGMOID) return MF_EINVAL;
     if (desc->vram_slot < 0 || desc->vram_slot >= A || !std::isfinite(desc->vram_cap)) return MF_EINVAL;
     mf_problem *p = new (std::nothrow) mf_problem();
     if (!p) return MF_ENOMEM;
     p->N = N; p->L = L; p->A = A; p->H1 = H1; p->H2 = H2;
     p->bf16 = desc->dtype == MF_BF16;
+    p->act = desc->output_act;
     p->vram_slot = desc->vram_slot;
     p->vram_cap = desc->vram_cap;
     p->K.assign(desc->h_n_options, desc->h_n_options + N);
@@ -1082,10 +1086,19 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
             }
         for (int i = 0; i < N; i++)
             model_bounds(*p, F, W, i, &p->fc.bound_lat[i], &p->fc.bound_thr[i], &p->fc.mag_thr[i]);
+        if (p->act == MF_ACT_SIGMOID)
+            for (int i = 0; i < N; i++) {
+                // the sigmoid is 1/4-Lipschitz, and its fp32 evaluation is within
+                // 2^-20; the latency bound stays on the pre-activation scale (its
+                // decision compares the pre-activation with logit thresholds)
+                p->fc.bound_thr[i] = p->fc.bound_thr[i] * 0.25 + 0x1p-20;
+                p->fc.mag_thr[i] = 1.0;
+            }
     }
     {
         FastConst &fc = p->fc;
         fc.n_models = N;
+        fc.act = p->act;
         for (int i = 0; i < N; i++) {
             fc.K[i] = p->K[i];
             fc.opt_off[i] = p->opt_off[i];
@@ -1135,6 +1148,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
                                     W3[o2 * H + 32 * mb + 8 * q + 4 * hf + j];
             float cst[12] = {};
             bf16_bounds(*p, F, W, i, cst, &p->bcst.mag_thr[i]);
+            if (p->act == MF_ACT_SIGMOID) p->bcst.mag_thr[i] = 1.0f;
             cst[0] = b3[0];
             cst[1] = b3[1];
             for (int t = 0; t < 12; t++) blk[bl.off_cst + t] = cst[t];
@@ -1151,6 +1165,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
         p->bcst.g2 = f32_up_host(gam(2.0 * bl.KS, kU32));
         p->bcst.g3 = f32_up_host(gam(H / 8 + 4, kU32));
         p->bcst.gN = f32_up_host(gam(N, kU32));
+        p->bcst.act = p->act;
     }
 
     // ---- canonical image: per model W1T[nin][H1] b1 W2T[H1][H2] b2 W3[2][H2] b3
@@ -1381,7 +1396,7 @@ mf_status mf_eval_fast(mf_problem *p, const uint64_t *d_idx, int64_t n, float *d
     fa.n = (uint64_t)n;
     fa.idx_list = d_idx;
     const uint64_t tiles = ((uint64_t)n + 31) / 32;
-    fa.waves = fast_waves_for(p->N, p->lay, 16);
+    fa.waves = fast_waves_for(p->N, p->lay, 16, p->act);
     const int grid = (int)std::max<uint64_t>(1, std::min<uint64_t>((tiles + fa.waves - 1) / fa.waves,
                                                                     (uint64_t)p->num_cus));
     fa.total_waves = grid * fa.waves;
@@ -1397,7 +1412,7 @@ mf_status mf_eval_canonical(mf_problem *p, const uint64_t *d_idx, int64_t n, con
     if (!p || n < 0 || (n > 0 && (!d_idx || !d_sla || !d_omega))) return MF_EINVAL;
     if (n == 0) return MF_OK;
     CanonArgs ca{};
-    ca.n_models = p->N; ca.L = p->L; ca.A = p->A; ca.H1 = p->H1; ca.H2 = p->H2; ca.bf16 = p->bf16;
+    ca.n_models = p->N; ca.L = p->L; ca.A = p->A; ca.H1 = p->H1; ca.H2 = p->H2; ca.bf16 = p->bf16; ca.act = p->act;
     for (int i = 0; i < p->N; i++) { ca.K[i] = p->K[i]; ca.opt_off[i] = p->opt_off[i]; }
     ca.agg_cols = p->d_agg_cols; ca.vram_slot = p->vram_slot; ca.vram_cap = p->vram_cap;
     ca.features = p->d_features; ca.weights = p->d_canon; ca.wstride = p->wstride;
@@ -1482,7 +1497,7 @@ mf_status mf_ga_run(mf_problem *p, const mf_ga_args *args, void *d_ws, size_t ws
     uint64_t *bI = reinterpret_cast<uint64_t *>(ws + w.bI);
 
     GAConst c{};
-    c.N = p->N; c.L = p->L; c.A = p->A; c.H1 = p->H1; c.H2 = p->H2; c.bf16 = p->bf16;
+    c.N = p->N; c.L = p->L; c.A = p->A; c.H1 = p->H1; c.H2 = p->H2; c.bf16 = p->bf16; c.act = p->act;
     for (int i = 0; i < p->N; i++) { c.K[i] = p->K[i]; c.opt_off[i] = p->opt_off[i]; }
     c.vram_col = p->agg_cols[p->vram_slot];
     c.vram_slot = p->vram_slot;

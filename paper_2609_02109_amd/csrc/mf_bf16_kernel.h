@@ -126,7 +126,7 @@ __device__ __forceinline__ void layer3_row(const floatx16 &acc, int r, const flo
 // (no per-model range checks, no special case in the decode).
 // LIST: evaluate the configurations of args.idx_list (predictions only).
 // OBJ: score with the full utility of Eq. 3 (otherwise the linear objective).
-template <int MAXN, int A, int H, bool FULL, bool LIST, bool OBJ>
+template <int MAXN, int A, int H, bool FULL, bool LIST, bool OBJ, bool SIG = false>
 __global__ void __launch_bounds__(kBf16Waves * 64, 1)
 fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, const int mode, const int kp)
 {
@@ -140,7 +140,9 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
     const int N = FULL ? MAXN : fc.n_models;
     float *G = smem + CL.model_floats;            // [sumK][half][4]: slot 2s+half at [half][s]
     float *Gv = G + Ly.sumK * 8;                   // [sumK] VRAM column
-    // [0,16) sla [16,32) |thr| bound [32,48) omega [48,64) rows [64,80) floor tau [80,96) previous variant
+    // [0,16) sla (sigmoid outputs: the pass threshold of the pre-activation) [16,32) |thr| bound
+    // [32,48) omega [48,64) rows [64,80) floor tau [80,96) previous variant [96,112) miss threshold
+    // of the pre-activation (sigmoid outputs)
     float *par = Gv + Ly.gv_floats;
     int *par_off = reinterpret_cast<int *>(par + 48);
     int *par_prev = reinterpret_cast<int *>(par + 80);
@@ -152,6 +154,17 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
     for (int i = 0; i < kMaxN; i++) {
         if (threadIdx.x == (unsigned)i && i < N) {
             par[i] = args.sla[i];
+            if constexpr (SIG) {
+                // sigmoid outputs: the latency decision compares the
+                // pre-activation with logit thresholds (the canonical sigmoid
+                // is within 2^-49 relative of the exact one; outputs lie in [0, 1])
+                auto logit = [](double p) {
+                    return p <= 0.0 ? -INFINITY : (p >= 1.0 ? INFINITY : log(p / (1.0 - p)));
+                };
+                const double sd = (double)args.sla[i];
+                par[i] = (float)(sd >= 1.0 ? INFINITY : logit(sd * (1.0 - 0x1p-49)));
+                par[96 + i] = (float)(sd >= 1.0 ? INFINITY : logit(sd * (1.0 + 0x1p-48)));
+            }
             par[16 + i] = bc.mag_thr[i];
             par[32 + i] = args.omega[i];
             par_off[i] = fc.opt_off[i];
@@ -222,6 +235,7 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
             const float k0l = cst[2], k0t = cst[3], cbl = cst[4], cbt = cst[5], rml = cst[6], rmt = cst[7];
             const float m3l = cst[8], m3t = cst[9];
             const float sla_i = par[i], om_i = par[32 + i];
+            const float sla_hi_i = SIG ? par[96 + i] : 0.f;
             const float tau_i = OBJ ? par[64 + i] : 0.f;
             const int prev_i = OBJ ? par_prev[i] : -1;
             const uint32_t row0 = (uint32_t)par_off[i];
@@ -351,13 +365,17 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
                 ytf += __shfl_xor(ytf, 32);
                 s2 += __shfl_xor(s2, 32);
                 sh += __shfl_xor(sh, 32);
-                const float lat = ylf + b30, thr = ytf + b31;
+                const float lat = ylf + b30;
+                const float thr = SIG ? sigmoid_f32(ytf + b31) : ytf + b31;
                 // per-configuration bounds on |fast - canonical|, inflated
-                // for their own fp32 evaluation (sh and s2 are rounded sums)
+                // for their own fp32 evaluation (sh and s2 are rounded sums);
+                // through the sigmoid (1/4-Lipschitz, fp32 evaluation within
+                // 2^-20) for the throughput
                 const float el = (k0l + bc.g2 * (cbl + rml * sh * 1.001f) + bc.g3 * m3l * s2) * 1.001f + 1e-30f;
-                const float et = (k0t + bc.g2 * (cbt + rmt * sh * 1.001f) + bc.g3 * m3t * s2) * 1.001f + 1e-30f;
-                const float slack = el + (fabsf(lat) + fabsf(sla_i)) * 0x1p-20f;
-                bool pass = lat + slack <= sla_i, fail = lat - slack > sla_i;
+                float et = (k0t + bc.g2 * (cbt + rmt * sh * 1.001f) + bc.g3 * m3t * s2) * 1.001f + 1e-30f;
+                if constexpr (SIG) et = et * 0.25f + 0x1p-20f;
+                const float slack = SIG ? el + fabsf(lat) * 0x1p-20f + 1e-12f : el + (fabsf(lat) + fabsf(sla_i)) * 0x1p-20f;
+                bool pass = lat + slack <= sla_i, fail = lat - slack > (SIG ? sla_hi_i : sla_i);
                 float jn, en;
                 if constexpr (eq3) {
                     const Eq3Term q3 = eq3_term(args.obj.vrow[2 * row], args.obj.vrow[2 * row + 1], thr, et, om_i,
@@ -380,7 +398,7 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
                 Et[TW - 1] = en;
                 Ft[TW - 1] = fl;
                 if (args.pred && valid && half == 0) {
-                    args.pred[(off * (uint64_t)N + (uint64_t)i) * 2u + 0u] = lat;
+                    args.pred[(off * (uint64_t)N + (uint64_t)i) * 2u + 0u] = SIG ? sigmoid_f32(lat) : lat;
                     args.pred[(off * (uint64_t)N + (uint64_t)i) * 2u + 1u] = thr;
                 }
             }
@@ -443,12 +461,12 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
     }
 }
 
-template <int MAXN, int A, int H, bool FULL, bool LIST, bool OBJ>
+template <int MAXN, int A, int H, bool FULL, bool LIST, bool OBJ, bool SIG = false>
 hipError_t launch_bf16_t(const Bf16Args &a, const FastConst &fc, const Bf16Const &bc, int grid, int kp, int mode,
                          hipStream_t s)
 {
     const size_t lds = bf16_lds_bytes(a.lay, kp);
-    auto fn = fast_bf16_kernel<MAXN, A, H, FULL, LIST, OBJ>;
+    auto fn = fast_bf16_kernel<MAXN, A, H, FULL, LIST, OBJ, SIG>;
     hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(grid), dim3(kBf16Waves * 64), lds, s, a, fc, bc, mode, kp);
@@ -467,6 +485,11 @@ hipError_t launch_bf16_for_width(const Bf16Args &a, const FastConst &fc, const B
     for (int j = 0; j < N; j++) multi = multi && fc.K[j] > 1;
     const bool obj = a.obj.kind != 0;
 #define MF_BF_CASE(AA)                                                                                          \
+    if (A == AA && bc.act) {   /* sigmoid outputs: the generic kernel */                                        \
+        if (mode == kModeList) return launch_bf16_t<16, AA, H, false, true, false, true>(a, fc, bc, grid, kp, mode, s); \
+        if (obj) return launch_bf16_t<16, AA, H, false, false, true, true>(a, fc, bc, grid, kp, mode, s);       \
+        return launch_bf16_t<16, AA, H, false, false, false, true>(a, fc, bc, grid, kp, mode, s);               \
+    }                                                                                                           \
     if (A == AA) {                                                                                              \
         if (mode == kModeList) return launch_bf16_t<16, AA, H, false, true, false>(a, fc, bc, grid, kp, mode, s); \
         if (obj) {                                                                                              \

@@ -23,14 +23,47 @@ __device__ __forceinline__ double bf16_round_d(double x)
     return rint(x * scale) / scale;
 }
 
+// e^x for |x| <= 700, defined by its algorithm so that it is the same
+// function wherever it runs: x = k ln 2 + r with k = rint(x / ln 2) and r
+// from two fmas (ln 2 split into a 24-bit head and a tail: k ln2_hi is
+// exact), e^r by its Taylor series to degree 13 (Horner with fma, |r| <=
+// ln 2 / 2: truncation below 4e-18), then times 2^k (exact in this range).
+__device__ __forceinline__ double canon_exp(double x)
+{
+    constexpr double kInvLn2 = 1.4426950408889634;        // 1 / ln 2
+    constexpr double kLn2Hi = 0.693147182464599609375;    // ln 2 rounded to 24 significant bits
+    constexpr double kLn2Lo = -1.904654299957768e-09;     // ln 2 - kLn2Hi
+    const double k = rint(x * kInvLn2);
+    double r = fma(-k, kLn2Hi, x);
+    r = fma(-k, kLn2Lo, r);
+    double inv_fact[14];
+    double fact = 1.0;
+#pragma unroll
+    for (int n = 0; n < 14; n++) {
+        if (n > 0) fact *= (double)n;
+        inv_fact[n] = 1.0 / fact;
+    }
+    double p = inv_fact[13];
+#pragma unroll
+    for (int n = 12; n >= 0; n--) p = fma(p, r, inv_fact[n]);
+    return ldexp(p, (int)k);
+}
+
+// The surrogate's sigmoid output: 1 / (1 + e^-y), y clamped to [-700, 700].
+__device__ __forceinline__ double canon_sigmoid(double y)
+{
+    const double c = y < -700.0 ? -700.0 : (y > 700.0 ? 700.0 : y);
+    return 1.0 / (1.0 + canon_exp(-c));
+}
+
 // One model's surrogate (Eq. 6) on the inputs zs [nin] (shared memory), by one
 // 64-thread workgroup: lanes take hidden units; h1s, h2s are shared scratch.
 // w: the model's canonical image W1^T[nin][H1], b1, W2^T[H1][H2], b2,
-// W3[2][H2], b3.  Every lane returns (lat, thr).  Contains barriers: call
-// from all lanes.
+// W3[2][H2], b3; sigmoid: both outputs pass canon_sigmoid.  Every lane returns
+// (lat, thr).  Contains barriers: call from all lanes.
 template <bool BF16>
 __device__ inline void canon_model(const float *w, int nin, int H1, int H2, const double *zs, double *h1s,
-                                   double *h2s, int lane, double &lat, double &thr)
+                                   double *h2s, int lane, double &lat, double &thr, int sigmoid)
 {
     const float *W1T = w, *b1 = W1T + (int64_t)nin * H1, *W2T = b1 + H1, *b2 = W2T + (int64_t)H1 * H2,
                 *W3 = b2 + H2, *b3 = W3 + 2 * H2;
@@ -57,7 +90,7 @@ __device__ inline void canon_model(const float *w, int nin, int H1, int H2, cons
     if (lane < 2) {
         double c = (double)b3[lane];
         for (int v = 0; v < H2; v++) c = fma((double)W3[lane * H2 + v], h2s[v], c);
-        y = c;
+        y = sigmoid ? canon_sigmoid(c) : c;
     }
     lat = __shfl(y, 0);
     thr = __shfl(y, 1);

@@ -111,7 +111,7 @@ canon_kernel(const CanonArgs a, const int search_mode)
             for (int k = lane; k < nin; k += 64) zs[k] = k < L ? (double)x[k] : (double)aggs[k - L];
             __syncthreads();
             double lat, thr;
-            canon_model<BF16>(a.weights + (int64_t)i * a.wstride, nin, H1, H2, zs, h1s, h2s, lane, lat, thr);
+            canon_model<BF16>(a.weights + (int64_t)i * a.wstride, nin, H1, H2, zs, h1s, h2s, lane, lat, thr, a.act);
             if (!(lat <= (double)a.sla[i])) { sla_ok = false; fl |= 1u << (8 + i); }
             if (eq3) {
                 // Eq. 3 (Section II): per-variant min-max throughput, quality,

@@ -68,6 +68,13 @@ __device__ __forceinline__ Eq3Term eq3_term(const float4 r0, const float4 r1, fl
     return t;
 }
 
+// Fast-path sigmoid in fp32.  Against the exact sigmoid of the same input its
+// error stays below 2^-21: the exponential's relative error e (from rounding
+// the scaled argument, |y| 2^-24, and the instruction's own) moves the
+// result by s (1 - s) e <= max(|y| e^-|y|) 2^-24 + 2^-23, and the add and
+// divide round twice more.  The bound used for it is 2^-20.
+__device__ __forceinline__ float sigmoid_f32(float y) { return 1.0f / (1.0f + __expf(-y)); }
+
 // relu of a finite fp32 value as one integer max: negative values (and -0)
 // have a negative bit pattern and map to +0, the rest are unchanged
 __device__ __forceinline__ float relu_f32(float x) { return __int_as_float(max(__float_as_int(x), 0)); }

@@ -43,7 +43,7 @@ __global__ void __launch_bounds__(64) fixed_table_kernel(const FixedArgs a)
         for (int k = lane; k < nin; k += 64) zs[k] = k < a.L ? (double)x[k] : (double)a.state[k - a.L];
         __syncthreads();
         double lat, thr;
-        canon_model<BF16>(a.weights + (int64_t)i * a.wstride, nin, a.H1, a.H2, zs, h1s, h2s, lane, lat, thr);
+        canon_model<BF16>(a.weights + (int64_t)i * a.wstride, nin, a.H1, a.H2, zs, h1s, h2s, lane, lat, thr, a.act);
         if (lane == 0) {
             FixedRow row;
             FixedPen pp = {0.0, 0.0};

@@ -211,6 +211,10 @@ __global__ void __launch_bounds__(256) ga_fitness_kernel(const GAConst c, int S,
             y0 = fma(W3[v], a, y0);
             y1 = fma(W3[H2 + v], a, y1);
         }
+        if (c.act) {   // the predictor's sigmoid output
+            y0 = canon_sigmoid(y0);
+            y1 = canon_sigmoid(y1);
+        }
         if (!(y0 <= (double)sla[(int64_t)s * N + i])) sla_ok = false;
         const double om = (double)omega[(int64_t)s * N + i];
         if (c.obj.kind != 0) {
@@ -234,36 +238,40 @@ __device__ __forceinline__ bool ga_better(double fa, uint64_t ia, double fb, uin
     return fa > fb || (fa == fb && ia < ib);
 }
 
-constexpr int kOpThreads = 1024;
+constexpr int kOpPairs = 256;     // parent pairs (threads) per operator workgroup
 constexpr int kGaMaxPop = 4096;
 
-// One workgroup per scenario: best-ever update, then (g < gens) the next
-// population; at g == gens the final population is copied out.
-__global__ void __launch_bounds__(kOpThreads) ga_ops_kernel(const GAConst c, uint64_t seed, int P, int gen, int gens,
-                                                            int tk, float p_cx, float p_swap, float p_mut,
-                                                            const uint32_t *fl, const unsigned long long *n_fl_ptr,
-                                                            const uint64_t *pop, const double *fit, uint64_t *next,
-                                                            double *best_J, uint64_t *best_idx, uint64_t *final_pop)
+// Operators: a scenario's pairs are spread over ceil((P/2) / kOpPairs)
+// workgroups, each holding the scenario's population and fitness in LDS and
+// computing the elite itself; the first of them updates the best ever.  At
+// g == gens the final population is copied out.  Every Philox block is
+// computed once and its four words used in order.
+__global__ void __launch_bounds__(kOpPairs) ga_ops_kernel(const GAConst c, uint64_t seed, int P, int gen, int gens,
+                                                          int tk, float p_cx, float p_swap, float p_mut,
+                                                          const uint32_t *fl, const unsigned long long *n_fl_ptr,
+                                                          const uint64_t *pop, const double *fit, uint64_t *next,
+                                                          double *best_J, uint64_t *best_idx, uint64_t *final_pop,
+                                                          int wgs_per_scen)
 {
     __shared__ double sf[kGaMaxPop];
     __shared__ uint64_t si[kGaMaxPop];
-    __shared__ int red[kOpThreads];
-    const int s = blockIdx.x, tid = threadIdx.x;
+    __shared__ int red[kOpPairs];
+    const int s = blockIdx.x / wgs_per_scen, pb = blockIdx.x % wgs_per_scen, tid = threadIdx.x;
     const int N = c.N;
     const uint64_t *ps = pop + (int64_t)s * P;
     const double *fs = fit + (int64_t)s * P;
-    for (int j = tid; j < P; j += kOpThreads) {
+    for (int j = tid; j < P; j += kOpPairs) {
         sf[j] = fs[j];
         si[j] = ps[j];
     }
     __syncthreads();
     // elite: best (f desc, index asc, slot asc)
     int b = -1;
-    for (int j = tid; j < P; j += kOpThreads)
+    for (int j = tid; j < P; j += kOpPairs)
         if (b < 0 || ga_better(sf[j], si[j], sf[b], si[b])) b = j;
     red[tid] = b;
     __syncthreads();
-    for (int o = kOpThreads / 2; o > 0; o >>= 1) {
+    for (int o = kOpPairs / 2; o > 0; o >>= 1) {
         if (tid < o) {
             const int x = red[tid], y = red[tid + o];
             if (y >= 0 && (x < 0 || ga_better(sf[y], si[y], sf[x], si[x]) ||
@@ -273,7 +281,7 @@ __global__ void __launch_bounds__(kOpThreads) ga_ops_kernel(const GAConst c, uin
         __syncthreads();
     }
     const int e = red[0];
-    if (tid == 0) {
+    if (pb == 0 && tid == 0) {
         if (sf[e] > -INFINITY && ga_better(sf[e], si[e], best_J[s], best_idx[s])) {
             best_J[s] = sf[e];
             best_idx[s] = si[e];
@@ -281,57 +289,76 @@ __global__ void __launch_bounds__(kOpThreads) ga_ops_kernel(const GAConst c, uin
     }
     if (gen == gens) {
         if (final_pop)
-            for (int j = tid; j < P; j += kOpThreads) final_pop[(int64_t)s * P + j] = si[j];
+            for (int j = pb * kOpPairs + tid; j < P; j += wgs_per_scen * kOpPairs) final_pop[(int64_t)s * P + j] = si[j];
         return;
     }
     uint64_t *ns = next + (int64_t)s * P;
-    if (tid == 0) ns[0] = si[e];
+    if (pb == 0 && tid == 0) ns[0] = si[e];
     const uint64_t g1 = (uint64_t)gen + 1, sc = (uint64_t)s, n_fl = *n_fl_ptr;
-    for (int q = tid; q < P / 2; q += kOpThreads) {
-        int par[2];
-        for (int t = 0; t < 2; t++) {
-            int best = -1;
-            for (int m = t * tk; m < (t + 1) * tk; m++) {
-                const int dj = (int)ga_below(ga_draw(seed, (uint64_t)q, g1, sc, kPSel + m / 4, m % 4), (uint64_t)P);
-                if (best < 0 || ga_better(sf[dj], si[dj], sf[best], si[best])) best = dj;
+    const int q = pb * kOpPairs + tid;
+    if (q >= P / 2) return;
+    // tournaments: draws 0..tk-1 choose parent A, tk..2tk-1 parent B
+    int pa = -1, pbest = -1;
+    const int nsel = 2 * tk;
+    for (int bl = 0; 4 * bl < nsel; bl++) {
+        const Philox4 r = philox4x64_10((uint64_t)q, g1, sc, kPSel + bl, seed, 0);
+#pragma unroll
+        for (int w = 0; w < 4; w++) {
+            const int m = 4 * bl + w;
+            if (m < nsel) {
+                const int dj = (int)ga_below(r.w[w], (uint64_t)P);
+                if (m < tk) {
+                    if (pa < 0 || ga_better(sf[dj], si[dj], sf[pa], si[pa])) pa = dj;
+                } else {
+                    if (pbest < 0 || ga_better(sf[dj], si[dj], sf[pbest], si[pbest])) pbest = dj;
+                }
             }
-            par[t] = best;
         }
-        int32_t ch[2][kMaxN];
-        for (int t = 0; t < 2; t++) {
-            uint64_t x = si[par[t]];
-            for (int i = N - 1; i >= 0; i--) {
-                ch[t][i] = (int32_t)(x % (uint64_t)c.K[i]);
-                x /= (uint64_t)c.K[i];
-            }
+    }
+    int32_t ch[2][kMaxN];
+    {
+        uint64_t x0 = si[pa], x1 = si[pbest];
+        for (int i = N - 1; i >= 0; i--) {
+            ch[0][i] = (int32_t)(x0 % (uint64_t)c.K[i]);
+            x0 /= (uint64_t)c.K[i];
+            ch[1][i] = (int32_t)(x1 % (uint64_t)c.K[i]);
+            x1 /= (uint64_t)c.K[i];
         }
-        if (ga_uni(ga_draw(seed, (uint64_t)q, g1, sc, kPCx, 0)) < (double)p_cx) {
-            for (int i = 0; i < N; i++) {
-                if (ga_uni(ga_draw(seed, (uint64_t)q, g1, sc, kPSwap + i / 4, i % 4)) < (double)p_swap) {
+    }
+    if (ga_uni(ga_draw(seed, (uint64_t)q, g1, sc, kPCx, 0)) < (double)p_cx) {
+        for (int bl = 0; 4 * bl < N; bl++) {
+            const Philox4 r = philox4x64_10((uint64_t)q, g1, sc, kPSwap + bl, seed, 0);
+#pragma unroll
+            for (int w = 0; w < 4; w++) {
+                const int i = 4 * bl + w;
+                if (i < N && ga_uni(r.w[w]) < (double)p_swap) {
                     const int32_t tmp = ch[0][i];
                     ch[0][i] = ch[1][i];
                     ch[1][i] = tmp;
                 }
             }
         }
-        for (int t = 0; t < 2; t++) {
-            const int j = 1 + 2 * q + t;
-            if (j >= P) break;
-            for (int i = 0; i < N; i++) {
-                const Philox4 r = philox4x64_10((uint64_t)j, g1, sc, kPMut + (2 * i) / 4, seed, 0);
-                const uint64_t u = r.w[(2 * i) % 4], v = r.w[(2 * i + 1) % 4];
-                if (ga_uni(u) < (double)p_mut) ch[t][i] = (int32_t)ga_below(v, (uint64_t)c.K[i]);
-            }
-            float vs = 0.f;
-            uint64_t idx = 0;
-            for (int i = 0; i < N; i++) {
-                vs = vs + c.features[(int64_t)(c.opt_off[i] + ch[t][i]) * c.L + c.vram_col];
-                idx = idx * (uint64_t)c.K[i] + (uint64_t)ch[t][i];
-            }
-            if (!((double)vs <= (double)c.vram_cap))
-                idx = fl[ga_below(ga_draw(seed, (uint64_t)j, g1, sc, kPRep, 0), n_fl)];
-            ns[j] = idx;
+    }
+    for (int t = 0; t < 2; t++) {
+        const int j = 1 + 2 * q + t;
+        if (j >= P) break;
+        // mutation: gene i reads words 2i and 2i+1 of consecutive blocks,
+        // so block bl holds genes 2 bl (words 0, 1) and 2 bl + 1 (words 2, 3)
+        for (int bl = 0; 2 * bl < N; bl++) {
+            const Philox4 r = philox4x64_10((uint64_t)j, g1, sc, kPMut + bl, seed, 0);
+            const int i0 = 2 * bl, i1 = 2 * bl + 1;
+            if (ga_uni(r.w[0]) < (double)p_mut) ch[t][i0] = (int32_t)ga_below(r.w[1], (uint64_t)c.K[i0]);
+            if (i1 < N && ga_uni(r.w[2]) < (double)p_mut) ch[t][i1] = (int32_t)ga_below(r.w[3], (uint64_t)c.K[i1]);
         }
+        float vs = 0.f;
+        uint64_t idx = 0;
+        for (int i = 0; i < N; i++) {
+            vs = vs + c.features[(int64_t)(c.opt_off[i] + ch[t][i]) * c.L + c.vram_col];
+            idx = idx * (uint64_t)c.K[i] + (uint64_t)ch[t][i];
+        }
+        if (!((double)vs <= (double)c.vram_cap))
+            idx = fl[ga_below(ga_draw(seed, (uint64_t)j, g1, sc, kPRep, 0), n_fl)];
+        ns[j] = idx;
     }
 }
 
@@ -392,8 +419,9 @@ hipError_t launch_ga_ops(const GAConst &c, uint64_t seed, int S, int P, int gen,
                          const uint64_t *pop, const double *fit, uint64_t *next, double *best_J, uint64_t *best_idx,
                          uint64_t *final_pop, hipStream_t st)
 {
-    hipLaunchKernelGGL(ga_ops_kernel, dim3(S), dim3(kOpThreads), 0, st, c, seed, P, gen, gens, tk, p_cx, p_swap, p_mut,
-                       fl, n_fl, pop, fit, next, best_J, best_idx, final_pop);
+    const int wgs = (P / 2 + kOpPairs - 1) / kOpPairs > 0 ? (P / 2 + kOpPairs - 1) / kOpPairs : 1;
+    hipLaunchKernelGGL(ga_ops_kernel, dim3(S * wgs), dim3(kOpPairs), 0, st, c, seed, P, gen, gens, tk, p_cx, p_swap,
+                       p_mut, fl, n_fl, pop, fit, next, best_J, best_idx, final_pop, wgs);
     return hipGetLastError();
 }
 

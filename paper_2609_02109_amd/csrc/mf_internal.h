@@ -48,6 +48,8 @@ struct FastLayout {
 // Per-problem constants of the fast kernels (kernel-argument block).
 struct FastConst {
     int32_t n_models;
+    int32_t act;                // output activation: 0 identity, 1 sigmoid (bounds below are then
+                                // pre-activation for the latency, post-activation for the throughput)
     int32_t K[kMaxN];
     int32_t opt_off[kMaxN];     // first global option row of model i
     uint32_t magic[kMaxN];      // floor(2^32 / K) + 1 (K > 1), 0 for K == 1
@@ -170,6 +172,7 @@ constexpr Bf16Layout bf16_layout(int H, int A, int sumK)
 
 struct Bf16Const {
     float g2, g3, gN;          // gamma_{2 KS}, gamma_{H/8+4}, gamma_N at fp32 unit roundoff
+    int32_t act;               // output activation: 0 identity, 1 sigmoid
     float mag_thr[kMaxN];      // a-priori bound on |thr| of model i
 };
 
@@ -196,7 +199,7 @@ struct Bf16Args {
 
 // Canonical (fp64) evaluation of entries.
 struct CanonArgs {
-    int n_models, L, A, H1, H2, bf16;
+    int n_models, L, A, H1, H2, bf16, act;
     int32_t K[kMaxN];
     int32_t opt_off[kMaxN];
     const int32_t *agg_cols;    // device [A] (original order)
@@ -261,7 +264,7 @@ struct FixedPen {
 // wave takes blocks_per_wave consecutive blocks, computes the outer prefix of
 // the canonical chain once per block and the inner models per lane.
 struct FixedArgs {
-    int n_models, L, A, H1, H2, bf16, sumK;
+    int n_models, L, A, H1, H2, bf16, sumK, act;
     int32_t K[kMaxN];
     int32_t opt_off[kMaxN];
     uint32_t magic[kMaxN];
@@ -315,7 +318,7 @@ struct StaticArgs {
 
 // GA problem constants (kernel-argument block).
 struct GAConst {
-    int N, L, A, H1, H2, bf16;
+    int N, L, A, H1, H2, bf16, act;
     int32_t K[kMaxN];
     int32_t opt_off[kMaxN];
     int vram_col;               // option column of the VRAM aggregate slot
@@ -336,7 +339,7 @@ hipError_t launch_precompute_p(const float *features, const float *weights, cons
                                int n_rows, int L, int A, int H, int64_t wstride,
                                const int32_t *row_model, float *image_p, int pst, hipStream_t s);
 hipError_t launch_fast_impl(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode, hipStream_t s);
-int fast_waves_for(int n_models, const FastLayout &lay, int kp);
+int fast_waves_for(int n_models, const FastLayout &lay, int kp, int act);
 int fast_kernel_supported(int n_models, int A, int H, int kp);
 int bf16_kernel_supported(int n_models, int A, int H);
 size_t bf16_lds_bytes(const Bf16Layout &lay, int kp);

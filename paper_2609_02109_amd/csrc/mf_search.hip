@@ -28,8 +28,10 @@ namespace mfi {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-// OBJ: score with the full utility of Eq. 3 (otherwise the linear objective)
-template <int MAXN, int A, int H, int WAVES, bool OBJ>
+// OBJ: score with the full utility of Eq. 3 (otherwise the linear objective).
+// SIG: the surrogates' outputs pass a sigmoid; the latency decision then
+// compares the pre-activation with logit thresholds.
+template <int MAXN, int A, int H, int WAVES, bool OBJ, bool SIG = false>
 __global__ void __launch_bounds__(WAVES * 64, 1)
 fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int kp)
 {
@@ -53,10 +55,23 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
         // compile-time index into the argument block (keeps it out of scratch)
         if (threadIdx.x == (unsigned)i && i < N) {
             const double s = (double)args.sla[i], b = fc.bound_lat[i];
-            const double slack = (fabs(s) + b) * 0x1p-22 + 1e-30;
-            const bool inf = isinf(s);
-            par[i] = inf ? (float)s : (float)(s - b - slack);       // lat <= this  => canonical lat <= sla
-            par[16 + i] = inf ? (float)s : (float)(s + b + slack);  // lat >  this  => canonical lat >  sla
+            if constexpr (SIG) {
+                // canonical sigmoid within 2^-49 relative of the exact one:
+                // pre-activation <= logit(s (1 - 2^-49)) gives a sure pass,
+                // > logit(s (1 + 2^-48)) a sure miss (outputs lie in [0, 1])
+                auto logit = [](double p) {
+                    return p <= 0.0 ? -INFINITY : (p >= 1.0 ? INFINITY : log(p / (1.0 - p)));
+                };
+                const double lo = s >= 1.0 ? INFINITY : logit(s * (1.0 - 0x1p-49));
+                const double hi = s >= 1.0 ? INFINITY : logit(s * (1.0 + 0x1p-48));
+                par[i] = isinf(lo) ? (float)lo : (float)(lo - b - ((fabs(lo) + b) * 0x1p-22 + 1e-12));
+                par[16 + i] = isinf(hi) ? (float)hi : (float)(hi + b + ((fabs(hi) + b) * 0x1p-22 + 1e-12));
+            } else {
+                const double slack = (fabs(s) + b) * 0x1p-22 + 1e-30;
+                const bool inf = isinf(s);
+                par[i] = inf ? (float)s : (float)(s - b - slack);       // lat <= this  => canonical lat <= sla
+                par[16 + i] = inf ? (float)s : (float)(s + b + slack);  // lat >  this  => canonical lat >  sla
+            }
             par[32 + i] = args.omega[i];
             par_off[i] = fc.opt_off[i];
             if constexpr (OBJ) {
@@ -233,7 +248,8 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             pl += __shfl_xor(pl, 32);
             pt += __shfl_xor(pt, 32);
             const float *b3 = smem + Ly.off_b3 + 4 * i;
-            const float lat = pl + b3[0], thr = pt + b3[1];
+            const float lat = pl + b3[0];
+            const float thr = SIG ? sigmoid_f32(pt + b3[1]) : pt + b3[1];
             bool pass = lat <= par[i], fail = lat > par[16 + i];
             if constexpr (eq3) {
                 const Eq3Term t = eq3_term(args.obj.vrow[2 * row], args.obj.vrow[2 * row + 1], thr, par[96 + i],
@@ -250,7 +266,7 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             anyfail |= fail;
             umask |= (pass || fail) ? 0u : (1u << i);
             if (args.pred && valid && half == 0) {
-                args.pred[(off * (uint64_t)N + (uint64_t)i) * 2u + 0u] = lat;
+                args.pred[(off * (uint64_t)N + (uint64_t)i) * 2u + 0u] = SIG ? sigmoid_f32(lat) : lat;
                 args.pred[(off * (uint64_t)N + (uint64_t)i) * 2u + 1u] = thr;
             }
         }
@@ -354,6 +370,9 @@ static hipError_t launch_fast_t(const FastArgs &a, const FastConst &fc, int grid
 {
     const size_t lds = (size_t)a.lay.total_floats * 4 + kFastPar * 4 + (size_t)WAVES * kp * 8;
     auto fn = a.obj.kind != 0 ? fast_kernel<MAXN, A, H, WAVES, true> : fast_kernel<MAXN, A, H, WAVES, false>;
+    if constexpr (MAXN == kMaxN && WAVES == kSearchWaves)   // the sigmoid output runs on the generic kernel
+        if (fc.act) fn = a.obj.kind != 0 ? fast_kernel<MAXN, A, H, WAVES, true, true>
+                                         : fast_kernel<MAXN, A, H, WAVES, false, true>;
     hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(grid), dim3(WAVES * 64), lds, s, a, fc, mode, kp);
@@ -371,16 +390,26 @@ int fast_kernel_supported(int n_models, int A, int H, int kp)
 
 // 16 waves per workgroup (4 per SIMD) when the per-wave registers fit 128
 // VGPRs (up to 8 models) and the image plus 16 candidate lists fit in LDS.
-int fast_waves_for(int n_models, const FastLayout &lay, int kp)
+int fast_waves_for(int n_models, const FastLayout &lay, int kp, int act)
 {
     const size_t lds = (size_t)lay.total_floats * 4 + kFastPar * 4 + (size_t)kSearchWavesWide * kp * 8;
-    return (n_models <= 8 && lds <= 163840) ? kSearchWavesWide : kSearchWaves;
+    return (n_models <= 8 && lds <= 163840 && !act) ? kSearchWavesWide : kSearchWaves;
 }
 
 hipError_t launch_fast_impl(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode, hipStream_t s)
 {
     const int N = fc.n_models, A = a.lay.A, H = a.lay.H;
     const bool wide = a.waves == kSearchWavesWide;
+    if (fc.act) {   // sigmoid outputs: the generic kernel (16 models, base waves)
+        if (wide) return hipErrorInvalidValue;
+#define MF_FAST_CASE(MN, AA, HH) \
+    if (A == AA && H == HH) return launch_fast_t<MN, AA, HH, kSearchWaves>(a, fc, grid, kp, mode, s);
+#define MF_FAST_A(MN, HH) MF_FAST_CASE(MN, 2, HH) MF_FAST_CASE(MN, 4, HH) MF_FAST_CASE(MN, 6, HH) MF_FAST_CASE(MN, 8, HH)
+        MF_FAST_A(16, 32) MF_FAST_A(16, 64)
+#undef MF_FAST_A
+#undef MF_FAST_CASE
+        return hipErrorInvalidValue;
+    }
 #define MF_FAST_CASE(MN, AA, HH)                                                                        \
     if (N <= MN && A == AA && H == HH) {                                                                \
         if (wide) return launch_fast_t<MN, AA, HH, kSearchWavesWide>(a, fc, grid, kp, mode, s);         \

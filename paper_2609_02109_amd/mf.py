@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(HERE, "libmf.so")
 
 MF_OK, MF_EINVAL, MF_ENOMEM, MF_EDEVICE, MF_EUNSUPPORTED, MF_EOVERFLOW, MF_EINTERNAL = range(7)
 MF_F32, MF_BF16 = 0, 1
+MF_ACT_IDENTITY, MF_ACT_SIGMOID = 0, 1
 MF_DUMP = 1
 MF_FIXED_STATE = 2
 MAX_AGG = 16
@@ -48,7 +49,7 @@ class Desc(C.Structure):
                 ("hidden1", C.c_int32), ("hidden2", C.c_int32),
                 ("h_n_options", C.c_void_p), ("h_agg_cols", C.c_void_p),
                 ("vram_slot", C.c_int32), ("vram_cap", C.c_float), ("dtype", C.c_int32),
-                ("variants", C.c_void_p)]
+                ("variants", C.c_void_p), ("output_act", C.c_int32)]
 
 
 class Objective(C.Structure):
@@ -187,7 +188,8 @@ class Problem:
                          int(inst.hidden2), _ptr(self._n_options), _ptr(self._agg_cols),
                          int(inst.vram_slot), float(inst.vram_cap),
                          MF_BF16 if inst.dtype == "bf16" else MF_F32,
-                         C.addressof(self._var) if self._var is not None else None)
+                         C.addressof(self._var) if self._var is not None else None,
+                         MF_ACT_SIGMOID if getattr(inst, "act", "identity") == "sigmoid" else MF_ACT_IDENTITY)
         h = C.c_void_p()
         _check(lib.mf_problem_create(C.byref(self.desc), _ptr(feats), _ptr(w), _stream(stream),
                                      C.byref(h)), "mf_problem_create")
