@@ -175,14 +175,15 @@ def bench_fixed(mf, torch, seed, steps, warmup):
 
 
 def bench_protocol(seeds=(0, 1, 2), n_scen=8, n_steps=12):
-    """The scheduling protocol of Table II (Section IV-C) on the N=5 instance:
-    8 synthetic dynamic scenarios x 12 steps x 3 seeds, full utility of Eq. 3
-    with the observed state held fixed per step."""
+    """The scheduling protocol of Table II (Section IV-C) on the N=5 option
+    sets with the paper's predictor (64-32, sigmoid outputs): 8 synthetic
+    dynamic scenarios x 12 steps x 3 seeds, full utility of Eq. 3 with the
+    observed state held fixed per step."""
     import numpy as np
     from paper_2609_02109_amd import protocol, synth
     runs, t0 = [], time.perf_counter()
     for seed in seeds:
-        inst = synth.cfg1(seed)
+        inst = synth.paper_predictor(seed)
         ob = synth.make_objective(inst, seed)
         sc = synth.make_scenarios(inst, n_scen, n_steps, seed=seed)
         dr = synth.protocol_draws(inst, n_scen, n_steps, seed=seed)
@@ -193,7 +194,8 @@ def bench_protocol(seeds=(0, 1, 2), n_scen=8, n_steps=12):
            for name in ("exhaustive", "ga", "random")}
     log(f"protocol: {wall:.1f} s; " + "; ".join(f"{k} J={v['mean_J']:.4f} gap={v['avg_gap']:.2f}% "
                                                  f"sla={v['sla_pct']:.2f}%" for k, v in table.items()))
-    return {"workload": f"Table II protocol: N=5 instance (12,12,9,9,9 options), {n_scen} dynamic scenarios x "
+    return {"workload": f"Table II protocol: N=5 instance (12,12,9,9,9 options, 12-64-32-2 predictor with "
+                        f"sigmoid outputs), {n_scen} dynamic scenarios x "
                         f"{n_steps} steps x {len(seeds)} seeds, Eq. 3 with floors, observed state per step; "
                         "GA population 100, 30 generations, mutation 0.1",
             "table": table, "median_decision_ms": lat, "wall_s": wall}

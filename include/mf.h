@@ -101,9 +101,16 @@ typedef struct {
     const float *h_reload_cost;    /* [N] */
 } mf_variants;
 
-/* Problem shape.  Supported: 1 <= n_models <= 16; 1 <= n_options[i] <= 255;
- * n_local >= 1; n_agg in {2,4,6,8}; hidden1 == hidden2 in {32, 64} for MF_F32,
- * in {64, 128, 256} for MF_BF16.  (Other shapes return MF_EUNSUPPORTED.) */
+/* Problem shape.  Creation accepts 1 <= n_models <= 16, 1 <= n_options[i] <=
+ * 255, n_local >= 1, 1 <= n_agg <= 16, n_local + n_agg <= 64, hidden sizes up
+ * to 256.  The derived-state search (mf_search without MF_FIXED_STATE) needs
+ * n_agg in {2,4,6,8} and hidden1 == hidden2 in {32, 64} for MF_F32, in
+ * {64, 128, 256} for MF_BF16; the GA needs (hidden1, hidden2) in {(32, 32),
+ * (64, 32), (64, 64)} with fixed input widths (mf_ga_run); the fixed-state
+ * and static searches take any created shape.  Other combinations return
+ * MF_EUNSUPPORTED from the call that needs them.  Trained predictors with
+ * batch normalisation fold it into the preceding layer's weights and bias
+ * before creation (an affine map at inference). */
 typedef struct {
     int32_t n_models;           /* N */
     int32_t n_local;            /* L: local features per option row */

@@ -380,6 +380,7 @@ static hipError_t launch_fit_t(const GAConst &c, int S, int P, const uint64_t *p
 int ga_fitness_supported(int nin, int h1, int h2)
 {
     return (h1 == 32 && h2 == 32 && (nin == 10 || nin == 12 || nin == 14 || nin == 16)) ||
+           (h1 == 64 && h2 == 32 && (nin == 10 || nin == 12 || nin == 14 || nin == 16)) ||
            (h1 == 64 && h2 == 64 && (nin == 12 || nin == 16 || nin == 22));
 }
 
@@ -390,6 +391,7 @@ hipError_t launch_ga_fitness(const GAConst &c, int S, int P, const uint64_t *pop
 #define MF_GA_FIT(NI, HA, HB) \
     if (nin == NI && c.H1 == HA && c.H2 == HB) return launch_fit_t<NI, HA, HB>(c, S, P, pop, sla, omega, fit, st);
     MF_GA_FIT(10, 32, 32) MF_GA_FIT(12, 32, 32) MF_GA_FIT(14, 32, 32) MF_GA_FIT(16, 32, 32)
+    MF_GA_FIT(10, 64, 32) MF_GA_FIT(12, 64, 32) MF_GA_FIT(14, 64, 32) MF_GA_FIT(16, 64, 32)
     MF_GA_FIT(12, 64, 64) MF_GA_FIT(16, 64, 64) MF_GA_FIT(22, 64, 64)
 #undef MF_GA_FIT
     return hipErrorInvalidValue;

@@ -256,6 +256,15 @@ def cfg2(seed=0) -> Instance:
                          top_k=1, name="n6_k24_h64")
 
 
+def paper_predictor(seed=0) -> Instance:
+    """The N=5 option sets with the paper's predictor architecture (Section
+    III-B): hidden layers 64 and 32, sigmoid outputs (batch norm folded,
+    dropout the identity at inference).  The latency bounds sit at 0.75; the
+    scheduling protocol replaces them per step."""
+    return make_instance([12, 12, 9, 9, 9], 8, 4, 64, 32, seed=seed, vram_quantile=0.75, sla_range=(0.75, 0.75),
+                         top_k=16, name="n5_paper_64_32_sigmoid", act="sigmoid")
+
+
 def cfg4(seed=0) -> Instance:
     """N=8, 16 options each (2**32 joint configs), L=32, A=8,
     40->256->256->2 with bf16 weights, VRAM cap 288 GB, top-64."""

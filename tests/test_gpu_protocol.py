@@ -53,3 +53,19 @@ def test_protocol_with_latency_bounds_and_derived_gaps(proto, orc):
         np.testing.assert_array_equal(g[name]["idx"], r[name]["idx"], err_msg=name)
         assert g[name]["J"].tobytes() == r[name]["J"].tobytes(), name
         np.testing.assert_array_equal(g[name]["ok"], r[name]["ok"], err_msg=name)
+
+
+def test_protocol_with_the_papers_predictor(proto, orc):
+    # 64-32 hidden layers and sigmoid outputs (the paper's predictor)
+    import oracle.protocol as op
+    inst = synth.paper_predictor(2)
+    ob = synth.make_objective(inst, 2)
+    sc = synth.make_scenarios(inst, 2, 4, seed=2)
+    dr = synth.protocol_draws(inst, 2, 4, seed=2)
+    P = proto.ProtocolParams(ga_pop=32, ga_gens=8)
+    g = proto.Protocol(inst, ob, P).run(sc, dr)
+    r = op.run(inst, ob, sc, dr, P, proto.scheduler_names(P))
+    for name in proto.scheduler_names(P):
+        np.testing.assert_array_equal(g[name]["idx"], r[name]["idx"], err_msg=name)
+        assert g[name]["J"].tobytes() == r[name]["J"].tobytes(), name
+        np.testing.assert_array_equal(g[name]["ok"], r[name]["ok"], err_msg=name)
