@@ -1440,7 +1440,6 @@ static mf_status check_ga_args(const mf_problem *p, const mf_ga_args *a)
     mf_status st = check_objective(p, a->objective);
     if (st != MF_OK) return st;
     if (p->space > (1ull << 32)) return MF_EUNSUPPORTED;
-    if (!ga_fitness_supported(p->L + p->A, p->H1, p->H2)) return MF_EUNSUPPORTED;
     return MF_OK;
 }
 
@@ -1506,6 +1505,7 @@ mf_status mf_ga_run(mf_problem *p, const mf_ga_args *args, void *d_ws, size_t ws
     c.features = p->d_features;
     c.agg_cols = p->d_agg_cols;
     c.w64 = p->d_w64;
+    c.canon = p->d_canon;
     c.wstride = p->wstride;
     c.fixed = (args->flags & MF_FIXED_STATE) ? 1 : 0;
     for (int k = 0; k < p->A; k++) c.state[k] = c.fixed ? args->state[k] : 0.f;

@@ -70,11 +70,13 @@ __device__ inline void canon_model(const float *w, int nin, int H1, int H2, cons
     for (int u = lane; u < H1; u += 64) {
         if (BF16) {
             float c = b1[u];
+            #pragma unroll 8
             for (int k = 0; k < nin; k++) c = fmaf(W1T[(int64_t)k * H1 + u], (float)zs[k], c);
             c = c > 0.f ? c : 0.f;
             h1s[u] = bf16_round_d((double)c);
         } else {
             double c = (double)b1[u];
+            #pragma unroll 8
             for (int k = 0; k < nin; k++) c = fma((double)W1T[(int64_t)k * H1 + u], zs[k], c);
             h1s[u] = c > 0.0 ? c : 0.0;
         }
@@ -82,6 +84,7 @@ __device__ inline void canon_model(const float *w, int nin, int H1, int H2, cons
     __syncthreads();
     for (int v = lane; v < H2; v += 64) {
         double c = (double)b2[v];
+        #pragma unroll 8
         for (int u = 0; u < H1; u++) c = fma((double)W2T[(int64_t)u * H2 + v], h1s[u], c);
         h2s[v] = c > 0.0 ? c : 0.0;
     }
@@ -89,6 +92,7 @@ __device__ inline void canon_model(const float *w, int nin, int H1, int H2, cons
     double y = 0.0;
     if (lane < 2) {
         double c = (double)b3[lane];
+        #pragma unroll 8
         for (int v = 0; v < H2; v++) c = fma((double)W3[lane * H2 + v], h2s[v], c);
         y = sigmoid ? canon_sigmoid(c) : c;
     }

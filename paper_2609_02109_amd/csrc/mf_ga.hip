@@ -1,11 +1,12 @@
 // Genetic-algorithm scheduler (Section IV-C) on the GPU.
 //
 // Per generation two launches: the fitness of every individual of every
-// scenario (one lane per individual, the canonical fp64 surrogate chain, so
-// every tournament compares exactly the values the results are defined by),
-// then one workgroup per scenario applies the operators: elitism (slot 0),
-// tournaments of k draws with replacement, uniform crossover, per-gene
-// mutation, repair of VRAM-infeasible children from the feasible list.
+// scenario (the canonical fp64 surrogate chain, so every tournament compares
+// exactly the values the results are defined by: one lane per individual for
+// large populations, one workgroup per individual for small ones), then the
+// operators, 64 parent pairs per workgroup: elitism (slot 0), tournaments of
+// k draws with replacement, uniform crossover, per-gene mutation, repair of
+// VRAM-infeasible children from the feasible list.
 //
 // Random draws: Philox4x64-10 (Salmon et al., SC'11), key (seed, 0), counter
 // (item, generation, scenario, purpose), one 64-bit word per draw;
@@ -233,133 +234,290 @@ __global__ void __launch_bounds__(256) ga_fitness_kernel(const GAConst c, int S,
     fit[t] = (vram_ok && sla_ok) ? J : -INFINITY;
 }
 
+// Canonical fp64 fitness, one 64-lane workgroup per individual (small
+// populations, or shapes the one-lane kernel is not built for): the
+// certification kernel's evaluation, lanes over hidden units, model after
+// model.  The same canonical J as the one-lane kernel, bit for bit.
+// One workgroup per individual (small populations, and shapes the one-lane
+// kernel does not take): wave w runs the canonical forward of models w,
+// w + W, ... (W waves), each on its own LDS scratch; lane 0 then combines the
+// models' predictions in model order, as in the one-lane kernel.  STAGE: the
+// canonical weights of every model are first copied to LDS.  Dynamic LDS:
+// [staged weights][W x (H1 + H2 + nin) doubles].
+template <bool BF16, bool STAGE>
+__global__ void __launch_bounds__(64 * kGaWideWaves) ga_fitness_wide_kernel(const GAConst c, int S, int P,
+                                                                             const uint64_t *pop, const float *sla,
+                                                                             const float *omega, double *fit,
+                                                                             int stage_floats)
+{
+    extern __shared__ float4 dyn4[];
+    __shared__ double aggs[kMaxN];
+    __shared__ double s_lat[kMaxN], s_thr[kMaxN];
+    __shared__ float s_tau[kMaxN];
+    __shared__ int32_t s_prev[kMaxN];
+    __shared__ int32_t d[kMaxN];
+    __shared__ int s_vram_ok;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int W = (int)(blockDim.x >> 6);
+    if (tid < kMaxN) {
+        s_tau[tid] = c.obj.tau[tid];
+        s_prev[tid] = c.obj.prev[tid];
+        aggs[tid] = (double)c.state[tid];
+    }
+    const int N = c.N, L = c.L, A = c.A, nin = L + A, H1 = c.H1, H2 = c.H2;
+    const float *wbase = c.canon;
+    if (STAGE) {
+        const int n4 = (stage_floats + 3) / 4;
+        const float4 *src = reinterpret_cast<const float4 *>(c.canon);
+        for (int q = tid; q < n4; q += blockDim.x) dyn4[q] = src[q];
+        wbase = reinterpret_cast<const float *>(dyn4);
+    }
+    double *scr = reinterpret_cast<double *>(dyn4 + (STAGE ? (stage_floats + 3) / 4 : 0)) +
+                  (int64_t)wave * (H1 + H2 + nin);
+    double *h1s = scr, *h2s = scr + H1, *zs = scr + H1 + H2;
+    const int rounds = (N + W - 1) / W;
+    for (int64_t t = blockIdx.x; t < (int64_t)S * P; t += gridDim.x) {
+        const int s = (int)(t / P);
+        __syncthreads();
+        if (tid == 0) {
+            uint64_t idx = pop[t];
+            for (int i = N - 1; i >= 0; i--) {
+                d[i] = (int32_t)(idx % (uint64_t)c.K[i]);
+                idx /= (uint64_t)c.K[i];
+            }
+        }
+        __syncthreads();
+        // aggregate slot k (fp32, model order); the VRAM slot decides the cap
+        if (tid < A) {
+            float a = 0.f;
+            for (int i = 0; i < N; i++) a = a + c.features[(int64_t)(c.opt_off[i] + d[i]) * L + c.agg_cols[tid]];
+            if (!c.fixed) aggs[tid] = (double)a;
+            if (tid == c.vram_slot) s_vram_ok = a <= c.vram_cap;
+        }
+        // every wave takes part in every round (the forward has barriers); a
+        // wave past the last model repeats it and drops the result
+        for (int r = 0; r < rounds; r++) {
+            const int i = r * W + wave, ii = i < N ? i : N - 1;
+            __syncthreads();
+            const float *x = c.features + (int64_t)(c.opt_off[ii] + d[ii]) * L;
+            for (int k = lane; k < nin; k += 64) zs[k] = k < L ? (double)x[k] : aggs[k - L];
+            __syncthreads();
+            double lat, thr;
+            canon_model<BF16>(wbase + (int64_t)ii * c.wstride, nin, H1, H2, zs, h1s, h2s, lane, lat, thr, c.act);
+            if (i < N && lane == 0) {
+                s_lat[i] = lat;
+                s_thr[i] = thr;
+            }
+        }
+        __syncthreads();
+        if (tid == 0) {
+            bool ok = s_vram_ok != 0;
+            double J = 0.0;
+            for (int i = 0; i < N; i++) {
+                const double lat = s_lat[i], thr = s_thr[i];
+                if (!(lat <= (double)sla[(int64_t)s * N + i])) ok = false;
+                const double om = (double)omega[(int64_t)s * N + i];
+                if (c.obj.kind != 0) {
+                    double q, Pr, pen;
+                    bool do_P, do_pen;
+                    if (!canon_eq3(c.obj, c.opt_off[i] + d[i], thr, s_tau[i], s_prev[i], q, Pr, do_P, pen, do_pen))
+                        ok = false;
+                    J = fma(om, q, J);
+                    if (do_P) J = J - Pr;
+                    if (do_pen) J = J - pen;
+                } else {
+                    J = fma(om, thr, J);
+                }
+            }
+            fit[t] = ok ? J : -INFINITY;
+        }
+    }
+}
+
 __device__ __forceinline__ bool ga_better(double fa, uint64_t ia, double fb, uint64_t ib)
 {
     return fa > fb || (fa == fb && ia < ib);
 }
 
-constexpr int kOpPairs = 256;     // parent pairs (threads) per operator workgroup
-constexpr int kGaMaxPop = 4096;
+constexpr int kOpThreads = 256;                   // threads per operator workgroup
+constexpr int kOpTeam = 4;                        // lanes per parent pair
+constexpr int kOpPairs = kOpThreads / kOpTeam;    // parent pairs per operator workgroup
+
+// The Philox blocks one parent pair consumes, in a fixed order: the selection
+// blocks (2k draws), the crossover block, the swap blocks (one word per
+// gene), the mutation blocks of child 1 + 2q and of child 2 + 2q (two words
+// per gene), the repair block of each child.
+struct OpBlocks {
+    int nsel, nswap, nmut, total;
+    __host__ __device__ OpBlocks(int tk, int N)
+        : nsel((2 * tk + 3) / 4), nswap((N + 3) / 4), nmut((N + 1) / 2), total(nsel + 1 + nswap + 2 * nmut + 2)
+    {
+    }
+    __host__ __device__ int cx() const { return nsel; }
+    __host__ __device__ int swap() const { return nsel + 1; }
+    __host__ __device__ int mut(int t) const { return nsel + 1 + nswap + t * nmut; }
+    __host__ __device__ int rep(int t) const { return nsel + 1 + nswap + 2 * nmut + t; }
+};
+
+// Dynamic LDS of the operator kernel: the pairs' Philox words, the parents'
+// genes.
+inline size_t ops_lds_bytes(int tk, int N)
+{
+    return (size_t)kOpPairs * OpBlocks(tk, N).total * 32 + (size_t)kOpPairs * 2 * N * 4;
+}
 
 // Operators: a scenario's pairs are spread over ceil((P/2) / kOpPairs)
-// workgroups, each holding the scenario's population and fitness in LDS and
-// computing the elite itself; the first of them updates the best ever.  At
-// g == gens the final population is copied out.  Every Philox block is
-// computed once and its four words used in order.
-__global__ void __launch_bounds__(kOpPairs) ga_ops_kernel(const GAConst c, uint64_t seed, int P, int gen, int gens,
-                                                          int tk, float p_cx, float p_swap, float p_mut,
-                                                          const uint32_t *fl, const unsigned long long *n_fl_ptr,
-                                                          const uint64_t *pop, const double *fit, uint64_t *next,
-                                                          double *best_J, uint64_t *best_idx, uint64_t *final_pop,
-                                                          int wgs_per_scen)
+// workgroups; tournaments read fitness and population from global memory.
+// The first workgroup of a scenario finds the elite (slot 0 of the next
+// generation) and updates the best ever.  At g == gens the final population
+// is copied out.  The pairs' Philox blocks are first computed by all threads
+// together (each block once, its four words used in order); then, in each
+// team of lanes, lane t runs tournament t and decodes parent t, and builds
+// child t (crossover, mutation, repair).
+__global__ void __launch_bounds__(kOpThreads) ga_ops_kernel(const GAConst c, uint64_t seed, int P, int gen, int gens,
+                                                            int tk, float p_cx, float p_swap, float p_mut,
+                                                            const uint32_t *fl, const unsigned long long *n_fl_ptr,
+                                                            const uint64_t *pop, const double *fit, uint64_t *next,
+                                                            double *best_J, uint64_t *best_idx, uint64_t *final_pop,
+                                                            int wgs_per_scen)
 {
-    __shared__ double sf[kGaMaxPop];
-    __shared__ uint64_t si[kGaMaxPop];
-    __shared__ int red[kOpPairs];
+    extern __shared__ uint64_t ops_dyn[];
+    __shared__ int red[kOpThreads];
+    __shared__ double red_f[kOpThreads];
+    __shared__ uint64_t red_i[kOpThreads];
     const int s = blockIdx.x / wgs_per_scen, pb = blockIdx.x % wgs_per_scen, tid = threadIdx.x;
     const int N = c.N;
+    const OpBlocks ob(tk, N);
+    uint64_t *words = ops_dyn;                                                                // [kOpPairs][total][4]
+    int32_t *genes = reinterpret_cast<int32_t *>(words + (int64_t)kOpPairs * ob.total * 4);   // [kOpPairs][2][N]
     const uint64_t *ps = pop + (int64_t)s * P;
     const double *fs = fit + (int64_t)s * P;
-    for (int j = tid; j < P; j += kOpPairs) {
-        sf[j] = fs[j];
-        si[j] = ps[j];
-    }
-    __syncthreads();
-    // elite: best (f desc, index asc, slot asc)
-    int b = -1;
-    for (int j = tid; j < P; j += kOpPairs)
-        if (b < 0 || ga_better(sf[j], si[j], sf[b], si[b])) b = j;
-    red[tid] = b;
-    __syncthreads();
-    for (int o = kOpPairs / 2; o > 0; o >>= 1) {
-        if (tid < o) {
-            const int x = red[tid], y = red[tid + o];
-            if (y >= 0 && (x < 0 || ga_better(sf[y], si[y], sf[x], si[x]) ||
-                           (sf[y] == sf[x] && si[y] == si[x] && y < x)))
-                red[tid] = y;
-        }
-        __syncthreads();
-    }
-    const int e = red[0];
-    if (pb == 0 && tid == 0) {
-        if (sf[e] > -INFINITY && ga_better(sf[e], si[e], best_J[s], best_idx[s])) {
-            best_J[s] = sf[e];
-            best_idx[s] = si[e];
-        }
-    }
+    uint64_t *ns = next + (int64_t)s * P;
     if (gen == gens) {
         if (final_pop)
-            for (int j = pb * kOpPairs + tid; j < P; j += wgs_per_scen * kOpPairs) final_pop[(int64_t)s * P + j] = si[j];
-        return;
+            for (int j = pb * kOpThreads + tid; j < P; j += wgs_per_scen * kOpThreads)
+                final_pop[(int64_t)s * P + j] = ps[j];
     }
-    uint64_t *ns = next + (int64_t)s * P;
-    if (pb == 0 && tid == 0) ns[0] = si[e];
-    const uint64_t g1 = (uint64_t)gen + 1, sc = (uint64_t)s, n_fl = *n_fl_ptr;
-    const int q = pb * kOpPairs + tid;
-    if (q >= P / 2) return;
-    // tournaments: draws 0..tk-1 choose parent A, tk..2tk-1 parent B
-    int pa = -1, pbest = -1;
-    const int nsel = 2 * tk;
-    for (int bl = 0; 4 * bl < nsel; bl++) {
-        const Philox4 r = philox4x64_10((uint64_t)q, g1, sc, kPSel + bl, seed, 0);
-#pragma unroll
-        for (int w = 0; w < 4; w++) {
-            const int m = 4 * bl + w;
-            if (m < nsel) {
-                const int dj = (int)ga_below(r.w[w], (uint64_t)P);
-                if (m < tk) {
-                    if (pa < 0 || ga_better(sf[dj], si[dj], sf[pa], si[pa])) pa = dj;
-                } else {
-                    if (pbest < 0 || ga_better(sf[dj], si[dj], sf[pbest], si[pbest])) pbest = dj;
-                }
+    if (pb == 0) {
+        // elite: best (f desc, index asc, slot asc), reduced in LDS
+        int b = -1;
+        double fb = 0.0;
+        uint64_t ib = 0;
+        for (int j = tid; j < P; j += kOpThreads) {
+            const double f = fs[j];
+            const uint64_t i = ps[j];
+            if (b < 0 || ga_better(f, i, fb, ib)) {
+                b = j;
+                fb = f;
+                ib = i;
             }
         }
+        red[tid] = b;
+        red_f[tid] = fb;
+        red_i[tid] = ib;
+        __syncthreads();
+        for (int o = kOpThreads / 2; o > 0; o >>= 1) {
+            if (tid < o) {
+                const int x = red[tid], y = red[tid + o];
+                const double fx = red_f[tid], fy = red_f[tid + o];
+                const uint64_t ix = red_i[tid], iy = red_i[tid + o];
+                if (y >= 0 && (x < 0 || ga_better(fy, iy, fx, ix) || (fy == fx && iy == ix && y < x))) {
+                    red[tid] = y;
+                    red_f[tid] = fy;
+                    red_i[tid] = iy;
+                }
+            }
+            __syncthreads();
+        }
+        if (tid == 0) {
+            const double fe = red_f[0];
+            const uint64_t ie = red_i[0];
+            if (fe > -INFINITY && ga_better(fe, ie, best_J[s], best_idx[s])) {
+                best_J[s] = fe;
+                best_idx[s] = ie;
+            }
+            if (gen != gens) ns[0] = ie;
+        }
     }
-    int32_t ch[2][kMaxN];
-    {
-        uint64_t x0 = si[pa], x1 = si[pbest];
+    if (gen == gens) return;
+    const uint64_t g1 = (uint64_t)gen + 1, sc = (uint64_t)s;
+    const int q0 = pb * kOpPairs;
+    const int np = P / 2 - q0 < kOpPairs ? P / 2 - q0 : kOpPairs;
+    // every Philox block of this workgroup's pairs
+    for (int jb = tid; jb < np * ob.total; jb += kOpThreads) {
+        const int ql = jb / ob.total, k = jb - ql * ob.total;
+        const uint64_t q = (uint64_t)(q0 + ql);
+        uint64_t item = q, purpose;
+        if (k < ob.cx()) {
+            purpose = kPSel + k;
+        } else if (k == ob.cx()) {
+            purpose = kPCx;
+        } else if (k < ob.mut(0)) {
+            purpose = kPSwap + (k - ob.swap());
+        } else if (k < ob.rep(0)) {
+            const int t = (k - ob.mut(0)) / ob.nmut;
+            item = 1 + 2 * q + t;
+            purpose = kPMut + (k - ob.mut(t));
+        } else {
+            item = 1 + 2 * q + (k - ob.rep(0));
+            purpose = kPRep;
+        }
+        const Philox4 r = philox4x64_10(item, g1, sc, purpose, seed, 0);
+        uint64_t *w = words + (int64_t)jb * 4;
+#pragma unroll
+        for (int x = 0; x < 4; x++) w[x] = r.w[x];
+    }
+    __syncthreads();
+    const int ql = tid / kOpTeam, t = tid % kOpTeam;
+    const bool act = ql < np && t < 2;
+    const uint64_t *pw = words + (int64_t)ql * ob.total * 4;
+    int32_t *pg = genes + (ql * 2) * N;
+    if (act) {
+        // tournament t: draws t k .. t k + k - 1 of the selection words
+        int par = -1;
+        double fpar = 0.0;
+        uint64_t ipar = 0;
+        for (int m = t * tk; m < t * tk + tk; m++) {
+            const int dj = (int)ga_below(pw[m], (uint64_t)P);
+            const double f = fs[dj];
+            const uint64_t i = ps[dj];
+            if (par < 0 || ga_better(f, i, fpar, ipar)) {
+                par = dj;
+                fpar = f;
+                ipar = i;
+            }
+        }
+        uint64_t x = ipar;
         for (int i = N - 1; i >= 0; i--) {
-            ch[0][i] = (int32_t)(x0 % (uint64_t)c.K[i]);
-            x0 /= (uint64_t)c.K[i];
-            ch[1][i] = (int32_t)(x1 % (uint64_t)c.K[i]);
-            x1 /= (uint64_t)c.K[i];
+            pg[t * N + i] = (int32_t)(x % (uint64_t)c.K[i]);
+            x /= (uint64_t)c.K[i];
         }
     }
-    if (ga_uni(ga_draw(seed, (uint64_t)q, g1, sc, kPCx, 0)) < (double)p_cx) {
-        for (int bl = 0; 4 * bl < N; bl++) {
-            const Philox4 r = philox4x64_10((uint64_t)q, g1, sc, kPSwap + bl, seed, 0);
-#pragma unroll
-            for (int w = 0; w < 4; w++) {
-                const int i = 4 * bl + w;
-                if (i < N && ga_uni(r.w[w]) < (double)p_swap) {
-                    const int32_t tmp = ch[0][i];
-                    ch[0][i] = ch[1][i];
-                    ch[1][i] = tmp;
-                }
-            }
-        }
+    __syncthreads();
+    if (!act) return;
+    const int j = 1 + 2 * (q0 + ql) + t;
+    if (j >= P) return;
+    // child t starts as parent t; uniform crossover gives it the other
+    // parent's gene wherever the pair's swap draw falls below p_swap
+    int32_t ch[kMaxN];
+    const bool cx = ga_uni(pw[ob.cx() * 4]) < (double)p_cx;
+    for (int i = 0; i < N; i++) {
+        const bool sw = cx && ga_uni(pw[ob.swap() * 4 + i]) < (double)p_swap;
+        ch[i] = pg[(sw ? 1 - t : t) * N + i];
     }
-    for (int t = 0; t < 2; t++) {
-        const int j = 1 + 2 * q + t;
-        if (j >= P) break;
-        // mutation: gene i reads words 2i and 2i+1 of consecutive blocks,
-        // so block bl holds genes 2 bl (words 0, 1) and 2 bl + 1 (words 2, 3)
-        for (int bl = 0; 2 * bl < N; bl++) {
-            const Philox4 r = philox4x64_10((uint64_t)j, g1, sc, kPMut + bl, seed, 0);
-            const int i0 = 2 * bl, i1 = 2 * bl + 1;
-            if (ga_uni(r.w[0]) < (double)p_mut) ch[t][i0] = (int32_t)ga_below(r.w[1], (uint64_t)c.K[i0]);
-            if (i1 < N && ga_uni(r.w[2]) < (double)p_mut) ch[t][i1] = (int32_t)ga_below(r.w[3], (uint64_t)c.K[i1]);
-        }
-        float vs = 0.f;
-        uint64_t idx = 0;
-        for (int i = 0; i < N; i++) {
-            vs = vs + c.features[(int64_t)(c.opt_off[i] + ch[t][i]) * c.L + c.vram_col];
-            idx = idx * (uint64_t)c.K[i] + (uint64_t)ch[t][i];
-        }
-        if (!((double)vs <= (double)c.vram_cap))
-            idx = fl[ga_below(ga_draw(seed, (uint64_t)j, g1, sc, kPRep, 0), n_fl)];
-        ns[j] = idx;
+    // mutation: gene i reads words 2i (mutate?) and 2i + 1 (new value)
+    const uint64_t *mw = pw + ob.mut(t) * 4;
+    for (int i = 0; i < N; i++)
+        if (ga_uni(mw[2 * i]) < (double)p_mut) ch[i] = (int32_t)ga_below(mw[2 * i + 1], (uint64_t)c.K[i]);
+    float vs = 0.f;
+    uint64_t idx = 0;
+    for (int i = 0; i < N; i++) {
+        vs = vs + c.features[(int64_t)(c.opt_off[i] + ch[i]) * c.L + c.vram_col];
+        idx = idx * (uint64_t)c.K[i] + (uint64_t)ch[i];
     }
+    if (!((double)vs <= (double)c.vram_cap)) idx = fl[ga_below(pw[ob.rep(t) * 4], *n_fl_ptr)];
+    ns[j] = idx;
 }
 
 // ---------------------------------------------------------------- launchers
@@ -388,6 +546,25 @@ hipError_t launch_ga_fitness(const GAConst &c, int S, int P, const uint64_t *pop
                              double *fit, hipStream_t st)
 {
     const int nin = c.L + c.A;
+    if ((int64_t)S * P <= kGaWideMax || !ga_fitness_supported(nin, c.H1, c.H2)) {
+        const int64_t n = (int64_t)S * P;
+        // every model's weights in LDS when they fit (the canonical image is
+        // 16-byte aligned per problem and padded to 256 bytes)
+        const int W = c.N < kGaWideWaves ? c.N : kGaWideWaves;
+        const int64_t wfloats = (int64_t)c.N * c.wstride;
+        const bool stage = ((wfloats + 3) / 4) * 16 <= (int64_t)kGaStageBytes;
+        const size_t lds = (stage ? (size_t)((wfloats + 3) / 4) * 16 : 0) + (size_t)W * (c.H1 + c.H2 + nin) * 8;
+        const int64_t cap = stage ? kGaWideStagedWgs : 65536;
+        const int grid = (int)(n < cap ? n : cap);
+        auto fn = c.bf16 ? (stage ? ga_fitness_wide_kernel<true, true> : ga_fitness_wide_kernel<true, false>)
+                         : (stage ? ga_fitness_wide_kernel<false, true> : ga_fitness_wide_kernel<false, false>);
+        const hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                 (int)lds);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(fn, dim3(grid), dim3(64 * W), lds, st, c, S, P, pop, sla, omega, fit,
+                           stage ? (int)wfloats : 0);
+        return hipGetLastError();
+    }
 #define MF_GA_FIT(NI, HA, HB) \
     if (nin == NI && c.H1 == HA && c.H2 == HB) return launch_fit_t<NI, HA, HB>(c, S, P, pop, sla, omega, fit, st);
     MF_GA_FIT(10, 32, 32) MF_GA_FIT(12, 32, 32) MF_GA_FIT(14, 32, 32) MF_GA_FIT(16, 32, 32)
@@ -422,8 +599,12 @@ hipError_t launch_ga_ops(const GAConst &c, uint64_t seed, int S, int P, int gen,
                          uint64_t *final_pop, hipStream_t st)
 {
     const int wgs = (P / 2 + kOpPairs - 1) / kOpPairs > 0 ? (P / 2 + kOpPairs - 1) / kOpPairs : 1;
-    hipLaunchKernelGGL(ga_ops_kernel, dim3(S * wgs), dim3(kOpPairs), 0, st, c, seed, P, gen, gens, tk, p_cx, p_swap,
-                       p_mut, fl, n_fl, pop, fit, next, best_J, best_idx, final_pop, wgs);
+    const size_t lds = ops_lds_bytes(tk, c.N);
+    const hipError_t e = hipFuncSetAttribute((const void *)ga_ops_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(ga_ops_kernel, dim3(S * wgs), dim3(kOpThreads), lds, st, c, seed, P, gen, gens, tk, p_cx,
+                       p_swap, p_mut, fl, n_fl, pop, fit, next, best_J, best_idx, final_pop, wgs);
     return hipGetLastError();
 }
 

@@ -328,6 +328,7 @@ struct GAConst {
     const float *features;      // [sumK][L]
     const int32_t *agg_cols;    // [A]
     const double *w64;          // [N][stride] packed weights (W1 b1 W2 b2 W3 b3) as fp64
+    const float *canon;         // [N][stride] canonical image (W1^T b1 W2^T b2 W3 b3)
     int64_t wstride;
     int fixed;                  // the surrogates see state[] instead of the candidate's aggregate
     float state[kMaxN];
@@ -367,6 +368,10 @@ hipError_t launch_static_eval(const StaticArgs &a, hipStream_t s);
 int static_wgs_per_cu(const StaticArgs &a);
 int fixed_wgs_per_cu(const FixedArgs &a);
 hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
+constexpr int64_t kGaWideMax = 8192;   // populations (S x P) up to this size take the wide fitness kernel
+constexpr int kGaWideWaves = 8;             // ... with up to this many waves (models) per workgroup
+constexpr size_t kGaStageBytes = 64 * 1024;   // ... copying the weights to LDS when they fit in this
+constexpr int64_t kGaWideStagedWgs = 512;    // ... and then running this many workgroups at most
 int ga_fitness_supported(int nin, int h1, int h2);
 hipError_t launch_ga_feasible(const GAConst &c, uint32_t *blk_count, uint64_t *blk_off, unsigned long long *n_fl,
                               uint32_t *fl, hipStream_t st);

@@ -115,3 +115,26 @@ def test_ga_objective_and_state_apart(mf, orc):
     sc2 = synth.ga_scenarios(4, 2, seed=9)
     run_both_obj(mf, orc, bf, sc2.sla, sc2.omega, synth.make_objective(bf, 9), synth.make_state(bf, 9),
                  pop=32, gens=5, seed=2)
+
+
+def test_ga_small_population_shapes(mf, orc):
+    # small populations take the one-workgroup-per-individual fitness kernel:
+    # more models than waves (two rounds, idle waves in the second), weights
+    # staged in LDS and weights too large for it, a ragged last round
+    sm = synth.make_instance([3, 2, 3, 2, 3, 2, 3, 2, 3, 2], 8, 4, 16, 16, seed=4, vram_quantile=0.8)
+    sc = synth.ga_scenarios(10, 3, seed=4)
+    run_both_obj(mf, orc, sm, sc.sla, sc.omega, synth.make_objective(sm, 4), synth.make_state(sm, 4),
+                 pop=24, gens=6, seed=5)
+    big = synth.make_instance([4, 3, 2, 3, 2, 3, 2, 3, 4], 16, 4, 128, 128, seed=5, vram_quantile=0.8)
+    sc2 = synth.ga_scenarios(9, 2, seed=5)
+    run_both_obj(mf, orc, big, sc2.sla, sc2.omega, synth.make_objective(big, 5), None, pop=16, gens=4, seed=6)
+    run_both(mf, orc, big, sc2.sla, sc2.omega, pop=10, gens=3, seed=7)
+
+
+def test_ga_largest_operator_footprint(mf, orc):
+    # sixteen models, tournaments of eight, the largest population: the
+    # operator kernel's largest LDS layout (population, every Philox word of
+    # 64 pairs, parents' genes)
+    inst = synth.make_instance([2] * 16, 8, 4, 16, 16, seed=6, vram_quantile=0.7)
+    sc = synth.ga_scenarios(16, 1, seed=6)
+    run_both(mf, orc, inst, sc.sla, sc.omega, pop=4096, gens=2, tourn_k=8, p_mut=0.2, seed=11)
