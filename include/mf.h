@@ -321,7 +321,8 @@ mf_status mf_ga_workspace_size(const mf_problem *p, const mf_ga_args *args, size
 /* Runs the GA.  h_best_idx / h_best_J: host [S], the best individual ever
  * evaluated per scenario (J desc, index asc); UINT64_MAX / -inf if none was
  * feasible.  d_final_pop (optional, device uint64 [S][pop]): the last
- * population's joint indices.  Blocking. */
+ * population's joint indices, all UINT64_MAX when no configuration meets the
+ * VRAM cap.  Blocking (one synchronisation, at the end). */
 mf_status mf_ga_run(mf_problem *p, const mf_ga_args *args, void *d_ws, size_t ws_bytes,
                     void *stream, uint64_t *h_best_idx, double *h_best_J, uint64_t *d_final_pop);
 

@@ -1512,18 +1512,9 @@ mf_status mf_ga_run(mf_problem *p, const mf_ga_args *args, void *d_ws, size_t ws
     c.obj = obj_args(p, args->objective);
 
     const int S = args->n_scen, P = args->pop;
+    // an empty feasible list is handled on the device (the best stays unset,
+    // the final population reads all ones): no synchronisation mid-run
     MF_HIP(launch_ga_feasible(c, cnt, blk_off, n_fl, fl, s));
-    unsigned long long h_nfl = 0;
-    MF_HIP(hipMemcpyAsync(&h_nfl, n_fl, 8, hipMemcpyDeviceToHost, s));
-    MF_HIP(hipStreamSynchronize(s));
-    if (h_nfl == 0) {
-        for (int q = 0; q < S; q++) { h_best_idx[q] = UINT64_MAX; h_best_J[q] = -INFINITY; }
-        if (d_final_pop) {
-            MF_HIP(hipMemsetAsync(d_final_pop, 0xFF, (size_t)S * P * 8, s));
-            MF_HIP(hipStreamSynchronize(s));
-        }
-        return MF_OK;
-    }
     MF_HIP(launch_ga_init(args->seed, S, P, fl, n_fl, pa, bJ, bI, s));
     for (int g = 0; g <= args->gens; g++) {
         MF_HIP(launch_ga_fitness(c, S, P, pa, args->d_sla, args->d_omega, fit, s));

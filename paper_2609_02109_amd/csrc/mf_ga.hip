@@ -125,7 +125,10 @@ __global__ void ga_init_kernel(uint64_t seed, int S, int P, const uint32_t *fl, 
     const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (t >= (int64_t)S * P) return;
     const int s = (int)(t / P), j = (int)(t % P);
-    pop[t] = fl[ga_below(ga_draw(seed, (uint64_t)j, 0, (uint64_t)s, kPInit, 0), *n_fl)];
+    // no VRAM-feasible configuration: index 0 throughout (every fitness is
+    // -inf, the best stays unset and the final population reads all ones)
+    const unsigned long long nf = *n_fl;
+    pop[t] = nf ? fl[ga_below(ga_draw(seed, (uint64_t)j, 0, (uint64_t)s, kPInit, 0), nf)] : 0;
     if (j == 0) {
         best_J[s] = -INFINITY;
         best_idx[s] = ~0ull;
@@ -394,10 +397,11 @@ __global__ void __launch_bounds__(kOpThreads) ga_ops_kernel(const GAConst c, uin
     const uint64_t *ps = pop + (int64_t)s * P;
     const double *fs = fit + (int64_t)s * P;
     uint64_t *ns = next + (int64_t)s * P;
+    const unsigned long long n_fl = *n_fl_ptr;
     if (gen == gens) {
         if (final_pop)
             for (int j = pb * kOpThreads + tid; j < P; j += wgs_per_scen * kOpThreads)
-                final_pop[(int64_t)s * P + j] = ps[j];
+                final_pop[(int64_t)s * P + j] = n_fl ? ps[j] : ~0ull;
     }
     if (pb == 0) {
         // elite: best (f desc, index asc, slot asc), reduced in LDS
@@ -516,7 +520,7 @@ __global__ void __launch_bounds__(kOpThreads) ga_ops_kernel(const GAConst c, uin
         vs = vs + c.features[(int64_t)(c.opt_off[i] + ch[i]) * c.L + c.vram_col];
         idx = idx * (uint64_t)c.K[i] + (uint64_t)ch[i];
     }
-    if (!((double)vs <= (double)c.vram_cap)) idx = fl[ga_below(pw[ob.rep(t) * 4], *n_fl_ptr)];
+    if (!((double)vs <= (double)c.vram_cap)) idx = n_fl ? fl[ga_below(pw[ob.rep(t) * 4], n_fl)] : 0;
     ns[j] = idx;
 }
 

@@ -68,8 +68,15 @@ def test_ga_no_feasible_configuration(mf, orc):
     inst = synth.cfg1(0)
     inst.vram_cap = 1.0
     sc = synth.ga_scenarios(5, 3, seed=0)
-    g = mf.Problem(inst).ga(sc.sla, sc.omega, pop=16, gens=2, final_pop=True)
-    assert np.all(g["best_idx"] == np.uint64(2 ** 64 - 1)) and np.all(np.isneginf(g["best_J"]))
+    p = mf.Problem(inst)
+    # both fitness kernels: a small population, and 3 x 4096 individuals
+    for pop in (16, 4096):
+        g = p.ga(sc.sla, sc.omega, pop=pop, gens=2, final_pop=True)
+        assert np.all(g["best_idx"] == np.uint64(2 ** 64 - 1)) and np.all(np.isneginf(g["best_J"]))
+        assert np.all(g["final_pop"].cpu().numpy().astype(np.uint64) == np.uint64(2 ** 64 - 1))
+    # and a problem with feasible configurations right after, on the same device
+    inst2 = synth.cfg1(0)
+    run_both(mf, orc, inst2, sc.sla, sc.omega, pop=16, gens=2, seed=3)
 
 
 def test_ga_rejects_bad_arguments(mf):
