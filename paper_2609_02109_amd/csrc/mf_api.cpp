@@ -287,7 +287,7 @@ void stride_digits(const mf_problem &p, uint64_t stride, uint32_t *out)
 
 // Workspace layout for one search launch set over n configurations.
 struct WsLayout {
-    size_t res, work, workJ, collect, lists, cand, entJ, entF, total;
+    size_t res, work, workJ, collect, lists, counts, cand, entJ, entF, total;
     uint32_t work_cap, collect_cap;
     int kp, grid, waves;
 };
@@ -325,6 +325,7 @@ WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k)
     w.workJ = o; o = align256(o + (size_t)w.work_cap * 4);
     w.collect = o; o = align256(o + (size_t)w.collect_cap * 4);
     w.lists = o; o = align256(o + (size_t)w.grid * w.kp * 8);
+    w.counts = o; o = align256(o + (size_t)w.grid * 16);
     w.cand = o; o = align256(o + (size_t)w.kp * 8);
     const size_t n_ent = (size_t)w.kp + w.work_cap + w.collect_cap;
     w.entJ = o; o = align256(o + n_ent * 8);
@@ -412,6 +413,7 @@ hipError_t launch_fast_path(const mf_problem *p, const FastArgs &fa, int grid, i
     ba.collect_cap = fa.collect_cap;
     ba.theta = fa.theta;
     ba.wg_lists = fa.wg_lists;
+    ba.wg_counts = fa.wg_counts;
     ba.mask = fa.mask;
     ba.pred = fa.pred;
     ba.obj = fa.obj;
@@ -430,6 +432,7 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     float *workJ = reinterpret_cast<float *>(ws + w.workJ);
     uint32_t *collect = reinterpret_cast<uint32_t *>(ws + w.collect);
     unsigned long long *lists = reinterpret_cast<unsigned long long *>(ws + w.lists);
+    unsigned long long *counts = reinterpret_cast<unsigned long long *>(ws + w.counts);
     unsigned long long *cand = reinterpret_cast<unsigned long long *>(ws + w.cand);
     double *entJ = reinterpret_cast<double *>(ws + w.entJ);
     uint32_t *entF = reinterpret_cast<uint32_t *>(ws + w.entF);
@@ -454,6 +457,7 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     fa.collect = collect;
     fa.collect_cap = w.collect_cap;
     fa.wg_lists = lists;
+    fa.wg_counts = counts;
     fa.mask = dump ? args->d_mask + dump_off : nullptr;
     fa.pred = dump ? args->d_pred + dump_off * (uint64_t)p->N * 2u : nullptr;
     fa.obj = obj_args(p, args->objective);
@@ -491,7 +495,7 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     MF_HIP2(hipEventRecord(ev0, s));
     MF_HIP2(launch_fast_path(p, fa, w.grid, w.kp, kModeSearch, s));
     MF_HIP2(hipEventRecord(ev1, s));
-    MF_HIP2(launch_merge_lists(lists, w.grid, w.kp, cand, s));
+    MF_HIP2(launch_merge_lists(lists, w.grid, w.kp, cand, counts, &R->n_vram, s));
     ca.phase = 0;
     MF_HIP2(launch_canonical(ca, w.kp, true, s));
     MF_HIP2(launch_kth_candidate(cand, entJ, entF, w.kp, args->top_k, R, s));
@@ -593,7 +597,7 @@ constexpr uint64_t kFixedChunk = 1ull << 36;   // configurations per scan launch
 constexpr uint32_t kFixedInnerMin = 256;       // inner configurations per block (unless the space is smaller)
 
 struct FixedWs {
-    size_t res, rows, pens, prow, lists, total;
+    size_t res, rows, pens, prow, lists, counts, total;
     int grid;
 };
 
@@ -640,6 +644,7 @@ FixedWs fixed_ws_layout(const mf_problem &p, int grid, int top_k)
     w.pens = o; o = align256(o + (size_t)p.sumK * sizeof(FixedPen));
     w.prow = o; o = align256(o + (size_t)p.sumK * 8);
     w.lists = o; o = align256(o + (size_t)grid * top_k * sizeof(K128));
+    w.counts = o; o = align256(o + (size_t)grid * 16);
     w.total = o;
     return w;
 }
@@ -699,6 +704,7 @@ mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipS
     a.pens = reinterpret_cast<FixedPen *>(ws + w.pens);
     a.pred_rows = reinterpret_cast<float2 *>(ws + w.prow);
     a.wg_lists = reinterpret_cast<K128 *>(ws + w.lists);
+    a.wg_counts = reinterpret_cast<unsigned long long *>(ws + w.counts);
     a.res = reinterpret_cast<DevResult *>(ws + w.res);
     const bool dump = (args->flags & MF_DUMP) != 0;
     const int wgs_per_cu = fixed_wgs_per_cu(a);
@@ -751,7 +757,7 @@ mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipS
 // ---- static (multi-step) search
 
 struct StaticWs {
-    size_t res, rows, pens, prow, lists, total;
+    size_t res, rows, pens, prow, lists, counts, total;
 };
 
 StaticWs static_ws_layout(const mf_problem &p, int n_steps, int top_k)
@@ -764,6 +770,7 @@ StaticWs static_ws_layout(const mf_problem &p, int n_steps, int top_k)
     w.pens = o; o = align256(o + tr * sizeof(FixedPen));
     w.prow = o; o = align256(o + (size_t)p.sumK * 8);
     w.lists = o; o = align256(o + (size_t)p.num_cus * kFixedMaxWgsPerCu * top_k * sizeof(K128));
+    w.counts = o; o = align256(o + (size_t)p.num_cus * kFixedMaxWgsPerCu * 16);
     w.total = o;
     return w;
 }
@@ -815,6 +822,7 @@ mf_status static_setup(mf_problem *p, const mf_static_args *args, char *ws, int 
     a.rows = nullptr;
     a.pred_rows = reinterpret_cast<float2 *>(ws + w.prow);
     a.wg_lists = reinterpret_cast<K128 *>(ws + w.lists);
+    a.wg_counts = reinterpret_cast<unsigned long long *>(ws + w.counts);
     a.res = reinterpret_cast<DevResult *>(ws + w.res);
     sa = StaticArgs{};
     sa.n_steps = args->n_steps;

@@ -438,25 +438,26 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
     }
 
     if (!LIST && mode == kModeSearch) {
+        // counts and list per workgroup (the merge kernel sums and merges them)
+        __shared__ unsigned long long s_cnt[2 * WAVES];
         const unsigned long long sv = wave_sum64(c_vram), sf = wave_sum64(c_feas);
         if (lane == 0) {
-            if (sv) atomicAdd(&args.res->n_vram, sv);
-            if (sf) atomicAdd(&args.res->n_feas_sure, sf);
+            s_cnt[wv] = sv;
+            s_cnt[WAVES + wv] = sf;
         }
 #pragma unroll
         for (int j = 0; j < 2; j++)
             if (j * 64 + lane < kp) lst[wv * kp + j * 64 + lane] = wl.s[j];
-        __syncthreads();
+        wl_tree_merge<2, WAVES>(wl, lst, kp, wv, lane, kp);
         if (wv == 0) {
-            for (int w = 1; w < WAVES; w++)
-#pragma unroll
-                for (int j = 0; j < 2; j++) {
-                    const int q = j * 64 + lane;
-                    wl_offer(wl, q < kp ? lst[w * kp + q] : 0ull, lane, kp);
-                }
 #pragma unroll
             for (int j = 0; j < 2; j++)
                 if (j * 64 + lane < kp) args.wg_lists[(uint64_t)blockIdx.x * kp + j * 64 + lane] = wl.s[j];
+            if (lane < 2) {
+                unsigned long long t = 0;
+                for (int w = 0; w < WAVES; w++) t += s_cnt[lane * WAVES + w];
+                args.wg_counts[2 * (uint64_t)blockIdx.x + lane] = t;
+            }
         }
     }
 }

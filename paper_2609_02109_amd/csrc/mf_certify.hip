@@ -139,7 +139,6 @@ canon_kernel(const CanonArgs a, const int search_mode)
         if (lane == 0) {
             if (a.ent_J) a.ent_J[e] = (feas && need_J) ? J : -INFINITY;
             if (a.ent_flags) a.ent_flags[e] = fl;
-            if (work_entry && need_J && !a.collect_mode) atomicAdd(&a.res->n_full_J, 1ull);
             if (search_mode && a.mask && work_entry)
                 a.mask[off] = (uint8_t)((a.mask[off] & 1u) | (sla_ok ? 2u : 0u) | (feas ? 4u : 0u) | 8u);
         }

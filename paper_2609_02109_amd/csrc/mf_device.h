@@ -155,7 +155,97 @@ __device__ __forceinline__ void wl_insert(WaveList<NS> &L, unsigned long long nk
     L.thr = th;
 }
 
-// Offer every lane's key (0 = none) to the list.
+__device__ __forceinline__ unsigned long long shfl64(unsigned long long x, int src)
+{
+    const uint32_t lo = __shfl((int)(uint32_t)x, src);
+    const uint32_t hi = __shfl((int)(uint32_t)(x >> 32), src);
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+__device__ __forceinline__ unsigned long long shfl_xor64(unsigned long long x, int m)
+{
+    const uint32_t lo = __shfl_xor((int)(uint32_t)x, m);
+    const uint32_t hi = __shfl_xor((int)(uint32_t)(x >> 32), m);
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+// Compare-exchange with the lane j apart: the lower lane of the pair keeps
+// the larger key when `desc`, the smaller otherwise.
+__device__ __forceinline__ unsigned long long cx_lane(unsigned long long x, int j, int lane, bool desc)
+{
+    const unsigned long long o = shfl_xor64(x, j);
+    const bool keep_max = ((lane & j) == 0) == desc;
+    const unsigned long long hi = x > o ? x : o, lo = x > o ? o : x;
+    return keep_max ? hi : lo;
+}
+
+// Bitonic sort of one key per lane, descending across the wave.
+__device__ __forceinline__ unsigned long long wave_sort_desc(unsigned long long x, int lane)
+{
+#pragma unroll
+    for (int k = 2; k <= 64; k <<= 1)
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1) x = cx_lane(x, j, lane, (lane & k) == 0);
+    return x;
+}
+
+// Merge a sorted list b (the layout of WaveList, zeros past its end) into L:
+// L keeps the kp largest keys of both, sorted.  With both sides descending,
+// the elementwise max of L and b reversed holds the 64 NS largest keys of the
+// union as a bitonic sequence; the half-cleaner cascade sorts it.
+template <int NS>
+__device__ __forceinline__ void wl_merge_sorted(WaveList<NS> &L, const unsigned long long (&b)[NS], int lane,
+                                                int kp)
+{
+    unsigned long long c[NS];
+#pragma unroll
+    for (int j = 0; j < NS; j++) {
+        const unsigned long long r = shfl64(b[NS - 1 - j], 63 - lane);
+        c[j] = L.s[j] > r ? L.s[j] : r;
+    }
+    if constexpr (NS == 2) {   // stride 64: the two registers of a lane
+        const unsigned long long hi = c[0] > c[1] ? c[0] : c[1], lo = c[0] > c[1] ? c[1] : c[0];
+        c[0] = hi;
+        c[1] = lo;
+    }
+#pragma unroll
+    for (int j = 32; j > 0; j >>= 1)
+#pragma unroll
+        for (int r = 0; r < NS; r++) c[r] = cx_lane(c[r], j, lane, true);
+    unsigned long long th = 0ull;
+#pragma unroll
+    for (int j = 0; j < NS; j++) {
+        L.s[j] = j * 64 + lane < kp ? c[j] : 0ull;
+        if ((kp - 1) / 64 == j) th = readlane64(L.s[j], (kp - 1) % 64);
+    }
+    L.thr = th;
+}
+
+// Tree merge of a workgroup's per-wave lists: list w sits at lst + w stride
+// (slot q at q, zeros from kp on).  WAVES is a power of two; the result ends
+// in wave 0's L.  Every thread of the workgroup calls this.
+template <int NS, int WAVES>
+__device__ __forceinline__ void wl_tree_merge(WaveList<NS> &L, unsigned long long *lst, int stride, int wv,
+                                              int lane, int kp)
+{
+#pragma unroll
+    for (int h = WAVES / 2; h >= 1; h >>= 1) {
+        __syncthreads();
+        if (wv < h) {
+            unsigned long long b[NS];
+#pragma unroll
+            for (int j = 0; j < NS; j++) b[j] = j * 64 + lane < kp ? lst[(wv + h) * stride + j * 64 + lane] : 0ull;
+            wl_merge_sorted(L, b, lane, kp);
+            if (h > 1)
+#pragma unroll
+                for (int j = 0; j < NS; j++)
+                    if (j * 64 + lane < kp) lst[wv * stride + j * 64 + lane] = L.s[j];
+        }
+    }
+}
+
+// Offer every lane's key (0 = none) to the list, one key at a time (the
+// form for hot loops: it holds no extra registers).
 template <int NS>
 __device__ __forceinline__ void wl_offer(WaveList<NS> &L, unsigned long long mykey, int lane, int kp)
 {

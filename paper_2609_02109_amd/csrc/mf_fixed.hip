@@ -339,9 +339,11 @@ __global__ void __launch_bounds__(kFixedWaves * 64) fixed_scan_kernel(const Fixe
         }
     }
 
+    // counts and list per workgroup (the merge kernel sums and merges them)
+    __shared__ unsigned long long s_cnt[2 * kFixedWaves];
     if (lane == 0) {
-        if (c_vram) atomicAdd(&a.res->n_vram, c_vram);
-        if (c_feas) atomicAdd(&a.res->n_feas_sure, c_feas);
+        s_cnt[wv] = c_vram;
+        s_cnt[kFixedWaves + wv] = c_feas;
     }
     lst[wv * 64 + lane] = key_if(lane < k, slot);
     __syncthreads();
@@ -349,6 +351,11 @@ __global__ void __launch_bounds__(kFixedWaves * 64) fixed_scan_kernel(const Fixe
 #pragma unroll 1
         for (int w = 1; w < kFixedWaves; w++) list128_offer(slot, lst[w * 64 + lane], lane, k, thr);
         if (lane < k) a.wg_lists[(uint64_t)blockIdx.x * k + lane] = slot;
+        if (lane < 2) {
+            unsigned long long t = 0;
+            for (int w = 0; w < kFixedWaves; w++) t += s_cnt[lane * kFixedWaves + w];
+            a.wg_counts[2 * (uint64_t)blockIdx.x + lane] = t;
+        }
     }
 }
 
@@ -362,10 +369,23 @@ constexpr int kFixedMergeWaves = 16;
 constexpr int kMergeAhead = 4;
 
 __global__ void __launch_bounds__(kFixedMergeWaves * 64)
-fixed_merge_kernel(const K128 *lists, int n_lists, int k, DevResult *R)
+fixed_merge_kernel(const K128 *lists, const unsigned long long *wg_counts, int n_lists, int k, DevResult *R)
 {
     __shared__ K128 lst[kFixedMergeWaves * 64];
+    __shared__ unsigned long long s_cnt[2 * kFixedMergeWaves];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    // the workgroups' counts
+    unsigned long long cv = 0, cf = 0;
+    for (int l = threadIdx.x; l < n_lists; l += blockDim.x) {
+        cv += wg_counts[2 * (int64_t)l];
+        cf += wg_counts[2 * (int64_t)l + 1];
+    }
+    cv = wave_sum64(cv);
+    cf = wave_sum64(cf);
+    if (lane == 0) {
+        s_cnt[wv] = cv;
+        s_cnt[kFixedMergeWaves + wv] = cf;
+    }
     // the largest k-th key over the lists
     K128 lb = {0ull, 0ull};
     for (int l = threadIdx.x; l < n_lists; l += blockDim.x) {
@@ -412,6 +432,11 @@ fixed_merge_kernel(const K128 *lists, int n_lists, int k, DevResult *R)
             R->n_top = n_top;
             R->status |= kStatVerified;
         }
+        if (lane < 2) {
+            unsigned long long t = 0;
+            for (int w = 0; w < kFixedMergeWaves; w++) t += s_cnt[lane * kFixedMergeWaves + w];
+            (lane == 0 ? R->n_vram : R->n_feas_sure) = t;
+        }
     }
 }
 
@@ -456,8 +481,8 @@ hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s,
     hipLaunchKernelGGL(fn, dim3(grid), dim3(kFixedWaves * 64), lds, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = hipEventRecord(ev1, s)) != hipSuccess) return e;
-    hipLaunchKernelGGL(fixed_merge_kernel, dim3(1), dim3(kFixedMergeWaves * 64), 0, s, a.wg_lists, grid, a.top_k,
-                       a.res);
+    hipLaunchKernelGGL(fixed_merge_kernel, dim3(1), dim3(kFixedMergeWaves * 64), 0, s, a.wg_lists, a.wg_counts, grid,
+                       a.top_k, a.res);
     return hipGetLastError();
 }
 
@@ -629,9 +654,11 @@ __global__ void __launch_bounds__(kFixedWaves * 64) static_scan_kernel(const Sta
         }
     }
 
+    // counts and list per workgroup (the merge kernel sums and merges them)
+    __shared__ unsigned long long s_cnt[2 * kFixedWaves];
     if (lane == 0) {
-        if (c_vram) atomicAdd(&a.res->n_vram, c_vram);
-        if (c_feas) atomicAdd(&a.res->n_feas_sure, c_feas);
+        s_cnt[wv] = c_vram;
+        s_cnt[kFixedWaves + wv] = c_feas;
     }
     lst[wv * 64 + lane] = key_if(lane < k, slot);
     __syncthreads();
@@ -639,6 +666,11 @@ __global__ void __launch_bounds__(kFixedWaves * 64) static_scan_kernel(const Sta
 #pragma unroll 1
         for (int w = 1; w < kFixedWaves; w++) list128_offer(slot, lst[w * 64 + lane], lane, k, thr);
         if (lane < k) a.wg_lists[(uint64_t)blockIdx.x * k + lane] = slot;
+        if (lane < 2) {
+            unsigned long long t = 0;
+            for (int w = 0; w < kFixedWaves; w++) t += s_cnt[lane * kFixedWaves + w];
+            a.wg_counts[2 * (uint64_t)blockIdx.x + lane] = t;
+        }
     }
 }
 
@@ -724,8 +756,8 @@ hipError_t launch_static(const StaticArgs &a, int grid, hipStream_t s, hipEvent_
     hipLaunchKernelGGL(fn, dim3(grid), dim3(kFixedWaves * 64), lds, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = hipEventRecord(ev1, s)) != hipSuccess) return e;
-    hipLaunchKernelGGL(fixed_merge_kernel, dim3(1), dim3(kFixedMergeWaves * 64), 0, s, a.f.wg_lists, grid,
-                       a.f.top_k, a.f.res);
+    hipLaunchKernelGGL(fixed_merge_kernel, dim3(1), dim3(kFixedMergeWaves * 64), 0, s, a.f.wg_lists, a.f.wg_counts,
+                       grid, a.f.top_k, a.f.res);
     return hipGetLastError();
 }
 

@@ -72,7 +72,6 @@ struct ObjArgs {
 // Counters and results the search kernels fill in device memory.
 struct DevResult {
     unsigned long long n_vram, n_feas_sure, n_work, n_collect;
-    unsigned long long n_full_J;    // certification entries that needed the full canonical J
     unsigned long long n_feas_cert, n_cand;
     unsigned int status;        // see kStat*
     int n_top;
@@ -123,6 +122,7 @@ struct FastArgs {
     uint32_t collect_cap;
     double theta;               // collect mode threshold on U
     unsigned long long *wg_lists; // [grid][KP] top-KP keys (U, lowest index) per workgroup
+    unsigned long long *wg_counts; // [grid][2] VRAM-feasible and surely feasible counts per workgroup
     uint8_t *mask;              // dump (optional)
     float *pred;                // dump (optional)
     ObjArgs obj;
@@ -192,6 +192,7 @@ struct Bf16Args {
     uint32_t collect_cap;
     double theta;
     unsigned long long *wg_lists;
+    unsigned long long *wg_counts;
     uint8_t *mask;
     float *pred;
     ObjArgs obj;
@@ -292,6 +293,7 @@ struct FixedArgs {
     FixedPen *pens;                  // [sumK]
     float2 *pred_rows;               // [sumK] canonical (lat, thr) rounded to fp32
     K128 *wg_lists;                  // [grid][top_k]
+    unsigned long long *wg_counts;   // [grid][2] VRAM-feasible and feasible counts per workgroup
     DevResult *res;
     uint8_t *mask;                   // dump (optional)
     float *pred;                     // dump (optional)
@@ -354,8 +356,8 @@ hipError_t launch_bf16_h256(const Bf16Args &a, const FastConst &fc, const Bf16Co
                             hipStream_t s);
 hipError_t launch_precompute_phat(const float *features, const float *canon_w, int n_rows, int L, int A, int H,
                                   int64_t wstride, const int32_t *row_model, float *phat, int pst, hipStream_t s);
-hipError_t launch_merge_lists(const unsigned long long *lists, int n_lists, int kp,
-                              unsigned long long *out, hipStream_t s);
+hipError_t launch_merge_lists(const unsigned long long *lists, int n_lists, int kp, unsigned long long *out,
+                              const unsigned long long *wg_counts, unsigned long long *counts_out, hipStream_t s);
 hipError_t launch_canonical(const CanonArgs &a, int n_entries_max, bool search_mode, hipStream_t s);
 hipError_t launch_kth_candidate(const unsigned long long *cand_keys, const double *ent_J, const uint32_t *ent_flags,
                                 int kp, int k, DevResult *res, hipStream_t s);

@@ -317,19 +317,22 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
     }
 
     if (mode == kModeSearch) {
+        // counts and list per workgroup (the merge kernel sums and merges them)
+        __shared__ unsigned long long s_cnt[2 * WAVES];
         const unsigned long long sv = wave_sum64(c_vram), sf = wave_sum64(c_feas);
         if (lane == 0) {
-            if (sv) atomicAdd(&args.res->n_vram, sv);
-            if (sf) atomicAdd(&args.res->n_feas_sure, sf);
+            s_cnt[wv] = sv;
+            s_cnt[WAVES + wv] = sf;
         }
         if (lane < kp) lst[wv * kp + lane] = wl.s[0];
-        __syncthreads();
+        wl_tree_merge<1, WAVES>(wl, lst, kp, wv, lane, kp);
         if (wv == 0) {
-            for (int w = 1; w < WAVES; w++) {
-                const unsigned long long k2 = lane < kp ? lst[w * kp + lane] : 0ull;
-                wl_offer(wl, k2, lane, kp);
-            }
             if (lane < kp) args.wg_lists[(uint64_t)blockIdx.x * kp + lane] = wl.s[0];
+            if (lane < 2) {
+                unsigned long long t = 0;
+                for (int w = 0; w < WAVES; w++) t += s_cnt[lane * WAVES + w];
+                args.wg_counts[2 * (uint64_t)blockIdx.x + lane] = t;
+            }
         }
     }
 }
@@ -339,28 +342,68 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
 // ---------------------------------------------------------------------------
 constexpr int kMergeWaves = 16;
 
+constexpr int kMergeStageKeys = 4096;   // keys staged in LDS per pass
+
+// Each per-workgroup list is sorted: the lists are staged in LDS a batch at a
+// time (every thread loading), wave w merges lists w, w + 16, ... of the
+// batch into its own, then wave 0 merges the 16.  The workgroups' counts are
+// summed into counts_out[0..1] (VRAM-feasible, surely feasible).
 template <int NS>
 __global__ void __launch_bounds__(kMergeWaves * 64)
-merge_lists_kernel(const unsigned long long *lists, int n_keys, int kp, unsigned long long *out)
+merge_lists_kernel(const unsigned long long *lists, int n_lists, int kp, unsigned long long *out,
+                   const unsigned long long *wg_counts, unsigned long long *counts_out)
 {
+    __shared__ unsigned long long stage[kMergeStageKeys];
     __shared__ unsigned long long lst[kMergeWaves * 64 * NS];
+    __shared__ unsigned long long s_cnt[2 * kMergeWaves];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    WaveList<NS> L;
+    WaveList<NS> L, L2;   // two independent merge chains per wave
     wl_init(L);
-    for (int base = wv * 64; base < n_keys; base += kMergeWaves * 64) {
-        const int t = base + lane;
-        wl_offer(L, t < n_keys ? lists[t] : 0ull, lane, kp);
+    wl_init(L2);
+    const int per_pass = kMergeStageKeys / kp;   // kp <= 128: at least 32 lists
+    for (int l0 = 0; l0 < n_lists; l0 += per_pass) {
+        const int nl = n_lists - l0 < per_pass ? n_lists - l0 : per_pass;
+        __syncthreads();
+        for (int t = threadIdx.x; t < nl * kp; t += kMergeWaves * 64) stage[t] = lists[(uint64_t)l0 * kp + t];
+        __syncthreads();
+        for (int i = wv; i < nl; i += 2 * kMergeWaves) {
+            const int i2 = i + kMergeWaves;
+            unsigned long long b[NS], b2[NS];
+#pragma unroll
+            for (int j = 0; j < NS; j++) {
+                const bool in = j * 64 + lane < kp;
+                b[j] = in ? stage[i * kp + j * 64 + lane] : 0ull;
+                b2[j] = in && i2 < nl ? stage[i2 * kp + j * 64 + lane] : 0ull;
+            }
+            wl_merge_sorted(L, b, lane, kp);
+            wl_merge_sorted(L2, b2, lane, kp);
+        }
+    }
+    wl_merge_sorted(L, L2.s, lane, kp);
+    unsigned long long cv = 0, cf = 0;
+    if (wg_counts)
+        for (int i = threadIdx.x; i < n_lists; i += kMergeWaves * 64) {
+            cv += wg_counts[2 * (uint64_t)i];
+            cf += wg_counts[2 * (uint64_t)i + 1];
+        }
+    cv = wave_sum64(cv);
+    cf = wave_sum64(cf);
+    if (lane == 0) {
+        s_cnt[wv] = cv;
+        s_cnt[kMergeWaves + wv] = cf;
     }
 #pragma unroll
-    for (int j = 0; j < NS; j++) lst[(wv * NS + j) * 64 + lane] = (j * 64 + lane < kp) ? L.s[j] : 0ull;
-    __syncthreads();
+    for (int j = 0; j < NS; j++) lst[(wv * NS + j) * 64 + lane] = L.s[j];
+    wl_tree_merge<NS, kMergeWaves>(L, lst, NS * 64, wv, lane, kp);
     if (wv == 0) {
-        for (int w = 1; w < kMergeWaves; w++)
-#pragma unroll
-            for (int j = 0; j < NS; j++) wl_offer(L, lst[(w * NS + j) * 64 + lane], lane, kp);
 #pragma unroll
         for (int j = 0; j < NS; j++)
             if (j * 64 + lane < kp) out[j * 64 + lane] = L.s[j];
+        if (wg_counts && lane < 2) {
+            unsigned long long t = 0;
+            for (int w = 0; w < kMergeWaves; w++) t += s_cnt[lane * kMergeWaves + w];
+            counts_out[lane] = t;
+        }
     }
 }
 
@@ -427,12 +470,14 @@ hipError_t launch_fast_impl(const FastArgs &a, const FastConst &fc, int grid, in
 }
 
 hipError_t launch_merge_lists(const unsigned long long *lists, int n_lists, int kp, unsigned long long *out,
-                              hipStream_t s)
+                              const unsigned long long *wg_counts, unsigned long long *counts_out, hipStream_t s)
 {
     if (kp <= 64)
-        hipLaunchKernelGGL(merge_lists_kernel<1>, dim3(1), dim3(kMergeWaves * 64), 0, s, lists, n_lists * kp, kp, out);
+        hipLaunchKernelGGL(merge_lists_kernel<1>, dim3(1), dim3(kMergeWaves * 64), 0, s, lists, n_lists, kp, out,
+                           wg_counts, counts_out);
     else
-        hipLaunchKernelGGL(merge_lists_kernel<2>, dim3(1), dim3(kMergeWaves * 64), 0, s, lists, n_lists * kp, kp, out);
+        hipLaunchKernelGGL(merge_lists_kernel<2>, dim3(1), dim3(kMergeWaves * 64), 0, s, lists, n_lists, kp, out,
+                           wg_counts, counts_out);
     return hipGetLastError();
 }
 

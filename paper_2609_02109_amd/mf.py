@@ -10,6 +10,10 @@ import ctypes as C
 import os
 
 import numpy as np
+# torch first: it brings the HIP runtime it was built against, and the
+# library then binds to that same runtime (one runtime per process; loading
+# the library first would pull in another copy that torch then reuses)
+import torch  # noqa: F401
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmf.so")
@@ -153,7 +157,6 @@ def _ptr(t):
 
 
 def _stream(stream):
-    import torch
     s = stream if stream is not None else torch.cuda.current_stream()
     return C.c_void_p(s.cuda_stream)
 
@@ -163,7 +166,6 @@ class Problem:
     (n_options, features, agg_cols, weights, ...), e.g. a synth.Instance."""
 
     def __init__(self, inst, device="cuda", stream=None, variants=None):
-        import torch
         self.inst = inst
         self.N = int(inst.n_models)
         self.A = int(inst.n_agg)
@@ -219,7 +221,6 @@ class Problem:
         return d
 
     def _dev(self, a, dtype):
-        import torch
         if a is None:
             return None
         if isinstance(a, torch.Tensor):
@@ -227,7 +228,6 @@ class Problem:
         return torch.as_tensor(np.asarray(a), dtype=dtype, device=self.device).contiguous()
 
     def workspace(self, nbytes: int):
-        import torch
         if self._ws is None or self._ws.numel() < nbytes:
             self._ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
         return self._ws
@@ -240,7 +240,6 @@ class Problem:
         have been created with variants).  state: None (each candidate's own
         aggregate feeds the surrogates) or the observed aggregate [A] held
         fixed for the whole search (Section III-B)."""
-        import torch
         if hi is None:
             hi = self.space_size
         d_sla = self._dev(sla, torch.float32)
@@ -275,7 +274,6 @@ class Problem:
         return out
 
     def _static_args(self, states, slas, omegas, objective, k=1, lo=0, hi=None, mask=None):
-        import torch
         st = np.ascontiguousarray(states, np.float32).reshape(-1, self.A)
         T = int(st.shape[0])
         d_sla = self._dev(np.asarray(slas, np.float32).reshape(T, self.N), torch.float32)
@@ -290,7 +288,6 @@ class Problem:
         """One configuration held over T steps (states [T][A], slas and omegas
         [T][N]): the exact top-k of S = sum_t J_t among the configurations
         feasible at every step; with dump=True also the per-index mask."""
-        import torch
         if hi is None:
             hi = self.space_size
         mask = torch.zeros(max(hi - lo, 1), dtype=torch.uint8, device=self.device) if dump else None
@@ -310,7 +307,6 @@ class Problem:
         """Per-step utilities of an index list held over T steps: J [n][T],
         S [n] (step-order sum), flags [n][T] (bit0 VRAM, bit1 the step's
         service constraints)."""
-        import torch
         d_idx = self._dev(np.asarray(idx, np.uint64).astype(np.int64), torch.int64)
         n = int(d_idx.numel())
         args, ws, keep = self._static_args(states, slas, omegas, objective)
@@ -330,7 +326,6 @@ class Problem:
         return res
 
     def eval_fast(self, idx, stream=None):
-        import torch
         d_idx = self._dev(idx, torch.int64)
         n = int(d_idx.numel())
         pred = torch.zeros((max(n, 1), self.N, 2), dtype=torch.float32, device=self.device)
@@ -339,7 +334,6 @@ class Problem:
         return pred[:n]
 
     def eval_canonical(self, idx, sla, omega, stream=None):
-        import torch
         d_idx = self._dev(idx, torch.int64)
         n = int(d_idx.numel())
         pred = torch.zeros((max(n, 1), self.N, 2), dtype=torch.float64, device=self.device)
@@ -357,7 +351,6 @@ class Problem:
            seed=0, final_pop=False, stream=None, objective=None, state=None):
         """GA scheduler over S scenarios (rows of sla / omega); objective and
         state as in search()."""
-        import torch
         d_sla = self._dev(sla, torch.float32)
         d_om = self._dev(omega, torch.float32)
         S = int(d_sla.shape[0])
