@@ -145,3 +145,19 @@ def test_ga_largest_operator_footprint(mf, orc):
     inst = synth.make_instance([2] * 16, 8, 4, 16, 16, seed=6, vram_quantile=0.7)
     sc = synth.ga_scenarios(16, 1, seed=6)
     run_both(mf, orc, inst, sc.sla, sc.omega, pop=4096, gens=2, tourn_k=8, p_mut=0.2, seed=11)
+
+
+def test_ga_large_population_shapes(mf, orc):
+    # populations above 8,192 take the one-lane-per-individual fitness: the
+    # paper's 64-32 sigmoid predictor with Eq. 3 and a fixed state, 22 inputs
+    # at 64-64, 14 inputs at 32-32; ragged last workgroups
+    a = synth.make_instance([12, 12, 9, 9, 9], 8, 4, 64, 32, seed=11, vram_quantile=0.8, act="sigmoid")
+    sa = synth.ga_scenarios(5, 3, seed=11)
+    run_both_obj(mf, orc, a, sa.sla, sa.omega, synth.make_objective(a, 11), synth.make_state(a, 11),
+                 pop=2750, gens=3, p_mut=0.1, seed=12)
+    b = synth.make_instance([6, 5, 4], 16, 6, 64, 64, seed=12, vram_quantile=0.7)
+    sb = synth.ga_scenarios(3, 5, seed=12)
+    run_both(mf, orc, b, sb.sla, sb.omega, pop=1700, gens=2, seed=13)
+    c = synth.make_instance([7, 9, 3, 5], 10, 4, 32, 32, seed=13, vram_quantile=0.75)
+    sc = synth.ga_scenarios(4, 3, seed=13)
+    run_both_obj(mf, orc, c, sc.sla, sc.omega, synth.make_objective(c, 13), None, pop=3000, gens=3, seed=14)
