@@ -9,7 +9,10 @@
 #include <cstdlib>
 #include <cstring>
 #include <limits>
+#include <map>
+#include <mutex>
 #include <new>
+#include <utility>
 #include <vector>
 
 #include "mf_internal.h"
@@ -49,6 +52,26 @@ struct mf_problem {
     float4 *d_bmodels = nullptr, *d_bg = nullptr;
     float *d_phat = nullptr;
 };
+
+namespace mfi {
+
+hipError_t ensure_dyn_lds(const void *fn, size_t bytes)
+{
+    static std::mutex mu;
+    static std::map<std::pair<const void *, int>, size_t> done;   // (kernel, device) -> limit set
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> g(mu);
+    const auto key = std::make_pair(fn, dev);
+    const auto it = done.find(key);
+    if (it != done.end() && it->second >= bytes) return hipSuccess;
+    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e == hipSuccess) done[key] = bytes;
+    return e;
+}
+
+}  // namespace mfi
 
 namespace {
 

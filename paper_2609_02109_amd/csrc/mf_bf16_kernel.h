@@ -468,7 +468,7 @@ hipError_t launch_bf16_t(const Bf16Args &a, const FastConst &fc, const Bf16Const
 {
     const size_t lds = bf16_lds_bytes(a.lay, kp);
     auto fn = fast_bf16_kernel<MAXN, A, H, FULL, LIST, OBJ, SIG>;
-    hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipError_t e = ensure_dyn_lds((const void *)fn, lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(grid), dim3(kBf16Waves * 64), lds, s, a, fc, bc, mode, kp);
     return hipGetLastError();

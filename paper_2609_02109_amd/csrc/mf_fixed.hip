@@ -462,7 +462,7 @@ int fixed_wgs_per_cu(const FixedArgs &a)
 {
     const ScanFn fn = scan_fn(a);
     const size_t lds = fixed_lds_bytes(a.sumK, a.obj.kind != 0);
-    if (hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    if (ensure_dyn_lds((const void *)fn, lds) != hipSuccess)
         return 1;
     int n = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, kFixedWaves * 64, lds) != hipSuccess || n < 1) return 1;
@@ -475,7 +475,7 @@ hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s,
     if (table && (e = launch_fixed_table(a, s)) != hipSuccess) return e;
     const size_t lds = fixed_lds_bytes(a.sumK, a.obj.kind != 0);
     const ScanFn fn = scan_fn(a);
-    e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    e = ensure_dyn_lds((const void *)fn, lds);
     if (e != hipSuccess) return e;
     if ((e = hipEventRecord(ev0, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(grid), dim3(kFixedWaves * 64), lds, s, a);
@@ -730,7 +730,7 @@ int static_wgs_per_cu(const StaticArgs &a)
 {
     const StaticFn fn = static_fn(a);
     const size_t lds = static_lds_bytes(a.n_steps, a.f.sumK, a.f.n_models, a.f.obj.kind != 0);
-    if (hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    if (ensure_dyn_lds((const void *)fn, lds) != hipSuccess)
         return 1;
     int n = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, kFixedWaves * 64, lds) != hipSuccess || n < 1) return 1;
@@ -750,7 +750,7 @@ hipError_t launch_static(const StaticArgs &a, int grid, hipStream_t s, hipEvent_
 {
     const size_t lds = static_lds_bytes(a.n_steps, a.f.sumK, a.f.n_models, a.f.obj.kind != 0);
     const StaticFn fn = static_fn(a);
-    hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipError_t e = ensure_dyn_lds((const void *)fn, lds);
     if (e != hipSuccess) return e;
     if ((e = hipEventRecord(ev0, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(grid), dim3(kFixedWaves * 64), lds, s, a);

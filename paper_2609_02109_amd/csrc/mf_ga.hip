@@ -562,8 +562,7 @@ hipError_t launch_ga_fitness(const GAConst &c, int S, int P, const uint64_t *pop
         const int grid = (int)(n < cap ? n : cap);
         auto fn = c.bf16 ? (stage ? ga_fitness_wide_kernel<true, true> : ga_fitness_wide_kernel<true, false>)
                          : (stage ? ga_fitness_wide_kernel<false, true> : ga_fitness_wide_kernel<false, false>);
-        const hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                 (int)lds);
+        const hipError_t e = ensure_dyn_lds((const void *)fn, lds);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(fn, dim3(grid), dim3(64 * W), lds, st, c, S, P, pop, sla, omega, fit,
                            stage ? (int)wfloats : 0);
@@ -604,8 +603,7 @@ hipError_t launch_ga_ops(const GAConst &c, uint64_t seed, int S, int P, int gen,
 {
     const int wgs = (P / 2 + kOpPairs - 1) / kOpPairs > 0 ? (P / 2 + kOpPairs - 1) / kOpPairs : 1;
     const size_t lds = ops_lds_bytes(tk, c.N);
-    const hipError_t e = hipFuncSetAttribute((const void *)ga_ops_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             (int)lds);
+    const hipError_t e = ensure_dyn_lds((const void *)ga_ops_kernel, lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(ga_ops_kernel, dim3(S * wgs), dim3(kOpThreads), lds, st, c, seed, P, gen, gens, tk, p_cx,
                        p_swap, p_mut, fl, n_fl, pop, fit, next, best_J, best_idx, final_pop, wgs);

@@ -337,6 +337,11 @@ struct GAConst {
     ObjArgs obj;
 };
 
+// Raise a kernel's dynamic-LDS limit to at least `bytes` on the current
+// device; the attribute stays set, so it is applied once per kernel, device
+// and size increase (a call that changes nothing costs a table lookup).
+hipError_t ensure_dyn_lds(const void *fn, size_t bytes);
+
 // launchers (return hipError_t of the launch)
 hipError_t launch_precompute_p(const float *features, const float *weights, const float *centre,
                                int n_rows, int L, int A, int H, int64_t wstride,
@@ -371,6 +376,8 @@ int static_wgs_per_cu(const StaticArgs &a);
 int fixed_wgs_per_cu(const FixedArgs &a);
 hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 constexpr int64_t kGaWideMax = 8192;   // populations (S x P) up to this size take the wide fitness kernel
+constexpr int kCanonWaves = 8;             // waves (models) per workgroup of the certification kernel, at most
+constexpr int kCanonFewEntries = 1024;     // index lists up to this length use them
 constexpr int kGaWideWaves = 8;             // ... with up to this many waves (models) per workgroup
 constexpr size_t kGaStageBytes = 64 * 1024;   // ... copying the weights to LDS when they fit in this
 constexpr int64_t kGaWideStagedWgs = 512;    // ... and then running this many workgroups at most

@@ -416,7 +416,7 @@ static hipError_t launch_fast_t(const FastArgs &a, const FastConst &fc, int grid
     if constexpr (MAXN == kMaxN && WAVES == kSearchWaves)   // the sigmoid output runs on the generic kernel
         if (fc.act) fn = a.obj.kind != 0 ? fast_kernel<MAXN, A, H, WAVES, true, true>
                                          : fast_kernel<MAXN, A, H, WAVES, false, true>;
-    hipError_t e = hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipError_t e = ensure_dyn_lds((const void *)fn, lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(grid), dim3(WAVES * 64), lds, s, a, fc, mode, kp);
     return hipGetLastError();
