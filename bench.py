@@ -29,8 +29,8 @@ CPU_SAMPLE = 1 << 24
 # HBM bytes per launch of the fast search kernel from rocprofv3 FETCH_SIZE /
 # WRITE_SIZE passes (profiles/fast_kernel_n6_k24_h64_hbm_counters.md), valid
 # only for the kernel source they were taken on
-TRAFFIC_BYTES = 1_737_344 + 27_278_560
-TRAFFIC_SOURCE_SHA = "bd92cf451beb63b8"
+TRAFFIC_BYTES = 1_736_576 + 27_285_952
+TRAFFIC_SOURCE_SHA = "5e80b12ce9b9420c"
 
 
 def measured_traffic():
