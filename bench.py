@@ -30,15 +30,25 @@ CPU_SAMPLE = 1 << 24
 # WRITE_SIZE passes (profiles/fast_kernel_n6_k24_h64_hbm_counters.md), valid
 # only for the kernel source they were taken on
 TRAFFIC_BYTES = 1_736_576 + 27_285_952
-TRAFFIC_SOURCE_SHA = "5e80b12ce9b9420c"
+TRAFFIC_SOURCE_SHA = "71e21d2d0e72b4df"
+
+
+# the fast kernel's source: its file and the headers it includes
+TRAFFIC_SOURCES = ("paper_2609_02109_amd/csrc/mf_search.hip", "paper_2609_02109_amd/csrc/mf_device.h",
+                   "paper_2609_02109_amd/csrc/mf_internal.h", "include/mf.h")
+
+
+def source_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for name in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic():
-    import hashlib
-    src = os.path.join(ROOT, "paper_2609_02109_amd", "csrc", "mf_search.hip")
-    with open(src, "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()[:16]
-    return TRAFFIC_BYTES if sha == TRAFFIC_SOURCE_SHA else None
+    return TRAFFIC_BYTES if source_sha() == TRAFFIC_SOURCE_SHA else None
 
 
 def log(*a):
