@@ -179,16 +179,6 @@ __device__ __forceinline__ unsigned long long cx_lane(unsigned long long x, int 
     return keep_max ? hi : lo;
 }
 
-// Bitonic sort of one key per lane, descending across the wave.
-__device__ __forceinline__ unsigned long long wave_sort_desc(unsigned long long x, int lane)
-{
-#pragma unroll
-    for (int k = 2; k <= 64; k <<= 1)
-#pragma unroll
-        for (int j = k >> 1; j > 0; j >>= 1) x = cx_lane(x, j, lane, (lane & k) == 0);
-    return x;
-}
-
 // Merge a sorted list b (the layout of WaveList, zeros past its end) into L:
 // L keeps the kp largest keys of both, sorted.  With both sides descending,
 // the elementwise max of L and b reversed holds the 64 NS largest keys of the
