@@ -29,8 +29,8 @@ CPU_SAMPLE = 1 << 24
 # HBM bytes per launch of the fast search kernel from rocprofv3 FETCH_SIZE /
 # WRITE_SIZE passes (profiles/fast_kernel_n6_k24_h64_hbm_counters.md), valid
 # only for the kernel source they were taken on
-TRAFFIC_BYTES = 1_736_576 + 27_285_952
-TRAFFIC_SOURCE_SHA = "71e21d2d0e72b4df"
+TRAFFIC_BYTES = 1_737_216 + 27_283_072
+TRAFFIC_SOURCE_SHA = "1809fc6b61ddb73e"
 
 
 # the fast kernel's source: its file and the headers it includes
