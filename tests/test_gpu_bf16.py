@@ -108,7 +108,8 @@ def test_bf16_eval_sampled_full_size(mf, orc):
 def test_bf16_n8_full_space_properties(mf, orc):
     # the whole 2^32-configuration space: the top-64 are feasible with the
     # oracle's J bit for bit, sorted by (J desc, index asc), and no sampled
-    # feasible configuration beats the 64th
+    # feasible configuration, and no feasible configuration one option from a
+    # top-64 member or two options from the argmax, beats the 64th
     inst = synth.cfg4(0)
     print(f"[bf16] full N=8 space {inst.space_size}", flush=True)
     p = mf.Problem(inst)
@@ -132,6 +133,34 @@ def test_bf16_n8_full_space_properties(mf, orc):
     f = g["n_feas"] / inst.space_size
     sd = np.sqrt(f * (1 - f) / len(samp))
     assert abs(feas.mean() - f) <= 6 * sd + 1e-3
+    # the nearest competitors: every configuration one option away from a
+    # top-64 member, and two options away from the argmax (the oracle on each)
+    K = [int(k) for k in inst.n_options]
+    strides = [int(np.prod(K[i + 1:])) for i in range(len(K))]
+
+    def digits(x):
+        return [(int(x) // strides[i]) % K[i] for i in range(len(K))]
+
+    near = set()
+    for x in top:
+        d = digits(x)
+        for i in range(len(K)):
+            for o in range(K[i]):
+                if o != d[i]:
+                    near.add(int(x) + (o - d[i]) * strides[i])
+    d0 = digits(top[0])
+    for i in range(len(K)):
+        for j in range(i + 1, len(K)):
+            for oi in range(K[i]):
+                for oj in range(K[j]):
+                    if oi != d0[i] and oj != d0[j]:
+                        near.add(int(top[0]) + (oi - d0[i]) * strides[i] + (oj - d0[j]) * strides[j])
+    near = np.array(sorted(near - set(int(t) for t in top)), dtype=np.uint64)
+    rn = orc.Problem(inst).eval_list(near, inst.sla, inst.omega)
+    fn = (rn["flags"] & 4) != 0
+    print(f"[bf16] {len(near)} neighbours of the top-64, {int(fn.sum())} feasible", flush=True)
+    assert fn.sum() > 0
+    assert np.all((rn["J"][fn] < kth) | ((rn["J"][fn] == kth) & (near[fn] > top[-1])))
 
 
 def test_bf16_topk_fallback_on_exact_ties(mf, orc):
