@@ -9,8 +9,11 @@
 // here with that exact chain (v_fma_f64 is correctly rounded, so the values
 // are the canonical ones bit for bit).
 //
-// One single-wave workgroup per entry: lanes take hidden units, the uniform
-// parts (decode, aggregate, output units) run redundantly per lane.
+// One workgroup per entry, lanes over hidden units.  The long certification
+// lists run one wave per entry, model after model.  Few entries (the top-k
+// candidates, short index lists) are latency-bound: there (FEW) wave w runs
+// the forward of the entry's models w, w + W, ... on its own scratch, and
+// wave 0 combines them in model order.
 #include "mf_canon.h"
 
 namespace mfi {
@@ -18,27 +21,37 @@ namespace mfi {
 
 // Canonical image per model (fp32 values, exact in fp64):
 //   W1T[nin][H1], b1[H1], W2T[H1][H2], b2[H2], W3[2][H2], b3[2]
-template <bool BF16>
-__global__ void __launch_bounds__(64)
+template <bool BF16, bool FEW>
+__global__ void __launch_bounds__(FEW ? 64 * kCanonWaves : 64)
 canon_kernel(const CanonArgs a, const int search_mode)
 {
-    __shared__ double h1s[kCanonMaxH];
-    __shared__ double h2s[kCanonMaxH];
-    __shared__ double zs[kCanonMaxIn];
+    extern __shared__ double canon_dyn[];   // FEW: [W][H1 + H2 + nin]
+    __shared__ double h1s_1[FEW ? 1 : kCanonMaxH];
+    __shared__ double h2s_1[FEW ? 1 : kCanonMaxH];
+    __shared__ double zs_1[FEW ? 1 : kCanonMaxIn];
     __shared__ int32_t ds[kMaxN];
     __shared__ float aggs[16];
     __shared__ float s_tau[kMaxN];
     __shared__ int32_t s_prev[kMaxN];
-    const int lane = threadIdx.x;
+    __shared__ double s_lat[FEW ? kMaxN : 1], s_thr[FEW ? kMaxN : 1];
+    const int lane = threadIdx.x & 63;
+    const int wave = FEW ? __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)) : 0;
+    const int W = FEW ? (int)(blockDim.x >> 6) : 1;
 #pragma unroll
     for (int i = 0; i < kMaxN; i++)   // compile-time index into the argument block
-        if (lane == i) {
+        if (threadIdx.x == (unsigned)i) {
             s_tau[i] = a.obj.tau[i];
             s_prev[i] = a.obj.prev[i];
         }
-    __syncthreads();
     const bool eq3 = a.obj.kind != 0;
     const int N = a.n_models, L = a.L, A = a.A, H1 = a.H1, H2 = a.H2, nin = L + A;
+    double *h1s = h1s_1, *h2s = h2s_1, *zs = zs_1;
+    if (FEW) {
+        h1s = canon_dyn + (int64_t)wave * (H1 + H2 + nin);
+        h2s = h1s + H1;
+        zs = h2s + H2;
+    }
+    __syncthreads();
 
     int64_t n_cand = 0, n_work = 0, n_coll = 0, n_ent, e0 = 0;
     double jthr = -INFINITY;   // certification entries need the full J only from here up
@@ -69,7 +82,7 @@ canon_kernel(const CanonArgs a, const int search_mode)
             if (e < n_cand) {
                 const unsigned long long key = a.cand_keys[e];
                 if (key == 0ull) {
-                    if (lane == 0) { a.ent_J[e] = -INFINITY; a.ent_flags[e] = 0; }
+                    if (threadIdx.x == 0) { a.ent_J[e] = -INFINITY; a.ent_flags[e] = 0; }
                     continue;
                 }
                 off = 0xFFFFFFFFu - (uint32_t)(key & 0xFFFFFFFFull);
@@ -86,32 +99,63 @@ canon_kernel(const CanonArgs a, const int search_mode)
         } else {
             idx = a.idx64[e];
         }
-        // decode (model N-1 least significant): lane i < N takes digit i
-        if (lane < N) {
+        // decode (model N-1 least significant): thread i < N takes digit i
+        if (FEW) __syncthreads();   // the previous entry's combine has read ds and aggs
+        if (threadIdx.x < (unsigned)N) {
             uint64_t stride = 1;
             for (int j = N - 1; j > lane; j--) stride *= (uint64_t)a.K[j];
             ds[lane] = (int32_t)((idx / stride) % (uint64_t)a.K[lane]);
         }
         __syncthreads();
-        // aggregate field: lane k < A sums slot k in fp32, model order
-        if (lane < A) {
+        // aggregate field: thread k < A sums slot k in fp32, model order
+        if (threadIdx.x < (unsigned)A) {
             float s = 0.f;
             for (int i = 0; i < N; i++)
                 s = s + a.features[(int64_t)(a.opt_off[i] + ds[i]) * L + a.agg_cols[lane]];
             aggs[lane] = s;
         }
         __syncthreads();
+        if (FEW) {
+            // the entry's models, W at a time: every wave takes part in every
+            // round (the forward has barriers); a wave past the last model
+            // repeats the first one and drops the result
+            const uint32_t need = models & ((1u << N) - 1u);
+            const int n_need = __popc(need);
+            for (int r0 = 0; r0 < n_need; r0 += W) {
+                const int q = r0 + wave;
+                uint32_t m = need;
+                for (int j = 0; j < q && m; j++) m &= m - 1u;
+                const bool act = q < n_need;
+                const int i = act ? __ffs(m) - 1 : __ffs(need) - 1;
+                const float *x = a.features + (int64_t)(a.opt_off[i] + ds[i]) * L;
+                for (int k = lane; k < nin; k += 64) zs[k] = k < L ? (double)x[k] : (double)aggs[k - L];
+                __syncthreads();
+                double lat, thr;
+                canon_model<BF16>(a.weights + (int64_t)i * a.wstride, nin, H1, H2, zs, h1s, h2s, lane, lat, thr, a.act);
+                if (act && lane == 0) {
+                    s_lat[i] = lat;
+                    s_thr[i] = thr;
+                }
+            }
+            __syncthreads();
+            if (wave != 0) continue;
+        }
         const bool vram_ok = (double)aggs[a.vram_slot] <= (double)a.vram_cap;
         bool sla_ok = true;
         uint32_t fl = 0;
         double J = 0.0;
         for (int i = 0; i < N; i++) {
             if (!((models >> i) & 1u)) continue;
-            const float *x = a.features + (int64_t)(a.opt_off[i] + ds[i]) * L;
-            for (int k = lane; k < nin; k += 64) zs[k] = k < L ? (double)x[k] : (double)aggs[k - L];
-            __syncthreads();
             double lat, thr;
-            canon_model<BF16>(a.weights + (int64_t)i * a.wstride, nin, H1, H2, zs, h1s, h2s, lane, lat, thr, a.act);
+            if (FEW) {
+                lat = s_lat[i];
+                thr = s_thr[i];
+            } else {
+                const float *x = a.features + (int64_t)(a.opt_off[i] + ds[i]) * L;
+                for (int k = lane; k < nin; k += 64) zs[k] = k < L ? (double)x[k] : (double)aggs[k - L];
+                __syncthreads();
+                canon_model<BF16>(a.weights + (int64_t)i * a.wstride, nin, H1, H2, zs, h1s, h2s, lane, lat, thr, a.act);
+            }
             if (!(lat <= (double)a.sla[i])) { sla_ok = false; fl |= 1u << (8 + i); }
             if (eq3) {
                 // Eq. 3 (Section II): per-variant min-max throughput, quality,
@@ -131,7 +175,7 @@ canon_kernel(const CanonArgs a, const int search_mode)
                 a.pred[(e * N + i) * 2 + 0] = lat;
                 a.pred[(e * N + i) * 2 + 1] = thr;
             }
-            __syncthreads();
+            if (!FEW) __syncthreads();
         }
         const bool feas = vram_ok && sla_ok;
         fl |= (vram_ok ? 1u : 0u) | (sla_ok ? 2u : 0u) | (feas ? 4u : 0u);
@@ -149,10 +193,20 @@ hipError_t launch_canonical(const CanonArgs &a, int n_entries_max, bool search_m
 {
     int grid = n_entries_max < 1 ? 1 : n_entries_max;
     if (grid > 4096) grid = 4096;
-    if (a.bf16)
-        hipLaunchKernelGGL(canon_kernel<true>, dim3(grid), dim3(64), 0, s, a, search_mode ? 1 : 0);
-    else
-        hipLaunchKernelGGL(canon_kernel<false>, dim3(grid), dim3(64), 0, s, a, search_mode ? 1 : 0);
+    const int sm = search_mode ? 1 : 0;
+    const bool few = search_mode ? a.phase == 0 : n_entries_max <= kCanonFewEntries;
+    if (!few) {
+        if (a.bf16)
+            hipLaunchKernelGGL((canon_kernel<true, false>), dim3(grid), dim3(64), 0, s, a, sm);
+        else
+            hipLaunchKernelGGL((canon_kernel<false, false>), dim3(grid), dim3(64), 0, s, a, sm);
+        return hipGetLastError();
+    }
+    // a wave per model
+    const int W = a.n_models < kCanonWaves ? a.n_models : kCanonWaves;
+    const size_t lds = (size_t)W * (a.H1 + a.H2 + a.L + a.A) * 8;
+    auto fn = a.bf16 ? canon_kernel<true, true> : canon_kernel<false, true>;
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(64 * W), lds, s, a, sm);
     return hipGetLastError();
 }
 

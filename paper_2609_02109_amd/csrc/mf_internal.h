@@ -376,8 +376,8 @@ int static_wgs_per_cu(const StaticArgs &a);
 int fixed_wgs_per_cu(const FixedArgs &a);
 hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 constexpr int64_t kGaWideMax = 8192;   // populations (S x P) up to this size take the wide fitness kernel
-constexpr int kCanonWaves = 8;             // waves (models) per workgroup of the certification kernel, at most
-constexpr int kCanonFewEntries = 1024;     // index lists up to this length use them
+constexpr int kCanonWaves = 8;             // certification of few entries: waves (models) per workgroup, at most
+constexpr int kCanonFewEntries = 1024;     // index lists up to this length count as few
 constexpr int kGaWideWaves = 8;             // ... with up to this many waves (models) per workgroup
 constexpr size_t kGaStageBytes = 64 * 1024;   // ... copying the weights to LDS when they fit in this
 constexpr int64_t kGaWideStagedWgs = 512;    // ... and then running this many workgroups at most
