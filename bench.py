@@ -25,6 +25,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_FP32_TFLOPS = 157.3
+PEAK_FP64_TFLOPS = 78.6
 CPU_SAMPLE = 1 << 24
 # HBM bytes per launch of the fast search kernel from rocprofv3 FETCH_SIZE /
 # WRITE_SIZE passes (profiles/fast_kernel_n6_k24_h64_hbm_counters.md), valid
@@ -227,13 +228,23 @@ def bench_ga(args):
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / args.steps
     evals = gp.n_scen * gp.pop * (gp.gens + 1)
+    # canonical fp64 flops of one fitness evaluation: N x (2 (L+A) H1 + 2 H1 H2 + 4 H2)
+    flops = evals * inst.n_models * 2 * ((inst.n_local + inst.n_agg) * inst.hidden1 + inst.hidden1 * inst.hidden2
+                                         + 2 * inst.hidden2)
+    achieved = flops / (ms * 1e-3) / 1e12
     line = {"metric": "GA fitness evaluations/sec (64 scenarios, population 2048, 100 generations, N=5)",
             "value": evals / (ms * 1e-3), "unit": "evaluations/s", "n_gpus": 1, "steps": args.steps,
             "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
             "vs_baseline": None, "dtype": "f64", "data": "synthetic (seeded generator, seed %d)" % args.seed,
             "config": {"workload": "GA on the N=5 instance (12,12,9,9,9 options): 64 scenarios x 2048 x "
                                    "(100+1) generations, tournament 3, crossover 0.7, mutation 0.05",
-                       "ms_per_ga_run": ms, "best_J_mean": float(r["best_J"].mean())}}
+                       "ms_per_ga_run": ms, "best_J_mean": float(r["best_J"].mean())},
+            # the fitness flops over the whole run's time (operators and the
+            # feasible list included), against the fp64 vector peak
+            "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_FP64_TFLOPS, "unit": "TFLOP/s",
+                         "frac": achieved / PEAK_FP64_TFLOPS, "traffic": None,
+                         "kernel": "whole GA run (fitness, operators, feasible list)",
+                         "flops_per_evaluation": flops // evals}}
     print(json.dumps(line), flush=True)
 
 
