@@ -52,14 +52,6 @@ __device__ __forceinline__ floatx16 load16(const float *p)
     return r;
 }
 
-__device__ __forceinline__ bf16x8 pack8(const float *x)
-{
-    bf16x8 r;
-#pragma unroll
-    for (int j = 0; j < 8; j++) r[j] = (__bf16)x[j];   // round to nearest even
-    return r;
-}
-
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short short2v __attribute__((ext_vector_type(2)));
 
