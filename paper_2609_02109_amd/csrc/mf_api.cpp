@@ -310,9 +310,9 @@ void stride_digits(const mf_problem &p, uint64_t stride, uint32_t *out)
 
 // Workspace layout for one search launch set over n configurations.
 struct WsLayout {
-    size_t res, work, workJ, collect, lists, counts, cand, entJ, entF, total;
+    size_t res, work, workJ, collect, lists, counts, cand, entJ, entF, parts, total;
     uint32_t work_cap, collect_cap;
-    int kp, grid, waves;
+    int kp, grid, waves, n_parts;
 };
 
 WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k)
@@ -353,6 +353,9 @@ WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k)
     const size_t n_ent = (size_t)w.kp + w.work_cap + w.collect_cap;
     w.entJ = o; o = align256(o + n_ent * 8);
     w.entF = o; o = align256(o + n_ent * 4);
+    // the exact selection runs in two levels over long ranges
+    w.n_parts = n > kSelSingleMax ? kSelParts : 1;
+    w.parts = o; o = align256(o + (w.n_parts > 1 ? (size_t)w.n_parts * sizeof(SelPart) : 0));
     w.total = o;
     return w;
 }
@@ -504,6 +507,8 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     sa.top_k = args->top_k; sa.kp = w.kp; sa.cand_keys = cand; sa.work = work; sa.collect = collect;
     sa.work_cap = w.work_cap; sa.collect_cap = w.collect_cap; sa.ent_J = entJ; sa.ent_flags = entF;
     sa.lo = lo; sa.collect_mode = 0; sa.res = R;
+    sa.parts = reinterpret_cast<SelPart *>(ws + w.parts);
+    sa.n_parts = w.n_parts;
 
     hipEvent_t ev0 = nullptr, ev1 = nullptr;
     MF_HIP(hipEventCreate(&ev0));
@@ -524,7 +529,7 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     MF_HIP2(launch_kth_candidate(cand, entJ, entF, w.kp, args->top_k, R, s));
     ca.phase = 1;
     MF_HIP2(launch_canonical(ca, (int)std::min<uint64_t>(w.work_cap, 1u << 20), true, s));
-    MF_HIP2(launch_select(sa, p->fc, args->d_omega, s));
+    MF_HIP2(launch_select(sa, s));
     DevResult h{};
     MF_HIP2(hipMemcpyAsync(&h, R, sizeof(DevResult), hipMemcpyDeviceToHost, s));
     MF_HIP2(hipStreamSynchronize(s));
@@ -553,7 +558,7 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
         ca.mask = nullptr;
         MF_HIP2(launch_canonical(ca, (int)std::min<uint64_t>((uint64_t)w.work_cap + w.collect_cap, 1u << 20), true, s));
         sa.collect_mode = 1;
-        MF_HIP2(launch_select(sa, p->fc, args->d_omega, s));
+        MF_HIP2(launch_select(sa, s));
         DevResult h2{};
         MF_HIP2(hipMemcpyAsync(&h2, R, sizeof(DevResult), hipMemcpyDeviceToHost, s));
         MF_HIP2(hipStreamSynchronize(s));

@@ -245,8 +245,13 @@ hipError_t launch_kth_candidate(const unsigned long long *cand_keys, const doubl
 }
 
 
+// MODE 0: one workgroup over every entry, then the result.  MODE 1: each
+// workgroup of a grid over a stride of the entries, its top-k, count and
+// checks to parts[blockIdx.x].  MODE 2: one workgroup merges the parts, then
+// the result.
+template <int MODE>
 __global__ void __launch_bounds__(kSelWaves * 64)
-select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
+select_kernel(const SelectArgs a, SelPart *parts, int n_parts)
 {
     __shared__ K128 lst[kSelWaves * 64];
     __shared__ unsigned long long s_feas;
@@ -256,8 +261,6 @@ select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
     DevResult *R = a.res;
     if (threadIdx.x == 0) { s_feas = 0; s_stat = 0; s_maxd = 0.0; }
     __syncthreads();
-    (void)fc;
-    (void)omega;
     const int64_t n_cand = a.collect_mode ? 0 : a.kp;
     const int64_t n_work = (int64_t)min(R->n_work, (unsigned long long)a.work_cap);
     const int64_t n_coll = a.collect_mode ? (int64_t)min(R->n_collect, (unsigned long long)a.collect_cap) : 0;
@@ -265,7 +268,18 @@ select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
     const int k = a.top_k;
     K128 slot = {0, 0}, thr = {0, 0};
     unsigned long long my_feas = 0;
-    for (int64_t base = (int64_t)wv * 64; base < n_ent; base += kSelWaves * 64) {
+    if (MODE == 2) {
+        // the parts: lists (sorted, zeros past k), counts, checks
+        for (int p = wv; p < n_parts; p += kSelWaves) list128_offer(slot, parts[p].keys[lane], lane, k, thr);
+        for (int p = threadIdx.x; p < n_parts; p += kSelWaves * 64) {
+            my_feas += parts[p].feas;
+            if (parts[p].stat) atomicOr(&s_stat, parts[p].stat);
+            atomicMax((unsigned long long *)&s_maxd, (unsigned long long)__double_as_longlong(parts[p].maxd));
+        }
+    }
+    const int64_t e_first = MODE == 1 ? ((int64_t)blockIdx.x * kSelWaves + wv) * 64 : (int64_t)wv * 64;
+    const int64_t e_step = MODE == 1 ? (int64_t)gridDim.x * kSelWaves * 64 : kSelWaves * 64;
+    for (int64_t base = MODE == 2 ? n_ent : e_first; base < n_ent; base += e_step) {
         const int64_t e = base + lane;
         K128 key = {0, 0};
         if (e < n_ent) {
@@ -300,6 +314,19 @@ select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
     if (my_feas) atomicAdd(&s_feas, my_feas);
     lst[wv * 64 + lane] = key_if(lane < k, slot);
     __syncthreads();
+    if (MODE == 1) {
+        if (wv == 0) {
+            for (int w = 1; w < kSelWaves; w++) list128_offer(slot, lst[w * 64 + lane], lane, k, thr);
+            SelPart &pt = parts[blockIdx.x];
+            pt.keys[lane] = key_if(lane < k, slot);
+            if (lane == 0) {
+                pt.feas = s_feas;
+                pt.stat = s_stat;
+                pt.maxd = s_maxd;
+            }
+        }
+        return;
+    }
     if (wv == 0) {
         for (int w = 1; w < kSelWaves; w++) list128_offer(slot, lst[w * 64 + lane], lane, k, thr);
         const int n_top = __popcll(__ballot(lane < k && nz128(slot)));
@@ -343,9 +370,14 @@ select_kernel(const SelectArgs a, const FastConst fc, const float *omega)
     }
 }
 
-hipError_t launch_select(const SelectArgs &a, const FastConst &fc, const float *omega, hipStream_t s)
+hipError_t launch_select(const SelectArgs &a, hipStream_t s)
 {
-    hipLaunchKernelGGL(select_kernel, dim3(1), dim3(kSelWaves * 64), 0, s, a, fc, omega);
+    if (a.n_parts <= 1) {
+        hipLaunchKernelGGL(select_kernel<0>, dim3(1), dim3(kSelWaves * 64), 0, s, a, (SelPart *)nullptr, 0);
+    } else {
+        hipLaunchKernelGGL(select_kernel<1>, dim3(a.n_parts), dim3(kSelWaves * 64), 0, s, a, a.parts, a.n_parts);
+        hipLaunchKernelGGL(select_kernel<2>, dim3(1), dim3(kSelWaves * 64), 0, s, a, a.parts, a.n_parts);
+    }
     return hipGetLastError();
 }
 

@@ -229,7 +229,17 @@ struct CanonArgs {
     ObjArgs obj;
 };
 
+// One workgroup's share of the exact top-k selection over a long entry list.
+struct SelPart {
+    K128 keys[MF_MAX_TOPK];     // sorted, zeros past k
+    unsigned long long feas;    // certified feasible work entries
+    double maxd;                // largest U - J over the fast candidates
+    uint32_t stat, pad;         // self-check bits
+};
+
 struct SelectArgs {
+    SelPart *parts;             // [n_parts] when the selection runs in two levels
+    int n_parts;                // <= 1: one workgroup
     int top_k, kp;
     const unsigned long long *cand_keys;   // [kp] fast candidates (0 = empty)
     const unsigned long long *work; const uint32_t *collect;
@@ -366,7 +376,7 @@ hipError_t launch_merge_lists(const unsigned long long *lists, int n_lists, int 
 hipError_t launch_canonical(const CanonArgs &a, int n_entries_max, bool search_mode, hipStream_t s);
 hipError_t launch_kth_candidate(const unsigned long long *cand_keys, const double *ent_J, const uint32_t *ent_flags,
                                 int kp, int k, DevResult *res, hipStream_t s);
-hipError_t launch_select(const SelectArgs &a, const FastConst &fc, const float *omega, hipStream_t s);
+hipError_t launch_select(const SelectArgs &a, hipStream_t s);
 size_t fixed_lds_bytes(int sumK, bool eq3);
 size_t static_lds_bytes(int n_steps, int sumK, int n_models, bool eq3);
 hipError_t launch_fixed_table(const FixedArgs &a, hipStream_t s);
@@ -376,6 +386,8 @@ int static_wgs_per_cu(const StaticArgs &a);
 int fixed_wgs_per_cu(const FixedArgs &a);
 hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 constexpr int64_t kGaWideMax = 8192;   // populations (S x P) up to this size take the wide fitness kernel
+constexpr int kSelParts = 128;            // workgroups of the two-level selection over long entry lists
+constexpr uint64_t kSelSingleMax = 1ull << 20;   // ranges up to this size select in one workgroup
 constexpr int kCanonWaves = 8;             // certification of few entries: waves (models) per workgroup, at most
 constexpr int kCanonFewEntries = 1024;     // index lists up to this length count as few
 constexpr int kGaWideWaves = 8;             // ... with up to this many waves (models) per workgroup

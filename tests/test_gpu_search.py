@@ -219,3 +219,26 @@ def test_range_splits_when_certification_list_fills(mf, orc, monkeypatch):
     assert g["n_feas"] == r["n_feas"] and g["n_vram"] == r["n_vram"]
     assert list(g["top_idx"]) == list(r["top_idx"])
     assert g["top_J"].tobytes() == r["top_J"].tobytes()
+
+
+def test_two_level_selection_on_long_ranges(mf, orc):
+    # ranges above 2^20 configurations select the exact top-k in two levels
+    # (a grid of partial lists, then one merge): a full search, and exact
+    # ties that force the collect pass through the same path
+    inst = synth.make_instance([17, 16, 16, 16, 16], seed=6, vram_quantile=0.6, sla_range=(0.3, 1.2))
+    assert inst.space_size > 2 ** 20
+    r = orc.Problem(inst).search(inst.sla, inst.omega, k=16)
+    g = mf.Problem(inst).search(inst.sla, inst.omega, k=16)
+    assert g["n_vram"] == r["n_vram"] and g["n_feas"] == r["n_feas"]
+    assert list(g["top_idx"]) == list(r["top_idx"])
+    assert g["top_J"].tobytes() == r["top_J"].tobytes()
+    for i in range(inst.n_models):
+        W1, b1, W2, b2, W3, b3 = inst.model_weights(i)
+        W3[1, :] = 0.0
+        b3[1] = 1.0
+    r = orc.Problem(inst).search(inst.sla, inst.omega, k=7)
+    g = mf.Problem(inst).search(inst.sla, inst.omega, k=7)
+    assert g["n_topk_collect"] > 0
+    assert g["n_feas"] == r["n_feas"]
+    assert list(g["top_idx"]) == list(r["top_idx"])
+    assert g["top_J"].tobytes() == r["top_J"].tobytes()
