@@ -192,7 +192,7 @@ canon_kernel(const CanonArgs a, const int search_mode)
 hipError_t launch_canonical(const CanonArgs &a, int n_entries_max, bool search_mode, hipStream_t s)
 {
     int grid = n_entries_max < 1 ? 1 : n_entries_max;
-    if (grid > 4096) grid = 4096;
+    if (grid > kCanonMaxGrid) grid = kCanonMaxGrid;
     const int sm = search_mode ? 1 : 0;
     const bool few = search_mode ? a.phase == 0 : n_entries_max <= kCanonFewEntries;
     if (!few) {

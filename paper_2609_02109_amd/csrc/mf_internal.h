@@ -388,6 +388,7 @@ hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s,
 constexpr int64_t kGaWideMax = 8192;   // populations (S x P) up to this size take the wide fitness kernel
 constexpr int kSelParts = 128;            // workgroups of the two-level selection over long entry lists
 constexpr uint64_t kSelSingleMax = 1ull << 20;   // ranges up to this size select in one workgroup
+constexpr int kCanonMaxGrid = 8192;        // certification workgroups (one wave each): 8 per SIMD
 constexpr int kCanonWaves = 8;             // certification of few entries: waves (models) per workgroup, at most
 constexpr int kCanonFewEntries = 1024;     // index lists up to this length count as few
 constexpr int kGaWideWaves = 8;             // ... with up to this many waves (models) per workgroup
