@@ -242,3 +242,60 @@ def test_two_level_selection_on_long_ranges(mf, orc):
     assert g["n_feas"] == r["n_feas"]
     assert list(g["top_idx"]) == list(r["top_idx"])
     assert g["top_J"].tobytes() == r["top_J"].tobytes()
+
+
+def test_search_argument_errors(mf, orc):
+    # every invalid argument is refused before any launch, with the status the
+    # header documents, and the problem still searches correctly afterwards
+    import ctypes as C
+    import torch
+    inst = synth.cfg1(1)
+    p = mf.Problem(inst)
+    d_sla = torch.as_tensor(inst.sla, dtype=torch.float32, device="cuda")
+    d_om = torch.as_tensor(inst.omega, dtype=torch.float32, device="cuda")
+
+    def args(**over):
+        a = dict(lo=0, hi=inst.space_size, top_k=4, flags=0, d_sla=d_sla.data_ptr(), d_omega=d_om.data_ptr(),
+                 d_mask=None, d_pred=None)
+        a.update(over)
+        return mf.SearchArgs(a["lo"], a["hi"], a["top_k"], a["flags"], a["d_sla"], a["d_omega"], a["d_mask"],
+                             a["d_pred"], mf.objective_args(None, inst.n_models))
+
+    def size(a):
+        n = C.c_size_t()
+        return mf.lib.mf_workspace_size(p.handle, C.byref(a), C.byref(n)), n.value
+
+    st, need = size(args())
+    assert st == mf.MF_OK and need > 0
+    ws = torch.empty(need + 256, dtype=torch.uint8, device="cuda")
+    assert ws.data_ptr() % 256 == 0
+    res = mf.Result()
+
+    def search(a, ptr=ws.data_ptr(), nbytes=need):
+        return mf.lib.mf_search(p.handle, C.byref(a), C.c_void_p(ptr), C.c_size_t(nbytes),
+                                C.c_void_p(torch.cuda.current_stream().cuda_stream), C.byref(res))
+
+    cases = [
+        (args(top_k=0), mf.MF_EINVAL),
+        (args(top_k=65), mf.MF_EINVAL),
+        (args(lo=10, hi=9), mf.MF_EINVAL),
+        (args(hi=inst.space_size + 1), mf.MF_EOVERFLOW),
+        (args(d_sla=None), mf.MF_EINVAL),
+        (args(d_omega=None), mf.MF_EINVAL),
+        (args(flags=1 << 7), mf.MF_EINVAL),
+        (args(flags=mf.MF_DUMP), mf.MF_EINVAL),          # dump without its buffers
+    ]
+    for a, want in cases:
+        assert size(a)[0] == want
+        assert search(a) == want
+    assert search(args(), nbytes=need - 1) == mf.MF_ENOMEM
+    assert search(args(), ptr=ws.data_ptr() + 128) == mf.MF_EINVAL   # workspace not 256-byte aligned
+    assert search(args(), ptr=0) == mf.MF_EINVAL
+    assert mf.lib.mf_search(p.handle, C.byref(args()), C.c_void_p(ws.data_ptr()), C.c_size_t(need), None,
+                            None) == mf.MF_EINVAL
+    assert search(args()) == mf.MF_OK
+    r = orc.Problem(inst).search(inst.sla, inst.omega, k=4)
+    assert res.n_feas == r["n_feas"] and res.n_vram == r["n_vram"]
+    assert [int(x) for x in res.top_idx[:res.n_top]] == list(r["top_idx"])
+    assert all(x == 2 ** 64 - 1 for x in res.top_idx[res.n_top:])
+    p.close()
