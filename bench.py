@@ -251,8 +251,8 @@ def bench_ga(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--workload", choices=["n6", "ga", "n8", "fixed", "protocol"], default="n6",
@@ -299,7 +299,7 @@ def main():
     flops = algorithmic_flops_per_config(inst) * n
     achieved = flops / (kms * 1e-3) / 1e12
     inst5 = synth.cfg1(args.seed)
-    ms5, kms5, r5 = measure_search(mf, torch, inst5, 16, max(args.steps, 20), max(args.warmup, 3))
+    ms5, kms5, r5 = measure_search(mf, torch, inst5, 16, max(args.steps, 200), max(args.warmup, 20))
     log(f"search: {ms:.2f} ms/step, fast kernel {kms:.2f} ms, n_feas={r.n_feas} "
         f"n_flagged={r.n_flagged} argmax={r.top_idx[0]} J={r.top_J[0]!r}")
 
