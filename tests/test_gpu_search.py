@@ -299,3 +299,23 @@ def test_search_argument_errors(mf, orc):
     assert [int(x) for x in res.top_idx[:res.n_top]] == list(r["top_idx"])
     assert all(x == 2 ** 64 - 1 for x in res.top_idx[res.n_top:])
     p.close()
+
+
+def test_repeated_runs_are_bit_identical(mf):
+    # the same search twice, and once more after other work on the problem:
+    # counts, top-k, masks and fast-path predictions identical byte for byte
+    inst = synth.cfg2(2)
+    p = mf.Problem(inst)
+    lo, hi = 12_345_678, 12_345_678 + 700_001
+    a = p.search(inst.sla, inst.omega, k=16, lo=lo, hi=hi, dump=True)
+    b = p.search(inst.sla, inst.omega, k=16, lo=lo, hi=hi, dump=True)
+    p.search(inst.sla * 1.1, inst.omega, k=64, lo=0, hi=3_000_000)
+    c = p.search(inst.sla, inst.omega, k=16, lo=lo, hi=hi, dump=True)
+    for x in (b, c):
+        for key in ("n_eval", "n_vram", "n_feas", "n_flagged"):
+            assert x[key] == a[key]
+        assert x["top_idx"].tobytes() == a["top_idx"].tobytes()
+        assert x["top_J"].tobytes() == a["top_J"].tobytes()
+        assert x["mask"].cpu().numpy().tobytes() == a["mask"].cpu().numpy().tobytes()
+        assert x["pred"].cpu().numpy().tobytes() == a["pred"].cpu().numpy().tobytes()
+    p.close()

@@ -1,0 +1,90 @@
+"""The seeded input generator: determinism, value grids and ranges, weight
+scales, workload shapes and the N=5 VRAM cap (CPU only; the generator holds
+none of the method's arithmetic)."""
+import itertools
+
+import numpy as np
+import pytest
+
+from paper_2609_02109_amd import synth
+
+
+def _arrays(inst):
+    return [inst.features, inst.weights, inst.sla, inst.omega, np.float32(inst.vram_cap), inst.n_options]
+
+
+def test_same_seed_same_instance_other_seed_differs():
+    a = synth.make_instance([5, 4, 3], 12, 6, 64, 64, seed=11, vram_quantile=0.6)
+    b = synth.make_instance([5, 4, 3], 12, 6, 64, 64, seed=11, vram_quantile=0.6)
+    c = synth.make_instance([5, 4, 3], 12, 6, 64, 64, seed=12, vram_quantile=0.6)
+    for x, y in zip(_arrays(a), _arrays(b)):
+        assert np.asarray(x).tobytes() == np.asarray(y).tobytes()
+    assert a.features.tobytes() != c.features.tobytes()
+    assert a.weights.tobytes() != c.weights.tobytes()
+
+
+@pytest.mark.parametrize("maker", [synth.cfg1, synth.cfg2, synth.cfg4])
+def test_feature_grid_and_ranges(maker):
+    inst = maker(0)
+    f = inst.features.astype(np.float64)
+    # every value sits on the 2^-14 grid, so aggregate sums stay exact in fp32
+    assert np.all(f * 2.0 ** 14 == np.round(f * 2.0 ** 14))
+    llm, vis, lb, sm, vr, bw = (f[:, synth.COL_LLM], f[:, synth.COL_VIS], f[:, synth.COL_LOG2B],
+                                f[:, synth.COL_SM], f[:, synth.COL_VRAM], f[:, synth.COL_BW])
+    assert set(np.unique(llm)) <= {0.0, 1.0} and np.all(llm + vis == 1.0)
+    assert set(np.unique(lb)) <= set(float(v) for v in range(6))
+    g = 2.0 ** -15
+    assert sm.min() >= 0.1 - g and sm.max() <= 1.0 + g
+    assert vr.min() >= 1.0 - g and vr.max() <= 40.0 + g
+    assert bw.min() >= 0.05 - g and bw.max() <= 0.6 + g
+    assert f[:, 6:].min() >= 0.0 and f[:, 6:].max() <= 1.0
+    # the first ceil(N/2) models are language models
+    offs = np.concatenate([[0], np.cumsum(inst.n_options)])
+    N = inst.n_models
+    for i in range(N):
+        assert np.all(llm[offs[i]:offs[i + 1]] == (1.0 if i < (N + 1) // 2 else 0.0))
+
+
+def test_weight_scales_and_bf16_values():
+    inst = synth.cfg4(0)
+    H, nin = inst.hidden1, inst.n_local + inst.n_agg
+    W1, b1, W2, b2, W3, b3 = inst.model_weights(3)
+    # N(0, 1/fan_in): sample standard deviations within a few percent
+    assert abs(np.std(W2) * np.sqrt(H) - 1.0) < 0.02
+    assert abs(np.std(W3) * np.sqrt(H) - 1.0) < 0.15
+    assert np.all(b2 == 0.0) and np.all(b3 == 0.0)
+    # bf16 weights: every value has a zero low half as an fp32 bit pattern
+    for w in (W1, W2, W3):
+        assert np.all((np.ascontiguousarray(w, np.float32).view(np.uint32) & 0xFFFF) == 0)
+    assert W1.shape == (H, nin) and W2.shape == (H, H) and W3.shape == (2, H)
+
+
+def test_workload_shapes():
+    assert synth.cfg0(0).space_size == 36
+    assert synth.cfg1(0).space_size == 104_976
+    assert list(synth.cfg1(0).n_options) == [12, 12, 9, 9, 9]
+    assert synth.cfg2(0).space_size == 24 ** 6 == 191_102_976
+    assert synth.cfg4(0).space_size == 2 ** 32
+    c2, c4 = synth.cfg2(0), synth.cfg4(0)
+    assert (c2.n_local, c2.n_agg, c2.hidden1, c2.vram_cap) == (16, 6, 64, 200.0)
+    assert (c4.n_local, c4.n_agg, c4.hidden1, c4.vram_cap, c4.dtype) == (32, 8, 256, 288.0, "bf16")
+    assert synth.cfg0(0).vram_cap == 80.0
+
+
+@pytest.mark.parametrize("seed,n_vram", [(0, 77_751), (1, 78_393), (2, 78_825)])
+def test_n5_cap_admits_about_the_papers_78732(seed, n_vram):
+    # the cap sits at the 75th percentile of the normal approximation of the
+    # joint VRAM sum; counted here by brute force over all 104,976 sums
+    inst = synth.cfg1(seed)
+    offs = np.concatenate([[0], np.cumsum(inst.n_options)])
+    cols = [inst.features[offs[i]:offs[i + 1], synth.COL_VRAM].astype(np.float64)
+            for i in range(inst.n_models)]
+    sums = np.zeros(1)
+    for c in cols:
+        sums = (sums[:, None] + c[None, :]).ravel()
+    count = int(np.count_nonzero(sums <= inst.vram_cap))
+    assert count == n_vram
+    assert abs(count - 78_732) / 78_732 < 0.02
+    # itertools order agrees with the broadcast order used above
+    first = list(itertools.islice(itertools.product(*[range(k) for k in inst.n_options]), 3))
+    assert sums[2] == sum(cols[i][first[2][i]] for i in range(inst.n_models))
