@@ -207,6 +207,9 @@ __global__ void __launch_bounds__(256) ga_fitness_kernel(const GAConst c, int S,
             }
         }
         double y0 = b3[0], y1 = b3[1];
+        // four layer-2 chains in flight (each still in input order; the
+        // layer-3 chains take them in unit order)
+#pragma unroll 4
         for (int v = 0; v < H2; v++) {
             double a = b2[v];
 #pragma unroll
@@ -237,14 +240,11 @@ __global__ void __launch_bounds__(256) ga_fitness_kernel(const GAConst c, int S,
     fit[t] = (vram_ok && sla_ok) ? J : -INFINITY;
 }
 
-// Canonical fp64 fitness, one 64-lane workgroup per individual (small
-// populations, or shapes the one-lane kernel is not built for): the
-// certification kernel's evaluation, lanes over hidden units, model after
-// model.  The same canonical J as the one-lane kernel, bit for bit.
-// One workgroup per individual (small populations, and shapes the one-lane
-// kernel does not take): wave w runs the canonical forward of models w,
-// w + W, ... (W waves), each on its own LDS scratch; lane 0 then combines the
-// models' predictions in model order, as in the one-lane kernel.  STAGE: the
+// Canonical fp64 fitness, one workgroup per individual (small populations,
+// and shapes the one-lane kernel does not take): wave w runs the canonical
+// forward of models w, w + W, ... (W waves), each on its own LDS scratch; lane
+// 0 then combines the models' predictions in model order, so J equals the
+// one-lane kernel's bit for bit.  STAGE: the
 // canonical weights of every model are first copied to LDS.  Dynamic LDS:
 // [staged weights][W x (H1 + H2 + nin) doubles].
 template <bool BF16, bool STAGE>
