@@ -52,14 +52,30 @@ __device__ __forceinline__ uint64_t ga_below(uint64_t r, uint64_t n) { return ((
 
 // ---------------------------------------------------------------- feasible list
 
+// Mixed-radix digits of a joint index, model 0 most significant (the decode of
+// Eq. 1's configuration vector); 32-bit divisions when the space fits 32 bits.
+__device__ __forceinline__ void ga_digits(const GAConst &c, uint64_t idx, int32_t *d)
+{
+    if (c.space <= 0x100000000ull) {
+        uint32_t x = (uint32_t)idx;
+        for (int i = c.N - 1; i >= 0; i--) {
+            const uint32_t k = (uint32_t)c.K[i], q = x / k;
+            d[i] = (int32_t)(x - q * k);
+            x = q;
+        }
+    } else {
+        for (int i = c.N - 1; i >= 0; i--) {
+            d[i] = (int32_t)(idx % (uint64_t)c.K[i]);
+            idx /= (uint64_t)c.K[i];
+        }
+    }
+}
+
 __device__ __forceinline__ bool vram_feasible(const GAConst &c, uint64_t idx)
 {
     // fp32 sum of the VRAM column in model order (the aggregate slot's value)
     int32_t d[kMaxN];
-    for (int i = c.N - 1; i >= 0; i--) {
-        d[i] = (int32_t)(idx % (uint64_t)c.K[i]);
-        idx /= (uint64_t)c.K[i];
-    }
+    ga_digits(c, idx, d);
     float s = 0.f;
     for (int i = 0; i < c.N; i++) s = s + c.features[(int64_t)(c.opt_off[i] + d[i]) * c.L + c.vram_col];
     return (double)s <= (double)c.vram_cap;
@@ -154,12 +170,8 @@ __global__ void __launch_bounds__(256) ga_fitness_kernel(const GAConst c, int S,
     if (t >= (int64_t)S * P) return;
     const int s = (int)(t / P);
     const int N = c.N, L = c.L;
-    uint64_t idx = pop[t];
     int32_t d[kMaxN];
-    for (int i = N - 1; i >= 0; i--) {
-        d[i] = (int32_t)(idx % (uint64_t)c.K[i]);
-        idx /= (uint64_t)c.K[i];
-    }
+    ga_digits(c, pop[t], d);
     double z[NIN];
     // aggregate: fp32, model order, each slot
 #pragma unroll
@@ -283,13 +295,7 @@ __global__ void __launch_bounds__(64 * kGaWideWaves) ga_fitness_wide_kernel(cons
     for (int64_t t = blockIdx.x; t < (int64_t)S * P; t += gridDim.x) {
         const int s = (int)(t / P);
         __syncthreads();
-        if (tid == 0) {
-            uint64_t idx = pop[t];
-            for (int i = N - 1; i >= 0; i--) {
-                d[i] = (int32_t)(idx % (uint64_t)c.K[i]);
-                idx /= (uint64_t)c.K[i];
-            }
-        }
+        if (tid == 0) ga_digits(c, pop[t], d);
         __syncthreads();
         // aggregate slot k (fp32, model order); the VRAM slot decides the cap
         if (tid < A) {
@@ -492,11 +498,9 @@ __global__ void __launch_bounds__(kOpThreads) ga_ops_kernel(const GAConst c, uin
                 ipar = i;
             }
         }
-        uint64_t x = ipar;
-        for (int i = N - 1; i >= 0; i--) {
-            pg[t * N + i] = (int32_t)(x % (uint64_t)c.K[i]);
-            x /= (uint64_t)c.K[i];
-        }
+        int32_t dp[kMaxN];
+        ga_digits(c, ipar, dp);
+        for (int i = 0; i < N; i++) pg[t * N + i] = dp[i];
     }
     __syncthreads();
     if (!act) return;
