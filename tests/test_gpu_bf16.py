@@ -109,7 +109,7 @@ def test_bf16_n8_full_space_properties(mf, orc):
     # the whole 2^32-configuration space: the top-64 are feasible with the
     # oracle's J bit for bit, sorted by (J desc, index asc), and no sampled
     # feasible configuration, and no feasible configuration one option from a
-    # top-64 member or two options from the argmax, beats the 64th
+    # top-64 member or two options from one of the best four, beats the 64th
     inst = synth.cfg4(0)
     print(f"[bf16] full N=8 space {inst.space_size}", flush=True)
     p = mf.Problem(inst)
@@ -134,7 +134,8 @@ def test_bf16_n8_full_space_properties(mf, orc):
     sd = np.sqrt(f * (1 - f) / len(samp))
     assert abs(feas.mean() - f) <= 6 * sd + 1e-3
     # the nearest competitors: every configuration one option away from a
-    # top-64 member, and two options away from the argmax (the oracle on each)
+    # top-64 member, and two options away from one of the best four (the
+    # oracle on each)
     K = [int(k) for k in inst.n_options]
     strides = [int(np.prod(K[i + 1:])) for i in range(len(K))]
 
@@ -148,13 +149,14 @@ def test_bf16_n8_full_space_properties(mf, orc):
             for o in range(K[i]):
                 if o != d[i]:
                     near.add(int(x) + (o - d[i]) * strides[i])
-    d0 = digits(top[0])
-    for i in range(len(K)):
-        for j in range(i + 1, len(K)):
-            for oi in range(K[i]):
-                for oj in range(K[j]):
-                    if oi != d0[i] and oj != d0[j]:
-                        near.add(int(top[0]) + (oi - d0[i]) * strides[i] + (oj - d0[j]) * strides[j])
+    for x in top[:4]:
+        d0 = digits(x)
+        for i in range(len(K)):
+            for j in range(i + 1, len(K)):
+                for oi in range(K[i]):
+                    for oj in range(K[j]):
+                        if oi != d0[i] and oj != d0[j]:
+                            near.add(int(x) + (oi - d0[i]) * strides[i] + (oj - d0[j]) * strides[j])
     near = np.array(sorted(near - set(int(t) for t in top)), dtype=np.uint64)
     rn = orc.Problem(inst).eval_list(near, inst.sla, inst.omega)
     fn = (rn["flags"] & 4) != 0
