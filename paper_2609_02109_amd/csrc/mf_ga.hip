@@ -378,9 +378,11 @@ inline size_t ops_lds_bytes(int tk, int N)
 
 // Operators: a scenario's pairs are spread over ceil((P/2) / kOpPairs)
 // workgroups; tournaments read fitness and population from global memory.
-// The first workgroup of a scenario finds the elite (slot 0 of the next
-// generation) and updates the best ever.  At g == gens the final population
-// is copied out.  The pairs' Philox blocks are first computed by all threads
+// The elite (slot 0 of the next generation, which no child writes) and the
+// best ever are found by the first operator workgroup of a scenario, or, for
+// populations of at most four operator workgroups, by one more workgroup
+// beside them (there the elite's reduction would otherwise sit on the critical
+// path).  At g == gens the final population is copied out.  The pairs' Philox blocks are first computed by all threads
 // together (each block once, its four words used in order); then, in each
 // team of lanes, lane t runs tournament t and decodes parent t, and builds
 // child t (crossover, mutation, repair).
@@ -389,13 +391,16 @@ __global__ void __launch_bounds__(kOpThreads) ga_ops_kernel(const GAConst c, uin
                                                             const uint32_t *fl, const unsigned long long *n_fl_ptr,
                                                             const uint64_t *pop, const double *fit, uint64_t *next,
                                                             double *best_J, uint64_t *best_idx, uint64_t *final_pop,
-                                                            int wgs_per_scen)
+                                                            int wgs_per_scen, int elite_wg)
 {
     extern __shared__ uint64_t ops_dyn[];
     __shared__ int red[kOpThreads];
     __shared__ double red_f[kOpThreads];
     __shared__ uint64_t red_i[kOpThreads];
-    const int s = blockIdx.x / wgs_per_scen, pb = blockIdx.x % wgs_per_scen, tid = threadIdx.x;
+    // per scenario: wgs_per_scen operator workgroups, then (elite_wg) one
+    // workgroup for the elite alone; otherwise operator workgroup 0 finds it
+    const int wgs_all = wgs_per_scen + elite_wg;
+    const int s = blockIdx.x / wgs_all, pb = blockIdx.x % wgs_all, tid = threadIdx.x;
     const int N = c.N;
     const OpBlocks ob(tk, N);
     uint64_t *words = ops_dyn;                                                                // [kOpPairs][total][4]
@@ -404,12 +409,12 @@ __global__ void __launch_bounds__(kOpThreads) ga_ops_kernel(const GAConst c, uin
     const double *fs = fit + (int64_t)s * P;
     uint64_t *ns = next + (int64_t)s * P;
     const unsigned long long n_fl = *n_fl_ptr;
-    if (gen == gens) {
+    if (gen == gens && pb < wgs_per_scen) {
         if (final_pop)
             for (int j = pb * kOpThreads + tid; j < P; j += wgs_per_scen * kOpThreads)
                 final_pop[(int64_t)s * P + j] = n_fl ? ps[j] : ~0ull;
     }
-    if (pb == 0) {
+    if (pb == (elite_wg ? wgs_per_scen : 0)) {
         // elite: best (f desc, index asc, slot asc), reduced in LDS
         int b = -1;
         double fb = 0.0;
@@ -449,6 +454,7 @@ __global__ void __launch_bounds__(kOpThreads) ga_ops_kernel(const GAConst c, uin
             }
             if (gen != gens) ns[0] = ie;
         }
+        if (elite_wg) return;
     }
     if (gen == gens) return;
     const uint64_t g1 = (uint64_t)gen + 1, sc = (uint64_t)s;
@@ -609,8 +615,9 @@ hipError_t launch_ga_ops(const GAConst &c, uint64_t seed, int S, int P, int gen,
     const size_t lds = ops_lds_bytes(tk, c.N);
     const hipError_t e = ensure_dyn_lds((const void *)ga_ops_kernel, lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(ga_ops_kernel, dim3(S * wgs), dim3(kOpThreads), lds, st, c, seed, P, gen, gens, tk, p_cx,
-                       p_swap, p_mut, fl, n_fl, pop, fit, next, best_J, best_idx, final_pop, wgs);
+    const int elite_wg = wgs <= 4 ? 1 : 0;
+    hipLaunchKernelGGL(ga_ops_kernel, dim3(S * (wgs + elite_wg)), dim3(kOpThreads), lds, st, c, seed, P, gen, gens, tk,
+                       p_cx, p_swap, p_mut, fl, n_fl, pop, fit, next, best_J, best_idx, final_pop, wgs, elite_wg);
     return hipGetLastError();
 }
 
