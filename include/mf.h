@@ -125,23 +125,39 @@ typedef struct {
     int32_t output_act;          /* mf_activation of both surrogate outputs (zero: identity) */
 } mf_desc;
 
-/* Create a problem.  d_features: float [sum K_i][L].  d_weights: float
- * [N][S] with S = H1*(L+A) + H1 + H2*H1 + H2 + 2*H2 + 2, per model packed as
- * W1[H1][L+A], b1[H1], W2[H2][H1], b2[H2], W3[2][H2], b3[2] (row-major).
- * Both are copied: the caller may free them after the call returns.
- * Validates every value is finite (and bf16-representable for MF_BF16 W*),
- * derives the fast path's error bounds, and builds the device-resident
- * tables (per-option first-layer precompute included) on `stream`; returns
- * after the stream has finished that work.  The library allocates the
- * problem's device tables itself (freed by mf_problem_destroy). */
+/* Bytes of caller-owned device memory a problem of this description needs
+ * for its tables (the option sets Lambda_i = V_i x P_i of Section II as
+ * option rows, one surrogate g_i per model, Section III-B / Eq. 6, and the
+ * fast paths' images of both).  A function of the description's shape only:
+ * the pointers to option counts and aggregate columns are read, no weights.
+ * Errors: MF_EINVAL / MF_EOVERFLOW as mf_problem_create. */
+mf_status mf_problem_bytes(const mf_desc *desc, size_t *bytes);
+
+/* Create a problem: the option sets Lambda_i (Section II), one row of L local
+ * features per option, and the per-model surrogates g_i of Eq. 6 (Section
+ * III-B).  d_features: float [sum K_i][L].  d_weights: float [N][S] with
+ * S = H1*(L+A) + H1 + H2*H1 + H2 + 2*H2 + 2, per model packed as W1[H1][L+A],
+ * b1[H1], W2[H2][H1], b2[H2], W3[2][H2], b3[2] (row-major).  Both are read on
+ * `stream` (device or host memory) and copied: the caller may free them after
+ * the call returns.  d_tables: caller-owned device memory of at least
+ * mf_problem_bytes(desc) bytes, 256-byte aligned (else MF_ENOMEM / MF_EINVAL),
+ * which the problem uses for all its tables; it must stay allocated and
+ * unmodified until mf_problem_destroy.  The library allocates no device
+ * memory.  Validates every value is finite (and bf16-representable for
+ * MF_BF16 W*), derives the fast path's error bounds, and writes the tables
+ * (per-option first-layer precompute included) on `stream`; returns after the
+ * stream has finished that work. */
 mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const float *d_weights,
-                            void *stream, mf_problem **out);
+                            void *d_tables, size_t table_bytes, void *stream, mf_problem **out);
+/* Releases the host state; d_tables is the caller's to free afterwards. */
 void mf_problem_destroy(mf_problem *p);
 
-/* |Lambda| = prod K_i. */
+/* |Lambda| = prod K_i, the size of the joint configuration space of Eq. 1. */
 mf_status mf_space_size(const mf_problem *p, uint64_t *out);
 
-/* Host helper: digits[N] of joint index idx (idx < |Lambda|). */
+/* Host helper: the options (lambda_0, ..., lambda_{N-1}) of joint index idx
+ * (Eq. 1: lexicographic order, model 0 most significant) into digits[N];
+ * MF_EINVAL when idx >= |Lambda|. */
 mf_status mf_decode(const mf_problem *p, uint64_t idx, int32_t *h_digits);
 
 /* ---------------------------------------------------------------- search */
@@ -201,6 +217,12 @@ typedef struct {
      * limits), d_pred receives the canonical (lat, thr) rounded to fp32, mask
      * bit3 and n_flagged / n_topk_collect / n_splits stay 0. */
     float state[MF_MAX_AGG];
+    /* Upper bound on the entries of the certification list (configurations
+     * whose service decision the fast path leaves to the canonical
+     * re-evaluation); 0 keeps the default (1/128 of the range, at least 2^20,
+     * at most 2^26).  A smaller list shrinks the workspace; a range that fills
+     * it is split in halves and searched again (n_splits). */
+    uint32_t worklist_cap;
 } mf_search_args;
 
 typedef struct {
@@ -276,13 +298,17 @@ mf_status mf_eval_static(mf_problem *p, const mf_static_args *args, const uint64
 
 /* ------------------------------------------------------------ evaluation */
 
-/* Fast-path (fp32 MFMA) predictions of an index list, as the search kernel
- * computes them.  d_idx: device uint64 [n], each < |Lambda|.  d_pred: device
- * float [n][N][2] (lat, thr).  Enqueues only. */
+/* Fast-path predictions of an index list: (lat_i, thr_i) = g_i([x_i | a])
+ * of Eq. 6 for every model of each joint configuration (aggregate derived
+ * from the configuration, Section II), as the search kernel computes them
+ * (fp32, or bf16 products with fp32 accumulation, on MFMA).  d_idx: device
+ * uint64 [n], each < |Lambda|.  d_pred: device float [n][N][2] (lat, thr).
+ * Enqueues only. */
 mf_status mf_eval_fast(mf_problem *p, const uint64_t *d_idx, int64_t n, float *d_pred, void *stream);
 
 /* Canonical fp64 evaluation of an index list (the semantics results are
- * defined by).  d_pred: device double [n][N][2]; d_J: device double [n]
+ * defined by): the predictions of Eq. 6, the constraints of Eq. 4 and the
+ * objective J of Section II for each joint configuration.  d_pred: device double [n][N][2]; d_J: device double [n]
  * (-inf when infeasible); d_flags: device uint32 [n] (bit0 VRAM ok, bit1 all
  * latency bounds met, bit2 feasible, bit 8+i model i misses its bound).  Any
  * output may be NULL.  Enqueues only. */

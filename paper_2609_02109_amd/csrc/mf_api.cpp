@@ -19,6 +19,13 @@
 
 using namespace mfi;
 
+namespace {
+// Start and end events of the timed kernel of one search.
+struct EventPair {
+    hipEvent_t a = nullptr, b = nullptr;
+};
+}  // namespace
+
 struct mf_problem {
     int N = 0, L = 0, A = 0, H1 = 0, H2 = 0;
     bool bf16 = false;
@@ -32,8 +39,8 @@ struct mf_problem {
     bool fast_ok = false;
     int num_cus = 0;
     int device = 0;
-    // device memory (one allocation)
-    void *d_mem = nullptr;
+    // device tables: pointers into the caller's buffer (borrowed until destroy)
+    void *d_tables = nullptr;
     float4 *d_image = nullptr;
     float *d_canon = nullptr, *d_features = nullptr, *d_zeros = nullptr, *d_centre = nullptr;
     double *d_w64 = nullptr;     // packed weights as fp64 (GA fitness)
@@ -51,6 +58,9 @@ struct mf_problem {
     Bf16Const bcst{};
     float4 *d_bmodels = nullptr, *d_bg = nullptr;
     float *d_phat = nullptr;
+    // timing events: created with the problem, handed to one call at a time
+    std::mutex ev_mu;
+    std::vector<EventPair> ev_free, ev_all;
 };
 
 namespace mfi {
@@ -74,6 +84,49 @@ hipError_t ensure_dyn_lds(const void *fn, size_t bytes)
 }  // namespace mfi
 
 namespace {
+
+bool create_event_pair(EventPair &e)
+{
+    if (hipEventCreate(&e.a) != hipSuccess) return false;
+    if (hipEventCreate(&e.b) != hipSuccess) {
+        (void)hipEventDestroy(e.a);
+        e.a = nullptr;
+        return false;
+    }
+    return true;
+}
+
+// A pair of the problem's timing events held by one call.  A call finding
+// none free creates one more pair for the pool when it may (concurrent calls
+// on several streams); otherwise it runs untimed.
+class EventLease {
+public:
+    EventLease(mf_problem *p, bool may_create) : p_(p)
+    {
+        std::lock_guard<std::mutex> g(p->ev_mu);
+        if (!p->ev_free.empty()) {
+            ev_ = p->ev_free.back();
+            p->ev_free.pop_back();
+        } else if (may_create && create_event_pair(ev_)) {
+            p->ev_all.push_back(ev_);
+        }
+    }
+    ~EventLease()
+    {
+        if (!ev_.a) return;
+        std::lock_guard<std::mutex> g(p_->ev_mu);
+        p_->ev_free.push_back(ev_);
+    }
+    EventLease(const EventLease &) = delete;
+    EventLease &operator=(const EventLease &) = delete;
+    hipEvent_t start() const { return ev_.a; }
+    hipEvent_t stop() const { return ev_.b; }
+
+private:
+    mf_problem *p_;
+    EventPair ev_{};
+};
+
 
 constexpr double kU32 = 0x1p-24;   // fp32 unit roundoff (round to nearest)
 constexpr double kU64 = 0x1p-53;   // fp64 unit roundoff
@@ -315,7 +368,7 @@ struct WsLayout {
     int kp, grid, waves, n_parts;
 };
 
-WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k)
+WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k, uint32_t worklist_cap)
 {
     WsLayout w{};
     if (p.bf_ok) {
@@ -335,11 +388,8 @@ WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k)
     // more than the range), at most 2^26
     const uint64_t want = std::min<uint64_t>(std::max<uint64_t>(n / 128, (uint64_t)kDefaultWorklist), 1ull << 26);
     uint64_t cap = std::max<uint64_t>(std::min<uint64_t>(want, n), 1024);
-    // MF_WORKLIST_CAP shrinks the certification list (tests of the range-split path)
-    if (const char *env = std::getenv("MF_WORKLIST_CAP")) {
-        const long long v = std::atoll(env);
-        if (v >= 1) cap = std::min<uint64_t>(cap, (uint64_t)v);
-    }
+    // the caller may bound the list (a full list splits the range)
+    if (worklist_cap >= 1) cap = std::min<uint64_t>(cap, (uint64_t)worklist_cap);
     w.work_cap = (uint32_t)cap;
     w.collect_cap = (uint32_t)std::max<uint64_t>(std::min<uint64_t>((uint64_t)kDefaultWorklist, n), 1024);
     size_t o = 0;
@@ -450,9 +500,9 @@ enum RangeOutcome { kRangeOk, kRangeSplit };
 
 // One launch set over [lo, lo + n), n <= 2^32.
 mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint64_t n, char *ws, hipStream_t s,
-                    mf_result &out, RangeOutcome &outcome)
+                    const EventLease &ev, mf_result &out, RangeOutcome &outcome)
 {
-    const WsLayout w = ws_layout(*p, n, args->top_k);
+    const WsLayout w = ws_layout(*p, n, args->top_k, args->worklist_cap);
     DevResult *R = reinterpret_cast<DevResult *>(ws + w.res);
     unsigned long long *work = reinterpret_cast<unsigned long long *>(ws + w.work);
     float *workJ = reinterpret_cast<float *>(ws + w.workJ);
@@ -510,19 +560,16 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     sa.parts = reinterpret_cast<SelPart *>(ws + w.parts);
     sa.n_parts = w.n_parts;
 
-    hipEvent_t ev0 = nullptr, ev1 = nullptr;
-    MF_HIP(hipEventCreate(&ev0));
-    if (hipEventCreate(&ev1) != hipSuccess) { (void)hipEventDestroy(ev0); return MF_EDEVICE; }
-    auto cleanup = [&]() { (void)hipEventDestroy(ev0); (void)hipEventDestroy(ev1); };
+    hipEvent_t ev0 = ev.start(), ev1 = ev.stop();
 #define MF_HIP2(x)                                  \
     do {                                            \
-        if ((x) != hipSuccess) { cleanup(); return MF_EDEVICE; } \
+        if ((x) != hipSuccess) return MF_EDEVICE;   \
     } while (0)
 
     MF_HIP2(hipMemsetAsync(R, 0, sizeof(DevResult), s));
-    MF_HIP2(hipEventRecord(ev0, s));
+    if (ev0) MF_HIP2(hipEventRecord(ev0, s));
     MF_HIP2(launch_fast_path(p, fa, w.grid, w.kp, kModeSearch, s));
-    MF_HIP2(hipEventRecord(ev1, s));
+    if (ev1) MF_HIP2(hipEventRecord(ev1, s));
     MF_HIP2(launch_merge_lists(lists, w.grid, w.kp, cand, counts, &R->n_vram, s));
     ca.phase = 0;
     MF_HIP2(launch_canonical(ca, w.kp, true, s));
@@ -534,14 +581,13 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     MF_HIP2(hipMemcpyAsync(&h, R, sizeof(DevResult), hipMemcpyDeviceToHost, s));
     MF_HIP2(hipStreamSynchronize(s));
     float ms = 0.f;
-    MF_HIP2(hipEventElapsedTime(&ms, ev0, ev1));
+    if (ev0) MF_HIP2(hipEventElapsedTime(&ms, ev0, ev1));
 
     if (h.status & kStatWorkOverflow) {
-        cleanup();
         outcome = kRangeSplit;
         return MF_OK;
     }
-    if (h.status & kStatSelfCheck) { cleanup(); return MF_EINTERNAL; }
+    if (h.status & kStatSelfCheck) return MF_EINTERNAL;
     uint64_t n_collect = 0;
     if (!(h.status & kStatVerified)) {
         // top-k fallback: gather every sure-feasible configuration whose fast
@@ -550,9 +596,9 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
         fa.mask = nullptr;
         fa.pred = nullptr;
         MF_HIP2(hipMemsetAsync(&R->n_collect, 0, sizeof(unsigned long long), s));
-        MF_HIP2(hipEventRecord(ev0, s));
+        if (ev0) MF_HIP2(hipEventRecord(ev0, s));
         MF_HIP2(launch_fast_path(p, fa, w.grid, w.kp, kModeCollect, s));
-        MF_HIP2(hipEventRecord(ev1, s));
+        if (ev1) MF_HIP2(hipEventRecord(ev1, s));
         ca.collect_mode = 1;
         ca.phase = 1;
         ca.mask = nullptr;
@@ -563,10 +609,9 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
         MF_HIP2(hipMemcpyAsync(&h2, R, sizeof(DevResult), hipMemcpyDeviceToHost, s));
         MF_HIP2(hipStreamSynchronize(s));
         float ms2 = 0.f;
-        MF_HIP2(hipEventElapsedTime(&ms2, ev0, ev1));
+        if (ev0) MF_HIP2(hipEventElapsedTime(&ms2, ev0, ev1));
         ms += ms2;
         if (h2.status & kStatCollectOverflow) {
-            cleanup();
             outcome = kRangeSplit;
             return MF_OK;
         }
@@ -575,7 +620,6 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
         std::memcpy(h.top_idx, h2.top_idx, sizeof(h.top_idx));
         std::memcpy(h.top_J, h2.top_J, sizeof(h.top_J));
     }
-    cleanup();
 #undef MF_HIP2
     empty_result(out);
     out.n_eval = n;
@@ -594,26 +638,26 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
 }
 
 mf_status search_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint64_t n, char *ws, hipStream_t s,
-                       mf_result &acc, int depth)
+                       const EventLease &ev, mf_result &acc, int depth)
 {
     if (n == 0) return MF_OK;
     if (n > kMaxLaunch) {
         const uint64_t h = n / 2;
-        mf_status st = search_range(p, args, lo, h, ws, s, acc, depth);
+        mf_status st = search_range(p, args, lo, h, ws, s, ev, acc, depth);
         if (st != MF_OK) return st;
-        return search_range(p, args, lo + h, n - h, ws, s, acc, depth);
+        return search_range(p, args, lo + h, n - h, ws, s, ev, acc, depth);
     }
     mf_result part;
     RangeOutcome oc;
-    mf_status st = run_range(p, args, lo, n, ws, s, part, oc);
+    mf_status st = run_range(p, args, lo, n, ws, s, ev, part, oc);
     if (st != MF_OK) return st;
     if (oc == kRangeSplit) {
         if (n < 2 || depth > 40) return MF_ENOMEM;
         const uint64_t h = n / 2;
         acc.n_splits += 1;
-        st = search_range(p, args, lo, h, ws, s, acc, depth + 1);
+        st = search_range(p, args, lo, h, ws, s, ev, acc, depth + 1);
         if (st != MF_OK) return st;
-        return search_range(p, args, lo + h, n - h, ws, s, acc, depth + 1);
+        return search_range(p, args, lo + h, n - h, ws, s, ev, acc, depth + 1);
     }
     merge_into(acc, part, args->top_k);
     return MF_OK;
@@ -720,7 +764,8 @@ FixedArgs fixed_base(const mf_problem *p, const mf_objective &objective, int top
     return a;
 }
 
-mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipStream_t s, mf_result &acc)
+mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipStream_t s, const EventLease &ev,
+                       mf_result &acc)
 {
     if (args->hi == args->lo) return MF_OK;
     const FixedWs w = fixed_ws_layout(*p, p->num_cus * kFixedMaxWgsPerCu, args->top_k);
@@ -737,9 +782,7 @@ mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipS
     const bool dump = (args->flags & MF_DUMP) != 0;
     const int wgs_per_cu = fixed_wgs_per_cu(a);
 
-    hipEvent_t ev0 = nullptr, ev1 = nullptr;
-    MF_HIP(hipEventCreate(&ev0));
-    if (hipEventCreate(&ev1) != hipSuccess) { (void)hipEventDestroy(ev0); return MF_EDEVICE; }
+    hipEvent_t ev0 = ev.start(), ev1 = ev.stop();
     mf_status st = MF_OK;
     for (uint64_t lo = args->lo; lo < args->hi;) {
         const uint64_t n = std::min<uint64_t>(args->hi - lo, kFixedChunk);
@@ -758,7 +801,8 @@ mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipS
         if (hipMemsetAsync(a.res, 0, sizeof(DevResult), s) != hipSuccess ||
             launch_fixed(a, grid, lo == args->lo, s, ev0, ev1) != hipSuccess ||
             hipMemcpyAsync(&h, a.res, sizeof(DevResult), hipMemcpyDeviceToHost, s) != hipSuccess ||
-            hipStreamSynchronize(s) != hipSuccess || hipEventElapsedTime(&ms, ev0, ev1) != hipSuccess) {
+            hipStreamSynchronize(s) != hipSuccess ||
+            (ev0 && hipEventElapsedTime(&ms, ev0, ev1) != hipSuccess)) {
             st = MF_EDEVICE;
             break;
         }
@@ -777,8 +821,6 @@ mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipS
         merge_into(acc, part, args->top_k);
         lo += n;
     }
-    (void)hipEventDestroy(ev0);
-    (void)hipEventDestroy(ev1);
     return st;
 }
 
@@ -881,9 +923,8 @@ mf_status search_static(mf_problem *p, const mf_static_args *args, char *ws, hip
     mf_status st = static_setup(p, args, ws, args->top_k, s, sa);
     if (st != MF_OK) return st;
     const int wgs_per_cu = static_wgs_per_cu(sa);
-    hipEvent_t ev0 = nullptr, ev1 = nullptr;
-    MF_HIP(hipEventCreate(&ev0));
-    if (hipEventCreate(&ev1) != hipSuccess) { (void)hipEventDestroy(ev0); return MF_EDEVICE; }
+    const EventLease ev(p, true);
+    hipEvent_t ev0 = ev.start(), ev1 = ev.stop();
     for (uint64_t lo = args->lo; lo < args->hi;) {
         const uint64_t n = std::min<uint64_t>(args->hi - lo, kFixedChunk);
         FixedArgs &a = sa.f;
@@ -899,7 +940,8 @@ mf_status search_static(mf_problem *p, const mf_static_args *args, char *ws, hip
         if (hipMemsetAsync(a.res, 0, sizeof(DevResult), s) != hipSuccess ||
             launch_static(sa, grid, s, ev0, ev1) != hipSuccess ||
             hipMemcpyAsync(&h, a.res, sizeof(DevResult), hipMemcpyDeviceToHost, s) != hipSuccess ||
-            hipStreamSynchronize(s) != hipSuccess || hipEventElapsedTime(&ms, ev0, ev1) != hipSuccess) {
+            hipStreamSynchronize(s) != hipSuccess ||
+            (ev0 && hipEventElapsedTime(&ms, ev0, ev1) != hipSuccess)) {
             st = MF_EDEVICE;
             break;
         }
@@ -918,14 +960,117 @@ mf_status search_static(mf_problem *p, const mf_static_args *args, char *ws, hip
         merge_into(acc, part, args->top_k);
         lo += n;
     }
-    (void)hipEventDestroy(ev0);
-    (void)hipEventDestroy(ev1);
     return st;
+}
+
+// ---- problem tables
+
+// Shape of a description: option counts, first row of each model, |Lambda|.
+struct Shape {
+    std::vector<int32_t> K, opt_off;
+    int sumK = 0;
+    uint64_t space = 0;
+    int64_t wstride = 0;
+};
+
+mf_status check_desc(const mf_desc *desc, Shape &sh)
+{
+    if (!desc) return MF_EINVAL;
+    const int N = desc->n_models, L = desc->n_local, A = desc->n_agg, H1 = desc->hidden1, H2 = desc->hidden2;
+    if (N < 1 || N > MF_MAX_MODELS || L < 1 || A < 1 || A > MF_MAX_AGG || L + A > 64 || H1 < 1 || H1 > 256 || H2 < 1 ||
+        H2 > 256 || !desc->h_n_options || !desc->h_agg_cols)
+        return MF_EINVAL;
+    if (desc->dtype != MF_F32 && desc->dtype != MF_BF16) return MF_EINVAL;
+    if (desc->output_act != MF_ACT_IDENTITY && desc->output_act != MF_ACT_SIGMOID) return MF_EINVAL;
+    if (desc->vram_slot < 0 || desc->vram_slot >= A || !std::isfinite(desc->vram_cap)) return MF_EINVAL;
+    sh.K.assign(desc->h_n_options, desc->h_n_options + N);
+    sh.opt_off.clear();
+    uint64_t space = 1;
+    int sumK = 0;
+    for (int i = 0; i < N; i++) {
+        const int k = sh.K[i];
+        if (k < 1 || k > 255) return MF_EINVAL;
+        if (space > UINT64_MAX / (uint64_t)k) return MF_EOVERFLOW;
+        space *= (uint64_t)k;
+        sh.opt_off.push_back(sumK);
+        sumK += k;
+    }
+    for (int k = 0; k < A; k++)
+        if (desc->h_agg_cols[k] < 0 || desc->h_agg_cols[k] >= L) return MF_EINVAL;
+    sh.sumK = sumK;
+    sh.space = space;
+    sh.wstride = (int64_t)H1 * (L + A) + H1 + (int64_t)H2 * H1 + H2 + 2 * H2 + 2;
+    return MF_OK;
+}
+
+// Where each table sits in the caller's device buffer (byte offsets, 256-byte
+// aligned).  A function of the description alone, so that the buffer can be
+// sized before creation.
+struct TableLayout {
+    bool fast_ok = false, bf_ok = false;
+    FastLayout lay{};
+    Bf16Layout blay{};
+    size_t o_img = 0, o_can = 0, o_fea = 0, o_agg = 0, o_rm = 0, o_z = 0, o_c = 0, o_w64 = 0, o_bm = 0, o_bg = 0,
+           o_ph = 0, o_vr = 0, total = 0;
+};
+
+TableLayout table_layout(const mf_desc &d, const Shape &sh)
+{
+    TableLayout t;
+    const int N = d.n_models, L = d.n_local, A = d.n_agg, H1 = d.hidden1, H2 = d.hidden2, sumK = sh.sumK;
+    const bool bf16 = d.dtype == MF_BF16;
+    const int H = H1;
+    // fp32 fast path: H1 == H2 in {32, 64}, A in {2,4,6,8}, the image within LDS
+    t.fast_ok = !bf16 && H1 == H2 && fast_kernel_supported(N, A, H1, 64);
+    if (t.fast_ok) {
+        FastLayout &ly = t.lay;
+        ly.H = H; ly.A = A; ly.AP = 8; ly.MB = H / 32; ly.S1 = A / 2; ly.PST = H + 4;
+        int o = 0;
+        ly.off_w1a = o; o += N * ly.MB * ly.S1 * 64;
+        ly.off_b2 = o; o += N * H;
+        ly.off_w2 = o; o += N * H * H;
+        ly.off_w3 = o; o += N * 2 * H;
+        ly.off_b3 = o; o += N * 4;
+        ly.off_p = o; o += sumK * ly.PST;
+        ly.off_g = o; o += sumK * ly.AP;
+        ly.off_c = o; o += 8;
+        ly.total_floats = (o + 3) & ~3;
+        const size_t lds = (size_t)ly.total_floats * 4 + kFastPar * 4 + (size_t)kSearchWaves * 64 * 8;
+        if (lds > 163840) t.fast_ok = false;
+    }
+    // bf16 fast path: H1 == H2 in {64, 128, 256}, A in {2,4,6,8}
+    t.bf_ok = bf16 && H1 == H2 && bf16_kernel_supported(N, A, H1);
+    if (t.bf_ok) {
+        t.blay = bf16_layout(H, A, sumK);
+        if (bf16_lds_bytes(t.blay, 128) > 163840) t.bf_ok = false;
+    }
+    const size_t n_img = t.fast_ok ? (size_t)t.lay.total_floats : 0;
+    const size_t n_w = (size_t)N * sh.wstride;
+    const size_t n_bimg = t.bf_ok ? (size_t)N * t.blay.model_floats : 0;
+    const size_t n_bg = t.bf_ok ? (size_t)sumK * 8 + t.blay.gv_floats : 0;
+    const size_t n_phat = t.bf_ok ? (size_t)sumK * t.blay.PST : 0;
+    const size_t n_vrow = d.variants ? (size_t)sumK * 8 : 0;
+    size_t off = 0;
+    t.o_img = off; off = align256(off + n_img * 4);
+    t.o_can = off; off = align256(off + n_w * 4);
+    t.o_fea = off; off = align256(off + (size_t)sumK * L * 4);
+    t.o_agg = off; off = align256(off + (size_t)A * 4);
+    t.o_rm = off; off = align256(off + (size_t)sumK * 4);
+    t.o_z = off; off = align256(off + 64 * 4);
+    t.o_c = off; off = align256(off + (size_t)A * 4);
+    t.o_w64 = off; off = align256(off + n_w * 8);
+    t.o_bm = off; off = align256(off + n_bimg * 4);
+    t.o_bg = off; off = align256(off + n_bg * 4);
+    t.o_ph = off; off = align256(off + n_phat * 4);
+    t.o_vr = off; off = align256(off + n_vrow * 4);
+    t.total = off;
+    return t;
 }
 
 }  // namespace
 
 extern "C" {
+
 
 const char *mf_status_string(mf_status s)
 {
@@ -941,18 +1086,28 @@ const char *mf_status_string(mf_status s)
     return "unknown mf_status";
 }
 
-mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const float *d_weights, void *stream,
-                            mf_problem **out)
+mf_status mf_problem_bytes(const mf_desc *desc, size_t *bytes)
 {
-    if (!desc || !d_features || !d_weights || !out) return MF_EINVAL;
+    if (!bytes) return MF_EINVAL;
+    Shape sh;
+    const mf_status st = check_desc(desc, sh);
+    if (st != MF_OK) return st;
+    *bytes = table_layout(*desc, sh).total;
+    return MF_OK;
+}
+
+mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const float *d_weights, void *d_tables,
+                            size_t table_bytes, void *stream, mf_problem **out)
+{
+    if (!desc || !d_features || !d_weights || !d_tables || !out) return MF_EINVAL;
     *out = nullptr;
+    Shape sh;
+    const mf_status st0 = check_desc(desc, sh);
+    if (st0 != MF_OK) return st0;
+    const TableLayout tl = table_layout(*desc, sh);
+    if (table_bytes < tl.total) return MF_ENOMEM;
+    if (((uintptr_t)d_tables & 255u) != 0) return MF_EINVAL;
     const int N = desc->n_models, L = desc->n_local, A = desc->n_agg, H1 = desc->hidden1, H2 = desc->hidden2;
-    if (N < 1 || N > MF_MAX_MODELS || L < 1 || A < 1 || A > MF_MAX_AGG || L + A > 64 || H1 < 1 || H1 > 256 || H2 < 1 ||
-        H2 > 256 || !desc->h_n_options || !desc->h_agg_cols)
-        return MF_EINVAL;
-    if (desc->dtype != MF_F32 && desc->dtype != MF_BF16) return MF_EINVAL;
-    if (desc->output_act != MF_ACT_IDENTITY && desc->output_act != MF_ACT_SIGMOID) return MF_EINVAL;
-    if (desc->vram_slot < 0 || desc->vram_slot >= A || !std::isfinite(desc->vram_cap)) return MF_EINVAL;
     mf_problem *p = new (std::nothrow) mf_problem();
     if (!p) return MF_ENOMEM;
     p->N = N; p->L = L; p->A = A; p->H1 = H1; p->H2 = H2;
@@ -960,40 +1115,36 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     p->act = desc->output_act;
     p->vram_slot = desc->vram_slot;
     p->vram_cap = desc->vram_cap;
-    p->K.assign(desc->h_n_options, desc->h_n_options + N);
+    p->K = sh.K;
+    p->opt_off = sh.opt_off;
     p->agg_cols.assign(desc->h_agg_cols, desc->h_agg_cols + A);
-    uint64_t space = 1;
-    int sumK = 0;
-    for (int i = 0; i < N; i++) {
-        const int k = p->K[i];
-        if (k < 1 || k > 255) { delete p; return MF_EINVAL; }
-        if (space > UINT64_MAX / (uint64_t)k) { delete p; return MF_EOVERFLOW; }
-        space *= (uint64_t)k;
-        p->opt_off.push_back(sumK);
-        sumK += k;
-    }
-    for (int k = 0; k < A; k++)
-        if (p->agg_cols[k] < 0 || p->agg_cols[k] >= L) { delete p; return MF_EINVAL; }
-    p->space = space;
-    p->sumK = sumK;
-    const int nin = L + A;
-    p->wstride = (int64_t)H1 * nin + H1 + (int64_t)H2 * H1 + H2 + 2 * H2 + 2;
+    p->space = sh.space;
+    p->sumK = sh.sumK;
+    p->wstride = sh.wstride;
+    const int sumK = sh.sumK, nin = L + A;
 
+    // the caller's inputs, read in the order of `stream`
     hipStream_t s = (hipStream_t)stream;
     std::vector<float> F((size_t)sumK * L), W((size_t)N * p->wstride);
-    if (hipMemcpy(F.data(), d_features, F.size() * 4, hipMemcpyDefault) != hipSuccess ||
-        hipMemcpy(W.data(), d_weights, W.size() * 4, hipMemcpyDefault) != hipSuccess) {
+    if (hipMemcpyAsync(F.data(), d_features, F.size() * 4, hipMemcpyDefault, s) != hipSuccess ||
+        hipMemcpyAsync(W.data(), d_weights, W.size() * 4, hipMemcpyDefault, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess) {
         delete p;
         return MF_EINVAL;
     }
     if (!all_finite(F) || !all_finite(W)) { delete p; return MF_EINVAL; }
-    std::vector<float> vrow;
+
+    // every table is written into one host image of the caller's buffer,
+    // uploaded with one copy (zero where nothing is written)
+    std::vector<unsigned char> himg(tl.total, 0);
+    auto at_f = [&](size_t off) { return reinterpret_cast<float *>(himg.data() + off); };
+
     if (desc->variants) {
         const mf_variants *mv = desc->variants;
         if (!mv->h_variant || !mv->h_n_variants || !mv->h_fmin || !mv->h_fmax || !mv->h_quality ||
             !mv->h_reload_cost) { delete p; return MF_EINVAL; }
         p->n_var.assign(mv->h_n_variants, mv->h_n_variants + N);
-        vrow.assign((size_t)sumK * 8, 0.f);
+        float *vrow = at_f(tl.o_vr);
         for (int i = 0; i < N; i++) {
             const int nv = p->n_var[i];
             const float c = mv->h_reload_cost[i];
@@ -1011,7 +1162,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
                 const int r = p->opt_off[i] + o, v = mv->h_variant[r];
                 if (v < 0 || v >= nv) { delete p; return MF_EINVAL; }
                 const float lo = mv->h_fmin[i * MF_MAX_VARIANTS + v], hi = mv->h_fmax[i * MF_MAX_VARIANTS + v];
-                float *e = vrow.data() + (size_t)r * 8;
+                float *e = vrow + (size_t)r * 8;
                 e[0] = lo;
                 e[1] = hi;
                 e[2] = (float)(1.0 / ((double)hi - (double)lo));
@@ -1054,27 +1205,12 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     }
 
     // ---- fast path (fp32, H1 == H2 in {32, 64}, A in {2,4,6,8})
-    p->fast_ok = !p->bf16 && H1 == H2 && fast_kernel_supported(N, A, H1, 64);
+    p->fast_ok = tl.fast_ok;
+    p->lay = tl.lay;
     const int H = H1;
-    FastLayout &ly = p->lay;
-    std::vector<float> img;
+    const FastLayout &ly = p->lay;
     if (p->fast_ok) {
-        ly.H = H; ly.A = A; ly.AP = 8; ly.MB = H / 32; ly.S1 = A / 2; ly.PST = H + 4;
-        int o = 0;
-        ly.off_w1a = o; o += N * ly.MB * ly.S1 * 64;
-        ly.off_b2 = o; o += N * H;
-        ly.off_w2 = o; o += N * H * H;
-        ly.off_w3 = o; o += N * 2 * H;
-        ly.off_b3 = o; o += N * 4;
-        ly.off_p = o; o += sumK * ly.PST;
-        ly.off_g = o; o += sumK * ly.AP;
-        ly.off_c = o; o += 8;
-        ly.total_floats = (o + 3) & ~3;
-        const size_t lds = (size_t)ly.total_floats * 4 + kFastPar * 4 + (size_t)kSearchWaves * 64 * 8;
-        if (lds > 163840) p->fast_ok = false;
-    }
-    if (p->fast_ok) {
-        img.assign(ly.total_floats, 0.f);
+        float *img = at_f(tl.o_img);
         // internal aggregate slot order: the VRAM slot first
         std::vector<int> perm;
         perm.push_back(p->vram_slot);
@@ -1084,7 +1220,6 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
             const float *w = W.data() + (int64_t)i * p->wstride;
             const float *W1 = w, *b1 = W1 + (int64_t)H * nin, *W2 = b1 + H, *b2 = W2 + (int64_t)H * H,
                         *W3 = b2 + H, *b3 = W3 + 2 * H;
-            (void)b1;
             for (int mb = 0; mb < ly.MB; mb++)
                 for (int st = 0; st < ly.S1; st++)
                     for (int l = 0; l < 64; l++)
@@ -1144,20 +1279,16 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     }
 
     // ---- bf16 fast path (H1 == H2 in {64, 128, 256}, A in {2,4,6,8})
-    p->bf_ok = p->bf16 && H1 == H2 && bf16_kernel_supported(N, A, H1);
-    Bf16Layout &bl = p->blay;
-    std::vector<float> bimg, bg;
+    p->bf_ok = tl.bf_ok;
+    p->blay = tl.blay;
+    const Bf16Layout &bl = p->blay;
     if (p->bf_ok) {
-        bl = bf16_layout(H, A, sumK);
-        if (bf16_lds_bytes(bl, 128) > 163840) p->bf_ok = false;
-    }
-    if (p->bf_ok) {
-        bimg.assign((size_t)N * bl.model_floats, 0.f);
+        float *bimg = at_f(tl.o_bm);
         for (int i = 0; i < N; i++) {
             const float *w = W.data() + (int64_t)i * p->wstride;
             const float *W1 = w, *b1 = W1 + (int64_t)H * nin, *W2 = b1 + H, *b2 = W2 + (int64_t)H * H,
                         *W3 = b2 + H, *b3 = W3 + 2 * H;
-            float *blk = bimg.data() + (size_t)i * bl.model_floats;
+            float *blk = bimg + (size_t)i * bl.model_floats;
             uint16_t *w2a = reinterpret_cast<uint16_t *>(blk + bl.off_w2a);
             for (int mb2 = 0; mb2 < bl.MB; mb2++)
                 for (int ks = 0; ks < bl.KS; ks++)
@@ -1189,7 +1320,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
             cst[1] = b3[1];
             for (int t = 0; t < 12; t++) blk[bl.off_cst + t] = cst[t];
         }
-        bg.assign((size_t)sumK * 8 + bl.gv_floats, 0.f);
+        float *bg = at_f(tl.o_bg);
         for (int r = 0; r < sumK; r++) {
             for (int hf = 0; hf < 2; hf++)
                 for (int st = 0; st < 4; st++) {
@@ -1205,10 +1336,10 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     }
 
     // ---- canonical image: per model W1T[nin][H1] b1 W2T[H1][H2] b2 W3[2][H2] b3
-    std::vector<float> canon((size_t)N * p->wstride);
+    float *canon = at_f(tl.o_can);
     for (int i = 0; i < N; i++) {
         const float *w = W.data() + (int64_t)i * p->wstride;
-        float *c = canon.data() + (int64_t)i * p->wstride;
+        float *c = canon + (int64_t)i * p->wstride;
         const float *W1 = w, *b1 = W1 + (int64_t)H1 * nin, *W2 = b1 + H1, *rest = W2 + (int64_t)H2 * H1;
         float *cW1T = c, *cb1 = c + (int64_t)nin * H1, *cW2T = cb1 + H1, *crest = cW2T + (int64_t)H1 * H2;
         for (int h = 0; h < H1; h++)
@@ -1218,52 +1349,31 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
             for (int h = 0; h < H1; h++) cW2T[(int64_t)h * H2 + v] = W2[(int64_t)v * H1 + h];
         std::memcpy(crest, rest, (size_t)(H2 + 2 * H2 + 2) * 4);
     }
-    std::vector<int32_t> row_model(sumK);
+    std::memcpy(himg.data() + tl.o_fea, F.data(), F.size() * 4);
+    std::memcpy(himg.data() + tl.o_agg, p->agg_cols.data(), (size_t)A * 4);
+    int32_t *row_model = reinterpret_cast<int32_t *>(himg.data() + tl.o_rm);
     for (int i = 0; i < N; i++)
         for (int o = 0; o < p->K[i]; o++) row_model[p->opt_off[i] + o] = i;
+    std::memcpy(himg.data() + tl.o_c, p->centre.data(), (size_t)A * 4);
+    double *w64 = reinterpret_cast<double *>(himg.data() + tl.o_w64);
+    for (size_t t = 0; t < W.size(); t++) w64[t] = (double)W[t];
 
-    // ---- one device allocation
-    size_t off = 0;
-    const size_t o_img = off; off = align256(off + img.size() * 4);
-    const size_t o_can = off; off = align256(off + canon.size() * 4);
-    const size_t o_fea = off; off = align256(off + F.size() * 4);
-    const size_t o_agg = off; off = align256(off + (size_t)A * 4);
-    const size_t o_rm = off; off = align256(off + (size_t)sumK * 4);
-    const size_t o_z = off; off = align256(off + 64 * 4);
-    const size_t o_c = off; off = align256(off + (size_t)A * 4);
-    const size_t o_w64 = off; off = align256(off + W.size() * 8);
-    const size_t o_bm = off; off = align256(off + bimg.size() * 4);
-    const size_t o_bg = off; off = align256(off + bg.size() * 4);
-    const size_t o_ph = off; off = align256(off + (p->bf_ok ? (size_t)sumK * bl.PST * 4 : 0));
-    const size_t o_vr = off; off = align256(off + vrow.size() * 4);
-    if (hipMalloc(&p->d_mem, off) != hipSuccess) { delete p; return MF_ENOMEM; }
-    char *base = (char *)p->d_mem;
-    p->d_image = reinterpret_cast<float4 *>(base + o_img);
-    p->d_canon = reinterpret_cast<float *>(base + o_can);
-    p->d_features = reinterpret_cast<float *>(base + o_fea);
-    p->d_agg_cols = reinterpret_cast<int32_t *>(base + o_agg);
-    p->d_row_model = reinterpret_cast<int32_t *>(base + o_rm);
-    p->d_zeros = reinterpret_cast<float *>(base + o_z);
-    p->d_centre = reinterpret_cast<float *>(base + o_c);
-    p->d_w64 = reinterpret_cast<double *>(base + o_w64);
-    p->d_bmodels = reinterpret_cast<float4 *>(base + o_bm);
-    p->d_bg = reinterpret_cast<float4 *>(base + o_bg);
-    p->d_phat = reinterpret_cast<float *>(base + o_ph);
-    p->d_vrow = reinterpret_cast<float4 *>(base + o_vr);
-    std::vector<double> w64(W.begin(), W.end());
-    bool ok = true;
-    ok = ok && hipMemsetAsync(p->d_zeros, 0, 64 * 4, s) == hipSuccess;
-    if (!img.empty()) ok = ok && hipMemcpyAsync(p->d_image, img.data(), img.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
-    ok = ok && hipMemcpyAsync(p->d_canon, canon.data(), canon.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
-    ok = ok && hipMemcpyAsync(p->d_features, F.data(), F.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
-    ok = ok && hipMemcpyAsync(p->d_agg_cols, p->agg_cols.data(), (size_t)A * 4, hipMemcpyHostToDevice, s) == hipSuccess;
-    ok = ok && hipMemcpyAsync(p->d_row_model, row_model.data(), (size_t)sumK * 4, hipMemcpyHostToDevice, s) == hipSuccess;
-    ok = ok && hipMemcpyAsync(p->d_centre, p->centre.data(), (size_t)A * 4, hipMemcpyHostToDevice, s) == hipSuccess;
-    ok = ok && hipMemcpyAsync(p->d_w64, w64.data(), w64.size() * 8, hipMemcpyHostToDevice, s) == hipSuccess;
-    if (!bimg.empty()) ok = ok && hipMemcpyAsync(p->d_bmodels, bimg.data(), bimg.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
-    if (!bg.empty()) ok = ok && hipMemcpyAsync(p->d_bg, bg.data(), bg.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
-    if (!vrow.empty())
-        ok = ok && hipMemcpyAsync(p->d_vrow, vrow.data(), vrow.size() * 4, hipMemcpyHostToDevice, s) == hipSuccess;
+    // ---- the caller's buffer
+    char *base = (char *)d_tables;
+    p->d_tables = d_tables;
+    p->d_image = reinterpret_cast<float4 *>(base + tl.o_img);
+    p->d_canon = reinterpret_cast<float *>(base + tl.o_can);
+    p->d_features = reinterpret_cast<float *>(base + tl.o_fea);
+    p->d_agg_cols = reinterpret_cast<int32_t *>(base + tl.o_agg);
+    p->d_row_model = reinterpret_cast<int32_t *>(base + tl.o_rm);
+    p->d_zeros = reinterpret_cast<float *>(base + tl.o_z);
+    p->d_centre = reinterpret_cast<float *>(base + tl.o_c);
+    p->d_w64 = reinterpret_cast<double *>(base + tl.o_w64);
+    p->d_bmodels = reinterpret_cast<float4 *>(base + tl.o_bm);
+    p->d_bg = reinterpret_cast<float4 *>(base + tl.o_bg);
+    p->d_phat = reinterpret_cast<float *>(base + tl.o_ph);
+    p->d_vrow = reinterpret_cast<float4 *>(base + tl.o_vr);
+    bool ok = hipMemcpyAsync(d_tables, himg.data(), tl.total, hipMemcpyHostToDevice, s) == hipSuccess;
     if (ok && p->bf_ok)
         ok = launch_precompute_phat(p->d_features, p->d_canon, sumK, L, A, H, p->wstride, p->d_row_model, p->d_phat,
                                     bl.PST, s) == hipSuccess;
@@ -1271,11 +1381,16 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
         ok = launch_precompute_p(p->d_features, p->d_canon, p->d_centre, sumK, L, A, H, p->wstride, p->d_row_model,
                                  reinterpret_cast<float *>(p->d_image) + ly.off_p, ly.PST, s) == hipSuccess;
     ok = ok && hipStreamSynchronize(s) == hipSuccess;
+    // one pair of timing events up front (searches on several streams at
+    // once take more from the pool)
+    EventPair ev{};
+    ok = ok && create_event_pair(ev);
     if (!ok) {
-        (void)hipFree(p->d_mem);
         delete p;
         return MF_EDEVICE;
     }
+    p->ev_free.push_back(ev);
+    p->ev_all.push_back(ev);
     *out = p;
     return MF_OK;
 }
@@ -1283,7 +1398,10 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
 void mf_problem_destroy(mf_problem *p)
 {
     if (!p) return;
-    if (p->d_mem) (void)hipFree(p->d_mem);
+    for (const EventPair &e : p->ev_all) {
+        (void)hipEventDestroy(e.a);
+        (void)hipEventDestroy(e.b);
+    }
     delete p;
 }
 
@@ -1322,17 +1440,35 @@ static mf_status check_search_args(const mf_problem *p, const mf_search_args *a)
     return check_objective(p, a->objective);
 }
 
+// Bytes of workspace a validated search needs.
+static size_t search_ws_bytes(const mf_problem *p, const mf_search_args *args)
+{
+    if (args->flags & MF_FIXED_STATE) return fixed_ws_bytes(*p, args->top_k);
+    const uint64_t n = std::min<uint64_t>(args->hi - args->lo, kMaxLaunch);
+    return ws_layout(*p, n, args->top_k, args->worklist_cap).total;
+}
+
+// A validated search on a workspace of at least search_ws_bytes.
+static mf_status search_impl(mf_problem *p, const mf_search_args *args, char *ws, hipStream_t s,
+                             bool may_create_events, mf_result *h_out)
+{
+    const EventLease ev(p, may_create_events);
+    mf_result acc;
+    empty_result(acc);
+    const mf_status st = (args->flags & MF_FIXED_STATE)
+                             ? search_fixed(p, args, ws, s, ev, acc)
+                             : search_range(p, args, args->lo, args->hi - args->lo, ws, s, ev, acc, 0);
+    if (st != MF_OK) return st;
+    *h_out = acc;
+    return MF_OK;
+}
+
 mf_status mf_workspace_size(const mf_problem *p, const mf_search_args *args, size_t *bytes)
 {
     if (!bytes) return MF_EINVAL;
     mf_status st = check_search_args(p, args);
     if (st != MF_OK) return st;
-    if (args->flags & MF_FIXED_STATE) {
-        *bytes = fixed_ws_bytes(*p, args->top_k);
-        return MF_OK;
-    }
-    const uint64_t n = std::min<uint64_t>(args->hi - args->lo, kMaxLaunch);
-    *bytes = ws_layout(*p, n, args->top_k).total;
+    *bytes = search_ws_bytes(p, args);
     return MF_OK;
 }
 
@@ -1342,21 +1478,9 @@ mf_status mf_search(mf_problem *p, const mf_search_args *args, void *d_ws, size_
     if (!h_out || !d_ws) return MF_EINVAL;
     mf_status st = check_search_args(p, args);
     if (st != MF_OK) return st;
-    const uint64_t n = args->hi - args->lo;
-    const bool fixed = (args->flags & MF_FIXED_STATE) != 0;
-    const size_t need = fixed ? fixed_ws_bytes(*p, args->top_k)
-                              : ws_layout(*p, std::min<uint64_t>(n, kMaxLaunch), args->top_k).total;
-    if (ws_bytes < need) return MF_ENOMEM;
+    if (ws_bytes < search_ws_bytes(p, args)) return MF_ENOMEM;
     if (((uintptr_t)d_ws & 255u) != 0) return MF_EINVAL;
-    mf_result acc;
-    empty_result(acc);
-    if (fixed)
-        st = search_fixed(p, args, (char *)d_ws, (hipStream_t)stream, acc);
-    else
-        st = search_range(p, args, args->lo, n, (char *)d_ws, (hipStream_t)stream, acc, 0);
-    if (st != MF_OK) return st;
-    *h_out = acc;
-    return MF_OK;
+    return search_impl(p, args, (char *)d_ws, (hipStream_t)stream, true, h_out);
 }
 
 mf_status mf_static_workspace_size(const mf_problem *p, const mf_static_args *args, size_t *bytes)

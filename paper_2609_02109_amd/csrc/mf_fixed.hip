@@ -477,10 +477,10 @@ hipError_t launch_fixed(const FixedArgs &a, int grid, bool table, hipStream_t s,
     const ScanFn fn = scan_fn(a);
     e = ensure_dyn_lds((const void *)fn, lds);
     if (e != hipSuccess) return e;
-    if ((e = hipEventRecord(ev0, s)) != hipSuccess) return e;
+    if (ev0 && (e = hipEventRecord(ev0, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(grid), dim3(kFixedWaves * 64), lds, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = hipEventRecord(ev1, s)) != hipSuccess) return e;
+    if (ev1 && (e = hipEventRecord(ev1, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(fixed_merge_kernel, dim3(1), dim3(kFixedMergeWaves * 64), 0, s, a.wg_lists, a.wg_counts, grid,
                        a.top_k, a.res);
     return hipGetLastError();
@@ -752,10 +752,10 @@ hipError_t launch_static(const StaticArgs &a, int grid, hipStream_t s, hipEvent_
     const StaticFn fn = static_fn(a);
     hipError_t e = ensure_dyn_lds((const void *)fn, lds);
     if (e != hipSuccess) return e;
-    if ((e = hipEventRecord(ev0, s)) != hipSuccess) return e;
+    if (ev0 && (e = hipEventRecord(ev0, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(grid), dim3(kFixedWaves * 64), lds, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = hipEventRecord(ev1, s)) != hipSuccess) return e;
+    if (ev1 && (e = hipEventRecord(ev1, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(fixed_merge_kernel, dim3(1), dim3(kFixedMergeWaves * 64), 0, s, a.f.wg_lists, a.f.wg_counts,
                        grid, a.f.top_k, a.f.res);
     return hipGetLastError();

@@ -8,6 +8,7 @@ from __future__ import annotations
 
 import ctypes as C
 import os
+import threading
 
 import numpy as np
 # torch first: it brings the HIP runtime it was built against, and the
@@ -27,7 +28,7 @@ MAX_AGG = 16
 MAX_TOPK = 64
 MAX_MODELS = 16
 
-EXPORTS = ["mf_problem_create", "mf_problem_destroy", "mf_space_size", "mf_decode",
+EXPORTS = ["mf_problem_bytes", "mf_problem_create", "mf_problem_destroy", "mf_space_size", "mf_decode",
            "mf_workspace_size", "mf_search", "mf_eval_fast", "mf_eval_canonical",
            "mf_static_workspace_size", "mf_search_static", "mf_eval_static",
            "mf_ga_workspace_size", "mf_ga_run", "mf_status_string"]
@@ -64,7 +65,8 @@ class Objective(C.Structure):
 class SearchArgs(C.Structure):
     _fields_ = [("lo", C.c_uint64), ("hi", C.c_uint64), ("top_k", C.c_int32), ("flags", C.c_uint32),
                 ("d_sla", C.c_void_p), ("d_omega", C.c_void_p), ("d_mask", C.c_void_p),
-                ("d_pred", C.c_void_p), ("objective", Objective), ("state", C.c_float * MAX_AGG)]
+                ("d_pred", C.c_void_p), ("objective", Objective), ("state", C.c_float * MAX_AGG),
+                ("worklist_cap", C.c_uint32)]
 
 
 def objective_args(obj, n_models: int) -> Objective:
@@ -113,7 +115,8 @@ def _load():
     P = C.c_void_p
     S = C.c_int
     sig = {
-        "mf_problem_create": (S, [P, P, P, P, P]),
+        "mf_problem_bytes": (S, [P, P]),
+        "mf_problem_create": (S, [P, P, P, P, C.c_size_t, P, P]),
         "mf_problem_destroy": (None, [P]),
         "mf_space_size": (S, [P, P]),
         "mf_decode": (S, [P, C.c_uint64, P]),
@@ -161,6 +164,17 @@ def _stream(stream):
     return C.c_void_p(s.cuda_stream)
 
 
+def _keep_for(stream, *tensors):
+    """Tensors read or written by work enqueued on `stream`: when that is not
+    torch's current stream, tell the caching allocator, so that their memory
+    is not handed out again before that work has run."""
+    if stream is None or stream == torch.cuda.current_stream():
+        return
+    for t in tensors:
+        if isinstance(t, torch.Tensor) and t.is_cuda:
+            t.record_stream(stream)
+
+
 class Problem:
     """A created problem (mf_problem).  `inst` carries the instance arrays
     (n_options, features, agg_cols, weights, ...), e.g. a synth.Instance."""
@@ -192,16 +206,26 @@ class Problem:
                          MF_BF16 if inst.dtype == "bf16" else MF_F32,
                          C.addressof(self._var) if self._var is not None else None,
                          MF_ACT_SIGMOID if getattr(inst, "act", "identity") == "sigmoid" else MF_ACT_IDENTITY)
+        # the problem's tables live in a caller-owned device buffer, kept
+        # alive as long as the problem
+        nb = C.c_size_t()
+        _check(lib.mf_problem_bytes(C.byref(self.desc), C.byref(nb)), "mf_problem_bytes")
+        self._tables = torch.empty(max(int(nb.value), 256), dtype=torch.uint8, device=self.device)
+        _keep_for(stream, feats, w, self._tables)
         h = C.c_void_p()
-        _check(lib.mf_problem_create(C.byref(self.desc), _ptr(feats), _ptr(w), _stream(stream),
-                                     C.byref(h)), "mf_problem_create")
+        _check(lib.mf_problem_create(C.byref(self.desc), _ptr(feats), _ptr(w), _ptr(self._tables),
+                                     C.c_size_t(self._tables.numel()), _stream(stream), C.byref(h)),
+               "mf_problem_create")
         self.handle = h
-        self._ws = None
+        # one workspace per (thread, stream): calls that overlap must not share one
+        self._ws = {}
+        self._ws_lock = threading.Lock()
 
     def close(self):
         if getattr(self, "handle", None):
             lib.mf_problem_destroy(self.handle)
             self.handle = None
+            self._tables = None
 
     def __del__(self):
         try:
@@ -227,19 +251,29 @@ class Problem:
             return a.to(self.device, dtype).contiguous()
         return torch.as_tensor(np.asarray(a), dtype=dtype, device=self.device).contiguous()
 
-    def workspace(self, nbytes: int):
-        if self._ws is None or self._ws.numel() < nbytes:
-            self._ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
-        return self._ws
+    def workspace(self, nbytes: int, stream=None):
+        """A device workspace of at least nbytes for calls from this thread on
+        `stream` (None: torch's current stream)."""
+        s = stream if stream is not None else torch.cuda.current_stream()
+        key = (threading.get_ident(), s.cuda_stream)
+        with self._ws_lock:
+            ws = self._ws.get(key)
+            if ws is None or ws.numel() < nbytes:
+                ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+                _keep_for(stream, ws)
+                self._ws[key] = ws
+        return ws
 
-    def search(self, sla, omega, k=1, lo=0, hi=None, dump=False, stream=None, objective=None, state=None):
+    def search(self, sla, omega, k=1, lo=0, hi=None, dump=False, stream=None, objective=None, state=None,
+               worklist_cap=0):
         """Exhaustive search over [lo, hi).  Returns a dict of counts and the
         exact top-k; with dump=True also the per-index mask and fast-path
         predictions (device tensors).  objective: None (linear) or an object
         with alpha, beta, delta, tau, prev_variant (Eq. 3; the problem must
         have been created with variants).  state: None (each candidate's own
         aggregate feeds the surrogates) or the observed aggregate [A] held
-        fixed for the whole search (Section III-B)."""
+        fixed for the whole search (Section III-B).  worklist_cap: bound on
+        the certification list (0: the library's default)."""
         if hi is None:
             hi = self.space_size
         d_sla = self._dev(sla, torch.float32)
@@ -251,6 +285,7 @@ class Problem:
         flags = (MF_DUMP if dump else 0) | (MF_FIXED_STATE if state is not None else 0)
         args = SearchArgs(lo, hi, int(k), flags, _ptr(d_sla), _ptr(d_om),
                           _ptr(mask), _ptr(pred), objective_args(objective, self.N))
+        args.worklist_cap = int(worklist_cap)
         if state is not None:
             st = np.asarray(state, np.float32).reshape(-1)
             if st.size != self.A:
@@ -259,7 +294,8 @@ class Problem:
                 args.state[t] = float(st[t])
         nbytes = C.c_size_t()
         _check(lib.mf_workspace_size(self.handle, C.byref(args), C.byref(nbytes)), "mf_workspace_size")
-        ws = self.workspace(nbytes.value)
+        ws = self.workspace(nbytes.value, stream)
+        _keep_for(stream, d_sla, d_om, mask, pred)
         res = Result()
         _check(lib.mf_search(self.handle, C.byref(args), _ptr(ws), C.c_size_t(ws.numel()),
                              _stream(stream), C.byref(res)), "mf_search")
@@ -273,7 +309,7 @@ class Problem:
             out.update(mask=mask[:hi - lo], pred=pred[:hi - lo])
         return out
 
-    def _static_args(self, states, slas, omegas, objective, k=1, lo=0, hi=None, mask=None):
+    def _static_args(self, states, slas, omegas, objective, k=1, lo=0, hi=None, mask=None, stream=None):
         st = np.ascontiguousarray(states, np.float32).reshape(-1, self.A)
         T = int(st.shape[0])
         d_sla = self._dev(np.asarray(slas, np.float32).reshape(T, self.N), torch.float32)
@@ -282,7 +318,7 @@ class Problem:
                           _ptr(st), objective_args(objective, self.N), _ptr(mask))
         nbytes = C.c_size_t()
         _check(lib.mf_static_workspace_size(self.handle, C.byref(args), C.byref(nbytes)), "mf_static_workspace_size")
-        return args, self.workspace(nbytes.value), (st, d_sla, d_om)
+        return args, self.workspace(nbytes.value, stream), (st, d_sla, d_om)
 
     def search_static(self, states, slas, omegas, k=1, lo=0, hi=None, objective=None, dump=False, stream=None):
         """One configuration held over T steps (states [T][A], slas and omegas
@@ -291,7 +327,8 @@ class Problem:
         if hi is None:
             hi = self.space_size
         mask = torch.zeros(max(hi - lo, 1), dtype=torch.uint8, device=self.device) if dump else None
-        args, ws, keep = self._static_args(states, slas, omegas, objective, k, lo, hi, mask)
+        args, ws, keep = self._static_args(states, slas, omegas, objective, k, lo, hi, mask, stream)
+        _keep_for(stream, mask, *keep[1:])
         res = Result()
         _check(lib.mf_search_static(self.handle, C.byref(args), _ptr(ws), C.c_size_t(ws.numel()), _stream(stream),
                                     C.byref(res)), "mf_search_static")
@@ -309,11 +346,12 @@ class Problem:
         service constraints)."""
         d_idx = self._dev(np.asarray(idx, np.uint64).astype(np.int64), torch.int64)
         n = int(d_idx.numel())
-        args, ws, keep = self._static_args(states, slas, omegas, objective)
+        args, ws, keep = self._static_args(states, slas, omegas, objective, stream=stream)
         T = int(args.n_steps)
         J = torch.zeros((max(n, 1), T), dtype=torch.float64, device=self.device)
         S = torch.zeros(max(n, 1), dtype=torch.float64, device=self.device)
         F = torch.zeros((max(n, 1), T), dtype=torch.int32, device=self.device)
+        _keep_for(stream, d_idx, J, S, F, *keep[1:])
         _check(lib.mf_eval_static(self.handle, C.byref(args), _ptr(d_idx), n, _ptr(J), _ptr(S), _ptr(F), _ptr(ws),
                                   C.c_size_t(ws.numel()), _stream(stream)), "mf_eval_static")
         return dict(J=J[:n].cpu().numpy(), S=S[:n].cpu().numpy(), flags=F[:n].cpu().numpy().astype(np.uint32))
@@ -329,6 +367,7 @@ class Problem:
         d_idx = self._dev(idx, torch.int64)
         n = int(d_idx.numel())
         pred = torch.zeros((max(n, 1), self.N, 2), dtype=torch.float32, device=self.device)
+        _keep_for(stream, d_idx, pred)
         _check(lib.mf_eval_fast(self.handle, _ptr(d_idx), n, _ptr(pred), _stream(stream)),
                "mf_eval_fast")
         return pred[:n]
@@ -339,13 +378,12 @@ class Problem:
         pred = torch.zeros((max(n, 1), self.N, 2), dtype=torch.float64, device=self.device)
         J = torch.zeros(max(n, 1), dtype=torch.float64, device=self.device)
         fl = torch.zeros(max(n, 1), dtype=torch.int32, device=self.device)
-        # the call only enqueues: inputs must stay alive (referenced) until it
-        # has been issued; stream order covers their later reuse
         d_sla = self._dev(sla, torch.float32)
         d_om = self._dev(omega, torch.float32)
+        _keep_for(stream, d_idx, d_sla, d_om, pred, J, fl)
         _check(lib.mf_eval_canonical(self.handle, _ptr(d_idx), n, _ptr(d_sla), _ptr(d_om), _ptr(pred),
                                      _ptr(J), _ptr(fl), _stream(stream)), "mf_eval_canonical")
-        return dict(pred=pred[:n], J=J[:n], flags=fl[:n], _inputs=(d_idx, d_sla, d_om))
+        return dict(pred=pred[:n], J=J[:n], flags=fl[:n])
 
     def ga(self, sla, omega, pop=2048, gens=100, tourn_k=3, p_cx=0.7, p_swap=0.5, p_mut=0.05,
            seed=0, final_pop=False, stream=None, objective=None, state=None):
@@ -367,10 +405,11 @@ class Problem:
         nbytes = C.c_size_t()
         _check(lib.mf_ga_workspace_size(self.handle, C.byref(args), C.byref(nbytes)),
                "mf_ga_workspace_size")
-        ws = self.workspace(nbytes.value)
+        ws = self.workspace(nbytes.value, stream)
         best_idx = np.zeros(S, np.uint64)
         best_J = np.zeros(S, np.float64)
         fp = torch.zeros((S, pop), dtype=torch.int64, device=self.device) if final_pop else None
+        _keep_for(stream, d_sla, d_om, fp)
         _check(lib.mf_ga_run(self.handle, C.byref(args), _ptr(ws), C.c_size_t(ws.numel()),
                              _stream(stream), _ptr(best_idx), _ptr(best_J), _ptr(fp)), "mf_ga_run")
         out = dict(best_idx=best_idx, best_J=best_J)

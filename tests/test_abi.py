@@ -17,7 +17,7 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for n in ["mf_problem_create", "mf_problem_destroy", "mf_search", "mf_workspace_size",
+    for n in ["mf_problem_bytes", "mf_problem_create", "mf_problem_destroy", "mf_search", "mf_workspace_size",
               "mf_eval_fast", "mf_eval_canonical", "mf_ga_run", "mf_ga_workspace_size",
               "mf_decode", "mf_space_size", "mf_status_string"]:
         assert n in names
@@ -50,8 +50,11 @@ def test_create_rejects_bad_descriptors_before_any_device_call():
         d.update(over)
         desc = mf.Desc(**d)
         h = C.c_void_p()
+        # a host stand-in for the table buffer: every call here fails before
+        # touching it
         return mf.lib.mf_problem_create(C.byref(desc), dummy.ctypes.data_as(C.c_void_p),
-                                        dummy.ctypes.data_as(C.c_void_p), None, C.byref(h))
+                                        dummy.ctypes.data_as(C.c_void_p), dummy.ctypes.data_as(C.c_void_p),
+                                        0, None, C.byref(h))
     bad_k = np.array([3, 0], np.int32)
     bad_cols = np.array([3, 4, 5, 9], np.int32)
     assert create(n_models=0) == mf.MF_EINVAL
@@ -65,7 +68,48 @@ def test_create_rejects_bad_descriptors_before_any_device_call():
     assert create(hidden1=0) == mf.MF_EINVAL
     big = np.full(9, 255, np.int32)
     assert create(n_models=9, h_n_options=big.ctypes.data) == mf.MF_EOVERFLOW
-    assert mf.lib.mf_problem_create(None, None, None, None, None) == mf.MF_EINVAL
+    assert mf.lib.mf_problem_create(None, None, None, None, 0, None, None) == mf.MF_EINVAL
+    # a valid description with a table buffer below mf_problem_bytes
+    assert create() == mf.MF_ENOMEM
+    desc = mf.Desc(n_models=2, n_local=8, n_agg=4, hidden1=32, hidden2=32, h_n_options=K.ctypes.data,
+                   h_agg_cols=cols.ctypes.data, vram_slot=1, vram_cap=80.0, dtype=mf.MF_F32)
+    h = C.c_void_p()
+    assert mf.lib.mf_problem_create(C.byref(desc), dummy.ctypes.data_as(C.c_void_p), dummy.ctypes.data_as(C.c_void_p),
+                                    None, 1 << 30, None, C.byref(h)) == mf.MF_EINVAL
+
+
+def _desc(mf, K, n_local, n_agg, h1, h2, dtype, cols=None):
+    import numpy as np
+    K = np.ascontiguousarray(K, np.int32)
+    cols = np.ascontiguousarray(cols if cols is not None else list(range(3, 3 + n_agg)), np.int32)
+    d = mf.Desc(n_models=len(K), n_local=n_local, n_agg=n_agg, hidden1=h1, hidden2=h2, h_n_options=K.ctypes.data,
+                h_agg_cols=cols.ctypes.data, vram_slot=1, vram_cap=80.0, dtype=dtype)
+    return d, (K, cols)
+
+
+def test_problem_bytes_sizes_the_caller_buffer():
+    # mf_problem_bytes needs no device: it covers at least the canonical
+    # weights (fp32 and fp64 copies), the option table and, for the fast paths,
+    # their LDS images
+    from paper_2609_02109_amd import mf
+    nb = C.c_size_t()
+    for K, L, A, H, dt in (([6, 6], 8, 4, 32, mf.MF_F32), ([24] * 6, 16, 6, 64, mf.MF_F32),
+                           ([16] * 8, 32, 8, 256, mf.MF_BF16), ([5, 7, 3], 8, 3, 48, mf.MF_F32)):
+        d, keep = _desc(mf, K, L, A, H, H, dt)
+        assert mf.lib.mf_problem_bytes(C.byref(d), C.byref(nb)) == mf.MF_OK
+        N, sumK = len(K), sum(K)
+        stride = H * (L + A) + H + H * H + H + 2 * H + 2
+        assert nb.value % 256 == 0
+        assert nb.value >= N * stride * 12 + sumK * L * 4
+    # the N=8 bf16 workload also stages one 140 KB block per model
+    d, keep = _desc(mf, [16] * 8, 32, 8, 256, 256, mf.MF_BF16)
+    mf.lib.mf_problem_bytes(C.byref(d), C.byref(nb))
+    assert nb.value >= 8 * 140 * 1024
+    bad, keep = _desc(mf, [3, 0], 8, 4, 32, 32, mf.MF_F32)
+    assert mf.lib.mf_problem_bytes(C.byref(bad), C.byref(nb)) == mf.MF_EINVAL
+    assert mf.lib.mf_problem_bytes(None, C.byref(nb)) == mf.MF_EINVAL
+    d, keep = _desc(mf, [6, 6], 8, 4, 32, 32, mf.MF_F32)
+    assert mf.lib.mf_problem_bytes(C.byref(d), None) == mf.MF_EINVAL
 
 
 def test_null_handles_rejected():

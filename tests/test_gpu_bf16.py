@@ -196,7 +196,7 @@ def test_bf16_degenerate_ranges(mf, orc):
         assert g["top_J"].tobytes() == r["top_J"].tobytes()
 
 
-def test_bf16_range_splits_when_certification_list_fills(mf, orc, monkeypatch):
+def test_bf16_range_splits_when_certification_list_fills(mf, orc):
     # model 0's latency is the constant 0.25 and its bound is exactly 0.25:
     # every configuration sits on the (inclusive) boundary, so every one is
     # certified, and a 4-entry certification list forces many range splits
@@ -210,8 +210,7 @@ def test_bf16_range_splits_when_certification_list_fills(mf, orc, monkeypatch):
     assert r["n_feas"] > 0
     g0 = mf.Problem(inst).search(inst.sla, inst.omega, k=16)
     assert g0["n_flagged"] >= r["n_feas"]
-    monkeypatch.setenv("MF_WORKLIST_CAP", "4")
-    g = mf.Problem(inst).search(inst.sla, inst.omega, k=16)
+    g = mf.Problem(inst).search(inst.sla, inst.omega, k=16, worklist_cap=4)
     assert g["n_splits"] > 0
     assert g["n_feas"] == r["n_feas"] and g["n_vram"] == r["n_vram"]
     assert list(g["top_idx"]) == list(r["top_idx"])

@@ -207,14 +207,13 @@ def test_topk_fallback_on_exact_ties(mf, orc):
     assert g["top_J"].tobytes() == r["top_J"].tobytes()
 
 
-def test_range_splits_when_certification_list_fills(mf, orc, monkeypatch):
+def test_range_splits_when_certification_list_fills(mf, orc):
     inst = synth.make_instance([12, 12, 9, 9, 9], seed=5, vram_quantile=0.75,
                                sla_range=(-0.15, 0.15), top_k=16)
     r = orc.Problem(inst).search(inst.sla, inst.omega, k=16)
     g0 = mf.Problem(inst).search(inst.sla, inst.omega, k=16)
     assert g0["n_flagged"] >= 8
-    monkeypatch.setenv("MF_WORKLIST_CAP", "4")
-    g = mf.Problem(inst).search(inst.sla, inst.omega, k=16)
+    g = mf.Problem(inst).search(inst.sla, inst.omega, k=16, worklist_cap=4)
     assert g["n_splits"] > 0, g0["n_flagged"]
     assert g["n_feas"] == r["n_feas"] and g["n_vram"] == r["n_vram"]
     assert list(g["top_idx"]) == list(r["top_idx"])

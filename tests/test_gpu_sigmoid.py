@@ -127,6 +127,7 @@ def test_sigmoid_rejects_unknown_activation(mf):
     import torch
     feats = torch.as_tensor(inst.features, device="cuda")
     w = torch.as_tensor(inst.weights, device="cuda")
-    st = mf.lib.mf_problem_create(C.byref(d), C.c_void_p(feats.data_ptr()), C.c_void_p(w.data_ptr()), None,
-                                  C.byref(h))
+    tables = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
+    st = mf.lib.mf_problem_create(C.byref(d), C.c_void_p(feats.data_ptr()), C.c_void_p(w.data_ptr()),
+                                  C.c_void_p(tables.data_ptr()), tables.numel(), None, C.byref(h))
     assert st == mf.MF_EINVAL
