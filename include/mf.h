@@ -72,7 +72,8 @@ typedef enum {
     MF_EDEVICE = 3,       /* a HIP runtime call or kernel launch failed */
     MF_EUNSUPPORTED = 4,  /* shape outside what the kernels are built for (see mf_desc) */
     MF_EOVERFLOW = 5,     /* prod K_i does not fit in 64 bits, or a range bound exceeds |Lambda| */
-    MF_EINTERNAL = 6      /* a self-check failed (fast-path error bound violated); result unusable */
+    MF_EINTERNAL = 6,     /* a self-check failed (fast-path error bound violated); result unusable */
+    MF_ESCRATCH = 7       /* mf_search_noalloc: the search needs more than MF_NOALLOC_SCRATCH_BYTES */
 } mf_status;
 
 typedef enum { MF_F32 = 0, MF_BF16 = 1 } mf_dtype;
@@ -249,6 +250,23 @@ mf_status mf_workspace_size(const mf_problem *p, const mf_search_args *args, siz
  * Empty feasible set: MF_OK with n_top = 0. */
 mf_status mf_search(mf_problem *p, const mf_search_args *args, void *d_ws, size_t ws_bytes,
                     void *stream, mf_result *h_out);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): mf_search
+ * with its workspace taken from a fixed device scratch array that the library
+ * holds, one copy per GPU, until the process ends.  Same arguments, results
+ * and blocking behaviour as mf_search; the call allocates nothing (no
+ * hipMalloc, no library allocation; timing uses events created with the
+ * problem, and runs untimed, main_kernel_ms = 0, when another call holds
+ * them).  MF_ESCRATCH when mf_workspace_size(args) exceeds
+ * MF_NOALLOC_SCRATCH_BYTES: lower args->worklist_cap or search a shorter
+ * range.  The current device must be the problem's (else MF_EINVAL).  Every
+ * call on one GPU uses that GPU's single scratch array: calls that overlap on
+ * one GPU (other threads, other streams) race and give wrong results;
+ * serialise them.  The scratch keeps the last call's contents; each call
+ * initialises what it reads. */
+#define MF_NOALLOC_SCRATCH_BYTES (64u << 20)
+mf_status mf_search_noalloc(mf_problem *p, const mf_search_args *args, void *stream, mf_result *h_out);
 
 /* ------------------------------------------------- static (multi-step) search */
 

@@ -41,6 +41,7 @@ struct mf_problem {
     int device = 0;
     // device tables: pointers into the caller's buffer (borrowed until destroy)
     void *d_tables = nullptr;
+    void *d_scratch = nullptr;   // this device's copy of the no-allocation scratch
     float4 *d_image = nullptr;
     float *d_canon = nullptr, *d_features = nullptr, *d_zeros = nullptr, *d_centre = nullptr;
     double *d_w64 = nullptr;     // packed weights as fp64 (GA fitness)
@@ -83,7 +84,32 @@ hipError_t ensure_dyn_lds(const void *fn, size_t bytes)
 
 }  // namespace mfi
 
+// Device scratch of mf_search_noalloc: a file-scope array, one copy per GPU,
+// held until the process ends.  Host code never uses the array's name as an
+// address: each device's address comes from hipGetSymbolAddress (scratch_ptr).
+static __device__ __align__(256) unsigned char scratch[MF_NOALLOC_SCRATCH_BYTES];
+
 namespace {
+
+// The device address of `scratch` on device `dev` (the current device),
+// looked up once per device.
+hipError_t scratch_ptr(int dev, void **out)
+{
+    static std::mutex mu;
+    static std::map<int, void *> ptrs;
+    std::lock_guard<std::mutex> g(mu);
+    const auto it = ptrs.find(dev);
+    if (it != ptrs.end()) {
+        *out = it->second;
+        return hipSuccess;
+    }
+    void *ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    ptrs[dev] = ptr;
+    *out = ptr;
+    return hipSuccess;
+}
 
 bool create_event_pair(EventPair &e)
 {
@@ -1082,6 +1108,7 @@ const char *mf_status_string(mf_status s)
         case MF_EUNSUPPORTED: return "MF_EUNSUPPORTED: shape not supported by the kernels";
         case MF_EOVERFLOW: return "MF_EOVERFLOW: joint space or range does not fit";
         case MF_EINTERNAL: return "MF_EINTERNAL: fast-path self-check failed";
+        case MF_ESCRATCH: return "MF_ESCRATCH: the search needs more workspace than mf_search_noalloc's scratch holds";
     }
     return "unknown mf_status";
 }
@@ -1186,7 +1213,8 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
         }
     }
     if (hipGetDevice(&p->device) != hipSuccess ||
-        hipDeviceGetAttribute(&p->num_cus, hipDeviceAttributeMultiprocessorCount, p->device) != hipSuccess) {
+        hipDeviceGetAttribute(&p->num_cus, hipDeviceAttributeMultiprocessorCount, p->device) != hipSuccess ||
+        scratch_ptr(p->device, &p->d_scratch) != hipSuccess) {
         delete p;
         return MF_EDEVICE;
     }
@@ -1481,6 +1509,19 @@ mf_status mf_search(mf_problem *p, const mf_search_args *args, void *d_ws, size_
     if (ws_bytes < search_ws_bytes(p, args)) return MF_ENOMEM;
     if (((uintptr_t)d_ws & 255u) != 0) return MF_EINVAL;
     return search_impl(p, args, (char *)d_ws, (hipStream_t)stream, true, h_out);
+}
+
+mf_status mf_search_noalloc(mf_problem *p, const mf_search_args *args, void *stream, mf_result *h_out)
+{
+    if (!h_out) return MF_EINVAL;
+    mf_status st = check_search_args(p, args);
+    if (st != MF_OK) return st;
+    if (search_ws_bytes(p, args) > (size_t)MF_NOALLOC_SCRATCH_BYTES) return MF_ESCRATCH;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return MF_EDEVICE;
+    if (dev != p->device) return MF_EINVAL;
+    // the problem's pre-created timing events only (none free: untimed)
+    return search_impl(p, args, (char *)p->d_scratch, (hipStream_t)stream, false, h_out);
 }
 
 mf_status mf_static_workspace_size(const mf_problem *p, const mf_static_args *args, size_t *bytes)

@@ -19,7 +19,8 @@ import torch  # noqa: F401
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmf.so")
 
-MF_OK, MF_EINVAL, MF_ENOMEM, MF_EDEVICE, MF_EUNSUPPORTED, MF_EOVERFLOW, MF_EINTERNAL = range(7)
+MF_OK, MF_EINVAL, MF_ENOMEM, MF_EDEVICE, MF_EUNSUPPORTED, MF_EOVERFLOW, MF_EINTERNAL, MF_ESCRATCH = range(8)
+NOALLOC_SCRATCH_BYTES = 64 << 20
 MF_F32, MF_BF16 = 0, 1
 MF_ACT_IDENTITY, MF_ACT_SIGMOID = 0, 1
 MF_DUMP = 1
@@ -29,7 +30,7 @@ MAX_TOPK = 64
 MAX_MODELS = 16
 
 EXPORTS = ["mf_problem_bytes", "mf_problem_create", "mf_problem_destroy", "mf_space_size", "mf_decode",
-           "mf_workspace_size", "mf_search", "mf_eval_fast", "mf_eval_canonical",
+           "mf_workspace_size", "mf_search", "mf_search_noalloc", "mf_eval_fast", "mf_eval_canonical",
            "mf_static_workspace_size", "mf_search_static", "mf_eval_static",
            "mf_ga_workspace_size", "mf_ga_run", "mf_status_string"]
 
@@ -122,6 +123,7 @@ def _load():
         "mf_decode": (S, [P, C.c_uint64, P]),
         "mf_workspace_size": (S, [P, P, P]),
         "mf_search": (S, [P, P, P, C.c_size_t, P, P]),
+        "mf_search_noalloc": (S, [P, P, P, P]),
         "mf_eval_fast": (S, [P, P, C.c_int64, P, P]),
         "mf_eval_canonical": (S, [P, P, C.c_int64, P, P, P, P, P, P]),
         "mf_static_workspace_size": (S, [P, P, P]),

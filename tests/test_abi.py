@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings():
     from paper_2609_02109_amd import mf
-    for s in range(7):
+    for s in range(8):
         assert mf.status_string(s).startswith("MF_")
     assert "unknown" in mf.status_string(99)
 
