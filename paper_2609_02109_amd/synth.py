@@ -20,8 +20,9 @@ Feature columns of an option row (L >= 8):
   4  VRAM (GB)            U[1, 40]
   5  bandwidth demand     U[0.05, 0.6]
   6+ noise                U[0, 1]
-Continuous columns are quantised to multiples of 2**-14, so every aggregate
-sum of at most 16 rows is exact in fp32 whatever the summation order.
+Continuous columns are quantised to multiples of 2**-14 by default, so every
+aggregate sum of at most 16 rows is exact in fp32 whatever the summation
+order; make_instance(..., quantise=False) keeps them off the grid.
 
 Aggregate slots (each the sum over all N models of one option column):
   A=2: [sum SM, sum VRAM]
@@ -124,7 +125,7 @@ class Instance:
 def make_instance(n_options, n_local=8, n_agg=4, hidden1=32, hidden2=32, *,
                   seed=0, dtype="f32", vram_cap=None, vram_quantile=None,
                   sla_range=(0.5, 2.0), top_k=1, types=None,
-                  symmetric=False, name="custom", act="identity") -> Instance:
+                  symmetric=False, name="custom", act="identity", quantise=True) -> Instance:
     """Draw one instance.
 
     n_options: option count per model.  types: per-model family (0 LLM, 1
@@ -135,6 +136,10 @@ def make_instance(n_options, n_local=8, n_agg=4, hidden1=32, hidden2=32, *,
     symmetric: copy model 0's option table and weights to every model (all
     options counts must agree).  act: the surrogates' output activation
     ("sigmoid": outputs in (0, 1), so latency bounds belong in (0, 1)).
+    quantise: put the continuous feature columns on the 2^-14 grid (default;
+    every aggregate sum is then exact in fp32 whatever the order); False keeps
+    the drawn values rounded to fp32 only, as real profiling tables would
+    come, so the aggregate's fp32 sums round.
     """
     if act not in ("identity", "sigmoid"):
         raise ValueError(f"unknown output activation {act!r}")
@@ -150,6 +155,7 @@ def make_instance(n_options, n_local=8, n_agg=4, hidden1=32, hidden2=32, *,
     rng = np.random.Generator(np.random.PCG64(seed))
     L, A = n_local, n_agg
     n_in = L + A
+    q = _quantise if quantise else (lambda v: v.astype(np.float32).astype(np.float64))
 
     # --- option tables ---
     rows = []
@@ -159,10 +165,10 @@ def make_instance(n_options, n_local=8, n_agg=4, hidden1=32, hidden2=32, *,
         f[:, COL_LLM] = 1.0 if types[i] == 0 else 0.0
         f[:, COL_VIS] = 1.0 if types[i] == 1 else 0.0
         f[:, COL_LOG2B] = rng.integers(0, 6, K)
-        f[:, COL_SM] = _quantise(rng.uniform(0.1, 1.0, K))
-        f[:, COL_VRAM] = _quantise(rng.uniform(1.0, 40.0, K))
-        f[:, COL_BW] = _quantise(rng.uniform(0.05, 0.6, K))
-        f[:, 6:] = _quantise(rng.uniform(0.0, 1.0, (K, L - 6)))
+        f[:, COL_SM] = q(rng.uniform(0.1, 1.0, K))
+        f[:, COL_VRAM] = q(rng.uniform(1.0, 40.0, K))
+        f[:, COL_BW] = q(rng.uniform(0.05, 0.6, K))
+        f[:, 6:] = q(rng.uniform(0.0, 1.0, (K, L - 6)))
         rows.append(f)
     if symmetric:
         if len(set(int(k) for k in n_options)) != 1:

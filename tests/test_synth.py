@@ -88,3 +88,18 @@ def test_n5_cap_admits_about_the_papers_78732(seed, n_vram):
     # itertools order agrees with the broadcast order used above
     first = list(itertools.islice(itertools.product(*[range(k) for k in inst.n_options]), 3))
     assert sums[2] == sum(cols[i][first[2][i]] for i in range(inst.n_models))
+
+
+def test_off_grid_option_keeps_the_drawn_values():
+    # quantise=False: the same draws, rounded to fp32 only (off the 2^-14
+    # grid); same seed, same bytes; the integer and one-hot columns and the
+    # weights are unchanged
+    a = synth.make_instance([12, 12, 9, 9, 9], seed=3, vram_quantile=0.75)
+    b = synth.make_instance([12, 12, 9, 9, 9], seed=3, vram_quantile=0.75, quantise=False)
+    c = synth.make_instance([12, 12, 9, 9, 9], seed=3, vram_quantile=0.75, quantise=False)
+    assert b.features.tobytes() == c.features.tobytes()
+    cont = b.features[:, 3:].astype(np.float64)
+    assert np.mean(cont * 2 ** 14 != np.round(cont * 2 ** 14)) > 0.9
+    assert np.array_equal(a.features[:, :3], b.features[:, :3])
+    assert np.all(np.abs(a.features[:, 3:] - b.features[:, 3:]) <= 2.0 ** -15)
+    assert np.all(np.isfinite(b.weights))
