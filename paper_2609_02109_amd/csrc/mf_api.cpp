@@ -20,9 +20,11 @@
 using namespace mfi;
 
 namespace {
-// Start and end events of the timed kernel of one search.
+// What one search call holds while it runs: the start and end events of its
+// timed kernel, and a pinned host copy of the small-range result block.
 struct EventPair {
     hipEvent_t a = nullptr, b = nullptr;
+    mfi::DevResult *h_res = nullptr;
 };
 }  // namespace
 
@@ -39,6 +41,7 @@ struct mf_problem {
     bool fast_ok = false;
     int num_cus = 0;
     int device = 0;
+    double wall_khz = 0.0;      // device wall-clock ticks per millisecond
     // device tables: pointers into the caller's buffer (borrowed until destroy)
     void *d_tables = nullptr;
     void *d_scratch = nullptr;   // this device's copy of the no-allocation scratch
@@ -119,6 +122,7 @@ bool create_event_pair(EventPair &e)
         e.a = nullptr;
         return false;
     }
+    if (hipHostMalloc((void **)&e.h_res, sizeof(DevResult), hipHostMallocDefault) != hipSuccess) e.h_res = nullptr;
     return true;
 }
 
@@ -147,6 +151,7 @@ public:
     EventLease &operator=(const EventLease &) = delete;
     hipEvent_t start() const { return ev_.a; }
     hipEvent_t stop() const { return ev_.b; }
+    DevResult *host_result() const { return ev_.h_res; }
 
 private:
     mf_problem *p_;
@@ -389,9 +394,11 @@ void stride_digits(const mf_problem &p, uint64_t stride, uint32_t *out)
 
 // Workspace layout for one search launch set over n configurations.
 struct WsLayout {
-    size_t res, work, workJ, collect, lists, counts, cand, entJ, entF, parts, total;
-    uint32_t work_cap, collect_cap;
-    int kp, grid, waves, n_parts;
+    size_t res, work, workJ, collect, lists, counts, cand, entJ, entF, parts, seg, segJ, segJc, segF, rec, candJ, candF,
+        total;
+    uint32_t work_cap, collect_cap, seg_cap;
+    int kp, grid, waves, n_parts, eval_top;
+    bool small;   // fp32 path over at most kSmallRange configurations: fast kernel + finish kernel
 };
 
 WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k, uint32_t worklist_cap)
@@ -432,6 +439,25 @@ WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k, uint32_t worklist
     // the exact selection runs in two levels over long ranges
     w.n_parts = n > kSelSingleMax ? kSelParts : 1;
     w.parts = o; o = align256(o + (w.n_parts > 1 ? (size_t)w.n_parts * sizeof(SelPart) : 0));
+    // small ranges: a certification segment per workgroup (its upper bounds,
+    // canonical J and flags), the canonical values of each workgroup's first
+    // eval_top list entries, and its record.  eval_top: at least 4 and k/2 + 1
+    // (the workgroups scan runs of consecutive configurations, so one of them
+    // may hold several of the best), and enough that the evaluated entries of
+    // all workgroups cover twice the top-k.  Too few evaluated entries only
+    // cost the fallback pass, never exactness.
+    w.small = !p.bf_ok && n <= kSmallRange && w.grid < 512;
+    w.seg_cap = w.small ? (uint32_t)(((uint64_t)w.work_cap + w.grid - 1) / w.grid) : 0;
+    w.eval_top = std::min(w.kp, std::max(std::max(4, top_k / 2 + 1), (2 * top_k + w.grid - 1) / w.grid + 2));
+    const size_t n_seg = (size_t)w.seg_cap * (w.small ? w.grid : 0);
+    const size_t n_cand = w.small ? (size_t)w.grid * w.eval_top : 0;
+    w.seg = o; o = align256(o + n_seg * 8);
+    w.segJ = o; o = align256(o + n_seg * 4);
+    w.segJc = o; o = align256(o + n_seg * 8);
+    w.segF = o; o = align256(o + n_seg * 4);
+    w.rec = o; o = align256(o + (w.small ? (size_t)w.grid * 32 : 0));
+    w.candJ = o; o = align256(o + n_cand * 8);
+    w.candF = o; o = align256(o + n_cand * 4);
     w.total = o;
     return w;
 }
@@ -592,22 +618,85 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
         if ((x) != hipSuccess) return MF_EDEVICE;   \
     } while (0)
 
-    MF_HIP2(hipMemsetAsync(R, 0, sizeof(DevResult), s));
-    if (ev0) MF_HIP2(hipEventRecord(ev0, s));
-    MF_HIP2(launch_fast_path(p, fa, w.grid, w.kp, kModeSearch, s));
-    if (ev1) MF_HIP2(hipEventRecord(ev1, s));
-    MF_HIP2(launch_merge_lists(lists, w.grid, w.kp, cand, counts, &R->n_vram, s));
-    ca.phase = 0;
-    MF_HIP2(launch_canonical(ca, w.kp, true, s));
-    MF_HIP2(launch_kth_candidate(cand, entJ, entF, w.kp, args->top_k, R, s));
-    ca.phase = 1;
-    MF_HIP2(launch_canonical(ca, (int)std::min<uint64_t>(w.work_cap, 1u << 20), true, s));
-    MF_HIP2(launch_select(sa, s));
     DevResult h{};
-    MF_HIP2(hipMemcpyAsync(&h, R, sizeof(DevResult), hipMemcpyDeviceToHost, s));
-    MF_HIP2(hipStreamSynchronize(s));
     float ms = 0.f;
-    if (ev0) MF_HIP2(hipEventElapsedTime(&ms, ev0, ev1));
+    // the small path's fast kernel keeps its certification tail's buffers
+    // after the workgroup lists in LDS
+    const size_t ep_bytes = fast_small_epilogue_bytes(p->N);
+    const size_t small_lds = (size_t)p->lay.total_floats * 4 + kFastPar * 4 + (size_t)w.waves * w.kp * 8 + ep_bytes;
+    if (w.small && small_lds <= 163840) {
+        // two launches and no memset: the fast kernel leaves per-workgroup
+        // lists, counts and certification segments; one workgroup completes
+        // the search and writes every field of the result block; the fast
+        // kernel's time comes from the workgroups' wall-clock stamps
+        fa.small = 1;
+        fa.ep_bytes = (int)ep_bytes;
+        fa.canon = p->d_canon;
+        fa.seg_cap = w.seg_cap;
+        fa.seg = reinterpret_cast<unsigned long long *>(ws + w.seg);
+        fa.seg_J = reinterpret_cast<float *>(ws + w.segJ);
+        fa.seg_Jc = reinterpret_cast<double *>(ws + w.segJc);
+        fa.seg_F = reinterpret_cast<uint32_t *>(ws + w.segF);
+        fa.wg_rec = reinterpret_cast<unsigned long long *>(ws + w.rec);
+        fa.eval_top = w.eval_top;
+        fa.cand_J = reinterpret_cast<double *>(ws + w.candJ);
+        fa.cand_F = reinterpret_cast<uint32_t *>(ws + w.candF);
+        fa.wstride = p->wstride;
+        fa.features = p->d_features;
+        fa.agg_cols = p->d_agg_cols;
+        fa.n_local = p->L;
+        fa.vram_slot = p->vram_slot;
+        MF_HIP2(launch_fast_path(p, fa, w.grid, w.kp, kModeSearch, s));
+        FinishArgs fin{};
+        fin.res = R;
+        fin.res_host = ev.host_result();
+        fin.omega = args->d_omega;
+        fin.lo = lo;
+        fin.top_k = args->top_k;
+        fin.kp = w.kp;
+        fin.eval_top = w.eval_top;
+        fin.n_wg = w.grid;
+        fin.seg_cap = w.seg_cap;
+        fin.work_cap = w.work_cap;
+        fin.work_out = work;
+        fin.work_J_out = workJ;
+        fin.wg_lists = lists;
+        fin.wg_counts = counts;
+        fin.wg_rec = fa.wg_rec;
+        fin.seg = fa.seg;
+        fin.seg_J = fa.seg_J;
+        fin.seg_Jc = fa.seg_Jc;
+        fin.seg_F = fa.seg_F;
+        fin.cand_J = fa.cand_J;
+        fin.cand_F = fa.cand_F;
+        MF_HIP2(launch_finish_small(fin, p->fc, s));
+        if (fin.res_host) {
+            // the finish kernel writes the result into pinned host memory
+            MF_HIP2(hipStreamSynchronize(s));
+            std::memcpy(&h, fin.res_host, sizeof(DevResult));
+        } else {
+            MF_HIP2(hipMemcpyAsync(&h, R, sizeof(DevResult), hipMemcpyDeviceToHost, s));
+            MF_HIP2(hipStreamSynchronize(s));
+        }
+        if (!(h.status & kStatWorkOverflow)) ms = (float)((double)h.fast_ticks / p->wall_khz);
+        fa.small = 0;
+        fa.ep_bytes = 0;
+    } else {
+        MF_HIP2(hipMemsetAsync(R, 0, sizeof(DevResult), s));
+        if (ev0) MF_HIP2(hipEventRecord(ev0, s));
+        MF_HIP2(launch_fast_path(p, fa, w.grid, w.kp, kModeSearch, s));
+        if (ev1) MF_HIP2(hipEventRecord(ev1, s));
+        MF_HIP2(launch_merge_lists(lists, w.grid, w.kp, cand, counts, &R->n_vram, s));
+        ca.phase = 0;
+        MF_HIP2(launch_canonical(ca, w.kp, true, s));
+        MF_HIP2(launch_kth_candidate(cand, entJ, entF, w.kp, args->top_k, R, s));
+        ca.phase = 1;
+        MF_HIP2(launch_canonical(ca, (int)std::min<uint64_t>(w.work_cap, 1u << 20), true, s));
+        MF_HIP2(launch_select(sa, s));
+        MF_HIP2(hipMemcpyAsync(&h, R, sizeof(DevResult), hipMemcpyDeviceToHost, s));
+        MF_HIP2(hipStreamSynchronize(s));
+        if (ev0) MF_HIP2(hipEventElapsedTime(&ms, ev0, ev1));
+    }
 
     if (h.status & kStatWorkOverflow) {
         outcome = kRangeSplit;
@@ -1063,6 +1152,18 @@ TableLayout table_layout(const mf_desc &d, const Shape &sh)
         ly.total_floats = (o + 3) & ~3;
         const size_t lds = (size_t)ly.total_floats * 4 + kFastPar * 4 + (size_t)kSearchWaves * 64 * 8;
         if (lds > 163840) t.fast_ok = false;
+        // the canonical first layer of every model goes into the image when
+        // the image, 16 waves' lists and the small-range tail still fit
+        ly.off_c1 = -1;
+        ly.off_feat = -1;
+        ly.c1_stride = (L + A) * H + H;
+        const int with_c1 = (ly.total_floats + N * ly.c1_stride + sumK * L + 3) & ~3;
+        if ((size_t)with_c1 * 4 + kFastPar * 4 + (size_t)kSearchWavesWide * 64 * 8 + fast_small_epilogue_bytes(N) <=
+            163840) {
+            ly.off_c1 = ly.total_floats;
+            ly.off_feat = ly.off_c1 + N * ly.c1_stride;
+            ly.total_floats = with_c1;
+        }
     }
     // bf16 fast path: H1 == H2 in {64, 128, 256}, A in {2,4,6,8}
     t.bf_ok = bf16 && H1 == H2 && bf16_kernel_supported(N, A, H1);
@@ -1212,12 +1313,15 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
                 if (!bf16_exact(w[n1 + H1 + n2 + H2 + t])) { delete p; return MF_EINVAL; }
         }
     }
+    int wall_rate = 0;
     if (hipGetDevice(&p->device) != hipSuccess ||
         hipDeviceGetAttribute(&p->num_cus, hipDeviceAttributeMultiprocessorCount, p->device) != hipSuccess ||
+        hipDeviceGetAttribute(&wall_rate, hipDeviceAttributeWallClockRate, p->device) != hipSuccess ||
         scratch_ptr(p->device, &p->d_scratch) != hipSuccess) {
         delete p;
         return MF_EDEVICE;
     }
+    p->wall_khz = wall_rate > 0 ? (double)wall_rate : 1e5;
 
     // aggregate centre per slot: the mean of the slot over the joint space
     // (sum over models of the mean option value), rounded to the 2^-14 grid
@@ -1282,6 +1386,16 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
             for (int st = 0; st < 4; st++) {
                 const int k = 2 * st + hf;
                 img[ly.off_c + hf * 4 + st] = k < A ? p->centre[perm[k]] : 0.f;
+            }
+        if (ly.off_feat >= 0) std::memcpy(img + ly.off_feat, F.data(), F.size() * 4);
+        if (ly.off_c1 >= 0)
+            for (int i = 0; i < N; i++) {
+                const float *w = W.data() + (int64_t)i * p->wstride;
+                float *c1 = img + ly.off_c1 + i * ly.c1_stride;
+                for (int h = 0; h < H; h++) {
+                    for (int k = 0; k < nin; k++) c1[k * H + h] = w[(int64_t)h * nin + k];
+                    c1[nin * H + h] = w[(int64_t)H * nin + h];
+                }
             }
         for (int i = 0; i < N; i++)
             model_bounds(*p, F, W, i, &p->fc.bound_lat[i], &p->fc.bound_thr[i], &p->fc.mag_thr[i]);
@@ -1385,7 +1499,6 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     std::memcpy(himg.data() + tl.o_c, p->centre.data(), (size_t)A * 4);
     double *w64 = reinterpret_cast<double *>(himg.data() + tl.o_w64);
     for (size_t t = 0; t < W.size(); t++) w64[t] = (double)W[t];
-
     // ---- the caller's buffer
     char *base = (char *)d_tables;
     p->d_tables = d_tables;
@@ -1429,6 +1542,7 @@ void mf_problem_destroy(mf_problem *p)
     for (const EventPair &e : p->ev_all) {
         (void)hipEventDestroy(e.a);
         (void)hipEventDestroy(e.b);
+        if (e.h_res) (void)hipHostFree(e.h_res);
     }
     delete p;
 }

@@ -14,6 +14,8 @@
 // candidates, short index lists) are latency-bound: there (FEW) wave w runs
 // the forward of the entry's models w, w + W, ... on its own scratch, and
 // wave 0 combines them in model order.
+#include <algorithm>
+
 #include "mf_canon.h"
 
 namespace mfi {
@@ -378,6 +380,263 @@ hipError_t launch_select(const SelectArgs &a, hipStream_t s)
         hipLaunchKernelGGL(select_kernel<1>, dim3(a.n_parts), dim3(kSelWaves * 64), 0, s, a, a.parts, a.n_parts);
         hipLaunchKernelGGL(select_kernel<2>, dim3(1), dim3(kSelWaves * 64), 0, s, a, a.parts, a.n_parts);
     }
+    return hipGetLastError();
+}
+
+}  // namespace mfi
+
+// ---------------------------------------------------------------------------
+// Small ranges: the rest of the search in one workgroup.  The fast kernel's
+// workgroups have already evaluated canonically their first list entries and
+// their certification segments; this kernel sums counts and selects.
+// ---------------------------------------------------------------------------
+namespace mfi {
+
+constexpr int kFinWaves = 8;
+
+// Segment of certification entry e: the last workgroup whose exclusive
+// prefix is <= e (empty segments share their offset with the next).
+__device__ __forceinline__ int seg_of(const uint32_t *off, int n_wg, uint32_t e)
+{
+    int lo = 0, hi = n_wg;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (off[mid] <= e) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ unsigned long long wave_max64(unsigned long long x)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+        const unsigned long long o = shfl_xor64(x, m);
+        x = o > x ? o : x;
+    }
+    return x;
+}
+
+__device__ __forceinline__ unsigned long long wave_min64(unsigned long long x)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+        const unsigned long long o = shfl_xor64(x, m);
+        x = o < x ? o : x;
+    }
+    return x;
+}
+
+__global__ void __launch_bounds__(kFinWaves * 64) finish_small_kernel(const FinishArgs f, const FastConst fc)
+{
+    extern __shared__ uint32_t woff[];   // [n_wg + 1] exclusive prefix of the segment lengths
+    __shared__ unsigned long long s_red[6][kFinWaves];
+    __shared__ unsigned int s_wsum[kFinWaves];
+    __shared__ unsigned long long s_feas;
+    __shared__ K128 klst[kFinWaves * 64];
+    constexpr int W = kFinWaves;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int k = f.top_k, T = f.eval_top, n_wg = f.n_wg;
+    DevResult *R = f.res;
+    if (tid == 0) s_feas = 0;
+
+    // ---- counts, wall-clock span, status bits and the largest unevaluated
+    // upper bound over the workgroups; exclusive prefix of the segment lengths
+    unsigned long long nv = 0, nf = 0, t0 = ~0ull, t1 = 0, ovf = 0, st = 0, rest = 0;
+    uint32_t len = 0;
+    if (tid < n_wg) {
+        const unsigned long long *r = f.wg_rec + 4 * (uint64_t)tid;
+        const unsigned long long nw = r[0];
+        ovf = nw > f.seg_cap ? 1u : 0u;
+        len = (uint32_t)(nw > f.seg_cap ? f.seg_cap : nw);
+        t0 = r[1];
+        t1 = r[2];
+        st = r[3] >> 32;
+        rest = r[3] & 0xFFFFFFFFull;
+        nv = f.wg_counts[2 * (uint64_t)tid];
+        nf = f.wg_counts[2 * (uint64_t)tid + 1];
+    }
+    nv = wave_sum64(nv);
+    nf = wave_sum64(nf);
+    ovf = wave_sum64(ovf);
+    t0 = wave_min64(t0);
+    t1 = wave_max64(t1);
+    rest = wave_max64(rest);
+    st = wave_max64(st);   // status bits: only kStatSelfCheck is set here
+    uint32_t incl = len;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t t = __shfl_up(incl, d);
+        if (lane >= d) incl += t;
+    }
+    if (lane == 63) {
+        s_wsum[wv] = incl;
+        s_red[0][wv] = nv;
+        s_red[1][wv] = nf;
+        s_red[2][wv] = ovf;
+        s_red[3][wv] = t0;
+        s_red[4][wv] = t1;
+        s_red[5][wv] = (rest << 32) | st;
+    }
+    __syncthreads();
+    uint32_t base = 0;
+    for (int w = 0; w < wv; w++) base += s_wsum[w];
+    if (tid <= n_wg) woff[tid] = base + incl - len;   // tid == n_wg: the total (len 0)
+    unsigned long long tnv = 0, tnf = 0, tovf = 0, tt0 = ~0ull, tt1 = 0, trest = 0, tst = 0;
+    for (int w = 0; w < W; w++) {
+        tnv += s_red[0][w];
+        tnf += s_red[1][w];
+        tovf += s_red[2][w];
+        tt0 = s_red[3][w] < tt0 ? s_red[3][w] : tt0;
+        tt1 = s_red[4][w] > tt1 ? s_red[4][w] : tt1;
+        const unsigned long long rs = s_red[5][w] >> 32;
+        trest = rs > trest ? rs : trest;
+        tst |= s_red[5][w] & 0xFFFFFFFFull;
+    }
+    __syncthreads();
+    const uint32_t n_work = woff[n_wg];
+    if (tovf || n_work > f.work_cap) {
+        if (tid == 0) {
+            R->status = kStatWorkOverflow;
+            R->n_work = (unsigned long long)f.work_cap + 1;
+            if (f.res_host) {
+                f.res_host->status = kStatWorkOverflow;
+                f.res_host->n_work = (unsigned long long)f.work_cap + 1;
+            }
+        }
+        return;
+    }
+    // the gathered certification list, for a fallback pass on the host's side
+    for (uint32_t e = tid; e < n_work; e += blockDim.x) {
+        const int g = seg_of(woff, n_wg, e);
+        const uint64_t at = (uint64_t)g * f.seg_cap + (e - woff[g]);
+        f.work_out[e] = f.seg[at];
+        f.work_J_out[e] = f.seg_J[at];
+    }
+
+    // ---- the exact top-k over the canonically evaluated entries: each
+    // workgroup's first T list entries (their keys, loaded with every load in
+    // flight at once, staged in LDS), then the certification entries
+    K128 slot = {0, 0}, thr = {0, 0};
+    const uint32_t n_cand = (uint32_t)n_wg * (uint32_t)T;
+    K128 *ckeys = reinterpret_cast<K128 *>(woff + ((n_wg + 4) & ~3));   // [n_cand]
+    for (uint32_t t = tid; t < n_cand; t += blockDim.x) {
+        const uint32_t g = t / T, j = t % T;
+        const uint32_t fl = f.cand_F[t];
+        const unsigned long long key = f.wg_lists[(uint64_t)g * f.kp + j];
+        const double J = f.cand_J[t];
+        const uint32_t off = 0xFFFFFFFFu - (uint32_t)(key & 0xFFFFFFFFull);
+        ckeys[t] = (fl & 4u) ? K128{ord_f64(J), ~(f.lo + off)} : K128{0, 0};
+    }
+    __syncthreads();
+    for (uint32_t b0 = (uint32_t)wv * 64; b0 < n_cand; b0 += W * 64) {
+        const uint32_t t = b0 + lane;
+        const K128 mine = t < n_cand ? ckeys[t] : K128{0, 0};
+        list128_offer_many(slot, mine, lane, k, thr);
+    }
+    unsigned long long my_feas = 0;
+    for (uint32_t b0 = (uint32_t)wv * 64; b0 < n_work; b0 += W * 64) {
+        const uint32_t e = b0 + lane;
+        K128 mine = {0, 0};
+        if (e < n_work) {
+            const int g = seg_of(woff, n_wg, e);
+            const uint64_t at = (uint64_t)g * f.seg_cap + (e - woff[g]);
+            if (f.seg_F[at] & 4u) {
+                my_feas++;
+                mine = {ord_f64(f.seg_Jc[at]), ~(f.lo + (uint32_t)(f.seg[at] & 0xFFFFFFFFull))};
+            }
+        }
+        list128_offer_many(slot, mine, lane, k, thr);
+    }
+    my_feas = wave_sum64(my_feas);
+    if (lane == 0 && my_feas) atomicAdd(&s_feas, my_feas);
+    // the waves' lists merge in a tree
+    klst[wv * 64 + lane] = key_if(lane < k, slot);
+#pragma unroll
+    for (int h = W / 2; h >= 1; h >>= 1) {
+        __syncthreads();
+        if (wv < h) {
+            list128_merge_sorted(slot, klst[(wv + h) * 64 + lane], lane, k, thr);
+            if (h > 1) klst[wv * 64 + lane] = slot;
+        }
+    }
+    if (wv == 0) {
+        const int n_top = __popcll(__ballot(lane < k && nz128(slot)));
+        const uint64_t kth_hi = readlane64(slot.hi, k - 1);
+        const bool ok = lane < n_top;
+        const unsigned long long tidx = ok ? ~slot.lo : ~0ull;
+        const double tJ = ok ? unord_f64(slot.hi) : -INFINITY;
+        R->top_idx[lane] = tidx;
+        R->top_J[lane] = tJ;
+        if (f.res_host) {
+            f.res_host->top_idx[lane] = tidx;
+            f.res_host->top_J[lane] = tJ;
+        }
+        if (lane == 0) {
+            // every sure-feasible configuration not evaluated has an upper
+            // bound U <= the largest first unevaluated list bound: exact when
+            // the k-th canonical J exceeds it (or nothing is unevaluated);
+            // otherwise the fallback collects every U >= C_k (every
+            // sure-feasible configuration when fewer than k were found)
+            const double restU = trest ? (double)unord_f32((uint32_t)trest) : -INFINITY;
+            unsigned stat = (unsigned)tst;
+            double Ck = -INFINITY;
+            bool verified;
+            if (n_top >= k) {
+                Ck = unord_f64(kth_hi);
+                verified = Ck > restU;
+            } else {
+                verified = trest == 0ull;
+            }
+            if (verified) stat |= kStatVerified;
+            R->n_vram = tnv;
+            R->n_feas_sure = tnf;
+            R->n_work = n_work;
+            R->n_collect = 0;
+            R->n_feas_cert = s_feas;
+            R->n_cand = 0;
+            R->status = stat;
+            R->n_top = n_top;
+            R->theta = Ck;
+            R->eJ = bound_eJ(fc, f.omega);
+            R->tail_U = restU;
+            R->check_max_dJ = 0.0;
+            R->ck_cand = Ck;
+            R->fast_ticks = tt1 > tt0 ? tt1 - tt0 : 0ull;
+            if (DevResult *H = f.res_host) {
+                // the host reads this copy after synchronising the stream
+                H->n_vram = tnv;
+                H->n_feas_sure = tnf;
+                H->n_work = n_work;
+                H->n_collect = 0;
+                H->n_feas_cert = s_feas;
+                H->n_cand = 0;
+                H->status = stat;
+                H->n_top = n_top;
+                H->theta = Ck;
+                H->tail_U = restU;
+                H->ck_cand = Ck;
+                H->fast_ticks = R->fast_ticks;
+            }
+        }
+    }
+}
+
+size_t finish_small_lds_bytes(const FinishArgs &f)
+{
+    return (size_t)((f.n_wg + 4) & ~3) * 4 + (size_t)f.n_wg * f.eval_top * sizeof(K128);
+}
+
+hipError_t launch_finish_small(const FinishArgs &f, const FastConst &fc, hipStream_t s)
+{
+    if (f.kp < 1 || f.kp > 64 || f.n_wg < 1 || f.n_wg >= kFinWaves * 64 || f.top_k < 1 || f.top_k > 64 ||
+        f.eval_top < 1 || f.eval_top > f.kp)
+        return hipErrorInvalidValue;
+    const size_t lds = finish_small_lds_bytes(f);
+    if (lds > 163840) return hipErrorInvalidValue;
+    hipError_t e = ensure_dyn_lds((const void *)finish_small_kernel, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(finish_small_kernel, dim3(1), dim3(kFinWaves * 64), lds, s, f, fc);
     return hipGetLastError();
 }
 

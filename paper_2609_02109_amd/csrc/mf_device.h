@@ -92,10 +92,17 @@ __device__ __forceinline__ unsigned long long readlane64(unsigned long long x, i
     return ((unsigned long long)hi << 32) | lo;
 }
 
+// x of lane - 1 (lane 0: unspecified), by the DPP whole-wave shift; the
+// whole wave must be active.
+__device__ __forceinline__ double readlane_f64(double x, int src)
+{
+    return __longlong_as_double((long long)readlane64((unsigned long long)__double_as_longlong(x), src));
+}
+
 __device__ __forceinline__ unsigned long long shfl_up1_64(unsigned long long x)
 {
-    const uint32_t lo = __shfl_up((int)(uint32_t)x, 1);
-    const uint32_t hi = __shfl_up((int)(uint32_t)(x >> 32), 1);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)x, 0x138, 0xF, 0xF, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)(x >> 32), 0x138, 0xF, 0xF, false);
     return ((unsigned long long)hi << 32) | lo;
 }
 
@@ -162,10 +169,45 @@ __device__ __forceinline__ unsigned long long shfl64(unsigned long long x, int s
     return ((unsigned long long)hi << 32) | lo;
 }
 
+// x of lane (lane ^ m), m in {1, 2, 4, 8, 16, 32} (a constant after
+// unrolling): DPP moves within rows of 16 lanes (quad permutations, the
+// half-row mirror, a rotation by 8) and the gfx950 permlane swaps across
+// rows, all VALU operations.  The whole wave must be active.
+__device__ __forceinline__ uint32_t xor_lane32(uint32_t x, int m)
+{
+    switch (m) {
+        case 1: return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+        case 2: return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+        case 4: {   // half-row mirror, then quad_perm [3,2,1,0]
+            const int h = __builtin_amdgcn_mov_dpp((int)x, 0x141, 0xF, 0xF, false);
+            return (uint32_t)__builtin_amdgcn_mov_dpp(h, 0x1B, 0xF, 0xF, false);
+        }
+        case 8: return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x128, 0xF, 0xF, false);  // row_ror:8
+        case 16: {
+            const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+            return (__lane_id() & 16) ? r[0] : r[1];
+        }
+        default: {
+            const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+            return (__lane_id() & 32) ? r[0] : r[1];
+        }
+    }
+}
+
 __device__ __forceinline__ unsigned long long shfl_xor64(unsigned long long x, int m)
 {
-    const uint32_t lo = __shfl_xor((int)(uint32_t)x, m);
-    const uint32_t hi = __shfl_xor((int)(uint32_t)(x >> 32), m);
+    const uint32_t lo = xor_lane32((uint32_t)x, m);
+    const uint32_t hi = xor_lane32((uint32_t)(x >> 32), m);
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+// x of lane 63 - lane: mirror within rows of 16, then swap the rows (lane ^ 48).
+__device__ __forceinline__ unsigned long long reverse64(unsigned long long x)
+{
+    uint32_t lo = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)x, 0x140, 0xF, 0xF, false);
+    uint32_t hi = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)(x >> 32), 0x140, 0xF, 0xF, false);
+    lo = xor_lane32(xor_lane32(lo, 16), 32);
+    hi = xor_lane32(xor_lane32(hi, 16), 32);
     return ((unsigned long long)hi << 32) | lo;
 }
 
@@ -190,7 +232,7 @@ __device__ __forceinline__ void wl_merge_sorted(WaveList<NS> &L, const unsigned 
     unsigned long long c[NS];
 #pragma unroll
     for (int j = 0; j < NS; j++) {
-        const unsigned long long r = shfl64(b[NS - 1 - j], 63 - lane);
+        const unsigned long long r = reverse64(b[NS - 1 - j]);
         c[j] = L.s[j] > r ? L.s[j] : r;
     }
     if constexpr (NS == 2) {   // stride 64: the two registers of a lane
@@ -248,6 +290,25 @@ __device__ __forceinline__ void wl_offer(WaveList<NS> &L, unsigned long long myk
     }
 }
 
+// wl_offer for one-register lists when many keys may pass at once (a list
+// still filling): above four passing keys the wave's keys are sorted
+// descending by a bitonic network and merged into the list in one step.
+__device__ __forceinline__ void wl_offer_many(WaveList<1> &L, unsigned long long mykey, int lane, int kp)
+{
+    const bool pass = mykey > L.thr;
+    if (__popcll(__ballot(pass)) <= 4) {
+        wl_offer(L, mykey, lane, kp);
+        return;
+    }
+    unsigned long long x = pass ? mykey : 0ull;
+#pragma unroll
+    for (int k = 2; k <= 64; k <<= 1)
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1) x = cx_lane(x, j, lane, (lane & k) == 0);
+    const unsigned long long b[1] = {x};
+    wl_merge_sorted(L, b, lane, kp);
+}
+
 // Selection on 128-bit keys (K128): a wave keeps the best k <= 64 keys
 // sorted, slot lane in lane (thr: the k-th key once the list is full, 0
 // before).
@@ -289,6 +350,55 @@ __device__ __forceinline__ void list128_offer(K128 &slot, const K128 &mine, int 
         }
         thr = {readlane64(slot.hi, k - 1), readlane64(slot.lo, k - 1)};
     }
+}
+
+__device__ __forceinline__ K128 shfl_xor128(const K128 &x, int m) { return {shfl_xor64(x.hi, m), shfl_xor64(x.lo, m)}; }
+
+// Compare-exchange of 128-bit keys with the lane m apart (the lower lane
+// of the pair keeps the larger key when desc).
+__device__ __forceinline__ K128 cx128(const K128 &x, int m, int lane, bool desc)
+{
+    const K128 o = shfl_xor128(x, m);
+    const bool xg = gt128(x, o);
+    const bool keep_max = ((lane & m) == 0) == desc;
+    const bool take_x = keep_max == xg;
+    return K128{take_x ? x.hi : o.hi, take_x ? x.lo : o.lo};
+}
+
+// list128_offer when many keys may pass at once: above four passing keys the
+// wave's keys are sorted descending (bitonic) and merged into the list (the
+// elementwise maximum of the list and the sorted keys reversed is bitonic;
+// six half-cleaner stages sort it); the list keeps its k best.
+__device__ __forceinline__ void list128_offer_many(K128 &slot, const K128 &mine, int lane, int k, K128 &thr)
+{
+    const bool pass = nz128(mine) && gt128(mine, thr);
+    if (__popcll(__ballot(pass)) <= 4) {
+        list128_offer(slot, mine, lane, k, thr);
+        return;
+    }
+    K128 x = key_if(pass, mine);
+#pragma unroll
+    for (int kk = 2; kk <= 64; kk <<= 1)
+#pragma unroll
+        for (int j = kk >> 1; j > 0; j >>= 1) x = cx128(x, j, lane, (lane & kk) == 0);
+    const K128 r = {reverse64(x.hi), reverse64(x.lo)};
+    K128 c = gt128(slot, r) ? slot : r;
+#pragma unroll
+    for (int j = 32; j > 0; j >>= 1) c = cx128(c, j, lane, true);
+    slot = key_if(lane < k, c);
+    thr = {readlane64(slot.hi, k - 1), readlane64(slot.lo, k - 1)};
+}
+
+// Merge another wave's sorted list b (slot lane, zeros past its end) into
+// this wave's list.
+__device__ __forceinline__ void list128_merge_sorted(K128 &slot, const K128 &b, int lane, int k, K128 &thr)
+{
+    const K128 r = {reverse64(b.hi), reverse64(b.lo)};
+    K128 c = gt128(slot, r) ? slot : r;
+#pragma unroll
+    for (int j = 32; j > 0; j >>= 1) c = cx128(c, j, lane, true);
+    slot = key_if(lane < k, c);
+    thr = {readlane64(slot.hi, k - 1), readlane64(slot.lo, k - 1)};
 }
 
 // Append flagged lanes' values to a device list; the counter keeps counting

@@ -15,7 +15,7 @@ constexpr int kSearchWaves = 8;          // waves per workgroup of the fast sear
 constexpr int kSearchWavesWide = 16;     // ... when registers and LDS allow 4 waves per SIMD
 constexpr int kCertWaves = 4;            // waves per workgroup of the canonical kernels
 constexpr int kDefaultWorklist = 1 << 20; // certification list capacity (entries)
-constexpr int kFastPar = 128;            // floats of per-model parameters after the fp32 fast image in LDS
+constexpr int kFastPar = 160;            // floats of per-model parameters after the fp32 fast image in LDS
 constexpr int kBf16Waves = 8;            // waves per workgroup of the bf16 fast kernel
 constexpr int kBf16Tiles = 8;            // 32-configuration tiles per wave and model staging
 constexpr int kBf16Par = 128;            // floats of per-model parameters after the bf16 tables in LDS
@@ -38,10 +38,15 @@ constexpr int kBf16Par = 128;            // floats of per-model parameters after
 //   c  [half][4]                   aggregate centre in the same order: layer 1
 //                                  takes a - c (exact on the 2^-14 grid) and
 //                                  P carries W1_agg c
+//   c1 [i][nin][H], [i][H]         (when it fits) each model's W1 transposed and
+//                                  b1 as given, for canonical evaluation
+//   feat [row][L]                  (with c1) the option table
 // ---------------------------------------------------------------------------
 struct FastLayout {
     int H, A, AP, MB, S1, PST;
     int off_w1a, off_b2, off_w2, off_w3, off_b3, off_p, off_g, off_c;
+    int off_c1, c1_stride;     // canonical first layer per model, W1T[nin][H] then b1[H] (-1: not in the image)
+    int off_feat;              // the option table [sumK][L] (with the c1 block; -1: not in the image)
     int total_floats;          // multiple of 4
 };
 
@@ -82,6 +87,8 @@ struct DevResult {
     double tail_U;              // upper bound U of the last fast candidate (list full)
     double check_max_dJ;        // max (U - canonical J) seen on candidates
     double ck_cand;             // k-th canonical J among the fast candidates
+    unsigned long long fast_ticks;  // small ranges: wall-clock ticks from the first workgroup's start
+                                    // to the last one's end of the fast kernel
 };
 constexpr unsigned kStatVerified = 1u;      // top-k exactness condition held
 constexpr unsigned kStatSelfCheck = 2u;     // a fast decision disagreed with canonical
@@ -126,6 +133,30 @@ struct FastArgs {
     uint8_t *mask;              // dump (optional)
     float *pred;                // dump (optional)
     ObjArgs obj;
+    int ep_bytes;               // LDS bytes after the workgroup lists for the small-range certification
+    const float *canon;         // canonical fp32 image [N][wstride] (W1T[nin][H1], b1, ...)
+    // Small ranges (search mode, completed by the finish kernel): no global
+    // counter.  Certification entries go to a segment of seg_cap entries per
+    // workgroup; after its scan each workgroup evaluates canonically its first
+    // eval_top list entries (cand_J / cand_F [grid][eval_top]) and its segment
+    // (seg_Jc / seg_F), and writes wg_rec[4 g] = {entries offered (may exceed
+    // seg_cap), start and end wall-clock ticks, status bits << 32 | the
+    // order-preserving bits of the upper bound U of list entry eval_top (0:
+    // none)}.
+    int small;
+    uint32_t seg_cap;
+    unsigned long long *seg;
+    float *seg_J;
+    double *seg_Jc;
+    uint32_t *seg_F;
+    unsigned long long *wg_rec;
+    int eval_top;
+    double *cand_J;
+    uint32_t *cand_F;
+    int64_t wstride;
+    const float *features;      // [sumK][n_local]
+    const int32_t *agg_cols;    // [A] (original slot order)
+    int n_local, vram_slot;
 };
 
 // ---------------------------------------------------------------------------
@@ -227,6 +258,33 @@ struct CanonArgs {
     double *pred;               // list mode optional [n][N][2]
     uint8_t *mask;              // search dump: patch worklist entries
     ObjArgs obj;
+};
+
+// The rest of a small-range search after the fast kernel, in one workgroup:
+// sum the workgroups' counts, gather the certification segments into one
+// list (for a fallback pass), select the exact top-k among the canonically
+// evaluated entries (each workgroup's first eval_top list entries and every
+// certification entry) and fill the result block.  The top-k is exact when
+// its k-th canonical J exceeds every workgroup's first unevaluated upper
+// bound; otherwise the status asks for the fallback (collect) pass.
+struct FinishArgs {
+    DevResult *res;
+    DevResult *res_host;            // optional copy in pinned host memory (counts, status, top-k)
+    const float *omega;
+    uint64_t lo;
+    int top_k, kp, eval_top, n_wg;
+    uint32_t seg_cap, work_cap;
+    unsigned long long *work_out;   // gathered certification list [work_cap]
+    float *work_J_out;
+    const unsigned long long *wg_lists;   // [n_wg][kp]
+    const unsigned long long *wg_counts;  // [n_wg][2]
+    const unsigned long long *wg_rec;     // [n_wg][4]
+    const unsigned long long *seg;
+    const float *seg_J;
+    const double *seg_Jc;
+    const uint32_t *seg_F;
+    const double *cand_J;
+    const uint32_t *cand_F;
 };
 
 // One workgroup's share of the exact top-k selection over a long entry list.
@@ -377,6 +435,10 @@ hipError_t launch_canonical(const CanonArgs &a, int n_entries_max, bool search_m
 hipError_t launch_kth_candidate(const unsigned long long *cand_keys, const double *ent_J, const uint32_t *ent_flags,
                                 int kp, int k, DevResult *res, hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, hipStream_t s);
+hipError_t launch_finish_small(const FinishArgs &f, const FastConst &fc, hipStream_t s);
+size_t finish_small_lds_bytes(const FinishArgs &f);
+size_t fast_small_epilogue_bytes(int n_models);
+constexpr uint64_t kSmallRange = 1ull << 20;   // fp32 ranges up to this size finish in one workgroup
 size_t fixed_lds_bytes(int sumK, bool eq3);
 size_t static_lds_bytes(int n_steps, int sumK, int n_models, bool eq3);
 hipError_t launch_fixed_table(const FixedArgs &a, hipStream_t s);

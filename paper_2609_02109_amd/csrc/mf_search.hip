@@ -22,11 +22,210 @@
 //                workgroup at the end
 // Everything the kernel reads per configuration lives in LDS; the only HBM
 // traffic is the image load in the prologue and O(K') results.
-#include "mf_device.h"
+#include "mf_canon.h"
 
 namespace mfi {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+// Bytes of LDS (after the workgroup lists) the certification tail needs: the
+// evaluated list keys, a status word, per (entry, model) predictions of one
+// chunk of kCertChunk entries, and each chunk entry's option rows.
+constexpr int kCertChunk = 64;
+size_t fast_small_epilogue_bytes(int n_models)
+{
+    return 64 * 8 + 16 + (size_t)kCertChunk * n_models * 16 + (size_t)kCertChunk * kMaxN * 4;
+}
+
+// One model's surrogate (Eq. 6) on canonical semantics for one configuration
+// by one wave, with no barriers: lane u computes hidden unit u (H <= 64), and
+// each unit's chain takes its inputs in ascending order, broadcast from the
+// lanes that hold them (input k in lane k).  Layers 2 and 3 read the fp32
+// weights of the fast image in LDS (each lane its own row: W2 as laid out for
+// the layer-2 MFMA, four consecutive inputs contiguous), layer 1 the
+// canonical W1T / b1 block c1 (LDS or global).  fp32 weights are exact in
+// fp64.
+template <int H>
+__device__ inline void canon_forward_image(const float *c1, const float *img, const FastLayout &Ly, int i, int nin,
+                                           double z, int lane, bool sigmoid, double &lat, double &thr)
+{
+    constexpr int MB = H / 32;
+    const int u = lane < H ? lane : H - 1;   // lanes past H repeat the last unit and are ignored
+    double c = (double)c1[nin * H + u];
+    int k = 0;
+    for (; k + 8 <= nin; k += 8) {
+        float wv[8];
+#pragma unroll
+        for (int j = 0; j < 8; j++) wv[j] = c1[(k + j) * H + u];
+#pragma unroll
+        for (int j = 0; j < 8; j++) c = fma((double)wv[j], readlane_f64(z, k + j), c);
+    }
+    for (; k < nin; k++) c = fma((double)c1[k * H + u], readlane_f64(z, k), c);
+    const double h1 = c > 0.0 ? c : 0.0;
+    // layer 2: lane v = u; W2[v][u'] sits at ((((mb2 MB + mb1) 4 + q) 64 + l) 4 + j)
+    // with v = 32 mb2 + l % 32, u' = 32 mb1 + 8 q + 4 (l / 32) + j
+    const float *w2 = img + Ly.off_w2 + i * (H * H);
+    const int mb2 = u / 32, lv = u % 32;
+    c = (double)img[Ly.off_b2 + i * H + u];
+#pragma unroll
+    for (int u0 = 0; u0 < H; u0 += 8) {
+        const int mb1 = u0 / 32, q = (u0 % 32) / 8;
+        const float4 a0 = *reinterpret_cast<const float4 *>(w2 + ((((mb2 * MB + mb1) * 4 + q) * 64 + lv) * 4));
+        const float4 a1 = *reinterpret_cast<const float4 *>(w2 + ((((mb2 * MB + mb1) * 4 + q) * 64 + lv + 32) * 4));
+        const float wv[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+#pragma unroll
+        for (int j = 0; j < 8; j++) c = fma((double)wv[j], readlane_f64(h1, u0 + j), c);
+    }
+    const double h2 = c > 0.0 ? c : 0.0;
+    // layer 3: lanes 0 and 1, W3[o][v] contiguous in v
+    const int o = lane & 1;
+    const float *w3 = img + Ly.off_w3 + i * (2 * H) + o * H;
+    c = (double)img[Ly.off_b3 + 4 * i + o];
+#pragma unroll
+    for (int v0 = 0; v0 < H; v0 += 8) {
+        const float4 a0 = *reinterpret_cast<const float4 *>(w3 + v0);
+        const float4 a1 = *reinterpret_cast<const float4 *>(w3 + v0 + 4);
+        const float wv[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+#pragma unroll
+        for (int j = 0; j < 8; j++) c = fma((double)wv[j], readlane_f64(h2, v0 + j), c);
+    }
+    const double y = sigmoid ? canon_sigmoid(c) : c;
+    lat = readlane_f64(y, 0);
+    thr = readlane_f64(y, 1);
+}
+
+// Small ranges, after the scan: the workgroup evaluates canonically (the
+// defining semantics) its first eval_top list entries and the configurations
+// of its certification segment, one wave per (entry, model), then each
+// entry's constraints and J in model order (Section II, Eq. 3 and 4).  The
+// image stays in LDS; the tail's buffers follow the workgroup lists.
+// listkey: wave 0 holds the workgroup's sorted list, slot lane.
+template <int H, int WAVES, bool OBJ, bool SIG>
+__device__ inline void small_certify(const FastArgs &args, const FastConst &fc, float *smem, float *par,
+                                     unsigned long long listkey, int kp, unsigned int n_offered, int lane, int wv,
+                                     unsigned long long t_start)
+{
+    const FastLayout &Ly = args.lay;
+    const int N = fc.n_models, L = args.n_local, A = Ly.A, nin = L + A, T = args.eval_top;
+    const uint64_t g = blockIdx.x;
+    const int *pK = reinterpret_cast<const int *>(par + 112), *pOff = reinterpret_cast<const int *>(par + 48);
+    const int *pPrev = reinterpret_cast<const int *>(par + 80);
+    unsigned long long *ekey = reinterpret_cast<unsigned long long *>(par + kFastPar) + WAVES * kp;   // [64]
+    unsigned int *estat = reinterpret_cast<unsigned int *>(ekey + 64);                               // status, rest
+    double *eout = reinterpret_cast<double *>(ekey + 66);                                            // [chunk][N][2]
+    int *erow = reinterpret_cast<int *>(eout + (size_t)kCertChunk * N * 2);                          // [chunk][kMaxN]
+    if (wv == 0) {
+        ekey[lane] = lane < T ? listkey : 0ull;
+        // a bound on the upper bound U of every sure-feasible configuration
+        // of the workgroup left unevaluated: list entry T when the list goes
+        // past T, its last entry (itself evaluated) when T covers the whole
+        // list; 0 when the list ends before (nothing left)
+        const unsigned long long rest = readlane64(listkey, T < kp ? T : kp - 1);
+        if (lane == 0) {
+            estat[0] = 0;
+            estat[1] = (uint32_t)(rest >> 32);
+        }
+    }
+    __syncthreads();
+    const int n_list = __popcll(__ballot(lane < T && ekey[lane] != 0ull));
+    const int n_seg = (int)(n_offered < args.seg_cap ? n_offered : args.seg_cap);
+    const int n_ent = n_list + n_seg;
+    const int *pCols = reinterpret_cast<const int *>(par + 144);
+    const float *feat = Ly.off_feat >= 0 ? smem + Ly.off_feat : args.features;
+    for (int c0 = 0; c0 < n_ent; c0 += kCertChunk) {
+        const int nc = n_ent - c0 < kCertChunk ? n_ent - c0 : kCertChunk;
+        // each entry's option rows (model order)
+        for (int t = threadIdx.x; t < nc; t += WAVES * 64) {
+            const int e = c0 + t;
+            uint64_t x = args.lo + (e < n_list ? 0xFFFFFFFFu - (uint32_t)(ekey[e] & 0xFFFFFFFFull)
+                                               : (uint32_t)args.seg[g * args.seg_cap + (e - n_list)]);
+            for (int j = N - 1; j >= 0; j--) {
+                const uint64_t kj = (uint64_t)pK[j];
+                erow[t * kMaxN + j] = pOff[j] + (int)(x % kj);
+                x /= kj;
+            }
+        }
+        __syncthreads();
+        for (int q = wv; q < nc * N; q += WAVES) {
+            const int t = q / N, i = q % N;
+            const int *rows = erow + t * kMaxN;
+            const int row_i = rows[i];
+            double z = 0.0;
+            if (lane < L) {
+                z = (double)feat[row_i * L + lane];
+            } else if (lane < nin) {
+                const int col = pCols[lane - L];
+                float sa = 0.f;
+                for (int j = 0; j < N; j++) sa = sa + feat[rows[j] * L + col];
+                z = (double)sa;
+            }
+            const float *c1 = Ly.off_c1 >= 0 ? smem + Ly.off_c1 + i * Ly.c1_stride
+                                             : args.canon + (int64_t)i * args.wstride;
+            double lat, thr;
+            canon_forward_image<H>(c1, smem, Ly, i, nin, z, lane, SIG, lat, thr);
+            if (lane == 0) {
+                eout[2 * q] = lat;
+                eout[2 * q + 1] = thr;
+            }
+        }
+        __syncthreads();
+        for (int t = threadIdx.x; t < nc; t += WAVES * 64) {
+            const int e = c0 + t;
+            const uint32_t off = e < n_list ? 0xFFFFFFFFu - (uint32_t)(ekey[e] & 0xFFFFFFFFull)
+                                            : (uint32_t)args.seg[g * args.seg_cap + (e - n_list)];
+            const int vcol = pCols[args.vram_slot];
+            float va = 0.f;
+            for (int j = 0; j < N; j++) va = va + feat[erow[t * kMaxN + j] * L + vcol];
+            const bool vram_ok = (double)va <= (double)fc.vram_cap;
+            bool sla_ok = true;
+            uint32_t fl = 0;
+            double J = 0.0;
+            for (int i = 0; i < N; i++) {
+                const double lat = eout[2 * (t * N + i)], thr = eout[2 * (t * N + i) + 1];
+                if (!(lat <= (double)par[128 + i])) { sla_ok = false; fl |= 1u << (8 + i); }
+                if constexpr (OBJ) {
+                    double qv, P, pen;
+                    bool do_P, do_pen;
+                    if (!canon_eq3(args.obj, erow[t * kMaxN + i], thr, par[64 + i], pPrev[i], qv, P, do_P, pen,
+                                   do_pen)) {
+                        sla_ok = false;
+                        fl |= 1u << (8 + i);
+                    }
+                    J = fma((double)par[32 + i], qv, J);
+                    if (do_P) J = J - P;
+                    if (do_pen) J = J - pen;
+                } else {
+                    J = fma((double)par[32 + i], thr, J);
+                }
+            }
+            const bool feas = vram_ok && sla_ok;
+            fl |= (vram_ok ? 1u : 0u) | (sla_ok ? 2u : 0u) | (feas ? 4u : 0u);
+            if (e < n_list) {
+                // a sure-feasible fast decision must be canonically feasible,
+                // and the key's U must bound the canonical J
+                const double U = (double)unord_f32((uint32_t)(ekey[e] >> 32));
+                if (!feas || !(U - J >= 0.0)) atomicOr(&estat[0], kStatSelfCheck);
+                args.cand_J[g * T + e] = feas ? J : -INFINITY;
+                args.cand_F[g * T + e] = fl;
+            } else {
+                const uint64_t at = g * args.seg_cap + (e - n_list);
+                args.seg_Jc[at] = J;
+                args.seg_F[at] = fl;
+                if (args.mask)
+                    args.mask[off] = (uint8_t)((vram_ok ? 1u : 0u) | (sla_ok ? 2u : 0u) | (feas ? 4u : 0u) | 8u);
+            }
+        }
+        __syncthreads();
+    }
+    for (int j = n_list + (int)threadIdx.x; j < T; j += WAVES * 64) args.cand_F[g * T + j] = 0;
+    if (threadIdx.x == 0) {
+        unsigned long long *r = args.wg_rec + 4 * g;
+        r[0] = n_offered;
+        r[1] = t_start;
+        r[2] = (unsigned long long)wall_clock64();
+        r[3] = ((unsigned long long)estat[0] << 32) | estat[1];
+    }
+}
 
 // OBJ: score with the full utility of Eq. 3 (otherwise the linear objective).
 // SIG: the surrogates' outputs pass a sigmoid; the latency decision then
@@ -46,6 +245,7 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
     for (int t = threadIdx.x; t < args.image_f4; t += blockDim.x) smem4[t] = args.image[t];
     // [0,16) sla_lo  [16,32) sla_hi  [32,48) omega  [48,64) first option row per model (int)
     // [64,80) floor tau  [80,96) previous variant (int)  [96,112) throughput bound
+    // [112,128) option count per model (int)  [128,144) latency bound  [144,160) aggregate column (int)
     float *par = smem + Ly.total_floats;
     int *par_off = reinterpret_cast<int *>(par + 48);
     int *par_prev = reinterpret_cast<int *>(par + 80);
@@ -74,6 +274,8 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             }
             par[32 + i] = args.omega[i];
             par_off[i] = fc.opt_off[i];
+            reinterpret_cast<int *>(par + 112)[i] = fc.K[i];
+            par[128 + i] = args.sla[i];
             if constexpr (OBJ) {
                 par[64 + i] = args.obj.tau[i];
                 par_prev[i] = args.obj.prev[i];
@@ -81,11 +283,21 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             }
         }
     }
+    if (mode == kModeSearch && args.small && threadIdx.x < (unsigned)Ly.A)
+        reinterpret_cast<int *>(par + 144)[threadIdx.x] = args.agg_cols[threadIdx.x];
     constexpr bool eq3 = OBJ;
     // global bound on |fast J - canonical J|: keys and certification entries
     // carry the upper bound U = J + eJ
     const double eJ = bound_eJ(fc, args.omega);
-    if (mode == kModeSearch && blockIdx.x == 0 && threadIdx.x == 0) args.res->eJ = eJ;
+    // small ranges: certification entries counted per workgroup in LDS
+    __shared__ unsigned int s_nwork;
+    unsigned long long t_start = 0;
+    const bool small = mode == kModeSearch && args.small;
+    if (threadIdx.x == 0) {
+        s_nwork = 0;
+        t_start = (unsigned long long)wall_clock64();
+    }
+    if (mode == kModeSearch && !small && blockIdx.x == 0 && threadIdx.x == 0) args.res->eJ = eJ;
     __syncthreads();
 
     const int lane = threadIdx.x & 63, half = lane >> 5, col = lane & 31;
@@ -287,12 +499,27 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             if (mode == kModeSearch) {
                 c_vram += (mine && vram_ok) ? 1u : 0u;
                 c_feas += feas_sure ? 1u : 0u;
-                work_append(unc, (unsigned long long)(uint32_t)off | ((unsigned long long)umask << 32), U, lane,
-                            &args.res->n_work, args.work, args.work_J, args.work_cap);
+                const unsigned long long went = (unsigned long long)(uint32_t)off | ((unsigned long long)umask << 32);
+                if (small) {
+                    const unsigned long long m = __ballot(unc);
+                    if (m) {
+                        unsigned int base = 0;
+                        if (lane == 0) base = atomicAdd(&s_nwork, (unsigned int)__popcll(m));
+                        base = (unsigned int)__builtin_amdgcn_readfirstlane((int)base);
+                        const unsigned int slot = base + (unsigned int)__popcll(m & ((1ull << lane) - 1ull));
+                        if (unc && slot < args.seg_cap) {
+                            const uint64_t at = (uint64_t)blockIdx.x * args.seg_cap + slot;
+                            args.seg[at] = went;
+                            args.seg_J[at] = U;
+                        }
+                    }
+                } else {
+                    work_append(unc, went, U, lane, &args.res->n_work, args.work, args.work_J, args.work_cap);
+                }
                 const unsigned long long key = feas_sure
                     ? (((unsigned long long)ord_f32(U) << 32) | (unsigned long long)(0xFFFFFFFFu - (uint32_t)off))
                     : 0ull;
-                wl_offer(wl, key, lane, kp);
+                wl_offer_many(wl, key, lane, kp);
                 if (args.mask && mine)
                     args.mask[off] = (uint8_t)((vram_ok ? 1u : 0u) | (sla_sure ? 2u : 0u) |
                                                (feas_sure ? 4u : 0u) | (unc ? 8u : 0u));
@@ -333,6 +560,10 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
                 for (int w = 0; w < WAVES; w++) t += s_cnt[lane * WAVES + w];
                 args.wg_counts[2 * (uint64_t)blockIdx.x + lane] = t;
             }
+        }
+        if (small) {
+            // s_nwork is final: every wave's appends precede the tree merge's barriers
+            small_certify<H, WAVES, OBJ, SIG>(args, fc, smem, par, wl.s[0], kp, s_nwork, lane, wv, t_start);
         }
     }
 }
@@ -411,7 +642,7 @@ template <int MAXN, int A, int H, int WAVES>
 static hipError_t launch_fast_t(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode,
                                 hipStream_t s)
 {
-    const size_t lds = (size_t)a.lay.total_floats * 4 + kFastPar * 4 + (size_t)WAVES * kp * 8;
+    const size_t lds = (size_t)a.lay.total_floats * 4 + kFastPar * 4 + (size_t)WAVES * kp * 8 + (size_t)a.ep_bytes;
     auto fn = a.obj.kind != 0 ? fast_kernel<MAXN, A, H, WAVES, true> : fast_kernel<MAXN, A, H, WAVES, false>;
     if constexpr (MAXN == kMaxN && WAVES == kSearchWaves)   // the sigmoid output runs on the generic kernel
         if (fc.act) fn = a.obj.kind != 0 ? fast_kernel<MAXN, A, H, WAVES, true, true>

@@ -95,16 +95,20 @@ def test_eq3_linear_special_case_matches_linear_search(mf):
 
 def test_eq3_reload_ties_use_the_fallback(mf, orc):
     # Q = 0, no penalty, no floor: J = -alpha sum_i c_i eta_i takes a handful
-    # of values, each shared by thousands of configurations
+    # of values, each shared by thousands of configurations; with no previous
+    # deployment as well, J = 0 everywhere and the exact top-k needs the
+    # fallback pass (every tied configuration with the lowest indices)
     inst = synth.make_instance([12, 12, 9, 9, 9], seed=4, vram_quantile=0.9, sla_range=(1e9, 1e9))
     ob = replace(synth.make_objective(inst, 4), quality=np.zeros((5, synth.MAX_VARIANTS), np.float32),
                  tau=np.full(5, -np.inf, np.float32), beta=0.0)
-    r = orc.Problem(inst, ob).search(inst.sla, inst.omega, k=64)
-    g = mf.Problem(inst, variants=ob).search(inst.sla, inst.omega, k=64, objective=ob)
-    assert g["n_topk_collect"] > 0
-    assert g["n_feas"] == r["n_feas"]
-    assert list(g["top_idx"]) == list(r["top_idx"])
-    assert g["top_J"].tobytes() == r["top_J"].tobytes()
+    for o, must_collect in ((ob, False), (replace(ob, prev_variant=np.full(5, -1, np.int32)), True)):
+        r = orc.Problem(inst, o).search(inst.sla, inst.omega, k=64)
+        g = mf.Problem(inst, variants=o).search(inst.sla, inst.omega, k=64, objective=o)
+        if must_collect:
+            assert g["n_topk_collect"] > 0
+        assert g["n_feas"] == r["n_feas"]
+        assert list(g["top_idx"]) == list(r["top_idx"])
+        assert g["top_J"].tobytes() == r["top_J"].tobytes()
 
 
 def test_eq3_argument_validation(mf):
