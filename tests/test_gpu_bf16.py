@@ -10,11 +10,16 @@ bounds cover.  Bars:
   * fast predictions: within 2e-2 relative (the bf16 tolerance), and in fact
     within 1e-4 relative to max(|oracle|, rms) by the path's design.
 """
+import hashlib
+import json
+import os
+
 import numpy as np
 import pytest
 
 from paper_2609_02109_amd import synth
-from test_gpu_search import check_predictions, run_range_parity
+from test_gpu_search import GOLDEN, check_predictions, run_range_parity
+from test_oracle import mitm_vram_count
 
 pytestmark = pytest.mark.gpu
 
@@ -116,6 +121,9 @@ def test_bf16_n8_full_space_properties(mf, orc):
     g = p.search(inst.sla, inst.omega, k=64)
     assert g["n_eval"] == inst.space_size
     assert len(g["top_idx"]) == 64 and 64 <= g["n_feas"] <= g["n_vram"]
+    # the VRAM-feasible count over all 2^32 configurations, exactly (an
+    # independent meet-in-the-middle count over the option tables)
+    assert g["n_vram"] == mitm_vram_count(inst, float(inst.vram_cap))
     top = np.asarray(g["top_idx"], dtype=np.uint64)
     ref = orc.Problem(inst).eval_list(top, inst.sla, inst.omega)
     assert np.all(ref["flags"] & 4)
@@ -163,6 +171,37 @@ def test_bf16_n8_full_space_properties(mf, orc):
     print(f"[bf16] {len(near)} neighbours of the top-64, {int(fn.sum())} feasible", flush=True)
     assert fn.sum() > 0
     assert np.all((rn["J"][fn] < kth) | ((rn["J"][fn] == kth) & (near[fn] > top[-1])))
+
+
+def _fingerprint(inst) -> str:
+    h = hashlib.sha256()
+    for a in (inst.n_options, inst.features, inst.agg_cols, inst.weights, inst.sla, inst.omega):
+        h.update(np.ascontiguousarray(a).tobytes())
+    h.update(np.float32(inst.vram_cap).tobytes())
+    return h.hexdigest()[:16]
+
+
+def test_bf16_n8_oracle_chunks(mf):
+    # 64 chunks of 2^18 consecutive configurations of the N=8 workload (the
+    # head, across the 2^31 midpoint, the tail and seeded offsets), each run
+    # through the oracle in full when the golden file was written: counts,
+    # the top-64 with canonical J, and every configuration's mask bits (as a
+    # SHA-256 over the chunk's flag bytes)
+    path = os.path.join(GOLDEN, "cfg4_s0_chunks.json")
+    rec = json.load(open(path))
+    inst = synth.cfg4(rec["seed"])
+    assert _fingerprint(inst) == rec["fingerprint"], "the generator changed since the golden file was written"
+    p = mf.Problem(inst)
+    assert len(rec["chunks"]) >= 64
+    for c in rec["chunks"]:
+        lo, hi = c["lo"], c["hi"]
+        print(f"[bf16] oracle chunk [{lo}, {hi})", flush=True)
+        g = p.search(inst.sla, inst.omega, k=rec["k"], lo=lo, hi=hi, dump=True)
+        assert g["n_vram"] == c["n_vram"] and g["n_feas"] == c["n_feas"], (lo, g["n_feas"], c["n_feas"])
+        assert [int(x) for x in g["top_idx"]] == c["top_idx"], lo
+        assert [float(x).hex() for x in g["top_J"]] == c["top_J"], lo
+        flags = (g["mask"].cpu().numpy() & 7).astype(np.uint8)
+        assert hashlib.sha256(flags.tobytes()).hexdigest() == c["flags_sha256"], lo
 
 
 def test_bf16_topk_fallback_on_exact_ties(mf, orc):
