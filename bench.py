@@ -26,7 +26,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_FP32_TFLOPS = 157.3
 PEAK_FP64_TFLOPS = 78.6
-CPU_SAMPLE = 1 << 24
+CPU_SAMPLE_PER_THREAD = 1 << 20
 # HBM bytes per launch of the fast search kernel from rocprofv3 FETCH_SIZE /
 # WRITE_SIZE passes (profiles/fast_kernel_n6_k24_h64_hbm_counters.md), valid
 # only for the kernel source they were taken on
@@ -63,16 +63,37 @@ def algorithmic_flops_per_config(inst):
     return inst.n_models * 2 * (A * H1 + H1 * H2 + 2 * H2)
 
 
-def cpu_baseline(inst, threads):
+def host_cores():
+    """The cores this process may run on (its affinity set), and the
+    machine's count."""
+    try:
+        allowed = len(os.sched_getaffinity(0))
+    except AttributeError:
+        allowed = os.cpu_count() or 1
+    return allowed, os.cpu_count() or allowed
+
+
+def cpu_baseline(inst, inst5, threads, machine_cores):
+    """The oracle on every core the process may use, over a contiguous sample
+    of the N=6 space sized to about ten seconds of work (2^20 configurations
+    per thread), plus one single-thread run over the whole N=5 space."""
     import oracle
     p = oracle.Problem(inst)
-    n = min(CPU_SAMPLE, inst.space_size)
+    n = min(CPU_SAMPLE_PER_THREAD * threads, inst.space_size)
     t0 = time.perf_counter()
     p.search(inst.sla, inst.omega, k=1, lo=0, hi=n, threads=threads)
     dt = time.perf_counter() - t0
+    p5 = oracle.Problem(inst5)
+    t0 = time.perf_counter()
+    r5 = p5.search(inst5.sla, inst5.omega, k=16, threads=1)
+    dt5 = time.perf_counter() - t0
     return {"value": n / dt, "unit": "joint configs/s", "cores": threads, "kind": "oracle",
-            "sample": f"indices [0, {n}) of the same N=6 space (first {n} joint configs), "
-                      f"fp64 brute force, {dt:.2f} s"}
+            "sample": f"indices [0, {n}) of the same N=6 space: {n / inst.space_size:.1%} of its "
+                      f"{inst.space_size} joint configs, fp64 brute force, {dt:.2f} s on {threads} threads "
+                      f"(the process's affinity set; the machine reports {machine_cores} cores)",
+            "n5_single_thread": {"workload": "the whole N=5 space (104,976 joint configs), top-16, 1 thread",
+                                 "ms": dt5 * 1e3, "joint_configs_per_s": inst5.space_size / dt5,
+                                 "argmax": int(r5["top_idx"][0])}}
 
 
 def measure_search(mf, torch, inst, k, steps, warmup, objective=None, state=None):
@@ -107,6 +128,17 @@ def measure_search(mf, torch, inst, k, steps, warmup, objective=None, state=None
 PEAK_BF16_TFLOPS = 2500.0
 
 
+def n8_bf16_roofline(inst, kernel_ms):
+    """All of the kernel's algorithmic flops per configuration (layer 1's
+    aggregate part, layer 2 and layer 3: N (2 A H + 2 H^2 + 4 H) = 1,089,536 at
+    N=8) against the dense bf16 matrix peak."""
+    N, A, H = inst.n_models, inst.n_agg, inst.hidden1
+    per = N * (2 * A * H + 2 * H * H + 4 * H)
+    ach = per * inst.space_size / (kernel_ms * 1e-3) / 1e12
+    return {"bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": ach / PEAK_BF16_TFLOPS, "flops_per_config": per}
+
+
 def n8_roofline(inst, kernel_ms):
     # The bf16 kernel mixes three pipes: layer 1's aggregate part on the fp32
     # matrix cores (an exact fp32 chain), layer 2 on the bf16 matrix cores,
@@ -133,7 +165,8 @@ def bench_n8(mf, torch, seed, steps, warmup):
                         "accumulation, VRAM cap 288 GB, top-64 + counts",
             "ms_to_top64": ms, "joint_configs_per_s": inst.space_size / (ms * 1e-3), "fast_kernel_ms": kms,
             "n_feas": int(r.n_feas), "n_flagged": int(r.n_flagged), "n_topk_collect": int(r.n_topk_collect),
-            "argmax": int(r.top_idx[0]), "roofline": n8_roofline(inst, kms)}
+            "argmax": int(r.top_idx[0]), "roofline": n8_roofline(inst, kms),
+            "roofline_bf16_peak": n8_bf16_roofline(inst, kms)}
 
 
 # Vector issue of the chip: one wave64 VALU instruction per clock per CU
@@ -205,46 +238,62 @@ def bench_protocol(seeds=(0, 1, 2), n_scen=8, n_steps=12):
            for name in ("exhaustive", "ga", "random")}
     log(f"protocol: {wall:.1f} s; " + "; ".join(f"{k} J={v['mean_J']:.4f} gap={v['avg_gap']:.2f}% "
                                                  f"sla={v['sla_pct']:.2f}%" for k, v in table.items()))
-    return {"workload": f"Table II protocol: N=5 instance (12,12,9,9,9 options, 12-64-32-2 predictor with "
+    return {"note": "synthetic scenarios, not the paper's: on them StaticFull and StaticBudget-5000 beat the "
+                    "per-step exhaustive scheduler, the reverse of Table II's ranking, because a greedy per-step "
+                    "argmax pays the reload term of Eq. 3 at every variant switch; this line is not a "
+                    "reproduction of Table II",
+            "workload": f"Table II protocol: N=5 instance (12,12,9,9,9 options, 12-64-32-2 predictor with "
                         f"sigmoid outputs), {n_scen} dynamic scenarios x "
                         f"{n_steps} steps x {len(seeds)} seeds, Eq. 3 with floors, observed state per step; "
                         "GA population 100, 30 generations, mutation 0.1",
             "table": table, "median_decision_ms": lat, "wall_s": wall}
 
 
-def bench_ga(args):
-    import torch
-    from paper_2609_02109_amd import mf, synth
-    inst, sc, gp = synth.cfg3(args.seed)
+GA_WORKLOAD = ("GA on the N=5 instance (12,12,9,9,9 options): 64 scenarios x population 2048 x (100+1) "
+               "generations, tournament 3, crossover 0.7, mutation 0.05, canonical fp64 fitness")
+
+
+def measure_ga(mf, torch, seed, steps, warmup):
+    """The GA scheduler (Section IV-C) on 64 scenarios: ms per whole run (call
+    to host result), evaluations/s, and the fitness flops over the run's time
+    against the fp64 vector peak (operators and the feasible list included)."""
+    from paper_2609_02109_amd import synth
+    inst, sc, gp = synth.cfg3(seed)
     p = mf.Problem(inst)
     run = lambda: p.ga(sc.sla, sc.omega, pop=gp.pop, gens=gp.gens, tourn_k=gp.tourn_k, p_cx=gp.p_cx,
                        p_swap=gp.p_swap, p_mut=gp.p_mut, seed=gp.seed)
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         run()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(steps):
         r = run()
     torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms = (time.perf_counter() - t0) * 1e3 / steps
     evals = gp.n_scen * gp.pop * (gp.gens + 1)
     # canonical fp64 flops of one fitness evaluation: N x (2 (L+A) H1 + 2 H1 H2 + 4 H2)
-    flops = evals * inst.n_models * 2 * ((inst.n_local + inst.n_agg) * inst.hidden1 + inst.hidden1 * inst.hidden2
-                                         + 2 * inst.hidden2)
-    achieved = flops / (ms * 1e-3) / 1e12
-    line = {"metric": "GA fitness evaluations/sec (64 scenarios, population 2048, 100 generations, N=5)",
-            "value": evals / (ms * 1e-3), "unit": "evaluations/s", "n_gpus": 1, "steps": args.steps,
-            "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
-            "vs_baseline": None, "dtype": "f64", "data": "synthetic (seeded generator, seed %d)" % args.seed,
-            "config": {"workload": "GA on the N=5 instance (12,12,9,9,9 options): 64 scenarios x 2048 x "
-                                   "(100+1) generations, tournament 3, crossover 0.7, mutation 0.05",
-                       "ms_per_ga_run": ms, "best_J_mean": float(r["best_J"].mean())},
-            # the fitness flops over the whole run's time (operators and the
-            # feasible list included), against the fp64 vector peak
+    per = inst.n_models * 2 * ((inst.n_local + inst.n_agg) * inst.hidden1 + inst.hidden1 * inst.hidden2
+                               + 2 * inst.hidden2)
+    achieved = per * evals / (ms * 1e-3) / 1e12
+    log(f"ga: {ms:.2f} ms per run, {evals / (ms * 1e-3):.3e} evaluations/s")
+    return {"workload": GA_WORKLOAD, "ms_per_ga_run": ms, "evaluations": evals,
+            "evaluations_per_s": evals / (ms * 1e-3), "best_J": [float(x) for x in r["best_J"]],
+            "best_idx": [int(x) for x in r["best_idx"]],
             "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_FP64_TFLOPS, "unit": "TFLOP/s",
                          "frac": achieved / PEAK_FP64_TFLOPS, "traffic": None,
-                         "kernel": "whole GA run (fitness, operators, feasible list)",
-                         "flops_per_evaluation": flops // evals}}
+                         "kernel": "whole GA run (fitness, operators, feasible list)", "flops_per_evaluation": per}}
+
+
+def bench_ga(args):
+    import torch
+    from paper_2609_02109_amd import mf
+    g = measure_ga(mf, torch, args.seed, args.steps, args.warmup)
+    line = {"metric": "GA fitness evaluations/sec (64 scenarios, population 2048, 100 generations, N=5)",
+            "value": g["evaluations_per_s"], "unit": "evaluations/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": g["ms_per_ga_run"], "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+            "data": "synthetic (seeded generator, seed %d)" % args.seed,
+            "config": {k: v for k, v in g.items() if k != "roofline"}, "roofline": g["roofline"]}
     print(json.dumps(line), flush=True)
 
 
@@ -262,6 +311,7 @@ def main():
     ap.add_argument("--no-n8", action="store_true", help="skip the N=8 bf16 search in the n6 line")
     ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-state searches in the n6 line")
     ap.add_argument("--no-protocol", action="store_true", help="skip the Table II protocol in the n6 line")
+    ap.add_argument("--no-ga", action="store_true", help="skip the GA scheduler in the n6 line")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="run one plain device copy kernel of this many bytes read (and written) "
                          "before the search: the calibration point for HBM byte counters")
@@ -311,13 +361,15 @@ def main():
     log(f"eq3 search: {ms3:.2f} ms/step, fast kernel {kms3:.2f} ms, n_feas={r3.n_feas} n_flagged={r3.n_flagged}")
 
     fixed = None if args.no_fixed else bench_fixed(mf, torch, args.seed, max(args.steps, 20), max(args.warmup, 3))
+    ga = None if args.no_ga else measure_ga(mf, torch, args.seed, args.steps, max(args.warmup, 2))
     proto = None if args.no_protocol else bench_protocol()
 
     cpu = None
     if not args.no_cpu:
-        threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or min(os.cpu_count() or 1, 16)
-        cpu = cpu_baseline(inst, threads)
-        log(f"cpu oracle: {cpu['value']:.3e} configs/s on {threads} threads")
+        threads, machine = host_cores()
+        cpu = cpu_baseline(inst, inst5, threads, machine)
+        log(f"cpu oracle: {cpu['value']:.3e} configs/s on {threads} threads (machine: {machine}); "
+            f"N=5 single thread {cpu['n5_single_thread']['ms']:.1f} ms")
 
     line = {
         "metric": "joint configs evaluated/sec (surrogate+mask+argmax), N=6 exhaustive; ms to argmax",
@@ -348,6 +400,7 @@ def main():
                               / PEAK_FP32_TFLOPS, "n_feas": int(r3.n_feas), "n_flagged": int(r3.n_flagged),
                               "argmax": int(r3.top_idx[0])},
                    "fixed_state": fixed,
+                   "ga": ga,
                    "protocol": proto},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_FP32_TFLOPS, "traffic": measured_traffic(),

@@ -63,9 +63,12 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB):
+        # MF_ORACLE_LIB names another build of the same sources (the
+        # sanitizer test loads an ASan/UBSan build this way)
+        path = os.environ.get("MF_ORACLE_LIB") or LIB
+        if path == LIB and not os.path.exists(LIB):
             build()
-        L = C.CDLL(LIB)
+        L = C.CDLL(path)
         P = C.c_void_p
         L.orc_space_size.restype = C.c_uint64
         L.orc_space_size.argtypes = [P]

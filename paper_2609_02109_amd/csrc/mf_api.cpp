@@ -1095,7 +1095,12 @@ mf_status check_desc(const mf_desc *desc, Shape &sh)
     if (N < 1 || N > MF_MAX_MODELS || L < 1 || A < 1 || A > MF_MAX_AGG || L + A > 64 || H1 < 1 || H1 > 256 || H2 < 1 ||
         H2 > 256 || !desc->h_n_options || !desc->h_agg_cols)
         return MF_EINVAL;
-    if (desc->dtype != MF_F32 && desc->dtype != MF_BF16) return MF_EINVAL;
+    // the enum field is read through its integer representation: a C caller
+    // may store any int there, which a C++ enum load may not see
+    int dtype;
+    static_assert(sizeof dtype == sizeof desc->dtype, "mf_dtype is int-sized");
+    std::memcpy(&dtype, &desc->dtype, sizeof dtype);
+    if (dtype != MF_F32 && dtype != MF_BF16) return MF_EINVAL;
     if (desc->output_act != MF_ACT_IDENTITY && desc->output_act != MF_ACT_SIGMOID) return MF_EINVAL;
     if (desc->vram_slot < 0 || desc->vram_slot >= A || !std::isfinite(desc->vram_cap)) return MF_EINVAL;
     sh.K.assign(desc->h_n_options, desc->h_n_options + N);
@@ -1201,7 +1206,13 @@ extern "C" {
 
 const char *mf_status_string(mf_status s)
 {
-    switch (s) {
+    // A C caller may pass any int; in C++ an enum object holding a value
+    // outside the enumerators' range is undefined, so the argument is read
+    // through its integer representation.
+    int v;
+    static_assert(sizeof v == sizeof s, "mf_status is int-sized");
+    std::memcpy(&v, &s, sizeof v);
+    switch (v) {
         case MF_OK: return "MF_OK";
         case MF_EINVAL: return "MF_EINVAL: invalid argument";
         case MF_ENOMEM: return "MF_ENOMEM: workspace too small or allocation failed";
