@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
+#include <atomic>
 #include <cstring>
 #include <limits>
 #include <map>
@@ -62,6 +63,7 @@ struct mf_problem {
     Bf16Const bcst{};
     float4 *d_bmodels = nullptr, *d_bg = nullptr;
     float *d_phat = nullptr;
+    std::atomic<unsigned long long> call_seq{0};   // sequence numbers of small-range searches
     // timing events: created with the problem, handed to one call at a time
     std::mutex ev_mu;
     std::vector<EventPair> ev_free, ev_all;
@@ -122,7 +124,8 @@ bool create_event_pair(EventPair &e)
         e.a = nullptr;
         return false;
     }
-    if (hipHostMalloc((void **)&e.h_res, sizeof(DevResult), hipHostMallocDefault) != hipSuccess) e.h_res = nullptr;
+    // coherent: the finish kernel's stores reach the host while it runs
+    if (hipHostMalloc((void **)&e.h_res, sizeof(DevResult), hipHostMallocCoherent) != hipSuccess) e.h_res = nullptr;
     return true;
 }
 
@@ -466,6 +469,29 @@ constexpr uint64_t kMaxLaunch = 1ull << 32;   // offsets within one launch set f
 
 mf_status hip_status(hipError_t e) { return e == hipSuccess ? MF_OK : MF_EDEVICE; }
 
+// Waits until the finish kernel has published sequence number `seq` in the
+// host copy of the result.  The stream is queried every 64 polls: if it has
+// finished without the number appearing, or reports an error, the wait ends
+// with MF_EDEVICE instead of spinning on.
+mf_status wait_done(const DevResult *h, unsigned long long seq, hipStream_t s)
+{
+    const volatile unsigned long long *flag = &h->done_seq;
+    for (unsigned it = 1;; it++) {
+        if (*flag == seq) break;
+        if ((it & 63u) == 0) {
+            const hipError_t q = hipStreamQuery(s);
+            if (q == hipSuccess) {
+                if (*flag == seq) break;
+                return MF_EDEVICE;
+            }
+            if (q != hipErrorNotReady) return MF_EDEVICE;
+        }
+        __builtin_ia32_pause();
+    }
+    std::atomic_thread_fence(std::memory_order_acquire);
+    return MF_OK;
+}
+
 #define MF_HIP(x)                                         \
     do {                                                  \
         hipError_t e_ = (x);                              \
@@ -650,6 +676,8 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
         FinishArgs fin{};
         fin.res = R;
         fin.res_host = ev.host_result();
+        fin.seq = p->call_seq.fetch_add(1) + 1;
+        if (fin.res_host) fin.res_host->done_seq = 0;
         fin.omega = args->d_omega;
         fin.lo = lo;
         fin.top_k = args->top_k;
@@ -671,8 +699,10 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
         fin.cand_F = fa.cand_F;
         MF_HIP2(launch_finish_small(fin, p->fc, s));
         if (fin.res_host) {
-            // the finish kernel writes the result into pinned host memory
-            MF_HIP2(hipStreamSynchronize(s));
+            // the finish kernel writes the result into pinned host memory,
+            // the sequence number last
+            const mf_status ws = wait_done(fin.res_host, fin.seq, s);
+            if (ws != MF_OK) return ws;
             std::memcpy(&h, fin.res_host, sizeof(DevResult));
         } else {
             MF_HIP2(hipMemcpyAsync(&h, R, sizeof(DevResult), hipMemcpyDeviceToHost, s));

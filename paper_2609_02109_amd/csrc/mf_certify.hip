@@ -426,6 +426,14 @@ __device__ __forceinline__ unsigned long long wave_min64(unsigned long long x)
     return x;
 }
 
+// The last store of a finish kernel to the host copy: the call's sequence
+// number, after a system-scope fence.
+__device__ __forceinline__ void publish_done(const FinishArgs &f)
+{
+    __threadfence_system();
+    *reinterpret_cast<volatile unsigned long long *>(&f.res_host->done_seq) = f.seq;
+}
+
 __global__ void __launch_bounds__(kFinWaves * 64) finish_small_kernel(const FinishArgs f, const FastConst fc)
 {
     extern __shared__ uint32_t woff[];   // [n_wg + 1] exclusive prefix of the segment lengths
@@ -433,12 +441,46 @@ __global__ void __launch_bounds__(kFinWaves * 64) finish_small_kernel(const Fini
     __shared__ unsigned int s_wsum[kFinWaves];
     __shared__ unsigned long long s_feas;
     __shared__ K128 klst[kFinWaves * 64];
+    __shared__ K128 s_floor;
     constexpr int W = kFinWaves;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int k = f.top_k, T = f.eval_top, n_wg = f.n_wg;
     DevResult *R = f.res;
     if (tid == 0) s_feas = 0;
+
+    // ---- the candidate keys (each workgroup's first T list entries with
+    // their canonical J) are loaded first, all at once, so that their round
+    // trip overlaps the records' below; staged in LDS after the prefix
+    const uint32_t n_cand = (uint32_t)n_wg * (uint32_t)T;
+    K128 *ckeys = reinterpret_cast<K128 *>(woff + ((n_wg + 4) & ~3));   // [n_cand]
+    constexpr int kCpt = 4;   // candidates per thread per pass
+    for (uint32_t base = 0; base < n_cand; base += kCpt * blockDim.x) {
+        uint32_t cf[kCpt];
+        unsigned long long ck[kCpt];
+        double cj[kCpt];
+#pragma unroll
+        for (int q = 0; q < kCpt; q++) {
+            const uint32_t t = base + q * blockDim.x + tid;
+            cf[q] = 0;
+            ck[q] = 0;
+            cj[q] = 0.0;
+            if (t < n_cand) {
+                const uint32_t g = t / T, j = t - g * T;
+                cf[q] = f.cand_F[t];
+                ck[q] = f.wg_lists[(uint64_t)g * f.kp + j];
+                cj[q] = f.cand_J[t];
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < kCpt; q++) {
+            const uint32_t t = base + q * blockDim.x + tid;
+            if (t < n_cand) {
+                const uint32_t off = 0xFFFFFFFFu - (uint32_t)(ck[q] & 0xFFFFFFFFull);
+                ckeys[t] = (cf[q] & 4u) ? K128{ord_f64(cj[q]), ~(f.lo + off)} : K128{0, 0};
+            }
+        }
+    }
 
     // ---- counts, wall-clock span, status bits and the largest unevaluated
     // upper bound over the workgroups; exclusive prefix of the segment lengths
@@ -502,38 +544,31 @@ __global__ void __launch_bounds__(kFinWaves * 64) finish_small_kernel(const Fini
             if (f.res_host) {
                 f.res_host->status = kStatWorkOverflow;
                 f.res_host->n_work = (unsigned long long)f.work_cap + 1;
+                publish_done(f);
             }
         }
         return;
     }
-    // the gathered certification list, for a fallback pass on the host's side
-    for (uint32_t e = tid; e < n_work; e += blockDim.x) {
-        const int g = seg_of(woff, n_wg, e);
-        const uint64_t at = (uint64_t)g * f.seg_cap + (e - woff[g]);
-        f.work_out[e] = f.seg[at];
-        f.work_J_out[e] = f.seg_J[at];
-    }
-
-    // ---- the exact top-k over the canonically evaluated entries: each
-    // workgroup's first T list entries (their keys, loaded with every load in
-    // flight at once, staged in LDS), then the certification entries
-    K128 slot = {0, 0}, thr = {0, 0};
-    const uint32_t n_cand = (uint32_t)n_wg * (uint32_t)T;
-    K128 *ckeys = reinterpret_cast<K128 *>(woff + ((n_wg + 4) & ~3));   // [n_cand]
-    for (uint32_t t = tid; t < n_cand; t += blockDim.x) {
-        const uint32_t g = t / T, j = t % T;
-        const uint32_t fl = f.cand_F[t];
-        const unsigned long long key = f.wg_lists[(uint64_t)g * f.kp + j];
-        const double J = f.cand_J[t];
-        const uint32_t off = 0xFFFFFFFFu - (uint32_t)(key & 0xFFFFFFFFull);
-        ckeys[t] = (fl & 4u) ? K128{ord_f64(J), ~(f.lo + off)} : K128{0, 0};
+    // ---- a lower bound of the k-th largest candidate key: the k-th largest
+    // of 64 group maxima (64 distinct candidates), so that the offers below
+    // skip every key under it
+    if (wv == 0) {
+        K128 m = {0, 0};
+        for (uint32_t t = lane; t < n_cand; t += 64) {
+            const K128 x = ckeys[t];
+            if (gt128(x, m)) m = x;
+        }
+        const K128 srt = sort128_desc(m, lane);
+        const K128 fk = {readlane64(srt.hi, k - 1), readlane64(srt.lo, k - 1)};
+        if (lane == 0) s_floor = fk;
     }
     __syncthreads();
-    for (uint32_t b0 = (uint32_t)wv * 64; b0 < n_cand; b0 += W * 64) {
-        const uint32_t t = b0 + lane;
-        const K128 mine = t < n_cand ? ckeys[t] : K128{0, 0};
-        list128_offer_many(slot, mine, lane, k, thr);
-    }
+    const K128 floor_key = s_floor;
+
+    // ---- the certification entries, each read once: copied out as the
+    // gathered certification list (for a fallback pass on the host's side)
+    // and offered by their canonical J; then the staged candidates
+    K128 slot = {0, 0}, thr = {0, 0};
     unsigned long long my_feas = 0;
     for (uint32_t b0 = (uint32_t)wv * 64; b0 < n_work; b0 += W * 64) {
         const uint32_t e = b0 + lane;
@@ -541,10 +576,25 @@ __global__ void __launch_bounds__(kFinWaves * 64) finish_small_kernel(const Fini
         if (e < n_work) {
             const int g = seg_of(woff, n_wg, e);
             const uint64_t at = (uint64_t)g * f.seg_cap + (e - woff[g]);
-            if (f.seg_F[at] & 4u) {
+            const unsigned long long key = f.seg[at];
+            const float fJ = f.seg_J[at];
+            const uint32_t fl = f.seg_F[at];
+            const double cJ = f.seg_Jc[at];
+            f.work_out[e] = key;
+            f.work_J_out[e] = fJ;
+            if (fl & 4u) {
                 my_feas++;
-                mine = {ord_f64(f.seg_Jc[at]), ~(f.lo + (uint32_t)(f.seg[at] & 0xFFFFFFFFull))};
+                mine = {ord_f64(cJ), ~(f.lo + (uint32_t)(key & 0xFFFFFFFFull))};
             }
+        }
+        list128_offer_many(slot, mine, lane, k, thr);
+    }
+    for (uint32_t b0 = (uint32_t)wv * 64; b0 < n_cand; b0 += W * 64) {
+        const uint32_t t = b0 + lane;
+        K128 mine = {0, 0};
+        if (t < n_cand) {
+            const K128 x = ckeys[t];
+            if (!gt128(floor_key, x)) mine = x;
         }
         list128_offer_many(slot, mine, lane, k, thr);
     }
@@ -618,6 +668,13 @@ __global__ void __launch_bounds__(kFinWaves * 64) finish_small_kernel(const Fini
                 H->ck_cand = Ck;
                 H->fast_ticks = R->fast_ticks;
             }
+        }
+        if (f.res_host) {
+            // every lane's stores to the host copy are ordered before the
+            // sequence number the host waits for
+            __threadfence_system();
+            __builtin_amdgcn_wave_barrier();
+            if (lane == 0) publish_done(f);
         }
     }
 }

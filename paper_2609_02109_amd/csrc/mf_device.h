@@ -369,6 +369,16 @@ __device__ __forceinline__ K128 cx128(const K128 &x, int m, int lane, bool desc)
 // wave's keys are sorted descending (bitonic) and merged into the list (the
 // elementwise maximum of the list and the sorted keys reversed is bitonic;
 // six half-cleaner stages sort it); the list keeps its k best.
+// Bitonic sort of one key per lane, descending (lane 0 the largest).
+__device__ __forceinline__ K128 sort128_desc(K128 x, int lane)
+{
+#pragma unroll
+    for (int kk = 2; kk <= 64; kk <<= 1)
+#pragma unroll
+        for (int j = kk >> 1; j > 0; j >>= 1) x = cx128(x, j, lane, (lane & kk) == 0);
+    return x;
+}
+
 __device__ __forceinline__ void list128_offer_many(K128 &slot, const K128 &mine, int lane, int k, K128 &thr)
 {
     const bool pass = nz128(mine) && gt128(mine, thr);
@@ -376,11 +386,7 @@ __device__ __forceinline__ void list128_offer_many(K128 &slot, const K128 &mine,
         list128_offer(slot, mine, lane, k, thr);
         return;
     }
-    K128 x = key_if(pass, mine);
-#pragma unroll
-    for (int kk = 2; kk <= 64; kk <<= 1)
-#pragma unroll
-        for (int j = kk >> 1; j > 0; j >>= 1) x = cx128(x, j, lane, (lane & kk) == 0);
+    const K128 x = sort128_desc(key_if(pass, mine), lane);
     const K128 r = {reverse64(x.hi), reverse64(x.lo)};
     K128 c = gt128(slot, r) ? slot : r;
 #pragma unroll

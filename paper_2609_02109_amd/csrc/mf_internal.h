@@ -89,6 +89,7 @@ struct DevResult {
     double ck_cand;             // k-th canonical J among the fast candidates
     unsigned long long fast_ticks;  // small ranges: wall-clock ticks from the first workgroup's start
                                     // to the last one's end of the fast kernel
+    unsigned long long done_seq;    // small ranges, host copy: the call's sequence number, written last
 };
 constexpr unsigned kStatVerified = 1u;      // top-k exactness condition held
 constexpr unsigned kStatSelfCheck = 2u;     // a fast decision disagreed with canonical
@@ -270,6 +271,7 @@ struct CanonArgs {
 struct FinishArgs {
     DevResult *res;
     DevResult *res_host;            // optional copy in pinned host memory (counts, status, top-k)
+    unsigned long long seq;         // written to res_host->done_seq after everything else
     const float *omega;
     uint64_t lo;
     int top_k, kp, eval_top, n_wg;

@@ -34,34 +34,52 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 constexpr int kCertChunk = 64;
 size_t fast_small_epilogue_bytes(int n_models)
 {
-    return 64 * 8 + 16 + (size_t)kCertChunk * n_models * 16 + (size_t)kCertChunk * kMaxN * 4;
+    return 64 * 8 + 16 + (size_t)kCertChunk * n_models * 16 + (size_t)kCertChunk * kMaxN * 4 +
+           (size_t)kSearchWavesWide * 64 * 8;
 }
 
-// One model's surrogate (Eq. 6) on canonical semantics for one configuration
-// by one wave, with no barriers: lane u computes hidden unit u (H <= 64), and
-// each unit's chain takes its inputs in ascending order, broadcast from the
-// lanes that hold them (input k in lane k).  Layers 2 and 3 read the fp32
-// weights of the fast image in LDS (each lane its own row: W2 as laid out for
-// the layer-2 MFMA, four consecutive inputs contiguous), layer 1 the
-// canonical W1T / b1 block c1 (LDS or global).  fp32 weights are exact in
-// fp64.
-template <int H>
-__device__ inline void canon_forward_image(const float *c1, const float *img, const FastLayout &Ly, int i, int nin,
-                                           double z, int lane, bool sigmoid, double &lat, double &thr)
+// One model's surrogate (Eq. 6) on canonical semantics, by one wave with no
+// barriers: one configuration (lane u computes hidden unit u, H <= 64), or,
+// when PAIR (H <= 32 and at most 32 inputs), two configurations of the same
+// model, one per 32-lane half.  Each unit's chain takes its inputs in
+// ascending order.  The inputs of a layer (z, then h1, then h2: input k of a
+// half in its lane k) pass through the wave's 64 doubles of LDS, xb, and are
+// read back at one address per half (a broadcast read), so that the VALU
+// issues the chains themselves.  Layers 2 and 3 read the fp32 weights of the
+// fast image in LDS (each lane its own row: W2 as laid out for the layer-2
+// MFMA, four consecutive inputs contiguous), layer 1 the canonical W1T / b1
+// block c1 (LDS or global).  fp32 weights are exact in fp64.  A wave's LDS
+// accesses complete in program order; wave barriers keep the compiler from
+// moving them across a layer's store.  Outputs: (lat, thr) of the
+// configuration of half h in lanes 32 h and 32 h + 1 of y.
+template <int H, bool PAIR>
+__device__ inline double canon_forward_image(const float *c1, const float *img, const FastLayout &Ly, int i,
+                                             int nin, double z, int lane, bool sigmoid, double *xb)
 {
-    constexpr int MB = H / 32;
-    const int u = lane < H ? lane : H - 1;   // lanes past H repeat the last unit and are ignored
+    static_assert(!PAIR || H <= 32, "two configurations per wave need H <= 32");
+    constexpr int MB = H / 32 > 0 ? H / 32 : 1;
+    const int uu = PAIR ? (lane & 31) : lane;
+    const int u = uu < H ? uu : H - 1;   // lanes past H repeat the last unit and are ignored
+    const int hb = PAIR ? (lane & 32) : 0;
+    xb[lane] = z;
+    __builtin_amdgcn_wave_barrier();
     double c = (double)c1[nin * H + u];
     int k = 0;
     for (; k + 8 <= nin; k += 8) {
         float wv[8];
+        double zk[8];
 #pragma unroll
-        for (int j = 0; j < 8; j++) wv[j] = c1[(k + j) * H + u];
+        for (int j = 0; j < 8; j++) {
+            wv[j] = c1[(k + j) * H + u];
+            zk[j] = xb[hb + k + j];
+        }
 #pragma unroll
-        for (int j = 0; j < 8; j++) c = fma((double)wv[j], readlane_f64(z, k + j), c);
+        for (int j = 0; j < 8; j++) c = fma((double)wv[j], zk[j], c);
     }
-    for (; k < nin; k++) c = fma((double)c1[k * H + u], readlane_f64(z, k), c);
-    const double h1 = c > 0.0 ? c : 0.0;
+    for (; k < nin; k++) c = fma((double)c1[k * H + u], xb[hb + k], c);
+    __builtin_amdgcn_wave_barrier();
+    xb[lane] = c > 0.0 ? c : 0.0;   // h1
+    __builtin_amdgcn_wave_barrier();
     // layer 2: lane v = u; W2[v][u'] sits at ((((mb2 MB + mb1) 4 + q) 64 + l) 4 + j)
     // with v = 32 mb2 + l % 32, u' = 32 mb1 + 8 q + 4 (l / 32) + j
     const float *w2 = img + Ly.off_w2 + i * (H * H);
@@ -73,11 +91,16 @@ __device__ inline void canon_forward_image(const float *c1, const float *img, co
         const float4 a0 = *reinterpret_cast<const float4 *>(w2 + ((((mb2 * MB + mb1) * 4 + q) * 64 + lv) * 4));
         const float4 a1 = *reinterpret_cast<const float4 *>(w2 + ((((mb2 * MB + mb1) * 4 + q) * 64 + lv + 32) * 4));
         const float wv[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+        double hk[8];
 #pragma unroll
-        for (int j = 0; j < 8; j++) c = fma((double)wv[j], readlane_f64(h1, u0 + j), c);
+        for (int j = 0; j < 8; j++) hk[j] = xb[hb + u0 + j];
+#pragma unroll
+        for (int j = 0; j < 8; j++) c = fma((double)wv[j], hk[j], c);
     }
-    const double h2 = c > 0.0 ? c : 0.0;
-    // layer 3: lanes 0 and 1, W3[o][v] contiguous in v
+    __builtin_amdgcn_wave_barrier();
+    xb[lane] = c > 0.0 ? c : 0.0;   // h2
+    __builtin_amdgcn_wave_barrier();
+    // layer 3: lanes 32 h + o, W3[o][v] contiguous in v
     const int o = lane & 1;
     const float *w3 = img + Ly.off_w3 + i * (2 * H) + o * H;
     c = (double)img[Ly.off_b3 + 4 * i + o];
@@ -86,12 +109,13 @@ __device__ inline void canon_forward_image(const float *c1, const float *img, co
         const float4 a0 = *reinterpret_cast<const float4 *>(w3 + v0);
         const float4 a1 = *reinterpret_cast<const float4 *>(w3 + v0 + 4);
         const float wv[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+        double hk[8];
 #pragma unroll
-        for (int j = 0; j < 8; j++) c = fma((double)wv[j], readlane_f64(h2, v0 + j), c);
+        for (int j = 0; j < 8; j++) hk[j] = xb[hb + v0 + j];
+#pragma unroll
+        for (int j = 0; j < 8; j++) c = fma((double)wv[j], hk[j], c);
     }
-    const double y = sigmoid ? canon_sigmoid(c) : c;
-    lat = readlane_f64(y, 0);
-    thr = readlane_f64(y, 1);
+    return sigmoid ? canon_sigmoid(c) : c;
 }
 
 // Small ranges, after the scan: the workgroup evaluates canonically (the
@@ -114,6 +138,8 @@ __device__ inline void small_certify(const FastArgs &args, const FastConst &fc, 
     unsigned int *estat = reinterpret_cast<unsigned int *>(ekey + 64);                               // status, rest
     double *eout = reinterpret_cast<double *>(ekey + 66);                                            // [chunk][N][2]
     int *erow = reinterpret_cast<int *>(eout + (size_t)kCertChunk * N * 2);                          // [chunk][kMaxN]
+    static_assert(WAVES <= kSearchWavesWide, "one 64-double forward buffer per wave");
+    double *xb = reinterpret_cast<double *>(erow + kCertChunk * kMaxN) + wv * 64;
     if (wv == 0) {
         ekey[lane] = lane < T ? listkey : 0ull;
         // a bound on the upper bound U of every sure-feasible configuration
@@ -132,6 +158,7 @@ __device__ inline void small_certify(const FastArgs &args, const FastConst &fc, 
     const int n_ent = n_list + n_seg;
     const int *pCols = reinterpret_cast<const int *>(par + 144);
     const float *feat = Ly.off_feat >= 0 ? smem + Ly.off_feat : args.features;
+    const bool pair = H <= 32 && nin <= 32;
     for (int c0 = 0; c0 < n_ent; c0 += kCertChunk) {
         const int nc = n_ent - c0 < kCertChunk ? n_ent - c0 : kCertChunk;
         // each entry's option rows (model order)
@@ -146,26 +173,49 @@ __device__ inline void small_certify(const FastArgs &args, const FastConst &fc, 
             }
         }
         __syncthreads();
-        for (int q = wv; q < nc * N; q += WAVES) {
-            const int t = q / N, i = q % N;
+        // items (entry group, model): one entry per wave, or two (one per
+        // half) when the model fits a half
+        const int per = pair ? 2 : 1;
+        const int n_grp = (nc + per - 1) / per;
+        for (int q = wv; q < n_grp * N; q += WAVES) {
+            const int p = q / N, i = q % N;
+            const int half = pair ? (lane >> 5) : 0, kl = pair ? (lane & 31) : lane;
+            const int t_raw = p * per + half;
+            const int t = t_raw < nc ? t_raw : nc - 1;   // a spare half repeats the last entry
             const int *rows = erow + t * kMaxN;
-            const int row_i = rows[i];
             double z = 0.0;
-            if (lane < L) {
-                z = (double)feat[row_i * L + lane];
-            } else if (lane < nin) {
-                const int col = pCols[lane - L];
+            if (kl < L) {
+                z = (double)feat[rows[i] * L + kl];
+            } else if (kl < nin) {
+                const int col = pCols[kl - L];
+                int rj[kMaxN];
+#pragma unroll
+                for (int j = 0; j < kMaxN; j++) rj[j] = j < N ? rows[j] : 0;
                 float sa = 0.f;
-                for (int j = 0; j < N; j++) sa = sa + feat[rows[j] * L + col];
+#pragma unroll
+                for (int j = 0; j < kMaxN; j++)
+                    if (j < N) sa = sa + feat[rj[j] * L + col];
                 z = (double)sa;
             }
             const float *c1 = Ly.off_c1 >= 0 ? smem + Ly.off_c1 + i * Ly.c1_stride
                                              : args.canon + (int64_t)i * args.wstride;
-            double lat, thr;
-            canon_forward_image<H>(c1, smem, Ly, i, nin, z, lane, SIG, lat, thr);
+            double y;
+            if constexpr (H <= 32) {
+                y = pair ? canon_forward_image<H, true>(c1, smem, Ly, i, nin, z, lane, SIG, xb)
+                         : canon_forward_image<H, false>(c1, smem, Ly, i, nin, z, lane, SIG, xb);
+            } else {
+                y = canon_forward_image<H, false>(c1, smem, Ly, i, nin, z, lane, SIG, xb);
+            }
+            const double lat0 = readlane_f64(y, 0), thr0 = readlane_f64(y, 1);
+            const double lat1 = readlane_f64(y, 32), thr1 = readlane_f64(y, 33);
             if (lane == 0) {
-                eout[2 * q] = lat;
-                eout[2 * q + 1] = thr;
+                const int tq = p * per;
+                eout[2 * (tq * N + i)] = lat0;
+                eout[2 * (tq * N + i) + 1] = thr0;
+                if (pair && tq + 1 < nc) {
+                    eout[2 * ((tq + 1) * N + i)] = lat1;
+                    eout[2 * ((tq + 1) * N + i) + 1] = thr1;
+                }
             }
         }
         __syncthreads();
