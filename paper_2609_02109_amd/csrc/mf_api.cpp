@@ -49,6 +49,7 @@ struct mf_problem {
     float4 *d_image = nullptr;
     float *d_canon = nullptr, *d_features = nullptr, *d_zeros = nullptr, *d_centre = nullptr;
     double *d_w64 = nullptr;     // packed weights as fp64 (GA fitness)
+    double *d_pre = nullptr;     // [sumK][H1] canonical layer-1 chain over the local features (GA fitness)
     std::vector<float> centre;   // aggregate centre per slot (original slot order)
     int32_t *d_agg_cols = nullptr, *d_row_model = nullptr;
     FastLayout lay{};
@@ -1160,6 +1161,7 @@ struct TableLayout {
     bool fast_ok = false, bf_ok = false;
     FastLayout lay{};
     Bf16Layout blay{};
+    size_t o_pre = 0;   // [sumK][H1] doubles: canonical layer-1 chain over each option's local features
     size_t o_img = 0, o_can = 0, o_fea = 0, o_agg = 0, o_rm = 0, o_z = 0, o_c = 0, o_w64 = 0, o_bm = 0, o_bg = 0,
            o_ph = 0, o_vr = 0, total = 0;
 };
@@ -1221,6 +1223,7 @@ TableLayout table_layout(const mf_desc &d, const Shape &sh)
     t.o_z = off; off = align256(off + 64 * 4);
     t.o_c = off; off = align256(off + (size_t)A * 4);
     t.o_w64 = off; off = align256(off + n_w * 8);
+    t.o_pre = off; off = align256(off + (size_t)sumK * d.hidden1 * 8);
     t.o_bm = off; off = align256(off + n_bimg * 4);
     t.o_bg = off; off = align256(off + n_bg * 4);
     t.o_ph = off; off = align256(off + n_phat * 4);
@@ -1540,6 +1543,34 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     std::memcpy(himg.data() + tl.o_c, p->centre.data(), (size_t)A * 4);
     double *w64 = reinterpret_cast<double *>(himg.data() + tl.o_w64);
     for (size_t t = 0; t < W.size(); t++) w64[t] = (double)W[t];
+    // the first L steps of each hidden unit's canonical layer-1 chain (Eq. 6:
+    // the option's local features come first in the input), per option row:
+    // fp64 fused multiply-adds, or fp32 ones for bf16 weights; both are
+    // correctly rounded here as on the device, so the GA fitness continues
+    // these values with the aggregate inputs bit for bit
+    {
+        double *pre = reinterpret_cast<double *>(himg.data() + tl.o_pre);
+        const int nin = L + A;
+        for (int i = 0; i < N; i++) {
+            const float *W1 = W.data() + (int64_t)i * p->wstride, *b1 = W1 + (int64_t)p->H1 * nin;
+            for (int o = 0; o < p->K[i]; o++) {
+                const int row = p->opt_off[i] + o;
+                const float *x = F.data() + (int64_t)row * L;
+                for (int u = 0; u < p->H1; u++) {
+                    double a;
+                    if (p->bf16) {
+                        float af = b1[u];
+                        for (int k = 0; k < L; k++) af = std::fmaf(W1[(int64_t)u * nin + k], x[k], af);
+                        a = (double)af;
+                    } else {
+                        a = (double)b1[u];
+                        for (int k = 0; k < L; k++) a = std::fma((double)W1[(int64_t)u * nin + k], (double)x[k], a);
+                    }
+                    pre[(int64_t)row * p->H1 + u] = a;
+                }
+            }
+        }
+    }
     // ---- the caller's buffer
     char *base = (char *)d_tables;
     p->d_tables = d_tables;
@@ -1551,6 +1582,7 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     p->d_zeros = reinterpret_cast<float *>(base + tl.o_z);
     p->d_centre = reinterpret_cast<float *>(base + tl.o_c);
     p->d_w64 = reinterpret_cast<double *>(base + tl.o_w64);
+    p->d_pre = reinterpret_cast<double *>(base + tl.o_pre);
     p->d_bmodels = reinterpret_cast<float4 *>(base + tl.o_bm);
     p->d_bg = reinterpret_cast<float4 *>(base + tl.o_bg);
     p->d_phat = reinterpret_cast<float *>(base + tl.o_ph);
@@ -1861,6 +1893,8 @@ mf_status mf_ga_run(mf_problem *p, const mf_ga_args *args, void *d_ws, size_t ws
     c.features = p->d_features;
     c.agg_cols = p->d_agg_cols;
     c.w64 = p->d_w64;
+    c.pre = p->d_pre;
+    c.sumK = p->sumK;
     c.canon = p->d_canon;
     c.wstride = p->wstride;
     c.fixed = (args->flags & MF_FIXED_STATE) ? 1 : 0;

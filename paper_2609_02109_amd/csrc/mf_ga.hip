@@ -252,6 +252,134 @@ __global__ void __launch_bounds__(256) ga_fitness_kernel(const GAConst c, int S,
     fit[t] = (vram_ok && sla_ok) ? J : -INFINITY;
 }
 
+// Canonical fitness, one lane per individual, layer 1 continued from each
+// option's precomputed local-feature chain (only the A aggregate steps are
+// left per individual).  Dynamic LDS: [sumK][H1 + 2] doubles of that chain
+// (rows padded by 16 bytes against bank conflicts), then [sumK][A] floats:
+// each option row's aggregate columns.  The workgroup's waves take the
+// models together (a barrier per model), so that the model's weights, read
+// through scalar loads, stay in the scalar cache.
+template <int A, int H1, int H2, bool BF16>
+__global__ void __launch_bounds__(kGaFitThreads) ga_fitness_pre_kernel(const GAConst c, int S, int P,
+                                                                       const uint64_t *pop, const float *sla,
+                                                                       const float *omega, double *fit)
+{
+    extern __shared__ __align__(16) double pre_s[];
+    constexpr int PS = H1 + 2;
+    float *agg_s = reinterpret_cast<float *>(pre_s + (size_t)c.sumK * PS);
+    __shared__ float s_tau[kMaxN];
+    __shared__ int32_t s_prev[kMaxN];
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int j = 0; j < kMaxN; j++)   // compile-time index into the argument block
+        if (tid == j) {
+            s_tau[j] = c.obj.tau[j];
+            s_prev[j] = c.obj.prev[j];
+        }
+    for (int t = tid; t < c.sumK * H1; t += blockDim.x) {
+        const int r = t / H1;
+        pre_s[r * PS + (t - r * H1)] = c.pre[t];
+    }
+    for (int t = tid; t < c.sumK * A; t += blockDim.x) {
+        const int r = t / A;
+        agg_s[t] = c.features[(int64_t)r * c.L + c.agg_cols[t - r * A]];
+    }
+    __syncthreads();
+    const int64_t n = (int64_t)S * P;
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + tid;
+    // lanes past the population leave: a wave that has ended no longer
+    // counts at the barriers below (and one that is partly done still
+    // executes them)
+    if (t >= n) return;
+    const int64_t tt = t;
+    const int s = (int)(tt / P);
+    const int N = c.N, L = c.L, NIN = L + A;
+    int32_t d[kMaxN];
+    ga_digits(c, pop[tt], d);
+    // aggregate slots: fp32 sums in model order; the surrogates see them, or
+    // the observed state held fixed (the VRAM cap still sees the candidate)
+    double za[A];
+    float agg_v = 0.f;
+#pragma unroll
+    for (int a = 0; a < A; a++) {
+        float x = 0.f;
+        for (int i = 0; i < N; i++) x = x + agg_s[(c.opt_off[i] + d[i]) * A + a];
+        za[a] = c.fixed ? (double)c.state[a] : (double)x;
+        if (a == c.vram_slot) agg_v = x;
+    }
+    const bool vram_ok = (double)agg_v <= (double)c.vram_cap;
+    bool sla_ok = true;
+    double J = 0.0;
+    for (int i = 0; i < N; i++) {
+        // a bare barrier: it orders no memory, so the weights below stay
+        // scalar loads (read-only for the whole kernel, in the constant
+        // address space)
+        __builtin_amdgcn_s_barrier();
+        typedef const __attribute__((address_space(4))) double cdouble;
+        const cdouble *w = (const cdouble *)(c.w64 + (int64_t)i * c.wstride);
+        const cdouble *W1a = w + L, *W2 = w + (int64_t)H1 * NIN + H1, *b2 = W2 + H2 * H1, *W3 = b2 + H2,
+                      *b3 = W3 + 2 * H2;
+        const double *pr = pre_s + (c.opt_off[i] + d[i]) * PS;
+        double h1[H1];
+#pragma unroll
+        for (int u = 0; u < H1; u += 2) {
+            const double2 v = *reinterpret_cast<const double2 *>(pr + u);
+            h1[u] = v.x;
+            h1[u + 1] = v.y;
+        }
+#pragma unroll
+        for (int u = 0; u < H1; u++) {
+            if (BF16) {
+                // the fp32 chain continues over the aggregate inputs, relu,
+                // round to bfloat16
+                float a = (float)h1[u];
+#pragma unroll
+                for (int k = 0; k < A; k++) a = fmaf((float)W1a[u * NIN + k], (float)za[k], a);
+                a = a > 0.f ? a : 0.f;
+                const uint32_t bits = __float_as_uint(a);
+                const uint32_t r = (bits + 0x7FFFu + ((bits >> 16) & 1u)) & 0xFFFF0000u;
+                h1[u] = (double)__uint_as_float(r);
+            } else {
+                double a = h1[u];
+#pragma unroll
+                for (int k = 0; k < A; k++) a = fma(W1a[u * NIN + k], za[k], a);
+                h1[u] = a > 0.0 ? a : 0.0;
+            }
+        }
+        double y0 = b3[0], y1 = b3[1];
+        // four layer-2 chains in flight (each in input order; the layer-3
+        // chains take them in unit order)
+#pragma unroll 4
+        for (int v = 0; v < H2; v++) {
+            double a = b2[v];
+#pragma unroll
+            for (int u = 0; u < H1; u++) a = fma(W2[v * H1 + u], h1[u], a);
+            a = a > 0.0 ? a : 0.0;
+            y0 = fma(W3[v], a, y0);
+            y1 = fma(W3[H2 + v], a, y1);
+        }
+        if (c.act) {   // the predictor's sigmoid output
+            y0 = canon_sigmoid(y0);
+            y1 = canon_sigmoid(y1);
+        }
+        if (!(y0 <= (double)sla[(int64_t)s * N + i])) sla_ok = false;
+        const double om = (double)omega[(int64_t)s * N + i];
+        if (c.obj.kind != 0) {
+            // the full utility of Eq. 3, canonical term order
+            double q, Pr, pen;
+            bool do_P, do_pen;
+            if (!canon_eq3(c.obj, c.opt_off[i] + d[i], y1, s_tau[i], s_prev[i], q, Pr, do_P, pen, do_pen))
+                sla_ok = false;
+            J = fma(om, q, J);
+            if (do_P) J = J - Pr;
+            if (do_pen) J = J - pen;
+        } else {
+            J = fma(om, y1, J);
+        }
+    }
+    fit[t] = (vram_ok && sla_ok) ? J : -INFINITY;
+}
+
 // Canonical fp64 fitness, one workgroup per individual (small populations,
 // and shapes the one-lane kernel does not take): wave w runs the canonical
 // forward of models w, w + W, ... (W waves), each on its own LDS scratch; lane
@@ -556,10 +684,34 @@ int ga_fitness_supported(int nin, int h1, int h2)
            (h1 == 64 && h2 == 64 && (nin == 12 || nin == 16 || nin == 22));
 }
 
+template <int A, int H1, int H2>
+static hipError_t launch_fit_pre_t(const GAConst &c, int S, int P, const uint64_t *pop, const float *sla,
+                                   const float *omega, double *fit, size_t lds, hipStream_t st)
+{
+    const int64_t n = (int64_t)S * P;
+    const int grid = (int)((n + kGaFitThreads - 1) / kGaFitThreads);
+    auto fn = c.bf16 ? ga_fitness_pre_kernel<A, H1, H2, true> : ga_fitness_pre_kernel<A, H1, H2, false>;
+    const hipError_t e = ensure_dyn_lds((const void *)fn, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(kGaFitThreads), lds, st, c, S, P, pop, sla, omega, fit);
+    return hipGetLastError();
+}
+
 hipError_t launch_ga_fitness(const GAConst &c, int S, int P, const uint64_t *pop, const float *sla, const float *omega,
                              double *fit, hipStream_t st)
 {
     const int nin = c.L + c.A;
+    // large populations: the kernel that continues each option's local chain,
+    // when the chain table and the aggregate columns fit in LDS
+    const size_t pre_lds = (size_t)c.sumK * (c.H1 + 2) * 8 + (size_t)c.sumK * c.A * 4;
+    if ((int64_t)S * P > kGaWideMax && c.pre && pre_lds <= kGaPreLdsBytes) {
+#define MF_GA_PRE(AA, HA, HB) \
+    if (c.A == AA && c.H1 == HA && c.H2 == HB) return launch_fit_pre_t<AA, HA, HB>(c, S, P, pop, sla, omega, fit, pre_lds, st);
+        MF_GA_PRE(2, 32, 32) MF_GA_PRE(4, 32, 32) MF_GA_PRE(6, 32, 32) MF_GA_PRE(8, 32, 32)
+        MF_GA_PRE(2, 64, 32) MF_GA_PRE(4, 64, 32) MF_GA_PRE(6, 64, 32) MF_GA_PRE(8, 64, 32)
+        MF_GA_PRE(2, 64, 64) MF_GA_PRE(4, 64, 64) MF_GA_PRE(6, 64, 64) MF_GA_PRE(8, 64, 64)
+#undef MF_GA_PRE
+    }
     if ((int64_t)S * P <= kGaWideMax || !ga_fitness_supported(nin, c.H1, c.H2)) {
         const int64_t n = (int64_t)S * P;
         // every model's weights in LDS when they fit (the canonical image is

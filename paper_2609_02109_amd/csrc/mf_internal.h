@@ -400,6 +400,8 @@ struct GAConst {
     const float *features;      // [sumK][L]
     const int32_t *agg_cols;    // [A]
     const double *w64;          // [N][stride] packed weights (W1 b1 W2 b2 W3 b3) as fp64
+    const double *pre;          // [sumK][H1] canonical layer-1 chain over each option's local features
+    int sumK;
     const float *canon;         // [N][stride] canonical image (W1^T b1 W2^T b2 W3 b3)
     int64_t wstride;
     int fixed;                  // the surrogates see state[] instead of the candidate's aggregate
@@ -457,6 +459,8 @@ constexpr int kCanonWaves = 8;             // certification of few entries: wave
 constexpr int kCanonFewEntries = 1024;     // index lists up to this length count as few
 constexpr int kGaWideWaves = 8;             // ... with up to this many waves (models) per workgroup
 constexpr size_t kGaStageBytes = 64 * 1024;   // ... copying the weights to LDS when they fit in this
+constexpr int kGaFitThreads = 512;             // large populations: lanes (individuals) per fitness workgroup
+constexpr size_t kGaPreLdsBytes = 96 * 1024;   // ... continuing the local-feature chains staged in this much LDS
 constexpr int64_t kGaWideStagedWgs = 512;    // ... and then running this many workgroups at most
 int ga_fitness_supported(int nin, int h1, int h2);
 hipError_t launch_ga_feasible(const GAConst &c, uint32_t *blk_count, uint64_t *blk_off, unsigned long long *n_fl,
