@@ -846,9 +846,18 @@ uint64_t fixed_blocks(const mf_problem &p, uint64_t lo, uint64_t n, uint64_t &bl
 
 // One wave per block at least; at most the workgroups the CUs hold at once
 // (every wave gets the same number of blocks, so one resident round).
+// Workgroups of the scan: at most wgs_per_cu per CU.  Every wave takes the
+// same number of consecutive blocks where a grid of wgs_per_cu or
+// wgs_per_cu - 1 workgroups per CU allows it (measured on the MI355X: an even
+// split beats one more workgroup per CU with a ragged one, e.g. the 24^6
+// scan on 3 per CU, the 16^8 one on 4); otherwise the largest grid.
 int fixed_grid(const mf_problem &p, uint64_t n_blocks, int wgs_per_cu)
 {
     const uint64_t g = (n_blocks + kFixedWaves - 1) / kFixedWaves;
+    for (int w = wgs_per_cu; w >= 1 && w >= wgs_per_cu - 1; w--) {
+        const uint64_t waves = (uint64_t)p.num_cus * w * kFixedWaves;
+        if (waves <= n_blocks && n_blocks % waves == 0) return (int)((uint64_t)p.num_cus * w);
+    }
     return (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)p.num_cus * wgs_per_cu));
 }
 
@@ -926,7 +935,6 @@ mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipS
     a.wg_counts = reinterpret_cast<unsigned long long *>(ws + w.counts);
     a.res = reinterpret_cast<DevResult *>(ws + w.res);
     const bool dump = (args->flags & MF_DUMP) != 0;
-    const int wgs_per_cu = fixed_wgs_per_cu(a);
 
     hipEvent_t ev0 = ev.start(), ev1 = ev.stop();
     mf_status st = MF_OK;
@@ -937,11 +945,16 @@ mf_status search_fixed(mf_problem *p, const mf_search_args *args, char *ws, hipS
         a.n_blocks = fixed_blocks(*p, lo, n, a.block0);
         a.part_block_lo = lo % a.inner ? lo / a.inner : ~0ull;
         a.part_block_hi = (lo + n) % a.inner ? (lo + n) / a.inner : ~0ull;
+        a.mask = dump ? args->d_mask + (lo - args->lo) : nullptr;
+        a.pred = dump ? args->d_pred + (lo - args->lo) * (uint64_t)p->N * 2u : nullptr;
+        // the scan kernel depends on these fields: its occupancy is queried
+        // with them set (blocks per wave at one workgroup per CU, a bound)
+        const uint64_t waves1 = (uint64_t)p->num_cus * kFixedWaves;
+        a.blocks_per_wave = (a.n_blocks + waves1 - 1) / waves1;
+        const int wgs_per_cu = fixed_wgs_per_cu(a);
         const int grid = fixed_grid(*p, a.n_blocks, wgs_per_cu);
         const uint64_t waves = (uint64_t)grid * kFixedWaves;
         a.blocks_per_wave = (a.n_blocks + waves - 1) / waves;
-        a.mask = dump ? args->d_mask + (lo - args->lo) : nullptr;
-        a.pred = dump ? args->d_pred + (lo - args->lo) * (uint64_t)p->N * 2u : nullptr;
         DevResult h{};
         float ms = 0.f;
         if (hipMemsetAsync(a.res, 0, sizeof(DevResult), s) != hipSuccess ||

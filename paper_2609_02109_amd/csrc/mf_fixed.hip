@@ -116,7 +116,7 @@ struct Tile {
     uint32_t rr[NI];
 };
 
-template <int NI, bool EQ3, bool LC>
+template <int NI, bool EQ3, bool LC, bool EXACT>
 __device__ __forceinline__ Tile<NI> eval_tile(const FixedArgs &a, const FixedRow *rows, const FixedPen *pens,
                                               uint32_t u, uint32_t t0, int ni, uint32_t M, const double *omi,
                                               double Jp, float vp, uint32_t flp, const FixedRow &rb,
@@ -131,6 +131,19 @@ __device__ __forceinline__ Tile<NI> eval_tile(const FixedArgs &a, const FixedRow
         o.rr[1] = row_b;
         chain_row<EQ3>(rows, pens, o.rr[0], omi[0], o.J, o.v, o.fl);
         chain_step<EQ3>(rb, pens, row_b, omi[1], o.J, o.v, o.fl);
+    } else if (EXACT) {
+        // exactly NI inner models, each but the first with at least two
+        // options, and u < M: the digits with no guards
+        uint32_t uu = u;
+#pragma unroll
+        for (int t = NI - 1; t > 0; t--) {
+            const uint32_t q = __umulhi(uu, a.in_magic[t]);
+            o.rr[t] = (uint32_t)a.in_off[t] + (uu - q * (uint32_t)a.in_K[t]);
+            uu = q;
+        }
+        o.rr[0] = (uint32_t)a.in_off[0] + uu;
+#pragma unroll
+        for (int t = 0; t < NI; t++) chain_row<EQ3>(rows, pens, o.rr[t], omi[t], o.J, o.v, o.fl);
     } else {
         uint32_t uu = u < M ? u : 0u;
 #pragma unroll
@@ -184,7 +197,7 @@ __device__ __forceinline__ void dump_tile(const FixedArgs &a, const Tile<NI> &x,
 // lane-constant (its row lives in registers) and the other inner digit is a
 // shift of the tile offset.
 // ---------------------------------------------------------------------------
-template <int NI, bool EQ3, bool LC>
+template <int NI, bool EQ3, bool LC, bool EXACT = false>
 __global__ void __launch_bounds__(kFixedWaves * 64) fixed_scan_kernel(const FixedArgs a)
 {
     extern __shared__ float4 smem4[];
@@ -291,8 +304,8 @@ __global__ void __launch_bounds__(kFixedWaves * 64) fixed_scan_kernel(const Fixe
                 const bool two = LC || t0 + 64 < M;
                 const uint32_t t1 = two ? t0 + 64 : t0;
                 const uint32_t ux = t0 + (uint32_t)lane, uy = t1 + (uint32_t)lane;
-                const Tile<NI> x = eval_tile<NI, EQ3, LC>(a, rows, pens, ux, t0, ni, M, omi, Jp, vp, flp, rb, row_a0, row_b);
-                const Tile<NI> y = eval_tile<NI, EQ3, LC>(a, rows, pens, uy, t1, ni, M, omi, Jp, vp, flp, rb, row_a0, row_b);
+                const Tile<NI> x = eval_tile<NI, EQ3, LC, EXACT>(a, rows, pens, ux, t0, ni, M, omi, Jp, vp, flp, rb, row_a0, row_b);
+                const Tile<NI> y = eval_tile<NI, EQ3, LC, EXACT>(a, rows, pens, uy, t1, ni, M, omi, Jp, vp, flp, rb, row_a0, row_b);
                 unsigned long long mvx = ~0ull, mvy = two ? ~0ull : 0ull;   // valid lanes
                 if (!WHOLE) {
                     mvx = ballot64(ux - u_lo < u_span);
@@ -339,6 +352,203 @@ __global__ void __launch_bounds__(kFixedWaves * 64) fixed_scan_kernel(const Fixe
         }
     }
 
+    // counts and list per workgroup (the merge kernel sums and merges them)
+    __shared__ unsigned long long s_cnt[2 * kFixedWaves];
+    if (lane == 0) {
+        s_cnt[wv] = c_vram;
+        s_cnt[kFixedWaves + wv] = c_feas;
+    }
+    lst[wv * 64 + lane] = key_if(lane < k, slot);
+    __syncthreads();
+    if (wv == 0) {
+#pragma unroll 1
+        for (int w = 1; w < kFixedWaves; w++) list128_offer(slot, lst[w * 64 + lane], lane, k, thr);
+        if (lane < k) a.wg_lists[(uint64_t)blockIdx.x * k + lane] = slot;
+        if (lane < 2) {
+            unsigned long long t = 0;
+            for (int w = 0; w < kFixedWaves; w++) t += s_cnt[lane * kFixedWaves + w];
+            a.wg_counts[2 * (uint64_t)blockIdx.x + lane] = t;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Scan with a periodic last digit: two inner models a (first) and b (last),
+// K_b options for b.  Over the inner configurations u = 64 t + lane of a
+// block, b = u mod K_b depends on the lane and on t mod P only, with
+// P = K_b / gcd(64, K_b), and a = G (t div P) + A_p(lane), G = 64 P / K_b.
+// Each lane keeps its P rows of model b in registers and its P first rows of
+// model a as LDS addresses; a tile is then one row read, the chain steps of
+// a and b in model order, and three compares.  Taken when the inner block is
+// a whole number of P-tile groups, every block of the range is whole and no
+// dump is asked for.  Under Eq. 3 the penalties are staged with zeros where a
+// row's flags do not apply them (subtracting +0 changes no value), so the
+// chain needs no test.  NG > 0: the block is exactly NG groups, unrolled
+// (row offsets then differ by constants); NG = 0: a loop over the groups.
+// ---------------------------------------------------------------------------
+template <int P, bool EQ3, int NG = 0>
+__global__ void __launch_bounds__(kFixedWaves * 64) fixed_periodic_kernel(const FixedArgs a)
+{
+    extern __shared__ float4 smem4[];
+    __shared__ double s_om[kMaxN];
+    __shared__ int32_t s_off[kMaxN], s_K[kMaxN];
+    __shared__ uint32_t s_od[kFixedWaves][kMaxN];
+    FixedRow *rows = reinterpret_cast<FixedRow *>(smem4);
+    FixedPen *pens = reinterpret_cast<FixedPen *>(rows + a.sumK);   // Eq. 3: zero where not applied
+    K128 *lst = reinterpret_cast<K128 *>(pens + (EQ3 ? a.sumK : 0));
+    const int N = a.n_models, nout = a.n_outer, k = a.top_k;
+#pragma unroll 1
+    for (int t = threadIdx.x; t < a.sumK; t += blockDim.x) {
+        const FixedRow r = a.rows[t];
+        rows[t] = r;
+        if (EQ3) {
+            const FixedPen pp = a.pens[t];
+            pens[t] = FixedPen{(r.flags & kRowP) ? pp.P : 0.0, (r.flags & kRowPen) ? pp.pen : 0.0};
+        }
+    }
+    if (threadIdx.x < (unsigned)N) s_om[threadIdx.x] = (double)a.omega[threadIdx.x];
+#pragma unroll
+    for (int j = 0; j < kMaxN; j++)   // compile-time index into the argument block
+        if (threadIdx.x == (unsigned)j) {
+            s_off[j] = a.opt_off[j];
+            s_K[j] = a.K[j];
+        }
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const uint64_t gw = (uint64_t)blockIdx.x * kFixedWaves + wv;
+    const uint64_t b_first = gw * a.blocks_per_wave;
+    const uint64_t b_begin = a.block0 + (b_first < a.n_blocks ? b_first : a.n_blocks);
+    const uint64_t b_end = a.block0 + (b_first + a.blocks_per_wave < a.n_blocks ? b_first + a.blocks_per_wave
+                                                                                : a.n_blocks);
+    const uint32_t M = a.inner, Kb = (uint32_t)a.in_K[1];
+    const uint32_t n_grp = M / (64u * P);              // P-tile groups per block
+    const uint32_t G = 64u * P / Kb;                   // rows of model a per group
+    const float cap = a.vram_cap;
+    uint32_t *od = s_od[wv];
+    if (lane == 0) {
+        uint64_t x = b_begin;
+        for (int j = nout - 1; j >= 0; j--) {
+            od[j] = (uint32_t)(x % (uint64_t)a.K[j]);
+            x /= (uint64_t)a.K[j];
+        }
+    }
+    __syncthreads();
+
+    // this lane's rows: model b for each phase p (registers), model a's first
+    // row for each phase (an LDS index, advanced by G per group)
+    const double oma = (double)a.omega[nout], omb = (double)a.omega[nout + 1];
+    double bq[P], bP[P], bpen[P];
+    float bv[P];
+    uint32_t bf[P], ra0[P];
+#pragma unroll
+    for (int p = 0; p < P; p++) {
+        const uint32_t u = 64u * p + (uint32_t)lane;
+        const uint32_t rb = (uint32_t)a.in_off[1] + u % Kb;
+        const FixedRow r = rows[rb];
+        bq[p] = r.q;
+        bv[p] = r.vram;
+        bf[p] = r.flags;
+        bP[p] = EQ3 ? pens[rb].P : 0.0;
+        bpen[p] = EQ3 ? pens[rb].pen : 0.0;
+        ra0[p] = (uint32_t)a.in_off[0] + u / Kb;
+    }
+    uint32_t aoff[P];   // byte offsets of this lane's first rows of model a (rows and penalties alike)
+#pragma unroll
+    for (int p = 0; p < P; p++) aoff[p] = ra0[p] * (uint32_t)sizeof(FixedRow);
+    static_assert(sizeof(FixedRow) == sizeof(FixedPen), "one offset serves both tables");
+
+    K128 slot = {0ull, 0ull}, thr = {0ull, 0ull};
+    double thrJ = -INFINITY;
+    unsigned long long c_vram = 0, c_feas = 0;   // wave-uniform
+    double Jc = 0.0;   // chain over outer models 0..nout-2
+    float vc = 0.f;
+    uint32_t flc = 0u;
+    bool need_full = true;
+    uint32_t dl = nout > 0 ? od[nout - 1] : 0u;
+    const uint32_t K_last = nout > 0 ? (uint32_t)a.K[nout - 1] : 1u;
+    const uint32_t off_last = nout > 0 ? (uint32_t)a.opt_off[nout - 1] : 0u;
+    const double om_last = nout > 0 ? (double)a.omega[nout - 1] : 0.0;
+
+    // counts in 32 bits over the whole run (the host keeps a run below 2^32
+    // configurations); the block's first joint index advances by M
+    const uint32_t n_blk = (uint32_t)(b_end - b_begin);
+    uint32_t cv = 0, cf = 0;
+    uint64_t base = b_begin * (uint64_t)M;
+#pragma unroll 1
+    for (uint32_t bi = 0; bi < n_blk; bi++, base += M) {
+        if (need_full) {
+            Jc = 0.0;
+            vc = 0.f;
+            flc = 0u;
+#pragma unroll 1
+            for (int j = 0; j < nout - 1; j++)
+                chain_row<EQ3>(rows, pens, (uint32_t)s_off[j] + od[j], s_om[j], Jc, vc, flc);
+            need_full = false;
+        }
+        double Jp = Jc;
+        float vp = vc;
+        uint32_t flp = flc;
+        if (nout > 0) chain_row<EQ3>(rows, pens, off_last + dl, om_last, Jp, vp, flp);
+        // model a's rows of group g: each lane's first rows (its byte
+        // offsets) plus one uniform offset per group
+        const char *grow = reinterpret_cast<const char *>(rows);
+        const char *gpen = reinterpret_cast<const char *>(pens);
+        uint64_t ibase = base;   // joint index of the group's first configuration
+        // one tile: phase p of a group whose model-a rows start at grow
+        auto tile = [&](const char *gr, const char *gp, uint64_t ib, int p) {
+            const FixedRow x = *reinterpret_cast<const FixedRow *>(gr + aoff[p]);
+            const float v = (vp + x.vram) + bv[p];
+            const uint32_t fl = flp | x.flags | bf[p];
+            double J = fma(oma, x.q, Jp);
+            if (EQ3) {
+                const FixedPen pa = *reinterpret_cast<const FixedPen *>(gp + aoff[p]);
+                J = (J - pa.P) - pa.pen;
+            }
+            J = fma(omb, bq[p], J);
+            if (EQ3) J = (J - bP[p]) - bpen[p];
+            const unsigned long long mv = ballot64(v <= cap);
+            const unsigned long long mf = mv & ballot64((int32_t)fl >= 0);
+            const unsigned long long mc = mf & ballot64(J >= thrJ);
+            cv += (uint32_t)__popcll(mv);
+            cf += (uint32_t)__popcll(mf);
+            if (mc) offer_mask(slot, thr, thrJ, mc, J, ib + (uint64_t)(p * 64 + lane), lane, k);
+        };
+        if constexpr (NG > 0) {
+#pragma unroll
+            for (int g = 0; g < NG; g++)
+#pragma unroll
+                for (int p = 0; p < P; p++)
+                    tile(grow + g * G * sizeof(FixedRow), gpen + g * G * sizeof(FixedPen), base + (uint64_t)g * 64u * P,
+                         p);
+        } else {
+#pragma unroll 1
+            for (uint32_t g = 0; g < n_grp; g++) {
+#pragma unroll
+                for (int p = 0; p < P; p++) tile(grow, gpen, ibase, p);
+                grow += G * sizeof(FixedRow);
+                gpen += G * sizeof(FixedPen);
+                ibase += 64u * P;
+            }
+        }
+        // next block: the last outer digit, and on its wrap the odometer of
+        // the others (lane 0 writes the wave's digits)
+        if (nout > 0 && ++dl == K_last) {
+            dl = 0u;
+            bool carry = true;
+            for (int j = nout - 2; j >= 0 && carry; j--) {
+                uint32_t d = od[j] + 1u;
+                carry = d == (uint32_t)s_K[j];
+                if (carry) d = 0u;
+                __builtin_amdgcn_wave_barrier();
+                if (lane == 0) od[j] = d;
+                __builtin_amdgcn_wave_barrier();
+            }
+            need_full = true;
+        }
+    }
+
+    c_vram = cv;
+    c_feas = cf;
     // counts and list per workgroup (the merge kernel sums and merges them)
     __shared__ unsigned long long s_cnt[2 * kFixedWaves];
     if (lane == 0) {
@@ -452,7 +662,36 @@ static ScanFn scan_fn(const FixedArgs &a)
 {
     const bool eq3 = a.obj.kind != 0;
     const int ni = a.n_models - a.n_outer;
+    // two inner models, a periodic last digit, whole blocks, no dump
+    if (ni == 2 && !a.mask && a.part_block_lo == ~0ull && a.part_block_hi == ~0ull && a.in_K[1] >= 1 &&
+        a.blocks_per_wave * (uint64_t)a.inner < (1ull << 32)) {
+        const uint32_t kb = (uint32_t)a.in_K[1];
+        uint32_t g = 64, x = kb;
+        while (x) {
+            const uint32_t t = g % x;
+            g = x;
+            x = t;
+        }
+        const uint32_t per = kb / g;
+        // option counts up to 255 give P = 1 (powers of two), 2 (128) or 3
+        // (3 times a power of two)
+        if (per <= 3 && a.inner % (64u * per) == 0) {
+            // blocks of 3 groups of 3 tiles (24 x 24 options) and of 4
+            // single tiles (16 x 16) unrolled
+            const uint32_t ng = a.inner / (64u * per);
+            if (per == 3 && ng == 3) return eq3 ? fixed_periodic_kernel<3, true, 3> : fixed_periodic_kernel<3, false, 3>;
+            if (per == 1 && ng == 4) return eq3 ? fixed_periodic_kernel<1, true, 4> : fixed_periodic_kernel<1, false, 4>;
+            switch (per) {
+                case 1: return eq3 ? fixed_periodic_kernel<1, true> : fixed_periodic_kernel<1, false>;
+                case 2: return eq3 ? fixed_periodic_kernel<2, true> : fixed_periodic_kernel<2, false>;
+                case 3: return eq3 ? fixed_periodic_kernel<3, true> : fixed_periodic_kernel<3, false>;
+            }
+        }
+    }
     if (a.lc_shift >= 0) return eq3 ? fixed_scan_kernel<2, true, true> : fixed_scan_kernel<2, false, true>;
+    // two inner models, the second with at least two options, whole 64-tiles
+    if (ni == 2 && a.in_K[1] >= 2 && a.inner % 64 == 0)
+        return eq3 ? fixed_scan_kernel<2, true, false, true> : fixed_scan_kernel<2, false, false, true>;
     return ni <= 2 ? (eq3 ? fixed_scan_kernel<2, true, false> : fixed_scan_kernel<2, false, false>)
          : ni <= 4 ? (eq3 ? fixed_scan_kernel<4, true, false> : fixed_scan_kernel<4, false, false>)
                    : (eq3 ? fixed_scan_kernel<kMaxN, true, false> : fixed_scan_kernel<kMaxN, false, false>);

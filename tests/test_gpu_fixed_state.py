@@ -69,6 +69,30 @@ def test_fixed_eq3_n5_full(mf, orc, seed):
     assert r["n_feas"] > 0
 
 
+# Shapes whose last two models form the scanned inner block with a periodic
+# last digit (its option count 3 x 2^j, 128 or 2^j): whole-space searches
+# without a dump take the scan that keeps each lane's rows of the last model
+# in registers.  Counts, top-k indices and canonical J against the oracle.
+# (instance seeds with feasible configurations under both objectives)
+@pytest.mark.parametrize("n_options,period,seed", [([5, 16, 24], 3, 0), ([3, 2, 128], 2, 3), ([7, 16, 16], 1, 0),
+                                                   ([2, 4, 8, 48], 3, 0), ([5, 24, 24], 3, 0), ([3, 16, 32], 1, 0)])
+@pytest.mark.parametrize("eq3", [False, True])
+def test_fixed_periodic_last_digit(mf, orc, n_options, period, seed, eq3):
+    inst = synth.make_instance(n_options, 8, 4, 32, 32, seed=seed, vram_quantile=0.7)
+    state = synth.make_state(inst, 3)
+    ob = synth.make_objective(inst, 3) if eq3 else None
+    k = 8 if eq3 else 16
+    print(f"[fixed periodic] K={n_options} eq3={eq3}", flush=True)
+    p = mf.Problem(inst, variants=ob)
+    g = p.search(inst.sla, inst.omega, k=k, objective=ob, state=state)
+    r = orc.Problem(inst, ob, state=state).search(inst.sla, inst.omega, k=k, lo=0, hi=inst.space_size)
+    p.close()
+    assert g["n_vram"] == r["n_vram"] and g["n_feas"] == r["n_feas"]
+    assert 0 < r["n_feas"] < inst.space_size
+    np.testing.assert_array_equal(g["top_idx"], r["top_idx"])
+    assert g["top_J"].tobytes() == r["top_J"].tobytes()
+
+
 def test_fixed_n6_ranges(mf, orc):
     inst = synth.cfg2(0)
     st = synth.make_state(inst, 0)
