@@ -212,7 +212,9 @@ def bench_fixed(mf, torch, seed, steps, warmup):
                      "n_feas": int(r.n_feas), "argmax": int(r.top_idx[0]),
                      "roofline": {"bound": "alu", "achieved": ach, "peak": PEAK_VALU_GINST,
                                   "unit": "G VALU wave-instr/s", "frac": ach / PEAK_VALU_GINST,
-                                  "alg_lane_ops_per_config": ops}}
+                                  "alg_lane_ops_per_config": ops,
+                                  "note": "the 9 operations include the J chain, which blocks whose exact J upper "
+                                          "bound is under the wave's k-th J skip (linear objective)"}}
     out["workload"] = ("the N=6 and N=8 searches with the surrogates' aggregate input held at a seeded observed "
                        "state (linear objective; N=6 also with Eq. 3)")
     return out

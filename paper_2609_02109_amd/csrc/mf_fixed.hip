@@ -452,6 +452,24 @@ __global__ void __launch_bounds__(kFixedWaves * 64) fixed_periodic_kernel(const 
         bpen[p] = EQ3 ? pens[rb].pen : 0.0;
         ra0[p] = (uint32_t)a.in_off[0] + u / Kb;
     }
+    // linear objective: the rows of a and of b with the largest omega q (the
+    // largest q for omega >= 0, the smallest otherwise).  RN and fma are
+    // monotone, so fma(omb, qb*, fma(oma, qa*, Jp)) bounds the J of every
+    // configuration of a block from above, bit for bit
+    double qa_star = 0.0, qb_star = 0.0;
+    if constexpr (!EQ3) {
+        for (int t = 0; t < 2; t++) {
+            const int K = a.in_K[t], off = a.in_off[t];
+            const bool up = (t == 0 ? oma : omb) >= 0.0;
+            double best = rows[off].q;
+            for (int r = 1; r < K; r++) {
+                const double q = rows[off + r].q;
+                if (up ? q > best : q < best) best = q;
+            }
+            if (t == 0) qa_star = best;
+            else qb_star = best;
+        }
+    }
     uint32_t aoff[P];   // byte offsets of this lane's first rows of model a (rows and penalties alike)
 #pragma unroll
     for (int p = 0; p < P; p++) aoff[p] = ra0[p] * (uint32_t)sizeof(FixedRow);
@@ -495,10 +513,21 @@ __global__ void __launch_bounds__(kFixedWaves * 64) fixed_periodic_kernel(const 
         const char *gpen = reinterpret_cast<const char *>(pens);
         uint64_t ibase = base;   // joint index of the group's first configuration
         // one tile: phase p of a group whose model-a rows start at grow
-        auto tile = [&](const char *gr, const char *gp, uint64_t ib, int p) {
+        // no configuration of the block can enter the wave's list when its
+        // prefix fails a bound or its largest J is under the k-th J: then
+        // only the counts are formed
+        const bool counts_only = !EQ3 && ((int32_t)flp < 0 || fma(omb, qb_star, fma(oma, qa_star, Jp)) < thrJ);
+        auto tile = [&](const char *gr, const char *gp, uint64_t ib, int p, auto co) {
+            constexpr bool CO = decltype(co)::value;
             const FixedRow x = *reinterpret_cast<const FixedRow *>(gr + aoff[p]);
             const float v = (vp + x.vram) + bv[p];
             const uint32_t fl = flp | x.flags | bf[p];
+            if constexpr (CO) {
+                const unsigned long long mv = ballot64(v <= cap);
+                cv += (uint32_t)__popcll(mv);
+                cf += (uint32_t)__popcll(mv & ballot64((int32_t)fl >= 0));
+                return;
+            }
             double J = fma(oma, x.q, Jp);
             if (EQ3) {
                 const FixedPen pa = *reinterpret_cast<const FixedPen *>(gp + aoff[p]);
@@ -513,23 +542,27 @@ __global__ void __launch_bounds__(kFixedWaves * 64) fixed_periodic_kernel(const 
             cf += (uint32_t)__popcll(mf);
             if (mc) offer_mask(slot, thr, thrJ, mc, J, ib + (uint64_t)(p * 64 + lane), lane, k);
         };
-        if constexpr (NG > 0) {
+        auto groups = [&](auto co) {
+            if constexpr (NG > 0) {
 #pragma unroll
-            for (int g = 0; g < NG; g++)
+                for (int g = 0; g < NG; g++)
 #pragma unroll
-                for (int p = 0; p < P; p++)
-                    tile(grow + g * G * sizeof(FixedRow), gpen + g * G * sizeof(FixedPen), base + (uint64_t)g * 64u * P,
-                         p);
-        } else {
+                    for (int p = 0; p < P; p++)
+                        tile(grow + g * G * sizeof(FixedRow), gpen + g * G * sizeof(FixedPen),
+                             base + (uint64_t)g * 64u * P, p, co);
+            } else {
 #pragma unroll 1
-            for (uint32_t g = 0; g < n_grp; g++) {
+                for (uint32_t g = 0; g < n_grp; g++) {
 #pragma unroll
-                for (int p = 0; p < P; p++) tile(grow, gpen, ibase, p);
-                grow += G * sizeof(FixedRow);
-                gpen += G * sizeof(FixedPen);
-                ibase += 64u * P;
+                    for (int p = 0; p < P; p++) tile(grow, gpen, ibase, p, co);
+                    grow += G * sizeof(FixedRow);
+                    gpen += G * sizeof(FixedPen);
+                    ibase += 64u * P;
+                }
             }
-        }
+        };
+        if (counts_only) groups(BoolC<true>{});
+        else groups(BoolC<false>{});
         // next block: the last outer digit, and on its wrap the odometer of
         // the others (lane 0 writes the wave's digits)
         if (nout > 0 && ++dl == K_last) {
