@@ -439,6 +439,57 @@ __device__ __forceinline__ void work_append(bool flag, unsigned long long entry,
     }
 }
 
+// A wave's certification entries buffered in registers, one per lane
+// (lanes [0, n) hold entries; n is wave-uniform), written to the device list
+// 64 at a time: one reservation and contiguous stores instead of a partial
+// line per append.  The list's order carries no meaning.
+struct WorkBuf {
+    unsigned long long e;
+    float j;
+    int n;
+};
+
+__device__ __forceinline__ void wb_flush(WorkBuf &b, int lane, unsigned long long *count, unsigned long long *list,
+                                         float *list_J, uint32_t cap)
+{
+    if (b.n == 0) return;
+    unsigned long long base = 0;
+    if (lane == 0) base = atomicAdd(count, (unsigned long long)b.n);
+    base = readlane64(base, 0);
+    if (lane < b.n) {
+        const unsigned long long slot = base + (unsigned long long)lane;
+        if (slot < cap) {
+            list[slot] = b.e;
+            list_J[slot] = b.j;
+        }
+    }
+    b.n = 0;
+}
+
+// Append the flagged lanes' (entry, fj).  Each flagged lane's values move to
+// buffer lane n + (its rank among the flagged lanes); the other lanes move to
+// the remaining lanes, so the move is a permutation of the wave.
+__device__ __forceinline__ void wb_append(WorkBuf &b, bool flag, unsigned long long entry, float fj, int lane,
+                                          unsigned long long *count, unsigned long long *list, float *list_J,
+                                          uint32_t cap)
+{
+    const unsigned long long m = __ballot(flag);
+    if (m == 0ull) return;
+    const int c = __popcll(m);
+    if (b.n + c > 64) wb_flush(b, lane, count, list, list_J, cap);
+    const unsigned long long lt = (1ull << lane) - 1ull;
+    const int r = flag ? __popcll(m & lt) : c + __popcll(~m & lt);
+    const int dst = ((b.n + r) & 63) * 4;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_ds_permute(dst, (int)(uint32_t)entry);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_ds_permute(dst, (int)(uint32_t)(entry >> 32));
+    const uint32_t jj = (uint32_t)__builtin_amdgcn_ds_permute(dst, __float_as_int(fj));
+    if (lane >= b.n && lane < b.n + c) {
+        b.e = (unsigned long long)lo | ((unsigned long long)hi << 32);
+        b.j = __int_as_float((int)jj);
+    }
+    b.n += c;
+}
+
 // Smallest float >= x (x finite double).
 __device__ __forceinline__ float f32_up(double x)
 {

@@ -377,6 +377,10 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
     WaveList<1> wl;
     wl_init(wl);
     uint32_t c_vram = 0, c_feas = 0;
+    WorkBuf wbuf;   // certification entries (the general search path)
+    wbuf.e = 0ull;
+    wbuf.j = 0.f;
+    wbuf.n = 0;
 
     for (uint64_t tile = gw; tile < n_tiles; tile += (uint64_t)args.total_waves) {
         const uint64_t off = tile * 32u + (uint64_t)col;
@@ -564,7 +568,7 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
                         }
                     }
                 } else {
-                    work_append(unc, went, U, lane, &args.res->n_work, args.work, args.work_J, args.work_cap);
+                    wb_append(wbuf, unc, went, U, lane, &args.res->n_work, args.work, args.work_J, args.work_cap);
                 }
                 const unsigned long long key = feas_sure
                     ? (((unsigned long long)ord_f32(U) << 32) | (unsigned long long)(0xFFFFFFFFu - (uint32_t)off))
@@ -593,6 +597,8 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
         }
     }
 
+    if (mode == kModeSearch && !small)
+        wb_flush(wbuf, lane, &args.res->n_work, args.work, args.work_J, args.work_cap);
     if (mode == kModeSearch) {
         // counts and list per workgroup (the merge kernel sums and merges them)
         __shared__ unsigned long long s_cnt[2 * WAVES];
