@@ -398,8 +398,7 @@ void stride_digits(const mf_problem &p, uint64_t stride, uint32_t *out)
 
 // Workspace layout for one search launch set over n configurations.
 struct WsLayout {
-    size_t res, work, workJ, collect, lists, counts, cand, entJ, entF, parts, seg, segJ, segJc, segF, rec, candJ, candF,
-        total;
+    size_t res, work, workJ, collect, lists, counts, cand, entJ, entF, parts, seg, segJ, rec, wtop, total;
     uint32_t work_cap, collect_cap, seg_cap;
     int kp, grid, waves, n_parts, eval_top;
     bool small;   // fp32 path over at most kSmallRange configurations: fast kernel + finish kernel
@@ -443,9 +442,10 @@ WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k, uint32_t worklist
     // the exact selection runs in two levels over long ranges
     w.n_parts = n > kSelSingleMax ? kSelParts : 1;
     w.parts = o; o = align256(o + (w.n_parts > 1 ? (size_t)w.n_parts * sizeof(SelPart) : 0));
-    // small ranges: a certification segment per workgroup (its upper bounds,
-    // canonical J and flags), the canonical values of each workgroup's first
-    // eval_top list entries, and its record.  eval_top: at least 4 and k/2 + 1
+    // small ranges: a certification segment per workgroup (its entries and
+    // upper bounds), the record and the best top_k canonical keys of each
+    // workgroup.  Each workgroup evaluates canonically its first eval_top list
+    // entries and its segment.  eval_top: at least 4 and k/2 + 1
     // (the workgroups scan runs of consecutive configurations, so one of them
     // may hold several of the best), and enough that the evaluated entries of
     // all workgroups cover twice the top-k.  Too few evaluated entries only
@@ -454,14 +454,10 @@ WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k, uint32_t worklist
     w.seg_cap = w.small ? (uint32_t)(((uint64_t)w.work_cap + w.grid - 1) / w.grid) : 0;
     w.eval_top = std::min(w.kp, std::max(std::max(4, top_k / 2 + 1), (2 * top_k + w.grid - 1) / w.grid + 2));
     const size_t n_seg = (size_t)w.seg_cap * (w.small ? w.grid : 0);
-    const size_t n_cand = w.small ? (size_t)w.grid * w.eval_top : 0;
     w.seg = o; o = align256(o + n_seg * 8);
     w.segJ = o; o = align256(o + n_seg * 4);
-    w.segJc = o; o = align256(o + n_seg * 8);
-    w.segF = o; o = align256(o + n_seg * 4);
-    w.rec = o; o = align256(o + (w.small ? (size_t)w.grid * 32 : 0));
-    w.candJ = o; o = align256(o + n_cand * 8);
-    w.candF = o; o = align256(o + n_cand * 4);
+    w.rec = o; o = align256(o + (w.small ? (size_t)w.grid * 64 : 0));
+    w.wtop = o; o = align256(o + (w.small ? (size_t)w.grid * top_k * sizeof(K128) : 0));
     w.total = o;
     return w;
 }
@@ -662,12 +658,10 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
         fa.seg_cap = w.seg_cap;
         fa.seg = reinterpret_cast<unsigned long long *>(ws + w.seg);
         fa.seg_J = reinterpret_cast<float *>(ws + w.segJ);
-        fa.seg_Jc = reinterpret_cast<double *>(ws + w.segJc);
-        fa.seg_F = reinterpret_cast<uint32_t *>(ws + w.segF);
         fa.wg_rec = reinterpret_cast<unsigned long long *>(ws + w.rec);
         fa.eval_top = w.eval_top;
-        fa.cand_J = reinterpret_cast<double *>(ws + w.candJ);
-        fa.cand_F = reinterpret_cast<uint32_t *>(ws + w.candF);
+        fa.wg_k = args->top_k;
+        fa.wg_top = reinterpret_cast<K128 *>(ws + w.wtop);
         fa.wstride = p->wstride;
         fa.features = p->d_features;
         fa.agg_cols = p->d_agg_cols;
@@ -680,24 +674,13 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
         fin.seq = p->call_seq.fetch_add(1) + 1;
         if (fin.res_host) fin.res_host->done_seq = 0;
         fin.omega = args->d_omega;
-        fin.lo = lo;
         fin.top_k = args->top_k;
-        fin.kp = w.kp;
-        fin.eval_top = w.eval_top;
         fin.n_wg = w.grid;
         fin.seg_cap = w.seg_cap;
         fin.work_cap = w.work_cap;
-        fin.work_out = work;
-        fin.work_J_out = workJ;
-        fin.wg_lists = lists;
         fin.wg_counts = counts;
         fin.wg_rec = fa.wg_rec;
-        fin.seg = fa.seg;
-        fin.seg_J = fa.seg_J;
-        fin.seg_Jc = fa.seg_Jc;
-        fin.seg_F = fa.seg_F;
-        fin.cand_J = fa.cand_J;
-        fin.cand_F = fa.cand_F;
+        fin.wg_top = fa.wg_top;
         MF_HIP2(launch_finish_small(fin, p->fc, s));
         if (fin.res_host) {
             // the finish kernel writes the result into pinned host memory,
@@ -710,6 +693,18 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
             MF_HIP2(hipStreamSynchronize(s));
         }
         if (!(h.status & kStatWorkOverflow)) ms = (float)((double)h.fast_ticks / p->wall_khz);
+        if (!(h.status & (kStatWorkOverflow | kStatSelfCheck | kStatVerified))) {
+            // the fallback reads the certification list in one piece
+            GatherArgs ga{};
+            ga.n_wg = w.grid;
+            ga.seg_cap = w.seg_cap;
+            ga.wg_rec = fa.wg_rec;
+            ga.seg = fa.seg;
+            ga.seg_J = fa.seg_J;
+            ga.work_out = work;
+            ga.work_J_out = workJ;
+            MF_HIP2(launch_gather_small(ga, s));
+        }
         fa.small = 0;
         fa.ep_bytes = 0;
     } else {

@@ -426,6 +426,13 @@ __device__ __forceinline__ unsigned long long wave_min64(unsigned long long x)
     return x;
 }
 
+__device__ __forceinline__ unsigned long long wave_or64(unsigned long long x)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) x |= shfl_xor64(x, m);
+    return x;
+}
+
 // The last store of a finish kernel to the host copy: the call's sequence
 // number, after a system-scope fence.
 __device__ __forceinline__ void publish_done(const FinishArgs &f)
@@ -434,110 +441,88 @@ __device__ __forceinline__ void publish_done(const FinishArgs &f)
     *reinterpret_cast<volatile unsigned long long *>(&f.res_host->done_seq) = f.seq;
 }
 
+// STAGED: the workgroups' keys are copied to LDS first (when they fit).
+template <bool STAGED>
 __global__ void __launch_bounds__(kFinWaves * 64) finish_small_kernel(const FinishArgs f, const FastConst fc)
 {
-    extern __shared__ uint32_t woff[];   // [n_wg + 1] exclusive prefix of the segment lengths
-    __shared__ unsigned long long s_red[6][kFinWaves];
-    __shared__ unsigned int s_wsum[kFinWaves];
-    __shared__ unsigned long long s_feas;
+    extern __shared__ K128 lkeys[];   // [n_wg][k] the workgroups' best canonical keys, sorted
+    const K128 *ckeys = STAGED ? lkeys : f.wg_top;
+    __shared__ unsigned long long s_red[8][kFinWaves];
     __shared__ K128 klst[kFinWaves * 64];
     __shared__ K128 s_floor;
     constexpr int W = kFinWaves;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int k = f.top_k, T = f.eval_top, n_wg = f.n_wg;
+    const int k = f.top_k, n_wg = f.n_wg;
     DevResult *R = f.res;
-    if (tid == 0) s_feas = 0;
 
-    // ---- the candidate keys (each workgroup's first T list entries with
-    // their canonical J) are loaded first, all at once, so that their round
-    // trip overlaps the records' below; staged in LDS after the prefix
-    const uint32_t n_cand = (uint32_t)n_wg * (uint32_t)T;
-    K128 *ckeys = reinterpret_cast<K128 *>(woff + ((n_wg + 4) & ~3));   // [n_cand]
-    constexpr int kCpt = 4;   // candidates per thread per pass
-    for (uint32_t base = 0; base < n_cand; base += kCpt * blockDim.x) {
-        uint32_t cf[kCpt];
-        unsigned long long ck[kCpt];
-        double cj[kCpt];
+    // ---- one round trip: every workgroup's keys (all loads in flight
+    // together, then staged in LDS) and its records
+    const uint32_t n_cand = (uint32_t)n_wg * (uint32_t)k;
+    constexpr int kCpt = 8;   // keys per thread per pass
+    for (uint32_t base = 0; STAGED && base < n_cand; base += kCpt * blockDim.x) {
+        K128 v[kCpt];
 #pragma unroll
         for (int q = 0; q < kCpt; q++) {
             const uint32_t t = base + q * blockDim.x + tid;
-            cf[q] = 0;
-            ck[q] = 0;
-            cj[q] = 0.0;
-            if (t < n_cand) {
-                const uint32_t g = t / T, j = t - g * T;
-                cf[q] = f.cand_F[t];
-                ck[q] = f.wg_lists[(uint64_t)g * f.kp + j];
-                cj[q] = f.cand_J[t];
-            }
+            v[q] = t < n_cand ? f.wg_top[t] : K128{0ull, 0ull};
         }
 #pragma unroll
         for (int q = 0; q < kCpt; q++) {
             const uint32_t t = base + q * blockDim.x + tid;
-            if (t < n_cand) {
-                const uint32_t off = 0xFFFFFFFFu - (uint32_t)(ck[q] & 0xFFFFFFFFull);
-                ckeys[t] = (cf[q] & 4u) ? K128{ord_f64(cj[q]), ~(f.lo + off)} : K128{0, 0};
-            }
+            if (t < n_cand) lkeys[t] = v[q];
         }
     }
-
-    // ---- counts, wall-clock span, status bits and the largest unevaluated
-    // upper bound over the workgroups; exclusive prefix of the segment lengths
-    unsigned long long nv = 0, nf = 0, t0 = ~0ull, t1 = 0, ovf = 0, st = 0, rest = 0;
-    uint32_t len = 0;
+    // counts, certification entries (offered, kept, found feasible), the
+    // wall-clock span, status bits and the largest unevaluated upper bound
+    unsigned long long nv = 0, nf = 0, nw = 0, ovf = 0, nfc = 0, t0 = ~0ull, t1 = 0, st = 0, rest = 0;
     if (tid < n_wg) {
-        const unsigned long long *r = f.wg_rec + 4 * (uint64_t)tid;
-        const unsigned long long nw = r[0];
-        ovf = nw > f.seg_cap ? 1u : 0u;
-        len = (uint32_t)(nw > f.seg_cap ? f.seg_cap : nw);
+        const unsigned long long *r = f.wg_rec + 8 * (uint64_t)tid;
+        const unsigned long long off = r[0];
+        ovf = off > f.seg_cap ? 1u : 0u;
+        nw = off > f.seg_cap ? f.seg_cap : off;
         t0 = r[1];
         t1 = r[2];
         st = r[3] >> 32;
         rest = r[3] & 0xFFFFFFFFull;
+        nfc = r[4];
         nv = f.wg_counts[2 * (uint64_t)tid];
         nf = f.wg_counts[2 * (uint64_t)tid + 1];
     }
     nv = wave_sum64(nv);
     nf = wave_sum64(nf);
+    nw = wave_sum64(nw);
     ovf = wave_sum64(ovf);
+    nfc = wave_sum64(nfc);
     t0 = wave_min64(t0);
     t1 = wave_max64(t1);
     rest = wave_max64(rest);
-    st = wave_max64(st);   // status bits: only kStatSelfCheck is set here
-    uint32_t incl = len;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t t = __shfl_up(incl, d);
-        if (lane >= d) incl += t;
-    }
-    if (lane == 63) {
-        s_wsum[wv] = incl;
+    st = wave_or64(st);
+    if (lane == 0) {
         s_red[0][wv] = nv;
         s_red[1][wv] = nf;
-        s_red[2][wv] = ovf;
-        s_red[3][wv] = t0;
-        s_red[4][wv] = t1;
-        s_red[5][wv] = (rest << 32) | st;
+        s_red[2][wv] = nw;
+        s_red[3][wv] = ovf;
+        s_red[4][wv] = nfc;
+        s_red[5][wv] = t0;
+        s_red[6][wv] = t1;
+        s_red[7][wv] = (rest << 32) | st;
     }
     __syncthreads();
-    uint32_t base = 0;
-    for (int w = 0; w < wv; w++) base += s_wsum[w];
-    if (tid <= n_wg) woff[tid] = base + incl - len;   // tid == n_wg: the total (len 0)
-    unsigned long long tnv = 0, tnf = 0, tovf = 0, tt0 = ~0ull, tt1 = 0, trest = 0, tst = 0;
+    unsigned long long tnv = 0, tnf = 0, tnw = 0, tovf = 0, tnfc = 0, tt0 = ~0ull, tt1 = 0, trest = 0, tst = 0;
     for (int w = 0; w < W; w++) {
         tnv += s_red[0][w];
         tnf += s_red[1][w];
-        tovf += s_red[2][w];
-        tt0 = s_red[3][w] < tt0 ? s_red[3][w] : tt0;
-        tt1 = s_red[4][w] > tt1 ? s_red[4][w] : tt1;
-        const unsigned long long rs = s_red[5][w] >> 32;
+        tnw += s_red[2][w];
+        tovf += s_red[3][w];
+        tnfc += s_red[4][w];
+        tt0 = s_red[5][w] < tt0 ? s_red[5][w] : tt0;
+        tt1 = s_red[6][w] > tt1 ? s_red[6][w] : tt1;
+        const unsigned long long rs = s_red[7][w] >> 32;
         trest = rs > trest ? rs : trest;
-        tst |= s_red[5][w] & 0xFFFFFFFFull;
+        tst |= s_red[7][w] & 0xFFFFFFFFull;
     }
-    __syncthreads();
-    const uint32_t n_work = woff[n_wg];
-    if (tovf || n_work > f.work_cap) {
+    if (tovf || tnw > f.work_cap) {
         if (tid == 0) {
             R->status = kStatWorkOverflow;
             R->n_work = (unsigned long long)f.work_cap + 1;
@@ -549,13 +534,13 @@ __global__ void __launch_bounds__(kFinWaves * 64) finish_small_kernel(const Fini
         }
         return;
     }
-    // ---- a lower bound of the k-th largest candidate key: the k-th largest
-    // of 64 group maxima (64 distinct candidates), so that the offers below
-    // skip every key under it
+
+    // ---- a lower bound of the k-th largest key: the k-th largest of up to
+    // 64 maxima of the workgroups' first (largest) keys, distinct candidates
     if (wv == 0) {
-        K128 m = {0, 0};
-        for (uint32_t t = lane; t < n_cand; t += 64) {
-            const K128 x = ckeys[t];
+        K128 m = {0ull, 0ull};
+        for (int g = lane; g < n_wg; g += 64) {
+            const K128 x = ckeys[(uint32_t)g * (uint32_t)k];
             if (gt128(x, m)) m = x;
         }
         const K128 srt = sort128_desc(m, lane);
@@ -565,42 +550,18 @@ __global__ void __launch_bounds__(kFinWaves * 64) finish_small_kernel(const Fini
     __syncthreads();
     const K128 floor_key = s_floor;
 
-    // ---- the certification entries, each read once: copied out as the
-    // gathered certification list (for a fallback pass on the host's side)
-    // and offered by their canonical J; then the staged candidates
-    K128 slot = {0, 0}, thr = {0, 0};
-    unsigned long long my_feas = 0;
-    for (uint32_t b0 = (uint32_t)wv * 64; b0 < n_work; b0 += W * 64) {
-        const uint32_t e = b0 + lane;
-        K128 mine = {0, 0};
-        if (e < n_work) {
-            const int g = seg_of(woff, n_wg, e);
-            const uint64_t at = (uint64_t)g * f.seg_cap + (e - woff[g]);
-            const unsigned long long key = f.seg[at];
-            const float fJ = f.seg_J[at];
-            const uint32_t fl = f.seg_F[at];
-            const double cJ = f.seg_Jc[at];
-            f.work_out[e] = key;
-            f.work_J_out[e] = fJ;
-            if (fl & 4u) {
-                my_feas++;
-                mine = {ord_f64(cJ), ~(f.lo + (uint32_t)(key & 0xFFFFFFFFull))};
-            }
-        }
-        list128_offer_many(slot, mine, lane, k, thr);
-    }
+    // ---- the exact top-k: the keys at or above the bound, offered per wave,
+    // the waves' lists merged in a tree
+    K128 slot = {0ull, 0ull}, thr = {0ull, 0ull};
     for (uint32_t b0 = (uint32_t)wv * 64; b0 < n_cand; b0 += W * 64) {
         const uint32_t t = b0 + lane;
-        K128 mine = {0, 0};
+        K128 mine = {0ull, 0ull};
         if (t < n_cand) {
             const K128 x = ckeys[t];
             if (!gt128(floor_key, x)) mine = x;
         }
         list128_offer_many(slot, mine, lane, k, thr);
     }
-    my_feas = wave_sum64(my_feas);
-    if (lane == 0 && my_feas) atomicAdd(&s_feas, my_feas);
-    // the waves' lists merge in a tree
     klst[wv * 64 + lane] = key_if(lane < k, slot);
 #pragma unroll
     for (int h = W / 2; h >= 1; h >>= 1) {
@@ -641,9 +602,9 @@ __global__ void __launch_bounds__(kFinWaves * 64) finish_small_kernel(const Fini
             if (verified) stat |= kStatVerified;
             R->n_vram = tnv;
             R->n_feas_sure = tnf;
-            R->n_work = n_work;
+            R->n_work = tnw;
             R->n_collect = 0;
-            R->n_feas_cert = s_feas;
+            R->n_feas_cert = tnfc;
             R->n_cand = 0;
             R->status = stat;
             R->n_top = n_top;
@@ -654,12 +615,12 @@ __global__ void __launch_bounds__(kFinWaves * 64) finish_small_kernel(const Fini
             R->ck_cand = Ck;
             R->fast_ticks = tt1 > tt0 ? tt1 - tt0 : 0ull;
             if (DevResult *H = f.res_host) {
-                // the host reads this copy after synchronising the stream
+                // the host reads this copy after the sequence number appears
                 H->n_vram = tnv;
                 H->n_feas_sure = tnf;
-                H->n_work = n_work;
+                H->n_work = tnw;
                 H->n_collect = 0;
-                H->n_feas_cert = s_feas;
+                H->n_feas_cert = tnfc;
                 H->n_cand = 0;
                 H->status = stat;
                 H->n_top = n_top;
@@ -679,21 +640,53 @@ __global__ void __launch_bounds__(kFinWaves * 64) finish_small_kernel(const Fini
     }
 }
 
-size_t finish_small_lds_bytes(const FinishArgs &f)
-{
-    return (size_t)((f.n_wg + 4) & ~3) * 4 + (size_t)f.n_wg * f.eval_top * sizeof(K128);
-}
-
 hipError_t launch_finish_small(const FinishArgs &f, const FastConst &fc, hipStream_t s)
 {
-    if (f.kp < 1 || f.kp > 64 || f.n_wg < 1 || f.n_wg >= kFinWaves * 64 || f.top_k < 1 || f.top_k > 64 ||
-        f.eval_top < 1 || f.eval_top > f.kp)
-        return hipErrorInvalidValue;
-    const size_t lds = finish_small_lds_bytes(f);
-    if (lds > 163840) return hipErrorInvalidValue;
-    hipError_t e = ensure_dyn_lds((const void *)finish_small_kernel, lds);
+    if (f.n_wg < 1 || f.n_wg >= kFinWaves * 64 || f.top_k < 1 || f.top_k > 64) return hipErrorInvalidValue;
+    // the keys are staged in LDS up to 128 KiB (8192 keys), read from global
+    // memory beyond
+    const size_t lds = (size_t)f.n_wg * f.top_k * sizeof(K128);
+    if (lds <= 131072) {
+        hipError_t e = ensure_dyn_lds((const void *)finish_small_kernel<true>, lds);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(finish_small_kernel<true>, dim3(1), dim3(kFinWaves * 64), lds, s, f, fc);
+    } else {
+        hipLaunchKernelGGL(finish_small_kernel<false>, dim3(1), dim3(kFinWaves * 64), 0, s, f, fc);
+    }
+    return hipGetLastError();
+}
+
+// The fallback's certification list: segment g's first min(offered, seg_cap)
+// entries at the exclusive prefix of those lengths.  Dynamic LDS: [n_wg + 1].
+__global__ void __launch_bounds__(1024) gather_small_kernel(const GatherArgs a)
+{
+    extern __shared__ uint32_t woff[];
+    if (threadIdx.x == 0) {
+        uint32_t o = 0;
+        for (int g = 0; g < a.n_wg; g++) {
+            woff[g] = o;
+            const unsigned long long off = a.wg_rec[8 * (uint64_t)g];
+            o += (uint32_t)(off > a.seg_cap ? a.seg_cap : off);
+        }
+        woff[a.n_wg] = o;
+    }
+    __syncthreads();
+    const uint32_t n = woff[a.n_wg];
+    for (uint32_t e = threadIdx.x; e < n; e += blockDim.x) {
+        const int g = seg_of(woff, a.n_wg, e);
+        const uint64_t at = (uint64_t)g * a.seg_cap + (e - woff[g]);
+        a.work_out[e] = a.seg[at];
+        a.work_J_out[e] = a.seg_J[at];
+    }
+}
+
+hipError_t launch_gather_small(const GatherArgs &g, hipStream_t s)
+{
+    if (g.n_wg < 1 || g.n_wg >= 65536) return hipErrorInvalidValue;
+    const size_t lds = ((size_t)g.n_wg + 1) * 4;
+    hipError_t e = ensure_dyn_lds((const void *)gather_small_kernel, lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(finish_small_kernel, dim3(1), dim3(kFinWaves * 64), lds, s, f, fc);
+    hipLaunchKernelGGL(gather_small_kernel, dim3(1), dim3(1024), lds, s, g);
     return hipGetLastError();
 }
 

@@ -139,21 +139,19 @@ struct FastArgs {
     // Small ranges (search mode, completed by the finish kernel): no global
     // counter.  Certification entries go to a segment of seg_cap entries per
     // workgroup; after its scan each workgroup evaluates canonically its first
-    // eval_top list entries (cand_J / cand_F [grid][eval_top]) and its segment
-    // (seg_Jc / seg_F), and writes wg_rec[4 g] = {entries offered (may exceed
-    // seg_cap), start and end wall-clock ticks, status bits << 32 | the
-    // order-preserving bits of the upper bound U of list entry eval_top (0:
-    // none)}.
+    // eval_top list entries and its segment, and writes its wg_k best
+    // canonical keys (wg_top [grid][wg_k], sorted, zeros past the last) and
+    // wg_rec[8 g] = {entries offered (may exceed seg_cap), start and end
+    // wall-clock ticks, status bits << 32 | the order-preserving bits of the
+    // upper bound U of list entry eval_top (0: none), segment entries found
+    // feasible, -, -, -}.
     int small;
     uint32_t seg_cap;
     unsigned long long *seg;
     float *seg_J;
-    double *seg_Jc;
-    uint32_t *seg_F;
     unsigned long long *wg_rec;
-    int eval_top;
-    double *cand_J;
-    uint32_t *cand_F;
+    int eval_top, wg_k;
+    K128 *wg_top;
     int64_t wstride;
     const float *features;      // [sumK][n_local]
     const int32_t *agg_cols;    // [A] (original slot order)
@@ -262,10 +260,9 @@ struct CanonArgs {
 };
 
 // The rest of a small-range search after the fast kernel, in one workgroup:
-// sum the workgroups' counts, gather the certification segments into one
-// list (for a fallback pass), select the exact top-k among the canonically
-// evaluated entries (each workgroup's first eval_top list entries and every
-// certification entry) and fill the result block.  The top-k is exact when
+// sum the workgroups' counts and records, select the exact top-k among the
+// workgroups' best canonical keys (drawn from each workgroup's first eval_top
+// list entries and its certification segment) and fill the result block.  The top-k is exact when
 // its k-th canonical J exceeds every workgroup's first unevaluated upper
 // bound; otherwise the status asks for the fallback (collect) pass.
 struct FinishArgs {
@@ -273,20 +270,22 @@ struct FinishArgs {
     DevResult *res_host;            // optional copy in pinned host memory (counts, status, top-k)
     unsigned long long seq;         // written to res_host->done_seq after everything else
     const float *omega;
-    uint64_t lo;
-    int top_k, kp, eval_top, n_wg;
+    int top_k, n_wg;
     uint32_t seg_cap, work_cap;
-    unsigned long long *work_out;   // gathered certification list [work_cap]
-    float *work_J_out;
-    const unsigned long long *wg_lists;   // [n_wg][kp]
     const unsigned long long *wg_counts;  // [n_wg][2]
-    const unsigned long long *wg_rec;     // [n_wg][4]
-    const unsigned long long *seg;
+    const unsigned long long *wg_rec;     // [n_wg][8]
+    const K128 *wg_top;                   // [n_wg][top_k]
+};
+
+// Small ranges, fallback only: the workgroups' certification segments
+// gathered into one list for the collect pass.
+struct GatherArgs {
+    int n_wg;
+    uint32_t seg_cap;
+    const unsigned long long *wg_rec, *seg;
     const float *seg_J;
-    const double *seg_Jc;
-    const uint32_t *seg_F;
-    const double *cand_J;
-    const uint32_t *cand_F;
+    unsigned long long *work_out;
+    float *work_J_out;
 };
 
 // One workgroup's share of the exact top-k selection over a long entry list.
@@ -439,8 +438,8 @@ hipError_t launch_canonical(const CanonArgs &a, int n_entries_max, bool search_m
 hipError_t launch_kth_candidate(const unsigned long long *cand_keys, const double *ent_J, const uint32_t *ent_flags,
                                 int kp, int k, DevResult *res, hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, hipStream_t s);
+hipError_t launch_gather_small(const GatherArgs &g, hipStream_t s);
 hipError_t launch_finish_small(const FinishArgs &f, const FastConst &fc, hipStream_t s);
-size_t finish_small_lds_bytes(const FinishArgs &f);
 size_t fast_small_epilogue_bytes(int n_models);
 constexpr uint64_t kSmallRange = 1ull << 20;   // fp32 ranges up to this size finish in one workgroup
 size_t fixed_lds_bytes(int sumK, bool eq3);

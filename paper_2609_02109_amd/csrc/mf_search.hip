@@ -35,7 +35,7 @@ constexpr int kCertChunk = 64;
 size_t fast_small_epilogue_bytes(int n_models)
 {
     return 64 * 8 + 16 + (size_t)kCertChunk * n_models * 16 + (size_t)kCertChunk * kMaxN * 4 +
-           (size_t)kSearchWavesWide * 64 * 8;
+           (size_t)kSearchWavesWide * 64 * 8 + (size_t)kCertChunk * sizeof(K128);
 }
 
 // One model's surrogate (Eq. 6) on canonical semantics, by one wave with no
@@ -140,6 +140,8 @@ __device__ inline void small_certify(const FastArgs &args, const FastConst &fc, 
     int *erow = reinterpret_cast<int *>(eout + (size_t)kCertChunk * N * 2);                          // [chunk][kMaxN]
     static_assert(WAVES <= kSearchWavesWide, "one 64-double forward buffer per wave");
     double *xb = reinterpret_cast<double *>(erow + kCertChunk * kMaxN) + wv * 64;
+    // the chunk's canonical keys (J, joint index; 0 when infeasible)
+    K128 *eck = reinterpret_cast<K128 *>(reinterpret_cast<double *>(erow + kCertChunk * kMaxN) + kSearchWavesWide * 64);
     if (wv == 0) {
         ekey[lane] = lane < T ? listkey : 0ull;
         // a bound on the upper bound U of every sure-feasible configuration
@@ -150,9 +152,12 @@ __device__ inline void small_certify(const FastArgs &args, const FastConst &fc, 
         if (lane == 0) {
             estat[0] = 0;
             estat[1] = (uint32_t)(rest >> 32);
+            estat[2] = 0;   // segment entries found feasible
         }
     }
     __syncthreads();
+    // wave 0: the workgroup's best wg_k canonical keys so far
+    K128 tslot = {0ull, 0ull}, tthr = {0ull, 0ull};
     const int n_list = __popcll(__ballot(lane < T && ekey[lane] != 0ull));
     const int n_seg = (int)(n_offered < args.seg_cap ? n_offered : args.seg_cap);
     const int n_ent = n_list + n_seg;
@@ -228,19 +233,16 @@ __device__ inline void small_certify(const FastArgs &args, const FastConst &fc, 
             for (int j = 0; j < N; j++) va = va + feat[erow[t * kMaxN + j] * L + vcol];
             const bool vram_ok = (double)va <= (double)fc.vram_cap;
             bool sla_ok = true;
-            uint32_t fl = 0;
             double J = 0.0;
             for (int i = 0; i < N; i++) {
                 const double lat = eout[2 * (t * N + i)], thr = eout[2 * (t * N + i) + 1];
-                if (!(lat <= (double)par[128 + i])) { sla_ok = false; fl |= 1u << (8 + i); }
+                if (!(lat <= (double)par[128 + i])) sla_ok = false;
                 if constexpr (OBJ) {
                     double qv, P, pen;
                     bool do_P, do_pen;
                     if (!canon_eq3(args.obj, erow[t * kMaxN + i], thr, par[64 + i], pPrev[i], qv, P, do_P, pen,
-                                   do_pen)) {
+                                   do_pen))
                         sla_ok = false;
-                        fl |= 1u << (8 + i);
-                    }
                     J = fma((double)par[32 + i], qv, J);
                     if (do_P) J = J - P;
                     if (do_pen) J = J - pen;
@@ -249,31 +251,32 @@ __device__ inline void small_certify(const FastArgs &args, const FastConst &fc, 
                 }
             }
             const bool feas = vram_ok && sla_ok;
-            fl |= (vram_ok ? 1u : 0u) | (sla_ok ? 2u : 0u) | (feas ? 4u : 0u);
+            eck[t] = feas ? K128{ord_f64(J), ~(args.lo + (uint64_t)off)} : K128{0ull, 0ull};
             if (e < n_list) {
                 // a sure-feasible fast decision must be canonically feasible,
                 // and the key's U must bound the canonical J
                 const double U = (double)unord_f32((uint32_t)(ekey[e] >> 32));
                 if (!feas || !(U - J >= 0.0)) atomicOr(&estat[0], kStatSelfCheck);
-                args.cand_J[g * T + e] = feas ? J : -INFINITY;
-                args.cand_F[g * T + e] = fl;
             } else {
-                const uint64_t at = g * args.seg_cap + (e - n_list);
-                args.seg_Jc[at] = J;
-                args.seg_F[at] = fl;
+                if (feas) atomicAdd(&estat[2], 1u);
                 if (args.mask)
                     args.mask[off] = (uint8_t)((vram_ok ? 1u : 0u) | (sla_ok ? 2u : 0u) | (feas ? 4u : 0u) | 8u);
             }
         }
         __syncthreads();
+        // wave 0 takes the chunk's keys (kCertChunk = 64: one per lane); the
+        // next chunk writes eck only after two more barriers
+        static_assert(kCertChunk == 64, "one key per lane");
+        if (wv == 0) list128_offer_many(tslot, lane < nc ? eck[lane] : K128{0ull, 0ull}, lane, args.wg_k, tthr);
     }
-    for (int j = n_list + (int)threadIdx.x; j < T; j += WAVES * 64) args.cand_F[g * T + j] = 0;
+    if (wv == 0 && lane < args.wg_k) args.wg_top[g * (uint64_t)args.wg_k + lane] = tslot;
     if (threadIdx.x == 0) {
-        unsigned long long *r = args.wg_rec + 4 * g;
+        unsigned long long *r = args.wg_rec + 8 * g;
         r[0] = n_offered;
         r[1] = t_start;
         r[2] = (unsigned long long)wall_clock64();
         r[3] = ((unsigned long long)estat[0] << 32) | estat[1];
+        r[4] = estat[2];
     }
 }
 
