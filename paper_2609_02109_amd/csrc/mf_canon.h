@@ -100,58 +100,6 @@ __device__ inline void canon_model(const float *w, int nin, int H1, int H2, cons
     thr = __shfl(y, 1);
 }
 
-// One model's surrogate (Eq. 6) on canonical semantics for one configuration
-// by one wave, with no barriers (H <= 64): lane u computes hidden unit u from
-// its own fp64 weight row; each unit's chain takes its inputs in ascending
-// order, broadcast from the lanes that hold them (input k in lane k, nin <=
-// 64).  w: the model's packed fp64 weights W1[H][nin], b1[H], W2[H][H],
-// b2[H], W3[2][H], b3[2].  The rows are read eight weights at a time ahead of
-// their fmas.  Every lane returns (lat, thr).
-template <int H>
-__device__ inline void canon_forward_units(const double *w, int nin, double z, int lane, bool sigmoid, double &lat,
-                                           double &thr)
-{
-    const double *W1 = w, *b1 = W1 + H * nin, *W2 = b1 + H, *b2 = W2 + H * H, *W3 = b2 + H, *b3 = W3 + 2 * H;
-    const int u = lane < H ? lane : H - 1;   // lanes past H repeat the last unit and are ignored
-    double c = b1[u];
-    const double *r1 = W1 + u * nin;
-    int k = 0;
-    for (; k + 8 <= nin; k += 8) {
-        double wv[8];
-#pragma unroll
-        for (int j = 0; j < 8; j++) wv[j] = r1[k + j];
-#pragma unroll
-        for (int j = 0; j < 8; j++) c = fma(wv[j], readlane_f64(z, k + j), c);
-    }
-    for (; k < nin; k++) c = fma(r1[k], readlane_f64(z, k), c);
-    const double h1 = c > 0.0 ? c : 0.0;
-    c = b2[u];
-    const double *r2 = W2 + u * H;
-#pragma unroll
-    for (int u0 = 0; u0 < H; u0 += 8) {
-        double wv[8];
-#pragma unroll
-        for (int j = 0; j < 8; j++) wv[j] = r2[u0 + j];
-#pragma unroll
-        for (int j = 0; j < 8; j++) c = fma(wv[j], readlane_f64(h1, u0 + j), c);
-    }
-    const double h2 = c > 0.0 ? c : 0.0;
-    const int o = lane & 1;
-    c = b3[o];
-    const double *r3 = W3 + o * H;
-#pragma unroll
-    for (int v0 = 0; v0 < H; v0 += 8) {
-        double wv[8];
-#pragma unroll
-        for (int j = 0; j < 8; j++) wv[j] = r3[v0 + j];
-#pragma unroll
-        for (int j = 0; j < 8; j++) c = fma(wv[j], readlane_f64(h2, v0 + j), c);
-    }
-    const double y = sigmoid ? canon_sigmoid(c) : c;
-    lat = readlane_f64(y, 0);
-    thr = readlane_f64(y, 1);
-}
-
 // The canonical term of model i under the full utility (Section II, Eq. 3)
 // for option row `row` and throughput thr: q = Q f with f = (thr - fmin) /
 // (fmax - fmin); reload (when the variant changed; *do_P) and soft-SLA

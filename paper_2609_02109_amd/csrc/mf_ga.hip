@@ -25,6 +25,18 @@ struct Philox4 {
     uint64_t w[4];
 };
 
+// The 128-bit product a b: its high and low 64 bits from four 32 x 32 -> 64
+// multiply-adds (no partial sum overflows 64 bits).
+__device__ __forceinline__ void mulhilo64(uint64_t a, uint64_t b, uint64_t &hi, uint64_t &lo)
+{
+    const uint64_t a0 = (uint32_t)a, a1 = a >> 32, b0 = (uint32_t)b, b1 = b >> 32;
+    const uint64_t p00 = a0 * b0;
+    const uint64_t t1 = a0 * b1 + (p00 >> 32);
+    const uint64_t t2 = a1 * b0 + (t1 & 0xFFFFFFFFull);
+    hi = a1 * b1 + (t1 >> 32) + (t2 >> 32);
+    lo = (t2 << 32) | (p00 & 0xFFFFFFFFull);
+}
+
 __device__ __forceinline__ Philox4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3, uint64_t k0,
                                                  uint64_t k1)
 {
@@ -33,8 +45,9 @@ __device__ __forceinline__ Philox4 philox4x64_10(uint64_t c0, uint64_t c1, uint6
 #pragma unroll
     for (int r = 0; r < 10; r++) {
         if (r) { k0 += W0; k1 += W1; }
-        const uint64_t h0 = __umul64hi(M0, c0), l0 = M0 * c0;
-        const uint64_t h1 = __umul64hi(M1, c2), l1 = M1 * c2;
+        uint64_t h0, l0, h1, l1;
+        mulhilo64(M0, c0, h0, l0);
+        mulhilo64(M1, c2, h1, l1);
         const uint64_t y0 = h1 ^ c1 ^ k0, y2 = h0 ^ c3 ^ k1;
         c0 = y0; c1 = l1; c2 = y2; c3 = l0;
     }
@@ -641,22 +654,22 @@ __global__ void __launch_bounds__(kOpThreads) ga_ops_kernel(const GAConst c, uin
     const int j = 1 + 2 * (q0 + ql) + t;
     if (j >= P) return;
     // child t starts as parent t; uniform crossover gives it the other
-    // parent's gene wherever the pair's swap draw falls below p_swap
-    int32_t ch[kMaxN];
+    // parent's gene wherever the pair's swap draw falls below p_swap; gene i
+    // mutates with words 2i (mutate?) and 2i + 1 (new value).  Gene by gene
+    // in model order, with a compile-time model index (no per-lane array).
     const bool cx = ga_uni(pw[ob.cx() * 4]) < (double)p_cx;
-    for (int i = 0; i < N; i++) {
-        const bool sw = cx && ga_uni(pw[ob.swap() * 4 + i]) < (double)p_swap;
-        ch[i] = pg[(sw ? 1 - t : t) * N + i];
-    }
-    // mutation: gene i reads words 2i (mutate?) and 2i + 1 (new value)
     const uint64_t *mw = pw + ob.mut(t) * 4;
-    for (int i = 0; i < N; i++)
-        if (ga_uni(mw[2 * i]) < (double)p_mut) ch[i] = (int32_t)ga_below(mw[2 * i + 1], (uint64_t)c.K[i]);
     float vs = 0.f;
     uint64_t idx = 0;
-    for (int i = 0; i < N; i++) {
-        vs = vs + c.features[(int64_t)(c.opt_off[i] + ch[i]) * c.L + c.vram_col];
-        idx = idx * (uint64_t)c.K[i] + (uint64_t)ch[i];
+#pragma unroll
+    for (int i = 0; i < kMaxN; i++) {
+        if (i < N) {
+            const bool sw = cx && ga_uni(pw[ob.swap() * 4 + i]) < (double)p_swap;
+            int32_t g = pg[(sw ? 1 - t : t) * N + i];
+            if (ga_uni(mw[2 * i]) < (double)p_mut) g = (int32_t)ga_below(mw[2 * i + 1], (uint64_t)c.K[i]);
+            vs = vs + c.features[(int64_t)(c.opt_off[i] + g) * c.L + c.vram_col];
+            idx = idx * (uint64_t)c.K[i] + (uint64_t)g;
+        }
     }
     if (!((double)vs <= (double)c.vram_cap)) idx = n_fl ? fl[ga_below(pw[ob.rep(t) * 4], n_fl)] : 0;
     ns[j] = idx;
