@@ -494,20 +494,19 @@ constexpr int kOpThreads = 256;                   // threads per operator workgr
 constexpr int kOpTeam = 4;                        // lanes per parent pair
 constexpr int kOpPairs = kOpThreads / kOpTeam;    // parent pairs per operator workgroup
 
-// The Philox blocks one parent pair consumes, in a fixed order: the selection
-// blocks (2k draws), the crossover block, the swap blocks (one word per
-// gene), the mutation blocks of child 1 + 2q and of child 2 + 2q (two words
-// per gene), the repair block of each child.
+// The Philox blocks of a parent pair kept in LDS, in a fixed order: the
+// selection blocks (2k draws), the crossover block, the swap blocks (one
+// word per gene), the mutation blocks of child 1 + 2q and of child 2 + 2q
+// (two words per gene).  A child's repair block is drawn where it is needed.
 struct OpBlocks {
     int nsel, nswap, nmut, total;
     __host__ __device__ OpBlocks(int tk, int N)
-        : nsel((2 * tk + 3) / 4), nswap((N + 3) / 4), nmut((N + 1) / 2), total(nsel + 1 + nswap + 2 * nmut + 2)
+        : nsel((2 * tk + 3) / 4), nswap((N + 3) / 4), nmut((N + 1) / 2), total(nsel + 1 + nswap + 2 * nmut)
     {
     }
     __host__ __device__ int cx() const { return nsel; }
     __host__ __device__ int swap() const { return nsel + 1; }
     __host__ __device__ int mut(int t) const { return nsel + 1 + nswap + t * nmut; }
-    __host__ __device__ int rep(int t) const { return nsel + 1 + nswap + 2 * nmut + t; }
 };
 
 // Dynamic LDS of the operator kernel: the pairs' Philox words, the parents'
@@ -523,10 +522,11 @@ inline size_t ops_lds_bytes(int tk, int N)
 // best ever are found by the first operator workgroup of a scenario, or, for
 // populations of at most four operator workgroups, by one more workgroup
 // beside them (there the elite's reduction would otherwise sit on the critical
-// path).  At g == gens the final population is copied out.  The pairs' Philox blocks are first computed by all threads
-// together (each block once, its four words used in order); then, in each
-// team of lanes, lane t runs tournament t and decodes parent t, and builds
-// child t (crossover, mutation, repair).
+// path).  At g == gens the final population is copied out.  The pairs'
+// Philox blocks are first computed by all threads together (each block once,
+// its four words used in order); then, in each team of lanes, lane t runs
+// tournament t and decodes parent t, and builds child t (crossover,
+// mutation, repair).
 __global__ void __launch_bounds__(kOpThreads) ga_ops_kernel(const GAConst c, uint64_t seed, int P, int gen, int gens,
                                                             int tk, float p_cx, float p_swap, float p_mut,
                                                             const uint32_t *fl, const unsigned long long *n_fl_ptr,
@@ -601,27 +601,34 @@ __global__ void __launch_bounds__(kOpThreads) ga_ops_kernel(const GAConst c, uin
     const uint64_t g1 = (uint64_t)gen + 1, sc = (uint64_t)s;
     const int q0 = pb * kOpPairs;
     const int np = P / 2 - q0 < kOpPairs ? P / 2 - q0 : kOpPairs;
-    // every Philox block of this workgroup's pairs
-    for (int jb = tid; jb < np * ob.total; jb += kOpThreads) {
-        const int ql = jb / ob.total, k = jb - ql * ob.total;
+    // the Philox blocks of this workgroup's pairs, each computed once by one
+    // thread: first the selection and crossover blocks, then the swap blocks
+    // of the pairs that cross over and the mutation blocks; a child's repair
+    // block only when it is needed (every draw is counter-addressed, so the
+    // values do not depend on which are computed)
+    const int nA = ob.nsel + 1, nB = ob.nswap + 2 * ob.nmut;
+    for (int jb = tid; jb < np * nA; jb += kOpThreads) {
+        const int ql = jb / nA, k = jb - ql * nA;
+        const Philox4 r = philox4x64_10((uint64_t)(q0 + ql), g1, sc, k < ob.cx() ? kPSel + k : kPCx, seed, 0);
+        uint64_t *w = words + ((int64_t)ql * ob.total + k) * 4;
+#pragma unroll
+        for (int x = 0; x < 4; x++) w[x] = r.w[x];
+    }
+    __syncthreads();
+    for (int jb = tid; jb < np * nB; jb += kOpThreads) {
+        const int ql = jb / nB, k = ob.swap() + (jb - ql * nB);
         const uint64_t q = (uint64_t)(q0 + ql);
         uint64_t item = q, purpose;
-        if (k < ob.cx()) {
-            purpose = kPSel + k;
-        } else if (k == ob.cx()) {
-            purpose = kPCx;
-        } else if (k < ob.mut(0)) {
+        if (k < ob.mut(0)) {
+            if (!(ga_uni(words[((int64_t)ql * ob.total + ob.cx()) * 4]) < (double)p_cx)) continue;
             purpose = kPSwap + (k - ob.swap());
-        } else if (k < ob.rep(0)) {
+        } else {
             const int t = (k - ob.mut(0)) / ob.nmut;
             item = 1 + 2 * q + t;
             purpose = kPMut + (k - ob.mut(t));
-        } else {
-            item = 1 + 2 * q + (k - ob.rep(0));
-            purpose = kPRep;
         }
         const Philox4 r = philox4x64_10(item, g1, sc, purpose, seed, 0);
-        uint64_t *w = words + (int64_t)jb * 4;
+        uint64_t *w = words + ((int64_t)ql * ob.total + k) * 4;
 #pragma unroll
         for (int x = 0; x < 4; x++) w[x] = r.w[x];
     }
@@ -671,7 +678,8 @@ __global__ void __launch_bounds__(kOpThreads) ga_ops_kernel(const GAConst c, uin
             idx = idx * (uint64_t)c.K[i] + (uint64_t)g;
         }
     }
-    if (!((double)vs <= (double)c.vram_cap)) idx = n_fl ? fl[ga_below(pw[ob.rep(t) * 4], n_fl)] : 0;
+    if (!((double)vs <= (double)c.vram_cap))
+        idx = n_fl ? fl[ga_below(philox4x64_10((uint64_t)j, g1, sc, kPRep, seed, 0).w[0], n_fl)] : 0;
     ns[j] = idx;
 }
 
