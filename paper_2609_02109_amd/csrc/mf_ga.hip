@@ -519,10 +519,10 @@ inline size_t ops_lds_bytes(int tk, int N)
 // Operators: a scenario's pairs are spread over ceil((P/2) / kOpPairs)
 // workgroups; tournaments read fitness and population from global memory.
 // The elite (slot 0 of the next generation, which no child writes) and the
-// best ever are found by the first operator workgroup of a scenario, or, for
-// populations of at most four operator workgroups, by one more workgroup
-// beside them (there the elite's reduction would otherwise sit on the critical
-// path).  At g == gens the final population is copied out.  The pairs'
+// best ever are found by one more workgroup beside a scenario's operator
+// workgroups (elite_wg = 1), off their critical path; with elite_wg = 0 the
+// first operator workgroup finds them.  At g == gens the final population is
+// copied out.  The pairs'
 // Philox blocks are first computed by all threads together (each block once,
 // its four words used in order); then, in each team of lanes, lane t runs
 // tournament t and decodes parent t, and builds child t (crossover,
@@ -788,7 +788,7 @@ hipError_t launch_ga_ops(const GAConst &c, uint64_t seed, int S, int P, int gen,
     const size_t lds = ops_lds_bytes(tk, c.N);
     const hipError_t e = ensure_dyn_lds((const void *)ga_ops_kernel, lds);
     if (e != hipSuccess) return e;
-    const int elite_wg = wgs <= 4 ? 1 : 0;
+    const int elite_wg = 1;   // the elite's reduction in a workgroup of its own
     hipLaunchKernelGGL(ga_ops_kernel, dim3(S * (wgs + elite_wg)), dim3(kOpThreads), lds, st, c, seed, P, gen, gens, tk,
                        p_cx, p_swap, p_mut, fl, n_fl, pop, fit, next, best_J, best_idx, final_pop, wgs, elite_wg);
     return hipGetLastError();
