@@ -78,6 +78,21 @@ def test_cfg1_full(mf, orc, seed):
     assert gold["n_feas"] == g["n_feas"] and gold["top_idx"] == [int(x) for x in g["top_idx"]]
 
 
+@pytest.mark.parametrize("k", [16, 64])
+def test_cfg1_small_range_finish(mf, orc, k):
+    # the N=5 space takes the small-range path: each fast workgroup keeps its
+    # k best canonical keys and one workgroup finishes; 206 workgroups x 16
+    # keys are staged in LDS by the finish kernel, 206 x 64 exceed its LDS
+    # limit and are read from global memory
+    inst = synth.cfg1(1)
+    print(f"[small-range] cfg1 seed=1 k={k}", flush=True)
+    g = mf.Problem(inst).search(inst.sla, inst.omega, k=k)
+    r = orc.Problem(inst).search(inst.sla, inst.omega, k=k)
+    assert g["n_vram"] == r["n_vram"] and g["n_feas"] == r["n_feas"]
+    np.testing.assert_array_equal(g["top_idx"], r["top_idx"])
+    assert g["top_J"].tobytes() == r["top_J"].tobytes()
+
+
 def test_tight_latency_bounds(mf, orc):
     # bounds drawn near the latency distribution: every model's bound binds
     # for a large share of configurations, so many decisions go to the
