@@ -214,7 +214,8 @@ def bench_fixed(mf, torch, seed, steps, warmup):
                                   "unit": "G VALU wave-instr/s", "frac": ach / PEAK_VALU_GINST,
                                   "alg_lane_ops_per_config": ops,
                                   "note": "the 9 operations include the J chain, which blocks whose exact J upper "
-                                          "bound is under the wave's k-th J skip (linear objective)"}}
+                                          "bound is under the wave's k-th J skip; under Eq. 3 the chain's four "
+                                          "penalty subtractions per configuration are not counted"}}
     out["workload"] = ("the N=6 and N=8 searches with the surrogates' aggregate input held at a seeded observed "
                        "state (linear objective; N=6 also with Eq. 3)")
     return out

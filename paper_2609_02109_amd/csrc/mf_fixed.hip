@@ -452,22 +452,35 @@ __global__ void __launch_bounds__(kFixedWaves * 64) fixed_periodic_kernel(const 
         bpen[p] = EQ3 ? pens[rb].pen : 0.0;
         ra0[p] = (uint32_t)a.in_off[0] + u / Kb;
     }
-    // linear objective: the rows of a and of b with the largest omega q (the
-    // largest q for omega >= 0, the smallest otherwise).  RN and fma are
-    // monotone, so fma(omb, qb*, fma(oma, qa*, Jp)) bounds the J of every
-    // configuration of a block from above, bit for bit
-    double qa_star = 0.0, qb_star = 0.0;
-    if constexpr (!EQ3) {
-        for (int t = 0; t < 2; t++) {
-            const int K = a.in_K[t], off = a.in_off[t];
-            const bool up = (t == 0 ? oma : omb) >= 0.0;
-            double best = rows[off].q;
-            for (int r = 1; r < K; r++) {
-                const double q = rows[off + r].q;
-                if (up ? q > best : q < best) best = q;
+    // the rows of a and of b with the largest omega q (the largest q for
+    // omega >= 0, the smallest otherwise) and, under Eq. 3, the smallest
+    // staged P and pen of each.  RN and fma are monotone, J falls as P or pen
+    // grows, and the chain below applies them in the kernel's own order, so
+    // it bounds the J of every configuration of a block from above, bit for
+    // bit (a NaN extreme gives a NaN bound, which prunes nothing)
+    double qa_star = 0.0, qb_star = 0.0, Pa_min = 0.0, pena_min = 0.0, Pb_min = 0.0, penb_min = 0.0;
+    for (int t = 0; t < 2; t++) {
+        const int K = a.in_K[t], off = a.in_off[t];
+        const bool up = (t == 0 ? oma : omb) >= 0.0;
+        double best = rows[off].q;
+        double Pm = EQ3 ? pens[off].P : 0.0, pm = EQ3 ? pens[off].pen : 0.0;
+        for (int r = 1; r < K; r++) {
+            const double q = rows[off + r].q;
+            if (up ? q > best : q < best) best = q;
+            if (EQ3) {
+                const FixedPen pp = pens[off + r];
+                if (pp.P < Pm) Pm = pp.P;
+                if (pp.pen < pm) pm = pp.pen;
             }
-            if (t == 0) qa_star = best;
-            else qb_star = best;
+        }
+        if (t == 0) {
+            qa_star = best;
+            Pa_min = Pm;
+            pena_min = pm;
+        } else {
+            qb_star = best;
+            Pb_min = Pm;
+            penb_min = pm;
         }
     }
     uint32_t aoff[P];   // byte offsets of this lane's first rows of model a (rows and penalties alike)
@@ -516,7 +529,11 @@ __global__ void __launch_bounds__(kFixedWaves * 64) fixed_periodic_kernel(const 
         // no configuration of the block can enter the wave's list when its
         // prefix fails a bound or its largest J is under the k-th J: then
         // only the counts are formed
-        const bool counts_only = !EQ3 && ((int32_t)flp < 0 || fma(omb, qb_star, fma(oma, qa_star, Jp)) < thrJ);
+        double Jub = fma(oma, qa_star, Jp);
+        if (EQ3) Jub = (Jub - Pa_min) - pena_min;
+        Jub = fma(omb, qb_star, Jub);
+        if (EQ3) Jub = (Jub - Pb_min) - penb_min;
+        const bool counts_only = (int32_t)flp < 0 || Jub < thrJ;
         auto tile = [&](const char *gr, const char *gp, uint64_t ib, int p, auto co) {
             constexpr bool CO = decltype(co)::value;
             const FixedRow x = *reinterpret_cast<const FixedRow *>(gr + aoff[p]);

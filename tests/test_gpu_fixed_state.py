@@ -93,6 +93,28 @@ def test_fixed_periodic_last_digit(mf, orc, n_options, period, seed, eq3):
     assert g["top_J"].tobytes() == r["top_J"].tobytes()
 
 
+# Whole spaces of 6-9 million configurations with a periodic last digit:
+# several blocks per wave, so a wave's list fills and the later blocks whose
+# largest possible J falls under its k-th J form only the counts.  Any block
+# skipped wrongly would drop a configuration of the oracle's exact top-k.
+@pytest.mark.parametrize("n_options", [[24, 32, 32, 16, 16], [16, 32, 32, 24, 24]])
+@pytest.mark.parametrize("eq3", [False, True])
+def test_fixed_periodic_pruned_blocks(mf, orc, n_options, eq3):
+    inst = synth.make_instance(n_options, 8, 4, 32, 32, seed=0, vram_quantile=0.7)
+    state = synth.make_state(inst, 3)
+    ob = synth.make_objective(inst, 3) if eq3 else None
+    k = 8
+    print(f"[fixed pruned] K={n_options} eq3={eq3}", flush=True)
+    p = mf.Problem(inst, variants=ob)
+    g = p.search(inst.sla, inst.omega, k=k, objective=ob, state=state)
+    p.close()
+    r = orc.Problem(inst, ob, state=state).search(inst.sla, inst.omega, k=k, lo=0, hi=inst.space_size)
+    assert g["n_vram"] == r["n_vram"] and g["n_feas"] == r["n_feas"]
+    assert r["n_feas"] > 100_000
+    np.testing.assert_array_equal(g["top_idx"], r["top_idx"])
+    assert g["top_J"].tobytes() == r["top_J"].tobytes()
+
+
 def test_fixed_n6_ranges(mf, orc):
     inst = synth.cfg2(0)
     st = synth.make_state(inst, 0)
