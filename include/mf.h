@@ -220,7 +220,7 @@ typedef struct {
     float state[MF_MAX_AGG];
     /* Upper bound on the entries of the certification list (configurations
      * whose service decision the fast path leaves to the canonical
-     * re-evaluation); 0 keeps the default (1/128 of the range, at least 2^20,
+     * re-evaluation); 0 keeps the default (1/64 of the range, at least 2^20,
      * at most 2^26).  A smaller list shrinks the workspace; a range that fills
      * it is split in halves and searched again (n_splits). */
     uint32_t worklist_cap;
@@ -265,7 +265,7 @@ mf_status mf_search(mf_problem *p, const mf_search_args *args, void *d_ws, size_
  * one GPU (other threads, other streams) race and give wrong results;
  * serialise them.  The scratch keeps the last call's contents; each call
  * initialises what it reads. */
-#define MF_NOALLOC_SCRATCH_BYTES (64u << 20)
+#define MF_NOALLOC_SCRATCH_BYTES (128u << 20)
 mf_status mf_search_noalloc(mf_problem *p, const mf_search_args *args, void *stream, mf_result *h_out);
 
 /* ------------------------------------------------- static (multi-step) search */

@@ -54,6 +54,7 @@ struct mf_problem {
     int32_t *d_agg_cols = nullptr, *d_row_model = nullptr;
     FastLayout lay{};
     FastConst fc{};
+    int fast_e1[kMaxN] = {}, fast_e2[kMaxN] = {};   // fast image scales: layer 1 by 2^e1, W2 by 2^e2
     // variant metadata of the full utility (Eq. 3)
     bool has_var = false;
     std::vector<int32_t> n_var;
@@ -184,6 +185,43 @@ bool bf16_exact(float x)
     return (b & 0xFFFFu) == 0u;
 }
 
+// x rounded to the nearest binary16 value (ties to even), as a double; x
+// finite with |x| < 65504.  Subnormal binary16 values are spaced 2^-24.
+double f16_rne(double x)
+{
+    const double a = std::fabs(x);
+    if (a == 0.0) return 0.0;
+    int e;
+    (void)std::frexp(a, &e);                                  // a in [2^(e-1), 2^e)
+    const double q = std::ldexp(1.0, std::max(e - 1, -14) - 10);   // spacing at a
+    const double r = std::nearbyint(a / q) * q;               // default rounding: to nearest even
+    return x < 0 ? -r : r;
+}
+
+// IEEE binary16 encoding of a value f16_rne returned.
+uint16_t f16_bits(double v)
+{
+    const uint16_t sign = v < 0 ? 0x8000u : 0u;
+    const double a = std::fabs(v);
+    if (a < 0x1p-14) return (uint16_t)(sign | (uint16_t)std::lround(a * 0x1p24));   // subnormal (or zero)
+    int e;
+    const double f = std::frexp(a, &e);                       // a = f 2^e, f in [0.5, 1)
+    const int ex = e - 1 + 15;
+    const uint32_t mant = (uint32_t)std::lround((2.0 * f - 1.0) * 1024.0);
+    return (uint16_t)(sign | (uint16_t)(ex << 10) | (uint16_t)mant);
+}
+
+// A weight w (already scaled) as two binary16 pieces w1 = RNE(w), w2 =
+// RNE(w - w1); *ew = |w - w1 - w2| (exact).  The matrix cores take binary16
+// subnormals as they are (a probe on the MI355X: every product with a
+// subnormal operand exact), so subnormal pieces count at their value.
+void split_w_f16(double w, double *w1, double *w2, double *ew)
+{
+    *w1 = f16_rne(w);
+    *w2 = f16_rne(w - *w1);   // w - w1 is exact in double
+    *ew = std::fabs(w - *w1 - *w2);
+}
+
 // Per model: a-priori bounds on |fast fp32 path - canonical fp64| for both
 // outputs, and a magnitude bound on throughput.  Each dot product of n terms
 // computed as any sequence of n correctly rounded fused multiply-adds (the
@@ -196,17 +234,14 @@ bool bf16_exact(float x)
 // Fast path, layer 1: P'[o] = b1 + W1_loc x_o + W1_agg c (fp64 chain of L+A
 // terms, rounded to fp32), then A fp32 fmas W1_agg (a - c) onto it, with
 // a - c rounded to fp32 (exact on the generator's grid).
-void model_bounds(const mf_problem &p, const std::vector<float> &F, const std::vector<float> &W, int i,
-                  double *b_lat, double *b_thr, double *m_thr)
+// Per aggregate column k (original order): amax[k] bounds |a_k| and amaxc[k]
+// bounds |a_k - c_k| over the joint space.
+void agg_ranges(const mf_problem &p, const std::vector<float> &F, std::vector<double> &amax,
+                std::vector<double> &amaxc)
 {
-    const int L = p.L, A = p.A, H1 = p.H1, H2 = p.H2, nin = L + A;
-    const float *w = W.data() + (int64_t)i * p.wstride;
-    const float *W1 = w, *b1 = W1 + (int64_t)H1 * nin, *W2 = b1 + H1, *b2 = W2 + (int64_t)H2 * H1, *W3 = b2 + H2,
-                *b3 = W3 + 2 * H2;
-    std::vector<double> xmax(L, 0.0), amax(A, 0.0), amaxc(A, 0.0);
-    for (int o = 0; o < p.K[i]; o++)
-        for (int k = 0; k < L; k++)
-            xmax[k] = std::max(xmax[k], (double)std::fabs(F[(int64_t)(p.opt_off[i] + o) * L + k]));
+    const int L = p.L, A = p.A;
+    amax.assign(A, 0.0);
+    amaxc.assign(A, 0.0);
     for (int k = 0; k < A; k++) {
         double smax = 0.0, smin = 0.0, sabs = 0.0;
         for (int j = 0; j < p.N; j++) {
@@ -222,9 +257,38 @@ void model_bounds(const mf_problem &p, const std::vector<float> &F, const std::v
             sabs += ma;
         }
         amax[k] = sabs;
-        amaxc[k] = std::max(std::fabs(smax - p.centre[k]), std::fabs(smin - p.centre[k])) * (1 + 1e-12);
+        // the fp32 aggregate (model order) is within N u sabs of the exact sum
+        amaxc[k] = (std::max(std::fabs(smax - p.centre[k]), std::fabs(smin - p.centre[k])) + 2.0 * p.N * kU32 * sabs) *
+                   (1 + 1e-12);
     }
-    std::vector<double> M1(H1), e1f(H1), e1c(H1), M2(H2), e2f(H2), e2c(H2);
+}
+
+// Power-of-two scale 2^ex[k] of each aggregate column's binary16 layer-1
+// operand: |2^ex (a - c)| <= 2^14.
+std::vector<int> agg_exponents(const std::vector<double> &amaxc)
+{
+    std::vector<int> ex(amaxc.size(), 0);
+    for (size_t k = 0; k < amaxc.size(); k++) {
+        if (amaxc[k] > 0.0) ex[k] = (int)std::floor(std::log2(0x1p14 / amaxc[k]));
+        ex[k] = std::min(std::max(ex[k], -60), 60);
+        while (ex[k] > -60 && amaxc[k] * (1 + kU32) * std::ldexp(1.0, ex[k]) > 0x1p14) ex[k]--;
+    }
+    return ex;
+}
+
+bool model_bounds(const mf_problem &p, const std::vector<float> &F, const std::vector<float> &W, int i,
+                  const std::vector<int> &ex, double *b_lat, double *b_thr, double *m_thr, int *e1_out, int *e2_out)
+{
+    const int L = p.L, A = p.A, H1 = p.H1, H2 = p.H2, nin = L + A;
+    const float *w = W.data() + (int64_t)i * p.wstride;
+    const float *W1 = w, *b1 = W1 + (int64_t)H1 * nin, *W2 = b1 + H1, *b2 = W2 + (int64_t)H2 * H1, *W3 = b2 + H2,
+                *b3 = W3 + 2 * H2;
+    std::vector<double> xmax(L, 0.0), amax, amaxc;
+    for (int o = 0; o < p.K[i]; o++)
+        for (int k = 0; k < L; k++)
+            xmax[k] = std::max(xmax[k], (double)std::fabs(F[(int64_t)(p.opt_off[i] + o) * L + k]));
+    agg_ranges(p, F, amax, amaxc);
+    std::vector<double> M1(H1), e1f(H1), e1c(H1), M2(H2), e2f(H2), e2c(H2), pmax_h(H1);
     for (int h = 0; h < H1; h++) {
         // |P'| over this model's options, and the magnitudes of its fp64 chain
         double pmax = 0.0, pchain = 0.0;
@@ -252,24 +316,110 @@ void model_bounds(const mf_problem &p, const std::vector<float> &F, const std::v
         }
         for (int k = 0; k < L; k++) am_full += std::fabs((double)W1[(int64_t)h * nin + k]) * xmax[k];
         M1[h] = pmax + am;
+        pmax_h[h] = pmax;
         e1f[h] = gam(L + A, kU64) * pchain            // fp64 precompute
                  + kU32 * pmax                         // rounding P' to fp32
                  + kU32 * aw                           // rounding a - c to fp32
-                 + gam(A, kU32) * M1[h] * (1 + 2 * kU32);   // A fp32 fmas
+                 + 0x1p-80;                            // fp32 subnormals under the layer-1 scale
         e1c[h] = gam(nin, kU64) * am_full;             // canonical chain on uncentred inputs
     }
-    for (int v = 0; v < H2; v++) {
-        double m = std::fabs((double)b2[v]), pf = 0.0, pc = 0.0, mf = m, mc = m;
+    // Layer 1's aggregate part on binary16 pieces, in scaled units: x_k =
+    // 2^ex_k (a_k - c_k) (|x| <= X_k) as x1 + x2 (|x - x1 - x2| <= 2^-21 |x| +
+    // 2^-24), w = 2^(e1 - ex_k) W1_agg as w1 + w2 (|w - w1 - w2| = ew), all
+    // four cross products on two v_mfma_f32_32x32x16_f16 (one when A <= 4)
+    // onto P' = 2^e1 P, each counted as 17 u (|C| + sum |products|) (see
+    // layer 2 below).  The
+    // scale 2^e1 keeps |2^e1 h1| <= 2^14 and the weight pieces in range.
+    std::vector<double> e1m(H1, 0.0);
+    double w1a_max = 0.0, x_max0 = 0.0;
+    for (int h = 0; h < H1; h++) {
+        x_max0 = std::max(x_max0, M1[h] + e1f[h]);
+        for (int k = 0; k < A; k++)
+            w1a_max = std::max(w1a_max, std::fabs((double)W1[(int64_t)h * nin + L + k]) * std::ldexp(1.0, -ex[k]));
+    }
+    int e1 = x_max0 > 0.0 ? (int)std::floor(std::log2(0x1p13 / x_max0)) : 0;
+    if (w1a_max > 0.0) e1 = std::min(e1, (int)std::floor(std::log2(0x1p14 / w1a_max)));
+    e1 = std::min(std::max(e1, -60), 60);
+    auto layer1_terms = [&](int e) {
+        const double s1 = std::ldexp(1.0, e);
         for (int h = 0; h < H1; h++) {
-            const double aw = std::fabs((double)W2[(int64_t)v * H1 + h]);
+            double er = 0.0, sp = 0.0;
+            for (int k = 0; k < A; k++) {
+                const double X = std::ldexp(amaxc[k] * (1 + kU32), ex[k]);
+                double w1, w2, ew;
+                const double wk = s1 * std::ldexp((double)W1[(int64_t)h * nin + L + k], -ex[k]);
+                split_w_f16(wk, &w1, &w2, &ew);
+                er += (0x1p-21 * X + 0x1p-24) * (std::fabs(wk) + ew) + X * ew;
+                sp += (X * (1.0 + 0x1p-10) + 0x1p-23) * (std::fabs(w1) + std::fabs(w2));
+            }
+            e1m[h] = (er + gam(A <= 4 ? 17.0 : 34.0, kU32) * (s1 * pmax_h[h] + sp)) / s1;
+        }
+    };
+    for (;;) {
+        layer1_terms(e1);
+        double xm = 0.0;
+        for (int h = 0; h < H1; h++) xm = std::max(xm, M1[h] + e1f[h] + e1m[h]);
+        if (xm * std::ldexp(1.0, e1) <= 0x1p14 || e1 <= -60) break;
+        e1--;
+    }
+    for (int h = 0; h < H1; h++) e1f[h] += e1m[h];
+    // Layer 2 runs on binary16 pieces in scaled units: x = 2^e1 h1 (fast h1,
+    // |x| <= X = 2^e1 (M1 + e1f) <= 2^14) as x1 = x truncated and x2 = (x -
+    // x1) rounded to nearest (|x2| <= 2^-10 |x| + 2^-23, |x - x1 - x2| <=
+    // 2^-21 |x| + 2^-24, the absolute parts for binary16 subnormals) and
+    // w = 2^e2 W2 as w1 + w2 (rounded on the host, |w - w1 - w2| = ew);
+    // x w - (x1 w1 + x1 w2 + x2 w1) = x2 w2 + (x - x1 - x2) w + (x1 + x2) ew.
+    // Accumulation, 3 H1 / 16 v_mfma_f32_32x32x16_f16 per output: each is
+    // counted as 17 u (|C| + sum |products|), what 17 terms aligned to the
+    // largest within a window of at least 24 bits, truncated, then rounded
+    // once, can lose (a probe on the MI355X over 8 M outputs, exponents of
+    // the products spread over 2^30 and cancelling accumulators included,
+    // found at most 5.8 u; the matrix core does not round each product sum
+    // separately, so the error is not that of one rounding).
+    double x_max = 0.0, w_max = 0.0;
+    for (int h = 0; h < H1; h++) x_max = std::max(x_max, M1[h] + e1f[h]);
+    for (int64_t t = 0; t < (int64_t)H2 * H1; t++) w_max = std::max(w_max, (double)std::fabs(W2[t]));
+    if (x_max * std::ldexp(1.0, e1) > 0x1p14) return false;
+    int e2 = 0;
+    if (w_max > 0.0) e2 = (int)std::floor(std::log2(0x1p14 / w_max));
+    e2 = std::min(std::max(e2, -60), 60);
+    while (e2 > -60 && w_max * std::ldexp(1.0, e2) > 0x1p14) e2--;
+    // W3 / 2^(e1+e2) and b2 2^(e1+e2) must stay normal and finite in fp32
+    auto scaled_ok = [&](int es) {
+        for (int t = 0; t < 2 * H2; t++) {
+            const double a = std::fabs((double)W3[t]) * std::ldexp(1.0, -es);
+            if (W3[t] != 0.f && (a < 0x1p-126 || a > 0x1p127)) return false;
+        }
+        for (int v = 0; v < H2; v++) {
+            const double a = std::fabs((double)b2[v]) * std::ldexp(1.0, es);
+            if (b2[v] != 0.f && (a < 0x1p-126 || a > 0x1p127)) return false;
+        }
+        return true;
+    };
+    // a smaller W2 scale only costs binary16 range at the small end
+    while (!scaled_ok(e1 + e2) && e2 > -60 && e1 + e2 > 0) e2--;
+    if (!scaled_ok(e1 + e2)) return false;
+    *e1_out = e1;
+    *e2_out = e2;
+    const double s1 = std::ldexp(1.0, e1), s2 = std::ldexp(1.0, e2), S = s1 * s2;
+    const double gacc = gam(17.0 * 3.0 * (H1 / 16), kU32);
+    for (int v = 0; v < H2; v++) {
+        double m = std::fabs((double)b2[v]), pf = 0.0, pc = 0.0, mc = m, er = 0.0, sp = 0.0;
+        for (int h = 0; h < H1; h++) {
+            const double w = (double)W2[(int64_t)v * H1 + h], aw = std::fabs(w);
+            double w1, w2, ew;
+            split_w_f16(s2 * w, &w1, &w2, &ew);
+            const double X = s1 * (M1[h] + e1f[h]);
+            er += (0x1p-10 * X + 0x1p-23) * std::fabs(w2) + (0x1p-21 * X + 0x1p-24) * s2 * aw +
+                  (X * (1.0 + 0x1p-20) + 0x1p-24) * ew;
+            sp += (X * (1.0 + 0x1p-10) + 0x1p-23) * (std::fabs(w1) + std::fabs(w2));
             m += aw * M1[h];
             pf += aw * e1f[h];
             pc += aw * e1c[h];
-            mf += aw * (M1[h] + e1f[h]);
             mc += aw * (M1[h] + e1c[h]);
         }
         M2[v] = m;
-        e2f[v] = pf + gam(H1, kU32) * mf;
+        e2f[v] = pf + (er + gacc * (S * std::fabs((double)b2[v]) + sp)) / S;
         e2c[v] = pc + gam(H1, kU64) * mc;
     }
     double out_b[2], out_m = 0.0;
@@ -292,6 +442,7 @@ void model_bounds(const mf_problem &p, const std::vector<float> &F, const std::v
     *b_lat = out_b[0];
     *b_thr = out_b[1];
     *m_thr = out_m;
+    return true;
 }
 
 // Smallest float >= x.
@@ -420,9 +571,9 @@ WsLayout ws_layout(const mf_problem &p, uint64_t n, int top_k, uint32_t worklist
         const uint64_t g = (tiles + w.waves - 1) / w.waves;
         w.grid = (int)std::max<uint64_t>(1, std::min<uint64_t>(g, (uint64_t)p.num_cus));
     }
-    // certification list: 1/128 of the range, at least 2^20 entries (never
+    // certification list: 1/64 of the range, at least 2^20 entries (never
     // more than the range), at most 2^26
-    const uint64_t want = std::min<uint64_t>(std::max<uint64_t>(n / 128, (uint64_t)kDefaultWorklist), 1ull << 26);
+    const uint64_t want = std::min<uint64_t>(std::max<uint64_t>(n / 64, (uint64_t)kDefaultWorklist), 1ull << 26);
     uint64_t cap = std::max<uint64_t>(std::min<uint64_t>(want, n), 1024);
     // the caller may bound the list (a full list splits the range)
     if (worklist_cap >= 1) cap = std::min<uint64_t>(cap, (uint64_t)worklist_cap);
@@ -646,8 +797,8 @@ mf_status run_range(mf_problem *p, const mf_search_args *args, uint64_t lo, uint
     // the small path's fast kernel keeps its certification tail's buffers
     // after the workgroup lists in LDS
     const size_t ep_bytes = fast_small_epilogue_bytes(p->N);
-    const size_t small_lds = (size_t)p->lay.total_floats * 4 + kFastPar * 4 + (size_t)w.waves * w.kp * 8 + ep_bytes;
-    if (w.small && small_lds <= 163840) {
+    const size_t small_lds = fast_dyn_lds(p->lay, w.waves, w.kp, ep_bytes);
+    if (w.small && small_lds <= (size_t)kFastLdsMax) {
         // two launches and no memset: the fast kernel leaves per-workgroup
         // lists, counts and certification segments; one workgroup completes
         // the search and writes every field of the result block; the fast
@@ -1186,7 +1337,7 @@ TableLayout table_layout(const mf_desc &d, const Shape &sh)
         FastLayout &ly = t.lay;
         ly.H = H; ly.A = A; ly.AP = 8; ly.MB = H / 32; ly.S1 = A / 2; ly.PST = H + 4;
         int o = 0;
-        ly.off_w1a = o; o += N * ly.MB * ly.S1 * 64;
+        ly.off_w1a = o; o += N * ly.MB * 64 * (A <= 4 ? 2 : 4);
         ly.off_b2 = o; o += N * H;
         ly.off_w2 = o; o += N * H * H;
         ly.off_w3 = o; o += N * 2 * H;
@@ -1195,16 +1346,15 @@ TableLayout table_layout(const mf_desc &d, const Shape &sh)
         ly.off_g = o; o += sumK * ly.AP;
         ly.off_c = o; o += 8;
         ly.total_floats = (o + 3) & ~3;
-        const size_t lds = (size_t)ly.total_floats * 4 + kFastPar * 4 + (size_t)kSearchWaves * 64 * 8;
-        if (lds > 163840) t.fast_ok = false;
+        if (fast_dyn_lds(ly, kSearchWaves, 64, 0) > (size_t)kFastLdsMax) t.fast_ok = false;
         // the canonical first layer of every model goes into the image when
         // the image, 16 waves' lists and the small-range tail still fit
         ly.off_c1 = -1;
         ly.off_feat = -1;
-        ly.c1_stride = (L + A) * H + H;
+        ly.c1_stride = (int)((sh.wstride + 3) & ~(int64_t)3);
         const int with_c1 = (ly.total_floats + N * ly.c1_stride + sumK * L + 3) & ~3;
         if ((size_t)with_c1 * 4 + kFastPar * 4 + (size_t)kSearchWavesWide * 64 * 8 + fast_small_epilogue_bytes(N) <=
-            163840) {
+            (size_t)kFastLdsMax) {
             ly.off_c1 = ly.total_floats;
             ly.off_feat = ly.off_c1 + N * ly.c1_stride;
             ly.total_floats = with_c1;
@@ -1394,7 +1544,19 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
     const int H = H1;
     const FastLayout &ly = p->lay;
     if (p->fast_ok) {
+        std::vector<double> amax_all, amaxc_all;
+        agg_ranges(*p, F, amax_all, amaxc_all);
+        const std::vector<int> ex = agg_exponents(amaxc_all);
+        for (int i = 0; i < N && p->fast_ok; i++)
+            if (!model_bounds(*p, F, W, i, ex, &p->fc.bound_lat[i], &p->fc.bound_thr[i], &p->fc.mag_thr[i],
+                              &p->fast_e1[i], &p->fast_e2[i]))
+                p->fast_ok = false;   // no binary16 scaling fits this model's ranges
+    }
+    if (p->fast_ok) {
         float *img = at_f(tl.o_img);
+        std::vector<double> amax_all, amaxc_all;
+        agg_ranges(*p, F, amax_all, amaxc_all);
+        const std::vector<int> ex = agg_exponents(amaxc_all);
         // internal aggregate slot order: the VRAM slot first
         std::vector<int> perm;
         perm.push_back(p->vram_slot);
@@ -1404,26 +1566,49 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
             const float *w = W.data() + (int64_t)i * p->wstride;
             const float *W1 = w, *b1 = W1 + (int64_t)H * nin, *W2 = b1 + H, *b2 = W2 + (int64_t)H * H,
                         *W3 = b2 + H, *b3 = W3 + 2 * H;
+            // power-of-two scales (exact): 2^e1 on layer 1, 2^e2 on W2, so
+            // the layer-2 accumulator holds 2^(e1+e2) z2 and W3 takes it back
+            const int e1 = p->fast_e1[i], e2 = p->fast_e2[i];
+            const double s1 = std::ldexp(1.0, e1), s2 = std::ldexp(1.0, e2), S = s1 * s2;
+            // layer 1's aggregate columns: per (block, lane) w1 of the lane
+            // half's internal slots 2j + l/32 (j < ns: 4 slots, or 2 when
+            // A <= 4), then their w2
+            const int ns = A <= 4 ? 2 : 4;
+            uint16_t *w1p = reinterpret_cast<uint16_t *>(img + ly.off_w1a + i * (ly.MB * 64 * ns));
             for (int mb = 0; mb < ly.MB; mb++)
-                for (int st = 0; st < ly.S1; st++)
-                    for (int l = 0; l < 64; l++)
-                        img[ly.off_w1a + ((i * ly.MB + mb) * ly.S1 + st) * 64 + l] =
-                            W1[(int64_t)(32 * mb + l % 32) * nin + L + perm[2 * st + l / 32]];
-            for (int h = 0; h < H; h++) img[ly.off_b2 + i * H + h] = b2[h];
+                for (int l = 0; l < 64; l++)
+                    for (int j = 0; j < ns; j++) {
+                        const int k = 2 * j + l / 32;
+                        double w1 = 0.0, w2 = 0.0, ew;
+                        if (k < A)
+                            split_w_f16(s1 * std::ldexp((double)W1[(int64_t)(32 * mb + l % 32) * nin + L + perm[k]],
+                                                        -ex[perm[k]]),
+                                        &w1, &w2, &ew);
+                        w1p[(mb * 64 + l) * 2 * ns + j] = f16_bits(w1);
+                        w1p[(mb * 64 + l) * 2 * ns + ns + j] = f16_bits(w2);
+                    }
+            for (int h = 0; h < H; h++) img[ly.off_b2 + i * H + h] = (float)(S * b2[h]);
+            uint16_t *w2p = reinterpret_cast<uint16_t *>(img + ly.off_w2 + i * H * H);
             for (int mb2 = 0; mb2 < ly.MB; mb2++)
                 for (int mb1 = 0; mb1 < ly.MB; mb1++)
-                    for (int q = 0; q < 4; q++)
+                    for (int kh = 0; kh < 2; kh++)
                         for (int l = 0; l < 64; l++)
-                            for (int j = 0; j < 4; j++)
-                                img[ly.off_w2 + i * H * H + ((((mb2 * ly.MB + mb1) * 4 + q) * 64 + l) * 4 + j)] =
-                                    W2[(int64_t)(32 * mb2 + l % 32) * H + 32 * mb1 + 8 * q + 4 * (l / 32) + j];
+                            for (int j = 0; j < 8; j++) {
+                                const double w = s2 * W2[(int64_t)(32 * mb2 + l % 32) * H + 32 * mb1 + 16 * kh +
+                                                         8 * (j / 4) + 4 * (l / 32) + j % 4];
+                                double w1, w2, ew;
+                                split_w_f16(w, &w1, &w2, &ew);
+                                const int64_t at = ((((int64_t)(mb2 * ly.MB + mb1) * 2 + kh) * 2) * 64 + l) * 8 + j;
+                                w2p[at] = f16_bits(w1);
+                                w2p[at + 64 * 8] = f16_bits(w2);
+                            }
             for (int o2 = 0; o2 < 2; o2++)
                 for (int mb = 0; mb < ly.MB; mb++)
                     for (int q = 0; q < 4; q++)
                         for (int hf = 0; hf < 2; hf++)
                             for (int j = 0; j < 4; j++)
                                 img[ly.off_w3 + i * 2 * H + (((o2 * ly.MB + mb) * 4 + q) * 2 + hf) * 4 + j] =
-                                    W3[o2 * H + 32 * mb + 8 * q + 4 * hf + j];
+                                    (float)(W3[o2 * H + 32 * mb + 8 * q + 4 * hf + j] / S);
             img[ly.off_b3 + 4 * i + 0] = b3[0];
             img[ly.off_b3 + 4 * i + 1] = b3[1];
         }
@@ -1438,19 +1623,9 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
             for (int st = 0; st < 4; st++) {
                 const int k = 2 * st + hf;
                 img[ly.off_c + hf * 4 + st] = k < A ? p->centre[perm[k]] : 0.f;
+                p->fc.agg_scale[hf][st] = k < A ? (float)std::ldexp(1.0, ex[perm[k]]) : 1.f;
             }
         if (ly.off_feat >= 0) std::memcpy(img + ly.off_feat, F.data(), F.size() * 4);
-        if (ly.off_c1 >= 0)
-            for (int i = 0; i < N; i++) {
-                const float *w = W.data() + (int64_t)i * p->wstride;
-                float *c1 = img + ly.off_c1 + i * ly.c1_stride;
-                for (int h = 0; h < H; h++) {
-                    for (int k = 0; k < nin; k++) c1[k * H + h] = w[(int64_t)h * nin + k];
-                    c1[nin * H + h] = w[(int64_t)H * nin + h];
-                }
-            }
-        for (int i = 0; i < N; i++)
-            model_bounds(*p, F, W, i, &p->fc.bound_lat[i], &p->fc.bound_thr[i], &p->fc.mag_thr[i]);
         if (p->act == MF_ACT_SIGMOID)
             for (int i = 0; i < N; i++) {
                 // the sigmoid is 1/4-Lipschitz, and its fp32 evaluation is within
@@ -1543,6 +1718,12 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
             for (int h = 0; h < H1; h++) cW2T[(int64_t)h * H2 + v] = W2[(int64_t)v * H1 + h];
         std::memcpy(crest, rest, (size_t)(H2 + 2 * H2 + 2) * 4);
     }
+    // the fast image's copy of each model's canonical block (small-range
+    // certification reads it from LDS)
+    if (p->fast_ok && ly.off_c1 >= 0)
+        for (int i = 0; i < N; i++)
+            std::memcpy(at_f(tl.o_img) + ly.off_c1 + i * ly.c1_stride, canon + (int64_t)i * p->wstride,
+                        (size_t)p->wstride * 4);
     std::memcpy(himg.data() + tl.o_fea, F.data(), F.size() * 4);
     std::memcpy(himg.data() + tl.o_agg, p->agg_cols.data(), (size_t)A * 4);
     int32_t *row_model = reinterpret_cast<int32_t *>(himg.data() + tl.o_rm);
@@ -1600,8 +1781,12 @@ mf_status mf_problem_create(const mf_desc *desc, const float *d_features, const 
         ok = launch_precompute_phat(p->d_features, p->d_canon, sumK, L, A, H, p->wstride, p->d_row_model, p->d_phat,
                                     bl.PST, s) == hipSuccess;
     if (ok && p->fast_ok)
+    {
+        Pow2Scales sc{};
+        for (int i = 0; i < N; i++) sc.e[i] = p->fast_e1[i];
         ok = launch_precompute_p(p->d_features, p->d_canon, p->d_centre, sumK, L, A, H, p->wstride, p->d_row_model,
-                                 reinterpret_cast<float *>(p->d_image) + ly.off_p, ly.PST, s) == hipSuccess;
+                                 reinterpret_cast<float *>(p->d_image) + ly.off_p, ly.PST, sc, s) == hipSuccess;
+    }
     ok = ok && hipStreamSynchronize(s) == hipSuccess;
     // one pair of timing events up front (searches on several streams at
     // once take more from the pool)

@@ -16,6 +16,7 @@ constexpr int kSearchWavesWide = 16;     // ... when registers and LDS allow 4 w
 constexpr int kCertWaves = 4;            // waves per workgroup of the canonical kernels
 constexpr int kDefaultWorklist = 1 << 20; // certification list capacity (entries)
 constexpr int kFastPar = 160;            // floats of per-model parameters after the fp32 fast image in LDS
+constexpr int kFastLdsMax = 163840 - 512; // dynamic LDS of the fp32 fast kernel (its static LDS takes < 512 bytes)
 constexpr int kBf16Waves = 8;            // waves per workgroup of the bf16 fast kernel
 constexpr int kBf16Tiles = 8;            // 32-configuration tiles per wave and model staging
 constexpr int kBf16Par = 128;            // floats of per-model parameters after the bf16 tables in LDS
@@ -24,9 +25,20 @@ constexpr int kBf16Par = 128;            // floats of per-model parameters after
 // Fast-path LDS image.  The device copy of the image is laid out exactly as
 // the fast kernel wants it in LDS, so its prologue is one straight copy.
 // Offsets are in floats from the image start; every block is 16-byte aligned.
-//   w1a[i][mb][s][lane]            A operand of layer 1 (aggregate columns)
+// Model i's layer-1 rows (w1a, p) are scaled by 2^e1[i], b2 by 2^(e1+e2),
+// W2 by 2^e2 and W3 by 2^-(e1+e2): exact power-of-two scalings that keep the
+// binary16 pieces of layer 2 in range and leave every fp32 rounding as it
+// would be unscaled.
+//   w1a[i][mb][lane][j]            A operand of layer 1 (aggregate columns):
+//                                  binary16 w1 (j < ns) and w2 (j >= ns) of
+//                                  2^(e1 - ex) W1[32 mb + lane%32][slot
+//                                  2 (j%ns) + lane/32]; ns = 4 slots (16
+//                                  bytes per lane), 2 when A <= 4 (8 bytes)
 //   b2 [i][H]                      layer-2 bias (accumulator init)
-//   w2 [i][mb2][mb1][q][lane][j]   A operand of layer 2
+//   w2 [i][mb2][mb1][kh][pc][lane][j]  A operands of layer 2: binary16 pieces
+//                                  pc = 0 (w1), 1 (w2) of W2[32 mb2 + lane%32]
+//                                  [32 mb1 + 16 kh + 8 (j/4) + 4 (lane/32) + j%4],
+//                                  8 per lane (16 bytes; one float slot per weight)
 //   w3 [i][o][mb2][q][half][j]     layer-3 weights in accumulator row order
 //   b3 [i][2]  (padded to 4)
 //   p  [row][pst]                  per-option first-layer precompute
@@ -38,17 +50,32 @@ constexpr int kBf16Par = 128;            // floats of per-model parameters after
 //   c  [half][4]                   aggregate centre in the same order: layer 1
 //                                  takes a - c (exact on the 2^-14 grid) and
 //                                  P carries W1_agg c
-//   c1 [i][nin][H], [i][H]         (when it fits) each model's W1 transposed and
-//                                  b1 as given, for canonical evaluation
+//   c1 [i][c1_stride]              (when it fits) each model's canonical block
+//                                  (W1T, b1, W2T, b2, W3, b3 as given), for
+//                                  canonical evaluation
 //   feat [row][L]                  (with c1) the option table
 // ---------------------------------------------------------------------------
 struct FastLayout {
     int H, A, AP, MB, S1, PST;
     int off_w1a, off_b2, off_w2, off_w3, off_b3, off_p, off_g, off_c;
-    int off_c1, c1_stride;     // canonical first layer per model, W1T[nin][H] then b1[H] (-1: not in the image)
+    int off_c1, c1_stride;     // canonical block per model, W1T b1 W2T b2 W3 b3 as in the canonical image (-1: not in the image)
     int off_feat;              // the option table [sumK][L] (with the c1 block; -1: not in the image)
     int total_floats;          // multiple of 4
 };
+
+// The fp32 fast kernel's per-wave candidate lists are merged after the scan,
+// when the image's blocks before g (weights and the per-option precompute)
+// are no longer read: they take that space when it is large enough, else
+// they follow the parameter block.
+inline bool fast_lists_in_image(const FastLayout &ly, int waves, int kp)
+{
+    return (size_t)waves * kp * 8 <= (size_t)ly.off_g * 4;
+}
+inline size_t fast_dyn_lds(const FastLayout &ly, int waves, int kp, size_t ep_bytes)
+{
+    return (size_t)ly.total_floats * 4 + kFastPar * 4 +
+           (fast_lists_in_image(ly, waves, kp) ? 0 : (size_t)waves * kp * 8) + ep_bytes;
+}
 
 // Per-problem constants of the fast kernels (kernel-argument block).
 struct FastConst {
@@ -59,6 +86,9 @@ struct FastConst {
     int32_t opt_off[kMaxN];     // first global option row of model i
     uint32_t magic[kMaxN];      // floor(2^32 / K) + 1 (K > 1), 0 for K == 1
     float vram_cap;
+    // power-of-two scale 2^ex of internal aggregate slot 2s + half at
+    // [half][s] (the fast kernel's binary16 layer-1 operand; 1 past A)
+    float agg_scale[2][4];
     // a-priori bound on |fast - canonical| for (lat, thr) of model i, and on |thr|
     double bound_lat[kMaxN], bound_thr[kMaxN], mag_thr[kMaxN];
 };
@@ -135,6 +165,7 @@ struct FastArgs {
     float *pred;                // dump (optional)
     ObjArgs obj;
     int ep_bytes;               // LDS bytes after the workgroup lists for the small-range certification
+    int lst_off;                // floats from the LDS start to the per-wave lists (0: over the fast weights)
     const float *canon;         // canonical fp32 image [N][wstride] (W1T[nin][H1], b1, ...)
     // Small ranges (search mode, completed by the finish kernel): no global
     // counter.  Certification entries go to a segment of seg_cap entries per
@@ -413,10 +444,16 @@ struct GAConst {
 // and size increase (a call that changes nothing costs a table lookup).
 hipError_t ensure_dyn_lds(const void *fn, size_t bytes);
 
+// Per-model power-of-two exponents (kernel argument).
+struct Pow2Scales {
+    int32_t e[kMaxN];
+};
+
 // launchers (return hipError_t of the launch)
 hipError_t launch_precompute_p(const float *features, const float *weights, const float *centre,
                                int n_rows, int L, int A, int H, int64_t wstride,
-                               const int32_t *row_model, float *image_p, int pst, hipStream_t s);
+                               const int32_t *row_model, float *image_p, int pst, const Pow2Scales &sc,
+                               hipStream_t s);
 hipError_t launch_fast_impl(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode, hipStream_t s);
 int fast_waves_for(int n_models, const FastLayout &lay, int kp, int act);
 int fast_kernel_supported(int n_models, int A, int H, int kp);

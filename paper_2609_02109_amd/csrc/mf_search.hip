@@ -10,9 +10,17 @@
 //   surrogate    per model (Eq. 6): layer 1 = per-option precompute
 //                P[row] = b1 + W1_local x (the option's own columns, done once
 //                per option) as the accumulator init, plus W1_agg a on MFMA;
-//                layer 2 on v_mfma_f32_32x32x2f32 with the layer-1 accumulator
-//                registers fed back directly as the B operand (the accumulator
-//                row order is absorbed into the A-operand layout of W2);
+//                layer 2 on binary16 matrix cores at fp32-level accuracy: the
+//                layer-1 accumulator registers are split into two binary16
+//                pieces each (x1 = x truncated, x2 = the rest truncated), W2
+//                into two precomputed pieces (w1 + w2), and the three leading
+//                cross products x1 w1 + x1 w2 + x2 w1 run on
+//                v_mfma_f32_32x32x16_f16 with fp32 accumulation (the dropped
+//                term and the pieces' truncation are below 2^-20 relative, and
+//                go into the a-priori bound); power-of-two scales folded into
+//                the layer-1, b2 and W3 tables keep every piece inside the
+//                binary16 range without changing any fp32 rounding; the
+//                accumulator row order is absorbed into W2's A-operand layout;
 //                layer 3 (2 outputs) on VALU with one cross-half add
 //   mask/score   latency bound per model decided with an a-priori error bound:
 //                sure pass, sure fail, or "left to canonical re-evaluation";
@@ -27,6 +35,63 @@
 namespace mfi {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ f16x8 as_f16x8(uint4 v)
+{
+    f16x8 r;
+    __builtin_memcpy(&r, &v, 16);
+    return r;
+}
+
+__device__ __forceinline__ uint32_t pk_f16_rtz(float a, float b)
+{
+    const auto h = __builtin_amdgcn_cvt_pkrtz(a, b);
+    uint32_t u;
+    __builtin_memcpy(&u, &h, 4);
+    return u;
+}
+
+// x - x1 for the binary16 value x1 in the low (HI = false) or high half of
+// the packed register p: one mixed-precision fma, exact (x1 is x truncated).
+// Its result feeds only vector instructions the compiler emits itself (the
+// packing below), so the compiler's own wait states cover every matrix-core
+// read of the pieces.
+template <bool HI>
+__device__ __forceinline__ float f16_residual(uint32_t p, float x)
+{
+    float r;
+    if constexpr (HI)
+        asm("v_fma_mix_f32 %0, -%1, 1.0, %2 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "=v"(r) : "v"(p), "v"(x));
+    else
+        asm("v_fma_mix_f32 %0, -%1, 1.0, %2 op_sel:[0,0,0] op_sel_hi:[1,0,0]" : "=v"(r) : "v"(p), "v"(x));
+    return r;
+}
+
+// The pair (a, b) as binary16 pieces: *x1 = (a, b) rounded toward zero,
+// return (a - a1, b - b1) rounded to nearest.  |x - x1 - x2| <= 2^-21 |x| +
+// 2^-24 (binary16 subnormals are kept, by the conversions under the kernel's
+// denormal mode and by the matrix cores).
+__device__ __forceinline__ uint32_t split_f16_pair(float a, float b, uint32_t *x1)
+{
+    const uint32_t h = pk_f16_rtz(a, b);
+    typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+    const f16x2 l = {(_Float16)f16_residual<false>(h, a), (_Float16)f16_residual<true>(h, b)};
+    uint32_t u;
+    __builtin_memcpy(&u, &l, 4);
+    *x1 = h;
+    return u;
+}
+
+// Eight fp32 values v[r0 .. r0 + 7] as two binary16 B operands (x1, x2).
+__device__ __forceinline__ void split_f16x8(const floatx16 &v, int r0, f16x8 &hi, f16x8 &lo)
+{
+    uint32_t h[4], l[4];
+#pragma unroll
+    for (int t = 0; t < 4; t++) l[t] = split_f16_pair(v[r0 + 2 * t], v[r0 + 2 * t + 1], &h[t]);
+    __builtin_memcpy(&hi, h, 16);
+    __builtin_memcpy(&lo, l, 16);
+}
 
 // Bytes of LDS (after the workgroup lists) the certification tail needs: the
 // evaluated list keys, a status word, per (entry, model) predictions of one
@@ -45,22 +110,21 @@ size_t fast_small_epilogue_bytes(int n_models)
 // ascending order.  The inputs of a layer (z, then h1, then h2: input k of a
 // half in its lane k) pass through the wave's 64 doubles of LDS, xb, and are
 // read back at one address per half (a broadcast read), so that the VALU
-// issues the chains themselves.  Layers 2 and 3 read the fp32 weights of the
-// fast image in LDS (each lane its own row: W2 as laid out for the layer-2
-// MFMA, four consecutive inputs contiguous), layer 1 the canonical W1T / b1
-// block c1 (LDS or global).  fp32 weights are exact in fp64.  A wave's LDS
-// accesses complete in program order; wave barriers keep the compiler from
-// moving them across a layer's store.  Outputs: (lat, thr) of the
-// configuration of half h in lanes 32 h and 32 h + 1 of y.
+// issues the chains themselves.  cb is the model's canonical fp32 block
+// (W1T[nin][H], b1[H], W2T[H][H], b2[H], W3[2][H], b3[2]; LDS or global):
+// lane u reads column u of a transposed matrix, consecutive lanes consecutive
+// words.  fp32 weights are exact in fp64.  A wave's LDS accesses complete in
+// program order; wave barriers keep the compiler from moving them across a
+// layer's store.  Outputs: (lat, thr) of the configuration of half h in lanes
+// 32 h and 32 h + 1 of y.
 template <int H, bool PAIR>
-__device__ inline double canon_forward_image(const float *c1, const float *img, const FastLayout &Ly, int i,
-                                             int nin, double z, int lane, bool sigmoid, double *xb)
+__device__ inline double canon_forward_block(const float *cb, int nin, double z, int lane, bool sigmoid, double *xb)
 {
     static_assert(!PAIR || H <= 32, "two configurations per wave need H <= 32");
-    constexpr int MB = H / 32 > 0 ? H / 32 : 1;
     const int uu = PAIR ? (lane & 31) : lane;
     const int u = uu < H ? uu : H - 1;   // lanes past H repeat the last unit and are ignored
     const int hb = PAIR ? (lane & 32) : 0;
+    const float *c1 = cb, *w2t = cb + nin * H + H, *b2 = w2t + H * H, *w3 = b2 + H, *b3 = w3 + 2 * H;
     xb[lane] = z;
     __builtin_amdgcn_wave_barrier();
     double c = (double)c1[nin * H + u];
@@ -80,20 +144,16 @@ __device__ inline double canon_forward_image(const float *c1, const float *img, 
     __builtin_amdgcn_wave_barrier();
     xb[lane] = c > 0.0 ? c : 0.0;   // h1
     __builtin_amdgcn_wave_barrier();
-    // layer 2: lane v = u; W2[v][u'] sits at ((((mb2 MB + mb1) 4 + q) 64 + l) 4 + j)
-    // with v = 32 mb2 + l % 32, u' = 32 mb1 + 8 q + 4 (l / 32) + j
-    const float *w2 = img + Ly.off_w2 + i * (H * H);
-    const int mb2 = u / 32, lv = u % 32;
-    c = (double)img[Ly.off_b2 + i * H + u];
+    c = (double)b2[u];
 #pragma unroll
     for (int u0 = 0; u0 < H; u0 += 8) {
-        const int mb1 = u0 / 32, q = (u0 % 32) / 8;
-        const float4 a0 = *reinterpret_cast<const float4 *>(w2 + ((((mb2 * MB + mb1) * 4 + q) * 64 + lv) * 4));
-        const float4 a1 = *reinterpret_cast<const float4 *>(w2 + ((((mb2 * MB + mb1) * 4 + q) * 64 + lv + 32) * 4));
-        const float wv[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+        float wv[8];
         double hk[8];
 #pragma unroll
-        for (int j = 0; j < 8; j++) hk[j] = xb[hb + u0 + j];
+        for (int j = 0; j < 8; j++) {
+            wv[j] = w2t[(u0 + j) * H + u];
+            hk[j] = xb[hb + u0 + j];
+        }
 #pragma unroll
         for (int j = 0; j < 8; j++) c = fma((double)wv[j], hk[j], c);
     }
@@ -102,16 +162,16 @@ __device__ inline double canon_forward_image(const float *c1, const float *img, 
     __builtin_amdgcn_wave_barrier();
     // layer 3: lanes 32 h + o, W3[o][v] contiguous in v
     const int o = lane & 1;
-    const float *w3 = img + Ly.off_w3 + i * (2 * H) + o * H;
-    c = (double)img[Ly.off_b3 + 4 * i + o];
+    c = (double)b3[o];
 #pragma unroll
     for (int v0 = 0; v0 < H; v0 += 8) {
-        const float4 a0 = *reinterpret_cast<const float4 *>(w3 + v0);
-        const float4 a1 = *reinterpret_cast<const float4 *>(w3 + v0 + 4);
-        const float wv[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+        float wv[8];
         double hk[8];
 #pragma unroll
-        for (int j = 0; j < 8; j++) hk[j] = xb[hb + v0 + j];
+        for (int j = 0; j < 8; j++) {
+            wv[j] = w3[o * H + v0 + j];
+            hk[j] = xb[hb + v0 + j];
+        }
 #pragma unroll
         for (int j = 0; j < 8; j++) c = fma((double)wv[j], hk[j], c);
     }
@@ -134,7 +194,8 @@ __device__ inline void small_certify(const FastArgs &args, const FastConst &fc, 
     const uint64_t g = blockIdx.x;
     const int *pK = reinterpret_cast<const int *>(par + 112), *pOff = reinterpret_cast<const int *>(par + 48);
     const int *pPrev = reinterpret_cast<const int *>(par + 80);
-    unsigned long long *ekey = reinterpret_cast<unsigned long long *>(par + kFastPar) + WAVES * kp;   // [64]
+    unsigned long long *ekey = reinterpret_cast<unsigned long long *>(par + kFastPar) +
+                               (args.lst_off == 0 ? 0 : WAVES * kp);   // [64]
     unsigned int *estat = reinterpret_cast<unsigned int *>(ekey + 64);                               // status, rest
     double *eout = reinterpret_cast<double *>(ekey + 66);                                            // [chunk][N][2]
     int *erow = reinterpret_cast<int *>(eout + (size_t)kCertChunk * N * 2);                          // [chunk][kMaxN]
@@ -202,14 +263,14 @@ __device__ inline void small_certify(const FastArgs &args, const FastConst &fc, 
                     if (j < N) sa = sa + feat[rj[j] * L + col];
                 z = (double)sa;
             }
-            const float *c1 = Ly.off_c1 >= 0 ? smem + Ly.off_c1 + i * Ly.c1_stride
+            const float *cb = Ly.off_c1 >= 0 ? smem + Ly.off_c1 + i * Ly.c1_stride
                                              : args.canon + (int64_t)i * args.wstride;
             double y;
             if constexpr (H <= 32) {
-                y = pair ? canon_forward_image<H, true>(c1, smem, Ly, i, nin, z, lane, SIG, xb)
-                         : canon_forward_image<H, false>(c1, smem, Ly, i, nin, z, lane, SIG, xb);
+                y = pair ? canon_forward_block<H, true>(cb, nin, z, lane, SIG, xb)
+                         : canon_forward_block<H, false>(cb, nin, z, lane, SIG, xb);
             } else {
-                y = canon_forward_image<H, false>(c1, smem, Ly, i, nin, z, lane, SIG, xb);
+                y = canon_forward_block<H, false>(cb, nin, z, lane, SIG, xb);
             }
             const double lat0 = readlane_f64(y, 0), thr0 = readlane_f64(y, 1);
             const double lat1 = readlane_f64(y, 32), thr1 = readlane_f64(y, 33);
@@ -288,7 +349,8 @@ __global__ void __launch_bounds__(WAVES * 64, 1)
 fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int kp)
 {
     constexpr int MB = H / 32;         // 32-row blocks of a hidden layer
-    constexpr int S1 = A / 2;          // layer-1 MFMA k-steps (K = 2 each)
+    static_assert(A <= 8, "layer 1 takes at most 4 aggregate slots per lane half");
+    constexpr bool L1ONE = A <= 4;     // two slots per lane half: one layer-1 instruction per block
     constexpr int AP = 8;              // aggregate row stride in LDS: [half][4]
     extern __shared__ float4 smem4[];
     float *smem = reinterpret_cast<float *>(smem4);
@@ -302,7 +364,7 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
     float *par = smem + Ly.total_floats;
     int *par_off = reinterpret_cast<int *>(par + 48);
     int *par_prev = reinterpret_cast<int *>(par + 80);
-    unsigned long long *lst = reinterpret_cast<unsigned long long *>(par + kFastPar);
+    unsigned long long *lst = reinterpret_cast<unsigned long long *>(smem + args.lst_off);
 #pragma unroll
     for (int i = 0; i < kMaxN; i++) {
         // compile-time index into the argument block (keeps it out of scratch)
@@ -355,8 +417,11 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
 
     const int lane = threadIdx.x & 63, half = lane >> 5, col = lane & 31;
     // aggregate centre of the slots this lane feeds to layer 1
-    const float4 cen = *reinterpret_cast<const float4 *>(smem + Ly.off_c + 4 * half);
-    const float cen_s[4] = {cen.x, cen.y, cen.z, cen.w};
+    // aggregate centre and power-of-two scale of the slots this lane feeds
+    // to layer 1 (read per tile: registers are the kernel's limit)
+    const float4 *cen_p = reinterpret_cast<const float4 *>(smem + Ly.off_c + 4 * half);
+    const float sx_s[4] = {half ? fc.agg_scale[1][0] : fc.agg_scale[0][0], half ? fc.agg_scale[1][1] : fc.agg_scale[0][1],
+                           half ? fc.agg_scale[1][2] : fc.agg_scale[0][2], half ? fc.agg_scale[1][3] : fc.agg_scale[0][3]};
     const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));   // wave-uniform
     const int gw = blockIdx.x * WAVES + wv;
     const uint64_t n = args.n;
@@ -435,6 +500,27 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             }
         }
         const bool vram_ok = ah[0] <= fc.vram_cap;
+        // layer 1's B operands, shared by every model of the tile: the lane's
+        // slots s (2s + half) as x = 2^ex (a - c) in binary16 pieces x1 + x2.
+        // Four slots (A > 4): in k = 8 half + j, j and j + 4 both hold slot
+        // j, bx1 its x1, bx2 its x2.  Two slots: one operand, j = 0, 1 and
+        // 2, 3 hold x1 of slots 0, 1, j = 4, 5 and 6, 7 their x2.
+        f16x8 bx1, bx2;
+        {
+            const float4 cen = cen_p[0];
+            uint32_t q[2], r[2];
+            r[0] = split_f16_pair((ah[0] - cen.x) * sx_s[0], (ah[1] - cen.y) * sx_s[1], &q[0]);
+            if constexpr (L1ONE) {
+                const uint32_t w1[4] = {q[0], q[0], r[0], r[0]};
+                __builtin_memcpy(&bx1, w1, 16);
+                bx2 = bx1;
+            } else {
+                r[1] = split_f16_pair((ah[2] - cen.z) * sx_s[2], (ah[3] - cen.w) * sx_s[3], &q[1]);
+                const uint32_t w1[4] = {q[0], q[1], q[0], q[1]}, w2[4] = {r[0], r[1], r[0], r[1]};
+                __builtin_memcpy(&bx1, w1, 16);
+                __builtin_memcpy(&bx2, w2, 16);
+            }
+        }
 
         float J = 0.f, EJ = 0.f, MJ = 0.f;   // fast J; under Eq. 3 its bound and magnitude
         bool anyfail = false;
@@ -456,19 +542,42 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
                     acc1[mb][4 * q + 2] = v.z;
                     acc1[mb][4 * q + 3] = v.w;
                 }
-            const float *w1a = smem + Ly.off_w1a + i * (MB * S1 * 64) + lane;
+            // W1_agg 2^(e1 - ex) in binary16 pieces w1 + w2, row 32 mb + l%32
+            // of lane l.  Four slots: 16 bytes per lane and block, w1 (j < 4)
+            // then w2 (j >= 4) of the slots 2 (j % 4) + l/32; one A operand
+            // for both instructions, w1 x1 + w2 x1, then w1 x2 + w2 x2.  Two
+            // slots: 8 bytes, w1 then w2 of slots l/32 and 2 + l/32, read
+            // twice into one operand, all four products in one instruction.
+            if constexpr (L1ONE) {
+                const uint2 *w1a = reinterpret_cast<const uint2 *>(smem + Ly.off_w1a + i * (MB * 64 * 2)) + lane;
 #pragma unroll
-            for (int s = 0; s < S1; s++) {
-                const float bop = ah[s] - cen_s[s];
+                for (int mb = 0; mb < MB; mb++) {
+                    const uint2 p = w1a[mb * 64];
+                    const uint4 a = {p.x, p.y, p.x, p.y};
+                    acc1[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_f16x8(a), bx1, acc1[mb], 0, 0, 0);
+                }
+            } else {
+                const uint4 *w1a = reinterpret_cast<const uint4 *>(smem + Ly.off_w1a + i * (MB * 64 * 4)) + lane;
 #pragma unroll
-                for (int mb = 0; mb < MB; mb++)
-                    acc1[mb] = __builtin_amdgcn_mfma_f32_32x32x2f32(w1a[(mb * S1 + s) * 64], bop, acc1[mb], 0, 0, 0);
+                for (int mb = 0; mb < MB; mb++) {
+                    const f16x8 a = as_f16x8(w1a[mb * 64]);
+                    acc1[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bx1, acc1[mb], 0, 0, 0);
+                    acc1[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bx2, acc1[mb], 0, 0, 0);
+                }
             }
 #pragma unroll
             for (int mb = 0; mb < MB; mb++)
 #pragma unroll
                 for (int r = 0; r < 16; r++) acc1[mb][r] = relu_f32(acc1[mb][r]);
-            // ---- layer 2: b2 + W2 h1
+            // ---- layer 2: b2 + W2 h1.  h1 (the relu'd layer-1 accumulators)
+            // becomes binary16 pieces first, K-block by K-block (accumulator
+            // registers 8 kh .. 8 kh + 7 of block mb1): x1 = x truncated, x2
+            // = (x - x1) truncated, as many registers as h1 itself
+            f16x8 xh[MB][2], xl[MB][2];
+#pragma unroll
+            for (int mb1 = 0; mb1 < MB; mb1++)
+#pragma unroll
+                for (int kh = 0; kh < 2; kh++) split_f16x8(acc1[mb1], 8 * kh, xh[mb1][kh], xl[mb1][kh]);
             floatx16 acc2[MB];
             const float *b2 = smem + Ly.off_b2 + i * H + 4 * half;
 #pragma unroll
@@ -481,23 +590,23 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
                     acc2[mb][4 * q + 2] = v.z;
                     acc2[mb][4 * q + 3] = v.w;
                 }
-            const float *w2 = smem + Ly.off_w2 + i * (H * H) + lane * 4;
+            // W2 as two binary16 pieces (w1 + w2 ~ 2^e2 W2) in the A-operand
+            // order of v_mfma_f32_32x32x16_f16: per (mb2, mb1, kh) 1 KB of w1
+            // then 1 KB of w2, lane l's 16 bytes holding K-block elements 0..7;
+            // the products x1 w1 + x1 w2 + x2 w1 accumulate in fp32
+            const uint4 *w2p = reinterpret_cast<const uint4 *>(smem + Ly.off_w2 + i * (H * H)) + lane;
 #pragma unroll
             for (int mb1 = 0; mb1 < MB; mb1++)
 #pragma unroll
-                for (int q = 0; q < 4; q++) {
-                    float4 wv4[MB];
-#pragma unroll
-                    for (int mb2 = 0; mb2 < MB; mb2++)
-                        wv4[mb2] = *reinterpret_cast<const float4 *>(w2 + ((mb2 * MB + mb1) * 4 + q) * 256);
+                for (int kh = 0; kh < 2; kh++)
 #pragma unroll
                     for (int mb2 = 0; mb2 < MB; mb2++) {
-                        acc2[mb2] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv4[mb2].x, acc1[mb1][4 * q + 0], acc2[mb2], 0, 0, 0);
-                        acc2[mb2] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv4[mb2].y, acc1[mb1][4 * q + 1], acc2[mb2], 0, 0, 0);
-                        acc2[mb2] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv4[mb2].z, acc1[mb1][4 * q + 2], acc2[mb2], 0, 0, 0);
-                        acc2[mb2] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv4[mb2].w, acc1[mb1][4 * q + 3], acc2[mb2], 0, 0, 0);
+                        const f16x8 wa = as_f16x8(w2p[(((mb2 * MB + mb1) * 2 + kh) * 2 + 0) * 64]);
+                        const f16x8 wb = as_f16x8(w2p[(((mb2 * MB + mb1) * 2 + kh) * 2 + 1) * 64]);
+                        acc2[mb2] = __builtin_amdgcn_mfma_f32_32x32x16_f16(wa, xh[mb1][kh], acc2[mb2], 0, 0, 0);
+                        acc2[mb2] = __builtin_amdgcn_mfma_f32_32x32x16_f16(wb, xh[mb1][kh], acc2[mb2], 0, 0, 0);
+                        acc2[mb2] = __builtin_amdgcn_mfma_f32_32x32x16_f16(wa, xl[mb1][kh], acc2[mb2], 0, 0, 0);
                     }
-                }
             // ---- layer 3 (2 outputs) on VALU
             const float *w3 = smem + Ly.off_w3 + i * (2 * H) + 4 * half;
             float pl = 0.f, pt = 0.f;
@@ -610,6 +719,7 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             s_cnt[wv] = sv;
             s_cnt[WAVES + wv] = sf;
         }
+        if (args.lst_off == 0) __syncthreads();   // the lists overwrite the weights: every wave's scan is done
         if (lane < kp) lst[wv * kp + lane] = wl.s[0];
         wl_tree_merge<1, WAVES>(wl, lst, kp, wv, lane, kp);
         if (wv == 0) {
@@ -701,14 +811,16 @@ template <int MAXN, int A, int H, int WAVES>
 static hipError_t launch_fast_t(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode,
                                 hipStream_t s)
 {
-    const size_t lds = (size_t)a.lay.total_floats * 4 + kFastPar * 4 + (size_t)WAVES * kp * 8 + (size_t)a.ep_bytes;
+    FastArgs b = a;
+    b.lst_off = fast_lists_in_image(a.lay, WAVES, kp) ? 0 : a.lay.total_floats + kFastPar;
+    const size_t lds = fast_dyn_lds(a.lay, WAVES, kp, (size_t)a.ep_bytes);
     auto fn = a.obj.kind != 0 ? fast_kernel<MAXN, A, H, WAVES, true> : fast_kernel<MAXN, A, H, WAVES, false>;
     if constexpr (MAXN == kMaxN && WAVES == kSearchWaves)   // the sigmoid output runs on the generic kernel
         if (fc.act) fn = a.obj.kind != 0 ? fast_kernel<MAXN, A, H, WAVES, true, true>
                                          : fast_kernel<MAXN, A, H, WAVES, false, true>;
     hipError_t e = ensure_dyn_lds((const void *)fn, lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(fn, dim3(grid), dim3(WAVES * 64), lds, s, a, fc, mode, kp);
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(WAVES * 64), lds, s, b, fc, mode, kp);
     return hipGetLastError();
 }
 
@@ -725,8 +837,8 @@ int fast_kernel_supported(int n_models, int A, int H, int kp)
 // VGPRs (up to 8 models) and the image plus 16 candidate lists fit in LDS.
 int fast_waves_for(int n_models, const FastLayout &lay, int kp, int act)
 {
-    const size_t lds = (size_t)lay.total_floats * 4 + kFastPar * 4 + (size_t)kSearchWavesWide * kp * 8;
-    return (n_models <= 8 && lds <= 163840 && !act) ? kSearchWavesWide : kSearchWaves;
+    const size_t lds = fast_dyn_lds(lay, kSearchWavesWide, kp, 0);
+    return (n_models <= 8 && lds <= (size_t)kFastLdsMax && !act) ? kSearchWavesWide : kSearchWaves;
 }
 
 hipError_t launch_fast_impl(const FastArgs &a, const FastConst &fc, int grid, int kp, int mode, hipStream_t s)
@@ -781,7 +893,7 @@ namespace mfi {
 // one fp64 fma chain, rounded to fp32.  Reads the canonical image (W1T[k][h]).
 __global__ void precompute_p_kernel(const float *features, const float *canon_w, const float *centre, int n_rows,
                                     int L, int A, int H, int64_t wstride, const int32_t *row_model, float *image_p,
-                                    int pst)
+                                    int pst, Pow2Scales sc)
 {
     const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (t >= (int64_t)n_rows * H) return;
@@ -792,18 +904,19 @@ __global__ void precompute_p_kernel(const float *features, const float *canon_w,
     double c = (double)b1[h];
     for (int k = 0; k < L; k++) c = fma((double)W1T[(int64_t)k * H + h], (double)features[(int64_t)row * L + k], c);
     for (int k = 0; k < A; k++) c = fma((double)W1T[(int64_t)(L + k) * H + h], (double)centre[k], c);
-    image_p[(int64_t)row * pst + h] = (float)c;
+    // the fast image's layer-1 scale 2^e (exact: rounding commutes with it)
+    image_p[(int64_t)row * pst + h] = (float)ldexp(c, sc.e[row_model[row]]);
 }
 
 hipError_t launch_precompute_p(const float *features, const float *weights, const float *centre, int n_rows, int L,
                                int A, int H, int64_t wstride, const int32_t *row_model, float *image_p, int pst,
-                               hipStream_t s)
+                               const Pow2Scales &sc, hipStream_t s)
 {
     const int64_t total = (int64_t)n_rows * H;
     const int blk = 256;
     const int grid = (int)((total + blk - 1) / blk);
     hipLaunchKernelGGL(precompute_p_kernel, dim3(grid), dim3(blk), 0, s, features, weights, centre, n_rows, L, A, H,
-                       wstride, row_model, image_p, pst);
+                       wstride, row_model, image_p, pst, sc);
     return hipGetLastError();
 }
 

@@ -20,7 +20,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmf.so")
 
 MF_OK, MF_EINVAL, MF_ENOMEM, MF_EDEVICE, MF_EUNSUPPORTED, MF_EOVERFLOW, MF_EINTERNAL, MF_ESCRATCH = range(8)
-NOALLOC_SCRATCH_BYTES = 64 << 20
+NOALLOC_SCRATCH_BYTES = 128 << 20
 MF_F32, MF_BF16 = 0, 1
 MF_ACT_IDENTITY, MF_ACT_SIGMOID = 0, 1
 MF_DUMP = 1
