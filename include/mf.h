@@ -358,6 +358,14 @@ typedef struct {
     uint32_t flags;            /* MF_FIXED_STATE: the surrogates see state[] (as in mf_search) */
     float state[MF_MAX_AGG];   /* MF_FIXED_STATE: observed aggregate, original slot order, finite */
     mf_objective objective;    /* zero-initialised: MF_OBJ_LINEAR; MF_OBJ_EQ3 as in mf_search */
+    /* Optional host output (NULL: none): the individuals of the run whose
+     * fitness ran the surrogates.  Large populations (S x pop > 8192, shapes
+     * with the one-lane fitness kernel) over joint spaces small enough to
+     * tabulate (|Lambda| (16 N + 4) bytes <= 256 MiB) keep a memo of each
+     * evaluated index's canonical predictions in the workspace for the rest of
+     * the run; later generations read it (the values, and so the trajectory,
+     * are the same).  Otherwise every individual counts. */
+    uint64_t *h_forwards;
 } mf_ga_args;
 
 mf_status mf_ga_workspace_size(const mf_problem *p, const mf_ga_args *args, size_t *bytes);

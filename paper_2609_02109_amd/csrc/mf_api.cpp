@@ -2025,8 +2025,20 @@ static mf_status check_ga_args(const mf_problem *p, const mf_ga_args *a)
 }
 
 struct GaWs {
-    size_t cnt, off, nfl, fl, popA, popB, fit, bJ, bI, total;
+    size_t cnt, off, nfl, fl, popA, popB, fit, bJ, bI, memo, tag, nfwd, total;
+    bool use_memo;
 };
+
+// The GAConst of a run without its device pointers' workspace parts (the
+// shape fields the kernels' choices depend on).
+static GAConst ga_shape(const mf_problem *p)
+{
+    GAConst c{};
+    c.N = p->N; c.L = p->L; c.A = p->A; c.H1 = p->H1; c.H2 = p->H2; c.bf16 = p->bf16; c.act = p->act;
+    c.pre = p->d_pre;
+    c.sumK = p->sumK;
+    return c;
+}
 
 static GaWs ga_ws(const mf_problem *p, const mf_ga_args *a)
 {
@@ -2043,6 +2055,13 @@ static GaWs ga_ws(const mf_problem *p, const mf_ga_args *a)
     w.fit = o; o = align256(o + sp * 8);
     w.bJ = o; o = align256(o + (size_t)a->n_scen * 8);
     w.bI = o; o = align256(o + (size_t)a->n_scen * 8);
+    // the run's memo of canonical predictions per joint index (large
+    // populations over spaces small enough to tabulate)
+    const uint64_t memo_bytes = p->space * (uint64_t)p->N * 16u + p->space * 4u;
+    w.use_memo = ga_memo_supported(ga_shape(p), a->n_scen, a->pop) && memo_bytes <= kGaMemoMaxBytes;
+    w.memo = o; o = align256(o + (w.use_memo ? p->space * (size_t)p->N * 16 : 0));
+    w.tag = o; o = align256(o + (w.use_memo ? p->space * 4 : 0));
+    w.nfwd = o; o = align256(o + 8);
     w.total = o;
     return w;
 }
@@ -2093,20 +2112,31 @@ mf_status mf_ga_run(mf_problem *p, const mf_ga_args *args, void *d_ws, size_t ws
     c.fixed = (args->flags & MF_FIXED_STATE) ? 1 : 0;
     for (int k = 0; k < p->A; k++) c.state[k] = c.fixed ? args->state[k] : 0.f;
     c.obj = obj_args(p, args->objective);
+    c.memo = w.use_memo ? reinterpret_cast<double *>(ws + w.memo) : nullptr;
+    c.memo_tag = w.use_memo ? reinterpret_cast<uint32_t *>(ws + w.tag) : nullptr;
+    c.n_forwards = reinterpret_cast<unsigned long long *>(ws + w.nfwd);
 
     const int S = args->n_scen, P = args->pop;
     // an empty feasible list is handled on the device (the best stays unset,
     // the final population reads all ones): no synchronisation mid-run
     MF_HIP(launch_ga_feasible(c, cnt, blk_off, n_fl, fl, s));
     MF_HIP(launch_ga_init(args->seed, S, P, fl, n_fl, pa, bJ, bI, s));
+    // generation 0 always runs the surrogates (and fills the memo); without
+    // the memo every generation does
+    const unsigned long long sp = (unsigned long long)S * (unsigned long long)P;
+    MF_HIP(launch_ga_memo_clear(c.memo_tag, c.memo ? p->space : 0, c.n_forwards,
+                                c.memo ? sp : sp * (unsigned long long)(args->gens + 1), s));
     for (int g = 0; g <= args->gens; g++) {
-        MF_HIP(launch_ga_fitness(c, S, P, pa, args->d_sla, args->d_omega, fit, s));
+        // generation g's entries carry tag g + 1
+        MF_HIP(launch_ga_fitness(c, S, P, pa, args->d_sla, args->d_omega, fit, s, (uint32_t)g + 1u));
         MF_HIP(launch_ga_ops(c, args->seed, S, P, g, args->gens, args->tourn_k, args->p_cx, args->p_swap,
                              args->p_mut, fl, n_fl, pa, fit, pb, bJ, bI, d_final_pop, s));
         std::swap(pa, pb);
     }
     MF_HIP(hipMemcpyAsync(h_best_J, bJ, (size_t)S * 8, hipMemcpyDeviceToHost, s));
     MF_HIP(hipMemcpyAsync(h_best_idx, bI, (size_t)S * 8, hipMemcpyDeviceToHost, s));
+    if (args->h_forwards)
+        MF_HIP(hipMemcpyAsync(args->h_forwards, c.n_forwards, 8, hipMemcpyDeviceToHost, s));
     MF_HIP(hipStreamSynchronize(s));
     return MF_OK;
 }

@@ -60,8 +60,11 @@ __device__ __forceinline__ double canon_sigmoid(double y)
 // 64-thread workgroup: lanes take hidden units; h1s, h2s are shared scratch.
 // w: the model's canonical image W1^T[nin][H1], b1, W2^T[H1][H2], b2,
 // W3[2][H2], b3; sigmoid: both outputs pass canon_sigmoid.  Every lane returns
-// (lat, thr).  Contains barriers: call from all lanes.
-template <bool BF16>
+// (lat, thr).  Contains barriers: call from all lanes.  WAVE: zs, h1s, h2s
+// belong to the calling wave alone, whose LDS accesses complete in program
+// order, so wave barriers (which only keep the compiler from moving the
+// accesses across them) replace the workgroup barriers.
+template <bool BF16, bool WAVE = false>
 __device__ inline void canon_model(const float *w, int nin, int H1, int H2, const double *zs, double *h1s,
                                    double *h2s, int lane, double &lat, double &thr, int sigmoid)
 {
@@ -81,14 +84,14 @@ __device__ inline void canon_model(const float *w, int nin, int H1, int H2, cons
             h1s[u] = c > 0.0 ? c : 0.0;
         }
     }
-    __syncthreads();
+    if (WAVE) __builtin_amdgcn_wave_barrier(); else __syncthreads();
     for (int v = lane; v < H2; v += 64) {
         double c = (double)b2[v];
         #pragma unroll 8
         for (int u = 0; u < H1; u++) c = fma((double)W2T[(int64_t)u * H2 + v], h1s[u], c);
         h2s[v] = c > 0.0 ? c : 0.0;
     }
-    __syncthreads();
+    if (WAVE) __builtin_amdgcn_wave_barrier(); else __syncthreads();
     double y = 0.0;
     if (lane < 2) {
         double c = (double)b3[lane];

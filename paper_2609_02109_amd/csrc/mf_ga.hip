@@ -275,7 +275,8 @@ __global__ void __launch_bounds__(256) ga_fitness_kernel(const GAConst c, int S,
 template <int A, int H1, int H2, bool BF16>
 __global__ void __launch_bounds__(kGaFitThreads) ga_fitness_pre_kernel(const GAConst c, int S, int P,
                                                                        const uint64_t *pop, const float *sla,
-                                                                       const float *omega, double *fit)
+                                                                       const float *omega, double *fit,
+                                                                       uint32_t memo_gen)
 {
     extern __shared__ __align__(16) double pre_s[];
     constexpr int PS = H1 + 2;
@@ -308,7 +309,8 @@ __global__ void __launch_bounds__(kGaFitThreads) ga_fitness_pre_kernel(const GAC
     const int s = (int)(tt / P);
     const int N = c.N, L = c.L, NIN = L + A;
     int32_t d[kMaxN];
-    ga_digits(c, pop[tt], d);
+    const uint64_t idx = pop[tt];
+    ga_digits(c, idx, d);
     // aggregate slots: fp32 sums in model order; the surrogates see them, or
     // the observed state held fixed (the VRAM cap still sees the candidate)
     double za[A];
@@ -375,6 +377,10 @@ __global__ void __launch_bounds__(kGaFitThreads) ga_fitness_pre_kernel(const GAC
             y0 = canon_sigmoid(y0);
             y1 = canon_sigmoid(y1);
         }
+        if (memo_gen) {   // into the run's memo (equal values where two lanes share an index)
+            c.memo[(idx * (uint64_t)N + (uint64_t)i) * 2u] = y0;
+            c.memo[(idx * (uint64_t)N + (uint64_t)i) * 2u + 1u] = y1;
+        }
         if (!(y0 <= (double)sla[(int64_t)s * N + i])) sla_ok = false;
         const double om = (double)omega[(int64_t)s * N + i];
         if (c.obj.kind != 0) {
@@ -391,6 +397,147 @@ __global__ void __launch_bounds__(kGaFitThreads) ga_fitness_pre_kernel(const GAC
         }
     }
     fit[t] = (vram_ok && sla_ok) ? J : -INFINITY;
+    if (memo_gen) c.memo_tag[idx] = 2u * memo_gen + (vram_ok ? 1u : 0u);
+}
+
+// One model's term of the canonical fitness, in the order every fitness
+// kernel takes it: the service constraint (Eq. 4), then J = fma(omega, thr,
+// J) or, under Eq. 3, the utility's terms (throughput floor as a constraint).
+__device__ __forceinline__ void ga_term(const GAConst &c, int s, int i, int64_t row, double lat, double thr,
+                                        const float *sla, const float *omega, const float *tau,
+                                        const int32_t *prev, double &J, bool &ok)
+{
+    if (!(lat <= (double)sla[(int64_t)s * c.N + i])) ok = false;
+    const double om = (double)omega[(int64_t)s * c.N + i];
+    if (c.obj.kind != 0) {
+        double q, Pr, pen;
+        bool do_P, do_pen;
+        if (!canon_eq3(c.obj, row, thr, tau[i], prev[i], q, Pr, do_P, pen, do_pen)) ok = false;
+        J = fma(om, q, J);
+        if (do_P) J = J - Pr;
+        if (do_pen) J = J - pen;
+    } else {
+        J = fma(om, thr, J);
+    }
+}
+
+// Generations after the first (large populations): the canonical fitness
+// from the run's memo of per-model predictions, which depend on the joint
+// index only (not on the scenario).  An individual whose index an earlier
+// generation evaluated (tag 2 g' + v, g' below this launch's) reads its
+// models' (lat, thr) there and combines them with its scenario's bounds and
+// weights.  The workgroup's other individuals (configurations new to the
+// run) are evaluated here, one wave per individual with lanes over hidden
+// units (the canonical forward, weights staged in LDS when they fit), and
+// written to the memo.  Entries written by this launch are not read by it
+// (evaluating an index twice gives equal values), so no workgroup waits on
+// another.  Dynamic LDS: [staged weights][W x (nin + H1 + H2) doubles].
+template <bool BF16, bool STAGE>
+__global__ void __launch_bounds__(kGaMemoThreads) ga_fitness_memo_kernel(const GAConst c, int S, int P,
+                                                                         const uint64_t *pop, const float *sla,
+                                                                         const float *omega, double *fit,
+                                                                         uint32_t memo_gen, int stage_floats)
+{
+    extern __shared__ float4 dyn4[];
+    __shared__ int s_miss[kGaMemoThreads];
+    __shared__ int s_nmiss;
+    __shared__ float s_tau[kMaxN];
+    __shared__ int32_t s_prev[kMaxN];
+    constexpr int W = kGaMemoThreads / 64;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    if (tid < kMaxN) {
+        s_tau[tid] = c.obj.tau[tid];
+        s_prev[tid] = c.obj.prev[tid];
+    }
+    if (tid == 0) s_nmiss = 0;
+    __syncthreads();
+    const int N = c.N, L = c.L, A = c.A, nin = L + A;
+    const int64_t n = (int64_t)S * P;
+    const int64_t t = (int64_t)blockIdx.x * kGaMemoThreads + tid;
+    if (t < n) {
+        const uint64_t idx = pop[t];
+        const uint32_t tg = c.memo_tag[idx];
+        // the entry's values are read beside its tag (used only on a hit)
+        double m[2 * kMaxN];
+        const double *mp = c.memo + idx * (uint64_t)N * 2u;
+#pragma unroll
+        for (int j = 0; j < 2 * kMaxN; j++)
+            if (j < 2 * N) m[j] = mp[j];
+        if ((tg >> 1) != 0u && (tg >> 1) < memo_gen) {
+            int32_t d[kMaxN];
+            ga_digits(c, idx, d);
+            const int s = (int)(t / P);
+            bool ok = (tg & 1u) != 0u;
+            double J = 0.0;
+#pragma unroll
+            for (int i = 0; i < kMaxN; i++)
+                if (i < N)
+                    ga_term(c, s, i, c.opt_off[i] + d[i], m[2 * i], m[2 * i + 1], sla, omega, s_tau, s_prev, J, ok);
+            fit[t] = ok ? J : -INFINITY;
+        } else {
+            s_miss[atomicAdd(&s_nmiss, 1)] = tid;
+        }
+    }
+    __syncthreads();
+    const int nm = s_nmiss;
+    if (nm == 0) return;   // uniform: the workgroup had no new configuration
+    if (tid == 0) atomicAdd(c.n_forwards, (unsigned long long)nm);
+    const float *wbase = c.canon;
+    if (STAGE) {
+        const int n4 = (stage_floats + 3) / 4;
+        const float4 *src = reinterpret_cast<const float4 *>(c.canon);
+        for (int q = tid; q < n4; q += blockDim.x) dyn4[q] = src[q];
+        wbase = reinterpret_cast<const float *>(dyn4);
+        __syncthreads();
+    }
+    double *zs = reinterpret_cast<double *>(dyn4 + (STAGE ? (stage_floats + 3) / 4 : 0)) +
+                 (int64_t)wave * (nin + c.H1 + c.H2);
+    double *h1s = zs + nin, *h2s = h1s + c.H1;
+    for (int q = wave; q < nm; q += W) {
+        const int64_t tt = (int64_t)blockIdx.x * kGaMemoThreads + s_miss[q];
+        const uint64_t idx = pop[tt];
+        const int s = (int)(tt / P);
+        int32_t d[kMaxN];
+        ga_digits(c, idx, d);
+        // aggregate slot `lane` (fp32, model order); the VRAM slot decides the cap
+        float a = 0.f;
+        if (lane < A)
+            for (int i = 0; i < N; i++) a = a + c.features[(int64_t)(c.opt_off[i] + d[i]) * L + c.agg_cols[lane]];
+        const float av = __shfl(a, c.vram_slot);
+        const bool vram_ok = (double)av <= (double)c.vram_cap;
+        if (lane < A) zs[L + lane] = c.fixed ? (double)c.state[lane] : (double)a;
+        bool ok = vram_ok;
+        double J = 0.0;
+        for (int i = 0; i < N; i++) {
+            const float *x = c.features + (int64_t)(c.opt_off[i] + d[i]) * L;
+            for (int k = lane; k < L; k += 64) zs[k] = (double)x[k];
+            __builtin_amdgcn_wave_barrier();
+            double lat, thr;
+            canon_model<BF16, true>(wbase + (int64_t)i * c.wstride, nin, c.H1, c.H2, zs, h1s, h2s, lane, lat, thr,
+                                    c.act);
+            if (lane == 0) {
+                c.memo[(idx * (uint64_t)N + (uint64_t)i) * 2u] = lat;
+                c.memo[(idx * (uint64_t)N + (uint64_t)i) * 2u + 1u] = thr;
+            }
+            ga_term(c, s, i, c.opt_off[i] + d[i], lat, thr, sla, omega, s_tau, s_prev, J, ok);
+            __builtin_amdgcn_wave_barrier();
+        }
+        if (lane == 0) {
+            fit[tt] = ok ? J : -INFINITY;
+            c.memo_tag[idx] = 2u * memo_gen + (vram_ok ? 1u : 0u);
+        }
+    }
+}
+
+// Zero a run's memo tags; the forward count starts at `first` (the
+// generations that do not read the memo).
+__global__ void ga_memo_clear_kernel(uint32_t *tag, uint64_t n, unsigned long long *n_forwards,
+                                     unsigned long long first)
+{
+    const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) tag[i] = 0u;
+    if (i == 0) *n_forwards = first;
 }
 
 // Canonical fp64 fitness, one workgroup per individual (small populations,
@@ -707,27 +854,67 @@ int ga_fitness_supported(int nin, int h1, int h2)
 
 template <int A, int H1, int H2>
 static hipError_t launch_fit_pre_t(const GAConst &c, int S, int P, const uint64_t *pop, const float *sla,
-                                   const float *omega, double *fit, size_t lds, hipStream_t st)
+                                   const float *omega, double *fit, size_t lds, hipStream_t st, uint32_t memo_gen)
 {
     const int64_t n = (int64_t)S * P;
     const int grid = (int)((n + kGaFitThreads - 1) / kGaFitThreads);
     auto fn = c.bf16 ? ga_fitness_pre_kernel<A, H1, H2, true> : ga_fitness_pre_kernel<A, H1, H2, false>;
     const hipError_t e = ensure_dyn_lds((const void *)fn, lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(fn, dim3(grid), dim3(kGaFitThreads), lds, st, c, S, P, pop, sla, omega, fit);
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(kGaFitThreads), lds, st, c, S, P, pop, sla, omega, fit, memo_gen);
+    return hipGetLastError();
+}
+
+static size_t ga_pre_lds(const GAConst &c)
+{
+    return (size_t)c.sumK * (c.H1 + 2) * 8 + (size_t)c.sumK * c.A * 4;
+}
+
+static bool ga_pre_shape(int A, int H1, int H2)
+{
+    return (A == 2 || A == 4 || A == 6 || A == 8) && ((H1 == 32 && H2 == 32) || (H1 == 64 && (H2 == 32 || H2 == 64)));
+}
+
+bool ga_memo_supported(const GAConst &c, int S, int P)
+{
+    return (int64_t)S * P > kGaWideMax && c.pre && ga_pre_lds(c) <= kGaPreLdsBytes && ga_pre_shape(c.A, c.H1, c.H2);
+}
+
+hipError_t launch_ga_memo_clear(uint32_t *tag, uint64_t n, unsigned long long *n_forwards,
+                                unsigned long long first, hipStream_t st)
+{
+    const uint64_t m = n > 0 ? n : 1;
+    hipLaunchKernelGGL(ga_memo_clear_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, st, tag, n,
+                       n_forwards, first);
     return hipGetLastError();
 }
 
 hipError_t launch_ga_fitness(const GAConst &c, int S, int P, const uint64_t *pop, const float *sla, const float *omega,
-                             double *fit, hipStream_t st)
+                             double *fit, hipStream_t st, uint32_t memo_gen)
 {
     const int nin = c.L + c.A;
+    if (c.memo && memo_gen >= 2) {
+        // later generations with the run's memo
+        const int64_t n = (int64_t)S * P;
+        const int64_t wfloats = (int64_t)c.N * c.wstride;
+        const bool stage = ((wfloats + 3) / 4) * 16 <= (int64_t)kGaStageBytes;
+        const size_t lds = (stage ? (size_t)((wfloats + 3) / 4) * 16 : 0) +
+                           (size_t)(kGaMemoThreads / 64) * (nin + c.H1 + c.H2) * 8;
+        auto fn = c.bf16 ? (stage ? ga_fitness_memo_kernel<true, true> : ga_fitness_memo_kernel<true, false>)
+                         : (stage ? ga_fitness_memo_kernel<false, true> : ga_fitness_memo_kernel<false, false>);
+        const hipError_t e = ensure_dyn_lds((const void *)fn, lds);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(fn, dim3((unsigned)((n + kGaMemoThreads - 1) / kGaMemoThreads)), dim3(kGaMemoThreads),
+                           lds, st, c, S, P, pop, sla, omega, fit, memo_gen, stage ? (int)wfloats : 0);
+        return hipGetLastError();
+    }
     // large populations: the kernel that continues each option's local chain,
     // when the chain table and the aggregate columns fit in LDS
-    const size_t pre_lds = (size_t)c.sumK * (c.H1 + 2) * 8 + (size_t)c.sumK * c.A * 4;
+    const size_t pre_lds = ga_pre_lds(c);
+    const uint32_t mg = c.memo ? memo_gen : 0u;
     if ((int64_t)S * P > kGaWideMax && c.pre && pre_lds <= kGaPreLdsBytes) {
 #define MF_GA_PRE(AA, HA, HB) \
-    if (c.A == AA && c.H1 == HA && c.H2 == HB) return launch_fit_pre_t<AA, HA, HB>(c, S, P, pop, sla, omega, fit, pre_lds, st);
+    if (c.A == AA && c.H1 == HA && c.H2 == HB) return launch_fit_pre_t<AA, HA, HB>(c, S, P, pop, sla, omega, fit, pre_lds, st, mg);
         MF_GA_PRE(2, 32, 32) MF_GA_PRE(4, 32, 32) MF_GA_PRE(6, 32, 32) MF_GA_PRE(8, 32, 32)
         MF_GA_PRE(2, 64, 32) MF_GA_PRE(4, 64, 32) MF_GA_PRE(6, 64, 32) MF_GA_PRE(8, 64, 32)
         MF_GA_PRE(2, 64, 64) MF_GA_PRE(4, 64, 64) MF_GA_PRE(6, 64, 64) MF_GA_PRE(8, 64, 64)

@@ -437,6 +437,12 @@ struct GAConst {
     int fixed;                  // the surrogates see state[] instead of the candidate's aggregate
     float state[kMaxN];
     ObjArgs obj;
+    // the run's memo of canonical predictions per joint index (null: none):
+    // memo[idx][N][2] (lat, thr) and tag[idx] = 2 g' + vram_ok, g' - 1 the
+    // generation that wrote it (0: not yet evaluated in this run)
+    double *memo;
+    uint32_t *memo_tag;
+    unsigned long long *n_forwards;   // individuals whose fitness ran the surrogates (with the memo)
 };
 
 // Raise a kernel's dynamic-LDS limit to at least `bytes` on the current
@@ -496,6 +502,8 @@ constexpr int kCanonFewEntries = 1024;     // index lists up to this length coun
 constexpr int kGaWideWaves = 8;             // ... with up to this many waves (models) per workgroup
 constexpr size_t kGaStageBytes = 64 * 1024;   // ... copying the weights to LDS when they fit in this
 constexpr int kGaFitThreads = 512;             // large populations: lanes (individuals) per fitness workgroup
+constexpr int kGaMemoThreads = 256;            // ... after the first generation: individuals per memo workgroup
+constexpr uint64_t kGaMemoMaxBytes = 256ull << 20;   // the run's memo of predictions, at most this large
 constexpr size_t kGaPreLdsBytes = 96 * 1024;   // ... continuing the local-feature chains staged in this much LDS
 constexpr int64_t kGaWideStagedWgs = 512;    // ... and then running this many workgroups at most
 int ga_fitness_supported(int nin, int h1, int h2);
@@ -504,7 +512,12 @@ hipError_t launch_ga_feasible(const GAConst &c, uint32_t *blk_count, uint64_t *b
 hipError_t launch_ga_init(uint64_t seed, int S, int P, const uint32_t *fl, const unsigned long long *n_fl,
                           uint64_t *pop, double *best_J, uint64_t *best_idx, hipStream_t st);
 hipError_t launch_ga_fitness(const GAConst &c, int S, int P, const uint64_t *pop, const float *sla,
-                             const float *omega, double *fit, hipStream_t st);
+                             const float *omega, double *fit, hipStream_t st, uint32_t memo_gen = 0);
+// Whether generation 0's fitness takes the one-lane kernel that continues the
+// local chains (the kernel that fills the run's memo for the later ones).
+bool ga_memo_supported(const GAConst &c, int S, int P);
+hipError_t launch_ga_memo_clear(uint32_t *tag, uint64_t n, unsigned long long *n_forwards,
+                                unsigned long long first, hipStream_t st);
 hipError_t launch_ga_ops(const GAConst &c, uint64_t seed, int S, int P, int gen, int gens, int tk, float p_cx,
                          float p_swap, float p_mut, const uint32_t *fl, const unsigned long long *n_fl,
                          const uint64_t *pop, const double *fit, uint64_t *next, double *best_J,

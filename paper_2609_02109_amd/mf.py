@@ -105,7 +105,8 @@ class GAArgs(C.Structure):
     _fields_ = [("n_scen", C.c_int32), ("pop", C.c_int32), ("gens", C.c_int32), ("tourn_k", C.c_int32),
                 ("p_cx", C.c_float), ("p_swap", C.c_float), ("p_mut", C.c_float), ("pad", C.c_float),
                 ("seed", C.c_uint64), ("d_sla", C.c_void_p), ("d_omega", C.c_void_p),
-                ("flags", C.c_uint32), ("state", C.c_float * MAX_AGG), ("objective", Objective)]
+                ("flags", C.c_uint32), ("state", C.c_float * MAX_AGG), ("objective", Objective),
+                ("h_forwards", C.c_void_p)]
 
 
 def _load():
@@ -410,11 +411,13 @@ class Problem:
         ws = self.workspace(nbytes.value, stream)
         best_idx = np.zeros(S, np.uint64)
         best_J = np.zeros(S, np.float64)
+        forwards = np.zeros(1, np.uint64)
+        args.h_forwards = _ptr(forwards)
         fp = torch.zeros((S, pop), dtype=torch.int64, device=self.device) if final_pop else None
         _keep_for(stream, d_sla, d_om, fp)
         _check(lib.mf_ga_run(self.handle, C.byref(args), _ptr(ws), C.c_size_t(ws.numel()),
                              _stream(stream), _ptr(best_idx), _ptr(best_J), _ptr(fp)), "mf_ga_run")
-        out = dict(best_idx=best_idx, best_J=best_J)
+        out = dict(best_idx=best_idx, best_J=best_J, forwards=int(forwards[0]))
         if final_pop:
             out["final_pop"] = fp
         return out

@@ -161,3 +161,33 @@ def test_ga_large_population_shapes(mf, orc):
     c = synth.make_instance([7, 9, 3, 5], 10, 4, 32, 32, seed=13, vram_quantile=0.75)
     sc = synth.ga_scenarios(4, 3, seed=13)
     run_both_obj(mf, orc, c, sc.sla, sc.omega, synth.make_objective(c, 13), None, pop=3000, gens=3, seed=14)
+
+
+def test_ga_memo_across_runs_and_forward_count(mf, orc):
+    # large populations keep a memo of canonical predictions per joint index
+    # for the run: later generations read it.  Runs on one problem reuse its
+    # workspace (the memo starts empty every run); every run still equals the
+    # oracle's replay, and the count of individuals that ran the surrogates
+    # lies between one generation and all of them.
+    inst, sc, gp = synth.cfg3(3)
+    p = mf.Problem(inst)
+    kw = dict(pop=2048, gens=30, tourn_k=3, p_cx=0.7, p_swap=0.5, p_mut=0.05)
+    first = None
+    for rows, seed in ((slice(0, 6), 1), (slice(6, 12), 2), (slice(0, 6), 1)):
+        sla, om = sc.sla[rows], sc.omega[rows]
+        print(f"[ga memo] rows={rows} seed={seed}", flush=True)
+        g = p.ga(sla, om, final_pop=True, seed=seed, **kw)
+        r = orc.Problem(inst).ga(sla, om, final_pop=True, seed=seed, **kw)
+        np.testing.assert_array_equal(g["best_idx"], r["best_idx"])
+        assert g["best_J"].tobytes() == r["best_J"].tobytes()
+        np.testing.assert_array_equal(g["final_pop"].cpu().numpy().astype(np.uint64), r["final_pop"])
+        n_gen = 6 * kw["pop"]
+        assert n_gen <= g["forwards"] < n_gen * (kw["gens"] + 1) // 2, g["forwards"]
+        if first is None:
+            first = g
+        elif seed == 1:
+            assert g["forwards"] == first["forwards"]
+            np.testing.assert_array_equal(g["best_idx"], first["best_idx"])
+    # small populations evaluate every individual
+    small = p.ga(sc.sla[:2], sc.omega[:2], pop=64, gens=4, seed=3)
+    assert small["forwards"] == 2 * 64 * 5
