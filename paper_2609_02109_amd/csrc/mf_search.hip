@@ -572,57 +572,56 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
             // ---- layer 2: b2 + W2 h1.  h1 (the relu'd layer-1 accumulators)
             // becomes binary16 pieces first, K-block by K-block (accumulator
             // registers 8 kh .. 8 kh + 7 of block mb1): x1 = x truncated, x2
-            // = (x - x1) truncated, as many registers as h1 itself
+            // = (x - x1) rounded to nearest, as many registers as h1 itself
             f16x8 xh[MB][2], xl[MB][2];
 #pragma unroll
             for (int mb1 = 0; mb1 < MB; mb1++)
 #pragma unroll
                 for (int kh = 0; kh < 2; kh++) split_f16x8(acc1[mb1], 8 * kh, xh[mb1][kh], xl[mb1][kh]);
-            floatx16 acc2[MB];
-            const float *b2 = smem + Ly.off_b2 + i * H + 4 * half;
-#pragma unroll
-            for (int mb = 0; mb < MB; mb++)
-#pragma unroll
-                for (int q = 0; q < 4; q++) {
-                    const float4 v = *reinterpret_cast<const float4 *>(b2 + 32 * mb + 8 * q);
-                    acc2[mb][4 * q + 0] = v.x;
-                    acc2[mb][4 * q + 1] = v.y;
-                    acc2[mb][4 * q + 2] = v.z;
-                    acc2[mb][4 * q + 3] = v.w;
-                }
             // W2 as two binary16 pieces (w1 + w2 ~ 2^e2 W2) in the A-operand
             // order of v_mfma_f32_32x32x16_f16: per (mb2, mb1, kh) 1 KB of w1
             // then 1 KB of w2, lane l's 16 bytes holding K-block elements 0..7;
-            // the products x1 w1 + x1 w2 + x2 w1 accumulate in fp32
+            // the products x1 w1 + x1 w2 + x2 w1 accumulate in fp32.  One
+            // output block at a time: block mb2's relu and layer-3 rows (VALU)
+            // are independent of block mb2 + 1's matrix instructions.
+            const float *b2 = smem + Ly.off_b2 + i * H + 4 * half;
             const uint4 *w2p = reinterpret_cast<const uint4 *>(smem + Ly.off_w2 + i * (H * H)) + lane;
-#pragma unroll
-            for (int mb1 = 0; mb1 < MB; mb1++)
-#pragma unroll
-                for (int kh = 0; kh < 2; kh++)
-#pragma unroll
-                    for (int mb2 = 0; mb2 < MB; mb2++) {
-                        const f16x8 wa = as_f16x8(w2p[(((mb2 * MB + mb1) * 2 + kh) * 2 + 0) * 64]);
-                        const f16x8 wb = as_f16x8(w2p[(((mb2 * MB + mb1) * 2 + kh) * 2 + 1) * 64]);
-                        acc2[mb2] = __builtin_amdgcn_mfma_f32_32x32x16_f16(wa, xh[mb1][kh], acc2[mb2], 0, 0, 0);
-                        acc2[mb2] = __builtin_amdgcn_mfma_f32_32x32x16_f16(wb, xh[mb1][kh], acc2[mb2], 0, 0, 0);
-                        acc2[mb2] = __builtin_amdgcn_mfma_f32_32x32x16_f16(wa, xl[mb1][kh], acc2[mb2], 0, 0, 0);
-                    }
-            // ---- layer 3 (2 outputs) on VALU
             const float *w3 = smem + Ly.off_w3 + i * (2 * H) + 4 * half;
             float pl = 0.f, pt = 0.f;
 #pragma unroll
-            for (int mb = 0; mb < MB; mb++)
+            for (int mb2 = 0; mb2 < MB; mb2++) {
+                floatx16 acc2;
 #pragma unroll
                 for (int q = 0; q < 4; q++) {
-                    const float4 wl = *reinterpret_cast<const float4 *>(w3 + ((0 * MB + mb) * 4 + q) * 8);
-                    const float4 wt = *reinterpret_cast<const float4 *>(w3 + ((1 * MB + mb) * 4 + q) * 8);
-                    const float h0 = relu_f32(acc2[mb][4 * q + 0]), h1 = relu_f32(acc2[mb][4 * q + 1]);
-                    const float h2 = relu_f32(acc2[mb][4 * q + 2]), h3 = relu_f32(acc2[mb][4 * q + 3]);
+                    const float4 v = *reinterpret_cast<const float4 *>(b2 + 32 * mb2 + 8 * q);
+                    acc2[4 * q + 0] = v.x;
+                    acc2[4 * q + 1] = v.y;
+                    acc2[4 * q + 2] = v.z;
+                    acc2[4 * q + 3] = v.w;
+                }
+#pragma unroll
+                for (int mb1 = 0; mb1 < MB; mb1++)
+#pragma unroll
+                    for (int kh = 0; kh < 2; kh++) {
+                        const f16x8 wa = as_f16x8(w2p[(((mb2 * MB + mb1) * 2 + kh) * 2 + 0) * 64]);
+                        const f16x8 wb = as_f16x8(w2p[(((mb2 * MB + mb1) * 2 + kh) * 2 + 1) * 64]);
+                        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(wa, xh[mb1][kh], acc2, 0, 0, 0);
+                        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(wb, xh[mb1][kh], acc2, 0, 0, 0);
+                        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(wa, xl[mb1][kh], acc2, 0, 0, 0);
+                    }
+                // ---- layer 3 (2 outputs) on VALU, this block's rows
+#pragma unroll
+                for (int q = 0; q < 4; q++) {
+                    const float4 wl = *reinterpret_cast<const float4 *>(w3 + ((0 * MB + mb2) * 4 + q) * 8);
+                    const float4 wt = *reinterpret_cast<const float4 *>(w3 + ((1 * MB + mb2) * 4 + q) * 8);
+                    const float h0 = relu_f32(acc2[4 * q + 0]), h1 = relu_f32(acc2[4 * q + 1]);
+                    const float h2 = relu_f32(acc2[4 * q + 2]), h3 = relu_f32(acc2[4 * q + 3]);
                     pl = fmaf(wl.x, h0, pl); pt = fmaf(wt.x, h0, pt);
                     pl = fmaf(wl.y, h1, pl); pt = fmaf(wt.y, h1, pt);
                     pl = fmaf(wl.z, h2, pl); pt = fmaf(wt.z, h2, pt);
                     pl = fmaf(wl.w, h3, pl); pt = fmaf(wt.w, h3, pt);
                 }
+            }
             pl += __shfl_xor(pl, 32);
             pt += __shfl_xor(pt, 32);
             const float *b3 = smem + Ly.off_b3 + 4 * i;
