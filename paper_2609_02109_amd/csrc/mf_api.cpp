@@ -375,7 +375,13 @@ bool model_bounds(const mf_problem &p, const std::vector<float> &F, const std::v
     // once, can lose (a probe on the MI355X over 8 M outputs, exponents of
     // the products spread over 2^30 and cancelling accumulators included,
     // found at most 5.8 u; the matrix core does not round each product sum
-    // separately, so the error is not that of one rounding).
+    // separately, so the error is not that of one rounding).  The kernel
+    // issues the 2 nb small cross products first (nb = H1 / 16 K-blocks),
+    // onto the bias B = 2^(e1+e2) |b2| (|C| <= B + Tc, Tc the corrections'
+    // magnitude), then the leading products of K-blocks j = 0 .. nb - 1
+    // (|C| <= B + Tc + T_0 + ... + T_(j-1)): in all
+    // 17 u (3 nb (B + Tc) + Tc + sum_j (nb - j) T_j), the accumulated errors
+    // inside C taken by a factor 1 + 2^-10.
     double x_max = 0.0, w_max = 0.0;
     for (int h = 0; h < H1; h++) x_max = std::max(x_max, M1[h] + e1f[h]);
     for (int64_t t = 0; t < (int64_t)H2 * H1; t++) w_max = std::max(w_max, (double)std::fabs(W2[t]));
@@ -402,24 +408,28 @@ bool model_bounds(const mf_problem &p, const std::vector<float> &F, const std::v
     *e1_out = e1;
     *e2_out = e2;
     const double s1 = std::ldexp(1.0, e1), s2 = std::ldexp(1.0, e2), S = s1 * s2;
-    const double gacc = gam(17.0 * 3.0 * (H1 / 16), kU32);
+    const int nb = H1 / 16;
     for (int v = 0; v < H2; v++) {
-        double m = std::fabs((double)b2[v]), pf = 0.0, pc = 0.0, mc = m, er = 0.0, sp = 0.0;
+        double m = std::fabs((double)b2[v]), pf = 0.0, pc = 0.0, mc = m, er = 0.0, tc = 0.0, tj[16] = {};
         for (int h = 0; h < H1; h++) {
             const double w = (double)W2[(int64_t)v * H1 + h], aw = std::fabs(w);
             double w1, w2, ew;
             split_w_f16(s2 * w, &w1, &w2, &ew);
-            const double X = s1 * (M1[h] + e1f[h]);
-            er += (0x1p-10 * X + 0x1p-23) * std::fabs(w2) + (0x1p-21 * X + 0x1p-24) * s2 * aw +
-                  (X * (1.0 + 0x1p-20) + 0x1p-24) * ew;
-            sp += (X * (1.0 + 0x1p-10) + 0x1p-23) * (std::fabs(w1) + std::fabs(w2));
+            const double X = s1 * (M1[h] + e1f[h]);       // |x1| <= |x| <= X
+            const double X2 = 0x1p-10 * (1.0 + 0x1p-10) * X + 0x1p-23;   // |x2|
+            er += X2 * std::fabs(w2) + (0x1p-21 * X + 0x1p-24) * s2 * aw + (X * (1.0 + 0x1p-20) + 0x1p-24) * ew;
+            tc += std::fabs(w2) * X + std::fabs(w1) * X2;
+            tj[h / 16] += std::fabs(w1) * X;
             m += aw * M1[h];
             pf += aw * e1f[h];
             pc += aw * e1c[h];
             mc += aw * (M1[h] + e1c[h]);
         }
+        const double B = S * std::fabs((double)b2[v]);
+        double acc = 3.0 * nb * (B + tc) + tc;
+        for (int j = 0; j < nb; j++) acc += (double)(nb - j) * tj[j];
         M2[v] = m;
-        e2f[v] = pf + (er + gacc * (S * std::fabs((double)b2[v]) + sp)) / S;
+        e2f[v] = pf + (er + 17.0 * kU32 * (1.0 + 0x1p-10) * acc) / S;
         e2c[v] = pc + gam(H1, kU64) * mc;
     }
     double out_b[2], out_m = 0.0;

@@ -599,16 +599,25 @@ fast_kernel(const FastArgs args, const FastConst fc, const int mode, const int k
                     acc2[4 * q + 2] = v.z;
                     acc2[4 * q + 3] = v.w;
                 }
+                // the small cross products first, while the accumulator holds
+                // only the bias (each matrix instruction's error grows with
+                // the accumulator it adds to), then the leading ones, K-block
+                // by K-block
+                f16x8 wa[MB][2];   // the w1 pieces, kept for the leading products
 #pragma unroll
                 for (int mb1 = 0; mb1 < MB; mb1++)
 #pragma unroll
                     for (int kh = 0; kh < 2; kh++) {
-                        const f16x8 wa = as_f16x8(w2p[(((mb2 * MB + mb1) * 2 + kh) * 2 + 0) * 64]);
+                        wa[mb1][kh] = as_f16x8(w2p[(((mb2 * MB + mb1) * 2 + kh) * 2 + 0) * 64]);
                         const f16x8 wb = as_f16x8(w2p[(((mb2 * MB + mb1) * 2 + kh) * 2 + 1) * 64]);
-                        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(wa, xh[mb1][kh], acc2, 0, 0, 0);
                         acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(wb, xh[mb1][kh], acc2, 0, 0, 0);
-                        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(wa, xl[mb1][kh], acc2, 0, 0, 0);
+                        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(wa[mb1][kh], xl[mb1][kh], acc2, 0, 0, 0);
                     }
+#pragma unroll
+                for (int mb1 = 0; mb1 < MB; mb1++)
+#pragma unroll
+                    for (int kh = 0; kh < 2; kh++)
+                        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(wa[mb1][kh], xh[mb1][kh], acc2, 0, 0, 0);
                 // ---- layer 3 (2 outputs) on VALU, this block's rows
 #pragma unroll
                 for (int q = 0; q < 4; q++) {
