@@ -32,8 +32,8 @@ CPU_SAMPLE_PER_THREAD = 1 << 20
 # HBM bytes per launch of the fast search kernel from rocprofv3 FETCH_SIZE /
 # WRITE_SIZE passes (profiles/fast_kernel_n6_k24_h64_hbm_counters.md), valid
 # only for the kernel source they were taken on
-TRAFFIC_BYTES = 17_134_080 + 28_266_048
-TRAFFIC_SOURCE_SHA = "ac2899c01d9826ad"
+TRAFFIC_BYTES = 15_930_880 + 20_811_552
+TRAFFIC_SOURCE_SHA = "7ae62e82fdc3c035"
 
 
 # the fast kernel's source: its file and the headers it includes
