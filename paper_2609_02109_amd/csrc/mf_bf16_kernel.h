@@ -273,15 +273,31 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
                         }
                     }
                 }
-                // aggregate (fp32, model order) and this model's option row
-                float ah[4] = {0.f, 0.f, 0.f, 0.f};
-                float vsum = 0.f;
+                // this model's option row first, so that the loads of its
+                // layer-1 seeds are in flight during the aggregate
                 uint64_t dig0 = 0, dig1 = 0;
 #pragma unroll
                 for (int j = 0; j < MAXN; j++) {
                     if (j < N) {
                         if (j < 8) dig0 |= (uint64_t)d[j] << (8 * j);
                         else dig1 |= (uint64_t)d[j] << (8 * (j - 8));
+                    }
+                }
+                const uint64_t sel = (uint64_t)0 - (uint64_t)(i >= 8);
+                const uint64_t dw = dig0 ^ ((dig0 ^ dig1) & sel);
+                const uint32_t row = row0 + (uint32_t)((dw >> (8 * (i & 7))) & 0xFFu);
+                const float *prow = args.phat + (size_t)row * CL.PST + 4 * half;
+                // the seeds of blocks mb and mb + 1 are in flight while block
+                // mb - 1 runs (H >= 64, so MB >= 2)
+                static_assert(MB >= 2, "two seed blocks in flight");
+                floatx16 seed0 = load16(prow), seed1 = load16(prow + 32);
+
+                // aggregate (fp32, model order)
+                float ah[4] = {0.f, 0.f, 0.f, 0.f};
+                float vsum = 0.f;
+#pragma unroll
+                for (int j = 0; j < MAXN; j++) {
+                    if (j < N) {
                         const uint32_t r = (uint32_t)fc.opt_off[j] + d[j];
                         const float4 v = *reinterpret_cast<const float4 *>(G + r * 8 + 4 * half);
                         ah[0] += v.x;
@@ -291,22 +307,18 @@ fast_bf16_kernel(const Bf16Args args, const FastConst fc, const Bf16Const bc, co
                         vsum += Gv[r];
                     }
                 }
-                const uint64_t sel = (uint64_t)0 - (uint64_t)(i >= 8);
-                const uint64_t dw = dig0 ^ ((dig0 ^ dig1) & sel);
-                const uint32_t row = row0 + (uint32_t)((dw >> (8 * (i & 7))) & 0xFFu);
-                const float *prow = args.phat + (size_t)row * CL.PST + 4 * half;
 
                 // ---- layer 1: the canonical fp32 chain, seeded with the
                 // option's local part; block mb's MFMAs overlap block mb-1's
                 // relu / bf16 packing
                 bf16x8 hp[KS];
                 float sh = 0.f;
-                floatx16 seed = load16(prow);
-                floatx16 prev1 = seed;
+                floatx16 prev1 = seed0;
 #pragma unroll
                 for (int mb = 0; mb < MB; mb++) {
-                    floatx16 acc = seed;
-                    if (mb + 1 < MB) seed = load16(prow + 32 * (mb + 1));
+                    floatx16 acc = seed0;
+                    seed0 = seed1;
+                    if (mb + 2 < MB) seed1 = load16(prow + 32 * (mb + 2));
 #pragma unroll
                     for (int s1 = 0; s1 < S1; s1++)
                         acc = __builtin_amdgcn_mfma_f32_32x32x2f32(w1a[(mb * S1 + s1) * 64], ah[s1], acc, 0, 0, 0);
